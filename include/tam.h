@@ -1,0 +1,241 @@
+/*
+ * tam.h -- trie-automaton token masks for constrained decoding over a finite
+ * set of strings, on AMD Instinct MI355X (gfx950).
+ *
+ * The method (Section 2, Eq. 1 and Section 4.1): a finite set E of K strings
+ * is an enum constraint.  A character-level (here: byte-level) trie over E has
+ * one node per distinct prefix.  For every node n the set valid[n] holds the
+ * vocabulary tokens whose bytes, walked from n, stay inside the trie; decoding
+ * masks the logits of every other token to -inf and then moves the state along
+ * the sampled token's bytes.  Because that valid-set test only needs the walk to
+ * survive (appendix "Correctness", conditions (i)-(ii)), the masks are exact,
+ * not an approximation.
+ *
+ * This library computes, on one GPU:
+ *   tam_compile    -- the trie (host) and the dense per-node bitmask table
+ *                     mask[n][v] = [token v is valid at node n] (device);
+ *   tam_apply_mask -- logits[b, v] = -inf where mask[node_ids[b]][v] == 0, in place;
+ *   tam_advance    -- out[b] = the node reached from node_ids[b] by the bytes of
+ *                     token_ids[b], or TAM_DEAD.
+ *
+ * Conventions fixed by this interface (the paper leaves them open):
+ *   - End of a value: every string is followed by a terminator byte T
+ *     (tam_options.terminator, default '"' = 0x22) inserted as an ordinary trie
+ *     edge.  The node after T is final; its row is empty (a caller stops
+ *     decoding there).  A token that runs past T is invalid.
+ *   - A set string containing T is rejected (TAM_E_TERMINATOR).  Duplicate
+ *     strings collapse; the empty string is allowed.
+ *   - Node ids: the rank of the node's prefix in bytewise lexicographic order
+ *     with a proper prefix before its extensions (DFS preorder, children in
+ *     ascending byte order); the root of a single set is 0.  In a forest of S
+ *     sets, set j occupies ids [roots[j], roots[j] + N_j) after sets 0..j-1.
+ *   - TAM_DEAD (-1) is the absorbing dead state.  A node id outside [0, N) is
+ *     treated as dead; a token id outside [0, V) or an empty token is never
+ *     valid (empty tokens are the paper's special tokens without characters).
+ *   - Canonical mask row (tam_export_rows): W = ceil(V/64) little-endian 64-bit
+ *     words, token v is bit (v & 63) of word (v >> 6), bits >= V are zero.
+ *
+ * Memory and streams: device memory comes from the caller's allocator
+ * (tam_allocator; NULL = hipMalloc/hipFree).  Every device operation is
+ * enqueued on the caller's HIP stream (`stream`, a hipStream_t passed as void*;
+ * NULL = the null stream) and returns without synchronising, except where a
+ * function says otherwise.  A handle is immutable after tam_compile (only
+ * tam_rebuild rewrites its table in place), so apply/advance/export calls may
+ * run concurrently on any streams once the compile stream has been waited on.
+ *
+ * Errors: every entry point returns a tam_status; a negative status leaves a
+ * message in tam_last_error() (thread-local).  No exception crosses the ABI.
+ * Per-row conditions on the device (dead or out-of-range ids) are not errors.
+ * An asynchronous HIP failure surfaces as TAM_E_DEVICE on a later call.
+ */
+#ifndef TAM_H
+#define TAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TAM_DEAD (-1)
+
+typedef struct tam_handle tam_handle;
+
+typedef enum {
+    TAM_OK = 0,
+    TAM_E_INVAL = -1,      /* bad argument (null pointer, negative size, bad dtype, ...) */
+    TAM_E_TERMINATOR = -2, /* a set string contains the terminator byte */
+    TAM_E_NOMEM = -3,      /* host allocation or the device allocator failed */
+    TAM_E_DEVICE = -4,     /* a HIP call failed */
+    TAM_E_TOOLARGE = -5,   /* sizes beyond the 32-bit index limits of the tables */
+    TAM_E_STATE = -6       /* operation not available for this handle (see flags) */
+} tam_status;
+
+enum { TAM_DTYPE_FP32 = 0, TAM_DTYPE_BF16 = 1 };
+
+enum {
+    /* Build the host tables only: no HIP call, no device memory.  tam_info_get
+     * works; every device entry point returns TAM_E_STATE. */
+    TAM_FLAG_HOST_ONLY = 1u << 0,
+    /* Keep only the sparse per-node valid lists, no dense [N, W] table: apply
+     * and export then build each requested row on the fly (for forests whose
+     * dense table would not fit, e.g. hundreds of per-query sets). */
+    TAM_FLAG_NO_TABLE = 1u << 1,
+    /* Record HIP events around each device phase of tam_compile/tam_rebuild
+     * so that tam_timing_get can report per-phase times. */
+    TAM_FLAG_TIMING = 1u << 2
+};
+
+/* Device allocator.  alloc returns device memory aligned to at least 256 bytes
+ * (or NULL); free releases it.  Both are called on the calling thread, from
+ * tam_compile and tam_destroy only. */
+typedef struct {
+    void *(*alloc)(size_t bytes, void *ctx);
+    void (*free)(void *ptr, void *ctx);
+    void *ctx;
+} tam_allocator;
+
+typedef struct {
+    int terminator;  /* 0..255; default 0x22 */
+    uint32_t flags;  /* TAM_FLAG_* */
+} tam_options;
+
+/* Read-only view of a compiled handle.  Host pointers stay valid until
+ * tam_destroy; `table` is device memory owned by the handle. */
+typedef struct {
+    int64_t num_nodes;        /* N over all sets, including roots and final nodes */
+    int64_t num_sets;         /* S */
+    int64_t num_strings;      /* distinct strings over all sets */
+    int64_t vocab_size;       /* V */
+    int64_t words_per_row;    /* W = ceil(V/64), canonical row length */
+    int64_t row_stride_words; /* stride of the dense table in words (>= W); 0 without a table */
+    int64_t max_token_len;    /* longest token in bytes */
+    int64_t device_bytes;     /* device memory held by the handle */
+    uint32_t flags;
+    int32_t terminator;
+    const int32_t *roots;     /* [S] root id of each set */
+    const int32_t *parent;    /* [N] parent id, -1 at roots */
+    const int32_t *depth;     /* [N] prefix length in bytes (roots: 0) */
+    const uint8_t *edge_byte; /* [N] byte on the edge into the node (roots: 0) */
+    const uint8_t *is_final;  /* [N] 1 if the node is reached by the terminator */
+    const uint64_t *table;    /* device [N][row_stride_words]; NULL with TAM_FLAG_NO_TABLE */
+} tam_info;
+
+/* Host-side wall times of the last tam_compile and device times (HIP events,
+ * only with TAM_FLAG_TIMING; else -1) of the last tam_compile/tam_rebuild. */
+typedef struct {
+    double host_trie_ms;   /* dedupe, sort, preorder trie, child tables */
+    double host_vocab_ms;  /* token offsets, vocabulary hash, length table */
+    double upload_ms;      /* allocation + enqueue of the host-to-device copies */
+    float dev_count_ms;    /* suffix probes counting valid tokens per node */
+    float dev_scan_ms;     /* prefix sum of the counts into row offsets */
+    float dev_fill_ms;     /* suffix probes writing the sparse valid lists */
+    float dev_table_ms;    /* dense [N, W] bitmask table written from the lists */
+    float dev_total_ms;    /* first device phase start to last device phase end */
+} tam_timing;
+
+/*
+ * tam_compile -- build the trie of each set and its per-node token masks
+ * (Section 4.1; the valid[n] sets, precomputed once per set).
+ *
+ *   str_bytes, str_off  K strings in CSR form: string k is
+ *                       str_bytes[str_off[k] .. str_off[k+1]); str_off has K+1
+ *                       non-decreasing entries, str_off[0] = 0.  Host memory.
+ *   K                   number of strings, >= 1.
+ *   tok_bytes, tok_off  V vocabulary tokens in the same CSR form (token id = index).
+ *                       Host memory.  Tokens may repeat (each id gets its own bit)
+ *                       and may be empty (never valid).
+ *   V                   vocabulary size, >= 1.
+ *   set_off, S          forest: set j is strings set_off[j] .. set_off[j+1]-1
+ *                       (S+1 entries, set_off[0] = 0, set_off[S] = K, every set
+ *                       non-empty).  NULL / 0 = one set of all K strings.
+ *   opt                 NULL = defaults (terminator '"', no flags).
+ *   alloc               NULL = hipMalloc / hipFree.
+ *   stream              HIP stream for the uploads and kernels.
+ *   out                 receives the handle (NULL on failure).
+ *
+ * All host inputs are copied before return.  The device work is enqueued on
+ * `stream` and may still be running when tam_compile returns; wait on the
+ * stream before using the table from another stream.
+ * Errors: TAM_E_INVAL, TAM_E_TERMINATOR, TAM_E_NOMEM, TAM_E_DEVICE,
+ * TAM_E_TOOLARGE (N, the string bytes or the token bytes beyond 2^31-1).
+ */
+tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
+                       const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V,
+                       const int64_t *set_off, int64_t S,
+                       const tam_options *opt, const tam_allocator *alloc, void *stream,
+                       tam_handle **out);
+
+enum {
+    TAM_PHASE_LISTS = 1u << 0, /* per-node valid lists (suffix probes, scan, fill) */
+    TAM_PHASE_TABLE = 1u << 1  /* dense table written from the lists */
+};
+
+/*
+ * tam_rebuild -- rerun device phases of tam_compile from the handle's resident
+ * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask, 0 =
+ * both; TAM_PHASE_TABLE alone re-uses the current lists.  Used to time the
+ * device phase kernel by kernel and to restore a table.
+ */
+tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
+
+/* tam_info_get -- sizes and host tables of a handle (no device access). */
+tam_status tam_info_get(const tam_handle *h, tam_info *out);
+
+/*
+ * tam_apply_mask -- Eq. 1 with the precomputed masks: for every row b in
+ * [0, B) and token v in [0, V),
+ *     logits[b * row_stride + v] = -inf   if token v is not valid at node_ids[b],
+ * and the entry is left bit-for-bit unchanged otherwise (NaN payloads, -0.0 and
+ * denormals survive).  A dead or out-of-range node masks the whole row.
+ * Columns v >= V of a row are not touched.
+ *
+ *   node_ids    device int32[B].
+ *   logits      device, B rows of row_stride elements, dtype TAM_DTYPE_FP32
+ *               (-inf = 0xFF800000) or TAM_DTYPE_BF16 (-inf = 0xFF80).
+ *   row_stride  elements between rows, >= V.
+ * Rows whose base is 16-byte aligned take the vector path; any other layout is
+ * still handled (element path).  B = 0 is a no-op.
+ */
+tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t B, void *logits,
+                          int dtype, int64_t row_stride, void *stream);
+
+/*
+ * tam_advance -- the state transition extended over a token's bytes
+ * (Section 2, the start state moved along the characters of the output):
+ *     out[b] = delta*(node_ids[b], bytes(token_ids[b]))   or TAM_DEAD.
+ * node_ids, token_ids and out are device int32[B]; out may alias node_ids.
+ */
+tam_status tam_advance(const tam_handle *h, const int32_t *node_ids, const int32_t *token_ids,
+                       int64_t B, int32_t *out, void *stream);
+
+/*
+ * tam_export_rows -- canonical mask rows of n nodes: out is device
+ * uint64[n][W] (W = words_per_row); row r is the mask of node_ids[r], or all
+ * zero when node_ids[r] is dead or out of range.
+ */
+tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t n, uint64_t *out,
+                           void *stream);
+
+/*
+ * tam_valid_pairs -- M = sum over all nodes of |valid[n]|, the number of
+ * (node, token) pairs that are valid.  Copies one value from the device and
+ * synchronises `stream`.
+ */
+tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out);
+
+/* tam_timing_get -- see tam_timing.  Waits for the last recorded device event. */
+tam_status tam_timing_get(const tam_handle *h, tam_timing *out);
+
+/* tam_destroy -- waits for the handle's outstanding device work, then frees it.  NULL is a no-op. */
+void tam_destroy(tam_handle *h);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *tam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TAM_H */

@@ -1,0 +1,13 @@
+"""Trie-automaton token masks for constrained decoding on MI355X (gfx950).
+
+``compile`` builds the trie of a finite set of strings and the per-node
+vocabulary bitmasks; ``Handle.apply_mask`` / ``Handle.advance`` are the
+per-step serving operations.  All of them call ``libtam.so`` (C ABI in
+``include/tam.h``).
+"""
+from .tam import (DTYPE_BF16, DTYPE_FP32, FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, PHASE_LISTS, PHASE_TABLE,
+                  TAM_DEAD,
+                  Handle, TamError, compile, lib)
+
+__all__ = ["compile", "Handle", "TamError", "lib", "TAM_DEAD", "DTYPE_FP32", "DTYPE_BF16",
+           "FLAG_HOST_ONLY", "FLAG_NO_TABLE", "FLAG_TIMING", "PHASE_LISTS", "PHASE_TABLE"]

@@ -1,0 +1,411 @@
+// The C ABI of libtam (declared in include/tam.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "host_build.hpp"
+#include "tam_internal.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+tam_status fail(tam_status st, const std::string &msg) {
+    g_err = msg;
+    return st;
+}
+
+tam_status hip_fail(hipError_t e, const char *what) {
+    return fail(TAM_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define TAM_HIP(expr)                                      \
+    do {                                                   \
+        const hipError_t e_ = (expr);                      \
+        if (e_ != hipSuccess) return hip_fail(e_, #expr);  \
+    } while (0)
+
+double ms_since(std::chrono::steady_clock::time_point t0) {
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+}
+
+bool csr_ok(const int64_t *off, int64_t n) {
+    if (!off || off[0] != 0) return false;
+    for (int64_t i = 0; i < n; ++i)
+        if (off[i + 1] < off[i]) return false;
+    return true;
+}
+
+void *dev_alloc(tam_handle *h, size_t bytes) {
+    bytes = std::max<size_t>(bytes, 256);
+    void *p = nullptr;
+    if (h->own_alloc) {
+        if (hipMalloc(&p, bytes) != hipSuccess) return nullptr;
+    } else {
+        p = h->alloc.alloc(bytes, h->alloc.ctx);
+    }
+    if (p) h->dev_ptrs.push_back(p);
+    return p;
+}
+
+void release_device(tam_handle *h) {
+    if (h->work_done) (void)hipEventSynchronize(h->work_done);
+    if (h->have_events) (void)hipEventSynchronize(h->ev[4]);
+    for (void *p : h->dev_ptrs) {
+        if (h->own_alloc)
+            (void)hipFree(p);
+        else
+            h->alloc.free(p, h->alloc.ctx);
+    }
+    h->dev_ptrs.clear();
+    if (h->have_events)
+        for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
+    if (h->work_done) (void)hipEventDestroy(h->work_done);
+    h->have_events = false;
+    h->work_done = nullptr;
+}
+
+// Sub-allocation of the small tables inside one device arena.
+struct Arena {
+    size_t used = 0;
+    template <typename T>
+    size_t take(int64_t count) {
+        const size_t at = used;
+        used += ((size_t)std::max<int64_t>(count, 1) * sizeof(T) + 255) & ~size_t(255);
+        return at;
+    }
+};
+
+// The device part of compile: valid lists, then the dense table.  Phase events
+// are recorded only when both phases run.
+tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
+    const tam::DevTables &t = h->dt;
+    const bool timing = h->have_events && phases == (TAM_PHASE_LISTS | TAM_PHASE_TABLE);
+    if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
+    if (phases & TAM_PHASE_LISTS) {
+        TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
+        TAM_HIP(tam::launch_count(t, s));
+        if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
+        TAM_HIP(tam::launch_scan(t, s));
+        if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
+        TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
+        TAM_HIP(tam::launch_fill_lists(t, s));
+        if (timing) TAM_HIP(hipEventRecord(h->ev[3], s));
+    }
+    if ((phases & TAM_PHASE_TABLE) && t.table) TAM_HIP(tam::launch_rows(t, nullptr, t.N, t.table, t.Wp, t.Wp, s));
+    if (timing) {
+        TAM_HIP(hipEventRecord(h->ev[4], s));
+        h->events_recorded = true;
+    }
+    if (h->work_done) TAM_HIP(hipEventRecord(h->work_done, s));
+    return TAM_OK;
+}
+
+tam_status check_device_handle(const tam_handle *h) {
+    if (!h) return fail(TAM_E_INVAL, "null handle");
+    if (h->flags & TAM_FLAG_HOST_ONLY) return fail(TAM_E_STATE, "handle was compiled with TAM_FLAG_HOST_ONLY");
+    return TAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tam_last_error(void) { return g_err.c_str(); }
+
+tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
+                       const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V,
+                       const int64_t *set_off, int64_t S, const tam_options *opt,
+                       const tam_allocator *alloc, void *stream, tam_handle **out) {
+    g_err.clear();
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    *out = nullptr;
+    if (K <= 0) return fail(TAM_E_INVAL, "K must be >= 1");
+    if (V <= 0) return fail(TAM_E_INVAL, "V must be >= 1");
+    if (!csr_ok(str_off, K)) return fail(TAM_E_INVAL, "str_off must start at 0 and be non-decreasing");
+    if (!csr_ok(tok_off, V)) return fail(TAM_E_INVAL, "tok_off must start at 0 and be non-decreasing");
+    if (!str_bytes && str_off[K] > 0) return fail(TAM_E_INVAL, "str_bytes is null");
+    if (!tok_bytes && tok_off[V] > 0) return fail(TAM_E_INVAL, "tok_bytes is null");
+    if (V >= INT32_MAX) return fail(TAM_E_TOOLARGE, "V must be < 2^31-1");
+    const int64_t one_set[2] = {0, K};
+    if (!set_off || S == 0) {
+        set_off = one_set;
+        S = 1;
+    }
+    if (S < 0 || set_off[0] != 0 || set_off[S] != K) return fail(TAM_E_INVAL, "set_off must run from 0 to K");
+    for (int64_t j = 0; j < S; ++j)
+        if (set_off[j + 1] <= set_off[j]) return fail(TAM_E_INVAL, "every set must hold at least one string");
+    tam_options o{0x22, 0};
+    if (opt) o = *opt;
+    if (o.terminator < 0 || o.terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
+    if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
+
+    tam_handle *h = new (std::nothrow) tam_handle();
+    if (!h) return fail(TAM_E_NOMEM, "out of host memory");
+    h->terminator = o.terminator;
+    h->flags = o.flags;
+    std::string err;
+    tam_status st;
+    try {
+        auto t0 = std::chrono::steady_clock::now();
+        st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);
+        h->timing.host_trie_ms = ms_since(t0);
+        if (st == TAM_OK) {
+            t0 = std::chrono::steady_clock::now();
+            st = tam::build_vocab(tok_bytes, tok_off, V, h, &err);
+            h->timing.host_vocab_ms = ms_since(t0);
+        }
+        if (st == TAM_OK) {
+            h->entry_bound = tam::entry_upper_bound(h);
+            if (h->entry_bound >= INT32_MAX) {
+                st = TAM_E_TOOLARGE;
+                err = "more than 2^31-1 valid (node, token) pairs are possible";
+            }
+        }
+    } catch (const std::bad_alloc &) {
+        st = TAM_E_NOMEM;
+        err = "out of host memory";
+    }
+    if (st != TAM_OK) {
+        delete h;
+        return fail(st, err);
+    }
+    h->W = (V + 63) / 64;
+    h->Wp = (h->W + 7) & ~int64_t(7);  // rows 64-byte aligned
+    h->timing.dev_count_ms = h->timing.dev_scan_ms = h->timing.dev_fill_ms = -1.f;
+    h->timing.dev_table_ms = h->timing.dev_total_ms = -1.f;
+    if (h->flags & TAM_FLAG_HOST_ONLY) {
+        *out = h;
+        return TAM_OK;
+    }
+
+    // ---- device: allocate, upload, build the lists and the table ----
+    const auto t0 = std::chrono::steady_clock::now();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        delete h;
+        return fail(TAM_E_DEVICE, "no HIP device");
+    }
+    h->own_alloc = alloc == nullptr;
+    if (alloc) h->alloc = *alloc;
+
+    Arena a;
+    const size_t o_blob = a.take<uint8_t>(h->blob_bytes);
+    const size_t o_node_at = a.take<int32_t>(h->blob_bytes);
+    const size_t o_node_pos = a.take<int32_t>(h->N);
+    const size_t o_depth = a.take<int32_t>(h->N);
+    const size_t o_child_off = a.take<int32_t>(h->N + 1);
+    const size_t o_child_byte = a.take<uint8_t>((int64_t)h->child_byte.size());
+    const size_t o_child_node = a.take<int32_t>((int64_t)h->child_node.size());
+    const size_t o_tok_off = a.take<uint32_t>(V + 1);
+    const size_t o_tok_blob = a.take<uint8_t>((int64_t)h->tok_blob.size());
+    const size_t o_slots = a.take<tam::HashSlot>((int64_t)h->slots.size());
+    const size_t o_dup = a.take<int32_t>(V);
+    const size_t o_len = a.take<uint8_t>((int64_t)h->len_present.size());
+    const size_t o_count = a.take<int32_t>(h->N);
+    const size_t o_row_ptr = a.take<int32_t>(h->N + 1);
+    const size_t o_cursor = a.take<int32_t>(h->N);
+    const size_t o_entries = a.take<int32_t>(h->entry_bound);
+    const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
+
+    uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
+    uint64_t *table = nullptr;
+    const size_t table_bytes = (size_t)h->N * (size_t)h->Wp * sizeof(uint64_t);
+    if (base && !(h->flags & TAM_FLAG_NO_TABLE)) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
+    if (!base || (!table && !(h->flags & TAM_FLAG_NO_TABLE))) {
+        release_device(h);
+        delete h;
+        return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
+                                     " bytes requested)");
+    }
+    h->device_bytes = (int64_t)a.used + (table ? (int64_t)table_bytes : 0);
+
+    tam::DevTables &t = h->dt;
+    t.blob = base + o_blob;
+    t.node_at = reinterpret_cast<const int32_t *>(base + o_node_at);
+    t.node_pos = reinterpret_cast<const int32_t *>(base + o_node_pos);
+    t.depth = reinterpret_cast<const int32_t *>(base + o_depth);
+    t.child_off = reinterpret_cast<const int32_t *>(base + o_child_off);
+    t.child_byte = base + o_child_byte;
+    t.child_node = reinterpret_cast<const int32_t *>(base + o_child_node);
+    t.tok_off = reinterpret_cast<const uint32_t *>(base + o_tok_off);
+    t.tok_blob = base + o_tok_blob;
+    t.slots = reinterpret_cast<const tam::HashSlot *>(base + o_slots);
+    t.dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
+    t.len_present = base + o_len;
+    t.count = reinterpret_cast<int32_t *>(base + o_count);
+    t.row_ptr = reinterpret_cast<int32_t *>(base + o_row_ptr);
+    t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
+    t.entries = reinterpret_cast<int32_t *>(base + o_entries);
+    t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
+    t.table = table;
+    t.N = h->N;
+    t.V = h->V;
+    t.W = h->W;
+    t.Wp = h->Wp;
+    t.blob_bytes = h->blob_bytes;
+    t.slot_mask = (uint64_t)h->slots.size() - 1;
+    t.max_len = (int32_t)h->max_tok_len;
+
+    auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
+        if (bytes == 0) return hipSuccess;
+        return hipMemcpyAsync(base + off, src, bytes, hipMemcpyHostToDevice, s);
+    };
+    hipError_t e = hipSuccess;
+    if (e == hipSuccess) e = up(o_blob, h->blob.data(), h->blob.size());
+    if (e == hipSuccess) e = up(o_node_at, h->node_at.data(), h->node_at.size() * 4);
+    if (e == hipSuccess) e = up(o_node_pos, h->node_pos.data(), h->node_pos.size() * 4);
+    if (e == hipSuccess) e = up(o_depth, h->depth.data(), h->depth.size() * 4);
+    if (e == hipSuccess) e = up(o_child_off, h->child_off.data(), h->child_off.size() * 4);
+    if (e == hipSuccess) e = up(o_child_byte, h->child_byte.data(), h->child_byte.size());
+    if (e == hipSuccess) e = up(o_child_node, h->child_node.data(), h->child_node.size() * 4);
+    if (e == hipSuccess) e = up(o_tok_off, h->tok_off.data(), h->tok_off.size() * 4);
+    if (e == hipSuccess) e = up(o_tok_blob, h->tok_blob.data(), h->tok_blob.size());
+    if (e == hipSuccess) e = up(o_slots, h->slots.data(), h->slots.size() * sizeof(tam::HashSlot));
+    if (e == hipSuccess) e = up(o_dup, h->dup_next.data(), h->dup_next.size() * 4);
+    if (e == hipSuccess) e = up(o_len, h->len_present.data(), h->len_present.size());
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
+    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
+        for (hipEvent_t &ev : h->ev) {
+            if (e == hipSuccess) e = hipEventCreate(&ev);
+        }
+        h->have_events = e == hipSuccess;
+    }
+    h->timing.upload_ms = ms_since(t0);
+    if (e != hipSuccess) {
+        st = hip_fail(e, "upload");
+        release_device(h);
+        delete h;
+        return st;
+    }
+    st = run_device_phase(h, TAM_PHASE_LISTS | TAM_PHASE_TABLE, s);
+    if (st != TAM_OK) {
+        const std::string msg = g_err;
+        release_device(h);
+        delete h;
+        return fail(st, msg);
+    }
+    *out = h;
+    return TAM_OK;
+}
+
+tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
+    g_err.clear();
+    tam_status st = check_device_handle(h);
+    if (st != TAM_OK) return st;
+    if (phases == 0) phases = TAM_PHASE_LISTS | TAM_PHASE_TABLE;
+    if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
+    return run_device_phase(h, phases, static_cast<hipStream_t>(stream));
+}
+
+tam_status tam_info_get(const tam_handle *h, tam_info *out) {
+    if (!h || !out) return fail(TAM_E_INVAL, "null argument");
+    out->num_nodes = h->N;
+    out->num_sets = h->S;
+    out->num_strings = h->K_unique;
+    out->vocab_size = h->V;
+    out->words_per_row = h->W;
+    out->row_stride_words = h->dt.table ? h->Wp : 0;
+    out->max_token_len = h->max_tok_len;
+    out->device_bytes = h->device_bytes;
+    out->flags = h->flags;
+    out->terminator = h->terminator;
+    out->roots = h->roots.data();
+    out->parent = h->parent.data();
+    out->depth = h->depth.data();
+    out->edge_byte = h->edge.data();
+    out->is_final = h->is_final.data();
+    out->table = h->dt.table;
+    return TAM_OK;
+}
+
+tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t B, void *logits,
+                          int dtype, int64_t row_stride, void *stream) {
+    g_err.clear();
+    tam_status st = check_device_handle(h);
+    if (st != TAM_OK) return st;
+    if (B < 0) return fail(TAM_E_INVAL, "B must be >= 0");
+    if (B == 0) return TAM_OK;
+    if (!node_ids || !logits) return fail(TAM_E_INVAL, "null device pointer");
+    if (dtype != TAM_DTYPE_FP32 && dtype != TAM_DTYPE_BF16) return fail(TAM_E_INVAL, "dtype must be FP32 or BF16");
+    if (row_stride < h->V) return fail(TAM_E_INVAL, "row_stride must be >= V");
+    const size_t elem = dtype == TAM_DTYPE_BF16 ? 2 : 4;
+    if ((reinterpret_cast<uintptr_t>(logits) % elem) != 0) return fail(TAM_E_INVAL, "logits are not element-aligned");
+    TAM_HIP(hipGetLastError());
+    TAM_HIP(tam::launch_apply(h->dt, node_ids, B, logits, dtype, row_stride, static_cast<hipStream_t>(stream)));
+    return TAM_OK;
+}
+
+tam_status tam_advance(const tam_handle *h, const int32_t *node_ids, const int32_t *token_ids, int64_t B,
+                       int32_t *out, void *stream) {
+    g_err.clear();
+    tam_status st = check_device_handle(h);
+    if (st != TAM_OK) return st;
+    if (B < 0) return fail(TAM_E_INVAL, "B must be >= 0");
+    if (B == 0) return TAM_OK;
+    if (!node_ids || !token_ids || !out) return fail(TAM_E_INVAL, "null device pointer");
+    TAM_HIP(hipGetLastError());
+    TAM_HIP(tam::launch_advance(h->dt, node_ids, token_ids, B, out, static_cast<hipStream_t>(stream)));
+    return TAM_OK;
+}
+
+tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t n, uint64_t *out,
+                           void *stream) {
+    g_err.clear();
+    tam_status st = check_device_handle(h);
+    if (st != TAM_OK) return st;
+    if (n < 0) return fail(TAM_E_INVAL, "n must be >= 0");
+    if (n == 0) return TAM_OK;
+    if (!node_ids || !out) return fail(TAM_E_INVAL, "null device pointer");
+    if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return fail(TAM_E_INVAL, "out must be 8-byte aligned");
+    TAM_HIP(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (h->dt.table)
+        TAM_HIP(tam::launch_export_dense(h->dt, node_ids, n, out, s));
+    else
+        TAM_HIP(tam::launch_rows(h->dt, node_ids, n, out, h->W, h->W, s));
+    return TAM_OK;
+}
+
+tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
+    g_err.clear();
+    tam_status st = check_device_handle(h);
+    if (st != TAM_OK) return st;
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    int32_t m = 0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    TAM_HIP(hipMemcpyAsync(&m, h->dt.row_ptr + h->N, sizeof(m), hipMemcpyDeviceToHost, s));
+    TAM_HIP(hipStreamSynchronize(s));
+    *out = m;
+    return TAM_OK;
+}
+
+tam_status tam_timing_get(const tam_handle *h, tam_timing *out) {
+    if (!h || !out) return fail(TAM_E_INVAL, "null argument");
+    *out = h->timing;
+    if (h->have_events && h->events_recorded) {
+        TAM_HIP(hipEventSynchronize(h->ev[4]));
+        float ms[4];
+        for (int i = 0; i < 4; ++i) TAM_HIP(hipEventElapsedTime(&ms[i], h->ev[i], h->ev[i + 1]));
+        out->dev_count_ms = ms[0];
+        out->dev_scan_ms = ms[1];
+        out->dev_fill_ms = ms[2];
+        out->dev_table_ms = ms[3];
+        TAM_HIP(hipEventElapsedTime(&out->dev_total_ms, h->ev[0], h->ev[4]));
+    }
+    return TAM_OK;
+}
+
+void tam_destroy(tam_handle *h) {
+    if (!h) return;
+    if (!(h->flags & TAM_FLAG_HOST_ONLY)) release_device(h);
+    delete h;
+}
+
+}  // extern "C"

@@ -1,0 +1,119 @@
+// Internal definitions shared by the host code and the HIP kernels of libtam.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/tam.h"
+
+namespace tam {
+
+// ---------------------------------------------------------------------------
+// Vocabulary hash: keys are the token bytes read last-to-first, so that a
+// suffix of a trie path can be hashed incrementally while walking backwards
+// from the node where it ends.  Host (table build) and device (probe) must
+// agree bit for bit, hence one definition for both.
+// ---------------------------------------------------------------------------
+constexpr uint64_t kHashSeed = 0xcbf29ce484222325ull;
+
+__host__ __device__ __forceinline__ uint64_t hash_step(uint64_t h, uint32_t byte) {
+    return (h ^ (byte + 1u)) * 0x100000001b3ull;
+}
+
+__host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len) {
+    uint64_t z = h + 0x9e3779b97f4a7c15ull * (uint64_t)(len + 1u);
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    z ^= z >> 31;
+    return z | 1ull;  // 0 never occurs as a key
+}
+
+// One open-addressing slot per distinct non-empty token string.
+struct alignas(16) HashSlot {
+    uint64_t key;    // hash_final(...) of the string, 0 = empty slot
+    int32_t first;   // smallest token id with this string (-1 = empty)
+    int32_t count;   // number of token ids with this string
+};
+
+// ---------------------------------------------------------------------------
+// Device-side view of a compiled handle (plain pointers, passed to kernels).
+// ---------------------------------------------------------------------------
+struct DevTables {
+    // trie (a1)
+    const uint8_t *blob;        // per string: [pad][bytes][T]
+    const int32_t *node_at;     // [blob_bytes] node whose edge byte is that blob byte (pad: root)
+    const int32_t *node_pos;    // [N] blob offset of the node's edge byte (-1 at roots)
+    const int32_t *depth;       // [N]
+    const int32_t *child_off;   // [N+1]
+    const uint8_t *child_byte;  // [N-S]
+    const int32_t *child_node;  // [N-S]
+    // vocabulary (a2)
+    const uint32_t *tok_off;    // [V+1]
+    const uint8_t *tok_blob;
+    const HashSlot *slots;      // [slot_mask+1]
+    const int32_t *dup_next;    // [V] next id with the same bytes, -1 at the end
+    const uint8_t *len_present; // [max_len+1] 1 if some token has that length
+    // valid lists (a4) and dense table
+    int32_t *count;             // [N]
+    int32_t *row_ptr;           // [N+1]
+    int32_t *cursor;            // [N]
+    int32_t *entries;           // [entry_bound]
+    uint64_t *table;            // [N][Wp] or null
+    int32_t *scan_tmp;          // block sums of the scan
+    int64_t N, V, W, Wp;
+    int64_t blob_bytes;
+    uint64_t slot_mask;
+    int32_t max_len;
+};
+
+// Launchers (kernels.hip).  All return hipSuccess or the launch error.
+hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
+hipError_t launch_count(const DevTables &t, hipStream_t s);
+hipError_t launch_scan(const DevTables &t, hipStream_t s);
+hipError_t launch_fill_lists(const DevTables &t, hipStream_t s);
+hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
+                       int64_t out_stride_words, int64_t out_words, hipStream_t s);
+hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, void *logits,
+                        int dtype, int64_t row_stride, hipStream_t s);
+hipError_t launch_advance(const DevTables &t, const int32_t *node_ids, const int32_t *token_ids,
+                          int64_t B, int32_t *out, hipStream_t s);
+hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
+                               hipStream_t s);
+int64_t scan_tmp_elems(int64_t N);
+
+}  // namespace tam
+
+// ---------------------------------------------------------------------------
+// The handle.
+// ---------------------------------------------------------------------------
+struct tam_handle {
+    int terminator = 0x22;
+    uint32_t flags = 0;
+    int device = 0;
+    bool own_alloc = false;
+    tam_allocator alloc{};
+
+    int64_t N = 0, S = 0, K_unique = 0, V = 0, W = 0, Wp = 0;
+    int64_t blob_bytes = 0, max_tok_len = 0, entry_bound = 0, device_bytes = 0;
+
+    // host trie tables
+    std::vector<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
+    std::vector<uint8_t> edge, is_final, blob, child_byte;
+    // host vocabulary tables
+    std::vector<uint32_t> tok_off;
+    std::vector<uint8_t> tok_blob, len_present;
+    std::vector<tam::HashSlot> slots;
+    std::vector<int32_t> dup_next;
+
+    std::vector<void *> dev_ptrs;  // everything allocated for this handle
+    tam::DevTables dt{};
+
+    hipEvent_t ev[5] = {};
+    bool have_events = false;
+    bool events_recorded = false;
+    hipEvent_t work_done = nullptr;  // end of the last upload / device phase
+    tam_timing timing{};
+};

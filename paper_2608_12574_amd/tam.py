@@ -1,0 +1,287 @@
+"""Python binding of ``libtam.so`` (ctypes; argument marshalling only).
+
+Every step of the path runs in the library: the host trie and vocabulary
+tables in its C++ code, everything else in its HIP kernels.  PyTorch only
+provides device memory (through the allocator callbacks) and the stream
+(``torch.cuda.current_stream()``).  The library must have been built
+(``python -m paper_2608_12574_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libtam.so")
+
+TAM_OK = 0
+TAM_DEAD = -1
+DTYPE_FP32, DTYPE_BF16 = 0, 1
+FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING = 1, 2, 4
+PHASE_LISTS, PHASE_TABLE = 1, 2
+
+STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOMEM",
+          -4: "TAM_E_DEVICE", -5: "TAM_E_TOOLARGE", -6: "TAM_E_STATE"}
+
+# the entry points declared in include/tam.h
+ENTRY_POINTS = ("tam_compile", "tam_rebuild", "tam_info_get", "tam_apply_mask", "tam_advance",
+                "tam_export_rows", "tam_valid_pairs", "tam_timing_get", "tam_destroy",
+                "tam_last_error")
+
+
+class TamError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class Allocator(ctypes.Structure):
+    _fields_ = [("alloc", ALLOC_FN), ("free", FREE_FN), ("ctx", ctypes.c_void_p)]
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("terminator", ctypes.c_int), ("flags", ctypes.c_uint32)]
+
+
+class Info(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int64), ("num_sets", ctypes.c_int64),
+                ("num_strings", ctypes.c_int64), ("vocab_size", ctypes.c_int64),
+                ("words_per_row", ctypes.c_int64), ("row_stride_words", ctypes.c_int64),
+                ("max_token_len", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
+                ("flags", ctypes.c_uint32), ("terminator", ctypes.c_int32),
+                ("roots", ctypes.POINTER(ctypes.c_int32)), ("parent", ctypes.POINTER(ctypes.c_int32)),
+                ("depth", ctypes.POINTER(ctypes.c_int32)), ("edge_byte", ctypes.POINTER(ctypes.c_uint8)),
+                ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p)]
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("host_trie_ms", ctypes.c_double), ("host_vocab_ms", ctypes.c_double),
+                ("upload_ms", ctypes.c_double), ("dev_count_ms", ctypes.c_float),
+                ("dev_scan_ms", ctypes.c_float), ("dev_fill_ms", ctypes.c_float),
+                ("dev_table_ms", ctypes.c_float), ("dev_total_ms", ctypes.c_float)]
+
+    def as_dict(self) -> dict:
+        return {k: float(getattr(self, k)) for k, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_12574_amd.build` (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.tam_compile.argtypes = [P, P, i64, P, P, i64, P, i64, ctypes.POINTER(Options),
+                                  ctypes.POINTER(Allocator), P, ctypes.POINTER(P)]
+        L.tam_rebuild.argtypes = [P, ctypes.c_uint, P]
+        L.tam_info_get.argtypes = [P, ctypes.POINTER(Info)]
+        L.tam_apply_mask.argtypes = [P, P, i64, P, ctypes.c_int, i64, P]
+        L.tam_advance.argtypes = [P, P, P, i64, P, P]
+        L.tam_export_rows.argtypes = [P, P, i64, P, P]
+        L.tam_valid_pairs.argtypes = [P, P, ctypes.POINTER(i64)]
+        L.tam_timing_get.argtypes = [P, ctypes.POINTER(Timing)]
+        L.tam_destroy.argtypes = [P]
+        L.tam_destroy.restype = None
+        L.tam_last_error.restype = ctypes.c_char_p
+        for name in ENTRY_POINTS[:-2]:
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str):
+    if rc != TAM_OK:
+        raise TamError(rc, where, lib().tam_last_error().decode(errors="replace"))
+
+
+def csr(items) -> tuple:
+    """list[bytes] -> (uint8 blob, int64 offsets[len+1]) as numpy arrays."""
+    items = list(items)
+    off = np.zeros(len(items) + 1, dtype=np.int64)
+    if items:
+        np.cumsum(np.fromiter((len(x) for x in items), dtype=np.int64, count=len(items)), out=off[1:])
+    blob = np.frombuffer(b"".join(items), dtype=np.uint8)
+    if blob.size == 0:
+        blob = np.zeros(1, dtype=np.uint8)
+    return np.ascontiguousarray(blob), off
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+class _TorchAllocator:
+    """Device memory for the library, taken from torch's caching allocator."""
+
+    def __init__(self, device):
+        import torch
+        self.torch = torch
+        self.device = device
+        self.live = {}
+        self.c_alloc = ALLOC_FN(self._alloc)
+        self.c_free = FREE_FN(self._free)
+        self.struct = Allocator(self.c_alloc, self.c_free, None)
+
+    def _alloc(self, nbytes, ctx):
+        try:
+            t = self.torch.empty(int(nbytes), dtype=self.torch.uint8, device=self.device)
+        except Exception:  # out of memory: the library reports TAM_E_NOMEM
+            return None
+        p = t.data_ptr()
+        self.live[p] = t
+        return p
+
+    def _free(self, p, ctx):
+        self.live.pop(p, None)
+
+
+def _stream_ptr(stream, host_only=False):
+    if host_only:
+        return ctypes.c_void_p(None)
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Handle:
+    """A compiled set (or forest of sets) with its per-node token masks."""
+
+    def __init__(self, raw, allocator, device, host_only):
+        self._raw = raw
+        self._alloc = allocator
+        self.device = device
+        self.host_only = host_only
+        info = Info()
+        _check(lib().tam_info_get(raw, ctypes.byref(info)), "tam_info_get")
+        self.num_nodes = int(info.num_nodes)
+        self.num_sets = int(info.num_sets)
+        self.num_strings = int(info.num_strings)
+        self.vocab_size = int(info.vocab_size)
+        self.words_per_row = int(info.words_per_row)
+        self.row_stride_words = int(info.row_stride_words)
+        self.max_token_len = int(info.max_token_len)
+        self.device_bytes = int(info.device_bytes)
+        self.flags = int(info.flags)
+        self.terminator = int(info.terminator)
+        N, S = self.num_nodes, self.num_sets
+        self.roots = np.ctypeslib.as_array(info.roots, shape=(S,)).copy()
+        self.parent = np.ctypeslib.as_array(info.parent, shape=(N,)).copy()
+        self.depth = np.ctypeslib.as_array(info.depth, shape=(N,)).copy()
+        self.edge_byte = np.ctypeslib.as_array(info.edge_byte, shape=(N,)).copy()
+        self.is_final = np.ctypeslib.as_array(info.is_final, shape=(N,)).copy()
+        self.table_ptr = info.table
+
+    # -- lifetime ------------------------------------------------------------
+    def close(self):
+        if self._raw is not None:
+            lib().tam_destroy(self._raw)
+            self._raw = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- serving ---------------------------------------------------------------
+    def apply_mask(self, node_ids, logits, stream=None):
+        """In place: logits[b, v] = -inf where token v is not valid at node_ids[b]."""
+        import torch
+        assert node_ids.dtype == torch.int32 and node_ids.is_cuda and node_ids.is_contiguous()
+        assert logits.is_cuda and logits.dim() == 2 and logits.stride(1) == 1
+        assert logits.shape[0] == node_ids.numel() and logits.shape[1] >= self.vocab_size
+        dtype = {torch.float32: DTYPE_FP32, torch.bfloat16: DTYPE_BF16}[logits.dtype]
+        _check(lib().tam_apply_mask(self._raw, ctypes.c_void_p(node_ids.data_ptr()), node_ids.numel(),
+                                    ctypes.c_void_p(logits.data_ptr()), dtype, logits.stride(0),
+                                    _stream_ptr(stream, self.host_only)), "tam_apply_mask")
+        return logits
+
+    def advance(self, node_ids, token_ids, out=None, stream=None):
+        """out[b] = node reached from node_ids[b] by the bytes of token_ids[b], or -1."""
+        import torch
+        assert node_ids.dtype == torch.int32 and token_ids.dtype == torch.int32
+        assert node_ids.is_contiguous() and token_ids.is_contiguous()
+        assert node_ids.numel() == token_ids.numel()
+        if out is None:
+            out = torch.empty_like(node_ids)
+        assert out.dtype == torch.int32 and out.is_contiguous() and out.numel() == node_ids.numel()
+        _check(lib().tam_advance(self._raw, ctypes.c_void_p(node_ids.data_ptr()),
+                                 ctypes.c_void_p(token_ids.data_ptr()), node_ids.numel(),
+                                 ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream, self.host_only)), "tam_advance")
+        return out
+
+    def export_rows(self, node_ids, stream=None):
+        """Canonical rows: int64 tensor [n, W] holding the uint64 mask words."""
+        import torch
+        assert node_ids.dtype == torch.int32 and node_ids.is_contiguous()
+        out = torch.empty((node_ids.numel(), self.words_per_row), dtype=torch.int64,
+                          device=node_ids.device)
+        _check(lib().tam_export_rows(self._raw, ctypes.c_void_p(node_ids.data_ptr()), node_ids.numel(),
+                                     ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream, self.host_only)),
+               "tam_export_rows")
+        return out
+
+    def rebuild(self, phases: int = 0, stream=None):
+        """Rerun the device phases (PHASE_LISTS | PHASE_TABLE; 0 = both)."""
+        _check(lib().tam_rebuild(self._raw, phases, _stream_ptr(stream, self.host_only)), "tam_rebuild")
+
+    def valid_pairs(self, stream=None) -> int:
+        m = ctypes.c_int64()
+        _check(lib().tam_valid_pairs(self._raw, _stream_ptr(stream, self.host_only), ctypes.byref(m)),
+               "tam_valid_pairs")
+        return int(m.value)
+
+    def timing(self) -> dict:
+        t = Timing()
+        _check(lib().tam_timing_get(self._raw, ctypes.byref(t)), "tam_timing_get")
+        return t.as_dict()
+
+
+def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, device=None,
+            stream=None) -> Handle:
+    """tam_compile over ``strings`` (list[bytes]) and ``vocab`` (list[bytes], id = index).
+
+    ``sets``: optional forest offsets (S+1 ints) splitting ``strings`` into S sets.
+    With ``FLAG_HOST_ONLY`` no GPU is touched (host tables only).
+    """
+    sb, so = csr(strings)
+    tb, to = csr(vocab)
+    set_arr = None
+    S = 0
+    if sets is not None:
+        set_arr = np.ascontiguousarray(np.asarray(sets, dtype=np.int64))
+        S = set_arr.size - 1
+    opt = Options(terminator, flags)
+    raw = ctypes.c_void_p()
+    host_only = bool(flags & FLAG_HOST_ONLY)
+    allocator = None
+    stream_p = ctypes.c_void_p(None)
+    if not host_only:
+        import torch
+        device = torch.device(device if device is not None else "cuda")
+        if device.index is None:
+            device = torch.device("cuda", torch.cuda.current_device())
+        allocator = _TorchAllocator(device)
+        with torch.cuda.device(device):
+            stream_p = _stream_ptr(stream)
+            rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1,
+                                   _ptr(set_arr) if set_arr is not None else None, S,
+                                   ctypes.byref(opt), ctypes.byref(allocator.struct), stream_p,
+                                   ctypes.byref(raw))
+    else:
+        rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1,
+                               _ptr(set_arr) if set_arr is not None else None, S, ctypes.byref(opt),
+                               None, None, ctypes.byref(raw))
+    _check(rc, "tam_compile")
+    return Handle(raw, allocator, device, host_only)

@@ -1,0 +1,150 @@
+"""The C ABI without a GPU: symbols, argument checks, and the host trie tables.
+
+``TAM_FLAG_HOST_ONLY`` runs the library's host phase (dedupe, sort, preorder
+trie, child tables, vocabulary hash) and no HIP call, so the trie it builds can
+be compared with the oracle's on the CPU.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import Oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tam.h")
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2608_12574_amd as P
+    try:
+        P.lib()
+    except RuntimeError:
+        from paper_2608_12574_amd import build
+        build.build()
+    return P
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tam_[a-z_]+)\s*\(", src)))
+
+
+def test_header_symbols_exported(P):
+    names = declared_functions()
+    assert "tam_compile" in names and "tam_apply_mask" in names and "tam_advance" in names
+    L = ctypes.CDLL(P.tam.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(P.tam.ENTRY_POINTS)
+
+
+def host(P, strings, vocab, sets=None, terminator=0x22):
+    return P.compile(strings, vocab, sets=sets, terminator=terminator, flags=P.FLAG_HOST_ONLY)
+
+
+def same_trie(h, o):
+    assert h.num_nodes == o.N
+    assert np.array_equal(h.roots, o.roots)
+    assert np.array_equal(h.parent, o.parent)
+    assert np.array_equal(h.depth, o.depth)
+    assert np.array_equal(h.edge_byte, o.edge)
+    assert np.array_equal(h.is_final, o.is_final)
+
+
+def test_host_trie_worked_example(P):
+    strings = [b"medical_billing", b"medical_coding", b"medical_records"]
+    vocab = [b"medical", b"_bill", b"_cod", b"_rec", b"ing", b"ords"]
+    h = host(P, strings, vocab)
+    same_trie(h, Oracle(strings, vocab))
+    assert h.num_nodes == 32 and h.words_per_row == 1 and h.max_token_len == 7
+
+
+@pytest.mark.parametrize("name,strings,vocab", W.edge_cases(), ids=[e[0] for e in W.edge_cases()])
+def test_host_trie_edge_suite(P, name, strings, vocab):
+    h = host(P, strings, vocab)
+    o = Oracle(strings, vocab)
+    same_trie(h, o)
+    assert h.num_strings == len(set(strings))
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4])
+def test_host_trie_configs(P, cid):
+    w = W.config(cid)
+    h = host(P, w.strings, w.vocab)
+    same_trie(h, Oracle(w.strings, [b"x"]))
+    assert h.vocab_size == w.V and h.words_per_row == (w.V + 63) // 64
+
+
+def test_host_trie_forest(P):
+    w = W.config(5)
+    sets = w.set_offsets[:33]  # the first 32 sets
+    strings = w.strings[: sets[-1]]
+    h = host(P, strings, [b"x"], sets=sets)
+    same_trie(h, Oracle(strings, [b"x"], set_offsets=sets))
+    assert h.num_sets == 32
+
+
+def test_other_terminator(P):
+    strings = [b'say "hi"', b"say"]
+    h = host(P, strings, [b"a"], terminator=ord("|"))
+    same_trie(h, Oracle(strings, [b"a"], terminator=ord("|")))
+
+
+def raw_compile(P, sb, so, K, tb, to, V, set_off=None, S=0, terminator=0x22, flags=1):
+    L = P.lib()
+    opt = P.tam.Options(terminator, flags)
+    out = ctypes.c_void_p()
+    p = lambda a: None if a is None else ctypes.c_void_p(a.ctypes.data)  # noqa: E731
+    rc = L.tam_compile(p(sb), p(so), K, p(tb), p(to), V, p(set_off), S, ctypes.byref(opt), None, None,
+                       ctypes.byref(out))
+    if rc == 0:
+        L.tam_destroy(out)
+    return rc, L.tam_last_error().decode()
+
+
+def test_error_paths(P):
+    sb, so = P.tam.csr([b"ab", b"cd"])
+    tb, to = P.tam.csr([b"a", b"b"])
+    assert raw_compile(P, sb, so, 2, tb, to, 2)[0] == 0
+    assert raw_compile(P, sb, so, 0, tb, to, 2)[0] == -1                      # K = 0
+    assert raw_compile(P, sb, so, 2, tb, to, 0)[0] == -1                      # V = 0
+    assert raw_compile(P, sb, None, 2, tb, to, 2)[0] == -1                    # null offsets
+    bad = so.copy()
+    bad[1] = 5
+    bad[2] = 4
+    assert raw_compile(P, sb, bad, 2, tb, to, 2)[0] == -1                     # decreasing offsets
+    assert raw_compile(P, sb, so, 2, tb, to, 2, terminator=300)[0] == -1      # not a byte
+    rc, msg = raw_compile(P, sb, so, 2, tb, to, 2, terminator=ord("c"))
+    assert rc == -2 and "string 1" in msg                                     # terminator inside
+    sets = np.array([0, 2, 2], dtype=np.int64)
+    assert raw_compile(P, sb, so, 2, tb, to, 2, set_off=sets, S=2)[0] == -1   # empty set
+    sets = np.array([0, 1], dtype=np.int64)
+    assert raw_compile(P, sb, so, 2, tb, to, 2, set_off=sets, S=1)[0] == -1   # does not end at K
+
+
+def test_host_only_handle_refuses_device_work(P):
+    h = host(P, [b"ab"], [b"a"])
+    with pytest.raises(P.TamError) as e:
+        h.rebuild()
+    assert e.value.status == -6
+    L = P.lib()
+    assert L.tam_rebuild(h._raw, 0, None) == -6
+    assert L.tam_apply_mask(h._raw, None, 0, None, 0, 1, None) == -6
+    assert L.tam_advance(h._raw, None, None, 0, None, None) == -6
+    assert L.tam_export_rows(h._raw, None, 0, None, None) == -6
+    h.close()
+    h.close()
+
+
+def test_missing_library_fails_loudly(P, monkeypatch):
+    import paper_2608_12574_amd.tam as T
+    monkeypatch.setattr(T, "_lib", None)
+    monkeypatch.setattr(T, "LIB_PATH", "/nonexistent/libtam.so")
+    with pytest.raises(RuntimeError, match="no fallback"):
+        T.lib()

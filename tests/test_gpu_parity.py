@@ -1,0 +1,312 @@
+"""GPU parity: the HIP path against the oracle, bit for bit.
+
+Masks, advanced states and masked logits are integers / raw bit patterns, so
+every comparison here is exact.  Small cases compare every row and every
+(node, token) advance; the full-size configurations compare sampled rows (the
+root, every depth-1 node, random nodes, the last node), every row visited by
+the decode loops, and whole-table properties that hold at any size.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import Oracle
+from oracle.brute import Brute
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def P():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_12574_amd as P
+    P.lib()  # fails loudly when the library is missing
+    return P
+
+
+def rows_np(t) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint64)
+
+
+def gpu_rows(h, nodes):
+    ids = torch.as_tensor(np.asarray(nodes, dtype=np.int32), device="cuda")
+    return rows_np(h.export_rows(ids))
+
+
+def gpu_advance(h, nodes, toks):
+    n = torch.as_tensor(np.asarray(nodes, dtype=np.int32), device="cuda")
+    t = torch.as_tensor(np.asarray(toks, dtype=np.int32), device="cuda")
+    return h.advance(n, t).cpu().numpy()
+
+
+def bits_of(x):
+    return x.view(torch.int16 if x.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
+
+
+def host_logits(B, cols, dtype, seed):
+    rng = np.random.default_rng(seed)
+    x = torch.from_numpy(rng.standard_normal((B, cols), dtype=np.float32))
+    flat = x.view(-1)
+    k = min(flat.numel(), 256)
+    idx = torch.from_numpy(rng.choice(flat.numel(), size=k, replace=False))
+    flat[idx] = torch.tensor([float("nan"), -0.0, 0.0, float("inf"), 1e-40, -1e-40, 3e38, -5.0] * 32)[:k]
+    return x.to(torch.bfloat16) if dtype == "bf16" else x
+
+
+def check_apply(P, h, o, nodes, dtype, cols=None, seed=0, stride=None):
+    """GPU apply vs the oracle's apply on the same bits (optionally padded rows)."""
+    B = len(nodes)
+    cols = cols or o.V
+    x = host_logits(B, cols, dtype, seed)
+    if stride is not None and stride != cols:
+        big = torch.zeros((B, stride), dtype=x.dtype)
+        big[:, :cols] = x
+        dev = big.cuda()[:, :cols]
+    else:
+        dev = x.cuda()
+    ids = torch.as_tensor(np.asarray(nodes, dtype=np.int32), device="cuda")
+    h.apply_mask(ids, dev)
+    got = bits_of(dev)
+    ref_bits = bits_of(x)
+    exp = o.apply(np.asarray(nodes, dtype=np.int32),
+                  ref_bits.view(np.uint16 if dtype == "bf16" else np.uint32), 1 if dtype == "bf16" else 0)
+    assert np.array_equal(got.view(exp.dtype), exp)
+
+
+# ----------------------------------------------------------- small / exact --
+
+def full_check(P, strings, vocab, sets=None, flags=0, terminator=0x22):
+    o = Oracle(strings, vocab, set_offsets=sets, terminator=terminator)
+    h = P.compile(strings, vocab, sets=sets, flags=flags, terminator=terminator)
+    assert h.num_nodes == o.N
+    assert np.array_equal(h.roots, o.roots)
+    nodes = np.arange(-2, o.N + 2)
+    assert np.array_equal(gpu_rows(h, nodes), np.concatenate(
+        [np.zeros((2, o.W), np.uint64), o.mask_rows(np.arange(o.N)), np.zeros((2, o.W), np.uint64)]))
+    nn, tt = np.meshgrid(nodes, np.arange(-1, o.V + 1), indexing="ij")
+    assert np.array_equal(gpu_advance(h, nn.ravel(), tt.ravel()), o.advance(nn.ravel(), tt.ravel()))
+    for dtype in ("fp32", "bf16"):
+        check_apply(P, h, o, nodes, dtype, seed=len(nodes))
+    return h, o
+
+
+def test_worked_example(P):
+    vocab = [b"medical", b"_bill", b"_cod", b"_rec", b"ing", b"ords", b'"']
+    h, o = full_check(P, [b"medical_billing", b"medical_coding", b"medical_records"], vocab)
+    assert h.valid_pairs() == 10  # rows 0,7,12,19,26 (1+3+1+1+1) + '"' at 15,22,30
+    rows = gpu_rows(h, [0, 7, 12, 19, 26])
+    assert [int(r[0]) for r in rows] == [1, 0b1110, 0b10000, 0b10000, 0b100000]
+
+
+@pytest.mark.parametrize("name,strings,vocab", W.edge_cases(), ids=[e[0] for e in W.edge_cases()])
+def test_edge_suite(P, name, strings, vocab):
+    full_check(P, strings, vocab)
+
+
+@pytest.mark.parametrize("flags", [0, 2], ids=["dense", "no_table"])
+def test_tiny_random_sets(P, flags):
+    rng = np.random.default_rng(123)
+    alphabet = np.frombuffer(b'ab"\x80', dtype=np.uint8)
+    vocab = [b""] + [bytes(alphabet[rng.integers(0, 4, size=rng.integers(1, 5))]) for _ in range(150)]
+    for trial in range(12):
+        strings = [bytes(alphabet[rng.integers(0, 2, size=rng.integers(0, 7))]).replace(b'"', b"a")
+                   for _ in range(rng.integers(1, 7))]
+        h, o = full_check(P, strings, vocab, flags=flags)
+        b = Brute(strings, vocab)
+        for n in range(o.N):
+            got = np.unpackbits(gpu_rows(h, [n])[0].view(np.uint8), bitorder="little")[: len(vocab)]
+            assert set(np.flatnonzero(got).tolist()) == b.valid_set(n)
+
+
+def test_tiny_forest(P):
+    sets = [[b"ab", b"a"], [b""], [b"ba", b"bb", b"b"], [b"abc"]]
+    flat = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    vocab = [b"a", b"b", b"c", b'"', b"ab", b"b\"", b"abc\"", b""]
+    for flags in (0, 2):
+        full_check(P, flat, vocab, sets=offs, flags=flags)
+
+
+def test_other_terminator_and_high_bytes(P):
+    full_check(P, [b'x"y', b"x", b"\xff\x00"], [b"x", b'"', b'"y', b"|", b"y|", b"\xff", b"\x00|"],
+               terminator=ord("|"))
+
+
+# ------------------------------------------------------------ configurations --
+
+def sample_nodes(o: Oracle, k: int, seed: int):
+    rng = np.random.default_rng(seed)
+    depth1 = np.flatnonzero(o.depth == 1)
+    finals = np.flatnonzero(o.is_final)[:4]
+    pick = np.concatenate([o.roots, depth1[:64], rng.integers(0, o.N, size=k), finals, [o.N - 1]])
+    return np.unique(pick).astype(np.int32)
+
+
+@pytest.fixture(scope="module", params=[1, 2, 3, 4], ids=["c1", "c2", "c3", "c4"])
+def compiled(request, P):
+    w = W.config(request.param)
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab)
+    yield w, o, h
+    h.close()
+    torch.cuda.empty_cache()
+
+
+def test_config_rows(P, compiled):
+    w, o, h = compiled
+    assert h.num_nodes == o.N
+    nodes = np.arange(o.N, dtype=np.int32) if w.config_id == 1 else sample_nodes(o, 96, w.config_id)
+    for i in range(0, len(nodes), 512):
+        assert np.array_equal(gpu_rows(h, nodes[i:i + 512]), o.mask_rows(nodes[i:i + 512]))
+
+
+def test_config_table_properties(P, compiled):
+    """Whole-table facts at full size: with all 256 byte tokens in the vocabulary,
+    a row is empty exactly at final nodes, and padding words stay zero."""
+    w, o, h = compiled
+    table = h._alloc.live[h.table_ptr].view(torch.int64).view(h.num_nodes, h.row_stride_words)
+    nonempty = torch.zeros(h.num_nodes, dtype=torch.bool, device="cuda")
+    for i in range(0, h.num_nodes, 16384):
+        blk = table[i:i + 16384]
+        nonempty[i:i + 16384] = blk[:, : h.words_per_row].ne(0).any(dim=1)
+        if h.row_stride_words > h.words_per_row:
+            assert not blk[:, h.words_per_row:].ne(0).any().item()
+    assert np.array_equal(nonempty.cpu().numpy(), o.is_final == 0)
+    if w.config_id <= 2:
+        # total number of valid pairs against the oracle's full table
+        M = 0
+        for i in range(0, o.N, 4096):
+            rows = o.mask_rows(np.arange(i, min(o.N, i + 4096), dtype=np.int32))
+            M += int(np.unpackbits(rows.view(np.uint8)).sum())
+        assert h.valid_pairs() == M
+
+
+def test_config_rows_vs_advance(P, compiled):
+    """mask[n][v] <=> advance(n, v) != dead, on GPU outputs, for sampled nodes."""
+    w, o, h = compiled
+    nodes = sample_nodes(o, 6, 100 + w.config_id)[:12]
+    rows = gpu_rows(h, nodes)
+    for r, n in enumerate(nodes):
+        adv = gpu_advance(h, np.full(o.V, n), np.arange(o.V))
+        bits = np.unpackbits(rows[r].view(np.uint8), bitorder="little")[: o.V].astype(bool)
+        assert np.array_equal(adv != -1, bits)
+        assert np.array_equal(adv, o.advance(np.full(o.V, n, np.int32), np.arange(o.V, dtype=np.int32)))
+
+
+def test_config_apply(P, compiled):
+    w, o, h = compiled
+    if w.node_mode == "uniform":
+        nodes = W.uniform_nodes(w.config_id, o.N, w.batch)
+    else:
+        nodes = np.full(w.batch, 0, np.int32)
+    check_apply(P, h, o, nodes, w.dtype, seed=w.config_id)
+
+
+def test_config_decode(P, compiled):
+    """The serving loop: apply the mask, pick a valid token (uniformly, from the
+    oracle's row), advance on GPU and oracle; finished rows restart at the root."""
+    w, o, h = compiled
+    rng = np.random.default_rng([w.config_id, W.ROLE_CHOICE, 2])
+    nodes = W.uniform_nodes(w.config_id, o.N, w.batch) if w.node_mode == "uniform" \
+        else np.zeros(w.batch, np.int32)
+    nodes = np.where(o.is_final[nodes] == 1, 0, nodes).astype(np.int32)
+    steps = min(w.decode_steps, 32)
+    for step in range(steps):
+        rows = o.mask_rows(nodes)
+        if step % 8 == 0:
+            assert np.array_equal(gpu_rows(h, nodes), rows)
+        toks = W.choose_valid_tokens(rng, rows, o.V)
+        got = gpu_advance(h, nodes, toks)
+        exp = o.advance(nodes, toks)
+        assert np.array_equal(got, exp), step
+        nodes = np.where(o.is_final[exp] == 1, 0, exp).astype(np.int32)
+
+
+def test_config_rebuild_identical(P, compiled):
+    w, o, h = compiled
+    nodes = sample_nodes(o, 32, 7)
+    before = gpu_rows(h, nodes)
+    M = h.valid_pairs()
+    h.rebuild()
+    assert np.array_equal(gpu_rows(h, nodes), before)
+    assert h.valid_pairs() == M
+
+
+# ---------------------------------------------------------- sparse / forest --
+
+def test_no_table_matches_dense_c4(P):
+    w = W.config(4)
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=P.FLAG_NO_TABLE)
+    assert h.row_stride_words == 0
+    nodes = sample_nodes(o, 64, 44)
+    assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+    check_apply(P, h, o, W.uniform_nodes(4, o.N, 256), "bf16", seed=4)
+    check_apply(P, h, o, W.uniform_nodes(4, o.N, 16, 1), "fp32", seed=5)
+
+
+def test_forest_c5(P):
+    """Config 5: 256 per-query sets of 500 strings as one forest (sparse rows).
+    The oracle runs on sampled rows and on every row the 16-step decode visits."""
+    w = W.config(5)
+    o = Oracle(w.strings, w.vocab, set_offsets=w.set_offsets)
+    h = P.compile(w.strings, w.vocab, sets=w.set_offsets, flags=P.FLAG_NO_TABLE)
+    assert h.num_nodes == o.N and np.array_equal(h.roots, o.roots)
+    nodes = sample_nodes(o, 64, 55)
+    assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+    rng = np.random.default_rng([5, W.ROLE_CHOICE, 2])
+    cur = o.roots.astype(np.int32).copy()
+    for step in range(w.decode_steps):
+        rows = o.mask_rows(cur)
+        assert np.array_equal(gpu_rows(h, cur), rows)
+        if step in (0, 7):
+            check_apply(P, h, o, cur, "bf16", seed=50 + step)
+        toks = W.choose_valid_tokens(rng, rows, o.V)
+        exp = o.advance(cur, toks)
+        assert np.array_equal(gpu_advance(h, cur, toks), exp)
+        cur = np.where(o.is_final[exp] == 1, o.roots, exp).astype(np.int32)
+    h.close()
+
+
+# ------------------------------------------------------------ layouts / edges --
+
+def test_ragged_vocab_and_strides(P):
+    w = W.config(1)
+    vocab = w.vocab[:1037]                      # V not a multiple of 8 or 64
+    o = Oracle(w.strings, vocab)
+    h = P.compile(w.strings, vocab)
+    nodes = np.array([0, 1, 5, o.N - 1, -1, o.N, 2 ** 30], dtype=np.int32)
+    for dtype in ("fp32", "bf16"):
+        check_apply(P, h, o, nodes, dtype, seed=1)                  # contiguous rows
+        check_apply(P, h, o, nodes, dtype, cols=1037, stride=1040, seed=2)   # aligned padded rows
+        check_apply(P, h, o, nodes, dtype, cols=1037, stride=1045, seed=3)   # unaligned rows
+    assert np.array_equal(gpu_rows(h, nodes), np.concatenate(
+        [o.mask_rows(nodes[:4]), np.zeros((3, o.W), np.uint64)]))
+    # zero-sized calls are no-ops
+    empty = torch.empty(0, dtype=torch.int32, device="cuda")
+    h.apply_mask(empty, torch.empty((0, 1037), device="cuda"))
+    assert h.advance(empty, empty).numel() == 0
+
+
+def test_many_rows_grid_split(P):
+    """More than 65,535 batch rows in one call (the launcher splits the grid)."""
+    strings = [b"ab", b"b"]
+    vocab = [b"a", b"b", b"ab", b'"', b'b"'] + [b"z"] * 123
+    o = Oracle(strings, vocab)
+    h = P.compile(strings, vocab)
+    B = 70000
+    nodes = np.random.default_rng(0).integers(-1, o.N + 1, size=B).astype(np.int32)
+    ids = torch.as_tensor(nodes, device="cuda")
+    x = torch.zeros((B, 128), dtype=torch.bfloat16, device="cuda")
+    h.apply_mask(ids, x)
+    rows = o.mask_rows(np.arange(o.N, dtype=np.int32))
+    valid = np.unpackbits(rows.view(np.uint8), axis=1, bitorder="little")[:, :128].astype(bool)
+    exp = np.zeros((B, 128), dtype=bool)
+    live = (nodes >= 0) & (nodes < o.N)
+    exp[live] = valid[nodes[live]]
+    assert np.array_equal(~torch.isinf(x).cpu().numpy(), exp)
+    assert np.array_equal(gpu_rows(h, nodes[:66000]), np.where(
+        live[:66000, None], rows[np.clip(nodes[:66000], 0, o.N - 1)], np.uint64(0)))
