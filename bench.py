@@ -1,8 +1,9 @@
 """Benchmark of the trie-automaton mask path on one MI355X.
 
 One step = one pass of the whole device hot path over one batch:
-  1. the per-node valid lists (suffix probes + scan + fill),
-  2. the dense [N, W] bitmask table written from them (the dominant kernel),
+  1. the device compile: the zero fill of the dense [N, W] bitmask table (the
+     dominant kernel) with the suffix probes running beside it on a second
+     stream, then every valid (node, token) bit set by 64-bit atomics,
   3. the mask apply on [B, V] logits,
   4. the state advance of the B rows.
 Inputs (trie and vocabulary tables, node ids, tokens, logits) are resident in
@@ -130,29 +131,26 @@ def main():
     out = torch.empty_like(ids)
     del probe
 
-    LISTS, TABLE = P.PHASE_LISTS, P.PHASE_TABLE
     has_table = h.row_stride_words > 0
 
     def step(i, ev=None):
+        """device compile (table: probes beside the zero fill, then the marks;
+        sparse handles: the lists), apply, advance."""
         if ev is not None:
             ev[0].record()
-        h.rebuild(phases=LISTS)
+        h.rebuild()
         if ev is not None:
             ev[1].record()
-        if has_table:
-            h.rebuild(phases=TABLE)
-        if ev is not None:
-            ev[2].record()
         h.apply_mask(ids, bufs[i % nbuf])
         if ev is not None:
-            ev[3].record()
+            ev[2].record()
         h.advance(ids, toks, out=out)
         if ev is not None:
-            ev[4].record()
+            ev[3].record()
 
     for i in range(args.warmup):
         step(i)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -160,13 +158,26 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    lists_ms = np.mean([e[0].elapsed_time(e[1]) for e in evs])
-    table_ms = np.mean([e[1].elapsed_time(e[2]) for e in evs])
-    apply_ms = np.mean([e[2].elapsed_time(e[3]) for e in evs])
-    adv_ms = np.mean([e[3].elapsed_time(e[4]) for e in evs])
+    dev_ms = np.mean([e[0].elapsed_time(e[1]) for e in evs])     # device compile of one step
+    apply_ms = np.mean([e[1].elapsed_time(e[2]) for e in evs])
+    adv_ms = np.mean([e[2].elapsed_time(e[3]) for e in evs])
     pairs_per_s = N * V / (ms_step / 1e3)
-    print(f"[bench] step {ms_step:.3f} ms (lists {lists_ms:.3f}, table {table_ms:.3f}, apply {apply_ms:.4f}, "
-          f"advance {adv_ms:.4f})", flush=True)
+
+    # ---- the dominant kernel alone: the table's zero fill (one launch per rebuild) ----
+    zero_ms = mark_ms = float("nan")
+    if has_table:
+        zev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for e in zev:
+            e[0].record()
+            h.rebuild(phases=P.PHASE_ZERO)
+            e[1].record()
+            h.rebuild(phases=P.PHASE_MARK)
+            e[2].record()
+        torch.cuda.synchronize()
+        zero_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in zev]))
+        mark_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in zev]))
+    print(f"[bench] step {ms_step:.3f} ms (device compile {dev_ms:.3f}, apply {apply_ms:.4f}, advance {adv_ms:.4f}); "
+          f"alone: zero {zero_ms:.3f}, probes+marks {mark_ms:.3f}", flush=True)
 
     # ---- mask apply alone: the paper's protocol (200 warm-up + 1,000 timed) ----
     for i in range(args.apply_warmup):
@@ -210,19 +221,20 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # ---- roofline of the dominant kernel (the dense table write) ----
-    table_bytes = N * Wd * 8                 # algorithmic: the canonical rows
-    tr = load_traffic(f"k_rows_{w.name}_traffic.json", sha)
+    # ---- roofline of the dominant kernel: the table's zero fill ----
+    table_bytes = N * Wd * 8                 # algorithmic: the canonical rows, written once
+    tr = load_traffic(f"k_zero_{w.name}_traffic.json", sha) if has_table else None
+    kern_ms = zero_ms if has_table else dev_ms
     roofline = {
-        "kernel": "k_rows" if has_table else "k_probe",
+        "kernel": "k_zero" if has_table else "k_probe+k_count+k_scan+k_fill",
         "bound": "hbm",
-        "achieved": round(table_bytes / (table_ms * 1e-3) / 1e9, 1),
+        "achieved": round(table_bytes / (kern_ms * 1e-3) / 1e9, 1),
         "peak": HBM_PEAK_GBPS,
         "unit": "GB/s",
-        "frac": round(table_bytes / (table_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "frac": round(table_bytes / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "traffic": tr["bytes_per_launch"] if tr else None,
         "algorithmic_bytes": table_bytes,
-        "avg_launch_ms": round(float(table_ms), 4),
+        "avg_launch_ms": round(float(kern_ms), 4),
     }
     tra = load_traffic(f"k_apply_{w.name}_traffic.json", sha)
     roofline_apply = {
@@ -286,9 +298,10 @@ def main():
         "roofline_apply": roofline_apply,
         "cpu_baseline": cpu,
         "compile_ms": {"end_to_end_min": round(min(e2e), 3), "end_to_end_all": [round(x, 3) for x in e2e],
-                       "device": round(float(lists_ms + table_ms), 4),
-                       "device_frac_of_hbm_roofline": round(table_bytes / ((lists_ms + table_ms) * 1e-3) / 1e9
-                                                            / HBM_PEAK_GBPS, 4),
+                       "device": round(float(dev_ms), 4),
+                       "device_zero_alone_ms": round(zero_ms, 4),
+                       "device_probe_mark_alone_ms": round(mark_ms, 4),
+                       "device_frac_of_hbm_roofline": round(table_bytes / (dev_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                        "phases_last_compile": phases},
         "apply": {"us": round(apply_us, 3), "GBps": round(apply_gbps, 1), "bytes": apply_bytes,
                   "frac_of_hbm_roofline": round(apply_gbps / HBM_PEAK_GBPS, 4), "iters": args.apply_iters},

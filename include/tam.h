@@ -122,16 +122,16 @@ typedef struct {
     const uint64_t *table;    /* device [N][row_stride_words]; NULL with TAM_FLAG_NO_TABLE */
 } tam_info;
 
-/* Host-side wall times of the last tam_compile and device times (HIP events,
- * only with TAM_FLAG_TIMING; else -1) of the last tam_compile/tam_rebuild. */
+/* Host-side wall times of the last tam_compile, and device times (HIP events,
+ * only with TAM_FLAG_TIMING; else -1) of the last tam_compile/tam_rebuild that
+ * ran the handle's default phases. */
 typedef struct {
     double host_trie_ms;   /* dedupe, sort, preorder trie, child tables */
     double host_vocab_ms;  /* token offsets, vocabulary hash, length table */
     double upload_ms;      /* allocation + enqueue of the host-to-device copies */
-    float dev_count_ms;    /* suffix probes counting valid tokens per node */
-    float dev_scan_ms;     /* prefix sum of the counts into row offsets */
-    float dev_fill_ms;     /* suffix probes writing the sparse valid lists */
-    float dev_table_ms;    /* dense [N, W] bitmask table written from the lists */
+    float dev_lists_ms;    /* sparse valid lists: suffix probes, prefix sum, fill */
+    float dev_zero_ms;     /* zero fill of the dense table */
+    float dev_mark_ms;     /* suffix probes setting the valid bits of the dense table */
     float dev_total_ms;    /* first device phase start to last device phase end */
 } tam_timing;
 
@@ -168,15 +168,18 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
                        tam_handle **out);
 
 enum {
-    TAM_PHASE_LISTS = 1u << 0, /* per-node valid lists (suffix probes, scan, fill) */
-    TAM_PHASE_TABLE = 1u << 1  /* dense table written from the lists */
+    TAM_PHASE_LISTS = 1u << 0, /* sparse per-node valid lists (suffix probes, prefix sum, fill) */
+    TAM_PHASE_ZERO = 1u << 1,  /* zero fill of the dense table */
+    TAM_PHASE_MARK = 1u << 2,  /* suffix probes setting the valid bits of the zeroed table */
+    TAM_PHASE_TABLE = TAM_PHASE_ZERO | TAM_PHASE_MARK
 };
 
 /*
  * tam_rebuild -- rerun device phases of tam_compile from the handle's resident
- * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask, 0 =
- * both; TAM_PHASE_TABLE alone re-uses the current lists.  Used to time the
- * device phase kernel by kernel and to restore a table.
+ * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask; 0 =
+ * the handle's default (TAM_PHASE_TABLE with a dense table, TAM_PHASE_LISTS
+ * with TAM_FLAG_NO_TABLE).  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the same
+ * bits into the current table.  Used to time the device phase kernel by kernel.
  */
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
 
@@ -220,8 +223,9 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
 
 /*
  * tam_valid_pairs -- M = sum over all nodes of |valid[n]|, the number of
- * (node, token) pairs that are valid.  Copies one value from the device and
- * synchronises `stream`.
+ * (node, token) pairs that are valid, as found by the last table or list
+ * build.  Copies the per-block counts from the device and synchronises
+ * `stream`.
  */
 tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out);
 

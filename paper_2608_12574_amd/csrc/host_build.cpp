@@ -65,8 +65,11 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->edge.reserve((size_t)reserve_nodes);
     h->is_final.reserve((size_t)reserve_nodes);
     h->node_pos.reserve((size_t)reserve_nodes);
-    h->blob.reserve((size_t)(total + 2 * K));
-    h->node_at.reserve((size_t)(total + 2 * K));
+    h->blob.reserve((size_t)(total + 2 * K + 2 * kBlobPad));
+    h->node_at.reserve((size_t)(total + 2 * K + 2 * kBlobPad));
+    // zero pad in front, so that a node's 16-byte path window never starts before the blob
+    h->blob.assign((size_t)kBlobPad, 0);
+    h->node_at.assign((size_t)kBlobPad, 0);
 
     std::vector<int64_t> order;
     std::vector<int32_t> path;
@@ -126,6 +129,9 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             }
         }
     }
+    // zero pad behind, so that aligned window loads stay inside the blob
+    h->blob.insert(h->blob.end(), (size_t)kBlobPad, 0);
+    h->node_at.insert(h->node_at.end(), (size_t)kBlobPad, 0);
     h->N = N;
     h->S = S;
     h->blob_bytes = (int64_t)h->blob.size();
@@ -151,9 +157,11 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
 
 /*
  * Vocabulary tables (the paper's vocabulary decoding and its per-tokenizer
- * matcher, built here as an exact open-addressing hash of every distinct token
- * string keyed by its bytes read last-to-first).  Duplicate strings share a
- * slot and chain their ids in ascending order.
+ * matcher, built here as an exact hash of every distinct token string keyed by
+ * its bytes read last-to-first).  Slots live in buckets of kBucket 32-bit
+ * fingerprints; a key starts at its home bucket and moves to the next bucket
+ * only when the bucket is full.  Duplicate strings share a slot and chain their
+ * ids in ascending order.
  */
 tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_handle *h,
                        std::string *err) {
@@ -170,48 +178,69 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_hand
     int64_t max_len = 0;
     for (int64_t v = 0; v <= V; ++v) h->tok_off[(size_t)v] = (uint32_t)(to[v] - to[0]);
     for (int64_t v = 0; v < V; ++v) max_len = std::max<int64_t>(max_len, to[v + 1] - to[v]);
+    if (max_len > 65535) {
+        *err = "a token is longer than 65535 bytes";
+        return TAM_E_TOOLARGE;
+    }
     h->max_tok_len = max_len;
     h->len_present.assign((size_t)(max_len + 1), 0);
+    h->len_mask = 0;
 
-    uint64_t cap = 1024;
+    uint64_t cap = 64;
     while (cap < (uint64_t)(2 * V)) cap <<= 1;
-    h->slots.assign(cap, HashSlot{0, -1, 0});
+    const uint64_t nbuckets = cap / kBucket;
+    h->fps.assign(cap, 0u);
+    h->srev.assign(cap, SlotRev{0, 0});
+    h->smeta.assign(cap, SlotMeta{-1, 0, 0});
     h->dup_next.assign((size_t)V, -1);
     std::vector<int32_t> last(cap, -1);
-    const uint64_t mask = cap - 1;
     const uint8_t *blob = h->tok_blob.data();
     for (int64_t v = 0; v < V; ++v) {
         const uint32_t off = h->tok_off[(size_t)v];
         const uint32_t len = h->tok_off[(size_t)v + 1] - off;
         if (len == 0) continue;
         h->len_present[len] = 1;
+        if (len < 64) h->len_mask |= 1ull << len;
         uint64_t hh = kHashSeed;
         for (int64_t i = (int64_t)len - 1; i >= 0; --i) hh = hash_step(hh, blob[off + i]);
         const uint64_t key = hash_final(hh, len);
-        uint64_t i = key & mask;
-        for (;;) {
-            HashSlot &s = h->slots[i];
-            if (s.first < 0) {
-                s.key = key;
-                s.first = (int32_t)v;
-                s.count = 1;
-                last[i] = (int32_t)v;
-                break;
-            }
-            if (s.key == key) {
-                const uint32_t o2 = h->tok_off[(size_t)s.first];
-                const uint32_t l2 = h->tok_off[(size_t)s.first + 1] - o2;
-                if (l2 == len && std::memcmp(blob + o2, blob + off, len) == 0) {
-                    h->dup_next[(size_t)last[i]] = (int32_t)v;
-                    last[i] = (int32_t)v;
-                    ++s.count;
-                    break;
+        const uint32_t fp = fingerprint(key);
+        uint64_t b = (key & (cap - 1)) / kBucket;
+        bool placed = false;
+        while (!placed) {
+            for (int i = 0; i < kBucket && !placed; ++i) {
+                const uint64_t s = b * kBucket + (uint64_t)i;
+                if (h->fps[s] == 0) {
+                    h->fps[s] = fp;
+                    SlotRev r{0, 0};
+                    for (uint32_t k = 0; k < len && k < 16; ++k) {
+                        const uint64_t c = blob[off + len - 1 - k];
+                        if (k < 8)
+                            r.lo |= c << (8 * k);
+                        else
+                            r.hi |= c << (8 * (k - 8));
+                    }
+                    h->srev[s] = r;
+                    h->smeta[s] = SlotMeta{(int32_t)v, (uint16_t)len, 1};
+                    last[s] = (int32_t)v;
+                    placed = true;
+                } else if (h->fps[s] == fp && h->smeta[s].len == len) {
+                    const uint32_t o2 = h->tok_off[(size_t)h->smeta[s].first];
+                    if (std::memcmp(blob + o2, blob + off, len) == 0) {
+                        if (h->smeta[s].count == 65535) {
+                            *err = "more than 65535 tokens share one byte string";
+                            return TAM_E_TOOLARGE;
+                        }
+                        h->dup_next[(size_t)last[s]] = (int32_t)v;
+                        last[s] = (int32_t)v;
+                        ++h->smeta[s].count;
+                        placed = true;
+                    }
                 }
             }
-            i = (i + 1) & mask;
+            b = (b + 1) % nbuckets;
         }
     }
-    (void)err;
     return TAM_OK;
 }
 
@@ -224,10 +253,9 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_hand
 int64_t entry_upper_bound(const tam_handle *h) {
     const int64_t L = h->max_tok_len;
     std::vector<int64_t> dup(L + 1, 0);
-    for (const HashSlot &s : h->slots) {
+    for (const SlotMeta &s : h->smeta) {
         if (s.first < 0) continue;
-        const int64_t len = h->tok_off[(size_t)s.first + 1] - h->tok_off[(size_t)s.first];
-        dup[(size_t)len] = std::max<int64_t>(dup[(size_t)len], s.count);
+        dup[(size_t)s.len] = std::max<int64_t>(dup[(size_t)s.len], s.count);
     }
     std::vector<int64_t> cum(L + 1, 0);
     for (int64_t d = 1; d <= L; ++d) cum[(size_t)d] = cum[(size_t)d - 1] + dup[(size_t)d];

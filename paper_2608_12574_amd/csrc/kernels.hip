@@ -1,25 +1,25 @@
 // HIP kernels of libtam for gfx950 (CDNA4, wave64).
 //
 // Mask compile (Section 4.1, valid[n] for every trie node n):
-//   k_probe<false>  count   -- every non-root node m walks back over the last
-//                              d <= min(depth(m), max_len) bytes of its prefix and
-//                              looks each suffix up in the vocabulary hash; a hit
-//                              of token t at distance d = |t| means t is valid at
-//                              the ancestor d levels up (its walk ends at m).  This
-//                              is the paper's "credit the match to the node |t|
-//                              bytes back" (Section 4.2), done for all nodes at
-//                              once instead of along a DFS.
-//   k_scan_*                -- exclusive prefix sum of the per-node counts.
-//   k_probe<true>   fill    -- the same probes, writing the token ids into the
-//                              per-node lists (order within a list is irrelevant).
-//   k_rows                  -- one (row, tile) per work item: the tile's bits are
-//                              OR-ed into an LDS image from the row's list, then
-//                              the image is streamed to HBM with 16-byte
-//                              non-temporal stores and cleared for the next item.
+//   k_count  -- one lane per non-root node m: the last d <= min(depth(m), ℓ)
+//               bytes of prefix(m) are hashed (read backwards from a 16-byte
+//               register window) and looked up in the vocabulary table; a hit of
+//               token t at d = |t| means t is valid at the ancestor d levels up,
+//               because t's walk from there ends at m.  This is the paper's
+//               crediting of a match to the node |t| bytes back (Section 4.2),
+//               done for all nodes at once instead of along a DFS.  Counts per
+//               ancestor; keeps the hit slots for the fill pass.
+//   k_scan_* -- exclusive prefix sum of the counts into row offsets.
+//   k_fill   -- writes the hits' token ids into the per-node lists.
+//   k_zero   -- zero fill of the dense table (pure streaming stores).
+//   k_mark   -- the same probes as k_count, each hit OR-ed into the table with
+//               a 64-bit atomic (dense tables need no lists).
+//   k_rows   -- one wave per row builds rows in registers from the lists
+//               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
-//   k_apply                 -- write-mostly masking of [B, V] logits.
-//   k_advance               -- B byte walks over the child tables.
-//   k_export_dense          -- canonical rows out of the dense table.
+//   k_apply  -- write-mostly masking of [B, V] logits.
+//   k_advance-- B byte walks over the child tables.
+//   k_export_dense -- canonical rows out of the dense table.
 #include <hip/hip_runtime.h>
 
 #include "tam_internal.hpp"
@@ -29,8 +29,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
-constexpr int kTileWords = 4096;     // 64-bit words per LDS row image (32 KiB)
-constexpr int kApplyUnits = 4;       // 16-byte chunks per thread in k_apply
+constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -59,58 +58,265 @@ __global__ void __launch_bounds__(kBlock) k_fill_i32(int32_t *p, int64_t n, int3
 
 // ---------------------------------------------------------------- probes ---
 
-// Slot of the token string equal to blob[pos-d+1 .. pos] (key = its hash), or -1.
-__device__ __forceinline__ int64_t probe(const DevTables &t, uint64_t key, int64_t pos, int d) {
-    uint64_t i = key & t.slot_mask;
+// Reversed 16-byte path window ending at blob[pos]: byte k of (lo, hi) is
+// blob[pos - k].  Five aligned dword loads; the blob carries 16 zero bytes on
+// both sides, so they stay inside it.
+__device__ __forceinline__ void load_window(const uint8_t *blob, int64_t pos, uint64_t &lo, uint64_t &hi) {
+    const int64_t ws = pos - (kWin - 1);
+    const int64_t a = ws & ~int64_t(3);
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(blob + a);
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
+    const uint32_t sh = (uint32_t)(ws - a) * 8u;
+    const uint32_t x0 = (uint32_t)((((uint64_t)w1 << 32) | w0) >> sh);
+    const uint32_t x1 = (uint32_t)((((uint64_t)w2 << 32) | w1) >> sh);
+    const uint32_t x2 = (uint32_t)((((uint64_t)w3 << 32) | w2) >> sh);
+    const uint32_t x3 = (uint32_t)((((uint64_t)w4 << 32) | w3) >> sh);
+    lo = __builtin_bswap64(((uint64_t)x3 << 32) | x2);
+    hi = __builtin_bswap64(((uint64_t)x1 << 32) | x0);
+}
+
+__device__ __forceinline__ uint32_t window_byte(uint64_t lo, uint64_t hi, int k) {
+    return (uint32_t)((k < 8 ? lo >> (8 * k) : hi >> (8 * (k - 8))) & 0xffu);
+}
+
+__device__ __forceinline__ bool has_len(const DevTables &t, int d) {
+    return d < 64 ? ((t.len_mask >> d) & 1ull) != 0 : t.len_present[d] != 0;
+}
+
+// The first min(d, 16) reversed bytes of the suffix equal the slot's.
+__device__ __forceinline__ bool same_head(uint64_t lo, uint64_t hi, const SlotRev &r, int d) {
+    if (d >= 16) return lo == r.lo && hi == r.hi;
+    if (d >= 8) {
+        const uint64_t m = d == 8 ? 0ull : (~0ull >> (64 - 8 * (d - 8)));
+        return lo == r.lo && (hi & m) == r.hi;
+    }
+    return (lo & (~0ull >> (64 - 8 * d))) == r.lo && r.hi == 0ull;
+}
+
+// Slot whose token equals the suffix of length d ending at blob[pos] (key =
+// its hash, (lo, hi) = its reversed window), or -1; its payload goes to *meta.
+// Buckets are scanned from the key's home bucket until one with an empty slot
+// (load <= 1/2 guarantees one exists).  The 16 fingerprints of a bucket are
+// compared into a bit mask first, so a wave reads the payload of its matching
+// lanes in one step instead of one divergent branch per slot position.
+__device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d, uint64_t lo, uint64_t hi,
+                                         int64_t pos, SlotMeta *meta) {
+    const uint32_t fp = fingerprint(key);
+    const uint64_t bmask = t.slot_mask / kBucket;
+    uint64_t b = (key & t.slot_mask) / kBucket;
     for (;;) {
-        const HashSlot s = t.slots[i];
-        if (s.first < 0) return -1;
-        if (s.key == key) {
-            const uint32_t off = t.tok_off[s.first];
-            const uint32_t len = t.tok_off[s.first + 1] - off;
-            if (len == (uint32_t)d) {
-                const uint8_t *a = t.tok_blob + off;
-                const uint8_t *b = t.blob + (pos - d + 1);
+        const u32x4 *q = reinterpret_cast<const u32x4 *>(t.fps + b * kBucket);
+        const u32x4 f0 = q[0], f1 = q[1], f2 = q[2], f3 = q[3];
+        const uint32_t f[kBucket] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w,
+                                     f2.x, f2.y, f2.z, f2.w, f3.x, f3.y, f3.z, f3.w};
+        uint32_t match = 0, empty = 0;
+#pragma unroll
+        for (int i = 0; i < kBucket; ++i) {
+            match |= (f[i] == fp ? 1u : 0u) << i;
+            empty |= (f[i] == 0u ? 1u : 0u) << i;
+        }
+        while (match) {
+            const int i = __builtin_ctz(match);
+            match &= match - 1;
+            const int32_t s = (int32_t)(b * kBucket + (uint64_t)i);
+            const SlotMeta m = t.smeta[s];
+            const SlotRev r = t.srev[s];
+            if ((int)m.len == d && same_head(lo, hi, r, d)) {
                 bool eq = true;
-                for (int k = 0; k < d; ++k) {
-                    if (a[k] != b[k]) {
-                        eq = false;
-                        break;
-                    }
+                if (d > kWin) {  // bytes beyond the window: compare in memory
+                    const uint8_t *tb = t.tok_blob + t.tok_off[m.first];
+                    const uint8_t *pb = t.blob + (pos - d + 1);
+                    for (int k = 0; k < d - kWin && eq; ++k) eq = tb[k] == pb[k];
                 }
-                if (eq) return (int64_t)i;
+                if (eq) {
+                    *meta = m;
+                    return s;
+                }
             }
         }
-        i = (i + 1) & t.slot_mask;
+        if (empty) return -1;
+        b = (b + 1) & bmask;
     }
 }
 
-template <bool kFill>
+// Writes the token ids of slot s into the list of node n.
+__device__ __forceinline__ void emit(const DevTables &t, int32_t s, int32_t n) {
+    const SlotMeta m = t.smeta[s];
+    const int32_t at = t.row_ptr[n] + atomicAdd(&t.cursor[n], (int32_t)m.count);
+    int32_t v = m.first;
+    for (int k = 0; k < (int)m.count; ++k) {
+        t.entries[at + k] = v;
+        v = t.dup_next[v];
+    }
+}
+
+// Probe pass: one lane per node m.  The suffix of length d of prefix(m) equal to
+// token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
+// d <= 16 the hit slot (or -1) goes to hits[d-1][m]; the slots are kept in
+// registers and stored after the last probe, so no probe load waits behind a
+// store (loads and stores share one vector-memory counter here).  Longer tokens
+// are handled by the consumers, which probe those lengths again.
 __global__ void __launch_bounds__(kBlock) k_probe(DevTables t) {
     const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (m >= t.N) return;
     const int64_t pos = t.node_pos[m];
     if (pos < 0) return;  // a root ends no token
-    const int L = min(t.depth[m], t.max_len);
+    const int Lw = min(min(t.depth[m], t.max_len), kWin);
+    uint64_t lo, hi;
+    load_window(t.blob, pos, lo, hi);
     uint64_t h = kHashSeed;
-    for (int d = 1; d <= L; ++d) {
-        h = hash_step(h, t.blob[pos - d + 1]);
-        if (!t.len_present[d]) continue;
-        const int64_t si = probe(t, hash_final(h, (uint32_t)d), pos, d);
-        if (si < 0) continue;
-        const HashSlot s = t.slots[si];
-        const int32_t n = t.node_at[pos - d];  // the ancestor where the token starts
-        if (!kFill) {
-            atomicAdd(&t.count[n], s.count);
-        } else {
-            int32_t at = t.row_ptr[n] + atomicAdd(&t.cursor[n], s.count);
-            int32_t v = s.first;
-            for (int k = 0; k < s.count; ++k) {
-                t.entries[at + k] = v;
-                v = t.dup_next[v];
+    int32_t slot[kWin];
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d) {
+        slot[d - 1] = -1;
+        if (d <= Lw) {
+            h = hash_step(h, window_byte(lo, hi, d - 1));
+            if (has_len(t, d)) {
+                SlotMeta mt;
+                slot[d - 1] = probe(t, hash_final(h, (uint32_t)d), d, lo, hi, pos, &mt);
             }
         }
     }
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d)
+        if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = slot[d - 1];
+}
+
+// Calls f(slot, d) for every token string ending at node m longer than the
+// window (d > 16), probing those lengths again (vocabularies rarely have them).
+template <typename F>
+__device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L, F &&f) {
+    uint64_t lo, hi;
+    load_window(t.blob, pos, lo, hi);
+    uint64_t h = kHashSeed;
+    for (int d = 1; d <= kWin; ++d) h = hash_step(h, window_byte(lo, hi, d - 1));
+    for (int d = kWin + 1; d <= L; ++d) {
+        h = hash_step(h, t.blob[pos - d + 1]);
+        if (!has_len(t, d)) continue;
+        SlotMeta mt;
+        const int32_t s = probe(t, hash_final(h, (uint32_t)d), d, lo, hi, pos, &mt);
+        if (s >= 0) f(s, d);
+    }
+}
+
+// Count pass (lists): per-node numbers of valid token ids.
+__global__ void __launch_bounds__(kBlock) k_count(DevTables t) {
+    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (m >= t.N) return;
+    const int64_t pos = t.node_pos[m];
+    if (pos < 0) return;
+    const int L = min(t.depth[m], t.max_len);
+    const int Lw = min(L, kWin);
+    int32_t s[kWin], n[kWin], c[kWin];
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d) {
+        n[d - 1] = 0;
+        c[d - 1] = 0;
+        if (s[d - 1] >= 0) {
+            n[d - 1] = t.node_at[pos - d];
+            c[d - 1] = t.smeta[s[d - 1]].count;
+        }
+    }
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d)
+        if (c[d - 1] > 0) atomicAdd(&t.count[n[d - 1]], c[d - 1]);
+    if (L > kWin)
+        long_hits(t, pos, L, [&](int32_t sl, int d) {
+            atomicAdd(&t.count[t.node_at[pos - d]], (int32_t)t.smeta[sl].count);
+        });
+}
+
+// Fill pass (lists): the hits' token ids written into the per-node lists.
+__global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
+    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (m >= t.N) return;
+    const int64_t pos = t.node_pos[m];
+    if (pos < 0) return;
+    const int L = min(t.depth[m], t.max_len);
+    const int Lw = min(L, kWin);
+    int32_t s[kWin];
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d)
+        if (s[d - 1] >= 0) emit(t, s[d - 1], t.node_at[pos - d]);
+    if (L > kWin) long_hits(t, pos, L, [&](int32_t sl, int d) { emit(t, sl, t.node_at[pos - d]); });
+}
+
+// Mark pass (dense table): every hit OR-ed into the zeroed table with a 64-bit
+// atomic, after all of the lane's loads.  Each block writes how many (node,
+// token) pairs it set into pairs[blockIdx.x].
+__global__ void __launch_bounds__(kBlock) k_mark(DevTables t, int32_t *__restrict__ pairs) {
+    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    int32_t found = 0;
+    const int64_t pos = m < t.N ? t.node_pos[m] : -1;
+    if (pos >= 0) {
+        const int L = min(t.depth[m], t.max_len);
+        const int Lw = min(L, kWin);
+        unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
+        int32_t s[kWin], n[kWin], v[kWin];
+        uint32_t multi = 0;
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d) {
+            n[d - 1] = 0;
+            v[d - 1] = -1;
+            if (s[d - 1] >= 0) {
+                const SlotMeta mt = t.smeta[s[d - 1]];
+                n[d - 1] = t.node_at[pos - d];
+                v[d - 1] = mt.first;
+                if (mt.count > 1) multi |= 1u << (d - 1);
+            }
+        }
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d) {
+            if (v[d - 1] >= 0) {
+                atomicOr(table + (int64_t)n[d - 1] * t.Wp + (v[d - 1] >> 6), 1ull << (v[d - 1] & 63));
+                ++found;
+            }
+        }
+        // duplicate token strings and tokens longer than the window (both rare)
+        auto mark_slot = [&](int32_t sl, int32_t node, bool skip_first) {
+            const SlotMeta mt = t.smeta[sl];
+            unsigned long long *row = table + (int64_t)node * t.Wp;
+            int32_t x = mt.first;
+            for (int k = 0; k < (int)mt.count; ++k) {
+                if (k > 0 || !skip_first) {
+                    atomicOr(row + (x >> 6), 1ull << (x & 63));
+                    ++found;
+                }
+                x = t.dup_next[x];
+            }
+        };
+        for (uint32_t mm = multi; mm; mm &= mm - 1) {
+            const int d = __builtin_ctz(mm) + 1;
+            mark_slot(t.hits[(int64_t)(d - 1) * t.N + m], t.node_at[pos - d], true);
+        }
+        if (L > kWin) long_hits(t, pos, L, [&](int32_t sl, int d) { mark_slot(sl, t.node_at[pos - d], false); });
+    }
+    // block sum of found
+    __shared__ int32_t wsum[kBlock / kWave];
+    for (int o = kWave / 2; o > 0; o >>= 1) found += __shfl_xor(found, o, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) wsum[threadIdx.x / kWave] = found;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t total = 0;
+        for (int w = 0; w < kBlock / kWave; ++w) total += wsum[w];
+        pairs[blockIdx.x] = total;
+    }
+}
+
+// Zero fill of n16 16-byte chunks: one chunk per thread, 256 threads (4 KiB)
+// per block, plain stores and no grid-stride loop.  Measured on MI355X this
+// shape sustains ~6.8 TB/s; more chunks per thread, non-temporal stores or a
+// persistent grid-stride grid all write slower, because the blocks in flight
+// then no longer sweep one compact window of memory.
+__global__ void __launch_bounds__(kBlock) k_zero(u32x4 *__restrict__ p, int64_t n16) {
+    const int64_t c = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (c < n16) p[c] = u32x4{0u, 0u, 0u, 0u};
 }
 
 // ------------------------------------------------------------------ scan ---
@@ -191,49 +397,76 @@ __global__ void __launch_bounds__(kBlock) k_scan_apply(const int32_t *in, int64_
 
 // ------------------------------------------------------------ row images ---
 
-// Work item (r, tile): the node is nodes[r] (or r when nodes is null); the tile
-// covers words [tile*kTileWords, ...) of the out_words-word row written at
-// out + r*out_stride.  `vec`: rows and tiles are 16-byte aligned.
-__global__ void __launch_bounds__(kBlock) k_rows(DevTables t, const int32_t *nodes, int64_t nrows,
-                                                 uint64_t *out, int64_t out_stride, int64_t out_words,
-                                                 int64_t ntiles, int tile_words, int vec) {
-    extern __shared__ u32x4 img[];  // tile_words * 8 bytes
-    uint32_t *img32 = reinterpret_cast<uint32_t *>(img);
-    uint64_t *img64 = reinterpret_cast<uint64_t *>(img);
-    for (int i = threadIdx.x; i < tile_words / 2; i += kBlock) img[i] = u32x4{0u, 0u, 0u, 0u};
-    __syncthreads();
-    const int64_t items = nrows * ntiles;
-    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
-        const int64_t r = it / ntiles;
-        const int64_t w0 = (it - r * ntiles) * tile_words;
-        const int wn = (int)min<int64_t>(tile_words, out_words - w0);
+constexpr int kRowSlots = 8;       // chunks per lane per pass
+constexpr int kRowRegBatches = 4;  // 64-entry batches of a row's list held in VGPRs
+
+// One wave per row (grid-stride over rows): the row's list (up to 256 ids) is
+// loaded into VGPRs once; each pass then builds 8 chunks per lane in registers
+// from it and streams them with non-temporal stores, 64 chunks (1 KiB for
+// 16-byte chunks) per store instruction.  No LDS, no barriers: every wave keeps
+// a whole row of stores in flight.  Row r is node nodes[r] (r if nodes is
+// null), written at out + r*out_stride; a dead or out-of-range node gives a
+// zero row.  CW = 64-bit words per chunk (2: 16-byte stores, 1: 8-byte).
+template <int CW>
+__global__ void __launch_bounds__(kBlock) k_rows(const int32_t *__restrict__ row_ptr,
+                                                 const int32_t *__restrict__ entries,
+                                                 const int32_t *__restrict__ nodes, int64_t nrows, int64_t N,
+                                                 uint64_t *__restrict__ out, int64_t out_stride,
+                                                 int64_t out_words) {
+    typedef uint32_t chunk_t __attribute__((ext_vector_type(2 * CW)));
+    constexpr int kBits = 64 * CW;             // tokens per chunk
+    constexpr int kPass = kWave * kRowSlots;   // chunks per pass
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t nwaves = (int64_t)gridDim.x * (kBlock / kWave);
+    const int64_t nchunks = out_words / CW;
+    for (int64_t r = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave; r < nrows; r += nwaves) {
         const int64_t n = nodes ? (int64_t)nodes[r] : r;
-        if (n >= 0 && n < t.N) {
-            const int32_t b = t.row_ptr[n], e = t.row_ptr[n + 1];
-            const uint32_t lo = (uint32_t)(w0 * 64);
-            const uint32_t span = (uint32_t)wn * 64u;
-            for (int32_t k = b + (int32_t)threadIdx.x; k < e; k += kBlock) {
-                const uint32_t v = (uint32_t)t.entries[k] - lo;
-                if (v < span) atomicOr(&img32[v >> 5], 1u << (v & 31));
+        int32_t b = 0, e = 0;
+        if (n >= 0 && n < N) {
+            b = row_ptr[n];
+            e = row_ptr[n + 1];
+        }
+        int32_t ent[kRowRegBatches];
+#pragma unroll
+        for (int i = 0; i < kRowRegBatches; ++i) {
+            const int32_t k = b + i * kWave + lane;
+            ent[i] = k < e ? entries[k] : 0;
+        }
+        const int32_t E = e - b;
+        chunk_t *dst = reinterpret_cast<chunk_t *>(out + r * out_stride);
+        for (int64_t c0 = 0; c0 < nchunks; c0 += kPass) {
+            chunk_t val[kRowSlots];
+#pragma unroll
+            for (int k = 0; k < kRowSlots; ++k) val[k] = chunk_t(0u);
+            for (int32_t j = 0; j < E; ++j) {
+                int32_t v;
+                if (j < kRowRegBatches * kWave) {
+                    const int bi = j / kWave;
+                    const int32_t src = bi == 0 ? ent[0] : bi == 1 ? ent[1] : bi == 2 ? ent[2] : ent[3];
+                    v = __builtin_amdgcn_readlane(src, j % kWave);
+                } else {
+                    v = entries[b + j];
+                }
+                const int64_t rel = (int64_t)(v / kBits) - c0;
+                if (rel < 0 || rel >= kPass) continue;
+                const int k = (int)(rel / kWave), l = (int)(rel % kWave);
+                const int dw = (v / 32) % (2 * CW);
+                const uint32_t bit = lane == l ? 1u << (v % 32) : 0u;
+#pragma unroll
+                for (int kk = 0; kk < kRowSlots; ++kk) {
+                    if (kk == k) {
+#pragma unroll
+                        for (int q = 0; q < 2 * CW; ++q)
+                            if (q == dw) val[kk][q] |= bit;
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kRowSlots; ++k) {
+                const int64_t c = c0 + k * kWave + lane;
+                if (c < nchunks) __builtin_nontemporal_store(val[k], dst + c);
             }
         }
-        __syncthreads();
-        uint64_t *dst = out + r * out_stride + w0;
-        if (vec) {
-            u32x4 *d4 = reinterpret_cast<u32x4 *>(dst);
-            for (int c = threadIdx.x; c < wn / 2; c += kBlock) {
-                const u32x4 x = img[c];
-                img[c] = u32x4{0u, 0u, 0u, 0u};
-                __builtin_nontemporal_store(x, d4 + c);
-            }
-        } else {
-            for (int c = threadIdx.x; c < wn; c += kBlock) {
-                const uint64_t x = img64[c];
-                img64[c] = 0;
-                __builtin_nontemporal_store(x, dst + c);
-            }
-        }
-        __syncthreads();
     }
 }
 
@@ -251,12 +484,18 @@ struct NegInf<uint32_t> {
 };
 
 // Grid: x = groups of kBlock*kApplyUnits chunks of one row, y = batch row.
-// A chunk is 16 bytes of logits (8 bf16 or 4 fp32).  kSparse: the mask bits of
-// the block's span come from the node's valid list via an LDS bitmap instead of
-// the dense table.  vec == 0: rows are not 16-byte aligned, go element by element.
+// A chunk is 16 bytes of logits (8 bf16 or 4 fp32); thread i of a block owns
+// chunks c0 + u*kBlock + i, so every store instruction covers 4 KiB per block
+// contiguously (one chunk per thread writes fastest, as for the table's zero
+// fill).  All mask bits of the thread are read before its first store.
+// Write-mostly: a chunk without a valid token gets one non-temporal -inf store
+// and no read; a fully valid chunk is skipped; only mixed chunks are read,
+// merged and written.  kSparse: the bits of the block's span come from the
+// node's valid list through an LDS bitmap instead of the dense table.
+// vec == 0: rows are not 16-byte aligned; go element by element.
 template <typename T, bool kSparse>
-__global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *node_ids, T *logits,
-                                                  int64_t stride, int vec) {
+__global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__restrict__ node_ids,
+                                                  T *__restrict__ logits, int64_t stride, int vec) {
     constexpr int E = 16 / (int)sizeof(T);
     constexpr uint32_t FULL = (1u << E) - 1u;
     constexpr T NEG = NegInf<T>::bits;
@@ -271,7 +510,7 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *no
     const int64_t nchunks = (V + E - 1) / E;
     T *row = logits + b * stride;
 
-    const uint8_t *mrow = nullptr;
+    uint32_t bits[kApplyUnits];
     if (kSparse) {
         for (int i = threadIdx.x; i < kSpan / 32; i += kBlock) bm[i] = 0;
         __syncthreads();
@@ -284,50 +523,48 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *no
             }
         }
         __syncthreads();
-    } else if (live) {
-        mrow = reinterpret_cast<const uint8_t *>(t.table + (int64_t)n * t.Wp);
+#pragma unroll
+        for (int u = 0; u < kApplyUnits; ++u) {
+            const uint32_t bit = (uint32_t)((u * kBlock + threadIdx.x) * E);
+            bits[u] = (bm[bit >> 5] >> (bit & 31)) & FULL;
+        }
+    } else {
+        const uint8_t *mrow = reinterpret_cast<const uint8_t *>(t.table + (live ? (int64_t)n * t.Wp : 0));
+#pragma unroll
+        for (int u = 0; u < kApplyUnits; ++u) {
+            const int64_t c = c0 + u * kBlock + threadIdx.x;
+            uint32_t x = 0;
+            if (live && c < nchunks) x = E == 8 ? (uint32_t)mrow[c] : ((uint32_t)mrow[c >> 1] >> ((c & 1) * 4)) & FULL;
+            bits[u] = x;
+        }
     }
 
 #pragma unroll
     for (int u = 0; u < kApplyUnits; ++u) {
-        const int64_t lc = (int64_t)u * kBlock + threadIdx.x;  // chunk within the block
-        const int64_t c = c0 + lc;
+        const int64_t c = c0 + u * kBlock + threadIdx.x;
         if (c >= nchunks) break;
-        uint32_t bits = 0;
-        if (kSparse) {
-            const uint32_t bit = (uint32_t)(lc * E);
-            bits = (bm[bit >> 5] >> (bit & 31)) & FULL;
-        } else if (live) {
-            bits = E == 8 ? (uint32_t)mrow[c] : ((uint32_t)mrow[c >> 1] >> ((c & 1) * 4)) & FULL;
-        }
-        if (bits == FULL) continue;
+        const uint32_t bu = bits[u];
+        if (bu == FULL) continue;
         const int64_t e0 = c * E;
         if (vec && e0 + E <= V) {
             u32x4 *p = reinterpret_cast<u32x4 *>(row + e0);
-            if (bits == 0) {
-                u32x4 neg;
-                if (sizeof(T) == 2) {
-                    const uint32_t w = 0xFF80FF80u;
-                    neg = u32x4{w, w, w, w};
-                } else {
-                    const uint32_t w = 0xFF800000u;
-                    neg = u32x4{w, w, w, w};
-                }
-                __builtin_nontemporal_store(neg, p);
+            if (bu == 0) {
+                const uint32_t w = sizeof(T) == 2 ? 0xFF80FF80u : 0xFF800000u;
+                __builtin_nontemporal_store(u32x4{w, w, w, w}, p);
             } else {
                 u32x4 x = *p;
                 T vals[E];
                 __builtin_memcpy(vals, &x, 16);
 #pragma unroll
                 for (int i = 0; i < E; ++i)
-                    if (!((bits >> i) & 1u)) vals[i] = NEG;
+                    if (!((bu >> i) & 1u)) vals[i] = NEG;
                 __builtin_memcpy(&x, vals, 16);
                 *p = x;
             }
         } else {
             const int lim = (int)min<int64_t>(E, V - e0);
             for (int i = 0; i < lim; ++i)
-                if (!((bits >> i) & 1u)) row[e0 + i] = NEG;
+                if (!((bu >> i) & 1u)) row[e0 + i] = NEG;
         }
     }
 }
@@ -394,17 +631,39 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s) 
     return hipGetLastError();
 }
 
+hipError_t launch_probe(const DevTables &t, hipStream_t s) {
+    if (t.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_probe, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+    return hipGetLastError();
+}
+
 hipError_t launch_count(const DevTables &t, hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_probe<false>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+    hipLaunchKernelGGL(k_count, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
     return hipGetLastError();
 }
 
 hipError_t launch_fill_lists(const DevTables &t, hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_probe<true>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+    hipLaunchKernelGGL(k_fill, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
     return hipGetLastError();
 }
+
+hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s) {
+    const int64_t n16 = words / 2;
+    if (n16 <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_zero, dim3(grid_for(n16, kBlock)), dim3(kBlock), 0, s,
+                       reinterpret_cast<u32x4 *>(p), n16);
+    return hipGetLastError();
+}
+
+hipError_t launch_mark(const DevTables &t, int32_t *pairs, hipStream_t s) {
+    if (t.N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_mark, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, pairs);
+    return hipGetLastError();
+}
+
+int64_t mark_blocks(int64_t N) { return (N + kBlock - 1) / kBlock; }
 
 hipError_t launch_scan(const DevTables &t, hipStream_t s) {
     const int64_t nb = grid_for(t.N, kScanTile);
@@ -418,21 +677,21 @@ hipError_t launch_scan(const DevTables &t, hipStream_t s) {
 hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
                        int64_t out_stride_words, int64_t out_words, hipStream_t s) {
     if (nrows <= 0 || out_words <= 0) return hipSuccess;
-    const int tile_words = (int)std::min<int64_t>(kTileWords, (out_words + 1) & ~int64_t(1));
-    const int64_t ntiles = (out_words + tile_words - 1) / tile_words;
-    const int vec = ((out_stride_words & 1) == 0 && (out_words & 1) == 0 &&
-                     (reinterpret_cast<uintptr_t>(out) & 15) == 0)
-                        ? 1
-                        : 0;
-    const size_t lds = (size_t)tile_words * 8;
+    const bool vec = (out_stride_words & 1) == 0 && (out_words & 1) == 0 &&
+                     (reinterpret_cast<uintptr_t>(out) & 15) == 0;
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_rows, kBlock, lds) != hipSuccess ||
-        per_cu <= 0)
-        per_cu = 4;
+    hipError_t e = vec ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_rows<2>, kBlock, 0)
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_rows<1>, kBlock, 0);
+    if (e != hipSuccess || per_cu <= 0) per_cu = 4;
+    const int64_t waves_needed = nrows;
     const int64_t cap = (int64_t)props_for_current_device().cus * per_cu;
-    const unsigned g = (unsigned)std::min<int64_t>(nrows * ntiles, cap);
-    hipLaunchKernelGGL(k_rows, dim3(g), dim3(kBlock), lds, s, t, nodes, nrows, out, out_stride_words,
-                       out_words, ntiles, tile_words, vec);
+    const unsigned g = (unsigned)std::max<int64_t>(1, std::min<int64_t>(cap, grid_for(waves_needed, kBlock / kWave)));
+    if (vec)
+        hipLaunchKernelGGL(k_rows<2>, dim3(g), dim3(kBlock), 0, s, t.row_ptr, t.entries, nodes, nrows, t.N, out,
+                           out_stride_words, out_words);
+    else
+        hipLaunchKernelGGL(k_rows<1>, dim3(g), dim3(kBlock), 0, s, t.row_ptr, t.entries, nodes, nrows, t.N, out,
+                           out_stride_words, out_words);
     return hipGetLastError();
 }
 

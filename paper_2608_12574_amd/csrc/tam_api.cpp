@@ -6,6 +6,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "host_build.hpp"
 #include "tam_internal.hpp"
@@ -54,7 +55,7 @@ void *dev_alloc(tam_handle *h, size_t bytes) {
 
 void release_device(tam_handle *h) {
     if (h->work_done) (void)hipEventSynchronize(h->work_done);
-    if (h->have_events) (void)hipEventSynchronize(h->ev[4]);
+    if (h->have_events) (void)hipEventSynchronize(h->ev[3]);
     for (void *p : h->dev_ptrs) {
         if (h->own_alloc)
             (void)hipFree(p);
@@ -65,8 +66,16 @@ void release_device(tam_handle *h) {
     if (h->have_events)
         for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
     if (h->work_done) (void)hipEventDestroy(h->work_done);
+    if (h->side) {
+        (void)hipStreamSynchronize(h->side);
+        (void)hipStreamDestroy(h->side);
+    }
+    if (h->fork) (void)hipEventDestroy(h->fork);
+    if (h->join) (void)hipEventDestroy(h->join);
     h->have_events = false;
     h->work_done = nullptr;
+    h->side = nullptr;
+    h->fork = h->join = nullptr;
 }
 
 // Sub-allocation of the small tables inside one device arena.
@@ -80,25 +89,48 @@ struct Arena {
     }
 };
 
-// The device part of compile: valid lists, then the dense table.  Phase events
-// are recorded only when both phases run.
+unsigned default_phases(const tam_handle *h) {
+    return h->dt.table ? unsigned(TAM_PHASE_TABLE) : unsigned(TAM_PHASE_LISTS);
+}
+
+// The device part of compile.  Lists: probes counting per node, prefix sum,
+// probes filling the lists.  Table: zero fill, then probes setting the bits.
+// Phase events are recorded only for the handle's default phases.
 tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     const tam::DevTables &t = h->dt;
-    const bool timing = h->have_events && phases == (TAM_PHASE_LISTS | TAM_PHASE_TABLE);
+    const bool timing = h->have_events && phases == default_phases(h);
     if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
     if (phases & TAM_PHASE_LISTS) {
         TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
+        TAM_HIP(tam::launch_probe(t, s));
         TAM_HIP(tam::launch_count(t, s));
-        if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
         TAM_HIP(tam::launch_scan(t, s));
-        if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
         TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
         TAM_HIP(tam::launch_fill_lists(t, s));
-        if (timing) TAM_HIP(hipEventRecord(h->ev[3], s));
+        h->lists_built = true;
     }
-    if ((phases & TAM_PHASE_TABLE) && t.table) TAM_HIP(tam::launch_rows(t, nullptr, t.N, t.table, t.Wp, t.Wp, s));
+    if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
+    // With both table phases, the probes (L2-latency bound) run on the side
+    // stream while the zero fill (HBM-write bound) runs on the caller's stream.
+    const bool overlap = t.table && (phases & TAM_PHASE_TABLE) == unsigned(TAM_PHASE_TABLE) && h->side;
+    if (overlap) {
+        TAM_HIP(hipEventRecord(h->fork, s));
+        TAM_HIP(hipStreamWaitEvent(h->side, h->fork, 0));
+        TAM_HIP(tam::launch_probe(t, h->side));
+        TAM_HIP(hipEventRecord(h->join, h->side));
+    }
+    if ((phases & TAM_PHASE_ZERO) && t.table) TAM_HIP(tam::launch_zero(t.table, t.N * t.Wp, s));
+    if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
+    if ((phases & TAM_PHASE_MARK) && t.table) {
+        if (overlap) {
+            TAM_HIP(hipStreamWaitEvent(s, h->join, 0));
+        } else {
+            TAM_HIP(tam::launch_probe(t, s));
+        }
+        TAM_HIP(tam::launch_mark(t, h->pairs, s));
+    }
     if (timing) {
-        TAM_HIP(hipEventRecord(h->ev[4], s));
+        TAM_HIP(hipEventRecord(h->ev[3], s));
         h->events_recorded = true;
     }
     if (h->work_done) TAM_HIP(hipEventRecord(h->work_done, s));
@@ -176,8 +208,8 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     }
     h->W = (V + 63) / 64;
     h->Wp = (h->W + 7) & ~int64_t(7);  // rows 64-byte aligned
-    h->timing.dev_count_ms = h->timing.dev_scan_ms = h->timing.dev_fill_ms = -1.f;
-    h->timing.dev_table_ms = h->timing.dev_total_ms = -1.f;
+    h->timing.dev_lists_ms = h->timing.dev_zero_ms = h->timing.dev_mark_ms = -1.f;
+    h->timing.dev_total_ms = -1.f;
     if (h->flags & TAM_FLAG_HOST_ONLY) {
         *out = h;
         return TAM_OK;
@@ -204,7 +236,10 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     const size_t o_child_node = a.take<int32_t>((int64_t)h->child_node.size());
     const size_t o_tok_off = a.take<uint32_t>(V + 1);
     const size_t o_tok_blob = a.take<uint8_t>((int64_t)h->tok_blob.size());
-    const size_t o_slots = a.take<tam::HashSlot>((int64_t)h->slots.size());
+    const size_t o_fps = a.take<uint32_t>((int64_t)h->fps.size());
+    const size_t o_srev = a.take<tam::SlotRev>((int64_t)h->srev.size());
+    const size_t o_smeta = a.take<tam::SlotMeta>((int64_t)h->smeta.size());
+    const size_t o_hits = a.take<int32_t>(tam::kWin * h->N);
     const size_t o_dup = a.take<int32_t>(V);
     const size_t o_len = a.take<uint8_t>((int64_t)h->len_present.size());
     const size_t o_count = a.take<int32_t>(h->N);
@@ -212,6 +247,7 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     const size_t o_cursor = a.take<int32_t>(h->N);
     const size_t o_entries = a.take<int32_t>(h->entry_bound);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
+    const size_t o_pairs = a.take<int32_t>(tam::mark_blocks(h->N));
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = nullptr;
@@ -235,7 +271,10 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     t.child_node = reinterpret_cast<const int32_t *>(base + o_child_node);
     t.tok_off = reinterpret_cast<const uint32_t *>(base + o_tok_off);
     t.tok_blob = base + o_tok_blob;
-    t.slots = reinterpret_cast<const tam::HashSlot *>(base + o_slots);
+    t.fps = reinterpret_cast<const uint32_t *>(base + o_fps);
+    t.srev = reinterpret_cast<const tam::SlotRev *>(base + o_srev);
+    t.smeta = reinterpret_cast<const tam::SlotMeta *>(base + o_smeta);
+    t.hits = reinterpret_cast<int32_t *>(base + o_hits);
     t.dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
     t.len_present = base + o_len;
     t.count = reinterpret_cast<int32_t *>(base + o_count);
@@ -243,13 +282,15 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
     t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
+    h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
     t.table = table;
     t.N = h->N;
     t.V = h->V;
     t.W = h->W;
     t.Wp = h->Wp;
     t.blob_bytes = h->blob_bytes;
-    t.slot_mask = (uint64_t)h->slots.size() - 1;
+    t.slot_mask = (uint64_t)h->fps.size() - 1;
+    t.len_mask = h->len_mask;
     t.max_len = (int32_t)h->max_tok_len;
 
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
@@ -266,11 +307,16 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     if (e == hipSuccess) e = up(o_child_node, h->child_node.data(), h->child_node.size() * 4);
     if (e == hipSuccess) e = up(o_tok_off, h->tok_off.data(), h->tok_off.size() * 4);
     if (e == hipSuccess) e = up(o_tok_blob, h->tok_blob.data(), h->tok_blob.size());
-    if (e == hipSuccess) e = up(o_slots, h->slots.data(), h->slots.size() * sizeof(tam::HashSlot));
+    if (e == hipSuccess) e = up(o_fps, h->fps.data(), h->fps.size() * sizeof(uint32_t));
+    if (e == hipSuccess) e = up(o_srev, h->srev.data(), h->srev.size() * sizeof(tam::SlotRev));
+    if (e == hipSuccess) e = up(o_smeta, h->smeta.data(), h->smeta.size() * sizeof(tam::SlotMeta));
     if (e == hipSuccess) e = up(o_dup, h->dup_next.data(), h->dup_next.size() * 4);
     if (e == hipSuccess) e = up(o_len, h->len_present.data(), h->len_present.size());
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
+    if (e == hipSuccess && table) e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
+    if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
+    if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
         for (hipEvent_t &ev : h->ev) {
             if (e == hipSuccess) e = hipEventCreate(&ev);
@@ -284,7 +330,7 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
         delete h;
         return st;
     }
-    st = run_device_phase(h, TAM_PHASE_LISTS | TAM_PHASE_TABLE, s);
+    st = run_device_phase(h, default_phases(h), s);
     if (st != TAM_OK) {
         const std::string msg = g_err;
         release_device(h);
@@ -299,8 +345,9 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
     g_err.clear();
     tam_status st = check_device_handle(h);
     if (st != TAM_OK) return st;
-    if (phases == 0) phases = TAM_PHASE_LISTS | TAM_PHASE_TABLE;
+    if (phases == 0) phases = default_phases(h);
     if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
+    if ((phases & TAM_PHASE_TABLE) && !h->dt.table) return fail(TAM_E_STATE, "handle has no dense table");
     return run_device_phase(h, phases, static_cast<hipStream_t>(stream));
 }
 
@@ -337,6 +384,7 @@ tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t 
     if (row_stride < h->V) return fail(TAM_E_INVAL, "row_stride must be >= V");
     const size_t elem = dtype == TAM_DTYPE_BF16 ? 2 : 4;
     if ((reinterpret_cast<uintptr_t>(logits) % elem) != 0) return fail(TAM_E_INVAL, "logits are not element-aligned");
+    if (!h->dt.table && !h->lists_built) return fail(TAM_E_STATE, "the valid lists have not been built");
     TAM_HIP(hipGetLastError());
     TAM_HIP(tam::launch_apply(h->dt, node_ids, B, logits, dtype, row_stride, static_cast<hipStream_t>(stream)));
     return TAM_OK;
@@ -366,6 +414,7 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
     if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return fail(TAM_E_INVAL, "out must be 8-byte aligned");
     TAM_HIP(hipGetLastError());
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!h->dt.table && !h->lists_built) return fail(TAM_E_STATE, "the valid lists have not been built");
     if (h->dt.table)
         TAM_HIP(tam::launch_export_dense(h->dt, node_ids, n, out, s));
     else
@@ -378,11 +427,20 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     tam_status st = check_device_handle(h);
     if (st != TAM_OK) return st;
     if (!out) return fail(TAM_E_INVAL, "out is null");
-    int32_t m = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    TAM_HIP(hipMemcpyAsync(&m, h->dt.row_ptr + h->N, sizeof(m), hipMemcpyDeviceToHost, s));
-    TAM_HIP(hipStreamSynchronize(s));
-    *out = m;
+    if (h->dt.table) {
+        std::vector<int32_t> part((size_t)tam::mark_blocks(h->N));
+        TAM_HIP(hipMemcpyAsync(part.data(), h->pairs, part.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        TAM_HIP(hipStreamSynchronize(s));
+        int64_t m = 0;
+        for (int32_t x : part) m += x;
+        *out = m;
+    } else {
+        int32_t m = 0;
+        TAM_HIP(hipMemcpyAsync(&m, h->dt.row_ptr + h->N, sizeof(m), hipMemcpyDeviceToHost, s));
+        TAM_HIP(hipStreamSynchronize(s));
+        *out = m;
+    }
     return TAM_OK;
 }
 
@@ -390,14 +448,11 @@ tam_status tam_timing_get(const tam_handle *h, tam_timing *out) {
     if (!h || !out) return fail(TAM_E_INVAL, "null argument");
     *out = h->timing;
     if (h->have_events && h->events_recorded) {
-        TAM_HIP(hipEventSynchronize(h->ev[4]));
-        float ms[4];
-        for (int i = 0; i < 4; ++i) TAM_HIP(hipEventElapsedTime(&ms[i], h->ev[i], h->ev[i + 1]));
-        out->dev_count_ms = ms[0];
-        out->dev_scan_ms = ms[1];
-        out->dev_fill_ms = ms[2];
-        out->dev_table_ms = ms[3];
-        TAM_HIP(hipEventElapsedTime(&out->dev_total_ms, h->ev[0], h->ev[4]));
+        TAM_HIP(hipEventSynchronize(h->ev[3]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_lists_ms, h->ev[0], h->ev[1]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_zero_ms, h->ev[1], h->ev[2]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_mark_ms, h->ev[2], h->ev[3]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_total_ms, h->ev[0], h->ev[3]));
     }
     return TAM_OK;
 }

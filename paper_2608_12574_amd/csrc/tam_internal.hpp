@@ -31,11 +31,26 @@ __host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len
     return z | 1ull;  // 0 never occurs as a key
 }
 
-// One open-addressing slot per distinct non-empty token string.
-struct alignas(16) HashSlot {
-    uint64_t key;    // hash_final(...) of the string, 0 = empty slot
-    int32_t first;   // smallest token id with this string (-1 = empty)
-    int32_t count;   // number of token ids with this string
+// Vocabulary table: open addressing over buckets of 16 32-bit fingerprints (one
+// 64-byte line per bucket), one slot per distinct non-empty token string.  A
+// slot's payload (its length, first id, duplicate count and its first 16 bytes
+// stored last byte first) is read only on a fingerprint match.
+constexpr int kBucket = 16;   // fingerprints per bucket
+constexpr int kWin = 16;      // path bytes a probing node keeps in registers
+constexpr int kBlobPad = 16;  // zero bytes before and after the string blob
+
+__host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
+    return (uint32_t)(key >> 32) | 1u;  // 0 marks an empty slot
+}
+
+struct alignas(16) SlotRev {
+    uint64_t lo, hi;  // byte k = token byte len-1-k for k < min(len, 16), then zeros
+};
+
+struct alignas(8) SlotMeta {
+    int32_t first;    // smallest token id with this string
+    uint16_t len;     // string length in bytes
+    uint16_t count;   // number of token ids with this string
 };
 
 // ---------------------------------------------------------------------------
@@ -43,7 +58,7 @@ struct alignas(16) HashSlot {
 // ---------------------------------------------------------------------------
 struct DevTables {
     // trie (a1)
-    const uint8_t *blob;        // per string: [pad][bytes][T]
+    const uint8_t *blob;        // [pad 16][per string: pad, bytes, T][pad 16]
     const int32_t *node_at;     // [blob_bytes] node whose edge byte is that blob byte (pad: root)
     const int32_t *node_pos;    // [N] blob offset of the node's edge byte (-1 at roots)
     const int32_t *depth;       // [N]
@@ -53,10 +68,13 @@ struct DevTables {
     // vocabulary (a2)
     const uint32_t *tok_off;    // [V+1]
     const uint8_t *tok_blob;
-    const HashSlot *slots;      // [slot_mask+1]
+    const uint32_t *fps;        // [slot_mask+1] fingerprints, kBucket per bucket
+    const SlotRev *srev;        // [slot_mask+1]
+    const SlotMeta *smeta;      // [slot_mask+1]
     const int32_t *dup_next;    // [V] next id with the same bytes, -1 at the end
     const uint8_t *len_present; // [max_len+1] 1 if some token has that length
     // valid lists (a4) and dense table
+    int32_t *hits;              // [kWin][N] slot hit by the suffix of length d+1 of node m, or -1
     int32_t *count;             // [N]
     int32_t *row_ptr;           // [N+1]
     int32_t *cursor;            // [N]
@@ -65,14 +83,19 @@ struct DevTables {
     int32_t *scan_tmp;          // block sums of the scan
     int64_t N, V, W, Wp;
     int64_t blob_bytes;
-    uint64_t slot_mask;
+    uint64_t slot_mask;         // slots - 1 (slots = a power of two, >= kBucket)
+    uint64_t len_mask;          // bit d (d < 64): some token has length d
     int32_t max_len;
 };
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
+hipError_t launch_probe(const DevTables &t, hipStream_t s);
 hipError_t launch_count(const DevTables &t, hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
+hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
+hipError_t launch_mark(const DevTables &t, int32_t *pairs, hipStream_t s);
+int64_t mark_blocks(int64_t N);
 hipError_t launch_fill_lists(const DevTables &t, hipStream_t s);
 hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
                        int64_t out_stride_words, int64_t out_words, hipStream_t s);
@@ -105,15 +128,22 @@ struct tam_handle {
     // host vocabulary tables
     std::vector<uint32_t> tok_off;
     std::vector<uint8_t> tok_blob, len_present;
-    std::vector<tam::HashSlot> slots;
+    std::vector<uint32_t> fps;
+    std::vector<tam::SlotRev> srev;
+    std::vector<tam::SlotMeta> smeta;
+    uint64_t len_mask = 0;
     std::vector<int32_t> dup_next;
 
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};
 
-    hipEvent_t ev[5] = {};
+    hipEvent_t ev[4] = {};
+    int32_t *pairs = nullptr;       // device [mark_blocks(N)] per-block valid-pair counts
+    bool lists_built = false;
     bool have_events = false;
     bool events_recorded = false;
     hipEvent_t work_done = nullptr;  // end of the last upload / device phase
+    hipStream_t side = nullptr;      // runs the table phase's probes beside its zero fill
+    hipEvent_t fork = nullptr, join = nullptr;
     tam_timing timing{};
 };

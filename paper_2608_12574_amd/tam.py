@@ -20,7 +20,8 @@ TAM_OK = 0
 TAM_DEAD = -1
 DTYPE_FP32, DTYPE_BF16 = 0, 1
 FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING = 1, 2, 4
-PHASE_LISTS, PHASE_TABLE = 1, 2
+PHASE_LISTS, PHASE_ZERO, PHASE_MARK = 1, 2, 4
+PHASE_TABLE = PHASE_ZERO | PHASE_MARK
 
 STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOMEM",
           -4: "TAM_E_DEVICE", -5: "TAM_E_TOOLARGE", -6: "TAM_E_STATE"}
@@ -62,9 +63,9 @@ class Info(ctypes.Structure):
 
 class Timing(ctypes.Structure):
     _fields_ = [("host_trie_ms", ctypes.c_double), ("host_vocab_ms", ctypes.c_double),
-                ("upload_ms", ctypes.c_double), ("dev_count_ms", ctypes.c_float),
-                ("dev_scan_ms", ctypes.c_float), ("dev_fill_ms", ctypes.c_float),
-                ("dev_table_ms", ctypes.c_float), ("dev_total_ms", ctypes.c_float)]
+                ("upload_ms", ctypes.c_double), ("dev_lists_ms", ctypes.c_float),
+                ("dev_zero_ms", ctypes.c_float), ("dev_mark_ms", ctypes.c_float),
+                ("dev_total_ms", ctypes.c_float)]
 
     def as_dict(self) -> dict:
         return {k: float(getattr(self, k)) for k, _ in self._fields_}
@@ -233,7 +234,7 @@ class Handle:
         return out
 
     def rebuild(self, phases: int = 0, stream=None):
-        """Rerun the device phases (PHASE_LISTS | PHASE_TABLE; 0 = both)."""
+        """Rerun device phases (PHASE_* mask; 0 = the handle's default)."""
         _check(lib().tam_rebuild(self._raw, phases, _stream_ptr(stream, self.host_only)), "tam_rebuild")
 
     def valid_pairs(self, stream=None) -> int:

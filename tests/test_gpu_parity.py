@@ -226,6 +226,8 @@ def test_config_decode(P, compiled):
 
 
 def test_config_rebuild_identical(P, compiled):
+    """Rebuilding (all phases, or marking again without the zero fill) gives the
+    same table; the sparse lists built on a dense handle count the same pairs."""
     w, o, h = compiled
     nodes = sample_nodes(o, 32, 7)
     before = gpu_rows(h, nodes)
@@ -233,6 +235,11 @@ def test_config_rebuild_identical(P, compiled):
     h.rebuild()
     assert np.array_equal(gpu_rows(h, nodes), before)
     assert h.valid_pairs() == M
+    h.rebuild(phases=P.PHASE_MARK)
+    assert np.array_equal(gpu_rows(h, nodes), before)
+    assert h.valid_pairs() == M
+    h.rebuild(phases=P.PHASE_LISTS)
+    assert np.array_equal(gpu_rows(h, nodes), before)
 
 
 # ---------------------------------------------------------- sparse / forest --
