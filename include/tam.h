@@ -61,6 +61,7 @@ extern "C" {
 #define TAM_DEAD (-1)
 
 typedef struct tam_handle tam_handle;
+typedef struct tam_vocab tam_vocab;
 
 typedef enum {
     TAM_OK = 0,
@@ -167,6 +168,43 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
                        const tam_options *opt, const tam_allocator *alloc, void *stream,
                        tam_handle **out);
 
+/*
+ * tam_vocab_create -- the vocabulary side of the masks, built once per
+ * tokenizer and shared by every compile against it (the paper keeps its
+ * vocabulary matcher per tokenizer and reuses it across schemas, Section 4.2
+ * and the deployment paragraph of Section 5): token offsets, an exact hash of
+ * every distinct token string, duplicate chains and the token-length table,
+ * uploaded on `stream`.
+ *
+ *   tok_bytes, tok_off  V tokens in CSR form (as for tam_compile).  Host memory,
+ *                       copied before return.
+ *   flags               TAM_FLAG_HOST_ONLY (no device copy, for host-only
+ *                       compiles) or 0; other bits are ignored.
+ *   alloc               NULL = hipMalloc / hipFree; it must stay valid until the
+ *                       vocabulary is freed (after its last handle).
+ * The vocabulary is reference counted: every handle compiled against it holds
+ * a reference, and tam_vocab_destroy drops the caller's.  Errors: TAM_E_INVAL,
+ * TAM_E_NOMEM, TAM_E_DEVICE, TAM_E_TOOLARGE (V or token bytes beyond 2^31-1, a
+ * token longer than 65,535 bytes, a byte string shared by more than 65,535 ids).
+ */
+tam_status tam_vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, uint32_t flags,
+                            const tam_allocator *alloc, void *stream, tam_vocab **out);
+
+/* tam_vocab_destroy -- drops the caller's reference (NULL is a no-op). */
+void tam_vocab_destroy(tam_vocab *vocab);
+
+/*
+ * tam_compile_vocab -- tam_compile against a vocabulary built by
+ * tam_vocab_create (same arguments otherwise, same result): per set, only the
+ * trie is built on the host; the vocabulary's device tables are reused.  The
+ * handle must live on the vocabulary's device; a device compile needs a
+ * vocabulary built without TAM_FLAG_HOST_ONLY (else TAM_E_STATE).
+ */
+tam_status tam_compile_vocab(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
+                             const tam_vocab *vocab, const int64_t *set_off, int64_t S,
+                             const tam_options *opt, const tam_allocator *alloc, void *stream,
+                             tam_handle **out);
+
 enum {
     TAM_PHASE_LISTS = 1u << 0, /* sparse per-node valid lists (suffix probes, prefix sum, fill) */
     TAM_PHASE_ZERO = 1u << 1,  /* zero fill of the dense table */
@@ -177,9 +215,10 @@ enum {
 /*
  * tam_rebuild -- rerun device phases of tam_compile from the handle's resident
  * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask; 0 =
- * the handle's default (TAM_PHASE_TABLE with a dense table, TAM_PHASE_LISTS
- * with TAM_FLAG_NO_TABLE).  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the same
- * bits into the current table.  Used to time the device phase kernel by kernel.
+ * the handle's default: TAM_PHASE_TABLE for a dense table, TAM_PHASE_LISTS
+ * with TAM_FLAG_NO_TABLE (the other kind returns TAM_E_STATE).  TAM_PHASE_MARK
+ * without TAM_PHASE_ZERO ORs the same bits into the current table.  Used to
+ * time the device phase kernel by kernel.
  */
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
 

@@ -8,8 +8,8 @@ per-step serving operations.  All of them call ``libtam.so`` (C ABI in
 from .tam import (DTYPE_BF16, DTYPE_FP32, FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, PHASE_LISTS, PHASE_MARK,
                   PHASE_TABLE, PHASE_ZERO,
                   TAM_DEAD,
-                  Handle, TamError, compile, lib)
+                  Handle, TamError, Vocab, compile, lib)
 
-__all__ = ["compile", "Handle", "TamError", "lib", "TAM_DEAD", "DTYPE_FP32", "DTYPE_BF16",
+__all__ = ["compile", "Vocab", "Handle", "TamError", "lib", "TAM_DEAD", "DTYPE_FP32", "DTYPE_BF16",
            "FLAG_HOST_ONLY", "FLAG_NO_TABLE", "FLAG_TIMING", "PHASE_LISTS", "PHASE_ZERO", "PHASE_MARK",
            "PHASE_TABLE"]

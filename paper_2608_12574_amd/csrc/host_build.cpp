@@ -163,7 +163,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
  * only when the bucket is full.  Duplicate strings share a slot and chain their
  * ids in ascending order.
  */
-tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_handle *h,
+tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_vocab *h,
                        std::string *err) {
     const int64_t total = to[V] - to[0];
     if (total >= INT32_MAX) {
@@ -250,10 +250,10 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_hand
  * token string of each length d <= min(depth(m), max_len), carrying at most the
  * largest duplicate count among strings of that length.
  */
-int64_t entry_upper_bound(const tam_handle *h) {
-    const int64_t L = h->max_tok_len;
+int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
+    const int64_t L = v->max_tok_len;
     std::vector<int64_t> dup(L + 1, 0);
-    for (const SlotMeta &s : h->smeta) {
+    for (const SlotMeta &s : v->smeta) {
         if (s.first < 0) continue;
         dup[(size_t)s.len] = std::max<int64_t>(dup[(size_t)s.len], s.count);
     }

@@ -41,44 +41,26 @@ bool csr_ok(const int64_t *off, int64_t n) {
     return true;
 }
 
-void *dev_alloc(tam_handle *h, size_t bytes) {
+void *alloc_with(bool own, const tam_allocator &a, size_t bytes) {
     bytes = std::max<size_t>(bytes, 256);
     void *p = nullptr;
-    if (h->own_alloc) {
+    if (own) {
         if (hipMalloc(&p, bytes) != hipSuccess) return nullptr;
     } else {
-        p = h->alloc.alloc(bytes, h->alloc.ctx);
+        p = a.alloc(bytes, a.ctx);
     }
-    if (p) h->dev_ptrs.push_back(p);
     return p;
 }
 
-void release_device(tam_handle *h) {
-    if (h->work_done) (void)hipEventSynchronize(h->work_done);
-    if (h->have_events) (void)hipEventSynchronize(h->ev[3]);
-    for (void *p : h->dev_ptrs) {
-        if (h->own_alloc)
-            (void)hipFree(p);
-        else
-            h->alloc.free(p, h->alloc.ctx);
-    }
-    h->dev_ptrs.clear();
-    if (h->have_events)
-        for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
-    if (h->work_done) (void)hipEventDestroy(h->work_done);
-    if (h->side) {
-        (void)hipStreamSynchronize(h->side);
-        (void)hipStreamDestroy(h->side);
-    }
-    if (h->fork) (void)hipEventDestroy(h->fork);
-    if (h->join) (void)hipEventDestroy(h->join);
-    h->have_events = false;
-    h->work_done = nullptr;
-    h->side = nullptr;
-    h->fork = h->join = nullptr;
+void free_with(bool own, const tam_allocator &a, void *p) {
+    if (!p) return;
+    if (own)
+        (void)hipFree(p);
+    else
+        a.free(p, a.ctx);
 }
 
-// Sub-allocation of the small tables inside one device arena.
+// Sub-allocation of small tables inside one device arena.
 struct Arena {
     size_t used = 0;
     template <typename T>
@@ -89,13 +71,141 @@ struct Arena {
     }
 };
 
+// ------------------------------------------------------------- vocabulary --
+
+void vocab_release(tam_vocab *v) {
+    if (!v) return;
+    if (v->refs.fetch_sub(1) != 1) return;
+    if (v->ready) {
+        (void)hipEventSynchronize(v->ready);
+        (void)hipEventDestroy(v->ready);
+    }
+    free_with(v->own_alloc, v->alloc, v->arena);
+    delete v;
+}
+
+tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, uint32_t flags,
+                        const tam_allocator *alloc, hipStream_t s, tam_vocab **out) {
+    *out = nullptr;
+    if (V <= 0) return fail(TAM_E_INVAL, "V must be >= 1");
+    if (V >= INT32_MAX) return fail(TAM_E_TOOLARGE, "V must be < 2^31-1");
+    if (!csr_ok(tok_off, V)) return fail(TAM_E_INVAL, "tok_off must start at 0 and be non-decreasing");
+    if (!tok_bytes && tok_off[V] > 0) return fail(TAM_E_INVAL, "tok_bytes is null");
+    if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
+    tam_vocab *v = new (std::nothrow) tam_vocab();
+    if (!v) return fail(TAM_E_NOMEM, "out of host memory");
+    v->flags = flags & TAM_FLAG_HOST_ONLY;
+    std::string err;
+    tam_status st;
+    const auto t0 = std::chrono::steady_clock::now();
+    try {
+        st = tam::build_vocab(tok_bytes, tok_off, V, v, &err);
+    } catch (const std::bad_alloc &) {
+        st = TAM_E_NOMEM;
+        err = "out of host memory";
+    }
+    v->host_ms = ms_since(t0);
+    if (st != TAM_OK) {
+        delete v;
+        return fail(st, err);
+    }
+    if (v->flags & TAM_FLAG_HOST_ONLY) {
+        *out = v;
+        return TAM_OK;
+    }
+    const auto t1 = std::chrono::steady_clock::now();
+    (void)hipGetLastError();
+    if (hipGetDevice(&v->device) != hipSuccess) {
+        delete v;
+        return fail(TAM_E_DEVICE, "no HIP device");
+    }
+    v->own_alloc = alloc == nullptr;
+    if (alloc) v->alloc = *alloc;
+    Arena a;
+    const size_t o_off = a.take<uint32_t>(V + 1);
+    const size_t o_blob = a.take<uint8_t>((int64_t)v->tok_blob.size());
+    const size_t o_fps = a.take<uint32_t>((int64_t)v->fps.size());
+    const size_t o_srev = a.take<tam::SlotRev>((int64_t)v->srev.size());
+    const size_t o_smeta = a.take<tam::SlotMeta>((int64_t)v->smeta.size());
+    const size_t o_dup = a.take<int32_t>(V);
+    const size_t o_len = a.take<uint8_t>((int64_t)v->len_present.size());
+    uint8_t *base = static_cast<uint8_t *>(alloc_with(v->own_alloc, v->alloc, a.used));
+    if (!base) {
+        delete v;
+        return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used) + " bytes requested)");
+    }
+    v->arena = base;
+    v->device_bytes = (int64_t)a.used;
+    v->d_tok_off = reinterpret_cast<const uint32_t *>(base + o_off);
+    v->d_tok_blob = base + o_blob;
+    v->d_fps = reinterpret_cast<const uint32_t *>(base + o_fps);
+    v->d_srev = reinterpret_cast<const tam::SlotRev *>(base + o_srev);
+    v->d_smeta = reinterpret_cast<const tam::SlotMeta *>(base + o_smeta);
+    v->d_dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
+    v->d_len_present = base + o_len;
+    auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
+        if (bytes == 0) return hipSuccess;
+        return hipMemcpyAsync(base + off, src, bytes, hipMemcpyHostToDevice, s);
+    };
+    hipError_t e = up(o_off, v->tok_off.data(), v->tok_off.size() * 4);
+    if (e == hipSuccess) e = up(o_blob, v->tok_blob.data(), v->tok_blob.size());
+    if (e == hipSuccess) e = up(o_fps, v->fps.data(), v->fps.size() * sizeof(uint32_t));
+    if (e == hipSuccess) e = up(o_srev, v->srev.data(), v->srev.size() * sizeof(tam::SlotRev));
+    if (e == hipSuccess) e = up(o_smeta, v->smeta.data(), v->smeta.size() * sizeof(tam::SlotMeta));
+    if (e == hipSuccess) e = up(o_dup, v->dup_next.data(), v->dup_next.size() * 4);
+    if (e == hipSuccess) e = up(o_len, v->len_present.data(), v->len_present.size());
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&v->ready, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(v->ready, s);
+    v->upload_ms = ms_since(t1);
+    if (e != hipSuccess) {
+        st = hip_fail(e, "vocabulary upload");
+        const std::string msg = g_err;
+        vocab_release(v);
+        return fail(st, msg);
+    }
+    *out = v;
+    return TAM_OK;
+}
+
+// ------------------------------------------------------------------ handle --
+
+void *dev_alloc(tam_handle *h, size_t bytes) {
+    void *p = alloc_with(h->own_alloc, h->alloc, bytes);
+    if (p) h->dev_ptrs.push_back(p);
+    return p;
+}
+
+void release_device(tam_handle *h) {
+    if (h->work_done) (void)hipEventSynchronize(h->work_done);
+    if (h->have_events) (void)hipEventSynchronize(h->ev[3]);
+    if (h->side) (void)hipStreamSynchronize(h->side);
+    for (void *p : h->dev_ptrs) free_with(h->own_alloc, h->alloc, p);
+    h->dev_ptrs.clear();
+    if (h->have_events)
+        for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
+    if (h->work_done) (void)hipEventDestroy(h->work_done);
+    if (h->side) (void)hipStreamDestroy(h->side);
+    if (h->fork) (void)hipEventDestroy(h->fork);
+    if (h->join) (void)hipEventDestroy(h->join);
+    h->have_events = false;
+    h->work_done = nullptr;
+    h->side = nullptr;
+    h->fork = h->join = nullptr;
+}
+
+void destroy_handle(tam_handle *h) {
+    if (!(h->flags & TAM_FLAG_HOST_ONLY)) release_device(h);
+    vocab_release(h->vocab);
+    delete h;
+}
+
 unsigned default_phases(const tam_handle *h) {
     return h->dt.table ? unsigned(TAM_PHASE_TABLE) : unsigned(TAM_PHASE_LISTS);
 }
 
-// The device part of compile.  Lists: probes counting per node, prefix sum,
-// probes filling the lists.  Table: zero fill, then probes setting the bits.
-// Phase events are recorded only for the handle's default phases.
+// The device part of compile.  Lists: probes, counts per node, prefix sum,
+// fill.  Table: zero fill with the probes beside it on the side stream, then
+// the marks.  Phase events are recorded only for the handle's default phases.
 tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     const tam::DevTables &t = h->dt;
     const bool timing = h->have_events && phases == default_phases(h);
@@ -122,11 +232,10 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     if ((phases & TAM_PHASE_ZERO) && t.table) TAM_HIP(tam::launch_zero(t.table, t.N * t.Wp, s));
     if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
     if ((phases & TAM_PHASE_MARK) && t.table) {
-        if (overlap) {
+        if (overlap)
             TAM_HIP(hipStreamWaitEvent(s, h->join, 0));
-        } else {
+        else
             TAM_HIP(tam::launch_probe(t, s));
-        }
         TAM_HIP(tam::launch_mark(t, h->pairs, s));
     }
     if (timing) {
@@ -143,26 +252,14 @@ tam_status check_device_handle(const tam_handle *h) {
     return TAM_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char *tam_last_error(void) { return g_err.c_str(); }
-
-tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
-                       const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V,
-                       const int64_t *set_off, int64_t S, const tam_options *opt,
-                       const tam_allocator *alloc, void *stream, tam_handle **out) {
-    g_err.clear();
-    if (!out) return fail(TAM_E_INVAL, "out is null");
+// Compile against a built vocabulary (the handle takes one reference to it).
+tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_t K, tam_vocab *vocab,
+                        const int64_t *set_off, int64_t S, const tam_options *opt, const tam_allocator *alloc,
+                        hipStream_t s, tam_handle **out) {
     *out = nullptr;
     if (K <= 0) return fail(TAM_E_INVAL, "K must be >= 1");
-    if (V <= 0) return fail(TAM_E_INVAL, "V must be >= 1");
     if (!csr_ok(str_off, K)) return fail(TAM_E_INVAL, "str_off must start at 0 and be non-decreasing");
-    if (!csr_ok(tok_off, V)) return fail(TAM_E_INVAL, "tok_off must start at 0 and be non-decreasing");
     if (!str_bytes && str_off[K] > 0) return fail(TAM_E_INVAL, "str_bytes is null");
-    if (!tok_bytes && tok_off[V] > 0) return fail(TAM_E_INVAL, "tok_bytes is null");
-    if (V >= INT32_MAX) return fail(TAM_E_TOOLARGE, "V must be < 2^31-1");
     const int64_t one_set[2] = {0, K};
     if (!set_off || S == 0) {
         set_off = one_set;
@@ -175,24 +272,24 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     if (opt) o = *opt;
     if (o.terminator < 0 || o.terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
     if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
+    const bool host_only = (o.flags & TAM_FLAG_HOST_ONLY) != 0;
+    if (!host_only && (vocab->flags & TAM_FLAG_HOST_ONLY))
+        return fail(TAM_E_STATE, "a device compile needs a vocabulary built without TAM_FLAG_HOST_ONLY");
 
     tam_handle *h = new (std::nothrow) tam_handle();
     if (!h) return fail(TAM_E_NOMEM, "out of host memory");
     h->terminator = o.terminator;
     h->flags = o.flags;
+    vocab->refs.fetch_add(1);
+    h->vocab = vocab;
     std::string err;
     tam_status st;
     try {
-        auto t0 = std::chrono::steady_clock::now();
+        const auto t0 = std::chrono::steady_clock::now();
         st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);
         h->timing.host_trie_ms = ms_since(t0);
         if (st == TAM_OK) {
-            t0 = std::chrono::steady_clock::now();
-            st = tam::build_vocab(tok_bytes, tok_off, V, h, &err);
-            h->timing.host_vocab_ms = ms_since(t0);
-        }
-        if (st == TAM_OK) {
-            h->entry_bound = tam::entry_upper_bound(h);
+            h->entry_bound = tam::entry_upper_bound(h, vocab);
             if (h->entry_bound >= INT32_MAX) {
                 st = TAM_E_TOOLARGE;
                 err = "more than 2^31-1 valid (node, token) pairs are possible";
@@ -203,28 +300,33 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
         err = "out of host memory";
     }
     if (st != TAM_OK) {
-        delete h;
+        destroy_handle(h);
         return fail(st, err);
     }
-    h->W = (V + 63) / 64;
+    h->V = vocab->V;
+    h->W = vocab->W;
     h->Wp = (h->W + 7) & ~int64_t(7);  // rows 64-byte aligned
     h->timing.dev_lists_ms = h->timing.dev_zero_ms = h->timing.dev_mark_ms = -1.f;
     h->timing.dev_total_ms = -1.f;
-    if (h->flags & TAM_FLAG_HOST_ONLY) {
+    if (host_only) {
         *out = h;
         return TAM_OK;
     }
 
-    // ---- device: allocate, upload, build the lists and the table ----
+    // ---- device: allocate, upload, build the lists or the table ----
     const auto t0 = std::chrono::steady_clock::now();
-    hipStream_t s = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
     if (hipGetDevice(&h->device) != hipSuccess) {
-        delete h;
+        destroy_handle(h);
         return fail(TAM_E_DEVICE, "no HIP device");
+    }
+    if (h->device != vocab->device) {
+        destroy_handle(h);
+        return fail(TAM_E_STATE, "the vocabulary lives on another device");
     }
     h->own_alloc = alloc == nullptr;
     if (alloc) h->alloc = *alloc;
+    const bool want_table = !(h->flags & TAM_FLAG_NO_TABLE);
 
     Arena a;
     const size_t o_blob = a.take<uint8_t>(h->blob_bytes);
@@ -234,32 +336,25 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     const size_t o_child_off = a.take<int32_t>(h->N + 1);
     const size_t o_child_byte = a.take<uint8_t>((int64_t)h->child_byte.size());
     const size_t o_child_node = a.take<int32_t>((int64_t)h->child_node.size());
-    const size_t o_tok_off = a.take<uint32_t>(V + 1);
-    const size_t o_tok_blob = a.take<uint8_t>((int64_t)h->tok_blob.size());
-    const size_t o_fps = a.take<uint32_t>((int64_t)h->fps.size());
-    const size_t o_srev = a.take<tam::SlotRev>((int64_t)h->srev.size());
-    const size_t o_smeta = a.take<tam::SlotMeta>((int64_t)h->smeta.size());
     const size_t o_hits = a.take<int32_t>(tam::kWin * h->N);
-    const size_t o_dup = a.take<int32_t>(V);
-    const size_t o_len = a.take<uint8_t>((int64_t)h->len_present.size());
     const size_t o_count = a.take<int32_t>(h->N);
     const size_t o_row_ptr = a.take<int32_t>(h->N + 1);
     const size_t o_cursor = a.take<int32_t>(h->N);
-    const size_t o_entries = a.take<int32_t>(h->entry_bound);
+    const size_t o_entries = a.take<int32_t>(want_table ? 1 : h->entry_bound);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
     const size_t o_pairs = a.take<int32_t>(tam::mark_blocks(h->N));
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = nullptr;
     const size_t table_bytes = (size_t)h->N * (size_t)h->Wp * sizeof(uint64_t);
-    if (base && !(h->flags & TAM_FLAG_NO_TABLE)) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
-    if (!base || (!table && !(h->flags & TAM_FLAG_NO_TABLE))) {
-        release_device(h);
-        delete h;
+    if (base && want_table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
+    if (!base || (want_table && !table)) {
+        destroy_handle(h);
         return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
                                      " bytes requested)");
     }
     h->device_bytes = (int64_t)a.used + (table ? (int64_t)table_bytes : 0);
+    h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
 
     tam::DevTables &t = h->dt;
     t.blob = base + o_blob;
@@ -269,35 +364,34 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     t.child_off = reinterpret_cast<const int32_t *>(base + o_child_off);
     t.child_byte = base + o_child_byte;
     t.child_node = reinterpret_cast<const int32_t *>(base + o_child_node);
-    t.tok_off = reinterpret_cast<const uint32_t *>(base + o_tok_off);
-    t.tok_blob = base + o_tok_blob;
-    t.fps = reinterpret_cast<const uint32_t *>(base + o_fps);
-    t.srev = reinterpret_cast<const tam::SlotRev *>(base + o_srev);
-    t.smeta = reinterpret_cast<const tam::SlotMeta *>(base + o_smeta);
+    t.tok_off = vocab->d_tok_off;
+    t.tok_blob = vocab->d_tok_blob;
+    t.fps = vocab->d_fps;
+    t.srev = vocab->d_srev;
+    t.smeta = vocab->d_smeta;
+    t.dup_next = vocab->d_dup_next;
+    t.len_present = vocab->d_len_present;
     t.hits = reinterpret_cast<int32_t *>(base + o_hits);
-    t.dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
-    t.len_present = base + o_len;
     t.count = reinterpret_cast<int32_t *>(base + o_count);
     t.row_ptr = reinterpret_cast<int32_t *>(base + o_row_ptr);
     t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
     t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
-    h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
     t.table = table;
     t.N = h->N;
     t.V = h->V;
     t.W = h->W;
     t.Wp = h->Wp;
     t.blob_bytes = h->blob_bytes;
-    t.slot_mask = (uint64_t)h->fps.size() - 1;
-    t.len_mask = h->len_mask;
-    t.max_len = (int32_t)h->max_tok_len;
+    t.slot_mask = (uint64_t)vocab->fps.size() - 1;
+    t.len_mask = vocab->len_mask;
+    t.max_len = (int32_t)vocab->max_tok_len;
 
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
         if (bytes == 0) return hipSuccess;
         return hipMemcpyAsync(base + off, src, bytes, hipMemcpyHostToDevice, s);
     };
-    hipError_t e = hipSuccess;
+    hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
     if (e == hipSuccess) e = up(o_blob, h->blob.data(), h->blob.size());
     if (e == hipSuccess) e = up(o_node_at, h->node_at.data(), h->node_at.size() * 4);
     if (e == hipSuccess) e = up(o_node_pos, h->node_pos.data(), h->node_pos.size() * 4);
@@ -305,40 +399,82 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     if (e == hipSuccess) e = up(o_child_off, h->child_off.data(), h->child_off.size() * 4);
     if (e == hipSuccess) e = up(o_child_byte, h->child_byte.data(), h->child_byte.size());
     if (e == hipSuccess) e = up(o_child_node, h->child_node.data(), h->child_node.size() * 4);
-    if (e == hipSuccess) e = up(o_tok_off, h->tok_off.data(), h->tok_off.size() * 4);
-    if (e == hipSuccess) e = up(o_tok_blob, h->tok_blob.data(), h->tok_blob.size());
-    if (e == hipSuccess) e = up(o_fps, h->fps.data(), h->fps.size() * sizeof(uint32_t));
-    if (e == hipSuccess) e = up(o_srev, h->srev.data(), h->srev.size() * sizeof(tam::SlotRev));
-    if (e == hipSuccess) e = up(o_smeta, h->smeta.data(), h->smeta.size() * sizeof(tam::SlotMeta));
-    if (e == hipSuccess) e = up(o_dup, h->dup_next.data(), h->dup_next.size() * 4);
-    if (e == hipSuccess) e = up(o_len, h->len_present.data(), h->len_present.size());
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && table) e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
     if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
     if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
-        for (hipEvent_t &ev : h->ev) {
+        for (hipEvent_t &ev : h->ev)
             if (e == hipSuccess) e = hipEventCreate(&ev);
-        }
         h->have_events = e == hipSuccess;
     }
     h->timing.upload_ms = ms_since(t0);
     if (e != hipSuccess) {
         st = hip_fail(e, "upload");
-        release_device(h);
-        delete h;
-        return st;
+        const std::string msg = g_err;
+        destroy_handle(h);
+        return fail(st, msg);
     }
     st = run_device_phase(h, default_phases(h), s);
     if (st != TAM_OK) {
         const std::string msg = g_err;
-        release_device(h);
-        delete h;
+        destroy_handle(h);
         return fail(st, msg);
     }
     *out = h;
     return TAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tam_last_error(void) { return g_err.c_str(); }
+
+tam_status tam_vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, uint32_t flags,
+                            const tam_allocator *alloc, void *stream, tam_vocab **out) {
+    g_err.clear();
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    return vocab_create(tok_bytes, tok_off, V, flags, alloc, static_cast<hipStream_t>(stream), out);
+}
+
+void tam_vocab_destroy(tam_vocab *v) { vocab_release(v); }
+
+tam_status tam_compile_vocab(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
+                             const tam_vocab *vocab, const int64_t *set_off, int64_t S,
+                             const tam_options *opt, const tam_allocator *alloc, void *stream,
+                             tam_handle **out) {
+    g_err.clear();
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    *out = nullptr;
+    if (!vocab) return fail(TAM_E_INVAL, "vocab is null");
+    return compile_with(str_bytes, str_off, K, const_cast<tam_vocab *>(vocab), set_off, S, opt, alloc,
+                        static_cast<hipStream_t>(stream), out);
+}
+
+tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
+                       const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V,
+                       const int64_t *set_off, int64_t S, const tam_options *opt,
+                       const tam_allocator *alloc, void *stream, tam_handle **out) {
+    g_err.clear();
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    *out = nullptr;
+    if (K <= 0) return fail(TAM_E_INVAL, "K must be >= 1");
+    if (!csr_ok(str_off, K)) return fail(TAM_E_INVAL, "str_off must start at 0 and be non-decreasing");
+    tam_options o{0x22, 0};
+    if (opt) o = *opt;
+    tam_vocab *v = nullptr;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    tam_status st = vocab_create(tok_bytes, tok_off, V, o.flags, alloc, s, &v);
+    if (st != TAM_OK) return st;
+    st = compile_with(str_bytes, str_off, K, v, set_off, S, &o, alloc, s, out);
+    if (st == TAM_OK) {
+        (*out)->timing.host_vocab_ms = v->host_ms;
+        (*out)->timing.upload_ms += v->upload_ms;
+    }
+    vocab_release(v);  // the handle keeps its own reference
+    return st;
 }
 
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
@@ -348,6 +484,8 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
     if (phases == 0) phases = default_phases(h);
     if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
     if ((phases & TAM_PHASE_TABLE) && !h->dt.table) return fail(TAM_E_STATE, "handle has no dense table");
+    if ((phases & TAM_PHASE_LISTS) && h->dt.table)
+        return fail(TAM_E_STATE, "valid lists are kept only by handles with TAM_FLAG_NO_TABLE");
     return run_device_phase(h, phases, static_cast<hipStream_t>(stream));
 }
 
@@ -359,7 +497,7 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
     out->vocab_size = h->V;
     out->words_per_row = h->W;
     out->row_stride_words = h->dt.table ? h->Wp : 0;
-    out->max_token_len = h->max_tok_len;
+    out->max_token_len = h->vocab->max_tok_len;
     out->device_bytes = h->device_bytes;
     out->flags = h->flags;
     out->terminator = h->terminator;
@@ -384,7 +522,6 @@ tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t 
     if (row_stride < h->V) return fail(TAM_E_INVAL, "row_stride must be >= V");
     const size_t elem = dtype == TAM_DTYPE_BF16 ? 2 : 4;
     if ((reinterpret_cast<uintptr_t>(logits) % elem) != 0) return fail(TAM_E_INVAL, "logits are not element-aligned");
-    if (!h->dt.table && !h->lists_built) return fail(TAM_E_STATE, "the valid lists have not been built");
     TAM_HIP(hipGetLastError());
     TAM_HIP(tam::launch_apply(h->dt, node_ids, B, logits, dtype, row_stride, static_cast<hipStream_t>(stream)));
     return TAM_OK;
@@ -414,7 +551,6 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
     if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return fail(TAM_E_INVAL, "out must be 8-byte aligned");
     TAM_HIP(hipGetLastError());
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (!h->dt.table && !h->lists_built) return fail(TAM_E_STATE, "the valid lists have not been built");
     if (h->dt.table)
         TAM_HIP(tam::launch_export_dense(h->dt, node_ids, n, out, s));
     else
@@ -459,8 +595,7 @@ tam_status tam_timing_get(const tam_handle *h, tam_timing *out) {
 
 void tam_destroy(tam_handle *h) {
     if (!h) return;
-    if (!(h->flags & TAM_FLAG_HOST_ONLY)) release_device(h);
-    delete h;
+    destroy_handle(h);
 }
 
 }  // extern "C"

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -110,6 +111,41 @@ int64_t scan_tmp_elems(int64_t N);
 }  // namespace tam
 
 // ---------------------------------------------------------------------------
+// A vocabulary's tables, built once per tokenizer and shared (reference
+// counted) by every handle compiled against it.
+// ---------------------------------------------------------------------------
+struct tam_vocab {
+    std::atomic<int> refs{1};
+    uint32_t flags = 0;
+    int device = 0;
+    bool own_alloc = false;
+    tam_allocator alloc{};
+
+    int64_t V = 0, W = 0, max_tok_len = 0, device_bytes = 0;
+    uint64_t len_mask = 0;
+    double host_ms = 0, upload_ms = 0;
+
+    // host tables
+    std::vector<uint32_t> tok_off;
+    std::vector<uint8_t> tok_blob, len_present;
+    std::vector<uint32_t> fps;
+    std::vector<tam::SlotRev> srev;
+    std::vector<tam::SlotMeta> smeta;
+    std::vector<int32_t> dup_next;
+
+    // device copies (one arena)
+    void *arena = nullptr;
+    const uint32_t *d_tok_off = nullptr;
+    const uint8_t *d_tok_blob = nullptr;
+    const uint32_t *d_fps = nullptr;
+    const tam::SlotRev *d_srev = nullptr;
+    const tam::SlotMeta *d_smeta = nullptr;
+    const int32_t *d_dup_next = nullptr;
+    const uint8_t *d_len_present = nullptr;
+    hipEvent_t ready = nullptr;  // recorded after the uploads
+};
+
+// ---------------------------------------------------------------------------
 // The handle.
 // ---------------------------------------------------------------------------
 struct tam_handle {
@@ -118,21 +154,14 @@ struct tam_handle {
     int device = 0;
     bool own_alloc = false;
     tam_allocator alloc{};
+    tam_vocab *vocab = nullptr;  // one reference held by the handle
 
     int64_t N = 0, S = 0, K_unique = 0, V = 0, W = 0, Wp = 0;
-    int64_t blob_bytes = 0, max_tok_len = 0, entry_bound = 0, device_bytes = 0;
+    int64_t blob_bytes = 0, entry_bound = 0, device_bytes = 0;
 
     // host trie tables
     std::vector<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
     std::vector<uint8_t> edge, is_final, blob, child_byte;
-    // host vocabulary tables
-    std::vector<uint32_t> tok_off;
-    std::vector<uint8_t> tok_blob, len_present;
-    std::vector<uint32_t> fps;
-    std::vector<tam::SlotRev> srev;
-    std::vector<tam::SlotMeta> smeta;
-    uint64_t len_mask = 0;
-    std::vector<int32_t> dup_next;
 
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};

@@ -27,9 +27,9 @@ STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOM
           -4: "TAM_E_DEVICE", -5: "TAM_E_TOOLARGE", -6: "TAM_E_STATE"}
 
 # the entry points declared in include/tam.h
-ENTRY_POINTS = ("tam_compile", "tam_rebuild", "tam_info_get", "tam_apply_mask", "tam_advance",
-                "tam_export_rows", "tam_valid_pairs", "tam_timing_get", "tam_destroy",
-                "tam_last_error")
+ENTRY_POINTS = ("tam_compile", "tam_vocab_create", "tam_compile_vocab", "tam_rebuild", "tam_info_get",
+                "tam_apply_mask", "tam_advance", "tam_export_rows", "tam_valid_pairs", "tam_timing_get",
+                "tam_vocab_destroy", "tam_destroy", "tam_last_error")
 
 
 class TamError(RuntimeError):
@@ -85,6 +85,12 @@ def lib() -> ctypes.CDLL:
         P, i64 = ctypes.c_void_p, ctypes.c_int64
         L.tam_compile.argtypes = [P, P, i64, P, P, i64, P, i64, ctypes.POINTER(Options),
                                   ctypes.POINTER(Allocator), P, ctypes.POINTER(P)]
+        L.tam_vocab_create.argtypes = [P, P, i64, ctypes.c_uint32, ctypes.POINTER(Allocator), P,
+                                       ctypes.POINTER(P)]
+        L.tam_compile_vocab.argtypes = [P, P, i64, P, P, i64, ctypes.POINTER(Options),
+                                        ctypes.POINTER(Allocator), P, ctypes.POINTER(P)]
+        L.tam_vocab_destroy.argtypes = [P]
+        L.tam_vocab_destroy.restype = None
         L.tam_rebuild.argtypes = [P, ctypes.c_uint, P]
         L.tam_info_get.argtypes = [P, ctypes.POINTER(Info)]
         L.tam_apply_mask.argtypes = [P, P, i64, P, ctypes.c_int, i64, P]
@@ -95,8 +101,9 @@ def lib() -> ctypes.CDLL:
         L.tam_destroy.argtypes = [P]
         L.tam_destroy.restype = None
         L.tam_last_error.restype = ctypes.c_char_p
-        for name in ENTRY_POINTS[:-2]:
-            getattr(L, name).restype = ctypes.c_int
+        for name in ENTRY_POINTS:
+            if name not in ("tam_vocab_destroy", "tam_destroy", "tam_last_error"):
+                getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -249,15 +256,54 @@ class Handle:
         return t.as_dict()
 
 
+class Vocab:
+    """A vocabulary's device tables, built once per tokenizer (tam_vocab_create)
+    and shared by every compile against it."""
+
+    def __init__(self, tokens, host_only: bool = False, device=None, stream=None):
+        tb, to = csr(tokens)
+        self.size = len(to) - 1
+        self.host_only = host_only
+        self._alloc = None
+        raw = ctypes.c_void_p()
+        if host_only:
+            rc = lib().tam_vocab_create(_ptr(tb), _ptr(to), self.size, FLAG_HOST_ONLY, None, None,
+                                        ctypes.byref(raw))
+            self.device = None
+        else:
+            import torch
+            dev = torch.device(device if device is not None else "cuda")
+            if dev.index is None:
+                dev = torch.device("cuda", torch.cuda.current_device())
+            self.device = dev
+            self._alloc = _TorchAllocator(dev)
+            with torch.cuda.device(dev):
+                rc = lib().tam_vocab_create(_ptr(tb), _ptr(to), self.size, 0, ctypes.byref(self._alloc.struct),
+                                            _stream_ptr(stream), ctypes.byref(raw))
+        _check(rc, "tam_vocab_create")
+        self._raw = raw
+
+    def close(self):
+        if getattr(self, "_raw", None) is not None:
+            lib().tam_vocab_destroy(self._raw)
+            self._raw = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, device=None,
             stream=None) -> Handle:
-    """tam_compile over ``strings`` (list[bytes]) and ``vocab`` (list[bytes], id = index).
+    """tam_compile over ``strings`` (list[bytes]) and ``vocab`` (a ``Vocab`` or a
+    list[bytes], token id = index).
 
     ``sets``: optional forest offsets (S+1 ints) splitting ``strings`` into S sets.
     With ``FLAG_HOST_ONLY`` no GPU is touched (host tables only).
     """
     sb, so = csr(strings)
-    tb, to = csr(vocab)
     set_arr = None
     S = 0
     if sets is not None:
@@ -267,7 +313,8 @@ def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, d
     raw = ctypes.c_void_p()
     host_only = bool(flags & FLAG_HOST_ONLY)
     allocator = None
-    stream_p = ctypes.c_void_p(None)
+    sets_p = _ptr(set_arr) if set_arr is not None else None
+    keep = None
     if not host_only:
         import torch
         device = torch.device(device if device is not None else "cuda")
@@ -276,13 +323,26 @@ def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, d
         allocator = _TorchAllocator(device)
         with torch.cuda.device(device):
             stream_p = _stream_ptr(stream)
-            rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1,
-                                   _ptr(set_arr) if set_arr is not None else None, S,
-                                   ctypes.byref(opt), ctypes.byref(allocator.struct), stream_p,
-                                   ctypes.byref(raw))
+            if isinstance(vocab, Vocab):
+                keep = vocab
+                rc = lib().tam_compile_vocab(_ptr(sb), _ptr(so), len(so) - 1, vocab._raw, sets_p, S,
+                                             ctypes.byref(opt), ctypes.byref(allocator.struct), stream_p,
+                                             ctypes.byref(raw))
+            else:
+                tb, to = csr(vocab)
+                rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1,
+                                       sets_p, S, ctypes.byref(opt), ctypes.byref(allocator.struct), stream_p,
+                                       ctypes.byref(raw))
     else:
-        rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1,
-                               _ptr(set_arr) if set_arr is not None else None, S, ctypes.byref(opt),
-                               None, None, ctypes.byref(raw))
+        if isinstance(vocab, Vocab):
+            keep = vocab
+            rc = lib().tam_compile_vocab(_ptr(sb), _ptr(so), len(so) - 1, vocab._raw, sets_p, S,
+                                         ctypes.byref(opt), None, None, ctypes.byref(raw))
+        else:
+            tb, to = csr(vocab)
+            rc = lib().tam_compile(_ptr(sb), _ptr(so), len(so) - 1, _ptr(tb), _ptr(to), len(to) - 1, sets_p, S,
+                                   ctypes.byref(opt), None, None, ctypes.byref(raw))
     _check(rc, "tam_compile")
-    return Handle(raw, allocator, device, host_only)
+    h = Handle(raw, allocator, device, host_only)
+    h._vocab = keep  # the vocabulary's allocator must outlive the handle
+    return h

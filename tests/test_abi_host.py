@@ -90,6 +90,19 @@ def test_host_trie_forest(P):
     assert h.num_sets == 32
 
 
+def test_host_only_vocabulary_reuse(P):
+    w = W.config(1)
+    voc = P.Vocab(w.vocab, host_only=True)
+    h1 = P.compile(w.strings, voc, flags=P.FLAG_HOST_ONLY)
+    h2 = P.compile(w.strings[:40], voc, flags=P.FLAG_HOST_ONLY)
+    voc.close()
+    same_trie(h1, Oracle(w.strings, [b"x"]))
+    same_trie(h2, Oracle(w.strings[:40], [b"x"]))
+    assert h1.vocab_size == w.V and h1.max_token_len == max(len(t) for t in w.vocab)
+    h1.close()
+    h2.close()
+
+
 def test_other_terminator(P):
     strings = [b'say "hi"', b"say"]
     h = host(P, strings, [b"a"], terminator=ord("|"))
@@ -126,6 +139,27 @@ def test_error_paths(P):
     assert raw_compile(P, sb, so, 2, tb, to, 2, set_off=sets, S=2)[0] == -1   # empty set
     sets = np.array([0, 1], dtype=np.int64)
     assert raw_compile(P, sb, so, 2, tb, to, 2, set_off=sets, S=1)[0] == -1   # does not end at K
+
+
+def test_vocab_error_paths(P):
+    L = P.lib()
+    out = ctypes.c_void_p()
+    tb, to = P.tam.csr([b"a", b"b"])
+    p = lambda a: ctypes.c_void_p(a.ctypes.data)  # noqa: E731
+    assert L.tam_vocab_create(p(tb), p(to), 0, 1, None, None, ctypes.byref(out)) == -1
+    assert L.tam_vocab_create(p(tb), None, 2, 1, None, None, ctypes.byref(out)) == -1
+    assert L.tam_vocab_create(p(tb), p(to), 2, 1, None, None, None) == -1
+    assert L.tam_vocab_create(p(tb), p(to), 2, 1, None, None, ctypes.byref(out)) == 0
+    sb, so = P.tam.csr([b"ab"])
+    h = ctypes.c_void_p()
+    # a device compile against a host-only vocabulary is refused before any HIP call
+    opt = P.tam.Options(0x22, 0)
+    assert L.tam_compile_vocab(p(sb), p(so), 1, out, None, 0, ctypes.byref(opt), None, None,
+                               ctypes.byref(h)) == -6
+    assert L.tam_compile_vocab(p(sb), p(so), 1, None, None, 0, ctypes.byref(opt), None, None,
+                               ctypes.byref(h)) == -1
+    L.tam_vocab_destroy(out)
+    L.tam_vocab_destroy(None)
 
 
 def test_host_only_handle_refuses_device_work(P):

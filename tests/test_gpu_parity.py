@@ -238,8 +238,30 @@ def test_config_rebuild_identical(P, compiled):
     h.rebuild(phases=P.PHASE_MARK)
     assert np.array_equal(gpu_rows(h, nodes), before)
     assert h.valid_pairs() == M
-    h.rebuild(phases=P.PHASE_LISTS)
-    assert np.array_equal(gpu_rows(h, nodes), before)
+    with pytest.raises(P.TamError):
+        h.rebuild(phases=P.PHASE_LISTS)  # lists are kept only without a dense table
+
+
+def test_shared_vocabulary(P):
+    """One vocabulary, built once, serves several compiles (dense and sparse),
+    and outlives its creator's reference through the handles."""
+    w = W.config(2)
+    voc = P.Vocab(w.vocab)
+    o = Oracle(w.strings, w.vocab)
+    h1 = P.compile(w.strings, voc)
+    h2 = P.compile(w.strings[:300], voc, flags=P.FLAG_NO_TABLE)
+    h3 = P.compile(w.strings, w.vocab)
+    o2 = Oracle(w.strings[:300], w.vocab)
+    voc.close()  # the handles keep the vocabulary alive
+    nodes = sample_nodes(o, 48, 21)
+    assert np.array_equal(gpu_rows(h1, nodes), o.mask_rows(nodes))
+    assert np.array_equal(gpu_rows(h3, nodes), o.mask_rows(nodes))
+    nodes2 = sample_nodes(o2, 48, 22)
+    assert np.array_equal(gpu_rows(h2, nodes2), o2.mask_rows(nodes2))
+    assert h1.valid_pairs() == h3.valid_pairs()
+    check_apply(P, h2, o2, W.uniform_nodes(2, o2.N, 8), "fp32", seed=9)
+    for h in (h1, h2, h3):
+        h.close()
 
 
 # ---------------------------------------------------------- sparse / forest --
