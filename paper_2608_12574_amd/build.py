@@ -17,7 +17,7 @@ LIB = os.path.join(PKG, "libtam.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result", f"-I{ROOT}/include"]
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-pthread", "-Wall", "-Wno-unused-result", f"-I{ROOT}/include"]
 # The packed-FP32 VALU forms are switched off for every GPU compile.
 GPU = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
@@ -46,7 +46,7 @@ def build(verbose: bool = False) -> str:
                 sys.stderr.write(e.stdout + e.stderr)
                 raise RuntimeError(f"hipcc failed on {futs[f]}") from e
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *GPU, "-shared", "-fPIC", "-o", tmp, *sorted(objs)]
+    cmd = [HIPCC, *GPU, "-shared", "-fPIC", "-pthread", "-o", tmp, *sorted(objs)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)

@@ -1,8 +1,10 @@
 // Host part of tam_compile: the trie of every set (Section 4.1) and the
 // vocabulary tables used by the device validity kernels.
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <numeric>
+#include <thread>
 
 #include "host_build.hpp"
 
@@ -27,14 +29,126 @@ struct TerminatedLess {
     }
 };
 
+// The trie of one set, with set-local node ids (root = 0) and blob offsets.
+struct SetTrie {
+    std::vector<int32_t> parent, depth, node_pos, node_at, child_off, child_node;
+    std::vector<uint8_t> edge, is_final, blob, child_byte;
+    int64_t K_unique = 0;
+    tam_status st = TAM_OK;
+    std::string err;
+};
+
+/*
+ * Trie construction of one set (Section 4.1: insert every value one byte at a
+ * time, shared prefixes merge).  Inserting the distinct terminated strings in
+ * sorted order creates the new nodes of each string right after its longest
+ * common prefix with the previous string, and that creation order is exactly
+ * the lexicographic preorder the interface fixes.  O(N_chars) after the sort.
+ * Blob layout per string: one pad byte standing for the root, the string, T.
+ */
+void build_one_set(const uint8_t *sb, const int64_t *so, int64_t k0, int64_t k1, uint8_t term, SetTrie &r) {
+    std::vector<int64_t> order((size_t)(k1 - k0));
+    std::iota(order.begin(), order.end(), k0);
+    std::sort(order.begin(), order.end(), TerminatedLess{sb, so, term});
+    const int64_t chars = so[k1] - so[k0];
+    const size_t est = (size_t)(chars + 2 * (k1 - k0) + 1);
+    r.parent.reserve(est);
+    r.depth.reserve(est);
+    r.edge.reserve(est);
+    r.is_final.reserve(est);
+    r.node_pos.reserve(est);
+    r.blob.reserve(est);
+    r.node_at.reserve(est);
+    r.parent.push_back(-1);
+    r.depth.push_back(0);
+    r.edge.push_back(0);
+    r.is_final.push_back(0);
+    r.node_pos.push_back(-1);
+    int64_t N = 1;
+    std::vector<int32_t> path;
+    const uint8_t *prev = nullptr;
+    int64_t prev_len = -1;
+    for (int64_t k : order) {
+        const uint8_t *s = sb + so[k];
+        const int64_t len = so[k + 1] - so[k];
+        int64_t l = 0;
+        if (prev) {
+            const int64_t m = std::min(len, prev_len);
+            while (l < m && prev[l] == s[l]) ++l;
+            if (l == len && len == prev_len) continue;  // duplicate string
+        }
+        prev = s;
+        prev_len = len;
+        ++r.K_unique;
+        if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
+        r.blob.push_back(0);
+        r.node_at.push_back(0);
+        for (int64_t i = 0; i <= len; ++i) {
+            const uint8_t c = i < len ? s[i] : term;
+            r.blob.push_back(c);
+            int32_t id;
+            if (i < l) {
+                id = path[(size_t)i];
+            } else {
+                id = (int32_t)N++;
+                r.parent.push_back(i == 0 ? 0 : path[(size_t)(i - 1)]);
+                r.depth.push_back((int32_t)(i + 1));
+                r.edge.push_back(c);
+                r.is_final.push_back(i == len ? 1 : 0);
+                r.node_pos.push_back((int32_t)(r.blob.size() - 1));
+            }
+            path[(size_t)i] = id;
+            r.node_at.push_back(id);
+        }
+        if (N >= INT32_MAX || (int64_t)r.blob.size() >= INT32_MAX) {
+            r.st = TAM_E_TOOLARGE;
+            r.err = "trie exceeds 2^31-1 nodes or string bytes";
+            return;
+        }
+    }
+    // children in ascending byte order = ascending ids (preorder)
+    r.child_off.assign((size_t)(N + 1), 0);
+    for (int64_t m = 1; m < N; ++m) ++r.child_off[(size_t)r.parent[(size_t)m] + 1];
+    for (int64_t n = 0; n < N; ++n) r.child_off[(size_t)n + 1] += r.child_off[(size_t)n];
+    r.child_node.resize((size_t)(N - 1));
+    r.child_byte.resize((size_t)(N - 1));
+    std::vector<int32_t> fill(r.child_off.begin(), r.child_off.end() - 1);
+    for (int64_t m = 1; m < N; ++m) {
+        const int32_t at = fill[(size_t)r.parent[(size_t)m]]++;
+        r.child_node[(size_t)at] = (int32_t)m;
+        r.child_byte[(size_t)at] = r.edge[(size_t)m];
+    }
+}
+
+// Runs f(j) for j in [0, n) on up to `threads` host threads.
+template <typename F>
+void parallel_for(int64_t n, int threads, F f) {
+    if (threads <= 1 || n <= 1) {
+        for (int64_t j = 0; j < n; ++j) f(j);
+        return;
+    }
+    std::atomic<int64_t> next{0};
+    std::vector<std::thread> pool;
+    for (int i = 0; i < threads; ++i)
+        pool.emplace_back([&] {
+            for (int64_t j = next.fetch_add(1); j < n; j = next.fetch_add(1)) f(j);
+        });
+    for (auto &th : pool) th.join();
+}
+
+int host_threads(int64_t work_items) {
+    const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    return (int)std::min<int64_t>({(int64_t)hw, (int64_t)16, work_items});
+}
+
 }  // namespace
 
 /*
- * Trie construction (Section 4.1: insert every value one byte at a time, shared
- * prefixes merge).  Inserting the distinct terminated strings in sorted order
- * creates the new nodes of each string right after its longest common prefix
- * with the previous string, and that creation order is exactly the
- * lexicographic preorder the interface fixes.  O(N_chars) after the sort.
+ * Tries of all sets: each set is built on its own (in parallel over host
+ * threads for a forest), then the sets are laid out one after another: set j
+ * takes node ids [roots[j], roots[j] + N_j) and its own range of the blob,
+ * which carries 16 zero bytes in front and behind so that a node's 16-byte
+ * path window never leaves it.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err) {
@@ -49,116 +163,76 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             return TAM_E_TERMINATOR;
         }
     }
-    h->roots.assign((size_t)S, 0);
-    h->parent.clear();
-    h->depth.clear();
-    h->edge.clear();
-    h->is_final.clear();
-    h->node_pos.clear();
-    h->blob.clear();
-    h->node_at.clear();
-    h->K_unique = 0;
-
-    int64_t reserve_nodes = total + 2 * K + S;
-    h->parent.reserve((size_t)reserve_nodes);
-    h->depth.reserve((size_t)reserve_nodes);
-    h->edge.reserve((size_t)reserve_nodes);
-    h->is_final.reserve((size_t)reserve_nodes);
-    h->node_pos.reserve((size_t)reserve_nodes);
-    h->blob.reserve((size_t)(total + 2 * K + 2 * kBlobPad));
-    h->node_at.reserve((size_t)(total + 2 * K + 2 * kBlobPad));
-    // zero pad in front, so that a node's 16-byte path window never starts before the blob
-    h->blob.assign((size_t)kBlobPad, 0);
-    h->node_at.assign((size_t)kBlobPad, 0);
-
-    std::vector<int64_t> order;
-    std::vector<int32_t> path;
-    int64_t N = 0;
-    for (int64_t j = 0; j < S; ++j) {
-        const int64_t k0 = set_off[j], k1 = set_off[j + 1];
-        order.resize((size_t)(k1 - k0));
-        std::iota(order.begin(), order.end(), k0);
-        std::sort(order.begin(), order.end(), TerminatedLess{sb, so, term});
-
-        const int32_t root = (int32_t)N++;
-        h->roots[(size_t)j] = root;
-        h->parent.push_back(-1);
-        h->depth.push_back(0);
-        h->edge.push_back(0);
-        h->is_final.push_back(0);
-        h->node_pos.push_back(-1);
-
-        const uint8_t *prev = nullptr;
-        int64_t prev_len = -1;
-        for (int64_t k : order) {
-            const uint8_t *s = sb + so[k];
-            const int64_t len = so[k + 1] - so[k];
-            int64_t l = 0;
-            if (prev) {
-                const int64_t m = std::min(len, prev_len);
-                while (l < m && prev[l] == s[l]) ++l;
-                if (l == len && len == prev_len) continue;  // duplicate string
-            }
-            prev = s;
-            prev_len = len;
-            ++h->K_unique;
-            if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
-            // blob segment: one pad byte standing for the root, the string, T
-            h->blob.push_back(0);
-            h->node_at.push_back(root);
-            for (int64_t i = 0; i <= len; ++i) {
-                const uint8_t c = i < len ? s[i] : term;
-                h->blob.push_back(c);
-                int32_t id;
-                if (i < l) {
-                    id = path[(size_t)i];
-                } else {
-                    id = (int32_t)N++;
-                    h->parent.push_back(i == 0 ? root : path[(size_t)(i - 1)]);
-                    h->depth.push_back((int32_t)(i + 1));
-                    h->edge.push_back(c);
-                    h->is_final.push_back(i == len ? 1 : 0);
-                    h->node_pos.push_back((int32_t)(h->blob.size() - 1));
-                }
-                path[(size_t)i] = id;
-                h->node_at.push_back(id);
-            }
-            if (N >= INT32_MAX || (int64_t)h->blob.size() >= INT32_MAX) {
-                *err = "trie exceeds 2^31-1 nodes or string bytes";
-                return TAM_E_TOOLARGE;
-            }
+    std::vector<SetTrie> sets((size_t)S);
+    std::atomic<bool> oom{false};
+    parallel_for(S, host_threads(S), [&](int64_t j) {
+        try {
+            build_one_set(sb, so, set_off[j], set_off[j + 1], term, sets[(size_t)j]);
+        } catch (const std::bad_alloc &) {
+            oom = true;
         }
+    });
+    if (oom) throw std::bad_alloc();
+    std::vector<int64_t> nbase((size_t)S + 1, 0), bbase((size_t)S + 1, kBlobPad), ebase((size_t)S + 1, 0);
+    h->K_unique = 0;
+    for (int64_t j = 0; j < S; ++j) {
+        const SetTrie &r = sets[(size_t)j];
+        if (r.st != TAM_OK) {
+            *err = r.err;
+            return r.st;
+        }
+        nbase[(size_t)j + 1] = nbase[(size_t)j] + (int64_t)r.parent.size();
+        bbase[(size_t)j + 1] = bbase[(size_t)j] + (int64_t)r.blob.size();
+        ebase[(size_t)j + 1] = ebase[(size_t)j] + (int64_t)r.child_node.size();
+        h->K_unique += r.K_unique;
     }
-    // zero pad behind, so that aligned window loads stay inside the blob
-    h->blob.insert(h->blob.end(), (size_t)kBlobPad, 0);
-    h->node_at.insert(h->node_at.end(), (size_t)kBlobPad, 0);
+    const int64_t N = nbase[(size_t)S];
+    const int64_t BB = bbase[(size_t)S] + kBlobPad;
+    const int64_t E = ebase[(size_t)S];
+    if (N >= INT32_MAX || BB >= INT32_MAX) {
+        *err = "trie exceeds 2^31-1 nodes or string bytes";
+        return TAM_E_TOOLARGE;
+    }
     h->N = N;
     h->S = S;
-    h->blob_bytes = (int64_t)h->blob.size();
-
-    // children of every node, ascending bytes = ascending ids (preorder)
-    h->child_off.assign((size_t)(N + 1), 0);
-    for (int64_t m = 0; m < N; ++m)
-        if (h->parent[(size_t)m] >= 0) ++h->child_off[(size_t)h->parent[(size_t)m] + 1];
-    for (int64_t n = 0; n < N; ++n) h->child_off[(size_t)n + 1] += h->child_off[(size_t)n];
-    const int64_t E = h->child_off[(size_t)N];
+    h->blob_bytes = BB;
+    h->roots.resize((size_t)S);
+    h->parent.resize((size_t)N);
+    h->depth.resize((size_t)N);
+    h->edge.resize((size_t)N);
+    h->is_final.resize((size_t)N);
+    h->node_pos.resize((size_t)N);
+    h->child_off.resize((size_t)N + 1);
     h->child_node.assign((size_t)std::max<int64_t>(E, 1), 0);
     h->child_byte.assign((size_t)std::max<int64_t>(E, 1), 0);
-    std::vector<int32_t> fill(h->child_off.begin(), h->child_off.end() - 1);
-    for (int64_t m = 0; m < N; ++m) {
-        const int32_t p = h->parent[(size_t)m];
-        if (p < 0) continue;
-        const int32_t at = fill[(size_t)p]++;
-        h->child_node[(size_t)at] = (int32_t)m;
-        h->child_byte[(size_t)at] = h->edge[(size_t)m];
-    }
+    h->blob.assign((size_t)BB, 0);
+    h->node_at.assign((size_t)BB, 0);
+    parallel_for(S, host_threads(S), [&](int64_t j) {
+        const SetTrie &r = sets[(size_t)j];
+        const int32_t nb = (int32_t)nbase[(size_t)j], bb = (int32_t)bbase[(size_t)j], eb = (int32_t)ebase[(size_t)j];
+        const size_t n = r.parent.size();
+        h->roots[(size_t)j] = nb;
+        for (size_t i = 0; i < n; ++i) {
+            h->parent[nb + i] = r.parent[i] < 0 ? -1 : r.parent[i] + nb;
+            h->node_pos[nb + i] = r.node_pos[i] < 0 ? -1 : r.node_pos[i] + bb;
+            h->child_off[nb + i] = r.child_off[i] + eb;
+        }
+        std::copy(r.depth.begin(), r.depth.end(), h->depth.begin() + nb);
+        std::copy(r.edge.begin(), r.edge.end(), h->edge.begin() + nb);
+        std::copy(r.is_final.begin(), r.is_final.end(), h->is_final.begin() + nb);
+        std::copy(r.blob.begin(), r.blob.end(), h->blob.begin() + bb);
+        for (size_t i = 0; i < r.node_at.size(); ++i) h->node_at[bb + i] = r.node_at[i] + nb;
+        for (size_t i = 0; i < r.child_node.size(); ++i) h->child_node[eb + i] = r.child_node[i] + nb;
+        std::copy(r.child_byte.begin(), r.child_byte.end(), h->child_byte.begin() + eb);
+    });
+    h->child_off[(size_t)N] = (int32_t)E;
     return TAM_OK;
 }
 
 /*
  * Vocabulary tables (the paper's vocabulary decoding and its per-tokenizer
  * matcher, built here as an exact hash of every distinct token string keyed by
- * its bytes read last-to-first).  Slots live in buckets of kBucket 32-bit
+ * its bytes read last-to-first).  Slots live in buckets of kBucket 16-bit
  * fingerprints; a key starts at its home bucket and moves to the next bucket
  * only when the bucket is full.  Duplicate strings share a slot and chain their
  * ids in ascending order.
@@ -189,9 +263,8 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     uint64_t cap = 64;
     while (cap < (uint64_t)(2 * V)) cap <<= 1;
     const uint64_t nbuckets = cap / kBucket;
-    h->fps.assign(cap, 0u);
-    h->srev.assign(cap, SlotRev{0, 0});
-    h->smeta.assign(cap, SlotMeta{-1, 0, 0});
+    h->fps.assign(cap, (uint16_t)0);
+    h->pay.assign(cap, SlotPay{0, 0, -1, 0, 0, {0, 0}});
     h->dup_next.assign((size_t)V, -1);
     std::vector<int32_t> last(cap, -1);
     const uint8_t *blob = h->tok_blob.data();
@@ -204,7 +277,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
         uint64_t hh = kHashSeed;
         for (int64_t i = (int64_t)len - 1; i >= 0; --i) hh = hash_step(hh, blob[off + i]);
         const uint64_t key = hash_final(hh, len);
-        const uint32_t fp = fingerprint(key);
+        const uint16_t fp = (uint16_t)fingerprint(key);
         uint64_t b = (key & (cap - 1)) / kBucket;
         bool placed = false;
         while (!placed) {
@@ -212,7 +285,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
                 const uint64_t s = b * kBucket + (uint64_t)i;
                 if (h->fps[s] == 0) {
                     h->fps[s] = fp;
-                    SlotRev r{0, 0};
+                    SlotPay r{0, 0, (int32_t)v, (uint16_t)len, 1, {0, 0}};
                     for (uint32_t k = 0; k < len && k < 16; ++k) {
                         const uint64_t c = blob[off + len - 1 - k];
                         if (k < 8)
@@ -220,20 +293,19 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
                         else
                             r.hi |= c << (8 * (k - 8));
                     }
-                    h->srev[s] = r;
-                    h->smeta[s] = SlotMeta{(int32_t)v, (uint16_t)len, 1};
+                    h->pay[s] = r;
                     last[s] = (int32_t)v;
                     placed = true;
-                } else if (h->fps[s] == fp && h->smeta[s].len == len) {
-                    const uint32_t o2 = h->tok_off[(size_t)h->smeta[s].first];
+                } else if (h->fps[s] == fp && h->pay[s].len == len) {
+                    const uint32_t o2 = h->tok_off[(size_t)h->pay[s].first];
                     if (std::memcmp(blob + o2, blob + off, len) == 0) {
-                        if (h->smeta[s].count == 65535) {
+                        if (h->pay[s].count == 65535) {
                             *err = "more than 65535 tokens share one byte string";
                             return TAM_E_TOOLARGE;
                         }
                         h->dup_next[(size_t)last[s]] = (int32_t)v;
                         last[s] = (int32_t)v;
-                        ++h->smeta[s].count;
+                        ++h->pay[s].count;
                         placed = true;
                     }
                 }
@@ -253,7 +325,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     const int64_t L = v->max_tok_len;
     std::vector<int64_t> dup(L + 1, 0);
-    for (const SlotMeta &s : v->smeta) {
+    for (const SlotPay &s : v->pay) {
         if (s.first < 0) continue;
         dup[(size_t)s.len] = std::max<int64_t>(dup[(size_t)s.len], s.count);
     }

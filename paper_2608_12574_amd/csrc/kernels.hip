@@ -1,19 +1,19 @@
 // HIP kernels of libtam for gfx950 (CDNA4, wave64).
 //
 // Mask compile (Section 4.1, valid[n] for every trie node n):
-//   k_count  -- one lane per non-root node m: the last d <= min(depth(m), ℓ)
+//   k_probe  -- one lane per non-root node m: the last d <= min(depth(m), ℓ)
 //               bytes of prefix(m) are hashed (read backwards from a 16-byte
 //               register window) and looked up in the vocabulary table; a hit of
 //               token t at d = |t| means t is valid at the ancestor d levels up,
 //               because t's walk from there ends at m.  This is the paper's
 //               crediting of a match to the node |t| bytes back (Section 4.2),
-//               done for all nodes at once instead of along a DFS.  Counts per
-//               ancestor; keeps the hit slots for the fill pass.
+//               done for all nodes at once instead of along a DFS.  Keeps the
+//               hits for the passes below; for lists it also counts per node.
 //   k_scan_* -- exclusive prefix sum of the counts into row offsets.
 //   k_fill   -- writes the hits' token ids into the per-node lists.
 //   k_zero   -- zero fill of the dense table (pure streaming stores).
-//   k_mark   -- the same probes as k_count, each hit OR-ed into the table with
-//               a 64-bit atomic (dense tables need no lists).
+//   k_mark   -- the hits of k_probe, each OR-ed into the table with a 64-bit
+//               atomic (dense tables need no lists).
 //   k_rows   -- one wave per row builds rows in registers from the lists
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
@@ -84,7 +84,7 @@ __device__ __forceinline__ bool has_len(const DevTables &t, int d) {
 }
 
 // The first min(d, 16) reversed bytes of the suffix equal the slot's.
-__device__ __forceinline__ bool same_head(uint64_t lo, uint64_t hi, const SlotRev &r, int d) {
+__device__ __forceinline__ bool same_head(uint64_t lo, uint64_t hi, const SlotPay &r, int d) {
     if (d >= 16) return lo == r.lo && hi == r.hi;
     if (d >= 8) {
         const uint64_t m = d == 8 ? 0ull : (~0ull >> (64 - 8 * (d - 8)));
@@ -93,35 +93,55 @@ __device__ __forceinline__ bool same_head(uint64_t lo, uint64_t hi, const SlotRe
     return (lo & (~0ull >> (64 - 8 * d))) == r.lo && r.hi == 0ull;
 }
 
+// The 16 fingerprints of the bucket holding `key` first (32 bytes, two loads).
+struct Bucket {
+    u32x4 a, b;
+};
+
+__device__ __forceinline__ uint64_t home_bucket(const DevTables &t, uint64_t key) {
+    return (key & t.slot_mask) / kBucket;
+}
+
+__device__ __forceinline__ Bucket load_bucket(const DevTables &t, uint64_t b) {
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(t.fps + b * kBucket);
+    return Bucket{q[0], q[1]};
+}
+
+// Bit i of *match: slot i holds fingerprint fp; bit i of *empty: slot i is empty.
+__device__ __forceinline__ void bucket_masks(const Bucket &bk, uint32_t fp, uint32_t *match, uint32_t *empty) {
+    const uint32_t w[8] = {bk.a.x, bk.a.y, bk.a.z, bk.a.w, bk.b.x, bk.b.y, bk.b.z, bk.b.w};
+    uint32_t mm = 0, ee = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint32_t lo16 = w[i] & 0xffffu, hi16 = w[i] >> 16;
+        mm |= ((lo16 == fp ? 1u : 0u) | (hi16 == fp ? 2u : 0u)) << (2 * i);
+        ee |= ((lo16 == 0u ? 1u : 0u) | (hi16 == 0u ? 2u : 0u)) << (2 * i);
+    }
+    *match = mm;
+    *empty = ee;
+}
+
 // Slot whose token equals the suffix of length d ending at blob[pos] (key =
-// its hash, (lo, hi) = its reversed window), or -1; its payload goes to *meta.
+// its hash, (lo, hi) = its reversed window), or -1; its payload goes to *pay.
 // Buckets are scanned from the key's home bucket until one with an empty slot
-// (load <= 1/2 guarantees one exists).  The 16 fingerprints of a bucket are
-// compared into a bit mask first, so a wave reads the payload of its matching
-// lanes in one step instead of one divergent branch per slot position.
+// (load <= 1/2 guarantees one exists): a key sits in a later bucket only if
+// every bucket before it was full when it was inserted.  The fingerprints of a
+// bucket are compared into a bit mask first, so a wave reads the payload of its
+// matching lanes in one step instead of one divergent branch per slot.
 __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d, uint64_t lo, uint64_t hi,
-                                         int64_t pos, SlotMeta *meta) {
+                                         int64_t pos, SlotPay *pay) {
     const uint32_t fp = fingerprint(key);
     const uint64_t bmask = t.slot_mask / kBucket;
-    uint64_t b = (key & t.slot_mask) / kBucket;
+    uint64_t b = home_bucket(t, key);
     for (;;) {
-        const u32x4 *q = reinterpret_cast<const u32x4 *>(t.fps + b * kBucket);
-        const u32x4 f0 = q[0], f1 = q[1], f2 = q[2], f3 = q[3];
-        const uint32_t f[kBucket] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w,
-                                     f2.x, f2.y, f2.z, f2.w, f3.x, f3.y, f3.z, f3.w};
-        uint32_t match = 0, empty = 0;
-#pragma unroll
-        for (int i = 0; i < kBucket; ++i) {
-            match |= (f[i] == fp ? 1u : 0u) << i;
-            empty |= (f[i] == 0u ? 1u : 0u) << i;
-        }
+        uint32_t match, empty;
+        bucket_masks(load_bucket(t, b), fp, &match, &empty);
         while (match) {
             const int i = __builtin_ctz(match);
             match &= match - 1;
             const int32_t s = (int32_t)(b * kBucket + (uint64_t)i);
-            const SlotMeta m = t.smeta[s];
-            const SlotRev r = t.srev[s];
-            if ((int)m.len == d && same_head(lo, hi, r, d)) {
+            const SlotPay m = t.pay[s];
+            if ((int)m.len == d && same_head(lo, hi, m, d)) {
                 bool eq = true;
                 if (d > kWin) {  // bytes beyond the window: compare in memory
                     const uint8_t *tb = t.tok_blob + t.tok_off[m.first];
@@ -129,7 +149,7 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
                     for (int k = 0; k < d - kWin && eq; ++k) eq = tb[k] == pb[k];
                 }
                 if (eq) {
-                    *meta = m;
+                    *pay = m;
                     return s;
                 }
             }
@@ -139,9 +159,74 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
     }
 }
 
-// Writes the token ids of slot s into the list of node n.
-__device__ __forceinline__ void emit(const DevTables &t, int32_t s, int32_t n) {
-    const SlotMeta m = t.smeta[s];
+// The hits (hit_of_slot, or -1) of the suffixes of length d <= Lw <= 16 of a
+// node's path, four lengths at a time: their bucket loads are issued together,
+// then their payload loads, so a node waits for about eight memory round trips
+// instead of sixteen dependent ones.  A length whose home bucket does not settle
+// it (a full bucket, or a second fingerprint match after a failed first) falls
+// back to the general probe.
+__device__ __forceinline__ void probe_window(const DevTables &t, int64_t pos, int Lw, uint64_t lo, uint64_t hi,
+                                             int32_t (&hit)[kWin]) {
+    uint64_t h = kHashSeed;
+#pragma unroll
+    for (int g = 0; g < kWin; g += 4) {
+        uint64_t key[4];
+        bool act[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int d = g + j + 1;
+            hit[d - 1] = -1;
+            act[j] = false;
+            key[j] = 0;
+            if (d <= Lw) {
+                h = hash_step(h, window_byte(lo, hi, d - 1));
+                act[j] = has_len(t, d);
+                key[j] = hash_final(h, (uint32_t)d);
+            }
+        }
+        Bucket bk[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (act[j]) bk[j] = load_bucket(t, home_bucket(t, key[j]));
+        uint32_t match[4], empty[4];
+        int32_t slot[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            match[j] = empty[j] = 0;
+            slot[j] = -1;
+            if (act[j]) {
+                bucket_masks(bk[j], fingerprint(key[j]), &match[j], &empty[j]);
+                if (match[j]) slot[j] = (int32_t)(home_bucket(t, key[j]) * kBucket + (uint64_t)__builtin_ctz(match[j]));
+            }
+        }
+        SlotPay p[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (slot[j] >= 0) p[j] = t.pay[slot[j]];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int d = g + j + 1;
+            if (!act[j]) continue;
+            if (slot[j] >= 0 && (int)p[j].len == d && same_head(lo, hi, p[j], d)) {
+                hit[d - 1] = hit_of_slot(slot[j], p[j].first, p[j].count);
+            } else if (empty[j] != 0 && (match[j] & (match[j] - 1)) == 0) {
+                hit[d - 1] = -1;  // the home bucket settles it: no such token
+            } else {
+                SlotPay mt;
+                const int32_t sl = probe(t, key[j], d, lo, hi, pos, &mt);
+                if (sl >= 0) hit[d - 1] = hit_of_slot(sl, mt.first, mt.count);
+            }
+        }
+    }
+}
+
+// Writes the token ids of hit x (see hit_of_slot) into the list of node n.
+__device__ __forceinline__ void emit(const DevTables &t, int32_t x, int32_t n) {
+    if (x >= 0) {
+        t.entries[t.row_ptr[n] + atomicAdd(&t.cursor[n], 1)] = x;
+        return;
+    }
+    const SlotPay m = t.pay[-2 - x];
     const int32_t at = t.row_ptr[n] + atomicAdd(&t.cursor[n], (int32_t)m.count);
     int32_t v = m.first;
     for (int k = 0; k < (int)m.count; ++k) {
@@ -150,39 +235,12 @@ __device__ __forceinline__ void emit(const DevTables &t, int32_t s, int32_t n) {
     }
 }
 
-// Probe pass: one lane per node m.  The suffix of length d of prefix(m) equal to
-// token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
-// d <= 16 the hit slot (or -1) goes to hits[d-1][m]; the slots are kept in
-// registers and stored after the last probe, so no probe load waits behind a
-// store (loads and stores share one vector-memory counter here).  Longer tokens
-// are handled by the consumers, which probe those lengths again.
-__global__ void __launch_bounds__(kBlock) k_probe(DevTables t) {
-    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (m >= t.N) return;
-    const int64_t pos = t.node_pos[m];
-    if (pos < 0) return;  // a root ends no token
-    const int Lw = min(min(t.depth[m], t.max_len), kWin);
-    uint64_t lo, hi;
-    load_window(t.blob, pos, lo, hi);
-    uint64_t h = kHashSeed;
-    int32_t slot[kWin];
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d) {
-        slot[d - 1] = -1;
-        if (d <= Lw) {
-            h = hash_step(h, window_byte(lo, hi, d - 1));
-            if (has_len(t, d)) {
-                SlotMeta mt;
-                slot[d - 1] = probe(t, hash_final(h, (uint32_t)d), d, lo, hi, pos, &mt);
-            }
-        }
-    }
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d)
-        if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = slot[d - 1];
+// Number of token ids of hit x.
+__device__ __forceinline__ int32_t hit_count(const DevTables &t, int32_t x) {
+    return x >= 0 ? 1 : (x == -1 ? 0 : (int32_t)t.pay[-2 - x].count);
 }
 
-// Calls f(slot, d) for every token string ending at node m longer than the
+// Calls f(hit, d) for every token string ending at node m longer than the
 // window (d > 16), probing those lengths again (vocabularies rarely have them).
 template <typename F>
 __device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L, F &&f) {
@@ -193,39 +251,51 @@ __device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L
     for (int d = kWin + 1; d <= L; ++d) {
         h = hash_step(h, t.blob[pos - d + 1]);
         if (!has_len(t, d)) continue;
-        SlotMeta mt;
+        SlotPay mt;
         const int32_t s = probe(t, hash_final(h, (uint32_t)d), d, lo, hi, pos, &mt);
-        if (s >= 0) f(s, d);
+        if (s >= 0) f(hit_of_slot(s, mt.first, mt.count), d);
     }
 }
 
-// Count pass (lists): per-node numbers of valid token ids.
-__global__ void __launch_bounds__(kBlock) k_count(DevTables t) {
+// Probe pass: one lane per node m.  The suffix of length d of prefix(m) equal to
+// token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
+// d <= 16 the hit (hit_of_slot: the token id, or the slot of a string with
+// several ids, or -1) goes to hits[d-1][m]; the hits are kept in registers and
+// stored after the last probe, so no probe load waits behind a store (loads and
+// stores share one vector-memory counter here).  Longer tokens are handled by
+// the consumers, which probe those lengths again.  kCount (sparse lists): the
+// lane then adds its hits to the per-node counts, after all its loads.
+template <bool kCount>
+__global__ void __launch_bounds__(kBlock) k_probe(DevTables t) {
     const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (m >= t.N) return;
     const int64_t pos = t.node_pos[m];
-    if (pos < 0) return;
+    if (pos < 0) return;  // a root ends no token
     const int L = min(t.depth[m], t.max_len);
     const int Lw = min(L, kWin);
-    int32_t s[kWin], n[kWin], c[kWin];
+    uint64_t lo, hi;
+    load_window(t.blob, pos, lo, hi);
+    int32_t hit[kWin];
+    probe_window(t, pos, Lw, lo, hi, hit);
+    int32_t n[kWin];
+    if (kCount) {
 #pragma unroll
-    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d) {
-        n[d - 1] = 0;
-        c[d - 1] = 0;
-        if (s[d - 1] >= 0) {
-            n[d - 1] = t.node_at[pos - d];
-            c[d - 1] = t.smeta[s[d - 1]].count;
-        }
+        for (int d = 1; d <= kWin; ++d) n[d - 1] = hit[d - 1] != -1 ? t.node_at[pos - d] : 0;
     }
 #pragma unroll
     for (int d = 1; d <= kWin; ++d)
-        if (c[d - 1] > 0) atomicAdd(&t.count[n[d - 1]], c[d - 1]);
-    if (L > kWin)
-        long_hits(t, pos, L, [&](int32_t sl, int d) {
-            atomicAdd(&t.count[t.node_at[pos - d]], (int32_t)t.smeta[sl].count);
-        });
+        if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = hit[d - 1];
+    if (kCount) {
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d)
+            if (hit[d - 1] >= 0) atomicAdd(&t.count[n[d - 1]], 1);
+        // strings with several token ids and tokens longer than the window (both rare)
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d)
+            if (hit[d - 1] <= -2) atomicAdd(&t.count[n[d - 1]], (int32_t)t.pay[-2 - hit[d - 1]].count);
+        if (L > kWin)
+            long_hits(t, pos, L, [&](int32_t hx, int d) { atomicAdd(&t.count[t.node_at[pos - d]], hit_count(t, hx)); });
+    }
 }
 
 // Fill pass (lists): the hits' token ids written into the per-node lists.
@@ -241,8 +311,8 @@ __global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
     for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
 #pragma unroll
     for (int d = 1; d <= kWin; ++d)
-        if (s[d - 1] >= 0) emit(t, s[d - 1], t.node_at[pos - d]);
-    if (L > kWin) long_hits(t, pos, L, [&](int32_t sl, int d) { emit(t, sl, t.node_at[pos - d]); });
+        if (s[d - 1] != -1) emit(t, s[d - 1], t.node_at[pos - d]);
+    if (L > kWin) long_hits(t, pos, L, [&](int32_t hx, int d) { emit(t, hx, t.node_at[pos - d]); });
 }
 
 // Mark pass (dense table): every hit OR-ed into the zeroed table with a 64-bit
@@ -256,46 +326,43 @@ __global__ void __launch_bounds__(kBlock) k_mark(DevTables t, int32_t *__restric
         const int L = min(t.depth[m], t.max_len);
         const int Lw = min(L, kWin);
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
-        int32_t s[kWin], n[kWin], v[kWin];
+        int32_t x[kWin], n[kWin];
         uint32_t multi = 0;
 #pragma unroll
-        for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+        for (int d = 1; d <= kWin; ++d) x[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
 #pragma unroll
         for (int d = 1; d <= kWin; ++d) {
-            n[d - 1] = 0;
-            v[d - 1] = -1;
-            if (s[d - 1] >= 0) {
-                const SlotMeta mt = t.smeta[s[d - 1]];
-                n[d - 1] = t.node_at[pos - d];
-                v[d - 1] = mt.first;
-                if (mt.count > 1) multi |= 1u << (d - 1);
-            }
+            n[d - 1] = x[d - 1] != -1 ? t.node_at[pos - d] : 0;
+            if (x[d - 1] <= -2) multi |= 1u << (d - 1);
         }
 #pragma unroll
         for (int d = 1; d <= kWin; ++d) {
-            if (v[d - 1] >= 0) {
-                atomicOr(table + (int64_t)n[d - 1] * t.Wp + (v[d - 1] >> 6), 1ull << (v[d - 1] & 63));
+            if (x[d - 1] >= 0) {
+                atomicOr(table + (int64_t)n[d - 1] * t.Wp + (x[d - 1] >> 6), 1ull << (x[d - 1] & 63));
                 ++found;
             }
         }
-        // duplicate token strings and tokens longer than the window (both rare)
-        auto mark_slot = [&](int32_t sl, int32_t node, bool skip_first) {
-            const SlotMeta mt = t.smeta[sl];
+        // strings with several token ids and tokens longer than the window (both rare)
+        auto mark_hit = [&](int32_t hx, int32_t node) {
             unsigned long long *row = table + (int64_t)node * t.Wp;
-            int32_t x = mt.first;
-            for (int k = 0; k < (int)mt.count; ++k) {
-                if (k > 0 || !skip_first) {
-                    atomicOr(row + (x >> 6), 1ull << (x & 63));
-                    ++found;
-                }
-                x = t.dup_next[x];
+            if (hx >= 0) {
+                atomicOr(row + (hx >> 6), 1ull << (hx & 63));
+                ++found;
+                return;
             }
+            const SlotPay mt = t.pay[-2 - hx];
+            int32_t v = mt.first;
+            for (int k = 0; k < (int)mt.count; ++k) {
+                atomicOr(row + (v >> 6), 1ull << (v & 63));
+                v = t.dup_next[v];
+            }
+            found += mt.count;
         };
         for (uint32_t mm = multi; mm; mm &= mm - 1) {
             const int d = __builtin_ctz(mm) + 1;
-            mark_slot(t.hits[(int64_t)(d - 1) * t.N + m], t.node_at[pos - d], true);
+            mark_hit(t.hits[(int64_t)(d - 1) * t.N + m], n[d - 1]);
         }
-        if (L > kWin) long_hits(t, pos, L, [&](int32_t sl, int d) { mark_slot(sl, t.node_at[pos - d], false); });
+        if (L > kWin) long_hits(t, pos, L, [&](int32_t hx, int d) { mark_hit(hx, t.node_at[pos - d]); });
     }
     // block sum of found
     __shared__ int32_t wsum[kBlock / kWave];
@@ -512,21 +579,37 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
 
     uint32_t bits[kApplyUnits];
     if (kSparse) {
-        for (int i = threadIdx.x; i < kSpan / 32; i += kBlock) bm[i] = 0;
-        __syncthreads();
-        if (live) {
-            const int32_t e0 = t.row_ptr[n], e1 = t.row_ptr[n + 1];
-            const uint32_t lo = (uint32_t)(c0 * E);
+#pragma unroll
+        for (int u = 0; u < kApplyUnits; ++u) bits[u] = 0;
+        const int32_t e0 = live ? t.row_ptr[n] : 0, e1 = live ? t.row_ptr[n + 1] : 0;
+        const uint32_t lo = (uint32_t)(c0 * E);
+        if (e1 - e0 <= kWave) {
+            // short list (block-uniform branch): every wave reads the ids into its
+            // lanes and each thread picks the bits of its own chunks
+            const int lane = threadIdx.x & (kWave - 1);
+            const int32_t mine = e0 + lane < e1 ? t.entries[e0 + lane] : 0;
+            for (int j = 0; j < e1 - e0; ++j) {
+                const uint32_t r = (uint32_t)__builtin_amdgcn_readlane(mine, j) - lo;
+                if (r >= (uint32_t)kSpan) continue;
+                const uint32_t lc = r / E;
+#pragma unroll
+                for (int u = 0; u < kApplyUnits; ++u)
+                    if (lc == (uint32_t)(u * kBlock + threadIdx.x)) bits[u] |= 1u << (r % E);
+            }
+        } else {
+            // long list: scatter through an LDS bitmap of the block's span
+            for (int i = threadIdx.x; i < kSpan / 32; i += kBlock) bm[i] = 0;
+            __syncthreads();
             for (int32_t k = e0 + (int32_t)threadIdx.x; k < e1; k += kBlock) {
                 const uint32_t v = (uint32_t)t.entries[k] - lo;
                 if (v < (uint32_t)kSpan) atomicOr(&bm[v >> 5], 1u << (v & 31));
             }
-        }
-        __syncthreads();
+            __syncthreads();
 #pragma unroll
-        for (int u = 0; u < kApplyUnits; ++u) {
-            const uint32_t bit = (uint32_t)((u * kBlock + threadIdx.x) * E);
-            bits[u] = (bm[bit >> 5] >> (bit & 31)) & FULL;
+            for (int u = 0; u < kApplyUnits; ++u) {
+                const uint32_t bit = (uint32_t)((u * kBlock + threadIdx.x) * E);
+                bits[u] = (bm[bit >> 5] >> (bit & 31)) & FULL;
+            }
         }
     } else {
         const uint8_t *mrow = reinterpret_cast<const uint8_t *>(t.table + (live ? (int64_t)n * t.Wp : 0));
@@ -631,15 +714,12 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s) 
     return hipGetLastError();
 }
 
-hipError_t launch_probe(const DevTables &t, hipStream_t s) {
+hipError_t launch_probe(const DevTables &t, bool count, hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_probe, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
-    return hipGetLastError();
-}
-
-hipError_t launch_count(const DevTables &t, hipStream_t s) {
-    if (t.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_count, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+    if (count)
+        hipLaunchKernelGGL(k_probe<true>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+    else
+        hipLaunchKernelGGL(k_probe<false>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
     return hipGetLastError();
 }
 

@@ -124,9 +124,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     Arena a;
     const size_t o_off = a.take<uint32_t>(V + 1);
     const size_t o_blob = a.take<uint8_t>((int64_t)v->tok_blob.size());
-    const size_t o_fps = a.take<uint32_t>((int64_t)v->fps.size());
-    const size_t o_srev = a.take<tam::SlotRev>((int64_t)v->srev.size());
-    const size_t o_smeta = a.take<tam::SlotMeta>((int64_t)v->smeta.size());
+    const size_t o_fps = a.take<uint16_t>((int64_t)v->fps.size());
+    const size_t o_pay = a.take<tam::SlotPay>((int64_t)v->pay.size());
     const size_t o_dup = a.take<int32_t>(V);
     const size_t o_len = a.take<uint8_t>((int64_t)v->len_present.size());
     uint8_t *base = static_cast<uint8_t *>(alloc_with(v->own_alloc, v->alloc, a.used));
@@ -138,9 +137,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     v->device_bytes = (int64_t)a.used;
     v->d_tok_off = reinterpret_cast<const uint32_t *>(base + o_off);
     v->d_tok_blob = base + o_blob;
-    v->d_fps = reinterpret_cast<const uint32_t *>(base + o_fps);
-    v->d_srev = reinterpret_cast<const tam::SlotRev *>(base + o_srev);
-    v->d_smeta = reinterpret_cast<const tam::SlotMeta *>(base + o_smeta);
+    v->d_fps = reinterpret_cast<const uint16_t *>(base + o_fps);
+    v->d_pay = reinterpret_cast<const tam::SlotPay *>(base + o_pay);
     v->d_dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
     v->d_len_present = base + o_len;
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
@@ -149,9 +147,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     };
     hipError_t e = up(o_off, v->tok_off.data(), v->tok_off.size() * 4);
     if (e == hipSuccess) e = up(o_blob, v->tok_blob.data(), v->tok_blob.size());
-    if (e == hipSuccess) e = up(o_fps, v->fps.data(), v->fps.size() * sizeof(uint32_t));
-    if (e == hipSuccess) e = up(o_srev, v->srev.data(), v->srev.size() * sizeof(tam::SlotRev));
-    if (e == hipSuccess) e = up(o_smeta, v->smeta.data(), v->smeta.size() * sizeof(tam::SlotMeta));
+    if (e == hipSuccess) e = up(o_fps, v->fps.data(), v->fps.size() * sizeof(uint16_t));
+    if (e == hipSuccess) e = up(o_pay, v->pay.data(), v->pay.size() * sizeof(tam::SlotPay));
     if (e == hipSuccess) e = up(o_dup, v->dup_next.data(), v->dup_next.size() * 4);
     if (e == hipSuccess) e = up(o_len, v->len_present.data(), v->len_present.size());
     if (e == hipSuccess) e = hipEventCreateWithFlags(&v->ready, hipEventDisableTiming);
@@ -203,7 +200,7 @@ unsigned default_phases(const tam_handle *h) {
     return h->dt.table ? unsigned(TAM_PHASE_TABLE) : unsigned(TAM_PHASE_LISTS);
 }
 
-// The device part of compile.  Lists: probes, counts per node, prefix sum,
+// The device part of compile.  Lists: probes counting per node, prefix sum,
 // fill.  Table: zero fill with the probes beside it on the side stream, then
 // the marks.  Phase events are recorded only for the handle's default phases.
 tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
@@ -212,8 +209,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
     if (phases & TAM_PHASE_LISTS) {
         TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
-        TAM_HIP(tam::launch_probe(t, s));
-        TAM_HIP(tam::launch_count(t, s));
+        TAM_HIP(tam::launch_probe(t, true, s));
         TAM_HIP(tam::launch_scan(t, s));
         TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
         TAM_HIP(tam::launch_fill_lists(t, s));
@@ -226,7 +222,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     if (overlap) {
         TAM_HIP(hipEventRecord(h->fork, s));
         TAM_HIP(hipStreamWaitEvent(h->side, h->fork, 0));
-        TAM_HIP(tam::launch_probe(t, h->side));
+        TAM_HIP(tam::launch_probe(t, false, h->side));
         TAM_HIP(hipEventRecord(h->join, h->side));
     }
     if ((phases & TAM_PHASE_ZERO) && t.table) TAM_HIP(tam::launch_zero(t.table, t.N * t.Wp, s));
@@ -235,7 +231,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
         if (overlap)
             TAM_HIP(hipStreamWaitEvent(s, h->join, 0));
         else
-            TAM_HIP(tam::launch_probe(t, s));
+            TAM_HIP(tam::launch_probe(t, false, s));
         TAM_HIP(tam::launch_mark(t, h->pairs, s));
     }
     if (timing) {
@@ -367,8 +363,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.tok_off = vocab->d_tok_off;
     t.tok_blob = vocab->d_tok_blob;
     t.fps = vocab->d_fps;
-    t.srev = vocab->d_srev;
-    t.smeta = vocab->d_smeta;
+    t.pay = vocab->d_pay;
     t.dup_next = vocab->d_dup_next;
     t.len_present = vocab->d_len_present;
     t.hits = reinterpret_cast<int32_t *>(base + o_hits);

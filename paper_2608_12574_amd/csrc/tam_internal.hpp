@@ -32,27 +32,32 @@ __host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len
     return z | 1ull;  // 0 never occurs as a key
 }
 
-// Vocabulary table: open addressing over buckets of 16 32-bit fingerprints (one
-// 64-byte line per bucket), one slot per distinct non-empty token string.  A
-// slot's payload (its length, first id, duplicate count and its first 16 bytes
-// stored last byte first) is read only on a fingerprint match.
+// Vocabulary table: open addressing over buckets of 16 16-bit fingerprints (32
+// bytes per bucket), one slot per distinct non-empty token string.  A
+// slot's 32-byte payload (its first 16 bytes stored last byte first, its
+// smallest token id, length and duplicate count) is read only on a fingerprint
+// match, with one load.
 constexpr int kBucket = 16;   // fingerprints per bucket
 constexpr int kWin = 16;      // path bytes a probing node keeps in registers
 constexpr int kBlobPad = 16;  // zero bytes before and after the string blob
 
 __host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
-    return (uint32_t)(key >> 32) | 1u;  // 0 marks an empty slot
+    return (uint32_t)(key >> 48) | 1u;  // 16 bits; 0 marks an empty slot
 }
 
-struct alignas(16) SlotRev {
+struct alignas(32) SlotPay {
     uint64_t lo, hi;  // byte k = token byte len-1-k for k < min(len, 16), then zeros
-};
-
-struct alignas(8) SlotMeta {
-    int32_t first;    // smallest token id with this string
+    int32_t first;    // smallest token id with this string (-1: empty slot)
     uint16_t len;     // string length in bytes
     uint16_t count;   // number of token ids with this string
+    uint32_t pad[2];
 };
+
+// What the probe pass stores per (node, suffix length): the token id when the
+// string has one id, -2 - slot when it has several, -1 when no token matches.
+__host__ __device__ __forceinline__ int32_t hit_of_slot(int32_t slot, int32_t first, int count) {
+    return count == 1 ? first : -2 - slot;
+}
 
 // ---------------------------------------------------------------------------
 // Device-side view of a compiled handle (plain pointers, passed to kernels).
@@ -69,13 +74,12 @@ struct DevTables {
     // vocabulary (a2)
     const uint32_t *tok_off;    // [V+1]
     const uint8_t *tok_blob;
-    const uint32_t *fps;        // [slot_mask+1] fingerprints, kBucket per bucket
-    const SlotRev *srev;        // [slot_mask+1]
-    const SlotMeta *smeta;      // [slot_mask+1]
+    const uint16_t *fps;        // [slot_mask+1] fingerprints, kBucket per bucket
+    const SlotPay *pay;         // [slot_mask+1]
     const int32_t *dup_next;    // [V] next id with the same bytes, -1 at the end
     const uint8_t *len_present; // [max_len+1] 1 if some token has that length
     // valid lists (a4) and dense table
-    int32_t *hits;              // [kWin][N] slot hit by the suffix of length d+1 of node m, or -1
+    int32_t *hits;              // [kWin][N] hit_of_slot of the suffix of length d+1 of node m, or -1
     int32_t *count;             // [N]
     int32_t *row_ptr;           // [N+1]
     int32_t *cursor;            // [N]
@@ -91,8 +95,7 @@ struct DevTables {
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
-hipError_t launch_probe(const DevTables &t, hipStream_t s);
-hipError_t launch_count(const DevTables &t, hipStream_t s);
+hipError_t launch_probe(const DevTables &t, bool count, hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 hipError_t launch_mark(const DevTables &t, int32_t *pairs, hipStream_t s);
@@ -128,18 +131,16 @@ struct tam_vocab {
     // host tables
     std::vector<uint32_t> tok_off;
     std::vector<uint8_t> tok_blob, len_present;
-    std::vector<uint32_t> fps;
-    std::vector<tam::SlotRev> srev;
-    std::vector<tam::SlotMeta> smeta;
+    std::vector<uint16_t> fps;
+    std::vector<tam::SlotPay> pay;
     std::vector<int32_t> dup_next;
 
     // device copies (one arena)
     void *arena = nullptr;
     const uint32_t *d_tok_off = nullptr;
     const uint8_t *d_tok_blob = nullptr;
-    const uint32_t *d_fps = nullptr;
-    const tam::SlotRev *d_srev = nullptr;
-    const tam::SlotMeta *d_smeta = nullptr;
+    const uint16_t *d_fps = nullptr;
+    const tam::SlotPay *d_pay = nullptr;
     const int32_t *d_dup_next = nullptr;
     const uint8_t *d_len_present = nullptr;
     hipEvent_t ready = nullptr;  // recorded after the uploads
