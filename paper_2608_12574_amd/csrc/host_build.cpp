@@ -147,8 +147,8 @@ int host_threads(int64_t work_items) {
  * Tries of all sets: each set is built on its own (in parallel over host
  * threads for a forest), then the sets are laid out one after another: set j
  * takes node ids [roots[j], roots[j] + N_j) and its own range of the blob,
- * which carries 16 zero bytes in front and behind so that a node's 16-byte
- * path window never leaves it.
+ * which carries kBlobPad zero bytes in front and behind so that 16-byte
+ * window loads around any node never leave it.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err) {
@@ -248,7 +248,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     h->W = (V + 63) / 64;
     h->tok_off.resize((size_t)(V + 1));
     h->tok_blob.assign(tb ? tb + to[0] : nullptr, tb ? tb + to[V] : nullptr);
-    if (h->tok_blob.empty()) h->tok_blob.push_back(0);
+    h->tok_blob.insert(h->tok_blob.end(), (size_t)kBlobPad, 0);  // room for 16-byte window loads
     int64_t max_len = 0;
     for (int64_t v = 0; v <= V; ++v) h->tok_off[(size_t)v] = (uint32_t)(to[v] - to[0]);
     for (int64_t v = 0; v < V; ++v) max_len = std::max<int64_t>(max_len, to[v + 1] - to[v]);

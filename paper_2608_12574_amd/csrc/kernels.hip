@@ -654,6 +654,63 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
 
 // --------------------------------------------------------------- advance ---
 
+// 16 bytes base[pos .. pos+16) at any alignment (byte j of (lo, hi) = base[pos+j]),
+// from five aligned dword loads; reads up to 3 bytes before and 4 after.
+__device__ __forceinline__ void load16(const uint8_t *base, int64_t pos, uint64_t &lo, uint64_t &hi) {
+    const int64_t a = pos & ~int64_t(3);
+    const uint32_t *w = reinterpret_cast<const uint32_t *>(base + a);
+    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
+    const uint32_t sh = (uint32_t)(pos - a) * 8u;
+    const uint32_t x0 = (uint32_t)((((uint64_t)w1 << 32) | w0) >> sh);
+    const uint32_t x1 = (uint32_t)((((uint64_t)w2 << 32) | w1) >> sh);
+    const uint32_t x2 = (uint32_t)((((uint64_t)w3 << 32) | w2) >> sh);
+    const uint32_t x3 = (uint32_t)((((uint64_t)w4 << 32) | w3) >> sh);
+    lo = ((uint64_t)x1 << 32) | x0;
+    hi = ((uint64_t)x3 << 32) | x2;
+}
+
+// Index of the first byte of (lo, hi) equal to c (16 if none).
+__device__ __forceinline__ int first_byte(uint64_t lo, uint64_t hi, uint32_t c) {
+    const uint64_t ones = 0x0101010101010101ull, highs = 0x8080808080808080ull;
+    uint64_t y = lo ^ (ones * c);
+    uint64_t z = (y - ones) & ~y & highs;  // exact for the lowest zero byte
+    if (z) return __builtin_ctzll(z) >> 3;
+    y = hi ^ (ones * c);
+    z = (y - ones) & ~y & highs;
+    return z ? 8 + (__builtin_ctzll(z) >> 3) : 16;
+}
+
+// Number of equal leading bytes of two 16-byte values.
+__device__ __forceinline__ int common_prefix(uint64_t alo, uint64_t ahi, uint64_t blo, uint64_t bhi) {
+    uint64_t x = alo ^ blo;
+    if (x) return __builtin_ctzll(x) >> 3;
+    x = ahi ^ bhi;
+    return x ? 8 + (__builtin_ctzll(x) >> 3) : 16;
+}
+
+// Child of node n along byte c (binary search over its sorted child bytes), or dead.
+__device__ __forceinline__ int32_t child(const DevTables &t, int32_t n, uint32_t c) {
+    int32_t lo = t.child_off[n], hi = t.child_off[n + 1];
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        const uint32_t cb = t.child_byte[mid];
+        if (cb < c)
+            lo = mid + 1;
+        else if (cb > c)
+            hi = mid;
+        else
+            return t.child_node[mid];
+    }
+    return TAM_DEAD;
+}
+
+// The extended transition function over one token per lane.  After each child
+// step the walk follows the node's owner string (the first set string through
+// it, stored in the blob right after the node's edge byte), comparing up to 16
+// token bytes at a time and jumping to node_at of the last matching position;
+// the comparison never runs past that string's terminator.  A token needs one
+// child search per point where it leaves the owner string's path, usually one
+// or two, instead of one per byte.
 __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *nodes, const int32_t *toks,
                                                     int64_t B, int32_t *out) {
     const int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -662,27 +719,28 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
     const int32_t v = toks[b];
     int32_t n = TAM_DEAD;
     if (n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V) {
-        const uint32_t a = t.tok_off[v], e = t.tok_off[v + 1];
-        if (e > a) {
-            n = n0;
-            for (uint32_t i = a; i < e && n >= 0; ++i) {
-                const uint8_t c = t.tok_blob[i];
-                int32_t lo = t.child_off[n], hi = t.child_off[n + 1];
-                int32_t next = TAM_DEAD;
-                while (lo < hi) {
-                    const int32_t mid = (lo + hi) >> 1;
-                    const uint8_t cb = t.child_byte[mid];
-                    if (cb < c) {
-                        lo = mid + 1;
-                    } else if (cb > c) {
-                        hi = mid;
-                    } else {
-                        next = t.child_node[mid];
-                        break;
-                    }
-                }
-                n = next;
+        const int64_t a = t.tok_off[v];
+        const int len = (int)(t.tok_off[v + 1] - (uint32_t)a);
+        const uint32_t T = (uint32_t)t.terminator;
+        int i = 0;
+        n = len > 0 ? n0 : TAM_DEAD;
+        while (i < len && n >= 0) {
+            const uint32_t c = t.tok_blob[a + i];
+            n = child(t, n, c);
+            ++i;
+            if (n < 0 || i >= len || c == T) continue;  // dead, done, or at a final node
+            int64_t p = t.node_pos[n];
+            for (;;) {
+                uint64_t blo, bhi, tlo, thi;
+                load16(t.blob, p + 1, blo, bhi);
+                load16(t.tok_blob, a + i, tlo, thi);
+                const int cap = min(first_byte(blo, bhi, T) + 1, 16);  // up to and including T
+                const int k = min(min(common_prefix(tlo, thi, blo, bhi), len - i), cap);
+                p += k;
+                i += k;
+                if (k < 16 || i >= len) break;
             }
+            n = t.node_at[p];
         }
     }
     out[b] = n;

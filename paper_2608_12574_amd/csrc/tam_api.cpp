@@ -381,6 +381,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.slot_mask = (uint64_t)vocab->fps.size() - 1;
     t.len_mask = vocab->len_mask;
     t.max_len = (int32_t)vocab->max_tok_len;
+    t.terminator = h->terminator;
 
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
         if (bytes == 0) return hipSuccess;

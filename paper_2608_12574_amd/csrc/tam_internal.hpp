@@ -39,7 +39,7 @@ __host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len
 // match, with one load.
 constexpr int kBucket = 16;   // fingerprints per bucket
 constexpr int kWin = 16;      // path bytes a probing node keeps in registers
-constexpr int kBlobPad = 16;  // zero bytes before and after the string blob
+constexpr int kBlobPad = 32;  // zero bytes before and after the string blob (and after the token blob)
 
 __host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
     return (uint32_t)(key >> 48) | 1u;  // 16 bits; 0 marks an empty slot
@@ -64,7 +64,7 @@ __host__ __device__ __forceinline__ int32_t hit_of_slot(int32_t slot, int32_t fi
 // ---------------------------------------------------------------------------
 struct DevTables {
     // trie (a1)
-    const uint8_t *blob;        // [pad 16][per string: pad, bytes, T][pad 16]
+    const uint8_t *blob;        // [pad 32][per string: pad, bytes, T][pad 32]
     const int32_t *node_at;     // [blob_bytes] node whose edge byte is that blob byte (pad: root)
     const int32_t *node_pos;    // [N] blob offset of the node's edge byte (-1 at roots)
     const int32_t *depth;       // [N]
@@ -91,6 +91,7 @@ struct DevTables {
     uint64_t slot_mask;         // slots - 1 (slots = a power of two, >= kBucket)
     uint64_t len_mask;          // bit d (d < 64): some token has length d
     int32_t max_len;
+    int32_t terminator;
 };
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.

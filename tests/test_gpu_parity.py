@@ -264,6 +264,40 @@ def test_shared_vocabulary(P):
         h.close()
 
 
+@pytest.mark.parametrize("flags", [0, 2], ids=["dense", "no_table"])
+def test_long_and_duplicate_tokens(P, flags):
+    """Tokens longer than the 16-byte probe window and duplicate token strings,
+    at scale: sampled rows, a decode loop and both apply dtypes."""
+    w = W.stress_case()
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=flags)
+    assert h.max_token_len >= 17
+    nodes = sample_nodes(o, 400, 77)
+    for i in range(0, len(nodes), 256):
+        assert np.array_equal(gpu_rows(h, nodes[i:i + 256]), o.mask_rows(nodes[i:i + 256]))
+    rows = o.mask_rows(nodes)
+    long_ids = np.arange(60000, 62000)
+    bits = np.unpackbits(rows.view(np.uint8), axis=1, bitorder="little")[:, : o.V]
+    assert bits[:, long_ids].any(), "sample should contain valid long tokens"
+    assert bits[:, 62000:].any(), "sample should contain valid duplicate tokens"
+    if flags == 0:  # the dense marks and the sparse lists count the same pairs
+        hs = P.compile(w.strings, w.vocab, flags=P.FLAG_NO_TABLE)
+        assert h.valid_pairs() == hs.valid_pairs()
+        hs.close()
+    rng = np.random.default_rng(11)
+    cur = W.uniform_nodes(7, o.N, 64)
+    for step in range(12):
+        r = o.mask_rows(cur)
+        assert np.array_equal(gpu_rows(h, cur), r)
+        toks = W.choose_valid_tokens(rng, r, o.V)
+        exp = o.advance(cur, toks)
+        assert np.array_equal(gpu_advance(h, cur, toks), exp)
+        cur = np.where((exp < 0) | (o.is_final[np.maximum(exp, 0)] == 1), 0, exp).astype(np.int32)
+    check_apply(P, h, o, W.uniform_nodes(7, o.N, 64, 3), "bf16", seed=71)
+    check_apply(P, h, o, W.uniform_nodes(7, o.N, 16, 4), "fp32", seed=72)
+    h.close()
+
+
 # ---------------------------------------------------------- sparse / forest --
 
 def test_no_table_matches_dense_c4(P):

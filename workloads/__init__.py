@@ -355,3 +355,35 @@ def edge_cases() -> list:
         ("long_token", [b"a" * 40, b"a" * 20 + b"b"], byte_tokens() + [b"a" * k for k in range(2, 45)]),
         ("ragged_vocab", [b"hello", b"help", b"helm"], [b"h", b"he", b"hel", b"l", b"lo", b"p", b"m", b"o"]),
     ]
+
+
+@functools.lru_cache(maxsize=None)
+def stress_case() -> Workload:
+    """3,000 code-like strings and a vocabulary that exercises the rare paths:
+    60,000 tokens of the c4 vocabulary, 2,000 long tokens (17-48 bytes) cut from
+    the set strings themselves (so they are valid somewhere), and 1,500 exact
+    duplicates of earlier tokens (short and long)."""
+    rng = rng_for(7, ROLE_SET)
+    lex = make_lexicon(rng_for(7, ROLE_LEXICON), 5000)
+    probs = zipf_probs(5000)
+    strings = code_strings(rng, lex, probs, 3000)
+    base = list(code_vocab_262k(4)[:60000])
+    vrng = rng_for(7, ROLE_VOCAB)
+    taken = set(base)
+    longs = []
+    while len(longs) < 2000:
+        s = strings[int(vrng.integers(0, len(strings)))]
+        if len(s) < 18:
+            continue
+        n = int(vrng.integers(17, min(48, len(s)) + 1))
+        st = int(vrng.integers(0, len(s) - n + 1))
+        t = s[st:st + n]
+        if t not in taken:
+            taken.add(t)
+            longs.append(t)
+    vocab = base + longs
+    dups = [vocab[int(i)] for i in vrng.integers(0, len(vocab), size=1500)]
+    vocab = vocab + dups
+    return Workload(7, "stress", strings, vocab, None, 64, "bf16", 16, "uniform",
+                    "3,000 code-like strings; 60,000 c4 tokens + 2,000 tokens of 17-48 bytes + 1,500 "
+                    "duplicate tokens")
