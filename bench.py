@@ -244,7 +244,7 @@ def main():
     tr = load_traffic(f"k_zero_{w.name}_traffic.json", sha) if has_table else None
     kern_ms = zero_ms if has_table else dev_ms
     roofline = {
-        "kernel": "k_zero" if has_table else "k_probe+k_count+k_scan+k_fill",
+        "kernel": "k_zero" if has_table else "k_probe+k_scan+k_fill",
         "bound": "hbm",
         "achieved": round(table_bytes / (kern_ms * 1e-3) / 1e9, 1),
         "peak": HBM_PEAK_GBPS,
