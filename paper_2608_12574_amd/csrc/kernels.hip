@@ -556,9 +556,11 @@ struct NegInf<uint32_t> {
 // contiguously (one chunk per thread writes fastest, as for the table's zero
 // fill).  All mask bits of the thread are read before its first store.
 // Write-mostly: a chunk without a valid token gets one non-temporal -inf store
-// and no read; a fully valid chunk is skipped; only mixed chunks are read,
-// merged and written.  kSparse: the bits of the block's span come from the
-// node's valid list through an LDS bitmap instead of the dense table.
+// and no read; a fully valid chunk is skipped; a mixed chunk is read, merged and
+// written (dense table), or gets -inf stores into its invalid elements only
+// (lists).  kSparse: the bits of the block's span come from the node's valid
+// list instead of the dense table (a ballot over a short list, an LDS bitmap
+// for a long one).
 // vec == 0: rows are not 16-byte aligned; go element by element.
 template <typename T, bool kSparse>
 __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__restrict__ node_ids,
@@ -585,12 +587,15 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
         const uint32_t lo = (uint32_t)(c0 * E);
         if (e1 - e0 <= kWave) {
             // short list (block-uniform branch): every wave reads the ids into its
-            // lanes and each thread picks the bits of its own chunks
+            // lanes, keeps those inside the block's span (a ballot), and each thread
+            // picks the bits of its own chunks from the few that remain
             const int lane = threadIdx.x & (kWave - 1);
-            const int32_t mine = e0 + lane < e1 ? t.entries[e0 + lane] : 0;
-            for (int j = 0; j < e1 - e0; ++j) {
-                const uint32_t r = (uint32_t)__builtin_amdgcn_readlane(mine, j) - lo;
-                if (r >= (uint32_t)kSpan) continue;
+            const uint32_t mine = lane < e1 - e0 ? (uint32_t)t.entries[e0 + lane] - lo : 0xffffffffu;
+            uint64_t in_span = __ballot(mine < (uint32_t)kSpan);
+            while (in_span) {
+                const int j = __builtin_ctzll(in_span);
+                in_span &= in_span - 1;
+                const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)mine, j);
                 const uint32_t lc = r / E;
 #pragma unroll
                 for (int u = 0; u < kApplyUnits; ++u)
@@ -634,7 +639,28 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
             if (bu == 0) {
                 const uint32_t w = sizeof(T) == 2 ? 0xFF80FF80u : 0xFF800000u;
                 __builtin_nontemporal_store(u32x4{w, w, w, w}, p);
+            } else if (kSparse) {
+                // mixed, lists: -inf into the invalid elements only, no read (the
+                // memory side merges the partial lines; measured faster for the
+                // short valid lists of forests)
+                uint32_t *q = reinterpret_cast<uint32_t *>(p);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (sizeof(T) == 2) {
+                        const uint32_t two = (bu >> (2 * i)) & 3u;
+                        if (two == 0)
+                            q[i] = 0xFF80FF80u;
+                        else if (two == 1)
+                            row[e0 + 2 * i + 1] = NEG;
+                        else if (two == 2)
+                            row[e0 + 2 * i] = NEG;
+                    } else if (!((bu >> i) & 1u)) {
+                        q[i] = 0xFF800000u;
+                    }
+                }
             } else {
+                // mixed, dense table: read, merge, write the whole chunk (measured
+                // faster where valid tokens are spread over many chunks)
                 u32x4 x = *p;
                 T vals[E];
                 __builtin_memcpy(vals, &x, 16);

@@ -326,7 +326,10 @@ def test_forest_c5(P):
         rows = o.mask_rows(cur)
         assert np.array_equal(gpu_rows(h, cur), rows)
         if step in (0, 7):
+            # roots: long lists (LDS bitmap); later steps: short lists (ballot);
+            # both with many mixed chunks, written without a read
             check_apply(P, h, o, cur, "bf16", seed=50 + step)
+            check_apply(P, h, o, cur[:32], "fp32", seed=60 + step)
         toks = W.choose_valid_tokens(rng, rows, o.V)
         exp = o.advance(cur, toks)
         assert np.array_equal(gpu_advance(h, cur, toks), exp)
