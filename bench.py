@@ -39,6 +39,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--repr", choices=["auto", "full", "tail", "lists"], default="auto",
+                    help="mask representation: full dense table, tail compression (dense rows for "
+                         "branching nodes, lists for tails), or lists only; auto = full for one set, "
+                         "lists for a forest")
     ap.add_argument("--apply-iters", type=int, default=1000)
     ap.add_argument("--apply-warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -90,7 +94,8 @@ def main():
     K, V, B = w.K, w.V, w.batch
     logit_dtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     esize = 2 if w.dtype == "bf16" else 4
-    flags = P.FLAG_TIMING | (P.FLAG_NO_TABLE if w.set_offsets is not None else 0)
+    rep = args.repr if args.repr != "auto" else ("lists" if w.set_offsets is not None else "full")
+    flags = P.FLAG_TIMING | {"full": 0, "tail": P.FLAG_TAIL_LISTS, "lists": P.FLAG_NO_TABLE}[rep]
     print(f"[bench] workload {w.name}: K={K} V={V} B={B} ({gen_s:.1f}s to generate)", flush=True)
 
     # ---- end-to-end compile (host trie + vocabulary + upload + device) ----
@@ -271,7 +276,7 @@ def main():
     # dense handles: the table's zero fill, N*W*8 bytes written once;
     # sparse handles (forests): the lists phase, whose algorithmic output is the
     # M valid token ids plus N+1 row offsets (4 bytes each).
-    table_bytes = N * Wd * 8 if has_table else (M + N + 1) * 4
+    table_bytes = h.dense_rows * Wd * 8 if has_table else (M + N + 1) * 4
     tr = load_traffic(f"k_zero_{w.name}_traffic.json", sha) if has_table else None
     kern_ms = zero_ms if has_table else dev_ms
     roofline = {
@@ -341,7 +346,7 @@ def main():
         "vs_baseline": None,
         "dtype": "u64",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {w.description}", "K": K, "V": V, "N": N, "B": B,
+        "config": {"workload": f"{w.name}: {w.description}", "repr": rep, "K": K, "V": V, "N": N, "B": B,
                    "logits_dtype": w.dtype, "num_sets": w.num_sets, "valid_pairs": M},
         "roofline": roofline,
         "roofline_apply": roofline_apply,

@@ -85,7 +85,19 @@ enum {
     TAM_FLAG_NO_TABLE = 1u << 1,
     /* Record HIP events around each device phase of tam_compile/tam_rebuild
      * so that tam_timing_get can report per-phase times. */
-    TAM_FLAG_TIMING = 1u << 2
+    TAM_FLAG_TIMING = 1u << 2,
+    /* Tail compression: dense rows only for branching nodes (two or more final
+     * nodes below them).  A tail node (its subtree is one path, ending in a
+     * single final node) has as valid tokens only prefixes of its one
+     * remaining suffix, at most one per length (per distinct token string):
+     * the short valid lists of the Appendix's memory-vs-speed trade-off.  They
+     * are not stored: the path below a tail has consecutive ids, so the token
+     * of length d starting below tail a is the suffix hit of node a+d, kept by
+     * the probe pass; tokens longer than 16 bytes go to per-node lists.
+     * Results are identical to the full table, which holds dense_rows rows
+     * instead of N (c. 2.5% of the nodes of a set of 10,000 code-like
+     * strings).  Ignored with TAM_FLAG_NO_TABLE. */
+    TAM_FLAG_TAIL_LISTS = 1u << 3
 };
 
 /* Device allocator.  alloc returns device memory aligned to at least 256 bytes
@@ -120,7 +132,11 @@ typedef struct {
     const int32_t *depth;     /* [N] prefix length in bytes (roots: 0) */
     const uint8_t *edge_byte; /* [N] byte on the edge into the node (roots: 0) */
     const uint8_t *is_final;  /* [N] 1 if the node is reached by the terminator */
-    const uint64_t *table;    /* device [N][row_stride_words]; NULL with TAM_FLAG_NO_TABLE */
+    const uint64_t *table;    /* device [dense_rows][row_stride_words]; NULL with TAM_FLAG_NO_TABLE */
+    int64_t dense_rows;       /* rows of `table`: N, or the branching nodes with TAM_FLAG_TAIL_LISTS, or 0 */
+    const int32_t *dense_row; /* [N] table row of each node (>= 0); for a tail node a,
+                                 -1 - (number of nodes below a).  NULL when row = node id
+                                 (full table) or there is no table */
 } tam_info;
 
 /* Host-side wall times of the last tam_compile, and device times (HIP events,
@@ -130,9 +146,9 @@ typedef struct {
     double host_trie_ms;   /* dedupe, sort, preorder trie, child tables */
     double host_vocab_ms;  /* token offsets, vocabulary hash, length table */
     double upload_ms;      /* allocation + enqueue of the host-to-device copies */
-    float dev_lists_ms;    /* sparse valid lists: suffix probes, prefix sum, fill */
+    float dev_lists_ms;    /* sparse valid lists after the probe pass: prefix sum, fill */
     float dev_zero_ms;     /* zero fill of the dense table */
-    float dev_mark_ms;     /* suffix probes setting the valid bits of the dense table */
+    float dev_mark_ms;     /* the probe pass: suffix probes, table marks, list counts */
     float dev_total_ms;    /* first device phase start to last device phase end */
 } tam_timing;
 
@@ -206,7 +222,8 @@ tam_status tam_compile_vocab(const uint8_t *str_bytes, const int64_t *str_off, i
                              tam_handle **out);
 
 enum {
-    TAM_PHASE_LISTS = 1u << 0, /* sparse per-node valid lists (suffix probes, prefix sum, fill) */
+    TAM_PHASE_LISTS = 1u << 0, /* sparse per-node valid lists (suffix probes, prefix sum, fill);
+                                  with TAM_PHASE_MARK one probe pass serves both */
     TAM_PHASE_ZERO = 1u << 1,  /* zero fill of the dense table */
     TAM_PHASE_MARK = 1u << 2,  /* suffix probes setting the valid bits of the zeroed table */
     TAM_PHASE_TABLE = TAM_PHASE_ZERO | TAM_PHASE_MARK
@@ -215,10 +232,12 @@ enum {
 /*
  * tam_rebuild -- rerun device phases of tam_compile from the handle's resident
  * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask; 0 =
- * the handle's default: TAM_PHASE_TABLE for a dense table, TAM_PHASE_LISTS
- * with TAM_FLAG_NO_TABLE (the other kind returns TAM_E_STATE).  TAM_PHASE_MARK
- * without TAM_PHASE_ZERO ORs the same bits into the current table.  Used to
- * time the device phase kernel by kernel.
+ * the handle's default: TAM_PHASE_TABLE for a table, TAM_PHASE_LISTS with
+ * TAM_FLAG_NO_TABLE, both with TAM_FLAG_TAIL_LISTS when the vocabulary has
+ * tokens longer than 16 bytes.  A phase the handle does not keep returns
+ * TAM_E_STATE.  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the
+ * same bits into the current table.  Used to time the device phase kernel by
+ * kernel.
  */
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
 

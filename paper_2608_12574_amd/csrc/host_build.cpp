@@ -331,9 +331,61 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     }
     std::vector<int64_t> cum(L + 1, 0);
     for (int64_t d = 1; d <= L; ++d) cum[(size_t)d] = cum[(size_t)d - 1] + dup[(size_t)d];
+    // A hit at distance d above node m lands in a list iff d <= the node's list
+    // span; with tail compression only the hits longer than the probe window do
+    // (the shorter ones are read straight from the probe's hits).
+    const bool split = !h->tail_span.empty();
     int64_t bound = 0;
-    for (int64_t m = 0; m < h->N; ++m) bound += cum[(size_t)std::min<int64_t>(h->depth[(size_t)m], L)];
+    for (int64_t m = 0; m < h->N; ++m) {
+        const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
+        bound += cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
+    }
     return bound;
+}
+
+/*
+ * Tail compression.  A node is a tail when its subtree holds exactly one final
+ * node, i.e. below it the trie is a single path; its valid tokens are then the
+ * tokens equal to a prefix of that one remaining suffix.  Every other node
+ * (two or more finals below) is a branching node and gets a dense table row,
+ * numbered in id order; a tail a gets row_of[a] = -1 - rem(a), rem(a) being the
+ * number of nodes below it.  In preorder a tail's path has consecutive ids
+ * a+1 .. a+rem(a), so the token of length d starting below a is the suffix hit
+ * of node a+d at distance d: tails need no stored masks.  Tails are closed
+ * under descent, so above any node m the tails form the first tail_span[m]
+ * ancestors: a hit at distance d above m lands on a tail iff d <= tail_span[m]
+ * = depth(m) - depth(highest tail ancestor-or-self of m), and 0 when m itself
+ * branches.  Every parent precedes its children: one backward pass counts the
+ * finals below each node (and the path lengths below tails), one forward pass
+ * finds the highest tail on each path.
+ */
+void split_tails(tam_handle *h) {
+    const int64_t N = h->N;
+    std::vector<int32_t> finals(h->is_final.begin(), h->is_final.end());
+    for (int64_t n = N - 1; n > 0; --n) {
+        const int32_t p = h->parent[(size_t)n];
+        if (p >= 0) finals[(size_t)p] += finals[(size_t)n];
+    }
+    std::vector<int32_t> rem((size_t)N, 0);  // nodes below a tail (its single child is n+1)
+    for (int64_t n = N - 1; n >= 0; --n)
+        if (finals[(size_t)n] == 1 && !h->is_final[(size_t)n]) rem[(size_t)n] = rem[(size_t)n + 1] + 1;
+    h->tail_span.assign((size_t)N, 0);
+    h->row_of.assign((size_t)N, -1);
+    std::vector<int32_t> top((size_t)N, -1);  // depth of the highest tail ancestor-or-self
+    int32_t rows = 0;
+    for (int64_t n = 0; n < N; ++n) {
+        if (finals[(size_t)n] >= 2) {
+            h->row_of[(size_t)n] = rows++;
+            continue;
+        }
+        const int32_t p = h->parent[(size_t)n];
+        top[(size_t)n] = (p >= 0 && top[(size_t)p] >= 0) ? top[(size_t)p] : h->depth[(size_t)n];
+        h->tail_span[(size_t)n] = h->depth[(size_t)n] - top[(size_t)n];
+        h->row_of[(size_t)n] = -1 - rem[(size_t)n];
+    }
+    h->dense_rows = rows;
+    h->row_at.resize(h->node_at.size());
+    for (size_t p = 0; p < h->node_at.size(); ++p) h->row_at[p] = h->row_of[(size_t)h->node_at[p]];
 }
 
 }  // namespace tam

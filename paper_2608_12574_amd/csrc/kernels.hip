@@ -1,26 +1,28 @@
 // HIP kernels of libtam for gfx950 (CDNA4, wave64).
 //
 // Mask compile (Section 4.1, valid[n] for every trie node n):
+//   k_zero   -- zero fill of the dense table (pure streaming stores).
 //   k_probe  -- one lane per non-root node m: the last d <= min(depth(m), ℓ)
 //               bytes of prefix(m) are hashed (read backwards from a 16-byte
 //               register window) and looked up in the vocabulary table; a hit of
 //               token t at d = |t| means t is valid at the ancestor d levels up,
 //               because t's walk from there ends at m.  This is the paper's
 //               crediting of a match to the node |t| bytes back (Section 4.2),
-//               done for all nodes at once instead of along a DFS.  Keeps the
-//               hits for the passes below; for lists it also counts per node.
+//               done for all nodes at once instead of along a DFS.  It keeps
+//               the hits, ORs them into the zeroed table with 64-bit atomics
+//               (nodes with a dense row) and, for lists, counts per node.
 //   k_scan_* -- exclusive prefix sum of the counts into row offsets.
 //   k_fill   -- writes the hits' token ids into the per-node lists.
-//   k_zero   -- zero fill of the dense table (pure streaming stores).
-//   k_mark   -- the hits of k_probe, each OR-ed into the table with a 64-bit
-//               atomic (dense tables need no lists).
 //   k_rows   -- one wave per row builds rows in registers from the lists
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
 //   k_apply  -- write-mostly masking of [B, V] logits.
 //   k_advance-- B byte walks over the child tables.
-//   k_export_dense -- canonical rows out of the dense table.
+//   k_export_dense, k_export_tail -- canonical rows out of the dense table and
+//               (tail compression) the probe's hits.
 #include <hip/hip_runtime.h>
+
+#include <climits>
 
 #include "tam_internal.hpp"
 
@@ -30,6 +32,9 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
 constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
+// k_apply row sources: the dense table, the valid lists, or per row either
+// (tail compression: dense rows for branching nodes, lists for tails)
+constexpr int kApplyTable = 0, kApplyLists = 1, kApplyTail = 2;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -257,114 +262,84 @@ __device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L
     }
 }
 
+// Hits at distance d <= list_span(m) above node m belong to the valid lists:
+// all of them with lists only, the tail ancestors of m with tail compression
+// (where the lists hold only tokens longer than the window).
+__device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
+    if (t.tail_span) return t.tail_span[m];
+    return t.table ? 0 : INT_MAX;
+}
+
 // Probe pass: one lane per node m.  The suffix of length d of prefix(m) equal to
 // token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
 // d <= 16 the hit (hit_of_slot: the token id, or the slot of a string with
-// several ids, or -1) goes to hits[d-1][m]; the hits are kept in registers and
-// stored after the last probe, so no probe load waits behind a store (loads and
-// stores share one vector-memory counter here).  Longer tokens are handled by
-// the consumers, which probe those lengths again.  kCount (sparse lists): the
-// lane then adds its hits to the per-node counts, after all its loads.
+// several ids, or -1) goes to hits[d-1][m]; the tails of tail compression read
+// their tokens back from there.  Longer tokens are probed again where needed
+// (long_hits).  All loads of a lane are issued before its first store or atomic
+// (loads, stores and atomics share one vector-memory counter here).
+//   do_mark (a table): every hit whose ancestor has a dense row (row_at of its
+//     blob position; not a tail) is OR-ed into the zeroed table with a 64-bit
+//     atomic, and each block writes the number of valid (node, token) pairs its
+//     hits make, tails included, into pairs[blockIdx.x].
+//   kCount (lists): the listed hits are counted per node.
 template <bool kCount>
-__global__ void __launch_bounds__(kBlock) k_probe(DevTables t) {
-    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (m >= t.N) return;
-    const int64_t pos = t.node_pos[m];
-    if (pos < 0) return;  // a root ends no token
-    const int L = min(t.depth[m], t.max_len);
-    const int Lw = min(L, kWin);
-    uint64_t lo, hi;
-    load_window(t.blob, pos, lo, hi);
-    int32_t hit[kWin];
-    probe_window(t, pos, Lw, lo, hi, hit);
-    int32_t n[kWin];
-    if (kCount) {
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d) n[d - 1] = hit[d - 1] != -1 ? t.node_at[pos - d] : 0;
-    }
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d)
-        if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = hit[d - 1];
-    if (kCount) {
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d)
-            if (hit[d - 1] >= 0) atomicAdd(&t.count[n[d - 1]], 1);
-        // strings with several token ids and tokens longer than the window (both rare)
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d)
-            if (hit[d - 1] <= -2) atomicAdd(&t.count[n[d - 1]], (int32_t)t.pay[-2 - hit[d - 1]].count);
-        if (L > kWin)
-            long_hits(t, pos, L, [&](int32_t hx, int d) { atomicAdd(&t.count[t.node_at[pos - d]], hit_count(t, hx)); });
-    }
-}
-
-// Fill pass (lists): the hits' token ids written into the per-node lists.
-__global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
-    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (m >= t.N) return;
-    const int64_t pos = t.node_pos[m];
-    if (pos < 0) return;
-    const int L = min(t.depth[m], t.max_len);
-    const int Lw = min(L, kWin);
-    int32_t s[kWin];
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
-#pragma unroll
-    for (int d = 1; d <= kWin; ++d)
-        if (s[d - 1] != -1) emit(t, s[d - 1], t.node_at[pos - d]);
-    if (L > kWin) long_hits(t, pos, L, [&](int32_t hx, int d) { emit(t, hx, t.node_at[pos - d]); });
-}
-
-// Mark pass (dense table): every hit OR-ed into the zeroed table with a 64-bit
-// atomic, after all of the lane's loads.  Each block writes how many (node,
-// token) pairs it set into pairs[blockIdx.x].
-__global__ void __launch_bounds__(kBlock) k_mark(DevTables t, int32_t *__restrict__ pairs) {
+__global__ void __launch_bounds__(kBlock, 4) k_probe(DevTables t, int do_mark, int32_t *__restrict__ pairs) {
     const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     int32_t found = 0;
-    const int64_t pos = m < t.N ? t.node_pos[m] : -1;
+    const int64_t pos = m < t.N ? t.node_pos[m] : -1;  // a root ends no token
     if (pos >= 0) {
         const int L = min(t.depth[m], t.max_len);
         const int Lw = min(L, kWin);
+        const int lspan = kCount ? list_span(t, m) : 0;              // listed up to here
+        const int sspan = t.row_of ? 0 : lspan;                      // short hits listed up to here
+        const int mspan = do_mark ? (t.tail_span ? t.tail_span[m] : 0) : INT_MAX;  // marked beyond
+        uint64_t lo, hi;
+        load_window(t.blob, pos, lo, hi);
+        int32_t hit[kWin];
+        probe_window(t, pos, Lw, lo, hi, hit);
+        int32_t n[kWin], r[kWin];
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d) {
+            n[d - 1] = kCount && hit[d - 1] != -1 && d <= sspan ? t.node_at[pos - d] : -1;
+            r[d - 1] = hit[d - 1] != -1 && d > mspan ? t.row_at[pos - d] : -1;
+        }
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d)
+            if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = hit[d - 1];
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
-        int32_t x[kWin], n[kWin];
-        uint32_t multi = 0;
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d) x[d - 1] = d <= Lw ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d) {
-            n[d - 1] = x[d - 1] != -1 ? t.node_at[pos - d] : 0;
-            if (x[d - 1] <= -2) multi |= 1u << (d - 1);
-        }
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d) {
-            if (x[d - 1] >= 0) {
-                atomicOr(table + (int64_t)n[d - 1] * t.Wp + (x[d - 1] >> 6), 1ull << (x[d - 1] & 63));
-                ++found;
-            }
-        }
-        // strings with several token ids and tokens longer than the window (both rare)
-        auto mark_hit = [&](int32_t hx, int32_t node) {
-            unsigned long long *row = table + (int64_t)node * t.Wp;
+        // one hit: the pairs it makes (do_mark), marked at table row `row` (>= 0),
+        // counted for list node `ln` (>= 0)
+        auto take = [&](int32_t hx, int32_t row, int32_t ln) {
             if (hx >= 0) {
-                atomicOr(row + (hx >> 6), 1ull << (hx & 63));
+                if (row >= 0) atomicOr(table + (int64_t)row * t.Wp + (hx >> 6), 1ull << (hx & 63));
+                if (ln >= 0) atomicAdd(&t.count[ln], 1);
                 ++found;
                 return;
             }
-            const SlotPay mt = t.pay[-2 - hx];
+            const SlotPay mt = t.pay[-2 - hx];  // a string with several token ids (rare)
+            if (ln >= 0) atomicAdd(&t.count[ln], (int32_t)mt.count);
+            found += mt.count;
+            if (row < 0) return;
             int32_t v = mt.first;
             for (int k = 0; k < (int)mt.count; ++k) {
-                atomicOr(row + (v >> 6), 1ull << (v & 63));
+                atomicOr(table + (int64_t)row * t.Wp + (v >> 6), 1ull << (v & 63));
                 v = t.dup_next[v];
             }
-            found += mt.count;
         };
-        for (uint32_t mm = multi; mm; mm &= mm - 1) {
-            const int d = __builtin_ctz(mm) + 1;
-            mark_hit(t.hits[(int64_t)(d - 1) * t.N + m], n[d - 1]);
-        }
-        if (L > kWin) long_hits(t, pos, L, [&](int32_t hx, int d) { mark_hit(hx, t.node_at[pos - d]); });
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d)
+            if (hit[d - 1] >= 0) take(hit[d - 1], r[d - 1], n[d - 1]);
+#pragma unroll
+        for (int d = 1; d <= kWin; ++d)
+            if (hit[d - 1] <= -2) take(hit[d - 1], r[d - 1], n[d - 1]);
+        // tokens longer than the window (rare)
+        if (L > kWin && (do_mark || lspan > kWin))
+            long_hits(t, pos, L, [&](int32_t hx, int d) {
+                take(hx, d > mspan ? t.row_at[pos - d] : -1, d <= lspan ? t.node_at[pos - d] : -1);
+            });
     }
-    // block sum of found
+    if (!do_mark) return;
+    // block sum of the pairs
     __shared__ int32_t wsum[kBlock / kWave];
     for (int o = kWave / 2; o > 0; o >>= 1) found += __shfl_xor(found, o, kWave);
     if ((threadIdx.x & (kWave - 1)) == 0) wsum[threadIdx.x / kWave] = found;
@@ -374,6 +349,29 @@ __global__ void __launch_bounds__(kBlock) k_mark(DevTables t, int32_t *__restric
         for (int w = 0; w < kBlock / kWave; ++w) total += wsum[w];
         pairs[blockIdx.x] = total;
     }
+}
+
+// Fill pass (lists): the hits' token ids written into the per-node lists (with
+// tail compression only those of tokens longer than the window).
+__global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
+    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (m >= t.N) return;
+    const int64_t pos = t.node_pos[m];
+    if (pos < 0) return;
+    const int L = min(t.depth[m], t.max_len);
+    const int Lw = min(L, kWin);
+    const int span = list_span(t, m);
+    const int Ls = t.row_of ? 0 : min(Lw, span);  // tail compression lists long hits only
+    int32_t s[kWin];
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Ls ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+#pragma unroll
+    for (int d = 1; d <= kWin; ++d)
+        if (s[d - 1] != -1) emit(t, s[d - 1], t.node_at[pos - d]);
+    if (L > kWin && span > kWin)
+        long_hits(t, pos, L, [&](int32_t hx, int d) {
+            if (d <= span) emit(t, hx, t.node_at[pos - d]);
+        });
 }
 
 // Zero fill of n16 16-byte chunks: one chunk per thread, 256 threads (4 KiB)
@@ -550,6 +548,33 @@ struct NegInf<uint32_t> {
     static constexpr uint32_t bits = 0xFF800000u;
 };
 
+// One token id per lane (rel = id minus the first element of the block's span;
+// >= kSpan: none or outside): each thread sets the bits of its own chunks.  The
+// ids inside the span are few, so a ballot keeps only those.
+template <int E, int kSpan>
+__device__ __forceinline__ void take_ids(uint32_t rel, uint32_t (&bits)[kApplyUnits]) {
+    uint64_t in_span = __ballot(rel < (uint32_t)kSpan);
+    while (in_span) {
+        const int j = __builtin_ctzll(in_span);
+        in_span &= in_span - 1;
+        const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)rel, j);
+        const uint32_t lc = r / E;
+#pragma unroll
+        for (int u = 0; u < kApplyUnits; ++u)
+            if (lc == (uint32_t)(u * kBlock + threadIdx.x)) bits[u] |= 1u << (r % E);
+    }
+}
+
+// The same for one id held by the whole wave.
+template <int E, int kSpan>
+__device__ __forceinline__ void set_id(uint32_t rel, uint32_t (&bits)[kApplyUnits]) {
+    if (rel >= (uint32_t)kSpan) return;
+    const uint32_t lc = rel / E;
+#pragma unroll
+    for (int u = 0; u < kApplyUnits; ++u)
+        if (lc == (uint32_t)(u * kBlock + threadIdx.x)) bits[u] |= 1u << (rel % E);
+}
+
 // Grid: x = groups of kBlock*kApplyUnits chunks of one row, y = batch row.
 // A chunk is 16 bytes of logits (8 bf16 or 4 fp32); thread i of a block owns
 // chunks c0 + u*kBlock + i, so every store instruction covers 4 KiB per block
@@ -558,18 +583,18 @@ struct NegInf<uint32_t> {
 // Write-mostly: a chunk without a valid token gets one non-temporal -inf store
 // and no read; a fully valid chunk is skipped; a mixed chunk is read, merged and
 // written (dense table), or gets -inf stores into its invalid elements only
-// (lists).  kSparse: the bits of the block's span come from the node's valid
-// list instead of the dense table (a ballot over a short list, an LDS bitmap
-// for a long one).
+// (lists).  List rows (kApplyLists, and the tail rows of kApplyTail): the bits
+// of the block's span come from the node's valid list instead of the dense
+// table (a ballot over a short list, an LDS bitmap for a long one).
 // vec == 0: rows are not 16-byte aligned; go element by element.
-template <typename T, bool kSparse>
+template <typename T, int kMode>
 __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__restrict__ node_ids,
                                                   T *__restrict__ logits, int64_t stride, int vec) {
     constexpr int E = 16 / (int)sizeof(T);
     constexpr uint32_t FULL = (1u << E) - 1u;
     constexpr T NEG = NegInf<T>::bits;
     constexpr int kSpan = kBlock * kApplyUnits * E;  // elements per block
-    __shared__ uint32_t bm[kSparse ? kSpan / 32 : 1];
+    __shared__ uint32_t bm[kMode != kApplyTable ? kSpan / 32 : 1];
 
     const int64_t V = t.V;
     const int64_t b = blockIdx.y;
@@ -578,29 +603,50 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
     const int64_t c0 = (int64_t)blockIdx.x * kBlock * kApplyUnits;
     const int64_t nchunks = (V + E - 1) / E;
     T *row = logits + b * stride;
+    // the row's source (uniform over the block): its dense table row, its list,
+    // or (a tail with tail compression) the probe's hits along its path
+    int64_t trow = live ? n : -1;
+    if (kMode == kApplyTail && live) trow = t.row_of[n];
+    const bool tail_row = kMode == kApplyTail && live && trow < 0;
+    const bool use_list = kMode == kApplyLists;
 
     uint32_t bits[kApplyUnits];
-    if (kSparse) {
 #pragma unroll
-        for (int u = 0; u < kApplyUnits; ++u) bits[u] = 0;
+    for (int u = 0; u < kApplyUnits; ++u) bits[u] = 0;
+    const uint32_t lo = (uint32_t)(c0 * E);
+    const int lane = threadIdx.x & (kWave - 1);
+    if (tail_row) {
+        // lane d-1 takes the token of length d starting below the tail: the hit
+        // of node n+d at distance d (the path below a tail has consecutive ids)
+        const int Lt = min(min(-1 - (int)trow, kWin), (int)t.max_len);
+        const int32_t x = lane < Lt ? t.hits[(int64_t)lane * t.N + n + lane + 1] : -1;
+        take_ids<E, kSpan>(x >= 0 ? (uint32_t)x - lo : 0xffffffffu, bits);
+        // strings with several token ids (rare): walk their id chains
+        uint64_t multi = __ballot(x <= -2);
+        while (multi) {
+            const int j = __builtin_ctzll(multi);
+            multi &= multi - 1;
+            const SlotPay pm = t.pay[-2 - __builtin_amdgcn_readlane(x, j)];
+            int32_t v = pm.first;
+            for (int k = 0; k < (int)pm.count; ++k) {
+                set_id<E, kSpan>((uint32_t)v - lo, bits);
+                v = t.dup_next[v];
+            }
+        }
+        if (t.tail_long) {  // tokens longer than the window: the tail's list
+            const int32_t e0 = t.row_ptr[n], e1 = t.row_ptr[n + 1];
+            for (int32_t k0 = e0; k0 < e1; k0 += kWave) {
+                const uint32_t rel = k0 + lane < e1 ? (uint32_t)t.entries[k0 + lane] - lo : 0xffffffffu;
+                take_ids<E, kSpan>(rel, bits);
+            }
+        }
+    } else if (use_list) {
         const int32_t e0 = live ? t.row_ptr[n] : 0, e1 = live ? t.row_ptr[n + 1] : 0;
-        const uint32_t lo = (uint32_t)(c0 * E);
         if (e1 - e0 <= kWave) {
             // short list (block-uniform branch): every wave reads the ids into its
             // lanes, keeps those inside the block's span (a ballot), and each thread
             // picks the bits of its own chunks from the few that remain
-            const int lane = threadIdx.x & (kWave - 1);
-            const uint32_t mine = lane < e1 - e0 ? (uint32_t)t.entries[e0 + lane] - lo : 0xffffffffu;
-            uint64_t in_span = __ballot(mine < (uint32_t)kSpan);
-            while (in_span) {
-                const int j = __builtin_ctzll(in_span);
-                in_span &= in_span - 1;
-                const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)mine, j);
-                const uint32_t lc = r / E;
-#pragma unroll
-                for (int u = 0; u < kApplyUnits; ++u)
-                    if (lc == (uint32_t)(u * kBlock + threadIdx.x)) bits[u] |= 1u << (r % E);
-            }
+            take_ids<E, kSpan>(lane < e1 - e0 ? (uint32_t)t.entries[e0 + lane] - lo : 0xffffffffu, bits);
         } else {
             // long list: scatter through an LDS bitmap of the block's span
             for (int i = threadIdx.x; i < kSpan / 32; i += kBlock) bm[i] = 0;
@@ -617,12 +663,13 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
             }
         }
     } else {
-        const uint8_t *mrow = reinterpret_cast<const uint8_t *>(t.table + (live ? (int64_t)n * t.Wp : 0));
+        const uint8_t *mrow = reinterpret_cast<const uint8_t *>(t.table + (trow >= 0 ? trow * t.Wp : 0));
 #pragma unroll
         for (int u = 0; u < kApplyUnits; ++u) {
             const int64_t c = c0 + u * kBlock + threadIdx.x;
             uint32_t x = 0;
-            if (live && c < nchunks) x = E == 8 ? (uint32_t)mrow[c] : ((uint32_t)mrow[c >> 1] >> ((c & 1) * 4)) & FULL;
+            if (trow >= 0 && c < nchunks)
+                x = E == 8 ? (uint32_t)mrow[c] : ((uint32_t)mrow[c >> 1] >> ((c & 1) * 4)) & FULL;
             bits[u] = x;
         }
     }
@@ -639,10 +686,10 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
             if (bu == 0) {
                 const uint32_t w = sizeof(T) == 2 ? 0xFF80FF80u : 0xFF800000u;
                 __builtin_nontemporal_store(u32x4{w, w, w, w}, p);
-            } else if (kSparse) {
-                // mixed, lists: -inf into the invalid elements only, no read (the
-                // memory side merges the partial lines; measured faster for the
-                // short valid lists of forests)
+            } else if (use_list || tail_row) {
+                // mixed, list or tail row: -inf into the invalid elements only, no
+                // read (the memory side merges the partial lines; measured faster
+                // for short valid lists)
                 uint32_t *q = reinterpret_cast<uint32_t *>(p);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -774,13 +821,45 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
 
 // ---------------------------------------------------------------- export ---
 
+// Rows of the nodes with a dense row; all zero for a dead node and (with tail
+// compression) for a tail, whose bits k_export_tail then sets.
 __global__ void __launch_bounds__(kBlock) k_export_dense(DevTables t, const int32_t *nodes, uint64_t *out) {
     const int64_t r = blockIdx.y;
     const int64_t w = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (w >= t.W) return;
     const int32_t n = nodes[r];
     const bool live = n >= 0 && (int64_t)n < t.N;
-    out[r * t.W + w] = live ? t.table[(int64_t)n * t.Wp + w] : 0ull;
+    const int64_t trow = live ? (t.row_of ? (int64_t)t.row_of[n] : (int64_t)n) : -1;
+    out[r * t.W + w] = trow >= 0 ? t.table[trow * t.Wp + w] : 0ull;
+}
+
+// Tail rows (tail compression), one wave per requested row: the ids of the
+// tail's hits (as in k_apply) OR-ed into the zeroed output row.
+__global__ void __launch_bounds__(kBlock) k_export_tail(DevTables t, const int32_t *nodes, int64_t nrows,
+                                                        uint64_t *out) {
+    const int64_t r = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (r >= nrows) return;
+    const int32_t n = nodes[r];
+    if (n < 0 || (int64_t)n >= t.N) return;
+    const int32_t trow = t.row_of[n];
+    if (trow >= 0) return;
+    unsigned long long *row = reinterpret_cast<unsigned long long *>(out + r * t.W);
+    auto set = [&](int32_t v) { atomicOr(row + (v >> 6), 1ull << (v & 63)); };
+    const int Lt = min(min(-1 - trow, kWin), (int)t.max_len);
+    const int32_t x = lane < Lt ? t.hits[(int64_t)lane * t.N + n + lane + 1] : -1;
+    if (x >= 0) {
+        set(x);
+    } else if (x <= -2) {
+        const SlotPay pm = t.pay[-2 - x];
+        int32_t v = pm.first;
+        for (int k = 0; k < (int)pm.count; ++k) {
+            set(v);
+            v = t.dup_next[v];
+        }
+    }
+    if (t.tail_long)
+        for (int32_t k = t.row_ptr[n] + lane; k < t.row_ptr[n + 1]; k += kWave) set(t.entries[k]);
 }
 
 inline unsigned grid_for(int64_t n, int per_block) {
@@ -798,12 +877,13 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s) 
     return hipGetLastError();
 }
 
-hipError_t launch_probe(const DevTables &t, bool count, hipStream_t s) {
+hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pairs, hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
+    const int do_mark = mark && t.table ? 1 : 0;
     if (count)
-        hipLaunchKernelGGL(k_probe<true>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+        hipLaunchKernelGGL(k_probe<true>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, do_mark, pairs);
     else
-        hipLaunchKernelGGL(k_probe<false>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t);
+        hipLaunchKernelGGL(k_probe<false>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, do_mark, pairs);
     return hipGetLastError();
 }
 
@@ -818,12 +898,6 @@ hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s) {
     if (n16 <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_zero, dim3(grid_for(n16, kBlock)), dim3(kBlock), 0, s,
                        reinterpret_cast<u32x4 *>(p), n16);
-    return hipGetLastError();
-}
-
-hipError_t launch_mark(const DevTables &t, int32_t *pairs, hipStream_t s) {
-    if (t.N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_mark, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, pairs);
     return hipGetLastError();
 }
 
@@ -868,23 +942,27 @@ hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, 
     const int vec = ((reinterpret_cast<uintptr_t>(logits) & 15) == 0 && ((row_stride * elem) & 15) == 0)
                         ? 1
                         : 0;
-    const bool sparse = t.table == nullptr;
+    const int mode = t.table == nullptr ? kApplyLists : (t.row_of ? kApplyTail : kApplyTable);
     // grid.y is limited to 65535 rows per launch
     for (int64_t r0 = 0; r0 < B; r0 += 65535) {
         const dim3 grid(gx, (unsigned)std::min<int64_t>(B - r0, 65535));
         const int32_t *ids = node_ids + r0;
         if (dtype == TAM_DTYPE_BF16) {
             uint16_t *p = static_cast<uint16_t *>(logits) + r0 * row_stride;
-            if (sparse)
-                hipLaunchKernelGGL((k_apply<uint16_t, true>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+            if (mode == kApplyLists)
+                hipLaunchKernelGGL((k_apply<uint16_t, kApplyLists>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+            else if (mode == kApplyTail)
+                hipLaunchKernelGGL((k_apply<uint16_t, kApplyTail>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
             else
-                hipLaunchKernelGGL((k_apply<uint16_t, false>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+                hipLaunchKernelGGL((k_apply<uint16_t, kApplyTable>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
         } else {
             uint32_t *p = static_cast<uint32_t *>(logits) + r0 * row_stride;
-            if (sparse)
-                hipLaunchKernelGGL((k_apply<uint32_t, true>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+            if (mode == kApplyLists)
+                hipLaunchKernelGGL((k_apply<uint32_t, kApplyLists>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+            else if (mode == kApplyTail)
+                hipLaunchKernelGGL((k_apply<uint32_t, kApplyTail>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
             else
-                hipLaunchKernelGGL((k_apply<uint32_t, false>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
+                hipLaunchKernelGGL((k_apply<uint32_t, kApplyTable>), grid, dim3(kBlock), 0, s, t, ids, p, row_stride, vec);
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -909,7 +987,9 @@ hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int6
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    return hipSuccess;
+    if (!t.row_of) return hipSuccess;
+    hipLaunchKernelGGL(k_export_tail, dim3(grid_for(n, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, n, out);
+    return hipGetLastError();
 }
 
 }  // namespace tam

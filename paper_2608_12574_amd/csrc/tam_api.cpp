@@ -175,19 +175,13 @@ void *dev_alloc(tam_handle *h, size_t bytes) {
 void release_device(tam_handle *h) {
     if (h->work_done) (void)hipEventSynchronize(h->work_done);
     if (h->have_events) (void)hipEventSynchronize(h->ev[3]);
-    if (h->side) (void)hipStreamSynchronize(h->side);
     for (void *p : h->dev_ptrs) free_with(h->own_alloc, h->alloc, p);
     h->dev_ptrs.clear();
     if (h->have_events)
         for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
     if (h->work_done) (void)hipEventDestroy(h->work_done);
-    if (h->side) (void)hipStreamDestroy(h->side);
-    if (h->fork) (void)hipEventDestroy(h->fork);
-    if (h->join) (void)hipEventDestroy(h->join);
     h->have_events = false;
     h->work_done = nullptr;
-    h->side = nullptr;
-    h->fork = h->join = nullptr;
 }
 
 void destroy_handle(tam_handle *h) {
@@ -196,43 +190,36 @@ void destroy_handle(tam_handle *h) {
     delete h;
 }
 
+// The handle keeps valid lists (all nodes without a table; with tail
+// compression the tails' tokens longer than the probe window, if the vocabulary
+// has any) and/or a dense table.
+bool keeps_lists(const tam_handle *h) { return !h->dt.table || h->dt.tail_long; }
+
 unsigned default_phases(const tam_handle *h) {
-    return h->dt.table ? unsigned(TAM_PHASE_TABLE) : unsigned(TAM_PHASE_LISTS);
+    return (keeps_lists(h) ? unsigned(TAM_PHASE_LISTS) : 0u) | (h->dt.table ? unsigned(TAM_PHASE_TABLE) : 0u);
 }
 
-// The device part of compile.  Lists: probes counting per node, prefix sum,
-// fill.  Table: zero fill with the probes beside it on the side stream, then
-// the marks.  Phase events are recorded only for the handle's default phases.
+// The device part of compile, on the caller's stream: zero fill of the table,
+// the probe pass (marks into the table, counts for the lists), then the lists'
+// prefix sum and fill.  Phase events are recorded only for the handle's
+// default phases.
 tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     const tam::DevTables &t = h->dt;
     const bool timing = h->have_events && phases == default_phases(h);
+    const bool lists = (phases & TAM_PHASE_LISTS) != 0;
+    const bool zero = (phases & TAM_PHASE_ZERO) && t.table;
+    const bool mark = (phases & TAM_PHASE_MARK) && t.table;
     if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
-    if (phases & TAM_PHASE_LISTS) {
-        TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
-        TAM_HIP(tam::launch_probe(t, true, s));
+    if (zero) TAM_HIP(tam::launch_zero(t.table, t.R * t.Wp, s));
+    if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
+    if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
+    if (lists || mark) TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+    if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
+    if (lists) {
         TAM_HIP(tam::launch_scan(t, s));
         TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
         TAM_HIP(tam::launch_fill_lists(t, s));
         h->lists_built = true;
-    }
-    if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
-    // With both table phases, the probes (L2-latency bound) run on the side
-    // stream while the zero fill (HBM-write bound) runs on the caller's stream.
-    const bool overlap = t.table && (phases & TAM_PHASE_TABLE) == unsigned(TAM_PHASE_TABLE) && h->side;
-    if (overlap) {
-        TAM_HIP(hipEventRecord(h->fork, s));
-        TAM_HIP(hipStreamWaitEvent(h->side, h->fork, 0));
-        TAM_HIP(tam::launch_probe(t, false, h->side));
-        TAM_HIP(hipEventRecord(h->join, h->side));
-    }
-    if ((phases & TAM_PHASE_ZERO) && t.table) TAM_HIP(tam::launch_zero(t.table, t.N * t.Wp, s));
-    if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
-    if ((phases & TAM_PHASE_MARK) && t.table) {
-        if (overlap)
-            TAM_HIP(hipStreamWaitEvent(s, h->join, 0));
-        else
-            TAM_HIP(tam::launch_probe(t, false, s));
-        TAM_HIP(tam::launch_mark(t, h->pairs, s));
     }
     if (timing) {
         TAM_HIP(hipEventRecord(h->ev[3], s));
@@ -283,6 +270,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     try {
         const auto t0 = std::chrono::steady_clock::now();
         st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);
+        if (st == TAM_OK && (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_NO_TABLE))
+            tam::split_tails(h);
         h->timing.host_trie_ms = ms_since(t0);
         if (st == TAM_OK) {
             h->entry_bound = tam::entry_upper_bound(h, vocab);
@@ -323,6 +312,12 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->own_alloc = alloc == nullptr;
     if (alloc) h->alloc = *alloc;
     const bool want_table = !(h->flags & TAM_FLAG_NO_TABLE);
+    const bool tails = want_table && !h->tail_span.empty();
+    const bool tail_long = tails && vocab->max_tok_len > tam::kWin;
+    const bool want_lists = !want_table || tail_long;
+    // dense rows: every node, or the branching nodes (at least one row is kept
+    // so that a tail-compressed handle always has a table)
+    const int64_t R = !want_table ? 0 : tails ? std::max<int64_t>(h->dense_rows, 1) : h->N;
 
     Arena a;
     const size_t o_blob = a.take<uint8_t>(h->blob_bytes);
@@ -336,13 +331,16 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_count = a.take<int32_t>(h->N);
     const size_t o_row_ptr = a.take<int32_t>(h->N + 1);
     const size_t o_cursor = a.take<int32_t>(h->N);
-    const size_t o_entries = a.take<int32_t>(want_table ? 1 : h->entry_bound);
+    const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
+    const size_t o_tail_span = a.take<int32_t>(tails ? h->N : 0);
+    const size_t o_row_of = a.take<int32_t>(tails ? h->N : 0);
+    const size_t o_row_at = a.take<int32_t>(tails ? h->blob_bytes : 0);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
     const size_t o_pairs = a.take<int32_t>(tam::mark_blocks(h->N));
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = nullptr;
-    const size_t table_bytes = (size_t)h->N * (size_t)h->Wp * sizeof(uint64_t);
+    const size_t table_bytes = (size_t)R * (size_t)h->Wp * sizeof(uint64_t);
     if (base && want_table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
     if (!base || (want_table && !table)) {
         destroy_handle(h);
@@ -373,6 +371,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
     t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
     t.table = table;
+    t.tail_span = tails ? reinterpret_cast<const int32_t *>(base + o_tail_span) : nullptr;
+    t.row_of = tails ? reinterpret_cast<const int32_t *>(base + o_row_of) : nullptr;
+    t.row_at = tails ? reinterpret_cast<const int32_t *>(base + o_row_at) : t.node_at;
+    t.R = R;
+    t.tail_long = tail_long ? 1 : 0;
     t.N = h->N;
     t.V = h->V;
     t.W = h->W;
@@ -395,11 +398,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     if (e == hipSuccess) e = up(o_child_off, h->child_off.data(), h->child_off.size() * 4);
     if (e == hipSuccess) e = up(o_child_byte, h->child_byte.data(), h->child_byte.size());
     if (e == hipSuccess) e = up(o_child_node, h->child_node.data(), h->child_node.size() * 4);
+    if (e == hipSuccess && tails) e = up(o_tail_span, h->tail_span.data(), h->tail_span.size() * 4);
+    if (e == hipSuccess && tails) e = up(o_row_of, h->row_of.data(), h->row_of.size() * 4);
+    if (e == hipSuccess && tails) e = up(o_row_at, h->row_at.data(), h->row_at.size() * 4);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
-    if (e == hipSuccess && table) e = hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking);
-    if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming);
-    if (e == hipSuccess && table) e = hipEventCreateWithFlags(&h->join, hipEventDisableTiming);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
         for (hipEvent_t &ev : h->ev)
             if (e == hipSuccess) e = hipEventCreate(&ev);
@@ -480,8 +483,9 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
     if (phases == 0) phases = default_phases(h);
     if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
     if ((phases & TAM_PHASE_TABLE) && !h->dt.table) return fail(TAM_E_STATE, "handle has no dense table");
-    if ((phases & TAM_PHASE_LISTS) && h->dt.table)
-        return fail(TAM_E_STATE, "valid lists are kept only by handles with TAM_FLAG_NO_TABLE");
+    if ((phases & TAM_PHASE_LISTS) && !keeps_lists(h))
+        return fail(TAM_E_STATE, "valid lists are kept only with TAM_FLAG_NO_TABLE, or with "
+                                 "TAM_FLAG_TAIL_LISTS and tokens longer than 16 bytes");
     return run_device_phase(h, phases, static_cast<hipStream_t>(stream));
 }
 
@@ -503,6 +507,9 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
     out->edge_byte = h->edge.data();
     out->is_final = h->is_final.data();
     out->table = h->dt.table;
+    const bool tails = !h->tail_span.empty();
+    out->dense_rows = tails ? h->dense_rows : (h->flags & TAM_FLAG_NO_TABLE) ? 0 : h->N;
+    out->dense_row = tails ? h->row_of.data() : nullptr;
     return TAM_OK;
 }
 
@@ -560,19 +567,17 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     if (st != TAM_OK) return st;
     if (!out) return fail(TAM_E_INVAL, "out is null");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (h->dt.table) {
-        std::vector<int32_t> part((size_t)tam::mark_blocks(h->N));
+    // a table's marks count every pair (tails' too); without one the lists do
+    std::vector<int32_t> part(h->dt.table ? (size_t)tam::mark_blocks(h->N) : 0);
+    int32_t listed = 0;
+    if (h->dt.table)
         TAM_HIP(hipMemcpyAsync(part.data(), h->pairs, part.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
-        TAM_HIP(hipStreamSynchronize(s));
-        int64_t m = 0;
-        for (int32_t x : part) m += x;
-        *out = m;
-    } else {
-        int32_t m = 0;
-        TAM_HIP(hipMemcpyAsync(&m, h->dt.row_ptr + h->N, sizeof(m), hipMemcpyDeviceToHost, s));
-        TAM_HIP(hipStreamSynchronize(s));
-        *out = m;
-    }
+    else
+        TAM_HIP(hipMemcpyAsync(&listed, h->dt.row_ptr + h->N, sizeof(listed), hipMemcpyDeviceToHost, s));
+    TAM_HIP(hipStreamSynchronize(s));
+    int64_t m = listed;
+    for (int32_t x : part) m += x;
+    *out = m;
     return TAM_OK;
 }
 
@@ -581,9 +586,9 @@ tam_status tam_timing_get(const tam_handle *h, tam_timing *out) {
     *out = h->timing;
     if (h->have_events && h->events_recorded) {
         TAM_HIP(hipEventSynchronize(h->ev[3]));
-        TAM_HIP(hipEventElapsedTime(&out->dev_lists_ms, h->ev[0], h->ev[1]));
-        TAM_HIP(hipEventElapsedTime(&out->dev_zero_ms, h->ev[1], h->ev[2]));
-        TAM_HIP(hipEventElapsedTime(&out->dev_mark_ms, h->ev[2], h->ev[3]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_zero_ms, h->ev[0], h->ev[1]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_mark_ms, h->ev[1], h->ev[2]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_lists_ms, h->ev[2], h->ev[3]));
         TAM_HIP(hipEventElapsedTime(&out->dev_total_ms, h->ev[0], h->ev[3]));
     }
     return TAM_OK;

@@ -84,9 +84,18 @@ struct DevTables {
     int32_t *row_ptr;           // [N+1]
     int32_t *cursor;            // [N]
     int32_t *entries;           // [entry_bound]
-    uint64_t *table;            // [N][Wp] or null
+    uint64_t *table;            // [R][Wp] or null
+    // tail compression (null unless the handle has both a table and lists):
+    // hits at distance d <= tail_span[m] above node m land on tail nodes (lists),
+    // the others on branching nodes (dense rows row_of[node])
+    const int32_t *tail_span;   // [N]
+    const int32_t *row_of;      // [N] dense row of a node; a tail a: -1 - (nodes below a); null: row = node id
+    const int32_t *row_at;      // [blob_bytes] row_of[node_at[p]]; equals node_at without row_of
     int32_t *scan_tmp;          // block sums of the scan
     int64_t N, V, W, Wp;
+    int64_t R;                  // dense rows (N for a full table, 0 without one)
+    int32_t tail_long;          // tail compression with tokens longer than kWin: their hits on
+                                // tails go to the lists (row_ptr / entries)
     int64_t blob_bytes;
     uint64_t slot_mask;         // slots - 1 (slots = a power of two, >= kBucket)
     uint64_t len_mask;          // bit d (d < 64): some token has length d
@@ -96,10 +105,9 @@ struct DevTables {
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
-hipError_t launch_probe(const DevTables &t, bool count, hipStream_t s);
+hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pairs, hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
-hipError_t launch_mark(const DevTables &t, int32_t *pairs, hipStream_t s);
 int64_t mark_blocks(int64_t N);
 hipError_t launch_fill_lists(const DevTables &t, hipStream_t s);
 hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
@@ -164,6 +172,9 @@ struct tam_handle {
     // host trie tables
     std::vector<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
     std::vector<uint8_t> edge, is_final, blob, child_byte;
+    // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
+    std::vector<int32_t> tail_span, row_of, row_at;
+    int64_t dense_rows = 0;
 
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};
@@ -174,7 +185,5 @@ struct tam_handle {
     bool have_events = false;
     bool events_recorded = false;
     hipEvent_t work_done = nullptr;  // end of the last upload / device phase
-    hipStream_t side = nullptr;      // runs the table phase's probes beside its zero fill
-    hipEvent_t fork = nullptr, join = nullptr;
     tam_timing timing{};
 };

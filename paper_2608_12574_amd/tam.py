@@ -9,6 +9,7 @@ provides device memory (through the allocator callbacks) and the stream
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 import numpy as np
@@ -19,7 +20,7 @@ LIB_PATH = os.path.join(PKG, "libtam.so")
 TAM_OK = 0
 TAM_DEAD = -1
 DTYPE_FP32, DTYPE_BF16 = 0, 1
-FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING = 1, 2, 4
+FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, FLAG_TAIL_LISTS = 1, 2, 4, 8
 PHASE_LISTS, PHASE_ZERO, PHASE_MARK = 1, 2, 4
 PHASE_TABLE = PHASE_ZERO | PHASE_MARK
 
@@ -58,7 +59,8 @@ class Info(ctypes.Structure):
                 ("flags", ctypes.c_uint32), ("terminator", ctypes.c_int32),
                 ("roots", ctypes.POINTER(ctypes.c_int32)), ("parent", ctypes.POINTER(ctypes.c_int32)),
                 ("depth", ctypes.POINTER(ctypes.c_int32)), ("edge_byte", ctypes.POINTER(ctypes.c_uint8)),
-                ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p)]
+                ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p),
+                ("dense_rows", ctypes.c_int64), ("dense_row", ctypes.POINTER(ctypes.c_int32))]
 
 
 class Timing(ctypes.Structure):
@@ -182,13 +184,39 @@ class Handle:
         self.device_bytes = int(info.device_bytes)
         self.flags = int(info.flags)
         self.terminator = int(info.terminator)
-        N, S = self.num_nodes, self.num_sets
-        self.roots = np.ctypeslib.as_array(info.roots, shape=(S,)).copy()
-        self.parent = np.ctypeslib.as_array(info.parent, shape=(N,)).copy()
-        self.depth = np.ctypeslib.as_array(info.depth, shape=(N,)).copy()
-        self.edge_byte = np.ctypeslib.as_array(info.edge_byte, shape=(N,)).copy()
-        self.is_final = np.ctypeslib.as_array(info.is_final, shape=(N,)).copy()
+        self.dense_rows = int(info.dense_rows)
+        self.roots = np.ctypeslib.as_array(info.roots, shape=(self.num_sets,)).copy()
         self.table_ptr = info.table
+        self._info = info  # per-node host arrays are copied on first use
+
+    def _host_array(self, name):
+        if self._raw is None:
+            raise TamError(-6, name, "handle is closed")
+        ptr = getattr(self._info, name)
+        return np.ctypeslib.as_array(ptr, shape=(self.num_nodes,)).copy()
+
+    @functools.cached_property
+    def parent(self):
+        return self._host_array("parent")
+
+    @functools.cached_property
+    def depth(self):
+        return self._host_array("depth")
+
+    @functools.cached_property
+    def edge_byte(self):
+        return self._host_array("edge_byte")
+
+    @functools.cached_property
+    def is_final(self):
+        return self._host_array("is_final")
+
+    @functools.cached_property
+    def dense_row(self):
+        """Table row of each node (-1: kept as a list), or None when row = node id."""
+        if not self._info.dense_row:
+            return None
+        return self._host_array("dense_row")
 
     # -- lifetime ------------------------------------------------------------
     def close(self):

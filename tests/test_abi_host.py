@@ -182,3 +182,43 @@ def test_missing_library_fails_loudly(P, monkeypatch):
     monkeypatch.setattr(T, "LIB_PATH", "/nonexistent/libtam.so")
     with pytest.raises(RuntimeError, match="no fallback"):
         T.lib()
+
+
+def _branching(o):
+    cnt = o.is_final.astype(np.int64)
+    for n in range(o.N - 1, 0, -1):
+        if o.parent[n] >= 0:
+            cnt[o.parent[n]] += cnt[n]
+    return cnt >= 2
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_tail_split_host_only(P, oracle_mod, cid):
+    """Tail compression keeps dense rows for exactly the nodes with two or more
+    final nodes below them, numbered in id order (host tables, no GPU)."""
+    w = W.config(cid)
+    o = oracle_mod.Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY | P.FLAG_TAIL_LISTS)
+    branch = _branching(o)
+    assert h.dense_rows == int(branch.sum())
+    assert np.array_equal(h.dense_row >= 0, branch)
+    assert np.array_equal(h.dense_row[branch], np.arange(h.dense_rows))
+    # a tail stores how many nodes lie below it on its path
+    size = np.ones(o.N, dtype=np.int64)
+    for n in range(o.N - 1, 0, -1):
+        size[o.parent[n]] += size[n]
+    assert np.array_equal(-1 - h.dense_row[~branch], size[~branch] - 1)
+    full = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY)
+    assert full.dense_row is None and full.dense_rows == o.N
+    lists = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY | P.FLAG_NO_TABLE | P.FLAG_TAIL_LISTS)
+    assert lists.dense_row is None and lists.dense_rows == 0
+
+
+def test_tail_split_forest_host_only(P, oracle_mod):
+    sets = [[b"ab", b"a"], [b""], [b"ba", b"bb", b"b"], [b"abc"]]
+    flat = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    vocab = [b"a", b"b", b"c", b'"']
+    o = oracle_mod.Oracle(flat, vocab, set_offsets=offs)
+    h = P.compile(flat, vocab, sets=offs, flags=P.FLAG_HOST_ONLY | P.FLAG_TAIL_LISTS)
+    assert np.array_equal(h.dense_row >= 0, _branching(o))

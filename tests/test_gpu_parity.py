@@ -93,9 +93,25 @@ def full_check(P, strings, vocab, sets=None, flags=0, terminator=0x22):
     return h, o
 
 
-def test_worked_example(P):
+# the three representations: full dense table, lists only, tail compression
+FLAGS3 = [0, 2, 8]
+FLAG_IDS3 = ["dense", "no_table", "tail"]
+
+
+def branching_nodes(o: Oracle) -> np.ndarray:
+    """Nodes with two or more final nodes below them (independent of the library)."""
+    cnt = o.is_final.astype(np.int64)
+    par = o.parent
+    for n in range(o.N - 1, 0, -1):
+        if par[n] >= 0:
+            cnt[par[n]] += cnt[n]
+    return cnt >= 2
+
+
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+def test_worked_example(P, flags):
     vocab = [b"medical", b"_bill", b"_cod", b"_rec", b"ing", b"ords", b'"']
-    h, o = full_check(P, [b"medical_billing", b"medical_coding", b"medical_records"], vocab)
+    h, o = full_check(P, [b"medical_billing", b"medical_coding", b"medical_records"], vocab, flags=flags)
     assert h.valid_pairs() == 10  # rows 0,7,12,19,26 (1+3+1+1+1) + '"' at 15,22,30
     rows = gpu_rows(h, [0, 7, 12, 19, 26])
     assert [int(r[0]) for r in rows] == [1, 0b1110, 0b10000, 0b10000, 0b100000]
@@ -103,10 +119,11 @@ def test_worked_example(P):
 
 @pytest.mark.parametrize("name,strings,vocab", W.edge_cases(), ids=[e[0] for e in W.edge_cases()])
 def test_edge_suite(P, name, strings, vocab):
-    full_check(P, strings, vocab)
+    for flags in FLAGS3:
+        full_check(P, strings, vocab, flags=flags)
 
 
-@pytest.mark.parametrize("flags", [0, 2], ids=["dense", "no_table"])
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
 def test_tiny_random_sets(P, flags):
     rng = np.random.default_rng(123)
     alphabet = np.frombuffer(b'ab"\x80', dtype=np.uint8)
@@ -115,6 +132,8 @@ def test_tiny_random_sets(P, flags):
         strings = [bytes(alphabet[rng.integers(0, 2, size=rng.integers(0, 7))]).replace(b'"', b"a")
                    for _ in range(rng.integers(1, 7))]
         h, o = full_check(P, strings, vocab, flags=flags)
+        if flags == 8:
+            assert np.array_equal(h.dense_row >= 0, branching_nodes(o))
         b = Brute(strings, vocab)
         for n in range(o.N):
             got = np.unpackbits(gpu_rows(h, [n])[0].view(np.uint8), bitorder="little")[: len(vocab)]
@@ -126,13 +145,21 @@ def test_tiny_forest(P):
     flat = [s for g in sets for s in g]
     offs = np.cumsum([0] + [len(g) for g in sets])
     vocab = [b"a", b"b", b"c", b'"', b"ab", b"b\"", b"abc\"", b""]
-    for flags in (0, 2):
+    for flags in FLAGS3:
         full_check(P, flat, vocab, sets=offs, flags=flags)
 
 
 def test_other_terminator_and_high_bytes(P):
-    full_check(P, [b'x"y', b"x", b"\xff\x00"], [b"x", b'"', b'"y', b"|", b"y|", b"\xff", b"\x00|"],
-               terminator=ord("|"))
+    for flags in FLAGS3:
+        full_check(P, [b'x"y', b"x", b"\xff\x00"], [b"x", b'"', b'"y', b"|", b"y|", b"\xff", b"\x00|"],
+                   terminator=ord("|"), flags=flags)
+
+
+def test_tail_single_string(P):
+    """One string: the whole trie is one path, so no node branches (the table
+    keeps one unused row) and every row comes from a list."""
+    h, o = full_check(P, [b"medical_billing"], [b"med", b"ical", b"_", b"billing", b'"', b"g\"", b"x"], flags=8)
+    assert h.dense_rows == 0 and np.array_equal(-1 - h.dense_row, o.N - 1 - np.arange(o.N))
 
 
 # ------------------------------------------------------------ configurations --
@@ -145,11 +172,19 @@ def sample_nodes(o: Oracle, k: int, seed: int):
     return np.unique(pick).astype(np.int32)
 
 
-@pytest.fixture(scope="module", params=[1, 2, 3, 4], ids=["c1", "c2", "c3", "c4"])
+_oracles = {}
+
+
+@pytest.fixture(scope="module", params=[(1, 0), (2, 0), (3, 0), (4, 0), (1, 8), (2, 8), (3, 8), (4, 8)],
+                ids=["c1", "c2", "c3", "c4", "c1-tail", "c2-tail", "c3-tail", "c4-tail"])
 def compiled(request, P):
-    w = W.config(request.param)
-    o = Oracle(w.strings, w.vocab)
-    h = P.compile(w.strings, w.vocab)
+    cid, flags = request.param
+    w = W.config(cid)
+    if cid not in _oracles:
+        _oracles.clear()
+        _oracles[cid] = Oracle(w.strings, w.vocab)
+    o = _oracles[cid]
+    h = P.compile(w.strings, w.vocab, flags=flags)
     yield w, o, h
     h.close()
     torch.cuda.empty_cache()
@@ -165,16 +200,30 @@ def test_config_rows(P, compiled):
 
 def test_config_table_properties(P, compiled):
     """Whole-table facts at full size: with all 256 byte tokens in the vocabulary,
-    a row is empty exactly at final nodes, and padding words stay zero."""
+    a row is empty exactly at final nodes, and padding words stay zero.  With
+    tail compression the table holds exactly the branching nodes (none final),
+    and the lists and the table together count the full table's pairs."""
     w, o, h = compiled
-    table = h._alloc.live[h.table_ptr].view(torch.int64).view(h.num_nodes, h.row_stride_words)
-    nonempty = torch.zeros(h.num_nodes, dtype=torch.bool, device="cuda")
-    for i in range(0, h.num_nodes, 16384):
+    R = h.dense_rows
+    table = h._alloc.live[h.table_ptr].view(torch.int64)[: R * h.row_stride_words].view(R, h.row_stride_words)
+    nonempty = torch.zeros(R, dtype=torch.bool, device="cuda")
+    for i in range(0, R, 16384):
         blk = table[i:i + 16384]
         nonempty[i:i + 16384] = blk[:, : h.words_per_row].ne(0).any(dim=1)
         if h.row_stride_words > h.words_per_row:
             assert not blk[:, h.words_per_row:].ne(0).any().item()
-    assert np.array_equal(nonempty.cpu().numpy(), o.is_final == 0)
+    if h.dense_row is None:
+        assert R == o.N
+        assert np.array_equal(nonempty.cpu().numpy(), o.is_final == 0)
+    else:
+        branch = branching_nodes(o)
+        assert R == int(branch.sum()) and np.array_equal(h.dense_row >= 0, branch)
+        assert np.array_equal(h.dense_row[branch], np.arange(R))
+        assert nonempty.all().item()
+        if w.config_id >= 3:
+            hf = P.compile(w.strings, w.vocab)
+            assert h.valid_pairs() == hf.valid_pairs()
+            hf.close()
     if w.config_id <= 2:
         # total number of valid pairs against the oracle's full table
         M = 0
@@ -238,8 +287,15 @@ def test_config_rebuild_identical(P, compiled):
     h.rebuild(phases=P.PHASE_MARK)
     assert np.array_equal(gpu_rows(h, nodes), before)
     assert h.valid_pairs() == M
-    with pytest.raises(P.TamError):
-        h.rebuild(phases=P.PHASE_LISTS)  # lists are kept only without a dense table
+    if h.dense_row is None:
+        with pytest.raises(P.TamError):
+            h.rebuild(phases=P.PHASE_LISTS)  # lists are kept only without a full table
+    else:
+        h.rebuild(phases=P.PHASE_TABLE)
+        assert np.array_equal(gpu_rows(h, nodes), before)
+        assert h.valid_pairs() == M
+        with pytest.raises(P.TamError):
+            h.rebuild(phases=P.PHASE_LISTS)  # no token is longer than 16 bytes: tails need no lists
 
 
 def test_shared_vocabulary(P):
@@ -248,7 +304,7 @@ def test_shared_vocabulary(P):
     w = W.config(2)
     voc = P.Vocab(w.vocab)
     o = Oracle(w.strings, w.vocab)
-    h1 = P.compile(w.strings, voc)
+    h1 = P.compile(w.strings, voc, flags=P.FLAG_TAIL_LISTS)
     h2 = P.compile(w.strings[:300], voc, flags=P.FLAG_NO_TABLE)
     h3 = P.compile(w.strings, w.vocab)
     o2 = Oracle(w.strings[:300], w.vocab)
@@ -264,7 +320,7 @@ def test_shared_vocabulary(P):
         h.close()
 
 
-@pytest.mark.parametrize("flags", [0, 2], ids=["dense", "no_table"])
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
 def test_long_and_duplicate_tokens(P, flags):
     """Tokens longer than the 16-byte probe window and duplicate token strings,
     at scale: sampled rows, a decode loop and both apply dtypes."""
@@ -273,6 +329,9 @@ def test_long_and_duplicate_tokens(P, flags):
     h = P.compile(w.strings, w.vocab, flags=flags)
     assert h.max_token_len >= 17
     nodes = sample_nodes(o, 400, 77)
+    if flags == 8:  # rows of tails whose path is longer than the window
+        tails = np.flatnonzero(h.dense_row <= -18)
+        nodes = np.unique(np.concatenate([nodes, tails[:: max(1, len(tails) // 200)]])).astype(np.int32)
     for i in range(0, len(nodes), 256):
         assert np.array_equal(gpu_rows(h, nodes[i:i + 256]), o.mask_rows(nodes[i:i + 256]))
     rows = o.mask_rows(nodes)
@@ -280,10 +339,17 @@ def test_long_and_duplicate_tokens(P, flags):
     bits = np.unpackbits(rows.view(np.uint8), axis=1, bitorder="little")[:, : o.V]
     assert bits[:, long_ids].any(), "sample should contain valid long tokens"
     assert bits[:, 62000:].any(), "sample should contain valid duplicate tokens"
-    if flags == 0:  # the dense marks and the sparse lists count the same pairs
+    if flags != 2:  # the dense marks (and the tails' lists) and the sparse lists count the same pairs
         hs = P.compile(w.strings, w.vocab, flags=P.FLAG_NO_TABLE)
         assert h.valid_pairs() == hs.valid_pairs()
         hs.close()
+    if flags == 8:  # tokens longer than 16 bytes: the tails keep lists for them
+        M = h.valid_pairs()
+        before = gpu_rows(h, nodes[:256])
+        for ph in (P.PHASE_LISTS, P.PHASE_TABLE, P.PHASE_LISTS | P.PHASE_TABLE):
+            h.rebuild(phases=ph)
+            assert np.array_equal(gpu_rows(h, nodes[:256]), before)
+            assert h.valid_pairs() == M
     rng = np.random.default_rng(11)
     cur = W.uniform_nodes(7, o.N, 64)
     for step in range(12):
@@ -339,11 +405,12 @@ def test_forest_c5(P):
 
 # ------------------------------------------------------------ layouts / edges --
 
-def test_ragged_vocab_and_strides(P):
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+def test_ragged_vocab_and_strides(P, flags):
     w = W.config(1)
     vocab = w.vocab[:1037]                      # V not a multiple of 8 or 64
     o = Oracle(w.strings, vocab)
-    h = P.compile(w.strings, vocab)
+    h = P.compile(w.strings, vocab, flags=flags)
     nodes = np.array([0, 1, 5, o.N - 1, -1, o.N, 2 ** 30], dtype=np.int32)
     for dtype in ("fp32", "bf16"):
         check_apply(P, h, o, nodes, dtype, seed=1)                  # contiguous rows
@@ -362,17 +429,19 @@ def test_many_rows_grid_split(P):
     strings = [b"ab", b"b"]
     vocab = [b"a", b"b", b"ab", b'"', b'b"'] + [b"z"] * 123
     o = Oracle(strings, vocab)
-    h = P.compile(strings, vocab)
     B = 70000
     nodes = np.random.default_rng(0).integers(-1, o.N + 1, size=B).astype(np.int32)
     ids = torch.as_tensor(nodes, device="cuda")
-    x = torch.zeros((B, 128), dtype=torch.bfloat16, device="cuda")
-    h.apply_mask(ids, x)
     rows = o.mask_rows(np.arange(o.N, dtype=np.int32))
     valid = np.unpackbits(rows.view(np.uint8), axis=1, bitorder="little")[:, :128].astype(bool)
     exp = np.zeros((B, 128), dtype=bool)
     live = (nodes >= 0) & (nodes < o.N)
     exp[live] = valid[nodes[live]]
-    assert np.array_equal(~torch.isinf(x).cpu().numpy(), exp)
-    assert np.array_equal(gpu_rows(h, nodes[:66000]), np.where(
-        live[:66000, None], rows[np.clip(nodes[:66000], 0, o.N - 1)], np.uint64(0)))
+    for flags in FLAGS3:
+        h = P.compile(strings, vocab, flags=flags)
+        x = torch.zeros((B, 128), dtype=torch.bfloat16, device="cuda")
+        h.apply_mask(ids, x)
+        assert np.array_equal(~torch.isinf(x).cpu().numpy(), exp)
+        assert np.array_equal(gpu_rows(h, nodes[:66000]), np.where(
+            live[:66000, None], rows[np.clip(nodes[:66000], 0, o.N - 1)], np.uint64(0)))
+        h.close()
