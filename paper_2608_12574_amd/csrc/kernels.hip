@@ -32,6 +32,7 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
 constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
+constexpr int kProbeLanes = 4;       // lanes per node in k_probe (each takes 16 / 4 suffix lengths)
 // k_apply row sources: the dense table, the valid lists, or per row either
 // (tail compression: dense rows for branching nodes, lists for tails)
 constexpr int kApplyTable = 0, kApplyLists = 1, kApplyTail = 2;
@@ -164,63 +165,62 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
     }
 }
 
-// The hits (hit_of_slot, or -1) of the suffixes of length d <= Lw <= 16 of a
-// node's path, four lengths at a time: their bucket loads are issued together,
-// then their payload loads, so a node waits for about eight memory round trips
-// instead of sixteen dependent ones.  A length whose home bucket does not settle
-// it (a full bucket, or a second fingerprint match after a failed first) falls
-// back to the general probe.
-__device__ __forceinline__ void probe_window(const DevTables &t, int64_t pos, int Lw, uint64_t lo, uint64_t hi,
-                                             int32_t (&hit)[kWin]) {
+// The hits (hit_of_slot, or -1) of the suffixes of length d = d0+1 .. d0+kPer
+// (only d <= Lw <= 16 probed) of a node's path: their bucket loads are issued
+// together, then their payload loads, so a lane waits for two memory round
+// trips.  A length whose home bucket does not settle it (a full bucket, or a
+// second fingerprint match after a failed first) falls back to the general
+// probe.  The hash of the first d0 bytes is recomputed by the lane.
+template <int kPer>
+__device__ __forceinline__ void probe_lengths(const DevTables &t, int64_t pos, int Lw, int d0, uint64_t lo,
+                                              uint64_t hi, int32_t (&hit)[kPer]) {
     uint64_t h = kHashSeed;
+    for (int d = 1; d <= d0; ++d) h = hash_step(h, window_byte(lo, hi, d - 1));
+    uint64_t key[kPer];
+    bool act[kPer];
 #pragma unroll
-    for (int g = 0; g < kWin; g += 4) {
-        uint64_t key[4];
-        bool act[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d = g + j + 1;
-            hit[d - 1] = -1;
-            act[j] = false;
-            key[j] = 0;
-            if (d <= Lw) {
-                h = hash_step(h, window_byte(lo, hi, d - 1));
-                act[j] = has_len(t, d);
-                key[j] = hash_final(h, (uint32_t)d);
-            }
+    for (int j = 0; j < kPer; ++j) {
+        const int d = d0 + j + 1;
+        hit[j] = -1;
+        act[j] = false;
+        key[j] = 0;
+        if (d <= Lw) {
+            h = hash_step(h, window_byte(lo, hi, d - 1));
+            act[j] = has_len(t, d);
+            key[j] = hash_final(h, (uint32_t)d);
         }
-        Bucket bk[4];
+    }
+    Bucket bk[kPer];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (act[j]) bk[j] = load_bucket(t, home_bucket(t, key[j]));
-        uint32_t match[4], empty[4];
-        int32_t slot[4];
+    for (int j = 0; j < kPer; ++j)
+        if (act[j]) bk[j] = load_bucket(t, home_bucket(t, key[j]));
+    uint32_t match[kPer], empty[kPer];
+    int32_t slot[kPer];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            match[j] = empty[j] = 0;
-            slot[j] = -1;
-            if (act[j]) {
-                bucket_masks(bk[j], fingerprint(key[j]), &match[j], &empty[j]);
-                if (match[j]) slot[j] = (int32_t)(home_bucket(t, key[j]) * kBucket + (uint64_t)__builtin_ctz(match[j]));
-            }
+    for (int j = 0; j < kPer; ++j) {
+        match[j] = empty[j] = 0;
+        slot[j] = -1;
+        if (act[j]) {
+            bucket_masks(bk[j], fingerprint(key[j]), &match[j], &empty[j]);
+            if (match[j]) slot[j] = (int32_t)(home_bucket(t, key[j]) * kBucket + (uint64_t)__builtin_ctz(match[j]));
         }
-        SlotPay p[4];
+    }
+    SlotPay p[kPer];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (slot[j] >= 0) p[j] = t.pay[slot[j]];
+    for (int j = 0; j < kPer; ++j)
+        if (slot[j] >= 0) p[j] = t.pay[slot[j]];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d = g + j + 1;
-            if (!act[j]) continue;
-            if (slot[j] >= 0 && (int)p[j].len == d && same_head(lo, hi, p[j], d)) {
-                hit[d - 1] = hit_of_slot(slot[j], p[j].first, p[j].count);
-            } else if (empty[j] != 0 && (match[j] & (match[j] - 1)) == 0) {
-                hit[d - 1] = -1;  // the home bucket settles it: no such token
-            } else {
-                SlotPay mt;
-                const int32_t sl = probe(t, key[j], d, lo, hi, pos, &mt);
-                if (sl >= 0) hit[d - 1] = hit_of_slot(sl, mt.first, mt.count);
-            }
+    for (int j = 0; j < kPer; ++j) {
+        const int d = d0 + j + 1;
+        if (!act[j]) continue;
+        if (slot[j] >= 0 && (int)p[j].len == d && same_head(lo, hi, p[j], d)) {
+            hit[j] = hit_of_slot(slot[j], p[j].first, p[j].count);
+        } else if (empty[j] != 0 && (match[j] & (match[j] - 1)) == 0) {
+            hit[j] = -1;  // the home bucket settles it: no such token
+        } else {
+            SlotPay mt;
+            const int32_t sl = probe(t, key[j], d, lo, hi, pos, &mt);
+            if (sl >= 0) hit[j] = hit_of_slot(sl, mt.first, mt.count);
         }
     }
 }
@@ -270,21 +270,26 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
     return t.table ? 0 : INT_MAX;
 }
 
-// Probe pass: one lane per node m.  The suffix of length d of prefix(m) equal to
+// Probe pass: kProbeLanes lanes per node m, lane g taking the suffix lengths
+// d = g*kPer+1 .. (g+1)*kPer.  The suffix of length d of prefix(m) equal to
 // token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
 // d <= 16 the hit (hit_of_slot: the token id, or the slot of a string with
 // several ids, or -1) goes to hits[d-1][m]; the tails of tail compression read
 // their tokens back from there.  Longer tokens are probed again where needed
-// (long_hits).  All loads of a lane are issued before its first store or atomic
-// (loads, stores and atomics share one vector-memory counter here).
+// (long_hits, by the node's last lane).  All loads of a lane are issued before
+// its first store or atomic (loads, stores and atomics share one vector-memory
+// counter here).
 //   do_mark (a table): every hit whose ancestor has a dense row (row_at of its
 //     blob position; not a tail) is OR-ed into the zeroed table with a 64-bit
 //     atomic, and each block writes the number of valid (node, token) pairs its
 //     hits make, tails included, into pairs[blockIdx.x].
 //   kCount (lists): the listed hits are counted per node.
 template <bool kCount>
-__global__ void __launch_bounds__(kBlock, 4) k_probe(DevTables t, int do_mark, int32_t *__restrict__ pairs) {
-    const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+__global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int do_mark, int32_t *__restrict__ pairs) {
+    constexpr int kPer = kWin / kProbeLanes;
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t m = i / kProbeLanes;
+    const int d0 = (int)(i % kProbeLanes) * kPer;
     int32_t found = 0;
     const int64_t pos = m < t.N ? t.node_pos[m] : -1;  // a root ends no token
     if (pos >= 0) {
@@ -293,19 +298,6 @@ __global__ void __launch_bounds__(kBlock, 4) k_probe(DevTables t, int do_mark, i
         const int lspan = kCount ? list_span(t, m) : 0;              // listed up to here
         const int sspan = t.row_of ? 0 : lspan;                      // short hits listed up to here
         const int mspan = do_mark ? (t.tail_span ? t.tail_span[m] : 0) : INT_MAX;  // marked beyond
-        uint64_t lo, hi;
-        load_window(t.blob, pos, lo, hi);
-        int32_t hit[kWin];
-        probe_window(t, pos, Lw, lo, hi, hit);
-        int32_t n[kWin], r[kWin];
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d) {
-            n[d - 1] = kCount && hit[d - 1] != -1 && d <= sspan ? t.node_at[pos - d] : -1;
-            r[d - 1] = hit[d - 1] != -1 && d > mspan ? t.row_at[pos - d] : -1;
-        }
-#pragma unroll
-        for (int d = 1; d <= kWin; ++d)
-            if (d <= Lw) t.hits[(int64_t)(d - 1) * t.N + m] = hit[d - 1];
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
         // one hit: the pairs it makes (do_mark), marked at table row `row` (>= 0),
         // counted for list node `ln` (>= 0)
@@ -326,14 +318,27 @@ __global__ void __launch_bounds__(kBlock, 4) k_probe(DevTables t, int do_mark, i
                 v = t.dup_next[v];
             }
         };
+        if (d0 < Lw) {
+            uint64_t lo, hi;
+            load_window(t.blob, pos, lo, hi);
+            int32_t hit[kPer];
+            probe_lengths<kPer>(t, pos, Lw, d0, lo, hi, hit);
+            int32_t n[kPer], r[kPer];
 #pragma unroll
-        for (int d = 1; d <= kWin; ++d)
-            if (hit[d - 1] >= 0) take(hit[d - 1], r[d - 1], n[d - 1]);
+            for (int j = 0; j < kPer; ++j) {
+                const int d = d0 + j + 1;
+                n[j] = kCount && hit[j] != -1 && d <= sspan ? t.node_at[pos - d] : -1;
+                r[j] = hit[j] != -1 && d > mspan ? t.row_at[pos - d] : -1;
+            }
 #pragma unroll
-        for (int d = 1; d <= kWin; ++d)
-            if (hit[d - 1] <= -2) take(hit[d - 1], r[d - 1], n[d - 1]);
-        // tokens longer than the window (rare)
-        if (L > kWin && (do_mark || lspan > kWin))
+            for (int j = 0; j < kPer; ++j)
+                if (d0 + j + 1 <= Lw) t.hits[(int64_t)(d0 + j) * t.N + m] = hit[j];
+#pragma unroll
+            for (int j = 0; j < kPer; ++j)
+                if (hit[j] != -1) take(hit[j], r[j], n[j]);
+        }
+        // tokens longer than the window (rare), by the node's last lane
+        if (d0 + kPer == kWin && L > kWin && (do_mark || lspan > kWin))
             long_hits(t, pos, L, [&](int32_t hx, int d) {
                 take(hx, d > mspan ? t.row_at[pos - d] : -1, d <= lspan ? t.node_at[pos - d] : -1);
             });
@@ -880,10 +885,11 @@ hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s) 
 hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pairs, hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
     const int do_mark = mark && t.table ? 1 : 0;
+    const dim3 grid((unsigned)mark_blocks(t.N));
     if (count)
-        hipLaunchKernelGGL(k_probe<true>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<true>, grid, dim3(kBlock), 0, s, t, do_mark, pairs);
     else
-        hipLaunchKernelGGL(k_probe<false>, dim3(grid_for(t.N, kBlock)), dim3(kBlock), 0, s, t, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<false>, grid, dim3(kBlock), 0, s, t, do_mark, pairs);
     return hipGetLastError();
 }
 
@@ -901,7 +907,7 @@ hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s) {
     return hipGetLastError();
 }
 
-int64_t mark_blocks(int64_t N) { return (N + kBlock - 1) / kBlock; }
+int64_t mark_blocks(int64_t N) { return (N * kProbeLanes + kBlock - 1) / kBlock; }
 
 hipError_t launch_scan(const DevTables &t, hipStream_t s) {
     const int64_t nb = grid_for(t.N, kScanTile);
