@@ -29,7 +29,8 @@ struct TerminatedLess {
     }
 };
 
-// The trie of one set, with set-local node ids (root = 0) and blob offsets.
+// The trie of one bucket of strings (all of one set, all with the same first
+// byte of s+T), with bucket-local node ids (root = 0) and blob offsets.
 struct SetTrie {
     std::vector<int32_t> parent, depth, node_pos, node_at, child_off, child_node;
     std::vector<uint8_t> edge, is_final, blob, child_byte;
@@ -38,20 +39,41 @@ struct SetTrie {
     std::string err;
 };
 
+// The first 8 bytes of s+T, big-endian and zero-padded: terminated strings are
+// prefix-free (T occurs only at their end), so two of them with different keys
+// are ordered by their keys, and equal keys leave the order to the full compare.
+uint64_t order_key(const uint8_t *s, int64_t len, uint8_t term) {
+    uint64_t k = 0;
+    for (int i = 0; i < 8; ++i) {
+        const uint64_t c = i < len ? s[i] : (i == len ? term : 0);
+        k = (k << 8) | c;
+    }
+    return k;
+}
+
 /*
- * Trie construction of one set (Section 4.1: insert every value one byte at a
- * time, shared prefixes merge).  Inserting the distinct terminated strings in
+ * Trie construction of one bucket (Section 4.1: insert every value one byte at
+ * a time, shared prefixes merge).  Inserting the distinct terminated strings in
  * sorted order creates the new nodes of each string right after its longest
  * common prefix with the previous string, and that creation order is exactly
  * the lexicographic preorder the interface fixes.  O(N_chars) after the sort.
  * Blob layout per string: one pad byte standing for the root, the string, T.
  */
-void build_one_set(const uint8_t *sb, const int64_t *so, int64_t k0, int64_t k1, uint8_t term, SetTrie &r) {
-    std::vector<int64_t> order((size_t)(k1 - k0));
-    std::iota(order.begin(), order.end(), k0);
-    std::sort(order.begin(), order.end(), TerminatedLess{sb, so, term});
-    const int64_t chars = so[k1] - so[k0];
-    const size_t est = (size_t)(chars + 2 * (k1 - k0) + 1);
+void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t count, uint8_t term,
+                  SetTrie &r) {
+    std::vector<std::pair<uint64_t, int64_t>> order((size_t)count);
+    int64_t chars = 0;
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t k = idx[i];
+        order[(size_t)i] = {order_key(sb + so[k], so[k + 1] - so[k], term), k};
+        chars += so[k + 1] - so[k];
+    }
+    const TerminatedLess less{sb, so, term};
+    std::sort(order.begin(), order.end(), [&](const std::pair<uint64_t, int64_t> &a,
+                                              const std::pair<uint64_t, int64_t> &b) {
+        return a.first != b.first ? a.first < b.first : less(a.second, b.second);
+    });
+    const size_t est = (size_t)(chars + 2 * count + 1);
     r.parent.reserve(est);
     r.depth.reserve(est);
     r.edge.reserve(est);
@@ -68,7 +90,8 @@ void build_one_set(const uint8_t *sb, const int64_t *so, int64_t k0, int64_t k1,
     std::vector<int32_t> path;
     const uint8_t *prev = nullptr;
     int64_t prev_len = -1;
-    for (int64_t k : order) {
+    for (const auto &kv : order) {
+        const int64_t k = kv.second;
         const uint8_t *s = sb + so[k];
         const int64_t len = so[k + 1] - so[k];
         int64_t l = 0;
@@ -144,11 +167,16 @@ int host_threads(int64_t work_items) {
 }  // namespace
 
 /*
- * Tries of all sets: each set is built on its own (in parallel over host
- * threads for a forest), then the sets are laid out one after another: set j
- * takes node ids [roots[j], roots[j] + N_j) and its own range of the blob,
- * which carries kBlobPad zero bytes in front and behind so that 16-byte
- * window loads around any node never leave it.
+ * Tries of all sets.  A set's trie is its root plus one subtrie per distinct
+ * first byte of s+T, and in preorder those subtries follow one another in byte
+ * order.  The unit of host work is a part: a whole set, or (for a large set)
+ * the strings of one first byte; parts are built on their own, in parallel over
+ * host threads, and laid out one after another with the part roots merged into
+ * their set's root.  Set j takes node ids [roots[j], roots[j] + N_j) and its
+ * own range of the blob, which carries kBlobPad zero bytes in front and behind
+ * so that 16-byte window loads around any node never leave it.  Edges: a set's
+ * root lists its first-byte children (those of its parts, in order), then the
+ * parts' other child lists follow in node order.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err) {
@@ -163,33 +191,88 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             return TAM_E_TERMINATOR;
         }
     }
-    std::vector<SetTrie> sets((size_t)S);
+    // parts: a set whole, or a large set cut by the first byte of s+T (its
+    // strings grouped by that byte, in byte order)
+    const int threads = host_threads(K);
+    const int64_t split_at = std::max<int64_t>(1024, K / (2 * (int64_t)threads));
+    std::vector<int64_t> idx((size_t)K);
+    std::vector<int64_t> pstart;  // part p holds idx[pstart[p] .. pstart[p+1])
+    std::vector<int64_t> pset;    // set of part p
+    std::vector<int64_t> set_first((size_t)S + 1, 0);  // first part of each set
+    {
+        std::vector<int64_t> cnt(256), pos(256);
+        for (int64_t j = 0; j < S; ++j) {
+            set_first[(size_t)j] = (int64_t)pset.size();
+            const int64_t k0 = set_off[j], k1 = set_off[j + 1];
+            if (k1 - k0 < split_at) {
+                for (int64_t k = k0; k < k1; ++k) idx[(size_t)k] = k;
+                pstart.push_back(k0);
+                pset.push_back(j);
+                continue;
+            }
+            std::fill(cnt.begin(), cnt.end(), 0);
+            for (int64_t k = k0; k < k1; ++k) ++cnt[so[k + 1] > so[k] ? sb[so[k]] : term];
+            int64_t at = k0;
+            for (int c = 0; c < 256; ++c) {
+                pos[(size_t)c] = at;
+                if (cnt[(size_t)c]) {
+                    pstart.push_back(at);
+                    pset.push_back(j);
+                }
+                at += cnt[(size_t)c];
+            }
+            for (int64_t k = k0; k < k1; ++k) idx[(size_t)pos[so[k + 1] > so[k] ? sb[so[k]] : term]++] = k;
+        }
+        set_first[(size_t)S] = (int64_t)pset.size();
+        pstart.push_back(K);
+    }
+    const int64_t NP = (int64_t)pset.size();
+    std::vector<SetTrie> parts((size_t)NP);
     std::atomic<bool> oom{false};
-    parallel_for(S, host_threads(S), [&](int64_t j) {
+    parallel_for(NP, host_threads(NP), [&](int64_t p) {
         try {
-            build_one_set(sb, so, set_off[j], set_off[j + 1], term, sets[(size_t)j]);
+            build_bucket(sb, so, idx.data() + pstart[(size_t)p], pstart[(size_t)p + 1] - pstart[(size_t)p], term,
+                         parts[(size_t)p]);
         } catch (const std::bad_alloc &) {
             oom = true;
         }
     });
     if (oom) throw std::bad_alloc();
-    std::vector<int64_t> nbase((size_t)S + 1, 0), bbase((size_t)S + 1, kBlobPad), ebase((size_t)S + 1, 0);
+    // bases: node ids (a part's local root is its set's root, the rest follow),
+    // blob offsets, edges (a set's root edges first)
+    std::vector<int64_t> nbase((size_t)NP), bbase((size_t)NP), ebase((size_t)NP), rbase((size_t)NP);
+    std::vector<int64_t> root((size_t)S), root_edges((size_t)S);
+    int64_t N = 0, BB = kBlobPad, E = 0;
     h->K_unique = 0;
     for (int64_t j = 0; j < S; ++j) {
-        const SetTrie &r = sets[(size_t)j];
-        if (r.st != TAM_OK) {
-            *err = r.err;
-            return r.st;
+        root[(size_t)j] = N++;
+        root_edges[(size_t)j] = E;
+        for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
+            const SetTrie &r = parts[(size_t)p];
+            if (r.st != TAM_OK) {
+                *err = r.err;
+                return r.st;
+            }
+            rbase[(size_t)p] = E;
+            E += r.child_off[1];  // the part root's children become the set root's
         }
-        nbase[(size_t)j + 1] = nbase[(size_t)j] + (int64_t)r.parent.size();
-        bbase[(size_t)j + 1] = bbase[(size_t)j] + (int64_t)r.blob.size();
-        ebase[(size_t)j + 1] = ebase[(size_t)j] + (int64_t)r.child_node.size();
-        h->K_unique += r.K_unique;
+        for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
+            const SetTrie &r = parts[(size_t)p];
+            nbase[(size_t)p] = N - 1;                // local id i >= 1 -> N - 1 + i
+            bbase[(size_t)p] = BB;
+            ebase[(size_t)p] = E - r.child_off[1];  // local edge e past the root's -> E - nr + e
+            N += (int64_t)r.parent.size() - 1;
+            BB += (int64_t)r.blob.size();
+            E += (int64_t)r.child_node.size() - r.child_off[1];
+            h->K_unique += r.K_unique;
+            if (N >= INT32_MAX || BB >= INT32_MAX) {
+                *err = "trie exceeds 2^31-1 nodes or string bytes";
+                return TAM_E_TOOLARGE;
+            }
+        }
     }
-    const int64_t N = nbase[(size_t)S];
-    const int64_t BB = bbase[(size_t)S] + kBlobPad;
-    const int64_t E = ebase[(size_t)S];
-    if (N >= INT32_MAX || BB >= INT32_MAX) {
+    BB += kBlobPad;
+    if (BB >= INT32_MAX) {
         *err = "trie exceeds 2^31-1 nodes or string bytes";
         return TAM_E_TOOLARGE;
     }
@@ -207,23 +290,42 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->child_byte.assign((size_t)std::max<int64_t>(E, 1), 0);
     h->blob.assign((size_t)BB, 0);
     h->node_at.assign((size_t)BB, 0);
-    parallel_for(S, host_threads(S), [&](int64_t j) {
-        const SetTrie &r = sets[(size_t)j];
-        const int32_t nb = (int32_t)nbase[(size_t)j], bb = (int32_t)bbase[(size_t)j], eb = (int32_t)ebase[(size_t)j];
+    for (int64_t j = 0; j < S; ++j) {
+        const int64_t rt = root[(size_t)j];
+        h->roots[(size_t)j] = (int32_t)rt;
+        h->parent[(size_t)rt] = -1;
+        h->depth[(size_t)rt] = 0;
+        h->edge[(size_t)rt] = 0;
+        h->is_final[(size_t)rt] = 0;
+        h->node_pos[(size_t)rt] = -1;
+        h->child_off[(size_t)rt] = (int32_t)root_edges[(size_t)j];
+    }
+    parallel_for(NP, host_threads(NP), [&](int64_t p) {
+        const SetTrie &r = parts[(size_t)p];
+        const int32_t rt = (int32_t)root[(size_t)pset[(size_t)p]];
+        const int64_t nb = nbase[(size_t)p], bb = bbase[(size_t)p], eb = ebase[(size_t)p], rb = rbase[(size_t)p];
+        const int32_t nr = r.child_off[1];
         const size_t n = r.parent.size();
-        h->roots[(size_t)j] = nb;
-        for (size_t i = 0; i < n; ++i) {
-            h->parent[nb + i] = r.parent[i] < 0 ? -1 : r.parent[i] + nb;
-            h->node_pos[nb + i] = r.node_pos[i] < 0 ? -1 : r.node_pos[i] + bb;
-            h->child_off[nb + i] = r.child_off[i] + eb;
+        auto gid = [&](int32_t local) { return local == 0 ? rt : (int32_t)(nb + local); };
+        for (size_t i = 1; i < n; ++i) {
+            const size_t g = (size_t)(nb + (int64_t)i);
+            h->parent[g] = gid(r.parent[i]);
+            h->node_pos[g] = (int32_t)(r.node_pos[i] + bb);
+            h->child_off[g] = (int32_t)(r.child_off[i] + eb);
+            h->depth[g] = r.depth[i];
+            h->edge[g] = r.edge[i];
+            h->is_final[g] = r.is_final[i];
         }
-        std::copy(r.depth.begin(), r.depth.end(), h->depth.begin() + nb);
-        std::copy(r.edge.begin(), r.edge.end(), h->edge.begin() + nb);
-        std::copy(r.is_final.begin(), r.is_final.end(), h->is_final.begin() + nb);
         std::copy(r.blob.begin(), r.blob.end(), h->blob.begin() + bb);
-        for (size_t i = 0; i < r.node_at.size(); ++i) h->node_at[bb + i] = r.node_at[i] + nb;
-        for (size_t i = 0; i < r.child_node.size(); ++i) h->child_node[eb + i] = r.child_node[i] + nb;
-        std::copy(r.child_byte.begin(), r.child_byte.end(), h->child_byte.begin() + eb);
+        for (size_t i = 0; i < r.node_at.size(); ++i) h->node_at[(size_t)bb + i] = gid(r.node_at[i]);
+        for (int32_t e = 0; e < nr; ++e) {  // the part root's children, on the set root
+            h->child_node[(size_t)(rb + e)] = gid(r.child_node[(size_t)e]);
+            h->child_byte[(size_t)(rb + e)] = r.child_byte[(size_t)e];
+        }
+        for (size_t e = (size_t)nr; e < r.child_node.size(); ++e) {
+            h->child_node[(size_t)(eb + (int64_t)e)] = gid(r.child_node[e]);
+            h->child_byte[(size_t)(eb + (int64_t)e)] = r.child_byte[e];
+        }
     });
     h->child_off[(size_t)N] = (int32_t)E;
     return TAM_OK;
@@ -357,35 +459,82 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
  * = depth(m) - depth(highest tail ancestor-or-self of m), and 0 when m itself
  * branches.  Every parent precedes its children: one backward pass counts the
  * finals below each node (and the path lengths below tails), one forward pass
- * finds the highest tail on each path.
+ * finds the highest tail on each path.  Both run in parallel over the subtrees
+ * of the roots' children (consecutive id ranges); the roots are done apart.
  */
 void split_tails(tam_handle *h) {
-    const int64_t N = h->N;
-    std::vector<int32_t> finals(h->is_final.begin(), h->is_final.end());
-    for (int64_t n = N - 1; n > 0; --n) {
-        const int32_t p = h->parent[(size_t)n];
-        if (p >= 0) finals[(size_t)p] += finals[(size_t)n];
+    const int64_t N = h->N, S = h->S;
+    // ranges: the subtree of each root child, in id order
+    std::vector<int64_t> lo, hi;
+    for (int64_t j = 0; j < S; ++j) {
+        const int32_t r = h->roots[(size_t)j];
+        const int64_t end = j + 1 < S ? h->roots[(size_t)j + 1] : N;
+        for (int32_t e = h->child_off[(size_t)r]; e < h->child_off[(size_t)r + 1]; ++e) {
+            lo.push_back(h->child_node[(size_t)e]);
+            hi.push_back(e + 1 < h->child_off[(size_t)r + 1] ? h->child_node[(size_t)e + 1] : end);
+        }
     }
+    const int64_t R = (int64_t)lo.size();
+    const int threads = host_threads(R);
+    std::vector<int32_t> finals(h->is_final.begin(), h->is_final.end());
     std::vector<int32_t> rem((size_t)N, 0);  // nodes below a tail (its single child is n+1)
-    for (int64_t n = N - 1; n >= 0; --n)
+    std::vector<int64_t> branching((size_t)R, 0);
+    auto backward = [&](int64_t n) {  // finals[n] is complete: all descendants are done
         if (finals[(size_t)n] == 1 && !h->is_final[(size_t)n]) rem[(size_t)n] = rem[(size_t)n + 1] + 1;
+    };
+    parallel_for(R, threads, [&](int64_t i) {
+        int64_t b = 0;
+        for (int64_t n = hi[(size_t)i] - 1; n >= lo[(size_t)i]; --n) {
+            backward(n);
+            b += finals[(size_t)n] >= 2;
+            if (n > lo[(size_t)i]) finals[(size_t)h->parent[(size_t)n]] += finals[(size_t)n];
+        }
+        branching[(size_t)i] = b;
+    });
+    // the roots, then the dense row numbering in id order (a root, its ranges, ...)
+    std::vector<int64_t> first_row((size_t)R, 0);
+    std::vector<int32_t> top((size_t)N, -1);  // depth of the highest tail ancestor-or-self
     h->tail_span.assign((size_t)N, 0);
     h->row_of.assign((size_t)N, -1);
-    std::vector<int32_t> top((size_t)N, -1);  // depth of the highest tail ancestor-or-self
-    int32_t rows = 0;
-    for (int64_t n = 0; n < N; ++n) {
-        if (finals[(size_t)n] >= 2) {
-            h->row_of[(size_t)n] = rows++;
-            continue;
+    int64_t rows = 0, i = 0;
+    for (int64_t j = 0; j < S; ++j) {
+        const int32_t r = h->roots[(size_t)j];
+        const int64_t i0 = i;
+        for (int32_t e = h->child_off[(size_t)r]; e < h->child_off[(size_t)r + 1]; ++e, ++i)
+            finals[(size_t)r] += finals[(size_t)lo[(size_t)i]];
+        backward(r);
+        if (finals[(size_t)r] >= 2) {
+            h->row_of[(size_t)r] = (int32_t)rows++;
+        } else {
+            top[(size_t)r] = 0;
+            h->row_of[(size_t)r] = -1 - rem[(size_t)r];
         }
-        const int32_t p = h->parent[(size_t)n];
-        top[(size_t)n] = (p >= 0 && top[(size_t)p] >= 0) ? top[(size_t)p] : h->depth[(size_t)n];
-        h->tail_span[(size_t)n] = h->depth[(size_t)n] - top[(size_t)n];
-        h->row_of[(size_t)n] = -1 - rem[(size_t)n];
+        for (int64_t k = i0; k < i; ++k) {
+            first_row[(size_t)k] = rows;
+            rows += branching[(size_t)k];
+        }
     }
     h->dense_rows = rows;
-    h->row_at.resize(h->node_at.size());
-    for (size_t p = 0; p < h->node_at.size(); ++p) h->row_at[p] = h->row_of[(size_t)h->node_at[p]];
+    parallel_for(R, threads, [&](int64_t k) {
+        int32_t row = (int32_t)first_row[(size_t)k];
+        for (int64_t n = lo[(size_t)k]; n < hi[(size_t)k]; ++n) {
+            if (finals[(size_t)n] >= 2) {
+                h->row_of[(size_t)n] = row++;
+                continue;
+            }
+            const int32_t p = h->parent[(size_t)n];
+            top[(size_t)n] = top[(size_t)p] >= 0 ? top[(size_t)p] : h->depth[(size_t)n];
+            h->tail_span[(size_t)n] = h->depth[(size_t)n] - top[(size_t)n];
+            h->row_of[(size_t)n] = -1 - rem[(size_t)n];
+        }
+    });
+    const int64_t B = (int64_t)h->node_at.size();
+    h->row_at.resize((size_t)B);
+    const int64_t chunk = 1 << 16;
+    parallel_for((B + chunk - 1) / chunk, host_threads((B + chunk - 1) / chunk), [&](int64_t c) {
+        for (int64_t p = c * chunk; p < std::min(B, (c + 1) * chunk); ++p)
+            h->row_at[(size_t)p] = h->row_of[(size_t)h->node_at[(size_t)p]];
+    });
 }
 
 }  // namespace tam

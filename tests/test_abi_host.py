@@ -222,3 +222,11 @@ def test_tail_split_forest_host_only(P, oracle_mod):
     o = oracle_mod.Oracle(flat, vocab, set_offsets=offs)
     h = P.compile(flat, vocab, sets=offs, flags=P.FLAG_HOST_ONLY | P.FLAG_TAIL_LISTS)
     assert np.array_equal(h.dense_row >= 0, _branching(o))
+
+
+def test_host_trie_forest_with_large_set(P):
+    """A large set (built in parts cut by first byte) among small ones."""
+    strings, vocab, offs = W.mixed_forest()
+    h = host(P, strings, vocab, sets=offs)
+    same_trie(h, Oracle(strings, [b"x"], set_offsets=offs))
+    assert h.num_strings == sum(len(set(strings[offs[j]:offs[j + 1]])) for j in range(len(offs) - 1))

@@ -403,6 +403,31 @@ def test_forest_c5(P):
     h.close()
 
 
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+def test_forest_with_large_set(P, flags):
+    """A large set (its host trie built in parts cut by first byte, with the
+    empty string and strings that prefix others) among small sets: sampled
+    rows, every root's row, and a decode loop in every set."""
+    strings, vocab, offs = W.mixed_forest()
+    o = Oracle(strings, vocab, set_offsets=offs)
+    h = P.compile(strings, vocab, sets=offs, flags=flags)
+    assert h.num_nodes == o.N and np.array_equal(h.roots, o.roots)
+    nodes = np.unique(np.concatenate([sample_nodes(o, 300, 81), o.roots])).astype(np.int32)
+    assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+    rng = np.random.default_rng(82)
+    start = np.repeat(o.roots, 16).astype(np.int32)
+    cur = start.copy()
+    for step in range(10):
+        rows = o.mask_rows(cur)
+        assert np.array_equal(gpu_rows(h, cur), rows)
+        toks = W.choose_valid_tokens(rng, rows, o.V)
+        exp = o.advance(cur, toks)
+        assert np.array_equal(gpu_advance(h, cur, toks), exp)
+        cur = np.where((exp < 0) | (o.is_final[np.maximum(exp, 0)] == 1), start, exp).astype(np.int32)
+    check_apply(P, h, o, cur, "bf16", seed=83)
+    h.close()
+
+
 # ------------------------------------------------------------ layouts / edges --
 
 @pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)

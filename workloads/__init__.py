@@ -387,3 +387,18 @@ def stress_case() -> Workload:
     return Workload(7, "stress", strings, vocab, None, 64, "bf16", 16, "uniform",
                     "3,000 code-like strings; 60,000 c4 tokens + 2,000 tokens of 17-48 bytes + 1,500 "
                     "duplicate tokens")
+
+
+def mixed_forest():
+    """A forest of one large set (over 1,024 strings, so the host cuts it by
+    first byte), holding the empty string and strings that prefix others, and
+    small sets, over the c1 vocabulary."""
+    w = config(1)
+    rng = rng_for(8, ROLE_SET)
+    lex = make_lexicon(rng_for(8, ROLE_LEXICON), 300)
+    big = word_strings(rng, lex, zipf_probs(len(lex)), 1500, 1, 3)
+    big = [b""] + big + [s[:3] for s in big[:50]]
+    small = [word_strings(rng, lex, zipf_probs(len(lex)), k, 1, 2) for k in (1, 7, 40)]
+    sets = [small[0], big, small[1], small[2]]
+    offs = np.cumsum([0] + [len(s) for s in sets])
+    return [s for g in sets for s in g], w.vocab, offs
