@@ -60,6 +60,10 @@ def lib():
         L.oracle_advance.restype = ctypes.c_int
         L.oracle_apply.argtypes = [P, P, P, i64, P, i64, P, i64, ctypes.c_int]
         L.oracle_apply.restype = ctypes.c_int
+        L.oracle_format_rows.argtypes = [P, i64, ctypes.c_int, P, P, i64, P, i64, P]
+        L.oracle_format_rows.restype = ctypes.c_int
+        L.oracle_format_advance.argtypes = [P, i64, ctypes.c_int, P, P, i64, P, P, i64, P]
+        L.oracle_format_advance.restype = ctypes.c_int
         L.oracle_last_error.restype = ctypes.c_char_p
         _lib = L
     return _lib
@@ -151,3 +155,44 @@ class Oracle:
         row = self.mask_rows([node])[0]
         bits = np.unpackbits(row.view(np.uint8), bitorder="little")[: self.V]
         return np.flatnonzero(bits)
+
+
+def class_rows(classes) -> np.ndarray:
+    """list of L byte strings (the allowed bytes of each position) -> [L, 32] uint8
+    bit rows: byte c allowed at position p iff bit c & 7 of row[p][c >> 3]."""
+    rows = np.zeros((max(len(classes), 1), 32), dtype=np.uint8)
+    for p, allowed in enumerate(classes):
+        for c in bytes(allowed):
+            rows[p, c >> 3] |= np.uint8(1 << (c & 7))
+    return rows
+
+
+class Format:
+    """Character-position masks of a fixed-format value (appendix "Constraint-Aware
+    Dispatch Beyond Finite Sets"): positions 0..L, then L+1 after the terminator."""
+
+    def __init__(self, classes, vocab, terminator=0x22):
+        lib()
+        self.L = len(classes)
+        self.N = self.L + 2
+        self.T = terminator
+        self._cls = class_rows(classes)
+        self._tb, self._to = csr(list(vocab))
+        self.V = len(vocab)
+        self.W = (self.V + 63) // 64
+
+    def mask_rows(self, pos) -> np.ndarray:
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        out = np.zeros((pos.size, self.W), dtype=np.uint64)
+        rc = lib().oracle_format_rows(_p(self._cls), self.L, self.T, _p(self._tb), _p(self._to), self.V,
+                                      _p(pos), pos.size, _p(out))
+        assert rc == 0
+        return out
+
+    def advance(self, pos, tokens) -> np.ndarray:
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        out = np.zeros(pos.size, dtype=np.int32)
+        lib().oracle_format_advance(_p(self._cls), self.L, self.T, _p(self._tb), _p(self._to), self.V,
+                                    _p(pos), _p(tokens), pos.size, _p(out))
+        return out

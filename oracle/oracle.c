@@ -395,3 +395,61 @@ int oracle_apply(const oracle *o, const uint8_t *tok_bytes, const int64_t *tok_o
     }
     return OR_OK;
 }
+
+/* ------------------------------------------------- fixed-format strings --- */
+
+/*
+ * Character-position masks (appendix "Constraint-Aware Dispatch Beyond Finite
+ * Sets"): a value of a fixed format has L characters, and character p may be
+ * any byte of the class C_p; the value is then closed by the terminator T, as
+ * the set strings are.  The states are the positions 0..L (p characters
+ * written) and L+1 (after T, final).  Token v is valid at position p iff it is
+ * non-empty, p + |t| <= L + 1, and every t[i] lies in C_{p+i}, with C_L = {T};
+ * the advance moves to p + |t|, or to the dead state.  A position outside
+ * 0..L+1 is dead.
+ *
+ * classes: L rows of 32 bytes; byte c is in C_p iff bit (c & 7) of
+ * classes[32 p + (c >> 3)] is set.
+ */
+static int fmt_valid(const uint8_t *classes, int64_t L, int T, int64_t p, const uint8_t *t, int64_t len) {
+    if (len <= 0 || p < 0 || p + len > L + 1) return 0;
+    for (int64_t i = 0; i < len; i++) {
+        const int64_t q = p + i;
+        const uint8_t c = t[i];
+        if (q == L) {
+            if (c != (uint8_t)T) return 0;
+        } else if (!((classes[q * 32 + (c >> 3)] >> (c & 7)) & 1)) {
+            return 0;
+        }
+    }
+    return 1;
+}
+
+/* Mask rows of the requested positions, one token at a time. */
+int oracle_format_rows(const uint8_t *classes, int64_t L, int T, const uint8_t *tok_bytes,
+                       const int64_t *tok_off, int64_t V, const int32_t *pos, int64_t n, uint64_t *out) {
+    if (V <= 0 || L < 0 || !tok_off || !pos || !out) return OR_E_INVAL;
+    int64_t W = (V + 63) / 64;
+    for (int64_t r = 0; r < n; r++) {
+        uint64_t *row = out + r * W;
+        memset(row, 0, (size_t)W * sizeof(uint64_t));
+        for (int64_t v = 0; v < V; v++)
+            if (fmt_valid(classes, L, T, pos[r], tok_bytes + tok_off[v], tok_off[v + 1] - tok_off[v]))
+                row[v >> 6] |= (uint64_t)1 << (v & 63);
+    }
+    return OR_OK;
+}
+
+/* Advance: out[b] = pos[b] + |t| when token tokens[b] is valid there, else -1. */
+int oracle_format_advance(const uint8_t *classes, int64_t L, int T, const uint8_t *tok_bytes,
+                          const int64_t *tok_off, int64_t V, const int32_t *pos, const int32_t *tokens,
+                          int64_t B, int32_t *out) {
+    for (int64_t b = 0; b < B; b++) {
+        const int64_t v = tokens[b];
+        out[b] = -1;
+        if (v < 0 || v >= V) continue;
+        const int64_t len = tok_off[v + 1] - tok_off[v];
+        if (fmt_valid(classes, L, T, pos[b], tok_bytes + tok_off[v], len)) out[b] = (int32_t)(pos[b] + len);
+    }
+    return OR_OK;
+}

@@ -259,3 +259,76 @@ def test_apply_matches_torch_where(oracle_mod, dtype):
         ref = torch.where(torch.from_numpy(full), x[b], torch.tensor(float("-inf"), dtype=x.dtype))
         ref_bits = ref.view(torch.int16 if dtype == "bf16" else torch.int32).numpy()
         assert np.array_equal(got[b].view(ref_bits.dtype), ref_bits)
+
+
+# ------------------------------------------------------ fixed-format strings --
+# Character-position masks (appendix "Constraint-Aware Dispatch Beyond Finite
+# Sets").  A fixed format with small classes is also a finite set (every string
+# the format admits), whose trie the set oracle builds on its own; every trie
+# node at depth p has the same continuations, so its row must equal the format's
+# row at position p, and its advance the format's advance.
+
+def _format_set(classes):
+    return [bytes(t) for t in itertools.product(*[list(c) for c in classes])]
+
+
+TINY_FORMATS = [
+    [b"ab"],
+    [b"ab", b"01"],
+    [b"a", b"-", b"01"],
+    [b"ab", b"ab", b"ab"],
+    [b"0123", b"ab", b"x"],
+]
+
+
+@pytest.mark.parametrize("classes", TINY_FORMATS, ids=["-".join(c.decode() for c in f) for f in TINY_FORMATS])
+def test_format_equals_trie_of_enumerated_set(oracle_mod, classes):
+    alphabet = sorted(set(b"".join(classes)) | {ord('"'), ord("z")})
+    vocab = [b""] + [bytes(t) for n in (1, 2, 3) for t in itertools.product(alphabet, repeat=n)]
+    f = oracle_mod.Format(classes, vocab)
+    strings = _format_set(classes)
+    o = Oracle(strings, vocab)
+    b = Brute(strings, vocab)
+    L = len(classes)
+    assert f.N == L + 2
+    frows = f.mask_rows(np.arange(L + 2))
+    trows = o.mask_rows(np.arange(o.N))
+    toks = np.arange(len(vocab), dtype=np.int32)
+    for n in range(o.N):
+        p = int(o.depth[n])
+        assert np.array_equal(trows[n], frows[p]), (n, p)
+        assert rowset(frows[p], len(vocab)) == b.valid_set(n)
+        fa = f.advance(np.full(len(vocab), p), toks)
+        ta = o.advance(np.full(len(vocab), n), toks)
+        assert np.array_equal(fa < 0, ta < 0)
+        assert np.array_equal(fa[fa >= 0], o.depth[ta[ta >= 0]])
+    # outside 0..L+1: dead, empty rows
+    assert not f.mask_rows([-1, L + 2, 10 ** 6]).any()
+    assert (f.advance([-1, L + 2], [1, 1]) == -1).all()
+
+
+def test_format_closed_form_digits(oracle_mod):
+    """L digit positions and a vocabulary of digit strings, with and without a
+    closing quote: at position p the valid tokens are the digit strings of length
+    <= L - p and the digit strings + '"' of length exactly L + 1 - p."""
+    L = 6
+    digits = b"0123456789"
+    rng = np.random.default_rng(3)
+    vocab = []
+    for _ in range(400):
+        n = int(rng.integers(1, 9))
+        s = bytes(rng.choice(list(digits), size=n).tolist())
+        vocab.append(s + b'"' if rng.random() < 0.3 else s)
+    vocab += [b"1a", b"a1", b'"', b'""', b""]
+    f = oracle_mod.Format([digits] * L, vocab)
+    rows = f.mask_rows(np.arange(L + 2))
+    for p in range(L + 2):
+        exp = set()
+        for v, t in enumerate(vocab):
+            body, closed = (t[:-1], True) if t.endswith(b'"') else (t, False)
+            if not t or not all(c in digits for c in body) or b'"' in body:
+                continue
+            if (not closed and 1 <= len(t) <= L - p) or (closed and len(t) == L + 1 - p):
+                exp.add(v)
+        assert rowset(rows[p], len(vocab)) == exp, p
+    assert not rowset(rows[L + 1], len(vocab))
