@@ -374,6 +374,34 @@ def main():
         cpu, exact = cpu_baseline(h, w, V, main_res["N"], args.cpu_seconds, torch, dev)
     h.close()
 
+    # character-position masks of fixed formats over the same vocabulary
+    # (Appendix, Constraint-Aware Dispatch Beyond Finite Sets): end-to-end
+    # compile with the vocabulary cached, and the device pass alone
+    formats = {}
+    for name, classes in W.formats().items():
+        e2e = []
+        for _ in range(5):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            hf = P.compile_format(classes, bench.voc)
+            torch.cuda.synchronize()
+            e2e.append((time.perf_counter() - t0) * 1e3)
+            if _ < 4:
+                hf.close()
+        ev = [[bench.event() for _ in range(2)] for _ in range(20)]
+        for e in ev:
+            e[0].record()
+            hf.rebuild()
+            e[1].record()
+        torch.cuda.synchronize()
+        formats[name] = {"L": len(classes), "compile_warm_ms": round(min(e2e), 3),
+                         "device_ms": round(float(np.mean([e[0].elapsed_time(e[1]) for e in ev])), 4),
+                         "valid_pairs": hf.valid_pairs()}
+        hf.close()
+    print("[bench] character-position masks: " + ", ".join(
+        f"{k} {v['device_ms'] * 1e3:.0f} us device / {v['compile_warm_ms']:.2f} ms" for k, v in formats.items()),
+        flush=True)
+
     secondary = None
     if not args.no_secondary and rep != "tail":
         h2, secondary = bench.measure("tail", args.steps, args.warmup, cold_runs=0)
@@ -409,6 +437,7 @@ def main():
         "advance_us": main_res["advance_us"],
         "device_bytes": main_res["device_bytes"],
         "tail_compression": secondary,
+        "char_position_masks": formats,
         "fill_GBps_4GiB": round(fill_gbps, 1),
         "bit_exact_sampled_rows": exact,
         "kernels_sha": sha,

@@ -221,6 +221,33 @@ tam_status tam_compile_vocab(const uint8_t *str_bytes, const int64_t *str_off, i
                              const tam_options *opt, const tam_allocator *alloc, void *stream,
                              tam_handle **out);
 
+/*
+ * tam_compile_format -- character-position masks of a fixed-format value
+ * (Appendix, Constraint-Aware Dispatch Beyond Finite Sets): character p
+ * (0 <= p < L) of a value may be any byte of class p, and the value is then
+ * closed by the terminator, as set strings are.  The handle's nodes are the
+ * positions: node p = p characters written (0..L), node L+1 = after the
+ * terminator (final, empty row).  Token v is valid at node p iff it is
+ * non-empty, p + |t_v| <= L + 1 and byte i of t_v lies in class p+i, class L
+ * being {terminator}; the advance moves to p + |t_v|, else TAM_DEAD.  Every
+ * serving entry point works on the handle; tam_info_get reports parent p-1,
+ * depth p, edge byte 0 (the terminator for node L+1), num_strings 0, and a
+ * dense table of L+2 rows.
+ *
+ *   classes  host uint8[L][32]: byte c is in class p iff bit (c & 7) of
+ *            classes[32 p + (c >> 3)] is set (copied).  No class may admit the
+ *            terminator (TAM_E_TERMINATOR).  L >= 1.
+ *   vocab    a vocabulary from tam_vocab_create (a device one unless
+ *            opt->flags asks for TAM_FLAG_HOST_ONLY); the handle keeps a
+ *            reference.
+ *   opt      terminator; flags TAM_FLAG_HOST_ONLY and TAM_FLAG_TIMING (the
+ *            representation flags do not apply).  NULL = defaults.
+ *   alloc, stream, out   as for tam_compile.
+ */
+tam_status tam_compile_format(const uint8_t *classes, int64_t L, const tam_vocab *vocab,
+                              const tam_options *opt, const tam_allocator *alloc, void *stream,
+                              tam_handle **out);
+
 enum {
     TAM_PHASE_LISTS = 1u << 0, /* sparse per-node valid lists (suffix probes, prefix sum, fill);
                                   with TAM_PHASE_MARK one probe pass serves both */
@@ -232,7 +259,8 @@ enum {
 /*
  * tam_rebuild -- rerun device phases of tam_compile from the handle's resident
  * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask; 0 =
- * the handle's default: TAM_PHASE_TABLE for a table, TAM_PHASE_LISTS with
+ * the handle's default: TAM_PHASE_TABLE for a table (TAM_PHASE_MARK for a
+ * format handle, which recomputes every word of its rows), TAM_PHASE_LISTS with
  * TAM_FLAG_NO_TABLE, both with TAM_FLAG_TAIL_LISTS when the vocabulary has
  * tokens longer than 16 bytes.  A phase the handle does not keep returns
  * TAM_E_STATE.  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the

@@ -9,8 +9,8 @@ from .tam import (DTYPE_BF16, DTYPE_FP32, FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TA
                   PHASE_LISTS, PHASE_MARK,
                   PHASE_TABLE, PHASE_ZERO,
                   TAM_DEAD,
-                  Handle, TamError, Vocab, compile, lib)
+                  Handle, TamError, Vocab, compile, compile_format, lib)
 
-__all__ = ["compile", "Vocab", "Handle", "TamError", "lib", "TAM_DEAD", "DTYPE_FP32", "DTYPE_BF16",
+__all__ = ["compile", "compile_format", "Vocab", "Handle", "TamError", "lib", "TAM_DEAD", "DTYPE_FP32", "DTYPE_BF16",
            "FLAG_HOST_ONLY", "FLAG_NO_TABLE", "FLAG_TAIL_LISTS", "FLAG_TIMING", "PHASE_LISTS", "PHASE_ZERO", "PHASE_MARK",
            "PHASE_TABLE"]

@@ -20,6 +20,8 @@
 //   k_advance-- B byte walks over the child tables.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
+// Fixed-format values (character-position masks):
+//   k_format -- every word of the rows of positions 0..L+1, by wave ballots.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -730,6 +732,60 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
     }
 }
 
+// ------------------------------------------------- fixed-format strings ---
+
+// Token bytes tb[0..len) at position p of a fixed format: non-empty, within
+// the L + 1 characters (the last being the terminator), every byte in its
+// position's class.
+__device__ __forceinline__ bool format_fits(const DevTables &t, int p, const uint8_t *tb, int len) {
+    const int L = t.fmt_L;
+    if (len <= 0 || p < 0 || p + len > L + 1) return false;
+    for (int i = 0; i < len; ++i) {
+        const int q = p + i;
+        const uint32_t c = tb[i];
+        const bool in = q == L ? c == (uint32_t)t.terminator
+                               : ((t.classes[(int64_t)q * 32 + (c >> 3)] >> (c & 7)) & 1u) != 0;
+        if (!in) return false;
+    }
+    return true;
+}
+
+// Character-position masks (Appendix, Constraint-Aware Dispatch Beyond Finite
+// Sets), written whole: one wave per 64-token word w of every row.  Lane i
+// tests token 64 w + i at each position p; the wave's ballot is word w of row p
+// (lane 0 stores it), so no zero fill is needed, and padding words come out
+// zero.  Each block writes its number of valid (position, token) pairs.
+__global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restrict__ pairs) {
+    const int64_t w = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t v = w * kWave + lane;
+    int32_t found = 0;
+    if (w < t.Wp) {
+        int len = 0;
+        const uint8_t *tb = t.tok_blob;
+        if (v < t.V) {
+            const uint32_t o = t.tok_off[v];
+            len = (int)(t.tok_off[v + 1] - o);
+            tb += o;
+        }
+        for (int p = 0; p <= t.fmt_L + 1; ++p) {
+            const bool ok = format_fits(t, p, tb, len);
+            const uint64_t word = __ballot(ok);
+            if (lane == 0) t.table[(int64_t)p * t.Wp + w] = word;
+            found += ok ? 1 : 0;
+        }
+    }
+    __shared__ int32_t wsum[kBlock / kWave];
+    for (int o = kWave / 2; o > 0; o >>= 1) found += __shfl_xor(found, o, kWave);
+    if (lane == 0) wsum[threadIdx.x / kWave] = found;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t total = 0;
+        for (int k = 0; k < kBlock / kWave; ++k) total += wsum[k];
+        pairs[blockIdx.x] = total;
+    }
+}
+
 // --------------------------------------------------------------- advance ---
 
 // 16 bytes base[pos .. pos+16) at any alignment (byte j of (lo, hi) = base[pos+j]),
@@ -796,6 +852,15 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
     const int32_t n0 = nodes[b];
     const int32_t v = toks[b];
     int32_t n = TAM_DEAD;
+    if (t.fmt_L >= 0) {  // character positions: p + |t| when the token fits the classes
+        if (n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V) {
+            const uint32_t o = t.tok_off[v];
+            const int len = (int)(t.tok_off[v + 1] - o);
+            if (format_fits(t, n0, t.tok_blob + o, len)) n = n0 + len;
+        }
+        out[b] = n;
+        return;
+    }
     if (n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V) {
         const int64_t a = t.tok_off[v];
         const int len = (int)(t.tok_off[v + 1] - (uint32_t)a);
@@ -908,6 +973,13 @@ hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s) {
 }
 
 int64_t mark_blocks(int64_t N) { return (N * kProbeLanes + kBlock - 1) / kBlock; }
+
+int64_t format_blocks(int64_t Wp) { return (Wp * kWave + kBlock - 1) / kBlock; }
+
+hipError_t launch_format(const DevTables &t, int32_t *pairs, hipStream_t s) {
+    hipLaunchKernelGGL(k_format, dim3((unsigned)format_blocks(t.Wp)), dim3(kBlock), 0, s, t, pairs);
+    return hipGetLastError();
+}
 
 hipError_t launch_scan(const DevTables &t, hipStream_t s) {
     const int64_t nb = grid_for(t.N, kScanTile);

@@ -196,6 +196,7 @@ void destroy_handle(tam_handle *h) {
 bool keeps_lists(const tam_handle *h) { return !h->dt.table || h->dt.tail_long; }
 
 unsigned default_phases(const tam_handle *h) {
+    if (h->fmt_L >= 0) return TAM_PHASE_MARK;  // k_format writes every word: no zero fill
     return (keeps_lists(h) ? unsigned(TAM_PHASE_LISTS) : 0u) | (h->dt.table ? unsigned(TAM_PHASE_TABLE) : 0u);
 }
 
@@ -213,7 +214,11 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     if (zero) TAM_HIP(tam::launch_zero(t.table, t.R * t.Wp, s));
     if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
     if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
-    if (lists || mark) TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+    if (t.fmt_L >= 0) {
+        if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
+    } else if (lists || mark) {
+        TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+    }
     if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
     if (lists) {
         TAM_HIP(tam::launch_scan(t, s));
@@ -336,7 +341,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_row_of = a.take<int32_t>(tails ? h->N : 0);
     const size_t o_row_at = a.take<int32_t>(tails ? h->blob_bytes : 0);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
-    const size_t o_pairs = a.take<int32_t>(tam::mark_blocks(h->N));
+    h->npairs = tam::mark_blocks(h->N);
+    const size_t o_pairs = a.take<int32_t>(h->npairs);
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = nullptr;
@@ -385,6 +391,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.len_mask = vocab->len_mask;
     t.max_len = (int32_t)vocab->max_tok_len;
     t.terminator = h->terminator;
+    t.classes = nullptr;
+    t.fmt_L = -1;
 
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
         if (bytes == 0) return hipSuccess;
@@ -425,6 +433,134 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     return TAM_OK;
 }
 
+// Character-position masks of a fixed-format value (see tam.h).
+tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, const tam_options *opt,
+                          const tam_allocator *alloc, hipStream_t s, tam_handle **out) {
+    *out = nullptr;
+    if (L < 1 || L > INT32_MAX - 3) return fail(TAM_E_INVAL, "L must be in [1, 2^31-4]");
+    if (!classes) return fail(TAM_E_INVAL, "classes is null");
+    tam_options o{0x22, 0};
+    if (opt) o = *opt;
+    if (o.terminator < 0 || o.terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
+    if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
+    const int T = o.terminator;
+    for (int64_t p = 0; p < L; ++p)
+        if ((classes[32 * p + (T >> 3)] >> (T & 7)) & 1)
+            return fail(TAM_E_TERMINATOR, "class " + std::to_string(p) + " admits the terminator byte");
+    const bool host_only = (o.flags & TAM_FLAG_HOST_ONLY) != 0;
+    if (!host_only && (vocab->flags & TAM_FLAG_HOST_ONLY))
+        return fail(TAM_E_STATE, "a device compile needs a vocabulary built without TAM_FLAG_HOST_ONLY");
+
+    tam_handle *h = new (std::nothrow) tam_handle();
+    if (!h) return fail(TAM_E_NOMEM, "out of host memory");
+    h->terminator = T;
+    h->flags = o.flags & (TAM_FLAG_HOST_ONLY | TAM_FLAG_TIMING);
+    vocab->refs.fetch_add(1);
+    h->vocab = vocab;
+    const auto t0 = std::chrono::steady_clock::now();
+    const int64_t N = L + 2;
+    try {
+        h->fmt_L = L;
+        h->classes.assign(classes, classes + 32 * L);
+        h->N = N;
+        h->S = 1;
+        h->K_unique = 0;
+        h->roots.assign(1, 0);
+        h->parent.resize((size_t)N);
+        h->depth.resize((size_t)N);
+        h->edge.assign((size_t)N, 0);
+        h->is_final.assign((size_t)N, 0);
+        for (int64_t p = 0; p < N; ++p) {
+            h->parent[(size_t)p] = (int32_t)(p - 1);
+            h->depth[(size_t)p] = (int32_t)p;
+        }
+        h->edge[(size_t)(N - 1)] = (uint8_t)T;
+        h->is_final[(size_t)(N - 1)] = 1;
+    } catch (const std::bad_alloc &) {
+        destroy_handle(h);
+        return fail(TAM_E_NOMEM, "out of host memory");
+    }
+    h->timing.host_trie_ms = ms_since(t0);
+    h->V = vocab->V;
+    h->W = vocab->W;
+    h->Wp = (h->W + 7) & ~int64_t(7);
+    h->dense_rows = N;
+    h->timing.dev_lists_ms = h->timing.dev_zero_ms = h->timing.dev_mark_ms = -1.f;
+    h->timing.dev_total_ms = -1.f;
+    if (host_only) {
+        *out = h;
+        return TAM_OK;
+    }
+
+    const auto t1 = std::chrono::steady_clock::now();
+    (void)hipGetLastError();
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        destroy_handle(h);
+        return fail(TAM_E_DEVICE, "no HIP device");
+    }
+    if (h->device != vocab->device) {
+        destroy_handle(h);
+        return fail(TAM_E_STATE, "the vocabulary lives on another device");
+    }
+    h->own_alloc = alloc == nullptr;
+    if (alloc) h->alloc = *alloc;
+    h->npairs = tam::format_blocks(h->Wp);
+    Arena a;
+    const size_t o_cls = a.take<uint8_t>(32 * L);
+    const size_t o_pairs = a.take<int32_t>(h->npairs);
+    uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
+    const size_t table_bytes = (size_t)N * (size_t)h->Wp * sizeof(uint64_t);
+    uint64_t *table = base ? static_cast<uint64_t *>(dev_alloc(h, table_bytes)) : nullptr;
+    if (!base || !table) {
+        destroy_handle(h);
+        return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
+                                     " bytes requested)");
+    }
+    h->device_bytes = (int64_t)(a.used + table_bytes);
+    h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
+    tam::DevTables &t = h->dt;
+    t = tam::DevTables{};
+    t.tok_off = vocab->d_tok_off;
+    t.tok_blob = vocab->d_tok_blob;
+    t.fps = vocab->d_fps;
+    t.pay = vocab->d_pay;
+    t.dup_next = vocab->d_dup_next;
+    t.len_present = vocab->d_len_present;
+    t.table = table;
+    t.row_at = nullptr;
+    t.N = N;
+    t.V = h->V;
+    t.W = h->W;
+    t.Wp = h->Wp;
+    t.R = N;
+    t.slot_mask = (uint64_t)vocab->fps.size() - 1;
+    t.len_mask = vocab->len_mask;
+    t.max_len = (int32_t)vocab->max_tok_len;
+    t.terminator = T;
+    t.classes = base + o_cls;
+    t.fmt_L = (int32_t)L;
+    hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
+    if (e == hipSuccess) e = hipMemcpyAsync(base + o_cls, h->classes.data(), h->classes.size(),
+                                            hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
+    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
+        for (hipEvent_t &ev : h->ev)
+            if (e == hipSuccess) e = hipEventCreate(&ev);
+        h->have_events = e == hipSuccess;
+    }
+    h->timing.upload_ms = ms_since(t1);
+    tam_status st = e == hipSuccess ? TAM_OK : hip_fail(e, "upload");
+    if (st == TAM_OK) st = run_device_phase(h, default_phases(h), s);
+    if (st != TAM_OK) {
+        const std::string msg = g_err;
+        destroy_handle(h);
+        return fail(st, msg);
+    }
+    *out = h;
+    return TAM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -450,6 +586,17 @@ tam_status tam_compile_vocab(const uint8_t *str_bytes, const int64_t *str_off, i
     if (!vocab) return fail(TAM_E_INVAL, "vocab is null");
     return compile_with(str_bytes, str_off, K, const_cast<tam_vocab *>(vocab), set_off, S, opt, alloc,
                         static_cast<hipStream_t>(stream), out);
+}
+
+tam_status tam_compile_format(const uint8_t *classes, int64_t L, const tam_vocab *vocab,
+                              const tam_options *opt, const tam_allocator *alloc, void *stream,
+                              tam_handle **out) {
+    g_err.clear();
+    if (!out) return fail(TAM_E_INVAL, "out is null");
+    *out = nullptr;
+    if (!vocab) return fail(TAM_E_INVAL, "vocab is null");
+    return compile_format(classes, L, const_cast<tam_vocab *>(vocab), opt, alloc, static_cast<hipStream_t>(stream),
+                          out);
 }
 
 tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
@@ -568,7 +715,7 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     if (!out) return fail(TAM_E_INVAL, "out is null");
     hipStream_t s = static_cast<hipStream_t>(stream);
     // a table's marks count every pair (tails' too); without one the lists do
-    std::vector<int32_t> part(h->dt.table ? (size_t)tam::mark_blocks(h->N) : 0);
+    std::vector<int32_t> part(h->dt.table ? (size_t)h->npairs : 0);
     int32_t listed = 0;
     if (h->dt.table)
         TAM_HIP(hipMemcpyAsync(part.data(), h->pairs, part.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));

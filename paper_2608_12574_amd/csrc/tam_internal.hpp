@@ -101,6 +101,9 @@ struct DevTables {
     uint64_t len_mask;          // bit d (d < 64): some token has length d
     int32_t max_len;
     int32_t terminator;
+    // character-position masks (tam_compile_format): classes of positions 0..L-1
+    const uint8_t *classes;     // [L][32] bit rows, or null for a trie handle
+    int32_t fmt_L;              // L, or -1 for a trie handle
 };
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
@@ -116,6 +119,8 @@ hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, 
                         int dtype, int64_t row_stride, hipStream_t s);
 hipError_t launch_advance(const DevTables &t, const int32_t *node_ids, const int32_t *token_ids,
                           int64_t B, int32_t *out, hipStream_t s);
+hipError_t launch_format(const DevTables &t, int32_t *pairs, hipStream_t s);
+int64_t format_blocks(int64_t Wp);
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
                                hipStream_t s);
 int64_t scan_tmp_elems(int64_t N);
@@ -175,6 +180,10 @@ struct tam_handle {
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
     std::vector<int32_t> tail_span, row_of, row_at;
     int64_t dense_rows = 0;
+    // character-position masks (tam_compile_format): L positions, their classes
+    int64_t fmt_L = -1;
+    std::vector<uint8_t> classes;
+    int64_t npairs = 0;  // per-block valid-pair counters in `pairs`
 
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};

@@ -28,7 +28,8 @@ STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOM
           -4: "TAM_E_DEVICE", -5: "TAM_E_TOOLARGE", -6: "TAM_E_STATE"}
 
 # the entry points declared in include/tam.h
-ENTRY_POINTS = ("tam_compile", "tam_vocab_create", "tam_compile_vocab", "tam_rebuild", "tam_info_get",
+ENTRY_POINTS = ("tam_compile", "tam_vocab_create", "tam_compile_vocab", "tam_compile_format", "tam_rebuild",
+                "tam_info_get",
                 "tam_apply_mask", "tam_advance", "tam_export_rows", "tam_valid_pairs", "tam_timing_get",
                 "tam_vocab_destroy", "tam_destroy", "tam_last_error")
 
@@ -91,6 +92,8 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(P)]
         L.tam_compile_vocab.argtypes = [P, P, i64, P, P, i64, ctypes.POINTER(Options),
                                         ctypes.POINTER(Allocator), P, ctypes.POINTER(P)]
+        L.tam_compile_format.argtypes = [P, i64, P, ctypes.POINTER(Options), ctypes.POINTER(Allocator), P,
+                                         ctypes.POINTER(P)]
         L.tam_vocab_destroy.argtypes = [P]
         L.tam_vocab_destroy.restype = None
         L.tam_rebuild.argtypes = [P, ctypes.c_uint, P]
@@ -373,4 +376,43 @@ def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, d
     _check(rc, "tam_compile")
     h = Handle(raw, allocator, device, host_only)
     h._vocab = keep  # the vocabulary's allocator must outlive the handle
+    return h
+
+
+def format_class_rows(classes) -> np.ndarray:
+    """Per-position allowed bytes (a list of L byte strings) as the [L][32] bit
+    rows of tam_compile_format: byte c of position p is bit c & 7 of row[p][c >> 3]."""
+    rows = np.zeros((len(classes), 32), dtype=np.uint8)
+    for p, allowed in enumerate(classes):
+        b = np.frombuffer(bytes(allowed), dtype=np.uint8)
+        np.bitwise_or.at(rows[p], b >> 3, (1 << (b & 7)).astype(np.uint8))
+    return rows
+
+
+def compile_format(classes, vocab, terminator: int = 0x22, flags: int = 0, device=None, stream=None) -> Handle:
+    """tam_compile_format: character-position masks of a fixed-format value whose
+    character p is any byte of ``classes[p]`` (a bytes object); node p = position
+    p, node L+1 = after the terminator.  ``vocab`` is a ``Vocab`` or a list[bytes]."""
+    rows = np.ascontiguousarray(format_class_rows(classes))
+    host_only = bool(flags & FLAG_HOST_ONLY)
+    if not isinstance(vocab, Vocab):
+        vocab = Vocab(vocab, host_only=host_only, device=device, stream=stream)
+    opt = Options(terminator, flags)
+    raw = ctypes.c_void_p()
+    allocator = None
+    if not host_only:
+        import torch
+        device = torch.device(device if device is not None else "cuda")
+        if device.index is None:
+            device = torch.device("cuda", torch.cuda.current_device())
+        allocator = _TorchAllocator(device)
+        with torch.cuda.device(device):
+            rc = lib().tam_compile_format(_ptr(rows), len(classes), vocab._raw, ctypes.byref(opt),
+                                          ctypes.byref(allocator.struct), _stream_ptr(stream), ctypes.byref(raw))
+    else:
+        rc = lib().tam_compile_format(_ptr(rows), len(classes), vocab._raw, ctypes.byref(opt), None, None,
+                                      ctypes.byref(raw))
+    _check(rc, "tam_compile_format")
+    h = Handle(raw, allocator, device, host_only)
+    h._vocab = vocab
     return h

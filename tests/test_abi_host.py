@@ -230,3 +230,27 @@ def test_host_trie_forest_with_large_set(P):
     h = host(P, strings, vocab, sets=offs)
     same_trie(h, Oracle(strings, [b"x"], set_offsets=offs))
     assert h.num_strings == sum(len(set(strings[offs[j]:offs[j + 1]])) for j in range(len(offs) - 1))
+
+
+def test_format_host_tables_and_errors(P):
+    """tam_compile_format on the host: positions 0..L+1 as a chain, the final
+    node last; classes admitting the terminator and empty formats are refused."""
+    classes = W.formats()["YYYY-MM-DD"]
+    h = P.compile_format(classes, [b"1", b"-", b'"'], flags=P.FLAG_HOST_ONLY)
+    L = len(classes)
+    assert h.num_nodes == L + 2 and h.num_sets == 1 and h.num_strings == 0
+    assert np.array_equal(h.roots, [0])
+    assert np.array_equal(h.parent, np.arange(-1, L + 1))
+    assert np.array_equal(h.depth, np.arange(L + 2))
+    assert np.array_equal(h.is_final, [0] * (L + 1) + [1])
+    assert h.dense_rows == L + 2 and h.dense_row is None
+    with pytest.raises(P.TamError) as e:
+        P.compile_format([b"0", b'9"'], [b"1"], flags=P.FLAG_HOST_ONLY)
+    assert e.value.status == -2
+    with pytest.raises(P.TamError) as e:
+        P.compile_format([], [b"1"], flags=P.FLAG_HOST_ONLY)
+    assert e.value.status == -1
+    h2 = P.compile_format([b"ab|"], [b"a"], terminator=ord('"'), flags=P.FLAG_HOST_ONLY)  # '|' is a plain byte here
+    assert h2.num_nodes == 3
+    with pytest.raises(P.TamError):
+        P.compile_format([b"ab|"], [b"a"], terminator=ord("|"), flags=P.FLAG_HOST_ONLY)

@@ -428,6 +428,82 @@ def test_forest_with_large_set(P, flags):
     h.close()
 
 
+# ------------------------------------------------------ fixed-format strings --
+
+@pytest.fixture(scope="module")
+def c4_vocab(P):
+    w = W.config(4)
+    return w.vocab, P.Vocab(w.vocab)
+
+
+@pytest.mark.parametrize("name", list(W.formats()))
+def test_format_masks(P, c4_vocab, name):
+    """Character-position masks over the 262,144-token vocabulary: every row,
+    every (position, token) advance, apply and the pair count, against the
+    oracle; rows again after a rebuild."""
+    from oracle import Format
+    classes = W.formats()[name]
+    vocab, voc = c4_vocab
+    f = Format(classes, vocab)
+    h = P.compile_format(classes, voc)
+    L = len(classes)
+    assert h.num_nodes == L + 2 and h.dense_rows == L + 2
+    pos = np.arange(-1, L + 3, dtype=np.int32)
+    rows = f.mask_rows(pos)
+    assert np.array_equal(gpu_rows(h, pos), rows)
+    assert h.valid_pairs() == int(np.unpackbits(rows.view(np.uint8)).sum())
+    V = len(vocab)
+    for p in range(-1, L + 3):
+        toks = np.arange(-1, V + 1, dtype=np.int32)
+        assert np.array_equal(gpu_advance(h, np.full(toks.size, p), toks), f.advance(np.full(toks.size, p), toks)), p
+    # apply: Eq. 1 on the oracle's rows, compared as raw bits
+    rng = np.random.default_rng(91)
+    ids = rng.integers(-1, L + 3, size=64).astype(np.int32)
+    for dtype in ("bf16", "fp32"):
+        x = host_logits(64, V, dtype, seed=92)
+        dev = x.cuda()
+        h.apply_mask(torch.as_tensor(ids, device="cuda"), dev)
+        valid = np.unpackbits(f.mask_rows(ids).view(np.uint8), axis=1, bitorder="little")[:, :V].astype(bool)
+        neg = np.uint16(0xFF80) if dtype == "bf16" else np.uint32(0xFF800000)
+        ref = bits_of(x)
+        ref = ref.view(np.uint16 if dtype == "bf16" else np.uint32)
+        exp = np.where(valid, ref, neg)
+        assert np.array_equal(bits_of(dev).view(exp.dtype), exp)
+    for ph in (P.PHASE_MARK, P.PHASE_TABLE, P.PHASE_ZERO | P.PHASE_MARK):
+        h.rebuild(phases=ph)
+        assert np.array_equal(gpu_rows(h, pos), rows)
+    with pytest.raises(P.TamError):
+        h.rebuild(phases=P.PHASE_LISTS)
+    h.close()
+
+
+def test_format_decode_reaches_final(P, c4_vocab):
+    """Decoding a date with uniformly random valid tokens always ends at the
+    final position, having written L characters and the terminator."""
+    from oracle import Format
+    classes = W.formats()["YYYY-MM-DD"]
+    vocab, voc = c4_vocab
+    f = Format(classes, vocab)
+    h = P.compile_format(classes, voc)
+    rng = np.random.default_rng(93)
+    cur = np.zeros(128, dtype=np.int32)
+    text = [b""] * 128
+    for step in range(len(classes) + 1):
+        live = cur < len(classes) + 1
+        rows = f.mask_rows(cur)
+        toks = W.choose_valid_tokens(rng, rows, len(vocab))
+        nxt = gpu_advance(h, cur, toks)
+        assert np.array_equal(nxt, f.advance(cur, toks))
+        for b in np.flatnonzero(live):
+            text[b] += vocab[toks[b]]
+        cur = np.where(live, nxt, cur).astype(np.int32)
+    assert (cur == len(classes) + 1).all()
+    for t in text:
+        assert len(t) == len(classes) + 1 and t.endswith(b'"')
+        assert all(c in cls for c, cls in zip(t, classes))
+    h.close()
+
+
 # ------------------------------------------------------------ layouts / edges --
 
 @pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)

@@ -402,3 +402,21 @@ def mixed_forest():
     sets = [small[0], big, small[1], small[2]]
     offs = np.cumsum([0] + [len(s) for s in sets])
     return [s for g in sets for s in g], w.vocab, offs
+
+
+DIGITS = b"0123456789"
+HEX = b"0123456789abcdef"
+
+
+def formats() -> dict:
+    """The fixed formats of the paper's character-position experiment, as byte
+    classes per position: an ISO date, a date-time, a date-time with
+    milliseconds, and a version-4 UUID (hex digits, the version digit 4, the
+    variant digit 8/9/a/b)."""
+    d = [DIGITS]
+    date = d * 4 + [b"-"] + d * 2 + [b"-"] + d * 2
+    dt = date + [b"T"] + d * 2 + [b":"] + d * 2 + [b":"] + d * 2
+    dtms = dt + [b"."] + d * 3
+    uuid = ([HEX] * 8 + [b"-"] + [HEX] * 4 + [b"-"] + [b"4"] + [HEX] * 3 + [b"-"] + [b"89ab"] + [HEX] * 3
+            + [b"-"] + [HEX] * 12)
+    return {"YYYY-MM-DD": date, "datetime": dt, "datetime.ms": dtms, "UUID v4": uuid}
