@@ -415,6 +415,13 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
             b = (b + 1) % nbuckets;
         }
     }
+    // per length d, the running sum over lengths <= d of the largest number of
+    // token ids sharing one string of that length (for the list size bound)
+    std::vector<int64_t> dup((size_t)max_len + 1, 0);
+    for (const SlotPay &sp : h->pay)
+        if (sp.first >= 0) dup[(size_t)sp.len] = std::max<int64_t>(dup[(size_t)sp.len], sp.count);
+    h->dup_cum.assign((size_t)max_len + 1, 0);
+    for (int64_t d = 1; d <= max_len; ++d) h->dup_cum[(size_t)d] = h->dup_cum[(size_t)d - 1] + dup[(size_t)d];
     return TAM_OK;
 }
 
@@ -426,13 +433,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
  */
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     const int64_t L = v->max_tok_len;
-    std::vector<int64_t> dup(L + 1, 0);
-    for (const SlotPay &s : v->pay) {
-        if (s.first < 0) continue;
-        dup[(size_t)s.len] = std::max<int64_t>(dup[(size_t)s.len], s.count);
-    }
-    std::vector<int64_t> cum(L + 1, 0);
-    for (int64_t d = 1; d <= L; ++d) cum[(size_t)d] = cum[(size_t)d - 1] + dup[(size_t)d];
+    const std::vector<int64_t> &cum = v->dup_cum;
     // A hit at distance d above node m lands in a list iff d <= the node's list
     // span; with tail compression only the hits longer than the probe window do
     // (the shorter ones are read straight from the probe's hits).

@@ -278,7 +278,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         if (st == TAM_OK && (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_NO_TABLE))
             tam::split_tails(h);
         h->timing.host_trie_ms = ms_since(t0);
-        if (st == TAM_OK) {
+        // the lists (and their size bound) are needed without a table, or with
+        // tail compression when tokens exceed the probe window
+        const bool lists = (o.flags & TAM_FLAG_NO_TABLE) ||
+                           ((o.flags & TAM_FLAG_TAIL_LISTS) && vocab->max_tok_len > tam::kWin);
+        if (st == TAM_OK && lists) {
             h->entry_bound = tam::entry_upper_bound(h, vocab);
             if (h->entry_bound >= INT32_MAX) {
                 st = TAM_E_TOOLARGE;

@@ -148,6 +148,7 @@ struct tam_vocab {
     std::vector<uint16_t> fps;
     std::vector<tam::SlotPay> pay;
     std::vector<int32_t> dup_next;
+    std::vector<int64_t> dup_cum;  // [max_len+1] see build_vocab (list size bound)
 
     // device copies (one arena)
     void *arena = nullptr;

@@ -119,11 +119,17 @@ def _check(rc: int, where: str):
 
 
 def csr(items) -> tuple:
-    """list[bytes] -> (uint8 blob, int64 offsets[len+1]) as numpy arrays."""
-    items = list(items)
+    """list[bytes] -> (uint8 blob, int64 offsets[len+1]) as numpy arrays.  A pair
+    (blob, offsets) of arrays is taken as already packed."""
+    if isinstance(items, tuple) and len(items) == 2 and isinstance(items[0], np.ndarray):
+        blob = np.ascontiguousarray(items[0], dtype=np.uint8)
+        off = np.ascontiguousarray(items[1], dtype=np.int64)
+        return (blob if blob.size else np.zeros(1, dtype=np.uint8)), off
+    if not isinstance(items, list):
+        items = list(items)
     off = np.zeros(len(items) + 1, dtype=np.int64)
     if items:
-        np.cumsum(np.fromiter((len(x) for x in items), dtype=np.int64, count=len(items)), out=off[1:])
+        np.cumsum(np.fromiter(map(len, items), dtype=np.int64, count=len(items)), out=off[1:])
     blob = np.frombuffer(b"".join(items), dtype=np.uint8)
     if blob.size == 0:
         blob = np.zeros(1, dtype=np.uint8)
@@ -328,8 +334,9 @@ class Vocab:
 
 def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, device=None,
             stream=None) -> Handle:
-    """tam_compile over ``strings`` (list[bytes]) and ``vocab`` (a ``Vocab`` or a
-    list[bytes], token id = index).
+    """tam_compile over ``strings`` (list[bytes], or a packed pair (uint8 blob,
+    int64 offsets[K+1])) and ``vocab`` (a ``Vocab`` or a list[bytes], token id =
+    index).
 
     ``sets``: optional forest offsets (S+1 ints) splitting ``strings`` into S sets.
     With ``FLAG_HOST_ONLY`` no GPU is touched (host tables only).

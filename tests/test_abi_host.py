@@ -254,3 +254,13 @@ def test_format_host_tables_and_errors(P):
     assert h2.num_nodes == 3
     with pytest.raises(P.TamError):
         P.compile_format([b"ab|"], [b"a"], terminator=ord("|"), flags=P.FLAG_HOST_ONLY)
+
+
+def test_packed_strings_input(P):
+    """compile() takes the strings as a packed (blob, offsets) pair as well."""
+    from paper_2608_12574_amd.tam import csr
+    w = W.config(2)
+    h1 = host(P, w.strings, w.vocab)
+    h2 = host(P, csr(w.strings), w.vocab)
+    assert h1.num_nodes == h2.num_nodes
+    assert np.array_equal(h1.parent, h2.parent) and np.array_equal(h1.edge_byte, h2.edge_byte)
