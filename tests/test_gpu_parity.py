@@ -546,3 +546,41 @@ def test_many_rows_grid_split(P):
         assert np.array_equal(gpu_rows(h, nodes[:66000]), np.where(
             live[:66000, None], rows[np.clip(nodes[:66000], 0, o.N - 1)], np.uint64(0)))
         h.close()
+
+
+def test_c_abi_with_library_allocator(P):
+    """The C ABI called directly: NULL allocator (the library's hipMalloc/hipFree)
+    and the NULL stream, for a vocabulary, a compile against it, apply, advance,
+    export and destroy, against the oracle."""
+    import ctypes
+    from paper_2608_12574_amd.tam import Options, csr
+    L = P.lib()
+    w = W.config(1)
+    o = Oracle(w.strings, w.vocab)
+    tb, to = csr(w.vocab)
+    sb, so = csr(w.strings)
+    voc = ctypes.c_void_p()
+    assert L.tam_vocab_create(tb.ctypes.data, to.ctypes.data, len(w.vocab), 0, None, None, ctypes.byref(voc)) == 0
+    for flags in FLAGS3:
+        h = ctypes.c_void_p()
+        opt = Options(0x22, flags)
+        assert L.tam_compile_vocab(sb.ctypes.data, so.ctypes.data, len(w.strings), voc, None, 0, ctypes.byref(opt),
+                                   None, None, ctypes.byref(h)) == 0
+        nodes = np.arange(-1, o.N + 1, dtype=np.int32)
+        ids = torch.as_tensor(nodes, device="cuda")
+        rows = torch.empty((nodes.size, o.W), dtype=torch.int64, device="cuda")
+        assert L.tam_export_rows(h, ids.data_ptr(), nodes.size, rows.data_ptr(), None) == 0
+        toks = torch.as_tensor(W.choose_valid_tokens(np.random.default_rng(5), o.mask_rows(nodes), o.V),
+                               device="cuda")
+        out = torch.empty_like(ids)
+        assert L.tam_advance(h, ids.data_ptr(), toks.data_ptr(), nodes.size, out.data_ptr(), None) == 0
+        x = host_logits(nodes.size, o.V, "bf16", seed=6)
+        dev = x.cuda()
+        assert L.tam_apply_mask(h, ids.data_ptr(), nodes.size, dev.data_ptr(), 1, o.V, None) == 0
+        torch.cuda.synchronize()
+        assert np.array_equal(rows.cpu().numpy().view(np.uint64), o.mask_rows(nodes))
+        assert np.array_equal(out.cpu().numpy(), o.advance(nodes, toks.cpu().numpy()))
+        exp = o.apply(nodes, bits_of(x).view(np.uint16), 1)
+        assert np.array_equal(bits_of(dev).view(np.uint16), exp)
+        L.tam_destroy(h)
+    L.tam_vocab_destroy(voc)
