@@ -286,10 +286,14 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->is_final.resize((size_t)N);
     h->node_pos.resize((size_t)N);
     h->child_off.resize((size_t)N + 1);
-    h->child_node.assign((size_t)std::max<int64_t>(E, 1), 0);
-    h->child_byte.assign((size_t)std::max<int64_t>(E, 1), 0);
-    h->blob.assign((size_t)BB, 0);
-    h->node_at.assign((size_t)BB, 0);
+    h->child_node.resize((size_t)std::max<int64_t>(E, 1));
+    h->child_byte.resize((size_t)std::max<int64_t>(E, 1));
+    h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
+    h->node_at.resize((size_t)BB);
+    for (int64_t p = 0; p < kBlobPad; ++p) {
+        h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
+        h->node_at[(size_t)p] = h->node_at[(size_t)(BB - 1 - p)] = 0;
+    }
     for (int64_t j = 0; j < S; ++j) {
         const int64_t rt = root[(size_t)j];
         h->roots[(size_t)j] = (int32_t)rt;
@@ -477,13 +481,16 @@ void split_tails(tam_handle *h) {
     }
     const int64_t R = (int64_t)lo.size();
     const int threads = host_threads(R);
-    std::vector<int32_t> finals(h->is_final.begin(), h->is_final.end());
-    std::vector<int32_t> rem((size_t)N, 0);  // nodes below a tail (its single child is n+1)
+    // per-node scratch, first touched by the threads of the passes below
+    hvec<int32_t> finals((size_t)N), rem((size_t)N), top((size_t)N);
     std::vector<int64_t> branching((size_t)R, 0);
-    auto backward = [&](int64_t n) {  // finals[n] is complete: all descendants are done
-        if (finals[(size_t)n] == 1 && !h->is_final[(size_t)n]) rem[(size_t)n] = rem[(size_t)n + 1] + 1;
+    // finals[n] is complete once all descendants are done; rem = nodes below a
+    // tail (its single child is n+1)
+    auto backward = [&](int64_t n) {
+        rem[(size_t)n] = finals[(size_t)n] == 1 && !h->is_final[(size_t)n] ? rem[(size_t)n + 1] + 1 : 0;
     };
     parallel_for(R, threads, [&](int64_t i) {
+        for (int64_t n = lo[(size_t)i]; n < hi[(size_t)i]; ++n) finals[(size_t)n] = h->is_final[(size_t)n];
         int64_t b = 0;
         for (int64_t n = hi[(size_t)i] - 1; n >= lo[(size_t)i]; --n) {
             backward(n);
@@ -494,16 +501,19 @@ void split_tails(tam_handle *h) {
     });
     // the roots, then the dense row numbering in id order (a root, its ranges, ...)
     std::vector<int64_t> first_row((size_t)R, 0);
-    std::vector<int32_t> top((size_t)N, -1);  // depth of the highest tail ancestor-or-self
-    h->tail_span.assign((size_t)N, 0);
-    h->row_of.assign((size_t)N, -1);
+    // top: depth of the highest tail ancestor-or-self (-1 for a branching node)
+    h->tail_span.resize((size_t)N);
+    h->row_of.resize((size_t)N);
     int64_t rows = 0, i = 0;
     for (int64_t j = 0; j < S; ++j) {
         const int32_t r = h->roots[(size_t)j];
         const int64_t i0 = i;
+        finals[(size_t)r] = 0;
+        top[(size_t)r] = -1;
         for (int32_t e = h->child_off[(size_t)r]; e < h->child_off[(size_t)r + 1]; ++e, ++i)
             finals[(size_t)r] += finals[(size_t)lo[(size_t)i]];
         backward(r);
+        h->tail_span[(size_t)r] = 0;
         if (finals[(size_t)r] >= 2) {
             h->row_of[(size_t)r] = (int32_t)rows++;
         } else {
@@ -521,6 +531,8 @@ void split_tails(tam_handle *h) {
         for (int64_t n = lo[(size_t)k]; n < hi[(size_t)k]; ++n) {
             if (finals[(size_t)n] >= 2) {
                 h->row_of[(size_t)n] = row++;
+                h->tail_span[(size_t)n] = 0;
+                top[(size_t)n] = -1;
                 continue;
             }
             const int32_t p = h->parent[(size_t)n];

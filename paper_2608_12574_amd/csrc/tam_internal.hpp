@@ -6,11 +6,37 @@
 #include <atomic>
 #include <cstdint>
 #include <string>
+#include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "../../include/tam.h"
 
 namespace tam {
+
+// An allocator whose value-initialisation (vector::resize) leaves elements of
+// trivial types unset, so that large host tables are first touched by the
+// threads that fill them instead of being zeroed serially beforehand.
+template <typename T>
+struct NoInitAlloc : std::allocator<T> {
+    template <typename U>
+    struct rebind {
+        using other = NoInitAlloc<U>;
+    };
+    NoInitAlloc() = default;
+    template <typename U>
+    NoInitAlloc(const NoInitAlloc<U> &) noexcept {}
+    template <typename U>
+    void construct(U *p) noexcept(std::is_nothrow_default_constructible<U>::value) {
+        ::new ((void *)p) U;
+    }
+    template <typename U, typename... A>
+    void construct(U *p, A &&...a) {
+        ::new ((void *)p) U(std::forward<A>(a)...);
+    }
+};
+template <typename T>
+using hvec = std::vector<T, NoInitAlloc<T>>;
 
 // ---------------------------------------------------------------------------
 // Vocabulary hash: keys are the token bytes read last-to-first, so that a
@@ -176,10 +202,10 @@ struct tam_handle {
     int64_t blob_bytes = 0, entry_bound = 0, device_bytes = 0;
 
     // host trie tables
-    std::vector<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
-    std::vector<uint8_t> edge, is_final, blob, child_byte;
+    tam::hvec<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
+    tam::hvec<uint8_t> edge, is_final, blob, child_byte;
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
-    std::vector<int32_t> tail_span, row_of, row_at;
+    tam::hvec<int32_t> tail_span, row_of, row_at;
     int64_t dense_rows = 0;
     // character-position masks (tam_compile_format): L positions, their classes
     int64_t fmt_L = -1;
