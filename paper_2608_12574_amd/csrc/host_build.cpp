@@ -374,15 +374,35 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     h->dup_next.assign((size_t)V, -1);
     std::vector<int32_t> last(cap, -1);
     const uint8_t *blob = h->tok_blob.data();
+    // keys and reversed heads of all tokens, in parallel; the placement below is
+    // serial, in id order (duplicate chains ascend)
+    std::vector<uint64_t> keys((size_t)V), heads((size_t)V * 2);
+    const int64_t chunk = 8192;
+    parallel_for((V + chunk - 1) / chunk, host_threads((V + chunk - 1) / chunk), [&](int64_t c) {
+        for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v) {
+            const uint32_t off = h->tok_off[(size_t)v];
+            const uint32_t len = h->tok_off[(size_t)v + 1] - off;
+            uint64_t hh = kHashSeed, lo = 0, hi = 0;
+            for (int64_t i = (int64_t)len - 1; i >= 0; --i) hh = hash_step(hh, blob[off + i]);
+            for (uint32_t k = 0; k < len && k < 16; ++k) {
+                const uint64_t ch = blob[off + len - 1 - k];
+                if (k < 8)
+                    lo |= ch << (8 * k);
+                else
+                    hi |= ch << (8 * (k - 8));
+            }
+            keys[(size_t)v] = len ? hash_final(hh, len) : 0;
+            heads[(size_t)(2 * v)] = lo;
+            heads[(size_t)(2 * v + 1)] = hi;
+        }
+    });
     for (int64_t v = 0; v < V; ++v) {
         const uint32_t off = h->tok_off[(size_t)v];
         const uint32_t len = h->tok_off[(size_t)v + 1] - off;
         if (len == 0) continue;
         h->len_present[len] = 1;
         if (len < 64) h->len_mask |= 1ull << len;
-        uint64_t hh = kHashSeed;
-        for (int64_t i = (int64_t)len - 1; i >= 0; --i) hh = hash_step(hh, blob[off + i]);
-        const uint64_t key = hash_final(hh, len);
+        const uint64_t key = keys[(size_t)v];
         const uint16_t fp = (uint16_t)fingerprint(key);
         uint64_t b = (key & (cap - 1)) / kBucket;
         bool placed = false;
@@ -391,15 +411,8 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
                 const uint64_t s = b * kBucket + (uint64_t)i;
                 if (h->fps[s] == 0) {
                     h->fps[s] = fp;
-                    SlotPay r{0, 0, (int32_t)v, (uint16_t)len, 1, {0, 0}};
-                    for (uint32_t k = 0; k < len && k < 16; ++k) {
-                        const uint64_t c = blob[off + len - 1 - k];
-                        if (k < 8)
-                            r.lo |= c << (8 * k);
-                        else
-                            r.hi |= c << (8 * (k - 8));
-                    }
-                    h->pay[s] = r;
+                    h->pay[s] = SlotPay{heads[(size_t)(2 * v)], heads[(size_t)(2 * v + 1)], (int32_t)v,
+                                        (uint16_t)len, 1, {0, 0}};
                     last[s] = (int32_t)v;
                     placed = true;
                 } else if (h->fps[s] == fp && h->pay[s].len == len) {
