@@ -268,6 +268,11 @@ enum {
  * kernel.
  */
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
+/* HIP graphs: tam_rebuild, tam_apply_mask, tam_advance and tam_export_rows only
+ * launch kernels on `stream`, so they may be captured into a graph (no memset
+ * or event nodes are recorded; the handle must outlive every replay, and
+ * tam_destroy does not wait for replays still running: synchronise first).
+ * tam_valid_pairs and tam_timing_get synchronise and must not be captured. */
 
 /* tam_info_get -- sizes and host tables of a handle (no device access). */
 tam_status tam_info_get(const tam_handle *h, tam_info *out);

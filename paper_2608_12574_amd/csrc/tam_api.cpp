@@ -206,7 +206,12 @@ unsigned default_phases(const tam_handle *h) {
 // default phases.
 tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     const tam::DevTables &t = h->dt;
-    const bool timing = h->have_events && phases == default_phases(h);
+    // Under stream capture (a HIP graph) only the kernels are recorded: no
+    // events, which belong to eager calls.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    TAM_HIP(hipStreamIsCapturing(s, &cap));
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    const bool timing = h->have_events && phases == default_phases(h) && !capturing;
     const bool lists = (phases & TAM_PHASE_LISTS) != 0;
     const bool zero = (phases & TAM_PHASE_ZERO) && t.table;
     const bool mark = (phases & TAM_PHASE_MARK) && t.table;
@@ -230,7 +235,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
         TAM_HIP(hipEventRecord(h->ev[3], s));
         h->events_recorded = true;
     }
-    if (h->work_done) TAM_HIP(hipEventRecord(h->work_done, s));
+    if (h->work_done && !capturing) TAM_HIP(hipEventRecord(h->work_done, s));
     return TAM_OK;
 }
 

@@ -584,3 +584,49 @@ def test_c_abi_with_library_allocator(P):
         assert np.array_equal(bits_of(dev).view(np.uint16), exp)
         L.tam_destroy(h)
     L.tam_vocab_destroy(voc)
+
+
+@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+def test_graph_capture_replays(P, flags):
+    """rebuild + apply + advance captured in a HIP graph: every replay, with eager
+    work and synchronisation between replays, gives the eager results."""
+    w = W.config(2)
+    h = P.compile(w.strings, w.vocab, flags=flags)
+    o = Oracle(w.strings, w.vocab)
+    B, V = 64, len(w.vocab)
+    nodes = W.uniform_nodes(2, o.N, B)
+    ids = torch.as_tensor(nodes, device="cuda")
+    src = torch.as_tensor(host_logits(B, V, "fp32", seed=12).numpy(), device="cuda")
+    toks_np = W.choose_valid_tokens(np.random.default_rng(13), o.mask_rows(nodes), V)
+    toks = torch.as_tensor(toks_np, device="cuda")
+    x = src.clone()
+    out = torch.empty_like(ids)
+    exp_x = o.apply(nodes, bits_of(src.cpu()).view(np.uint32), 0)
+    exp_out = o.advance(nodes, toks_np)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        h.rebuild()
+        h.apply_mask(ids, x)
+        h.advance(ids, toks, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        h.rebuild()
+        h.apply_mask(ids, x)
+        h.advance(ids, toks, out=out)
+    for r in range(5):
+        x.copy_(src)
+        out.fill_(-7)
+        if r % 2:
+            h.rebuild()  # eager work on the same handle between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits_of(x).view(np.uint32), exp_x), r
+        assert np.array_equal(out.cpu().numpy(), exp_out), r
+        assert np.array_equal(gpu_rows(h, nodes[:32]), o.mask_rows(nodes[:32])), r
+    del graph
+    torch.cuda.synchronize()
+    h.close()
