@@ -41,7 +41,8 @@
  * NULL = the null stream) and returns without synchronising, except where a
  * function says otherwise.  A handle is immutable after tam_compile (only
  * tam_rebuild rewrites its table in place), so apply/advance/export calls may
- * run concurrently on any streams once the compile stream has been waited on.
+ * run concurrently on any streams once the compile stream has been waited on;
+ * TAM_FLAG_LAZY_ROWS handles are the exception (their row cache changes).
  *
  * Errors: every entry point returns a tam_status; a negative status leaves a
  * message in tam_last_error() (thread-local).  No exception crosses the ABI.
@@ -97,7 +98,22 @@ enum {
      * Results are identical to the full table, which holds dense_rows rows
      * instead of N (c. 2.5% of the nodes of a set of 10,000 code-like
      * strings).  Ignored with TAM_FLAG_NO_TABLE. */
-    TAM_FLAG_TAIL_LISTS = 1u << 3
+    TAM_FLAG_TAIL_LISTS = 1u << 3,
+    /* Rows built on demand (the lazy computation of the Appendix's memory
+     * discussion, with the matching restricted to the subtree below the
+     * current node): compile computes no mask, only the trie, its subtree
+     * extents and an empty cache of tam_options.cache_rows dense rows.
+     * tam_apply_mask looks the rows of its nodes up in the cache; the row of a
+     * node that is not there is built in that call, by suffix probes over the
+     * node's subtree (every descendant at most max_token_len bytes deeper), in
+     * a cache slot freed by CLOCK replacement (second chance, an approximation
+     * of least-recently-used eviction).  Masks are identical to the
+     * precomputed table's.  tam_apply_mask and tam_export_rows (which builds
+     * the requested rows the same way, outside the cache) update device state
+     * held by the handle: their calls on one handle must not overlap (use one
+     * stream, or order the streams).  Takes precedence over TAM_FLAG_NO_TABLE
+     * and TAM_FLAG_TAIL_LISTS. */
+    TAM_FLAG_LAZY_ROWS = 1u << 4
 };
 
 /* Device allocator.  alloc returns device memory aligned to at least 256 bytes
@@ -110,8 +126,9 @@ typedef struct {
 } tam_allocator;
 
 typedef struct {
-    int terminator;  /* 0..255; default 0x22 */
-    uint32_t flags;  /* TAM_FLAG_* */
+    int terminator;      /* 0..255; default 0x22 */
+    uint32_t flags;      /* TAM_FLAG_* */
+    int64_t cache_rows;  /* TAM_FLAG_LAZY_ROWS: rows of the row cache; 0 = 4096; at most N is used */
 } tam_options;
 
 /* Read-only view of a compiled handle.  Host pointers stay valid until
@@ -137,6 +154,9 @@ typedef struct {
     const int32_t *dense_row; /* [N] table row of each node (>= 0); for a tail node a,
                                  -1 - (number of nodes below a).  NULL when row = node id
                                  (full table) or there is no table */
+    int64_t cache_rows;        /* TAM_FLAG_LAZY_ROWS: rows of the row cache (else 0) */
+    const int32_t *subtree_end; /* [N] with TAM_FLAG_LAZY_ROWS: one past the last node of the
+                                 node's subtree (preorder ids); else NULL */
 } tam_info;
 
 /* Host-side wall times of the last tam_compile, and device times (HIP events,
@@ -265,7 +285,8 @@ enum {
  * tokens longer than 16 bytes.  A phase the handle does not keep returns
  * TAM_E_STATE.  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the
  * same bits into the current table.  Used to time the device phase kernel by
- * kernel.
+ * kernel.  With TAM_FLAG_LAZY_ROWS the only phase is 0: it empties the row
+ * cache, so that every row is built again on its next use.
  */
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
 /* HIP graphs: tam_rebuild, tam_apply_mask, tam_advance and tam_export_rows only
@@ -290,7 +311,9 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out);
  *               (-inf = 0xFF800000) or TAM_DTYPE_BF16 (-inf = 0xFF80).
  *   row_stride  elements between rows, >= V.
  * Rows whose base is 16-byte aligned take the vector path; any other layout is
- * still handled (element path).  B = 0 is a no-op.
+ * still handled (element path).  B = 0 is a no-op.  With TAM_FLAG_LAZY_ROWS the
+ * rows of nodes missing from the row cache are built first (see the flag), in
+ * groups of at most min(1024, cache rows) batch rows.
  */
 tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t B, void *logits,
                           int dtype, int64_t row_stride, void *stream);
@@ -316,7 +339,7 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
  * tam_valid_pairs -- M = sum over all nodes of |valid[n]|, the number of
  * (node, token) pairs that are valid, as found by the last table or list
  * build.  Copies the per-block counts from the device and synchronises
- * `stream`.
+ * `stream`.  TAM_E_STATE with TAM_FLAG_LAZY_ROWS (no pass over all nodes).
  */
 tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out);
 

@@ -33,6 +33,7 @@ struct TerminatedLess {
 // byte of s+T), with bucket-local node ids (root = 0) and blob offsets.
 struct SetTrie {
     std::vector<int32_t> parent, depth, node_pos, node_at, child_off, child_node;
+    std::vector<int32_t> sub_end;  // one past the last node of each node's subtree (local ids)
     std::vector<uint8_t> edge, is_final, blob, child_byte;
     int64_t K_unique = 0;
     tam_status st = TAM_OK;
@@ -81,7 +82,9 @@ void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int6
     r.node_pos.reserve(est);
     r.blob.reserve(est);
     r.node_at.reserve(est);
+    r.sub_end.reserve(est);
     r.parent.push_back(-1);
+    r.sub_end.push_back(0);
     r.depth.push_back(0);
     r.edge.push_back(0);
     r.is_final.push_back(0);
@@ -99,6 +102,9 @@ void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int6
             const int64_t m = std::min(len, prev_len);
             while (l < m && prev[l] == s[l]) ++l;
             if (l == len && len == prev_len) continue;  // duplicate string
+            // the previous string's nodes below depth l have no more descendants:
+            // their subtrees end where this string's first new node starts
+            for (int64_t i = l; i <= prev_len; ++i) r.sub_end[(size_t)path[(size_t)i]] = (int32_t)N;
         }
         prev = s;
         prev_len = len;
@@ -119,6 +125,7 @@ void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int6
                 r.edge.push_back(c);
                 r.is_final.push_back(i == len ? 1 : 0);
                 r.node_pos.push_back((int32_t)(r.blob.size() - 1));
+                r.sub_end.push_back(0);
             }
             path[(size_t)i] = id;
             r.node_at.push_back(id);
@@ -129,6 +136,8 @@ void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int6
             return;
         }
     }
+    for (int64_t i = 0; i <= prev_len; ++i) r.sub_end[(size_t)path[(size_t)i]] = (int32_t)N;
+    r.sub_end[0] = (int32_t)N;
     // children in ascending byte order = ascending ids (preorder)
     r.child_off.assign((size_t)(N + 1), 0);
     for (int64_t m = 1; m < N; ++m) ++r.child_off[(size_t)r.parent[(size_t)m] + 1];
@@ -290,6 +299,8 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->child_byte.resize((size_t)std::max<int64_t>(E, 1));
     h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
     h->node_at.resize((size_t)BB);
+    const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
+    h->sub_end.resize(subtrees ? (size_t)N : 0);
     for (int64_t p = 0; p < kBlobPad; ++p) {
         h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
         h->node_at[(size_t)p] = h->node_at[(size_t)(BB - 1 - p)] = 0;
@@ -303,6 +314,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         h->is_final[(size_t)rt] = 0;
         h->node_pos[(size_t)rt] = -1;
         h->child_off[(size_t)rt] = (int32_t)root_edges[(size_t)j];
+        if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
     }
     parallel_for(NP, host_threads(NP), [&](int64_t p) {
         const SetTrie &r = parts[(size_t)p];
@@ -319,6 +331,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             h->depth[g] = r.depth[i];
             h->edge[g] = r.edge[i];
             h->is_final[g] = r.is_final[i];
+            if (subtrees) h->sub_end[g] = (int32_t)(nb + r.sub_end[i]);
         }
         std::copy(r.blob.begin(), r.blob.end(), h->blob.begin() + bb);
         for (size_t i = 0; i < r.node_at.size(); ++i) h->node_at[(size_t)bb + i] = gid(r.node_at[i]);

@@ -20,6 +20,10 @@
 //   k_advance-- B byte walks over the child tables.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
+// Rows built on demand (lazy computation with a bounded cache, Appendix):
+//   k_lazy_assign -- cache lookup and CLOCK replacement for a group of rows.
+//   k_lazy_zero, k_lazy_probe -- the missing rows, from the suffix probes of
+//               the node's subtree only; k_apply then reads the cache.
 // Fixed-format values (character-position masks):
 //   k_format -- every word of the rows of positions 0..L+1, by wave ballots.
 #include <hip/hip_runtime.h>
@@ -932,6 +936,239 @@ __global__ void __launch_bounds__(kBlock) k_export_tail(DevTables t, const int32
         for (int32_t k = t.row_ptr[n] + lane; k < t.row_ptr[n + 1]; k += kWave) set(t.entries[k]);
 }
 
+// -------------------------------------------------------- rows on demand ---
+
+constexpr int kLazyProbeBlocks = 1024;  // grid of k_lazy_probe (grid-stride)
+
+// Exclusive prefix sum of one value per thread over a block of kLazyGroup
+// threads; *total receives the sum.  sh holds kLazyGroup / kWave values.
+__device__ __forceinline__ int64_t group_scan(int64_t x, int64_t *total, int64_t *sh) {
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    int64_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(inc, o, kWave);
+        if (lane >= o) inc += y;
+    }
+    if (lane == kWave - 1) sh[wid] = inc;
+    __syncthreads();
+    int64_t before = 0, all = 0;
+    for (int w = 0; w < kLazyGroup / kWave; ++w) {
+        const int64_t v = sh[w];
+        if (w < wid) before += v;
+        all += v;
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - x;
+}
+
+// Cache words that other waves of the block read back after a barrier go
+// through L2 (device-scope atomics), not through this CU's L1.
+__device__ __forceinline__ uint32_t load_l2(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_l2(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Which rows a group of nb batch rows needs built, one block of kLazyGroup
+// threads, one thread per batch row.
+// kCache (tam_apply_mask):
+//   1. Each live row claims its node with a compare-and-swap on slot_of: a
+//      slot (>= 0) is a hit; -1 makes the row the builder of the node's row (a
+//      miss); -2 - b names builder b to the other rows of that node.
+//   2. Hits stamp their slot with the group's number, so it is not evicted.
+//   3. The misses take slots by CLOCK: sweeps from the hand over windows of up
+//      to kLazyGroup slots take those not used by the group and without a
+//      reference bit, in order, and clear the reference bit of the others they
+//      pass; the hand stops after the last slot taken.  With nb <= C at least
+//      as many slots are free as there are misses, so two turns of the hand
+//      suffice.
+//   4. A taken slot drops its old node; each builder records its node, slot
+//      and subtree size for the zero and probe passes, and every batch row
+//      its slot (rows_src).
+// !kCache (tam_export_rows): every live row is built, into output row b.
+template <bool kCache>
+__global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev z,
+                                                            const int32_t *__restrict__ ids, int32_t nb) {
+    __shared__ int32_t s_slot[kLazyGroup];
+    __shared__ int32_t s_victim[kLazyGroup];
+    __shared__ int64_t s_scan[kLazyGroup / kWave];
+    __shared__ uint32_t s_u[4];  // group number, hand, cut, counter wrapped
+    const int tid = threadIdx.x;
+    const int32_t n = tid < nb ? ids[tid] : -1;
+    const bool live = n >= 0 && (int64_t)n < t.N;
+    const int64_t below = live ? (int64_t)t.sub_end[n] - n - 1 : 0;
+    int32_t slot = -1, lead = -1;
+    bool miss = live;
+    uint32_t group = 0;
+    if (kCache) {
+        if (tid == 0) {
+            uint32_t g = z.state[0] + 1u;
+            s_u[3] = g == 0u ? 1u : 0u;
+            if (g == 0u) g = 1u;  // 0 marks a slot never used
+            z.state[0] = g;
+            s_u[0] = g;
+            s_u[1] = z.state[1];
+        }
+        if (live) {
+            const int32_t v = atomicCAS(&z.slot_of[n], -1, -2 - tid);
+            miss = v == -1;
+            if (v >= 0)
+                slot = v;
+            else if (v != -1)
+                lead = -2 - v;
+        }
+        __syncthreads();
+        group = s_u[0];
+        if (s_u[3]) {  // the group counter wrapped: forget every stamp
+            for (int64_t c = tid; c < z.C; c += kLazyGroup) store_l2(&z.stamp[c], 0u);
+            __threadfence();
+            __syncthreads();
+        }
+        if (slot >= 0) {
+            store_l2(&z.stamp[slot], group);
+            store_l2(&z.ref[slot], 1u);
+        }
+    }
+    s_slot[tid] = slot;
+    int64_t nmiss, total;
+    const int32_t rank = (int32_t)group_scan(miss ? 1 : 0, &nmiss, s_scan);
+    const int64_t off = group_scan(miss ? below : 0, &total, s_scan);
+    const int32_t M = (int32_t)nmiss;
+    if (kCache) {
+        __threadfence();  // the hits' stamps before the sweeps read them
+        __syncthreads();
+        const int64_t C = z.C;
+        const int win = (int)min<int64_t>(C, kLazyGroup);
+        int64_t hand = s_u[1];
+        int32_t taken = 0;
+        const int64_t max_sweeps = 2 * ((C + win - 1) / win) + 2;
+        for (int64_t it = 0; it < max_sweeps && taken < M; ++it) {
+            const bool in = tid < win;
+            int64_t c = hand + tid;
+            if (c >= C) c -= C;
+            const uint32_t st = in ? load_l2(&z.stamp[c]) : group;
+            const uint32_t rf = in ? load_l2(&z.ref[c]) : 1u;
+            const bool free_slot = in && st != group;
+            const bool take = free_slot && rf == 0u;
+            int64_t avail64;
+            const int32_t er = (int32_t)group_scan(take ? 1 : 0, &avail64, s_scan);
+            const int32_t need = M - taken, avail = (int32_t)avail64;
+            if (take && er == need - 1) s_u[2] = (uint32_t)tid;
+            __syncthreads();
+            const int cut = avail >= need ? (int)s_u[2] : win - 1;  // last slot the hand passes
+            if (tid <= cut) {
+                if (take && er < need) {
+                    s_victim[taken + er] = (int32_t)c;
+                    store_l2(&z.stamp[c], group);
+                } else if (free_slot && rf != 0u) {
+                    store_l2(&z.ref[c], 0u);  // second chance
+                }
+            }
+            taken += min(avail, need);
+            hand += cut + 1;
+            if (hand >= C) hand -= C;
+            __threadfence();
+            __syncthreads();
+        }
+        if (tid == 0) z.state[1] = (uint32_t)hand;
+        if (miss) {
+            const int32_t c = rank < taken ? s_victim[rank] : -1;
+            if (c >= 0) {
+                const int32_t old = z.node_of[c];
+                if (old >= 0) z.slot_of[old] = -1;
+                z.node_of[c] = n;
+                z.slot_of[n] = c;
+                store_l2(&z.ref[c], 1u);
+            } else {
+                z.slot_of[n] = -1;  // not reached while nb <= C; the rows stay fully masked
+            }
+            s_slot[tid] = c;
+        }
+        __syncthreads();
+        if (tid < nb) z.rows_src[tid] = lead >= 0 ? s_slot[lead] : s_slot[tid];
+    }
+    if (miss) {
+        z.miss_node[rank] = n;
+        z.miss_row[rank] = kCache ? s_slot[tid] : tid;
+        z.miss_off[rank] = off;
+    }
+    if (tid == 0) {
+        z.miss_off[M] = total;
+        *z.miss_count = M;
+    }
+}
+
+// Zero fill of the cache rows the group's misses build (grid.y = miss).
+__global__ void __launch_bounds__(kBlock) k_lazy_zero(LazyDev z, int64_t Wp) {
+    const int32_t u = (int32_t)blockIdx.y;
+    if (u >= *z.miss_count) return;
+    const int32_t row = z.miss_row[u];
+    const int64_t c = (int64_t)blockIdx.x * kBlock + threadIdx.x;  // 16-byte chunk of the row
+    if (row >= 0 && c < Wp / 2) reinterpret_cast<u32x4 *>(z.cache + (int64_t)row * Wp)[c] = u32x4{0u, 0u, 0u, 0u};
+}
+
+// The rows of the group's misses: valid[n] from the suffix probes of n's
+// subtree only.  Candidate i of miss u is node m = n + 1 + (i - miss_off[u]),
+// a descendant d = depth(m) - depth(n) bytes below n (preorder: the subtree is
+// [n, sub_end[n])).  When d <= max_len and the last d bytes of prefix(m), the
+// path from n to m, are a token string, its ids are valid at n and are set in
+// the row with 64-bit atomics; every token valid at n ends its walk at exactly
+// one such m.  Grid-stride over all candidates of the group.
+__global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, uint64_t *dest, int64_t stride) {
+    __shared__ int64_t s_off[kLazyGroup + 1];
+    __shared__ int32_t s_node[kLazyGroup];
+    __shared__ int32_t s_row[kLazyGroup];
+    __shared__ int32_t s_dep[kLazyGroup];
+    const int32_t M = *z.miss_count;
+    if (M <= 0) return;
+    const int64_t total = z.miss_off[M];
+    const int64_t first = (int64_t)blockIdx.x * kBlock;
+    if (first >= total) return;
+    for (int i = threadIdx.x; i <= M; i += kBlock) s_off[i] = z.miss_off[i];
+    for (int i = threadIdx.x; i < M; i += kBlock) {
+        const int32_t n = z.miss_node[i];
+        s_node[i] = n;
+        s_row[i] = z.miss_row[i];
+        s_dep[i] = t.depth[n];
+    }
+    __syncthreads();
+    unsigned long long *out = reinterpret_cast<unsigned long long *>(dest);
+    for (int64_t i = first + threadIdx.x; i < total; i += (int64_t)gridDim.x * kBlock) {
+        int lo = 0, hi = M - 1;  // the last miss whose candidates start at or before i
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_off[mid] <= i)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        const int32_t row = s_row[lo];
+        const int64_t m = (int64_t)s_node[lo] + 1 + (i - s_off[lo]);
+        const int d = t.depth[m] - s_dep[lo];
+        if (row < 0 || d > t.max_len || !has_len(t, d)) continue;
+        const int64_t pos = t.node_pos[m];
+        uint64_t wlo, whi;
+        load_window(t.blob, pos, wlo, whi);
+        uint64_t h = kHashSeed;
+        for (int k = 0; k < d; ++k) h = hash_step(h, k < kWin ? window_byte(wlo, whi, k) : (uint32_t)t.blob[pos - k]);
+        SlotPay mt;
+        if (probe(t, hash_final(h, (uint32_t)d), d, wlo, whi, pos, &mt) < 0) continue;
+        unsigned long long *r = out + (int64_t)row * stride;
+        int32_t v = mt.first;
+        for (int k = 0; k < (int)mt.count; ++k) {
+            atomicOr(r + (v >> 6), 1ull << (v & 63));
+            v = t.dup_next[v];
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) k_fill_u64(uint64_t *p, int64_t n, uint64_t value) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
+        p[i] = value;
+}
+
 inline unsigned grid_for(int64_t n, int per_block) {
     return (unsigned)((n + per_block - 1) / per_block);
 }
@@ -1054,6 +1291,53 @@ hipError_t launch_advance(const DevTables &t, const int32_t *node_ids, const int
     hipLaunchKernelGGL(k_advance, dim3(grid_for(B, kBlock)), dim3(kBlock), 0, s, t, node_ids, token_ids, B,
                        out);
     return hipGetLastError();
+}
+
+hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t *node_ids, int64_t nb,
+                             void *logits, int dtype, int64_t row_stride, hipStream_t s) {
+    if (nb <= 0) return hipSuccess;
+    if (nb > kLazyGroup || nb > z.C || !t.sub_end) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t, z, node_ids, (int32_t)nb);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lazy_zero, dim3(grid_for(t.Wp / 2, kBlock), (unsigned)nb), dim3(kBlock), 0, s, z, t.Wp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, z.cache, t.Wp);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // the masking reads the cache as a dense table indexed by slot
+    DevTables tc = t;
+    tc.table = z.cache;
+    tc.row_of = nullptr;
+    tc.N = z.C;
+    tc.R = z.C;
+    return launch_apply(tc, z.rows_src, nb, logits, dtype, row_stride, s);
+}
+
+hipError_t launch_lazy_export(const DevTables &t, const LazyDev &z, const int32_t *node_ids, int64_t nb,
+                              uint64_t *out, hipStream_t s) {
+    if (nb <= 0) return hipSuccess;
+    if (nb > kLazyGroup || !t.sub_end) return hipErrorInvalidValue;
+    const int64_t words = nb * t.W;
+    hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)std::min<int64_t>(grid_for(words, kBlock), 4096)), dim3(kBlock),
+                       0, s, out, words, 0ull);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lazy_assign<false>, dim3(1), dim3(kLazyGroup), 0, s, t, z, node_ids, (int32_t)nb);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, out, t.W);
+    return hipGetLastError();
+}
+
+hipError_t launch_lazy_reset(const DevTables &t, const LazyDev &z, hipStream_t s) {
+    hipError_t e = launch_fill_i32(z.slot_of, t.N, -1, s);
+    if (e == hipSuccess) e = launch_fill_i32(z.node_of, z.C, -1, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.stamp), z.C, 0, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.ref), z.C, 0, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.state), 2, 0, s);
+    return e;
 }
 
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,

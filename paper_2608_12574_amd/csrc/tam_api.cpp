@@ -193,9 +193,12 @@ void destroy_handle(tam_handle *h) {
 // The handle keeps valid lists (all nodes without a table; with tail
 // compression the tails' tokens longer than the probe window, if the vocabulary
 // has any) and/or a dense table.
-bool keeps_lists(const tam_handle *h) { return !h->dt.table || h->dt.tail_long; }
+bool is_lazy(const tam_handle *h) { return (h->flags & TAM_FLAG_LAZY_ROWS) != 0 && h->fmt_L < 0; }
+
+bool keeps_lists(const tam_handle *h) { return !is_lazy(h) && (!h->dt.table || h->dt.tail_long); }
 
 unsigned default_phases(const tam_handle *h) {
+    if (is_lazy(h)) return 0;                  // the cache is emptied; no rows are built
     if (h->fmt_L >= 0) return TAM_PHASE_MARK;  // k_format writes every word: no zero fill
     return (keeps_lists(h) ? unsigned(TAM_PHASE_LISTS) : 0u) | (h->dt.table ? unsigned(TAM_PHASE_TABLE) : 0u);
 }
@@ -212,6 +215,18 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
     TAM_HIP(hipStreamIsCapturing(s, &cap));
     const bool capturing = cap != hipStreamCaptureStatusNone;
     const bool timing = h->have_events && phases == default_phases(h) && !capturing;
+    if (is_lazy(h)) {  // rows built on demand: only the cache is reset
+        if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
+        TAM_HIP(tam::launch_lazy_reset(t, h->lazy, s));
+        if (timing) {
+            TAM_HIP(hipEventRecord(h->ev[1], s));
+            TAM_HIP(hipEventRecord(h->ev[2], s));
+            TAM_HIP(hipEventRecord(h->ev[3], s));
+            h->events_recorded = true;
+        }
+        if (h->work_done && !capturing) TAM_HIP(hipEventRecord(h->work_done, s));
+        return TAM_OK;
+    }
     const bool lists = (phases & TAM_PHASE_LISTS) != 0;
     const bool zero = (phases & TAM_PHASE_ZERO) && t.table;
     const bool mark = (phases & TAM_PHASE_MARK) && t.table;
@@ -279,14 +294,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     tam_status st;
     try {
         const auto t0 = std::chrono::steady_clock::now();
+        const bool lazy = (o.flags & TAM_FLAG_LAZY_ROWS) != 0;
         st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);
-        if (st == TAM_OK && (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_NO_TABLE))
+        if (st == TAM_OK && !lazy && (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_NO_TABLE))
             tam::split_tails(h);
         h->timing.host_trie_ms = ms_since(t0);
         // the lists (and their size bound) are needed without a table, or with
         // tail compression when tokens exceed the probe window
-        const bool lists = (o.flags & TAM_FLAG_NO_TABLE) ||
-                           ((o.flags & TAM_FLAG_TAIL_LISTS) && vocab->max_tok_len > tam::kWin);
+        const bool lists = !lazy && ((o.flags & TAM_FLAG_NO_TABLE) ||
+                                     ((o.flags & TAM_FLAG_TAIL_LISTS) && vocab->max_tok_len > tam::kWin));
         if (st == TAM_OK && lists) {
             h->entry_bound = tam::entry_upper_bound(h, vocab);
             if (h->entry_bound >= INT32_MAX) {
@@ -305,6 +321,13 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->V = vocab->V;
     h->W = vocab->W;
     h->Wp = (h->W + 7) & ~int64_t(7);  // rows 64-byte aligned
+    if (is_lazy(h)) {
+        if (o.cache_rows < 0) {
+            destroy_handle(h);
+            return fail(TAM_E_INVAL, "cache_rows must be >= 0");
+        }
+        h->cache_rows = std::max<int64_t>(1, std::min<int64_t>(o.cache_rows ? o.cache_rows : 4096, h->N));
+    }
     h->timing.dev_lists_ms = h->timing.dev_zero_ms = h->timing.dev_mark_ms = -1.f;
     h->timing.dev_total_ms = -1.f;
     if (host_only) {
@@ -325,7 +348,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     }
     h->own_alloc = alloc == nullptr;
     if (alloc) h->alloc = *alloc;
-    const bool want_table = !(h->flags & TAM_FLAG_NO_TABLE);
+    const bool lazy = is_lazy(h);
+    const bool want_table = !lazy && !(h->flags & TAM_FLAG_NO_TABLE);
     const bool tails = want_table && !h->tail_span.empty();
     const bool tail_long = tails && vocab->max_tok_len > tam::kWin;
     const bool want_lists = !want_table || tail_long;
@@ -341,23 +365,39 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_child_off = a.take<int32_t>(h->N + 1);
     const size_t o_child_byte = a.take<uint8_t>((int64_t)h->child_byte.size());
     const size_t o_child_node = a.take<int32_t>((int64_t)h->child_node.size());
-    const size_t o_hits = a.take<int32_t>(tam::kWin * h->N);
-    const size_t o_count = a.take<int32_t>(h->N);
-    const size_t o_row_ptr = a.take<int32_t>(h->N + 1);
-    const size_t o_cursor = a.take<int32_t>(h->N);
+    // the probe pass's tables (none when rows are built on demand)
+    const int64_t NP = lazy ? 0 : h->N;
+    const size_t o_hits = a.take<int32_t>(tam::kWin * NP);
+    const size_t o_count = a.take<int32_t>(NP);
+    const size_t o_row_ptr = a.take<int32_t>(NP + 1);
+    const size_t o_cursor = a.take<int32_t>(NP);
     const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
     const size_t o_tail_span = a.take<int32_t>(tails ? h->N : 0);
     const size_t o_row_of = a.take<int32_t>(tails ? h->N : 0);
     const size_t o_row_at = a.take<int32_t>(tails ? h->blob_bytes : 0);
-    const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(h->N));
-    h->npairs = tam::mark_blocks(h->N);
+    const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(NP));
+    h->npairs = lazy ? 0 : tam::mark_blocks(h->N);
     const size_t o_pairs = a.take<int32_t>(h->npairs);
+    // rows built on demand: subtree extents, the cache's bookkeeping, the
+    // scratch of one group of batch rows
+    const int64_t C = lazy ? h->cache_rows : 0, G = lazy ? tam::kLazyGroup : 0;
+    const size_t o_sub_end = a.take<int32_t>(lazy ? h->N : 0);
+    const size_t o_slot_of = a.take<int32_t>(lazy ? h->N : 0);
+    const size_t o_node_of = a.take<int32_t>(C);
+    const size_t o_stamp = a.take<uint32_t>(C);
+    const size_t o_ref = a.take<uint32_t>(C);
+    const size_t o_state = a.take<uint32_t>(2);
+    const size_t o_rows_src = a.take<int32_t>(G);
+    const size_t o_miss_node = a.take<int32_t>(G);
+    const size_t o_miss_row = a.take<int32_t>(G);
+    const size_t o_miss_off = a.take<int64_t>(G + 1);
+    const size_t o_miss_count = a.take<int32_t>(1);
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = nullptr;
-    const size_t table_bytes = (size_t)R * (size_t)h->Wp * sizeof(uint64_t);
-    if (base && want_table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
-    if (!base || (want_table && !table)) {
+    const size_t table_bytes = (size_t)(lazy ? C : R) * (size_t)h->Wp * sizeof(uint64_t);
+    if (base && (want_table || lazy)) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
+    if (!base || ((want_table || lazy) && !table)) {
         destroy_handle(h);
         return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
                                      " bytes requested)");
@@ -385,7 +425,23 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
     t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
-    t.table = table;
+    t.table = lazy ? nullptr : table;
+    t.sub_end = lazy ? reinterpret_cast<const int32_t *>(base + o_sub_end) : nullptr;
+    if (lazy) {
+        tam::LazyDev &z = h->lazy;
+        z.cache = table;
+        z.slot_of = reinterpret_cast<int32_t *>(base + o_slot_of);
+        z.node_of = reinterpret_cast<int32_t *>(base + o_node_of);
+        z.stamp = reinterpret_cast<uint32_t *>(base + o_stamp);
+        z.ref = reinterpret_cast<uint32_t *>(base + o_ref);
+        z.state = reinterpret_cast<uint32_t *>(base + o_state);
+        z.rows_src = reinterpret_cast<int32_t *>(base + o_rows_src);
+        z.miss_node = reinterpret_cast<int32_t *>(base + o_miss_node);
+        z.miss_row = reinterpret_cast<int32_t *>(base + o_miss_row);
+        z.miss_off = reinterpret_cast<int64_t *>(base + o_miss_off);
+        z.miss_count = reinterpret_cast<int32_t *>(base + o_miss_count);
+        z.C = C;
+    }
     t.tail_span = tails ? reinterpret_cast<const int32_t *>(base + o_tail_span) : nullptr;
     t.row_of = tails ? reinterpret_cast<const int32_t *>(base + o_row_of) : nullptr;
     t.row_at = tails ? reinterpret_cast<const int32_t *>(base + o_row_at) : t.node_at;
@@ -418,6 +474,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     if (e == hipSuccess && tails) e = up(o_tail_span, h->tail_span.data(), h->tail_span.size() * 4);
     if (e == hipSuccess && tails) e = up(o_row_of, h->row_of.data(), h->row_of.size() * 4);
     if (e == hipSuccess && tails) e = up(o_row_at, h->row_at.data(), h->row_at.size() * 4);
+    if (e == hipSuccess && lazy) e = up(o_sub_end, h->sub_end.data(), h->sub_end.size() * 4);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
@@ -636,6 +693,10 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
     g_err.clear();
     tam_status st = check_device_handle(h);
     if (st != TAM_OK) return st;
+    if (is_lazy(h)) {
+        if (phases != 0) return fail(TAM_E_STATE, "a handle with rows built on demand has only phase 0 (cache reset)");
+        return run_device_phase(h, 0, static_cast<hipStream_t>(stream));
+    }
     if (phases == 0) phases = default_phases(h);
     if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
     if ((phases & TAM_PHASE_TABLE) && !h->dt.table) return fail(TAM_E_STATE, "handle has no dense table");
@@ -666,6 +727,9 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
     const bool tails = !h->tail_span.empty();
     out->dense_rows = tails ? h->dense_rows : (h->flags & TAM_FLAG_NO_TABLE) ? 0 : h->N;
     out->dense_row = tails ? h->row_of.data() : nullptr;
+    out->cache_rows = is_lazy(h) ? h->cache_rows : 0;
+    out->subtree_end = h->sub_end.empty() ? nullptr : h->sub_end.data();
+    if (is_lazy(h)) out->dense_rows = 0;
     return TAM_OK;
 }
 
@@ -682,7 +746,16 @@ tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t 
     const size_t elem = dtype == TAM_DTYPE_BF16 ? 2 : 4;
     if ((reinterpret_cast<uintptr_t>(logits) % elem) != 0) return fail(TAM_E_INVAL, "logits are not element-aligned");
     TAM_HIP(hipGetLastError());
-    TAM_HIP(tam::launch_apply(h->dt, node_ids, B, logits, dtype, row_stride, static_cast<hipStream_t>(stream)));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (is_lazy(h)) {  // groups of rows: cache lookup, missing rows built, masking
+        const int64_t g = std::min<int64_t>(tam::kLazyGroup, h->lazy.C);
+        for (int64_t r0 = 0; r0 < B; r0 += g)
+            TAM_HIP(tam::launch_lazy_apply(h->dt, h->lazy, node_ids + r0, std::min(g, B - r0),
+                                           static_cast<uint8_t *>(logits) + r0 * row_stride * (int64_t)elem, dtype,
+                                           row_stride, s));
+        return TAM_OK;
+    }
+    TAM_HIP(tam::launch_apply(h->dt, node_ids, B, logits, dtype, row_stride, s));
     return TAM_OK;
 }
 
@@ -710,6 +783,12 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
     if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return fail(TAM_E_INVAL, "out must be 8-byte aligned");
     TAM_HIP(hipGetLastError());
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (is_lazy(h)) {
+        for (int64_t r0 = 0; r0 < n; r0 += tam::kLazyGroup)
+            TAM_HIP(tam::launch_lazy_export(h->dt, h->lazy, node_ids + r0, std::min<int64_t>(tam::kLazyGroup, n - r0),
+                                            out + r0 * h->W, s));
+        return TAM_OK;
+    }
     if (h->dt.table)
         TAM_HIP(tam::launch_export_dense(h->dt, node_ids, n, out, s));
     else
@@ -722,6 +801,7 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     tam_status st = check_device_handle(h);
     if (st != TAM_OK) return st;
     if (!out) return fail(TAM_E_INVAL, "out is null");
+    if (is_lazy(h)) return fail(TAM_E_STATE, "rows built on demand: no pass counts the valid pairs");
     hipStream_t s = static_cast<hipStream_t>(stream);
     // a table's marks count every pair (tails' too); without one the lists do
     std::vector<int32_t> part(h->dt.table ? (size_t)h->npairs : 0);

@@ -117,6 +117,7 @@ struct DevTables {
     const int32_t *tail_span;   // [N]
     const int32_t *row_of;      // [N] dense row of a node; a tail a: -1 - (nodes below a); null: row = node id
     const int32_t *row_at;      // [blob_bytes] row_of[node_at[p]]; equals node_at without row_of
+    const int32_t *sub_end;     // [N] one past the node's subtree (rows built on demand), or null
     int32_t *scan_tmp;          // block sums of the scan
     int64_t N, V, W, Wp;
     int64_t R;                  // dense rows (N for a full table, 0 without one)
@@ -130,6 +131,24 @@ struct DevTables {
     // character-position masks (tam_compile_format): classes of positions 0..L-1
     const uint8_t *classes;     // [L][32] bit rows, or null for a trie handle
     int32_t fmt_L;              // L, or -1 for a trie handle
+};
+
+// Rows built on demand (TAM_FLAG_LAZY_ROWS): the row cache, and the scratch
+// of one group of at most kLazyGroup batch rows.
+constexpr int kLazyGroup = 1024;
+struct LazyDev {
+    uint64_t *cache;       // [C][Wp] cached rows
+    int32_t *slot_of;      // [N] cache slot holding the node's row, or -1
+    int32_t *node_of;      // [C] node whose row a slot holds, or -1
+    uint32_t *stamp;       // [C] number of the group that last used the slot
+    uint32_t *ref;         // [C] CLOCK reference bit
+    uint32_t *state;       // [0] groups assigned so far, [1] CLOCK hand
+    int32_t *rows_src;     // [kLazyGroup] cache slot of each batch row of the group, -1 = dead
+    int32_t *miss_node;    // [kLazyGroup] nodes whose rows are built, in batch-row order
+    int32_t *miss_row;     // [kLazyGroup] their destination rows (slots, or output rows)
+    int64_t *miss_off;     // [kLazyGroup + 1] prefix sum of their subtree sizes (minus the node)
+    int32_t *miss_count;   // [1]
+    int64_t C;             // cache rows
 };
 
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
@@ -150,6 +169,15 @@ int64_t format_blocks(int64_t Wp);
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
                                hipStream_t s);
 int64_t scan_tmp_elems(int64_t N);
+// one group of nb <= min(kLazyGroup, C) batch rows: cache lookup and
+// replacement, rows of the misses built in the cache, then the masking
+hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t *node_ids, int64_t nb,
+                             void *logits, int dtype, int64_t row_stride, hipStream_t s);
+// one group of nb <= kLazyGroup rows built straight into out[nb][W] (no cache)
+hipError_t launch_lazy_export(const DevTables &t, const LazyDev &z, const int32_t *node_ids, int64_t nb,
+                              uint64_t *out, hipStream_t s);
+// empties the row cache
+hipError_t launch_lazy_reset(const DevTables &t, const LazyDev &z, hipStream_t s);
 
 }  // namespace tam
 
@@ -203,6 +231,7 @@ struct tam_handle {
 
     // host trie tables
     tam::hvec<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
+    tam::hvec<int32_t> sub_end;  // [N] with TAM_FLAG_LAZY_ROWS: one past the node's subtree
     tam::hvec<uint8_t> edge, is_final, blob, child_byte;
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
     tam::hvec<int32_t> tail_span, row_of, row_at;
@@ -211,6 +240,9 @@ struct tam_handle {
     int64_t fmt_L = -1;
     std::vector<uint8_t> classes;
     int64_t npairs = 0;  // per-block valid-pair counters in `pairs`
+    // rows built on demand (TAM_FLAG_LAZY_ROWS)
+    tam::LazyDev lazy{};
+    int64_t cache_rows = 0;
 
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};

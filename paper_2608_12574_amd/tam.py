@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG, "libtam.so")
 TAM_OK = 0
 TAM_DEAD = -1
 DTYPE_FP32, DTYPE_BF16 = 0, 1
-FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, FLAG_TAIL_LISTS = 1, 2, 4, 8
+FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, FLAG_TAIL_LISTS, FLAG_LAZY_ROWS = 1, 2, 4, 8, 16
 PHASE_LISTS, PHASE_ZERO, PHASE_MARK = 1, 2, 4
 PHASE_TABLE = PHASE_ZERO | PHASE_MARK
 
@@ -49,7 +49,7 @@ class Allocator(ctypes.Structure):
 
 
 class Options(ctypes.Structure):
-    _fields_ = [("terminator", ctypes.c_int), ("flags", ctypes.c_uint32)]
+    _fields_ = [("terminator", ctypes.c_int), ("flags", ctypes.c_uint32), ("cache_rows", ctypes.c_int64)]
 
 
 class Info(ctypes.Structure):
@@ -61,7 +61,8 @@ class Info(ctypes.Structure):
                 ("roots", ctypes.POINTER(ctypes.c_int32)), ("parent", ctypes.POINTER(ctypes.c_int32)),
                 ("depth", ctypes.POINTER(ctypes.c_int32)), ("edge_byte", ctypes.POINTER(ctypes.c_uint8)),
                 ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p),
-                ("dense_rows", ctypes.c_int64), ("dense_row", ctypes.POINTER(ctypes.c_int32))]
+                ("dense_rows", ctypes.c_int64), ("dense_row", ctypes.POINTER(ctypes.c_int32)),
+                ("cache_rows", ctypes.c_int64), ("subtree_end", ctypes.POINTER(ctypes.c_int32))]
 
 
 class Timing(ctypes.Structure):
@@ -194,6 +195,7 @@ class Handle:
         self.flags = int(info.flags)
         self.terminator = int(info.terminator)
         self.dense_rows = int(info.dense_rows)
+        self.cache_rows = int(info.cache_rows)
         self.roots = np.ctypeslib.as_array(info.roots, shape=(self.num_sets,)).copy()
         self.table_ptr = info.table
         self._info = info  # per-node host arrays are copied on first use
@@ -226,6 +228,13 @@ class Handle:
         if not self._info.dense_row:
             return None
         return self._host_array("dense_row")
+
+    @functools.cached_property
+    def subtree_end(self):
+        """One past the last node of each node's subtree (rows built on demand), or None."""
+        if not self._info.subtree_end:
+            return None
+        return self._host_array("subtree_end")
 
     # -- lifetime ------------------------------------------------------------
     def close(self):
@@ -278,7 +287,8 @@ class Handle:
         return out
 
     def rebuild(self, phases: int = 0, stream=None):
-        """Rerun device phases (PHASE_* mask; 0 = the handle's default)."""
+        """Rerun device phases (PHASE_* mask; 0 = the handle's default; with
+        FLAG_LAZY_ROWS, 0 empties the row cache)."""
         _check(lib().tam_rebuild(self._raw, phases, _stream_ptr(stream, self.host_only)), "tam_rebuild")
 
     def valid_pairs(self, stream=None) -> int:
@@ -333,13 +343,14 @@ class Vocab:
 
 
 def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, device=None,
-            stream=None) -> Handle:
+            stream=None, cache_rows: int = 0) -> Handle:
     """tam_compile over ``strings`` (list[bytes], or a packed pair (uint8 blob,
     int64 offsets[K+1])) and ``vocab`` (a ``Vocab`` or a list[bytes], token id =
     index).
 
     ``sets``: optional forest offsets (S+1 ints) splitting ``strings`` into S sets.
     With ``FLAG_HOST_ONLY`` no GPU is touched (host tables only).
+    ``cache_rows``: rows of the row cache with ``FLAG_LAZY_ROWS`` (0 = the default).
     """
     sb, so = csr(strings)
     set_arr = None
@@ -347,7 +358,7 @@ def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, d
     if sets is not None:
         set_arr = np.ascontiguousarray(np.asarray(sets, dtype=np.int64))
         S = set_arr.size - 1
-    opt = Options(terminator, flags)
+    opt = Options(terminator, flags, cache_rows)
     raw = ctypes.c_void_p()
     host_only = bool(flags & FLAG_HOST_ONLY)
     allocator = None

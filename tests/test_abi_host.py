@@ -264,3 +264,47 @@ def test_packed_strings_input(P):
     h2 = host(P, csr(w.strings), w.vocab)
     assert h1.num_nodes == h2.num_nodes
     assert np.array_equal(h1.parent, h2.parent) and np.array_equal(h1.edge_byte, h2.edge_byte)
+
+
+def _subtree_sizes(o):
+    size = np.ones(o.N, dtype=np.int64)
+    for n in range(o.N - 1, 0, -1):
+        if o.parent[n] >= 0:
+            size[o.parent[n]] += size[n]
+    return size
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_subtree_end_host_only(P, oracle_mod, cid):
+    """Rows built on demand scan a node's subtree as the preorder id range
+    [n, subtree_end[n]): it must equal n plus the subtree's size, counted from
+    the oracle's parent links."""
+    w = W.config(cid)
+    o = oracle_mod.Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY | P.FLAG_LAZY_ROWS)
+    assert np.array_equal(h.subtree_end, np.arange(o.N) + _subtree_sizes(o))
+    assert h.cache_rows == min(4096, o.N) and h.dense_rows == 0
+    assert P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY).subtree_end is None
+
+
+def test_subtree_end_forest_and_edges(P, oracle_mod):
+    strings, vocab, offs = W.mixed_forest()
+    o = oracle_mod.Oracle(strings, [b"x"], set_offsets=offs)
+    h = P.compile(strings, vocab, sets=offs, flags=P.FLAG_HOST_ONLY | P.FLAG_LAZY_ROWS, cache_rows=7)
+    assert np.array_equal(h.subtree_end, np.arange(o.N) + _subtree_sizes(o))
+    assert h.cache_rows == 7
+    for name, st, voc in W.edge_cases():
+        o = oracle_mod.Oracle(st, voc)
+        h = P.compile(st, voc, flags=P.FLAG_HOST_ONLY | P.FLAG_LAZY_ROWS, cache_rows=10 ** 9)
+        assert np.array_equal(h.subtree_end, np.arange(o.N) + _subtree_sizes(o)), name
+        assert h.cache_rows == o.N, name
+
+
+def test_lazy_rows_option_errors(P):
+    with pytest.raises(P.TamError) as e:
+        P.compile([b"ab"], [b"a"], flags=P.FLAG_HOST_ONLY | P.FLAG_LAZY_ROWS, cache_rows=-1)
+    assert e.value.status == -1
+    h = P.compile([b"ab"], [b"a"], flags=P.FLAG_HOST_ONLY | P.FLAG_LAZY_ROWS)
+    L = P.lib()
+    assert L.tam_rebuild(h._raw, 0, None) == -6  # host only: no device state
+    h.close()

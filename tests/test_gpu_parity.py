@@ -93,9 +93,11 @@ def full_check(P, strings, vocab, sets=None, flags=0, terminator=0x22):
     return h, o
 
 
-# the three representations: full dense table, lists only, tail compression
-FLAGS3 = [0, 2, 8]
-FLAG_IDS3 = ["dense", "no_table", "tail"]
+# the representations: full dense table, lists only, tail compression, rows
+# built on demand into a row cache
+LAZY = 16
+FLAGS = [0, 2, 8, LAZY]
+FLAG_IDS = ["dense", "no_table", "tail", "lazy"]
 
 
 def branching_nodes(o: Oracle) -> np.ndarray:
@@ -108,22 +110,23 @@ def branching_nodes(o: Oracle) -> np.ndarray:
     return cnt >= 2
 
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_worked_example(P, flags):
     vocab = [b"medical", b"_bill", b"_cod", b"_rec", b"ing", b"ords", b'"']
     h, o = full_check(P, [b"medical_billing", b"medical_coding", b"medical_records"], vocab, flags=flags)
-    assert h.valid_pairs() == 10  # rows 0,7,12,19,26 (1+3+1+1+1) + '"' at 15,22,30
+    if flags != LAZY:  # rows built on demand have no pass over all nodes to count
+        assert h.valid_pairs() == 10  # rows 0,7,12,19,26 (1+3+1+1+1) + '"' at 15,22,30
     rows = gpu_rows(h, [0, 7, 12, 19, 26])
     assert [int(r[0]) for r in rows] == [1, 0b1110, 0b10000, 0b10000, 0b100000]
 
 
 @pytest.mark.parametrize("name,strings,vocab", W.edge_cases(), ids=[e[0] for e in W.edge_cases()])
 def test_edge_suite(P, name, strings, vocab):
-    for flags in FLAGS3:
+    for flags in FLAGS:
         full_check(P, strings, vocab, flags=flags)
 
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_tiny_random_sets(P, flags):
     rng = np.random.default_rng(123)
     alphabet = np.frombuffer(b'ab"\x80', dtype=np.uint8)
@@ -145,12 +148,12 @@ def test_tiny_forest(P):
     flat = [s for g in sets for s in g]
     offs = np.cumsum([0] + [len(g) for g in sets])
     vocab = [b"a", b"b", b"c", b'"', b"ab", b"b\"", b"abc\"", b""]
-    for flags in FLAGS3:
+    for flags in FLAGS:
         full_check(P, flat, vocab, sets=offs, flags=flags)
 
 
 def test_other_terminator_and_high_bytes(P):
-    for flags in FLAGS3:
+    for flags in FLAGS:
         full_check(P, [b'x"y', b"x", b"\xff\x00"], [b"x", b'"', b'"y', b"|", b"y|", b"\xff", b"\x00|"],
                    terminator=ord("|"), flags=flags)
 
@@ -175,8 +178,10 @@ def sample_nodes(o: Oracle, k: int, seed: int):
 _oracles = {}
 
 
-@pytest.fixture(scope="module", params=[(1, 0), (2, 0), (3, 0), (4, 0), (1, 8), (2, 8), (3, 8), (4, 8)],
-                ids=["c1", "c2", "c3", "c4", "c1-tail", "c2-tail", "c3-tail", "c4-tail"])
+@pytest.fixture(scope="module", params=[(1, 0), (2, 0), (3, 0), (4, 0), (1, 8), (2, 8), (3, 8), (4, 8),
+                                        (1, LAZY), (2, LAZY), (3, LAZY), (4, LAZY)],
+                ids=["c1", "c2", "c3", "c4", "c1-tail", "c2-tail", "c3-tail", "c4-tail",
+                     "c1-lazy", "c2-lazy", "c3-lazy", "c4-lazy"])
 def compiled(request, P):
     cid, flags = request.param
     w = W.config(cid)
@@ -204,6 +209,8 @@ def test_config_table_properties(P, compiled):
     tail compression the table holds exactly the branching nodes (none final),
     and the lists and the table together count the full table's pairs."""
     w, o, h = compiled
+    if h.flags & LAZY:
+        pytest.skip("rows built on demand: no table")
     R = h.dense_rows
     table = h._alloc.live[h.table_ptr].view(torch.int64)[: R * h.row_stride_words].view(R, h.row_stride_words)
     nonempty = torch.zeros(R, dtype=torch.bool, device="cuda")
@@ -280,6 +287,17 @@ def test_config_rebuild_identical(P, compiled):
     w, o, h = compiled
     nodes = sample_nodes(o, 32, 7)
     before = gpu_rows(h, nodes)
+    if h.flags & LAZY:  # phase 0 empties the row cache; the rows come back the same
+        check_apply(P, h, o, nodes, "fp32", seed=8)
+        h.rebuild()
+        check_apply(P, h, o, nodes, "fp32", seed=9)
+        assert np.array_equal(gpu_rows(h, nodes), before)
+        for bad in (P.PHASE_MARK, P.PHASE_LISTS, P.PHASE_TABLE):
+            with pytest.raises(P.TamError):
+                h.rebuild(phases=bad)
+        with pytest.raises(P.TamError):
+            h.valid_pairs()
+        return
     M = h.valid_pairs()
     h.rebuild()
     assert np.array_equal(gpu_rows(h, nodes), before)
@@ -320,7 +338,7 @@ def test_shared_vocabulary(P):
         h.close()
 
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_long_and_duplicate_tokens(P, flags):
     """Tokens longer than the 16-byte probe window and duplicate token strings,
     at scale: sampled rows, a decode loop and both apply dtypes."""
@@ -339,7 +357,7 @@ def test_long_and_duplicate_tokens(P, flags):
     bits = np.unpackbits(rows.view(np.uint8), axis=1, bitorder="little")[:, : o.V]
     assert bits[:, long_ids].any(), "sample should contain valid long tokens"
     assert bits[:, 62000:].any(), "sample should contain valid duplicate tokens"
-    if flags != 2:  # the dense marks (and the tails' lists) and the sparse lists count the same pairs
+    if flags in (0, 8):  # the dense marks (and the tails' lists) and the sparse lists count the same pairs
         hs = P.compile(w.strings, w.vocab, flags=P.FLAG_NO_TABLE)
         assert h.valid_pairs() == hs.valid_pairs()
         hs.close()
@@ -377,12 +395,15 @@ def test_no_table_matches_dense_c4(P):
     check_apply(P, h, o, W.uniform_nodes(4, o.N, 16, 1), "fp32", seed=5)
 
 
-def test_forest_c5(P):
-    """Config 5: 256 per-query sets of 500 strings as one forest (sparse rows).
-    The oracle runs on sampled rows and on every row the 16-step decode visits."""
+@pytest.mark.parametrize("flags", [2, LAZY], ids=["no_table", "lazy"])
+def test_forest_c5(P, flags):
+    """Config 5: 256 per-query sets of 500 strings as one forest (sparse rows,
+    or rows built on demand into a 1024-row cache: 256 new rows per step evict
+    from the fifth step on).  The oracle runs on sampled rows and on every row
+    the 16-step decode visits."""
     w = W.config(5)
     o = Oracle(w.strings, w.vocab, set_offsets=w.set_offsets)
-    h = P.compile(w.strings, w.vocab, sets=w.set_offsets, flags=P.FLAG_NO_TABLE)
+    h = P.compile(w.strings, w.vocab, sets=w.set_offsets, flags=flags, cache_rows=1024)
     assert h.num_nodes == o.N and np.array_equal(h.roots, o.roots)
     nodes = sample_nodes(o, 64, 55)
     assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
@@ -391,7 +412,7 @@ def test_forest_c5(P):
     for step in range(w.decode_steps):
         rows = o.mask_rows(cur)
         assert np.array_equal(gpu_rows(h, cur), rows)
-        if step in (0, 7):
+        if step in (0, 7) or flags == LAZY:
             # roots: long lists (LDS bitmap); later steps: short lists (ballot);
             # both with many mixed chunks, written without a read
             check_apply(P, h, o, cur, "bf16", seed=50 + step)
@@ -403,7 +424,7 @@ def test_forest_c5(P):
     h.close()
 
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_forest_with_large_set(P, flags):
     """A large set (its host trie built in parts cut by first byte, with the
     empty string and strings that prefix others) among small sets: sampled
@@ -426,6 +447,58 @@ def test_forest_with_large_set(P, flags):
         cur = np.where((exp < 0) | (o.is_final[np.maximum(exp, 0)] == 1), start, exp).astype(np.int32)
     check_apply(P, h, o, cur, "bf16", seed=83)
     h.close()
+
+
+# ------------------------------------------------------ rows built on demand --
+
+@pytest.mark.parametrize("cache", [1, 7, 64])
+def test_lazy_cache_replacement(P, cache):
+    """Rows built on demand with a cache smaller than the batch: groups of at
+    most `cache` rows per assignment, evictions on every call, duplicate nodes
+    inside a group, dead and out-of-range ids, and a decode loop whose every
+    masked batch is checked against the oracle."""
+    w = W.config(2)
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=LAZY, cache_rows=cache)
+    assert h.cache_rows == cache and h.dense_rows == 0 and h.row_stride_words == 0
+    rng = np.random.default_rng([cache, 17])
+    start = W.uniform_nodes(2, o.N, 40, cache)
+    start[:4] = 0
+    start[4:8] = start[8:12]                      # the same nodes twice in one batch
+    start = np.where(o.is_final[start] == 1, 0, start).astype(np.int32)
+    cur = start.copy()
+    for step in range(8):
+        batch = cur.copy()
+        batch[12], batch[13] = -1, o.N + 3         # dead rows are masked entirely
+        check_apply(P, h, o, batch, "fp32" if step % 2 else "bf16", seed=step)
+        rows = o.mask_rows(cur)
+        toks = W.choose_valid_tokens(rng, rows, o.V)
+        exp = o.advance(cur, toks)
+        assert np.array_equal(gpu_advance(h, cur, toks), exp)
+        cur = np.where((exp < 0) | (o.is_final[np.maximum(exp, 0)] == 1), start, exp).astype(np.int32)
+    h.close()
+
+
+def test_lazy_large_batch_hits_and_reset(P):
+    """Batches larger than one group of 1024 rows; a second call on the same
+    nodes finds every row in the cache; a reset empties it; two handles do not
+    share cache state."""
+    w = W.config(2)
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=LAZY)
+    h2 = P.compile(w.strings, w.vocab, flags=LAZY, cache_rows=300)
+    nodes = W.uniform_nodes(2, o.N, 2500, 9)
+    nodes[::97] = 0
+    check_apply(P, h, o, nodes, "bf16", seed=1)
+    check_apply(P, h, o, nodes, "bf16", seed=2)
+    check_apply(P, h2, o, nodes[:1500], "fp32", seed=3)
+    check_apply(P, h, o, nodes[::-1].copy(), "fp32", seed=4)
+    h.rebuild()
+    check_apply(P, h, o, nodes[:100], "fp32", seed=5)
+    check_apply(P, h2, o, nodes[1000:], "bf16", seed=6)
+    assert np.array_equal(gpu_rows(h2, nodes[:700]), o.mask_rows(nodes[:700]))
+    h.close()
+    h2.close()
 
 
 # ------------------------------------------------------ fixed-format strings --
@@ -506,7 +579,7 @@ def test_format_decode_reaches_final(P, c4_vocab):
 
 # ------------------------------------------------------------ layouts / edges --
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_ragged_vocab_and_strides(P, flags):
     w = W.config(1)
     vocab = w.vocab[:1037]                      # V not a multiple of 8 or 64
@@ -538,7 +611,7 @@ def test_many_rows_grid_split(P):
     exp = np.zeros((B, 128), dtype=bool)
     live = (nodes >= 0) & (nodes < o.N)
     exp[live] = valid[nodes[live]]
-    for flags in FLAGS3:
+    for flags in FLAGS:
         h = P.compile(strings, vocab, flags=flags)
         x = torch.zeros((B, 128), dtype=torch.bfloat16, device="cuda")
         h.apply_mask(ids, x)
@@ -561,7 +634,7 @@ def test_c_abi_with_library_allocator(P):
     sb, so = csr(w.strings)
     voc = ctypes.c_void_p()
     assert L.tam_vocab_create(tb.ctypes.data, to.ctypes.data, len(w.vocab), 0, None, None, ctypes.byref(voc)) == 0
-    for flags in FLAGS3:
+    for flags in FLAGS:
         h = ctypes.c_void_p()
         opt = Options(0x22, flags)
         assert L.tam_compile_vocab(sb.ctypes.data, so.ctypes.data, len(w.strings), voc, None, 0, ctypes.byref(opt),
@@ -586,7 +659,7 @@ def test_c_abi_with_library_allocator(P):
     L.tam_vocab_destroy(voc)
 
 
-@pytest.mark.parametrize("flags", FLAGS3, ids=FLAG_IDS3)
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_graph_capture_replays(P, flags):
     """rebuild + apply + advance captured in a HIP graph: every replay, with eager
     work and synchronisation between replays, gives the eager results."""
