@@ -9,11 +9,14 @@ One step = one pass of the whole device hot path over one batch:
   3. the state advance of the B rows.
 Inputs (trie and vocabulary tables, node ids, tokens, logits) are resident in
 HBM before the timed region; the host trie build and the uploads are reported
-separately as the end-to-end compile time.
+separately as the end-to-end compile time, which starts from the strings in
+the C ABI's CSR form (packing a Python list into it is timed on its own).
 
 The same line also reports the workload under tail compression
 (TAM_FLAG_TAIL_LISTS: dense rows only for branching nodes, tails read back from
-the probe's hits), which gives bit-identical masks from a much smaller table.
+the probe's hits), which gives bit-identical masks from a much smaller table,
+and with rows built on demand (TAM_FLAG_LAZY_ROWS: no mask at compile, a row
+cache filled by the decode steps).
 
 value = (node, token) pairs resolved per second = N * V per step / step time.
 
@@ -99,6 +102,12 @@ class Bench:
                      .to(self.logit_dtype) for _ in range(self.nbuf)]
         self.voc = None
         self.vocab_ms = None
+        # the strings in the C ABI's input form (CSR bytes + offsets); packing a
+        # Python list is timed on its own
+        from paper_2608_12574_amd.tam import csr
+        t0 = time.perf_counter()
+        self.packed = csr(w.strings)
+        self.pack_ms = (time.perf_counter() - t0) * 1e3
 
     def event(self):
         return self.torch.cuda.Event(enable_timing=True)
@@ -119,7 +128,7 @@ class Bench:
         def timed(vocab):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            hh = P.compile(w.strings, vocab, sets=w.set_offsets, flags=flags)
+            hh = P.compile(self.packed, vocab, sets=w.set_offsets, flags=flags)
             torch.cuda.synchronize()
             return hh, (time.perf_counter() - t0) * 1e3
 
@@ -180,7 +189,7 @@ class Bench:
 
         # the timed steps run on a handle without timing events and with no
         # events of their own (event records between the kernels slow them)
-        timed_h = P.compile(w.strings, self.voc, sets=w.set_offsets, flags=FLAGS[rep])
+        timed_h = P.compile(self.packed, self.voc, sets=w.set_offsets, flags=FLAGS[rep])
         hh = h
         h = timed_h
         for i in range(warmup):
@@ -304,6 +313,75 @@ class Bench:
         return h, res
 
 
+    def measure_lazy(self, h_ref, reps=5):
+        """Rows built on demand (TAM_FLAG_LAZY_ROWS): compile end to end with the
+        vocabulary cached (no mask is computed), then a decode of up to 32 steps
+        from the workload's start rows, mask apply + advance per step, timed with
+        the row cache emptied first (every row built at its first use) and again
+        with the cache kept; the main representation's handle runs the same
+        trajectory."""
+        torch, P, W, w, dev = self.torch, self.P, self.W, self.w, self.dev
+        S = max(1, min(w.decode_steps, 32))
+        e2e, hz = [], None
+        for _ in range(3):
+            if hz is not None:
+                hz.close()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            hz = P.compile(self.packed, self.voc, sets=w.set_offsets, flags=P.FLAG_LAZY_ROWS | P.FLAG_TIMING)
+            torch.cuda.synchronize()
+            e2e.append((time.perf_counter() - t0) * 1e3)
+        N, B = hz.num_nodes, self.B
+        if w.node_mode == "uniform":
+            start = W.uniform_nodes(w.config_id, N, B)
+        elif w.node_mode == "set_roots":
+            start = hz.roots[:B].astype(np.int32)
+        else:
+            start = np.zeros(B, dtype=np.int32)
+        ids0 = torch.as_tensor(start, device=dev)
+        fin = torch.as_tensor(hz.is_final.astype(np.bool_), device=dev)
+        traj, toks, cur = [], [], ids0.clone()
+        for s in range(S):
+            lg = self.fresh_logits(1 + s)
+            hz.apply_mask(cur, lg)
+            tok = lg.float().argmax(dim=1).to(torch.int32)
+            nxt = hz.advance(cur, tok)
+            traj.append(cur.clone())
+            toks.append(tok)
+            cur = torch.where((nxt < 0) | fin[nxt.clamp(min=0).long()], ids0, nxt)
+            del lg
+        distinct = int(np.unique(torch.cat(traj).cpu().numpy()).size)
+        out = torch.empty_like(ids0)
+
+        def run(hh, reset):
+            ts = []
+            for r in range(reps):
+                if reset:
+                    hh.rebuild()
+                e0, e1 = self.event(), self.event()
+                e0.record()
+                for s in range(S):
+                    hh.apply_mask(traj[s], self.bufs[(r * S + s) % self.nbuf])
+                    hh.advance(traj[s], toks[s], out=out)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3 / S)
+            return float(np.median(ts))
+
+        cold, warm, ref = run(hz, True), run(hz, False), run(h_ref, False)
+        res = {"cache_rows": hz.cache_rows, "device_bytes": hz.device_bytes,
+               "compile_warm_ms": round(min(e2e), 3), "compile_warm_all": [round(x, 3) for x in e2e],
+               "compile_phases": hz.timing(),
+               "decode_steps": S, "batch": B, "distinct_rows": distinct,
+               "step_us_cache_emptied": round(cold, 2), "step_us_cache_kept": round(warm, 2),
+               "step_us_main_repr": round(ref, 2)}
+        hz.close()
+        print(f"[bench] lazy rows: compile {min(e2e):.2f} ms, {S} steps x {B} rows ({distinct} distinct): "
+              f"{cold:.1f} us/step from an empty cache, {warm:.1f} us/step cache kept, "
+              f"{ref:.1f} us/step precomputed", flush=True)
+        return res
+
+
 def cpu_baseline(h, w, V, N, seconds, torch, dev):
     """The oracle on a bounded sample of rows, one thread; the same rows from the
     GPU must be bit-identical."""
@@ -383,6 +461,7 @@ def main():
     cpu, exact = (None, None)
     if not args.no_cpu_baseline:
         cpu, exact = cpu_baseline(h, w, V, main_res["N"], args.cpu_seconds, torch, dev)
+    lazy = None if args.no_secondary else bench.measure_lazy(h)
     h.close()
 
     # character-position masks of fixed formats over the same vocabulary
@@ -443,11 +522,13 @@ def main():
                            "algorithmic_bytes": main_res["apply"]["bytes"],
                            "avg_launch_us": main_res["apply"]["us"]},
         "cpu_baseline": cpu,
-        "compile_ms": dict(main_res["compile_ms"], vocabulary_build_once=round(bench.vocab_ms, 3)),
+        "compile_ms": dict(main_res["compile_ms"], vocabulary_build_once=round(bench.vocab_ms, 3),
+                           python_list_packing=round(bench.pack_ms, 3)),
         "apply": main_res["apply"],
         "advance_us": main_res["advance_us"],
         "device_bytes": main_res["device_bytes"],
         "tail_compression": secondary,
+        "lazy_rows": lazy,
         "char_position_masks": formats,
         "fill_GBps_4GiB": round(fill_gbps, 1),
         "bit_exact_sampled_rows": exact,

@@ -938,11 +938,13 @@ __global__ void __launch_bounds__(kBlock) k_export_tail(DevTables t, const int32
 
 // -------------------------------------------------------- rows on demand ---
 
-constexpr int kLazyProbeBlocks = 1024;  // grid of k_lazy_probe (grid-stride)
+constexpr int kLazyProbeBlocks = 512;  // grid of k_lazy_probe (grid-stride)
 
 // Exclusive prefix sum of one value per thread over a block of kLazyGroup
-// threads; *total receives the sum.  sh holds kLazyGroup / kWave values.
+// threads; *total receives the sum.  sh holds kLazyGroup / kWave + 1 values.
+// Waves scan their lanes with shuffles; wave 0 then scans the wave totals.
 __device__ __forceinline__ int64_t group_scan(int64_t x, int64_t *total, int64_t *sh) {
+    constexpr int kWaves = kLazyGroup / kWave;
     const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
     int64_t inc = x;
     for (int o = 1; o < kWave; o <<= 1) {
@@ -951,24 +953,32 @@ __device__ __forceinline__ int64_t group_scan(int64_t x, int64_t *total, int64_t
     }
     if (lane == kWave - 1) sh[wid] = inc;
     __syncthreads();
-    int64_t before = 0, all = 0;
-    for (int w = 0; w < kLazyGroup / kWave; ++w) {
-        const int64_t v = sh[w];
-        if (w < wid) before += v;
-        all += v;
+    if (wid == 0) {
+        const int64_t v = lane < kWaves ? sh[lane] : 0;
+        int64_t vi = v;
+        for (int o = 1; o < kWaves; o <<= 1) {
+            const int64_t y = __shfl_up(vi, o, kWave);
+            if (lane >= o) vi += y;
+        }
+        if (lane < kWaves) sh[lane] = vi - v;
+        if (lane == kWaves - 1) sh[kWaves] = vi;
     }
     __syncthreads();
-    *total = all;
+    const int64_t before = sh[wid];
+    *total = sh[kWaves];
+    __syncthreads();
     return before + inc - x;
 }
 
-// Cache words that other waves of the block read back after a barrier go
-// through L2 (device-scope atomics), not through this CU's L1.
-__device__ __forceinline__ uint32_t load_l2(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Cache words that other waves of the same block read back after a barrier:
+// work-group scope (the block's waves share one CU and its L1), ordered by the
+// work-group fences of __syncthreads.  Nothing outside the block reads them
+// before the kernel ends.
+__device__ __forceinline__ uint32_t load_wg(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-__device__ __forceinline__ void store_l2(uint32_t *p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void store_wg(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Which rows a group of nb batch rows needs built, one block of kLazyGroup
@@ -989,16 +999,17 @@ __device__ __forceinline__ void store_l2(uint32_t *p, uint32_t v) {
 //      its slot (rows_src).
 // !kCache (tam_export_rows): every live row is built, into output row b.
 template <bool kCache>
-__global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev z,
-                                                            const int32_t *__restrict__ ids, int32_t nb) {
+__global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__restrict__ sub_end, int64_t N,
+                                                            LazyDev z, const int32_t *__restrict__ ids,
+                                                            int32_t nb) {
     __shared__ int32_t s_slot[kLazyGroup];
     __shared__ int32_t s_victim[kLazyGroup];
-    __shared__ int64_t s_scan[kLazyGroup / kWave];
+    __shared__ int64_t s_scan[kLazyGroup / kWave + 1];
     __shared__ uint32_t s_u[4];  // group number, hand, cut, counter wrapped
     const int tid = threadIdx.x;
     const int32_t n = tid < nb ? ids[tid] : -1;
-    const bool live = n >= 0 && (int64_t)n < t.N;
-    const int64_t below = live ? (int64_t)t.sub_end[n] - n - 1 : 0;
+    const bool live = n >= 0 && (int64_t)n < N;
+    const int64_t below = live ? (int64_t)sub_end[n] - n - 1 : 0;
     int32_t slot = -1, lead = -1;
     bool miss = live;
     uint32_t group = 0;
@@ -1022,13 +1033,12 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
         __syncthreads();
         group = s_u[0];
         if (s_u[3]) {  // the group counter wrapped: forget every stamp
-            for (int64_t c = tid; c < z.C; c += kLazyGroup) store_l2(&z.stamp[c], 0u);
-            __threadfence();
+            for (int64_t c = tid; c < z.C; c += kLazyGroup) store_wg(&z.stamp[c], 0u);
             __syncthreads();
         }
         if (slot >= 0) {
-            store_l2(&z.stamp[slot], group);
-            store_l2(&z.ref[slot], 1u);
+            store_wg(&z.stamp[slot], group);
+            store_wg(&z.ref[slot], 1u);
         }
     }
     s_slot[tid] = slot;
@@ -1037,8 +1047,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
     const int64_t off = group_scan(miss ? below : 0, &total, s_scan);
     const int32_t M = (int32_t)nmiss;
     if (kCache) {
-        __threadfence();  // the hits' stamps before the sweeps read them
-        __syncthreads();
+        __syncthreads();  // the hits' stamps before the sweeps read them
         const int64_t C = z.C;
         const int win = (int)min<int64_t>(C, kLazyGroup);
         int64_t hand = s_u[1];
@@ -1048,8 +1057,8 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
             const bool in = tid < win;
             int64_t c = hand + tid;
             if (c >= C) c -= C;
-            const uint32_t st = in ? load_l2(&z.stamp[c]) : group;
-            const uint32_t rf = in ? load_l2(&z.ref[c]) : 1u;
+            const uint32_t st = in ? load_wg(&z.stamp[c]) : group;
+            const uint32_t rf = in ? load_wg(&z.ref[c]) : 1u;
             const bool free_slot = in && st != group;
             const bool take = free_slot && rf == 0u;
             int64_t avail64;
@@ -1061,15 +1070,14 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
             if (tid <= cut) {
                 if (take && er < need) {
                     s_victim[taken + er] = (int32_t)c;
-                    store_l2(&z.stamp[c], group);
+                    store_wg(&z.stamp[c], group);
                 } else if (free_slot && rf != 0u) {
-                    store_l2(&z.ref[c], 0u);  // second chance
+                    store_wg(&z.ref[c], 0u);  // second chance
                 }
             }
             taken += min(avail, need);
             hand += cut + 1;
             if (hand >= C) hand -= C;
-            __threadfence();
             __syncthreads();
         }
         if (tid == 0) z.state[1] = (uint32_t)hand;
@@ -1080,7 +1088,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
                 if (old >= 0) z.slot_of[old] = -1;
                 z.node_of[c] = n;
                 z.slot_of[n] = c;
-                store_l2(&z.ref[c], 1u);
+                store_wg(&z.ref[c], 1u);
             } else {
                 z.slot_of[n] = -1;  // not reached while nb <= C; the rows stay fully masked
             }
@@ -1100,13 +1108,15 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(DevTables t, LazyDev
     }
 }
 
-// Zero fill of the cache rows the group's misses build (grid.y = miss).
+// Zero fill of the cache rows the group's misses build: one block per miss
+// (grid = group size, blocks past the misses exit), 16-byte stores.
 __global__ void __launch_bounds__(kBlock) k_lazy_zero(LazyDev z, int64_t Wp) {
-    const int32_t u = (int32_t)blockIdx.y;
+    const int32_t u = (int32_t)blockIdx.x;
     if (u >= *z.miss_count) return;
     const int32_t row = z.miss_row[u];
-    const int64_t c = (int64_t)blockIdx.x * kBlock + threadIdx.x;  // 16-byte chunk of the row
-    if (row >= 0 && c < Wp / 2) reinterpret_cast<u32x4 *>(z.cache + (int64_t)row * Wp)[c] = u32x4{0u, 0u, 0u, 0u};
+    if (row < 0) return;
+    u32x4 *p = reinterpret_cast<u32x4 *>(z.cache + (int64_t)row * Wp);
+    for (int64_t c = threadIdx.x; c < Wp / 2; c += kBlock) p[c] = u32x4{0u, 0u, 0u, 0u};
 }
 
 // The rows of the group's misses: valid[n] from the suffix probes of n's
@@ -1154,10 +1164,17 @@ __global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, u
         uint64_t h = kHashSeed;
         for (int k = 0; k < d; ++k) h = hash_step(h, k < kWin ? window_byte(wlo, whi, k) : (uint32_t)t.blob[pos - k]);
         SlotPay mt;
-        if (probe(t, hash_final(h, (uint32_t)d), d, wlo, whi, pos, &mt) < 0) continue;
+        const int32_t sl = probe(t, hash_final(h, (uint32_t)d), d, wlo, whi, pos, &mt);
+        if (sl < 0) continue;
+        const int32_t hx = hit_of_slot(sl, mt.first, mt.count);
         unsigned long long *r = out + (int64_t)row * stride;
-        int32_t v = mt.first;
-        for (int k = 0; k < (int)mt.count; ++k) {
+        if (hx >= 0) {  // one token id (the common case)
+            atomicOr(r + (hx >> 6), 1ull << (hx & 63));
+            continue;
+        }
+        const SlotPay pm = t.pay[sl];  // a string with several ids
+        int32_t v = pm.first;
+        for (int k = 0; k < (int)pm.count; ++k) {
             atomicOr(r + (v >> 6), 1ull << (v & 63));
             v = t.dup_next[v];
         }
@@ -1297,10 +1314,11 @@ hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t
                              void *logits, int dtype, int64_t row_stride, hipStream_t s) {
     if (nb <= 0) return hipSuccess;
     if (nb > kLazyGroup || nb > z.C || !t.sub_end) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t, z, node_ids, (int32_t)nb);
+    hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.N, z, node_ids,
+                       (int32_t)nb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_zero, dim3(grid_for(t.Wp / 2, kBlock), (unsigned)nb), dim3(kBlock), 0, s, z, t.Wp);
+    hipLaunchKernelGGL(k_lazy_zero, dim3((unsigned)nb), dim3(kBlock), 0, s, z, t.Wp);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, z.cache, t.Wp);
@@ -1324,7 +1342,8 @@ hipError_t launch_lazy_export(const DevTables &t, const LazyDev &z, const int32_
                        0, s, out, words, 0ull);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_assign<false>, dim3(1), dim3(kLazyGroup), 0, s, t, z, node_ids, (int32_t)nb);
+    hipLaunchKernelGGL(k_lazy_assign<false>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.N, z, node_ids,
+                       (int32_t)nb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, out, t.W);
