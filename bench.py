@@ -120,6 +120,31 @@ class Bench:
         g.manual_seed(1000 + seed)
         return torch.randn((self.B, self.V), generator=g, device=self.dev).to(self.logit_dtype)
 
+    def graph_us(self, call, n, replays=10):
+        """Microseconds per call of `call` (a library call that only launches
+        kernels), captured n times in a HIP graph and replayed."""
+        torch = self.torch
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            call()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                call()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = self.event(), self.event()
+        e0.record()
+        for _ in range(replays):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        del g
+        return e0.elapsed_time(e1) * 1e3 / (n * replays)
+
     def compile_times(self, flags, cold_runs):
         """End-to-end compile (host trie + vocabulary + upload + device), cold
         (vocabulary tables built by the call) and warm (from a Vocab built once)."""
@@ -270,7 +295,11 @@ class Bench:
             h.advance(ids, toks, out=out)
         a1.record()
         torch.cuda.synchronize()
-        advance_us = a0.elapsed_time(a1) * 1e3 / 1000
+        advance_eager_us = a0.elapsed_time(a1) * 1e3 / 1000
+        # the same calls replayed from a HIP graph: the device time without the
+        # Python call overhead that bounds the eager loop
+        advance_us = self.graph_us(lambda: h.advance(ids, toks, out=out), 100)
+        apply_graph_us = self.graph_us(lambda: h.apply_mask(ids, bufs[0]), 100)
 
         # the dominant compile kernel and its algorithmic bytes
         if rep == "lists":
@@ -307,9 +336,11 @@ class Bench:
                            "frac_of_hbm_roofline": round(apply_bytes / (root_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
                           if root_us is not None else None)},
             "advance_us": round(advance_us, 3),
+            "advance_us_eager": round(advance_eager_us, 3),
+            "apply_us_graph": round(apply_graph_us, 3),
         }
-        print(f"[bench] {rep}: apply {apply_us:.2f} us ({apply_gbps:.0f} GB/s), advance {advance_us:.2f} us",
-              flush=True)
+        print(f"[bench] {rep}: apply {apply_us:.2f} us ({apply_gbps:.0f} GB/s; graph-replayed {apply_graph_us:.2f} us), "
+              f"advance {advance_us:.2f} us (graph-replayed; eager loop {advance_eager_us:.2f} us)", flush=True)
         return h, res
 
 
@@ -368,17 +399,49 @@ class Bench:
                 ts.append(e0.elapsed_time(e1) * 1e3 / S)
             return float(np.median(ts))
 
+        def run_graph(hh, reset):
+            """The S steps captured once in a HIP graph and replayed."""
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                for st in range(S):
+                    hh.apply_mask(traj[st], self.bufs[st % self.nbuf])
+                    hh.advance(traj[st], toks[st], out=out)
+            torch.cuda.current_stream().wait_stream(s)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for st in range(S):
+                    hh.apply_mask(traj[st], self.bufs[st % self.nbuf])
+                    hh.advance(traj[st], toks[st], out=out)
+            ts = []
+            for r in range(reps):
+                if reset:
+                    hh.rebuild()
+                e0, e1 = self.event(), self.event()
+                e0.record()
+                g.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3 / S)
+            del g
+            return float(np.median(ts))
+
         cold, warm, ref = run(hz, True), run(hz, False), run(h_ref, False)
+        gcold, gwarm, gref = run_graph(hz, True), run_graph(hz, False), run_graph(h_ref, False)
         res = {"cache_rows": hz.cache_rows, "device_bytes": hz.device_bytes,
                "compile_warm_ms": round(min(e2e), 3), "compile_warm_all": [round(x, 3) for x in e2e],
                "compile_phases": hz.timing(),
                "decode_steps": S, "batch": B, "distinct_rows": distinct,
                "step_us_cache_emptied": round(cold, 2), "step_us_cache_kept": round(warm, 2),
-               "step_us_main_repr": round(ref, 2)}
+               "step_us_main_repr": round(ref, 2),
+               "graph_replayed": {"step_us_cache_emptied": round(gcold, 2), "step_us_cache_kept": round(gwarm, 2),
+                                  "step_us_main_repr": round(gref, 2)}}
         hz.close()
         print(f"[bench] lazy rows: compile {min(e2e):.2f} ms, {S} steps x {B} rows ({distinct} distinct): "
               f"{cold:.1f} us/step from an empty cache, {warm:.1f} us/step cache kept, "
-              f"{ref:.1f} us/step precomputed", flush=True)
+              f"{ref:.1f} us/step precomputed; graph-replayed {gcold:.1f} / {gwarm:.1f} / {gref:.1f} us/step",
+              flush=True)
         return res
 
 

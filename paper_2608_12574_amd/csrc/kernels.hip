@@ -17,7 +17,7 @@
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
 //   k_apply  -- write-mostly masking of [B, V] logits.
-//   k_advance-- B byte walks over the child tables.
+//   k_advance-- B byte walks over the child tables, one wave per row.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
 // Rows built on demand (lazy computation with a bounded cache, Appendix):
@@ -792,105 +792,86 @@ __global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restr
 
 // --------------------------------------------------------------- advance ---
 
-// 16 bytes base[pos .. pos+16) at any alignment (byte j of (lo, hi) = base[pos+j]),
-// from five aligned dword loads; reads up to 3 bytes before and 4 after.
-__device__ __forceinline__ void load16(const uint8_t *base, int64_t pos, uint64_t &lo, uint64_t &hi) {
-    const int64_t a = pos & ~int64_t(3);
-    const uint32_t *w = reinterpret_cast<const uint32_t *>(base + a);
-    const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
-    const uint32_t sh = (uint32_t)(pos - a) * 8u;
-    const uint32_t x0 = (uint32_t)((((uint64_t)w1 << 32) | w0) >> sh);
-    const uint32_t x1 = (uint32_t)((((uint64_t)w2 << 32) | w1) >> sh);
-    const uint32_t x2 = (uint32_t)((((uint64_t)w3 << 32) | w2) >> sh);
-    const uint32_t x3 = (uint32_t)((((uint64_t)w4 << 32) | w3) >> sh);
-    lo = ((uint64_t)x1 << 32) | x0;
-    hi = ((uint64_t)x3 << 32) | x2;
-}
-
-// Index of the first byte of (lo, hi) equal to c (16 if none).
-__device__ __forceinline__ int first_byte(uint64_t lo, uint64_t hi, uint32_t c) {
-    const uint64_t ones = 0x0101010101010101ull, highs = 0x8080808080808080ull;
-    uint64_t y = lo ^ (ones * c);
-    uint64_t z = (y - ones) & ~y & highs;  // exact for the lowest zero byte
-    if (z) return __builtin_ctzll(z) >> 3;
-    y = hi ^ (ones * c);
-    z = (y - ones) & ~y & highs;
-    return z ? 8 + (__builtin_ctzll(z) >> 3) : 16;
-}
-
-// Number of equal leading bytes of two 16-byte values.
-__device__ __forceinline__ int common_prefix(uint64_t alo, uint64_t ahi, uint64_t blo, uint64_t bhi) {
-    uint64_t x = alo ^ blo;
-    if (x) return __builtin_ctzll(x) >> 3;
-    x = ahi ^ bhi;
-    return x ? 8 + (__builtin_ctzll(x) >> 3) : 16;
-}
-
-// Child of node n along byte c (binary search over its sorted child bytes), or dead.
-__device__ __forceinline__ int32_t child(const DevTables &t, int32_t n, uint32_t c) {
-    int32_t lo = t.child_off[n], hi = t.child_off[n + 1];
-    while (lo < hi) {
-        const int32_t mid = (lo + hi) >> 1;
-        const uint32_t cb = t.child_byte[mid];
-        if (cb < c)
-            lo = mid + 1;
-        else if (cb > c)
-            hi = mid;
-        else
-            return t.child_node[mid];
-    }
-    return TAM_DEAD;
-}
-
-// The extended transition function over one token per lane.  After each child
-// step the walk follows the node's owner string (the first set string through
-// it, stored in the blob right after the node's edge byte), comparing up to 16
-// token bytes at a time and jumping to node_at of the last matching position;
-// the comparison never runs past that string's terminator.  A token needs one
-// child search per point where it leaves the owner string's path, usually one
-// or two, instead of one per byte.
+// The extended transition function, one wave per batch row.  A child step
+// compares up to 64 of the node's sorted child bytes at once (one ballot)
+// instead of a binary search.  Between child steps the walk follows the
+// node's owner string (the first set string through it, stored in the blob
+// right after the node's edge byte): lane j compares token byte i+j with the
+// string's byte j, 64 at a time, and the walk jumps to node_at of the last
+// matching position.  The run may include the owner string's terminator but
+// never goes past it (the node after T has no children).  A token needs one
+// child step per point where it leaves the owner string's path, usually one or
+// two.
 __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *nodes, const int32_t *toks,
                                                     int64_t B, int32_t *out) {
-    const int64_t b = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (b >= B) return;
+    const int64_t b = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (b >= B) return;  // uniform over the wave
     const int32_t n0 = nodes[b];
     const int32_t v = toks[b];
     int32_t n = TAM_DEAD;
+    const bool ok = n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V;
     if (t.fmt_L >= 0) {  // character positions: p + |t| when the token fits the classes
-        if (n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V) {
+        if (ok && lane == 0) {
             const uint32_t o = t.tok_off[v];
             const int len = (int)(t.tok_off[v + 1] - o);
             if (format_fits(t, n0, t.tok_blob + o, len)) n = n0 + len;
         }
-        out[b] = n;
+        if (lane == 0) out[b] = n;
         return;
     }
-    if (n0 >= 0 && (int64_t)n0 < t.N && v >= 0 && (int64_t)v < t.V) {
+    if (ok) {
         const int64_t a = t.tok_off[v];
         const int len = (int)(t.tok_off[v + 1] - (uint32_t)a);
         const uint32_t T = (uint32_t)t.terminator;
         int i = 0;
         n = len > 0 ? n0 : TAM_DEAD;
+        int32_t lo = t.child_off[n0], hi = t.child_off[n0 + 1];  // loaded beside the token's offsets
         while (i < len && n >= 0) {
             const uint32_t c = t.tok_blob[a + i];
-            n = child(t, n, c);
+            // child of n along c: its sorted child bytes and ids, 64 lanes at a
+            // time, loaded together with the token byte
+            int32_t nx = TAM_DEAD;
+            for (int32_t k0 = lo; k0 < hi; k0 += kWave) {
+                const int32_t k = k0 + lane;
+                const bool in = k < hi;
+                const uint32_t cb = in ? (uint32_t)t.child_byte[k] : 0x100u;
+                const int32_t cn = in ? t.child_node[k] : TAM_DEAD;
+                const uint64_t m = __ballot(cb == c);
+                if (m) {
+                    nx = __shfl(cn, (int)__builtin_ctzll(m), kWave);
+                    break;
+                }
+            }
+            n = nx;
             ++i;
-            if (n < 0 || i >= len || c == T) continue;  // dead, done, or at a final node
+            if (n < 0 || i >= len) break;  // dead or done
+            if (c == T) {                  // a final node: it has no children
+                n = TAM_DEAD;
+                break;
+            }
             int64_t p = t.node_pos[n];
             for (;;) {
-                uint64_t blo, bhi, tlo, thi;
-                load16(t.blob, p + 1, blo, bhi);
-                load16(t.tok_blob, a + i, tlo, thi);
-                const int cap = min(first_byte(blo, bhi, T) + 1, 16);  // up to and including T
-                const int k = min(min(common_prefix(tlo, thi, blo, bhi), len - i), cap);
+                const int64_t q = p + 1 + lane;
+                const uint32_t sb = q < t.blob_bytes ? (uint32_t)t.blob[q] : 0x200u;
+                const uint32_t tb = i + lane < len ? (uint32_t)t.tok_blob[a + i + lane] : 0x100u;
+                const uint64_t term = __ballot(sb == T);
+                const uint64_t diff = ~__ballot(sb == tb);
+                const int f = term ? (int)__builtin_ctzll(term) : kWave;  // first T of the window
+                const int run = diff ? (int)__builtin_ctzll(diff) : kWave;
+                const int k = min(run, f < kWave ? f + 1 : kWave);      // up to and including T
                 p += k;
                 i += k;
-                if (k < 16 || i >= len) break;
+                if (k < kWave || i >= len || f < kWave) break;
             }
             n = t.node_at[p];
+            if (i < len) {
+                lo = t.child_off[n];
+                hi = t.child_off[n + 1];
+            }
         }
     }
-    out[b] = n;
+    if (lane == 0) out[b] = n;
 }
 
 // ---------------------------------------------------------------- export ---
@@ -1305,7 +1286,7 @@ hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, 
 hipError_t launch_advance(const DevTables &t, const int32_t *node_ids, const int32_t *token_ids, int64_t B,
                           int32_t *out, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_advance, dim3(grid_for(B, kBlock)), dim3(kBlock), 0, s, t, node_ids, token_ids, B,
+    hipLaunchKernelGGL(k_advance, dim3(grid_for(B, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, token_ids, B,
                        out);
     return hipGetLastError();
 }

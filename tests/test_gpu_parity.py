@@ -158,6 +158,19 @@ def test_other_terminator_and_high_bytes(P):
                    terminator=ord("|"), flags=flags)
 
 
+def test_advance_stops_at_a_terminator(P):
+    """A token that runs through a string's terminator and on into the bytes
+    stored after it in the string blob (the next string's leading 0x00 pad)
+    must end dead: the node after the terminator has no children.  The
+    terminator falls at every offset of the walk's compare windows."""
+    strings = [b"a" * 80, b"b" * 3]
+    vocab = [b"\x00", b'"\x00', b"a", b'"']
+    for k in range(1, 81):
+        vocab += [b"a" * k + b'"' + b"\x00", b"a" * k + b'"', b"a" * k + b'"' + b"\x00b"]
+    for flags in FLAGS:
+        full_check(P, strings, vocab, flags=flags)
+
+
 def test_tail_single_string(P):
     """One string: the whole trie is one path, so no node branches (the table
     keeps one unused row) and every row comes from a list."""
