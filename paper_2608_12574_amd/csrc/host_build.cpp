@@ -29,13 +29,17 @@ struct TerminatedLess {
     }
 };
 
-// The trie of one bucket of strings (all of one set, all with the same first
-// byte of s+T), with bucket-local node ids (root = 0) and blob offsets.
-struct SetTrie {
-    std::vector<int32_t> parent, depth, node_pos, node_at, child_off, child_node;
-    std::vector<int32_t> sub_end;  // one past the last node of each node's subtree (local ids)
-    std::vector<uint8_t> edge, is_final, blob, child_byte;
-    int64_t K_unique = 0;
+// The sorted, distinct strings of one part (all of one set, or all of a set
+// with the same first byte of s+T), planned before any node is written: each
+// string's longest common prefix with the previous one fixes how many nodes
+// it creates, so every part's node, edge and blob ranges are known up front
+// and the parts then write straight into the handle's tables.
+struct PartPlan {
+    std::vector<int64_t> str;   // string indices in trie order, duplicates dropped
+    std::vector<int32_t> lcp;   // common prefix with the previous string (0 for the first)
+    int64_t nodes = 1;          // including the part's root (its set's root)
+    int64_t blob = 0;           // pad byte, bytes, T per string
+    int64_t root_children = 0;  // strings starting a new first byte
     tam_status st = TAM_OK;
     std::string err;
 };
@@ -53,44 +57,27 @@ uint64_t order_key(const uint8_t *s, int64_t len, uint8_t term) {
 }
 
 /*
- * Trie construction of one bucket (Section 4.1: insert every value one byte at
- * a time, shared prefixes merge).  Inserting the distinct terminated strings in
- * sorted order creates the new nodes of each string right after its longest
+ * Trie construction (Section 4.1: insert every value one byte at a time,
+ * shared prefixes merge), planned: inserting the distinct terminated strings
+ * in sorted order creates the new nodes of each string right after its longest
  * common prefix with the previous string, and that creation order is exactly
- * the lexicographic preorder the interface fixes.  O(N_chars) after the sort.
- * Blob layout per string: one pad byte standing for the root, the string, T.
+ * the lexicographic preorder the interface fixes.  A string of length len
+ * with common prefix l creates len + 1 - l nodes.  O(N_chars) after the sort.
  */
-void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t count, uint8_t term,
-                  SetTrie &r) {
+void plan_part(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t count, uint8_t term,
+               PartPlan &r) {
     std::vector<std::pair<uint64_t, int64_t>> order((size_t)count);
-    int64_t chars = 0;
     for (int64_t i = 0; i < count; ++i) {
         const int64_t k = idx[i];
         order[(size_t)i] = {order_key(sb + so[k], so[k + 1] - so[k], term), k};
-        chars += so[k + 1] - so[k];
     }
     const TerminatedLess less{sb, so, term};
     std::sort(order.begin(), order.end(), [&](const std::pair<uint64_t, int64_t> &a,
                                               const std::pair<uint64_t, int64_t> &b) {
         return a.first != b.first ? a.first < b.first : less(a.second, b.second);
     });
-    const size_t est = (size_t)(chars + 2 * count + 1);
-    r.parent.reserve(est);
-    r.depth.reserve(est);
-    r.edge.reserve(est);
-    r.is_final.reserve(est);
-    r.node_pos.reserve(est);
-    r.blob.reserve(est);
-    r.node_at.reserve(est);
-    r.sub_end.reserve(est);
-    r.parent.push_back(-1);
-    r.sub_end.push_back(0);
-    r.depth.push_back(0);
-    r.edge.push_back(0);
-    r.is_final.push_back(0);
-    r.node_pos.push_back(-1);
-    int64_t N = 1;
-    std::vector<int32_t> path;
+    r.str.reserve((size_t)count);
+    r.lcp.reserve((size_t)count);
     const uint8_t *prev = nullptr;
     int64_t prev_len = -1;
     for (const auto &kv : order) {
@@ -102,53 +89,96 @@ void build_bucket(const uint8_t *sb, const int64_t *so, const int64_t *idx, int6
             const int64_t m = std::min(len, prev_len);
             while (l < m && prev[l] == s[l]) ++l;
             if (l == len && len == prev_len) continue;  // duplicate string
-            // the previous string's nodes below depth l have no more descendants:
-            // their subtrees end where this string's first new node starts
-            for (int64_t i = l; i <= prev_len; ++i) r.sub_end[(size_t)path[(size_t)i]] = (int32_t)N;
         }
         prev = s;
         prev_len = len;
-        ++r.K_unique;
-        if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
-        r.blob.push_back(0);
-        r.node_at.push_back(0);
-        for (int64_t i = 0; i <= len; ++i) {
-            const uint8_t c = i < len ? s[i] : term;
-            r.blob.push_back(c);
-            int32_t id;
-            if (i < l) {
-                id = path[(size_t)i];
-            } else {
-                id = (int32_t)N++;
-                r.parent.push_back(i == 0 ? 0 : path[(size_t)(i - 1)]);
-                r.depth.push_back((int32_t)(i + 1));
-                r.edge.push_back(c);
-                r.is_final.push_back(i == len ? 1 : 0);
-                r.node_pos.push_back((int32_t)(r.blob.size() - 1));
-                r.sub_end.push_back(0);
-            }
-            path[(size_t)i] = id;
-            r.node_at.push_back(id);
-        }
-        if (N >= INT32_MAX || (int64_t)r.blob.size() >= INT32_MAX) {
+        r.str.push_back(k);
+        r.lcp.push_back((int32_t)l);
+        r.nodes += len + 1 - l;
+        r.blob += len + 2;
+        r.root_children += l == 0 ? 1 : 0;
+        if (r.nodes >= INT32_MAX || r.blob >= INT32_MAX) {
             r.st = TAM_E_TOOLARGE;
             r.err = "trie exceeds 2^31-1 nodes or string bytes";
             return;
         }
     }
-    for (int64_t i = 0; i <= prev_len; ++i) r.sub_end[(size_t)path[(size_t)i]] = (int32_t)N;
-    r.sub_end[0] = (int32_t)N;
-    // children in ascending byte order = ascending ids (preorder)
-    r.child_off.assign((size_t)(N + 1), 0);
-    for (int64_t m = 1; m < N; ++m) ++r.child_off[(size_t)r.parent[(size_t)m] + 1];
-    for (int64_t n = 0; n < N; ++n) r.child_off[(size_t)n + 1] += r.child_off[(size_t)n];
-    r.child_node.resize((size_t)(N - 1));
-    r.child_byte.resize((size_t)(N - 1));
-    std::vector<int32_t> fill(r.child_off.begin(), r.child_off.end() - 1);
-    for (int64_t m = 1; m < N; ++m) {
-        const int32_t at = fill[(size_t)r.parent[(size_t)m]]++;
-        r.child_node[(size_t)at] = (int32_t)m;
-        r.child_byte[(size_t)at] = r.edge[(size_t)m];
+}
+
+// Where a part's nodes, blob bytes and edges go in the handle's tables.
+struct PartBase {
+    int32_t root;         // its set's root
+    int64_t node;         // local node i >= 1 gets id node + i
+    int64_t blob;         // local blob offset b goes to blob + b
+    int64_t edge;         // first of its edges below depth 1
+    int64_t root_edge;    // first of its depth-1 nodes' slots among the set root's edges
+};
+
+/*
+ * Writes a planned part into the handle: per string, a pad byte (standing for
+ * the root), its bytes and T into the blob; the nodes it creates (parent,
+ * depth, edge byte, final flag, blob position); node_at along the string; and
+ * with subtree extents, the end of every node's subtree (a node's subtree ends
+ * where the first later string leaves its path).  Then the part's child lists:
+ * children in ascending id order, which is ascending byte order; depth-1 nodes
+ * are listed on the set root.
+ */
+void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, const PartBase &pb,
+               bool subtrees, tam_handle *h) {
+    const int64_t nloc = r.nodes;
+    std::vector<int32_t> path;  // global ids of the current string's nodes by depth - 1
+    int64_t N = 1, B = 0, prev_len = -1;
+    for (size_t u = 0; u < r.str.size(); ++u) {
+        const int64_t k = r.str[u];
+        const uint8_t *s = sb + so[k];
+        const int64_t len = so[k + 1] - so[k];
+        const int64_t l = r.lcp[u];
+        if (subtrees)  // the previous string's nodes below depth l end here
+            for (int64_t i = l; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + N);
+        prev_len = len;
+        if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
+        const int64_t at = pb.blob + B;
+        h->blob[(size_t)at] = 0;
+        h->node_at[(size_t)at] = pb.root;
+        for (int64_t i = 0; i <= len; ++i) {
+            const uint8_t c = i < len ? s[i] : term;
+            const size_t pos = (size_t)(at + 1 + i);
+            h->blob[pos] = c;
+            if (i >= l) {
+                const size_t g = (size_t)(pb.node + N++);
+                h->parent[g] = (int32_t)(i == 0 ? pb.root : path[(size_t)(i - 1)]);
+                h->depth[g] = (int32_t)(i + 1);
+                h->edge[g] = c;
+                h->is_final[g] = i == len ? 1 : 0;
+                h->node_pos[g] = (int32_t)pos;
+                path[(size_t)i] = (int32_t)g;
+            }
+            h->node_at[pos] = path[(size_t)i];
+        }
+        B += len + 2;
+    }
+    if (subtrees)
+        for (int64_t i = 0; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + nloc);
+    // child lists: count, offsets, then fill in id order
+    std::vector<int32_t> cnt((size_t)nloc, 0);
+    for (int64_t i = 1; i < nloc; ++i) {
+        const int64_t p = h->parent[(size_t)(pb.node + i)];
+        if (p != pb.root) ++cnt[(size_t)(p - pb.node)];
+    }
+    int64_t e = pb.edge;
+    for (int64_t i = 1; i < nloc; ++i) {
+        h->child_off[(size_t)(pb.node + i)] = (int32_t)e;
+        const int32_t c = cnt[(size_t)i];
+        cnt[(size_t)i] = (int32_t)(e - pb.edge);  // becomes the fill cursor
+        e += c;
+    }
+    int64_t re = pb.root_edge;
+    for (int64_t i = 1; i < nloc; ++i) {
+        const int64_t g = pb.node + i;
+        const int64_t p = h->parent[(size_t)g];
+        const int64_t slot = p == pb.root ? re++ : pb.edge + cnt[(size_t)(p - pb.node)]++;
+        h->child_node[(size_t)slot] = (int32_t)g;
+        h->child_byte[(size_t)slot] = h->edge[(size_t)g];
     }
 }
 
@@ -236,20 +266,20 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         pstart.push_back(K);
     }
     const int64_t NP = (int64_t)pset.size();
-    std::vector<SetTrie> parts((size_t)NP);
+    std::vector<PartPlan> parts((size_t)NP);
     std::atomic<bool> oom{false};
     parallel_for(NP, host_threads(NP), [&](int64_t p) {
         try {
-            build_bucket(sb, so, idx.data() + pstart[(size_t)p], pstart[(size_t)p + 1] - pstart[(size_t)p], term,
-                         parts[(size_t)p]);
+            plan_part(sb, so, idx.data() + pstart[(size_t)p], pstart[(size_t)p + 1] - pstart[(size_t)p], term,
+                      parts[(size_t)p]);
         } catch (const std::bad_alloc &) {
             oom = true;
         }
     });
     if (oom) throw std::bad_alloc();
     // bases: node ids (a part's local root is its set's root, the rest follow),
-    // blob offsets, edges (a set's root edges first)
-    std::vector<int64_t> nbase((size_t)NP), bbase((size_t)NP), ebase((size_t)NP), rbase((size_t)NP);
+    // blob offsets, edges (a set's root edges first, then its parts' others)
+    std::vector<PartBase> base((size_t)NP);
     std::vector<int64_t> root((size_t)S), root_edges((size_t)S);
     int64_t N = 0, BB = kBlobPad, E = 0;
     h->K_unique = 0;
@@ -257,23 +287,25 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         root[(size_t)j] = N++;
         root_edges[(size_t)j] = E;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
-            const SetTrie &r = parts[(size_t)p];
+            const PartPlan &r = parts[(size_t)p];
             if (r.st != TAM_OK) {
                 *err = r.err;
                 return r.st;
             }
-            rbase[(size_t)p] = E;
-            E += r.child_off[1];  // the part root's children become the set root's
+            base[(size_t)p].root_edge = E;
+            E += r.root_children;  // the part root's children become the set root's
         }
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
-            const SetTrie &r = parts[(size_t)p];
-            nbase[(size_t)p] = N - 1;                // local id i >= 1 -> N - 1 + i
-            bbase[(size_t)p] = BB;
-            ebase[(size_t)p] = E - r.child_off[1];  // local edge e past the root's -> E - nr + e
-            N += (int64_t)r.parent.size() - 1;
-            BB += (int64_t)r.blob.size();
-            E += (int64_t)r.child_node.size() - r.child_off[1];
-            h->K_unique += r.K_unique;
+            const PartPlan &r = parts[(size_t)p];
+            PartBase &pb = base[(size_t)p];
+            pb.root = (int32_t)root[(size_t)j];
+            pb.node = N - 1;
+            pb.blob = BB;
+            pb.edge = E;
+            N += r.nodes - 1;
+            BB += r.blob;
+            E += r.nodes - 1 - r.root_children;
+            h->K_unique += (int64_t)r.str.size();
             if (N >= INT32_MAX || BB >= INT32_MAX) {
                 *err = "trie exceeds 2^31-1 nodes or string bytes";
                 return TAM_E_TOOLARGE;
@@ -317,33 +349,13 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
     }
     parallel_for(NP, host_threads(NP), [&](int64_t p) {
-        const SetTrie &r = parts[(size_t)p];
-        const int32_t rt = (int32_t)root[(size_t)pset[(size_t)p]];
-        const int64_t nb = nbase[(size_t)p], bb = bbase[(size_t)p], eb = ebase[(size_t)p], rb = rbase[(size_t)p];
-        const int32_t nr = r.child_off[1];
-        const size_t n = r.parent.size();
-        auto gid = [&](int32_t local) { return local == 0 ? rt : (int32_t)(nb + local); };
-        for (size_t i = 1; i < n; ++i) {
-            const size_t g = (size_t)(nb + (int64_t)i);
-            h->parent[g] = gid(r.parent[i]);
-            h->node_pos[g] = (int32_t)(r.node_pos[i] + bb);
-            h->child_off[g] = (int32_t)(r.child_off[i] + eb);
-            h->depth[g] = r.depth[i];
-            h->edge[g] = r.edge[i];
-            h->is_final[g] = r.is_final[i];
-            if (subtrees) h->sub_end[g] = (int32_t)(nb + r.sub_end[i]);
-        }
-        std::copy(r.blob.begin(), r.blob.end(), h->blob.begin() + bb);
-        for (size_t i = 0; i < r.node_at.size(); ++i) h->node_at[(size_t)bb + i] = gid(r.node_at[i]);
-        for (int32_t e = 0; e < nr; ++e) {  // the part root's children, on the set root
-            h->child_node[(size_t)(rb + e)] = gid(r.child_node[(size_t)e]);
-            h->child_byte[(size_t)(rb + e)] = r.child_byte[(size_t)e];
-        }
-        for (size_t e = (size_t)nr; e < r.child_node.size(); ++e) {
-            h->child_node[(size_t)(eb + (int64_t)e)] = gid(r.child_node[e]);
-            h->child_byte[(size_t)(eb + (int64_t)e)] = r.child_byte[e];
+        try {
+            emit_part(sb, so, term, parts[(size_t)p], base[(size_t)p], subtrees, h);
+        } catch (const std::bad_alloc &) {
+            oom = true;
         }
     });
+    if (oom) throw std::bad_alloc();
     h->child_off[(size_t)N] = (int32_t)E;
     return TAM_OK;
 }
