@@ -112,7 +112,12 @@ struct PartBase {
     int64_t blob;         // local blob offset b goes to blob + b
     int64_t edge;         // first of its edges below depth 1
     int64_t root_edge;    // first of its depth-1 nodes' slots among the set root's edges
+    bool root_tail;       // its set has one string (the set root is then a tail)
+    int64_t branching;    // out (tail split): branching nodes of the part
 };
+
+// Marks a branching node's row_of entry until the dense rows are numbered.
+constexpr int32_t kBranchRow = INT32_MAX;
 
 /*
  * Writes a planned part into the handle: per string, a pad byte (standing for
@@ -123,20 +128,49 @@ struct PartBase {
  * children in ascending id order, which is ascending byte order; depth-1 nodes
  * are listed on the set root.
  */
-void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, const PartBase &pb,
-               bool subtrees, tam_handle *h) {
+void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, PartBase &pb,
+               bool subtrees, bool tails, tam_handle *h) {
     const int64_t nloc = r.nodes;
-    std::vector<int32_t> path;  // global ids of the current string's nodes by depth - 1
-    int64_t N = 1, B = 0, prev_len = -1;
+    std::vector<int32_t> path;   // global ids of the current string's nodes by depth - 1
+    std::vector<int64_t> first;  // (tail split) index of the string that created each of them
+    int64_t N = 1, B = 0, prev_len = -1, branching = 0;
+    // The previous string's nodes at path indices l..prev_len leave the path
+    // before string u: their subtrees end here, and u - first[i] strings pass
+    // through each (a node is final for exactly one string).  Tail split: two
+    // or more make a branching node (a dense row); a tail's subtree is one
+    // path, the rest of that string (prev_len - i nodes below it), and its
+    // highest tail ancestor-or-self is the first tail of the range (the node
+    // above the range is shared with string u, hence branching, unless it is
+    // the root of a one-string set, itself a tail at depth 0).
+    auto close = [&](int64_t l, int64_t u) {
+        if (subtrees)
+            for (int64_t i = l; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + N);
+        if (!tails) return;
+        int64_t top = -1;
+        for (int64_t i = l; i <= prev_len; ++i) {
+            const size_t g = (size_t)path[(size_t)i];
+            if (u - first[(size_t)i] >= 2) {
+                h->row_of[g] = kBranchRow;
+                h->tail_span[g] = 0;
+                ++branching;
+                continue;
+            }
+            if (top < 0) top = pb.root_tail ? 0 : i + 1;
+            h->row_of[g] = (int32_t)(-1 - (prev_len - i));
+            h->tail_span[g] = (int32_t)(i + 1 - top);
+        }
+    };
     for (size_t u = 0; u < r.str.size(); ++u) {
         const int64_t k = r.str[u];
         const uint8_t *s = sb + so[k];
         const int64_t len = so[k + 1] - so[k];
         const int64_t l = r.lcp[u];
-        if (subtrees)  // the previous string's nodes below depth l end here
-            for (int64_t i = l; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + N);
+        close(l, (int64_t)u);
         prev_len = len;
-        if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
+        if ((int64_t)path.size() < len + 1) {
+            path.resize((size_t)(len + 1));
+            if (tails) first.resize((size_t)(len + 1));
+        }
         const int64_t at = pb.blob + B;
         h->blob[(size_t)at] = 0;
         h->node_at[(size_t)at] = pb.root;
@@ -152,13 +186,14 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
                 h->is_final[g] = i == len ? 1 : 0;
                 h->node_pos[g] = (int32_t)pos;
                 path[(size_t)i] = (int32_t)g;
+                if (tails) first[(size_t)i] = (int64_t)u;
             }
             h->node_at[pos] = path[(size_t)i];
         }
         B += len + 2;
     }
-    if (subtrees)
-        for (int64_t i = 0; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + nloc);
+    close(0, (int64_t)r.str.size());
+    pb.branching = branching;
     // child lists: count, offsets, then fill in id order
     std::vector<int32_t> cnt((size_t)nloc, 0);
     for (int64_t i = 1; i < nloc; ++i) {
@@ -201,6 +236,58 @@ void parallel_for(int64_t n, int threads, F f) {
 int host_threads(int64_t work_items) {
     const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
     return (int)std::min<int64_t>({(int64_t)hw, (int64_t)16, work_items});
+}
+
+/*
+ * Tail compression.  A node is a tail when its subtree holds exactly one final
+ * node, i.e. below it the trie is a single path; its valid tokens are then the
+ * tokens equal to a prefix of that one remaining suffix.  Every other node
+ * (two or more finals below) is a branching node and gets a dense table row,
+ * numbered in id order; a tail a gets row_of[a] = -1 - rem(a), rem(a) being the
+ * number of nodes below it.  In preorder a tail's path has consecutive ids
+ * a+1 .. a+rem(a), so the token of length d starting below a is the suffix hit
+ * of node a+d at distance d: tails need no stored masks.  Tails are closed
+ * under descent, so above any node m the tails form the first tail_span[m]
+ * ancestors: a hit at distance d above m lands on a tail iff d <= tail_span[m]
+ * = depth(m) - depth(highest tail ancestor-or-self of m), and 0 when m itself
+ * branches.  emit_part classifies every node when it leaves the insertion
+ * path; here the branching nodes are numbered in id order (a set's root, then
+ * its parts' nodes), and row_at = row_of[node_at] is laid along the blob.
+ */
+void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::vector<int64_t> &set_first,
+                       const std::vector<PartPlan> &parts, const std::vector<PartBase> &base, tam_handle *h) {
+    const int64_t NP = (int64_t)parts.size();
+    std::vector<int64_t> first_row((size_t)NP, 0);
+    int64_t rows = 0;
+    for (int64_t j = 0; j < S; ++j) {
+        const size_t rt = (size_t)root[(size_t)j];
+        const int64_t p0 = set_first[(size_t)j], p1 = set_first[(size_t)j + 1];
+        h->tail_span[rt] = 0;
+        if (base[(size_t)p0].root_tail)  // one string: the whole path lies below the root
+            h->row_of[rt] = (int32_t)(-1 - (parts[(size_t)p0].nodes - 1));
+        else
+            h->row_of[rt] = (int32_t)rows++;
+        for (int64_t p = p0; p < p1; ++p) {
+            first_row[(size_t)p] = rows;
+            rows += base[(size_t)p].branching;
+        }
+    }
+    h->dense_rows = rows;
+    const int64_t BB = h->blob_bytes;
+    h->row_at.resize((size_t)BB);
+    parallel_for(NP, host_threads(NP), [&](int64_t p) {
+        const PartBase &pb = base[(size_t)p];
+        const PartPlan &r = parts[(size_t)p];
+        int32_t row = (int32_t)first_row[(size_t)p];
+        for (int64_t i = 1; i < r.nodes; ++i) {
+            const size_t g = (size_t)(pb.node + i);
+            if (h->row_of[g] == kBranchRow) h->row_of[g] = row++;
+        }
+        for (int64_t b = pb.blob; b < pb.blob + r.blob; ++b)
+            h->row_at[(size_t)b] = h->row_of[(size_t)h->node_at[(size_t)b]];
+    });
+    for (int64_t b = 0; b < kBlobPad; ++b)  // the outer pads stand for the first set's root
+        h->row_at[(size_t)b] = h->row_at[(size_t)(BB - 1 - b)] = h->row_of[0];
 }
 
 }  // namespace
@@ -295,9 +382,14 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             base[(size_t)p].root_edge = E;
             E += r.root_children;  // the part root's children become the set root's
         }
+        int64_t set_strings = 0;
+        for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p)
+            set_strings += (int64_t)parts[(size_t)p].str.size();
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
             const PartPlan &r = parts[(size_t)p];
             PartBase &pb = base[(size_t)p];
+            pb.root_tail = set_strings == 1;
+            pb.branching = 0;
             pb.root = (int32_t)root[(size_t)j];
             pb.node = N - 1;
             pb.blob = BB;
@@ -332,7 +424,10 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
     h->node_at.resize((size_t)BB);
     const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
+    const bool tails = (h->flags & TAM_FLAG_TAIL_LISTS) && !(h->flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
     h->sub_end.resize(subtrees ? (size_t)N : 0);
+    h->row_of.resize(tails ? (size_t)N : 0);
+    h->tail_span.resize(tails ? (size_t)N : 0);
     for (int64_t p = 0; p < kBlobPad; ++p) {
         h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
         h->node_at[(size_t)p] = h->node_at[(size_t)(BB - 1 - p)] = 0;
@@ -350,12 +445,13 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     }
     parallel_for(NP, host_threads(NP), [&](int64_t p) {
         try {
-            emit_part(sb, so, term, parts[(size_t)p], base[(size_t)p], subtrees, h);
+            emit_part(sb, so, term, parts[(size_t)p], base[(size_t)p], subtrees, tails, h);
         } catch (const std::bad_alloc &) {
             oom = true;
         }
     });
     if (oom) throw std::bad_alloc();
+    if (tails) number_dense_rows(S, root, set_first, parts, base, h);
     h->child_off[(size_t)N] = (int32_t)E;
     return TAM_OK;
 }
@@ -480,112 +576,19 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     // span; with tail compression only the hits longer than the probe window do
     // (the shorter ones are read straight from the probe's hits).
     const bool split = !h->tail_span.empty();
-    int64_t bound = 0;
-    for (int64_t m = 0; m < h->N; ++m) {
-        const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
-        bound += cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
-    }
-    return bound;
-}
-
-/*
- * Tail compression.  A node is a tail when its subtree holds exactly one final
- * node, i.e. below it the trie is a single path; its valid tokens are then the
- * tokens equal to a prefix of that one remaining suffix.  Every other node
- * (two or more finals below) is a branching node and gets a dense table row,
- * numbered in id order; a tail a gets row_of[a] = -1 - rem(a), rem(a) being the
- * number of nodes below it.  In preorder a tail's path has consecutive ids
- * a+1 .. a+rem(a), so the token of length d starting below a is the suffix hit
- * of node a+d at distance d: tails need no stored masks.  Tails are closed
- * under descent, so above any node m the tails form the first tail_span[m]
- * ancestors: a hit at distance d above m lands on a tail iff d <= tail_span[m]
- * = depth(m) - depth(highest tail ancestor-or-self of m), and 0 when m itself
- * branches.  Every parent precedes its children: one backward pass counts the
- * finals below each node (and the path lengths below tails), one forward pass
- * finds the highest tail on each path.  Both run in parallel over the subtrees
- * of the roots' children (consecutive id ranges); the roots are done apart.
- */
-void split_tails(tam_handle *h) {
-    const int64_t N = h->N, S = h->S;
-    // ranges: the subtree of each root child, in id order
-    std::vector<int64_t> lo, hi;
-    for (int64_t j = 0; j < S; ++j) {
-        const int32_t r = h->roots[(size_t)j];
-        const int64_t end = j + 1 < S ? h->roots[(size_t)j + 1] : N;
-        for (int32_t e = h->child_off[(size_t)r]; e < h->child_off[(size_t)r + 1]; ++e) {
-            lo.push_back(h->child_node[(size_t)e]);
-            hi.push_back(e + 1 < h->child_off[(size_t)r + 1] ? h->child_node[(size_t)e + 1] : end);
-        }
-    }
-    const int64_t R = (int64_t)lo.size();
-    const int threads = host_threads(R);
-    // per-node scratch, first touched by the threads of the passes below
-    hvec<int32_t> finals((size_t)N), rem((size_t)N), top((size_t)N);
-    std::vector<int64_t> branching((size_t)R, 0);
-    // finals[n] is complete once all descendants are done; rem = nodes below a
-    // tail (its single child is n+1)
-    auto backward = [&](int64_t n) {
-        rem[(size_t)n] = finals[(size_t)n] == 1 && !h->is_final[(size_t)n] ? rem[(size_t)n + 1] + 1 : 0;
-    };
-    parallel_for(R, threads, [&](int64_t i) {
-        for (int64_t n = lo[(size_t)i]; n < hi[(size_t)i]; ++n) finals[(size_t)n] = h->is_final[(size_t)n];
+    const int64_t chunk = 1 << 16, nchunks = (h->N + chunk - 1) / chunk;
+    std::vector<int64_t> part((size_t)nchunks, 0);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         int64_t b = 0;
-        for (int64_t n = hi[(size_t)i] - 1; n >= lo[(size_t)i]; --n) {
-            backward(n);
-            b += finals[(size_t)n] >= 2;
-            if (n > lo[(size_t)i]) finals[(size_t)h->parent[(size_t)n]] += finals[(size_t)n];
+        for (int64_t m = c * chunk; m < std::min(h->N, (c + 1) * chunk); ++m) {
+            const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
+            b += cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
         }
-        branching[(size_t)i] = b;
+        part[(size_t)c] = b;
     });
-    // the roots, then the dense row numbering in id order (a root, its ranges, ...)
-    std::vector<int64_t> first_row((size_t)R, 0);
-    // top: depth of the highest tail ancestor-or-self (-1 for a branching node)
-    h->tail_span.resize((size_t)N);
-    h->row_of.resize((size_t)N);
-    int64_t rows = 0, i = 0;
-    for (int64_t j = 0; j < S; ++j) {
-        const int32_t r = h->roots[(size_t)j];
-        const int64_t i0 = i;
-        finals[(size_t)r] = 0;
-        top[(size_t)r] = -1;
-        for (int32_t e = h->child_off[(size_t)r]; e < h->child_off[(size_t)r + 1]; ++e, ++i)
-            finals[(size_t)r] += finals[(size_t)lo[(size_t)i]];
-        backward(r);
-        h->tail_span[(size_t)r] = 0;
-        if (finals[(size_t)r] >= 2) {
-            h->row_of[(size_t)r] = (int32_t)rows++;
-        } else {
-            top[(size_t)r] = 0;
-            h->row_of[(size_t)r] = -1 - rem[(size_t)r];
-        }
-        for (int64_t k = i0; k < i; ++k) {
-            first_row[(size_t)k] = rows;
-            rows += branching[(size_t)k];
-        }
-    }
-    h->dense_rows = rows;
-    parallel_for(R, threads, [&](int64_t k) {
-        int32_t row = (int32_t)first_row[(size_t)k];
-        for (int64_t n = lo[(size_t)k]; n < hi[(size_t)k]; ++n) {
-            if (finals[(size_t)n] >= 2) {
-                h->row_of[(size_t)n] = row++;
-                h->tail_span[(size_t)n] = 0;
-                top[(size_t)n] = -1;
-                continue;
-            }
-            const int32_t p = h->parent[(size_t)n];
-            top[(size_t)n] = top[(size_t)p] >= 0 ? top[(size_t)p] : h->depth[(size_t)n];
-            h->tail_span[(size_t)n] = h->depth[(size_t)n] - top[(size_t)n];
-            h->row_of[(size_t)n] = -1 - rem[(size_t)n];
-        }
-    });
-    const int64_t B = (int64_t)h->node_at.size();
-    h->row_at.resize((size_t)B);
-    const int64_t chunk = 1 << 16;
-    parallel_for((B + chunk - 1) / chunk, host_threads((B + chunk - 1) / chunk), [&](int64_t c) {
-        for (int64_t p = c * chunk; p < std::min(B, (c + 1) * chunk); ++p)
-            h->row_at[(size_t)p] = h->row_of[(size_t)h->node_at[(size_t)p]];
-    });
+    int64_t bound = 0;
+    for (int64_t b : part) bound += b;
+    return bound;
 }
 
 }  // namespace tam

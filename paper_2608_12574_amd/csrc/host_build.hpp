@@ -13,6 +13,5 @@ tam_status build_trie(const uint8_t *str_bytes, const int64_t *str_off, int64_t 
 tam_status build_vocab(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, tam_vocab *h,
                        std::string *err);
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v);
-void split_tails(tam_handle *h);
 
 }  // namespace tam

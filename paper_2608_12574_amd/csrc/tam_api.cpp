@@ -295,9 +295,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     try {
         const auto t0 = std::chrono::steady_clock::now();
         const bool lazy = (o.flags & TAM_FLAG_LAZY_ROWS) != 0;
-        st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);
-        if (st == TAM_OK && !lazy && (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_NO_TABLE))
-            tam::split_tails(h);
+        st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);  // with the tail split
         h->timing.host_trie_ms = ms_since(t0);
         // the lists (and their size bound) are needed without a table, or with
         // tail compression when tokens exceed the probe window
