@@ -4,12 +4,82 @@
 #include <algorithm>
 #include <chrono>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "host_build.hpp"
 #include "tam_internal.hpp"
+
+namespace tam {
+
+namespace {
+
+struct PinnedPool {
+    std::mutex m;
+    std::multimap<size_t, void *> idle;        // blocks ready for reuse, by size
+    std::unordered_map<void *, size_t> owned;  // every block of the pool and its size
+    size_t idle_bytes = 0;
+};
+
+// Never destroyed: blocks may come back from handles destroyed at exit.
+PinnedPool &pinned_pool() {
+    static PinnedPool *p = new PinnedPool();
+    return *p;
+}
+
+thread_local bool t_pinned = false;
+constexpr size_t kPinnedKeep = size_t(4) << 30;  // idle bytes kept for reuse
+
+}  // namespace
+
+void *pinned_take(size_t bytes) {
+    if (!t_pinned || bytes < kPinnedMin) return nullptr;
+    const size_t want = (bytes + kPinnedMin - 1) / kPinnedMin * kPinnedMin;
+    PinnedPool &P = pinned_pool();
+    {
+        std::lock_guard<std::mutex> g(P.m);
+        auto it = P.idle.lower_bound(want);
+        if (it != P.idle.end() && it->first <= want + want / 4) {  // at most 25% larger
+            void *p = it->second;
+            P.idle_bytes -= it->first;
+            P.idle.erase(it);
+            return p;
+        }
+    }
+    void *p = nullptr;
+    if (hipHostMalloc(&p, want, hipHostMallocPortable) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> g(P.m);
+    P.owned[p] = want;
+    return p;
+}
+
+bool pinned_give(void *p) {
+    PinnedPool &P = pinned_pool();
+    std::lock_guard<std::mutex> g(P.m);
+    auto it = P.owned.find(p);
+    if (it == P.owned.end()) return false;
+    const size_t size = it->second;
+    if (P.idle_bytes + size > kPinnedKeep) {
+        P.owned.erase(it);
+        (void)hipHostFree(p);
+        return true;
+    }
+    P.idle.emplace(size, p);
+    P.idle_bytes += size;
+    return true;
+}
+
+PinnedScope::PinnedScope(bool on) : prev(t_pinned) { t_pinned = on; }
+PinnedScope::~PinnedScope() { t_pinned = prev; }
+
+}  // namespace tam
 
 namespace {
 
@@ -295,6 +365,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     try {
         const auto t0 = std::chrono::steady_clock::now();
         const bool lazy = (o.flags & TAM_FLAG_LAZY_ROWS) != 0;
+        const tam::PinnedScope pinned(!host_only);  // the uploaded trie tables go to pinned memory
         st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);  // with the tail split
         h->timing.host_trie_ms = ms_since(t0);
         // the lists (and their size bound) are needed without a table, or with

@@ -14,6 +14,23 @@
 
 namespace tam {
 
+// Large host tables of device compiles (the trie arrays that are uploaded)
+// live in pinned memory taken from a process-wide pool and handed back when
+// their handle is destroyed: their uploads are then direct DMA, and a compile
+// that reuses a block faults no pages while filling it.  pinned_take returns
+// null (ordinary memory is used) unless a PinnedScope is active on the
+// calling thread, for blocks under kPinnedMin, or when pinning fails.
+constexpr size_t kPinnedMin = size_t(1) << 20;
+void *pinned_take(size_t bytes);
+bool pinned_give(void *p);  // true if p is a pool block (now back in the pool)
+struct PinnedScope {
+    explicit PinnedScope(bool on);
+    ~PinnedScope();
+    PinnedScope(const PinnedScope &) = delete;
+    PinnedScope &operator=(const PinnedScope &) = delete;
+    bool prev;
+};
+
 // An allocator whose value-initialisation (vector::resize) leaves elements of
 // trivial types unset, so that large host tables are first touched by the
 // threads that fill them instead of being zeroed serially beforehand.
@@ -26,6 +43,15 @@ struct NoInitAlloc : std::allocator<T> {
     NoInitAlloc() = default;
     template <typename U>
     NoInitAlloc(const NoInitAlloc<U> &) noexcept {}
+    T *allocate(size_t n) {
+        if (n * sizeof(T) >= kPinnedMin)
+            if (void *p = pinned_take(n * sizeof(T))) return static_cast<T *>(p);
+        return std::allocator<T>::allocate(n);
+    }
+    void deallocate(T *p, size_t n) {
+        if (n * sizeof(T) >= kPinnedMin && pinned_give(p)) return;
+        std::allocator<T>::deallocate(p, n);
+    }
     template <typename U>
     void construct(U *p) noexcept(std::is_nothrow_default_constructible<U>::value) {
         ::new ((void *)p) U;

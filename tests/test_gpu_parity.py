@@ -329,6 +329,26 @@ def test_config_rebuild_identical(P, compiled):
             h.rebuild(phases=P.PHASE_LISTS)  # no token is longer than 16 bytes: tails need no lists
 
 
+def test_host_tables_recycled_between_compiles(P):
+    """Device compiles keep their large host tables in pinned blocks that are
+    recycled when a handle is destroyed: compiles of other sizes and
+    representations that reuse them still give the oracle's trie and rows."""
+    w = W.config(3)
+    voc = P.Vocab(w.vocab)
+    for k, flags in ((10000, 0), (4000, 8), (10000, LAZY), (7000, 2), (9000, 8)):
+        strings = w.strings[:k]
+        o = Oracle(strings, w.vocab)
+        h = P.compile(strings, voc, flags=flags)
+        assert h.num_nodes == o.N
+        assert np.array_equal(h.parent, o.parent) and np.array_equal(h.depth, o.depth)
+        assert np.array_equal(h.edge_byte, o.edge) and np.array_equal(h.is_final, o.is_final)
+        nodes = sample_nodes(o, 64, k)
+        assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+        check_apply(P, h, o, W.uniform_nodes(3, o.N, 32, k), "bf16", seed=k)
+        h.close()
+    voc.close()
+
+
 def test_shared_vocabulary(P):
     """One vocabulary, built once, serves several compiles (dense and sparse),
     and outlives its creator's reference through the handles."""
