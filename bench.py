@@ -589,6 +589,8 @@ def main():
                            python_list_packing=round(bench.pack_ms, 3)),
         "apply": main_res["apply"],
         "advance_us": main_res["advance_us"],
+        "advance_us_eager": main_res["advance_us_eager"],
+        "apply_us_graph": main_res["apply_us_graph"],
         "device_bytes": main_res["device_bytes"],
         "tail_compression": secondary,
         "lazy_rows": lazy,

@@ -36,7 +36,10 @@
  *     words, token v is bit (v & 63) of word (v >> 6), bits >= V are zero.
  *
  * Memory and streams: device memory comes from the caller's allocator
- * (tam_allocator; NULL = hipMalloc/hipFree).  Every device operation is
+ * (tam_allocator; NULL = hipMalloc/hipFree).  The large host tables of a device
+ * compile (1 MiB or more) are page-locked blocks (hipHostMalloc) from a
+ * process-wide pool: a destroyed handle's blocks are kept for reuse, up to
+ * 4 GiB of idle blocks, so later compiles upload them by direct DMA.  Every device operation is
  * enqueued on the caller's HIP stream (`stream`, a hipStream_t passed as void*;
  * NULL = the null stream) and returns without synchronising, except where a
  * function says otherwise.  A handle is immutable after tam_compile (only
