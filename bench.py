@@ -64,8 +64,17 @@ def parse():
 
 
 def kernels_sha() -> str:
-    p = os.path.join(ROOT, "paper_2608_12574_amd", "csrc", "kernels.hip")
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    """Hash of the device code in kernels.hip and the header it includes, with
+    comments and whitespace removed: the counter summaries under profiles/ are
+    valid while it matches (comment edits do not change what was measured)."""
+    import re
+    h = hashlib.sha256()
+    for name in ("kernels.hip", "tam_internal.hpp"):
+        src = open(os.path.join(ROOT, "paper_2608_12574_amd", "csrc", name), encoding="utf-8").read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(name: str, sha: str):

@@ -2,9 +2,10 @@
 //
 // Mask compile (Section 4.1, valid[n] for every trie node n):
 //   k_zero   -- zero fill of the dense table (pure streaming stores).
-//   k_probe  -- one lane per non-root node m: the last d <= min(depth(m), ℓ)
-//               bytes of prefix(m) are hashed (read backwards from a 16-byte
-//               register window) and looked up in the vocabulary table; a hit of
+//   k_probe  -- four lanes per non-root node m, four suffix lengths each: the
+//               last d <= min(depth(m), ℓ) bytes of prefix(m) are hashed (read
+//               backwards from a 16-byte register window) and looked up in the
+//               vocabulary table; a hit of
 //               token t at d = |t| means t is valid at the ancestor d levels up,
 //               because t's walk from there ends at m.  This is the paper's
 //               crediting of a match to the node |t| bytes back (Section 4.2),
