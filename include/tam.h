@@ -349,7 +349,9 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out);
 /* tam_timing_get -- see tam_timing.  Waits for the last recorded device event. */
 tam_status tam_timing_get(const tam_handle *h, tam_timing *out);
 
-/* tam_destroy -- waits for the handle's outstanding device work, then frees it.  NULL is a no-op. */
+/* tam_destroy -- waits for the device work the handle enqueued itself (its
+ * compile and tam_rebuild calls), then frees it.  Apply, advance and export
+ * calls are the caller's: wait for their streams first.  NULL is a no-op. */
 void tam_destroy(tam_handle *h);
 
 /* Message of the last failing call on this thread ("" if none). */
