@@ -555,6 +555,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     if (e != hipSuccess) {
         st = hip_fail(e, "upload");
         const std::string msg = g_err;
+        (void)hipStreamSynchronize(s);  // copies already enqueued still read the host tables
         destroy_handle(h);
         return fail(st, msg);
     }
