@@ -167,11 +167,18 @@ class _TorchAllocator:
 
 
 def _stream_ptr(stream, host_only=False):
+    """The HIP stream for a call: ``stream``, else torch's current stream on the
+    current device (read as a raw pointer: building a Stream object costs more
+    than the call it serves)."""
     if host_only:
         return ctypes.c_void_p(None)
     import torch
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+    if stream is not None:
+        return ctypes.c_void_p(stream.cuda_stream)
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return ctypes.c_void_p(raw(torch.cuda.current_device()))
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
 class Handle:
