@@ -185,6 +185,24 @@ class Bench:
             warm.append(ms)
         return h, cold, warm, phases_cold, h.timing()
 
+    def one_set_compile_ms(self, flags, runs=5):
+        """A forest's first set compiled on its own, warm (the latency of one new
+        query's set), minimum over runs; None for a single-set workload."""
+        torch, P, w = self.torch, self.P, self.w
+        if w.set_offsets is None:
+            return None
+        from paper_2608_12574_amd.tam import csr
+        one = csr(w.strings[int(w.set_offsets[0]):int(w.set_offsets[1])])
+        ts = []
+        for _ in range(runs):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            hh = P.compile(one, self.voc, flags=flags)
+            torch.cuda.synchronize()
+            ts.append((time.perf_counter() - t0) * 1e3)
+            hh.close()
+        return round(min(ts), 3)
+
     def measure(self, rep, steps, warmup, cold_runs):
         torch, P, W, w, dev = self.torch, self.P, self.W, self.w, self.dev
         B, V, bufs, nbuf = self.B, self.V, self.bufs, self.nbuf
@@ -333,6 +351,7 @@ class Bench:
                            "end_to_end_cold_all": [round(x, 3) for x in cold],
                            "end_to_end_warm_min": round(min(warm), 3),
                            "end_to_end_warm_all": [round(x, 3) for x in warm],
+                           "one_set_warm": self.one_set_compile_ms(FLAGS[rep]),
                            "phases_cold": phases_cold, "phases_warm": phases_warm},
             "apply": {"us": round(apply_us, 3), "GBps": round(apply_gbps, 1), "bytes": apply_bytes,
                       "frac_of_hbm_roofline": round(apply_gbps / HBM_PEAK_GBPS, 4),
@@ -348,6 +367,8 @@ class Bench:
             "advance_us_eager": round(advance_eager_us, 3),
             "apply_us_graph": round(apply_graph_us, 3),
         }
+        if res["compile_ms"]["one_set_warm"] is not None:
+            print(f"[bench] {rep}: one set alone compiles in {res['compile_ms']['one_set_warm']:.3f} ms (warm)", flush=True)
         print(f"[bench] {rep}: apply {apply_us:.2f} us ({apply_gbps:.0f} GB/s; graph-replayed {apply_graph_us:.2f} us), "
               f"advance {advance_us:.2f} us (graph-replayed; eager loop {advance_eager_us:.2f} us)", flush=True)
         return h, res
@@ -440,6 +461,7 @@ class Bench:
         gcold, gwarm, gref = run_graph(hz, True), run_graph(hz, False), run_graph(h_ref, False)
         res = {"cache_rows": hz.cache_rows, "device_bytes": hz.device_bytes,
                "compile_warm_ms": round(min(e2e), 3), "compile_warm_all": [round(x, 3) for x in e2e],
+               "one_set_compile_warm_ms": self.one_set_compile_ms(P.FLAG_LAZY_ROWS),
                "compile_phases": hz.timing(),
                "decode_steps": S, "batch": B, "distinct_rows": distinct,
                "step_us_cache_emptied": round(cold, 2), "step_us_cache_kept": round(warm, 2),
@@ -447,6 +469,9 @@ class Bench:
                "graph_replayed": {"step_us_cache_emptied": round(gcold, 2), "step_us_cache_kept": round(gwarm, 2),
                                   "step_us_main_repr": round(gref, 2)}}
         hz.close()
+        if res["one_set_compile_warm_ms"] is not None:
+            print(f"[bench] lazy rows: one set alone compiles in {res['one_set_compile_warm_ms']:.3f} ms (warm)",
+                  flush=True)
         print(f"[bench] lazy rows: compile {min(e2e):.2f} ms, {S} steps x {B} rows ({distinct} distinct): "
               f"{cold:.1f} us/step from an empty cache, {warm:.1f} us/step cache kept, "
               f"{ref:.1f} us/step precomputed; graph-replayed {gcold:.1f} / {gwarm:.1f} / {gref:.1f} us/step",

@@ -143,6 +143,25 @@ def test_tiny_random_sets(P, flags):
             assert set(np.flatnonzero(got).tolist()) == b.valid_set(n)
 
 
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_random_medium_sets(P, seed):
+    """Seeded random sets and vocabularies over a small alphabet: heavy prefix
+    sharing, tokens of 1-20 bytes that may hold the terminator, duplicate and
+    empty tokens.  Every row, every (node, token) advance and both apply
+    dtypes, for every representation."""
+    rng = np.random.default_rng(1000 + seed)
+    alpha = np.frombuffer(b'abc_"', dtype=np.uint8)
+
+    def rand_bytes(lo, hi, with_terminator):
+        n = int(rng.integers(lo, hi + 1))
+        return bytes(alpha[rng.integers(0, 5 if with_terminator else 4, size=n)])
+
+    strings = [rand_bytes(0, 24, False) for _ in range(300)]
+    vocab = [rand_bytes(1, 20, True) for _ in range(1500)] + [b"", b"a", b"a", b'"']
+    for flags in FLAGS:
+        full_check(P, strings, vocab, flags=flags)
+
+
 def test_tiny_forest(P):
     sets = [[b"ab", b"a"], [b""], [b"ba", b"bb", b"b"], [b"abc"]]
     flat = [s for g in sets for s in g]
