@@ -476,9 +476,19 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     h->tok_off.resize((size_t)(V + 1));
     h->tok_blob.assign(tb ? tb + to[0] : nullptr, tb ? tb + to[V] : nullptr);
     h->tok_blob.insert(h->tok_blob.end(), (size_t)kBlobPad, 0);  // room for 16-byte window loads
+    const int64_t chunk = 1 << 14, nchunks = (V + chunk - 1) / chunk;
+    std::vector<int64_t> cmax((size_t)nchunks, 0);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        int64_t m = 0;
+        for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v) {
+            h->tok_off[(size_t)v] = (uint32_t)(to[v] - to[0]);
+            m = std::max<int64_t>(m, to[v + 1] - to[v]);
+        }
+        cmax[(size_t)c] = m;
+    });
+    h->tok_off[(size_t)V] = (uint32_t)(to[V] - to[0]);
     int64_t max_len = 0;
-    for (int64_t v = 0; v <= V; ++v) h->tok_off[(size_t)v] = (uint32_t)(to[v] - to[0]);
-    for (int64_t v = 0; v < V; ++v) max_len = std::max<int64_t>(max_len, to[v + 1] - to[v]);
+    for (int64_t m : cmax) max_len = std::max(max_len, m);
     if (max_len > 65535) {
         *err = "a token is longer than 65535 bytes";
         return TAM_E_TOOLARGE;
@@ -490,16 +500,24 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     uint64_t cap = 64;
     while (cap < (uint64_t)(2 * V)) cap <<= 1;
     const uint64_t nbuckets = cap / kBucket;
-    h->fps.assign(cap, (uint16_t)0);
-    h->pay.assign(cap, SlotPay{0, 0, -1, 0, 0, {0, 0}});
-    h->dup_next.assign((size_t)V, -1);
-    std::vector<int32_t> last(cap, -1);
+    // the tables are first touched, and set empty, in parallel
+    h->fps.resize(cap);
+    h->pay.resize(cap);
+    h->dup_next.resize((size_t)V);
+    hvec<int32_t> last(cap);
+    const SlotPay empty{0, 0, -1, 0, 0, {0, 0}};
+    const int64_t pchunk = 1 << 15, npchunks = ((int64_t)cap + pchunk - 1) / pchunk;
+    parallel_for(npchunks, host_threads(npchunks), [&](int64_t c) {
+        for (int64_t q = c * pchunk; q < std::min<int64_t>((int64_t)cap, (c + 1) * pchunk); ++q) {
+            h->fps[(size_t)q] = 0;
+            h->pay[(size_t)q] = empty;
+            last[(size_t)q] = -1;
+        }
+    });
     const uint8_t *blob = h->tok_blob.data();
-    // keys and reversed heads of all tokens, in parallel; the placement below is
-    // serial, in id order (duplicate chains ascend)
-    std::vector<uint64_t> keys((size_t)V), heads((size_t)V * 2);
-    const int64_t chunk = 8192;
-    parallel_for((V + chunk - 1) / chunk, host_threads((V + chunk - 1) / chunk), [&](int64_t c) {
+    // keys, reversed heads and home buckets of all tokens, in parallel
+    hvec<uint64_t> keys((size_t)V), heads((size_t)V * 2), home((size_t)V);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v) {
             const uint32_t off = h->tok_off[(size_t)v];
             const uint32_t len = h->tok_off[(size_t)v + 1] - off;
@@ -515,49 +533,118 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
             keys[(size_t)v] = len ? hash_final(hh, len) : 0;
             heads[(size_t)(2 * v)] = lo;
             heads[(size_t)(2 * v + 1)] = hi;
+            home[(size_t)v] = (keys[(size_t)v] & (cap - 1)) / kBucket;
+            h->dup_next[(size_t)v] = -1;
         }
     });
     for (int64_t v = 0; v < V; ++v) {
-        const uint32_t off = h->tok_off[(size_t)v];
-        const uint32_t len = h->tok_off[(size_t)v + 1] - off;
+        const uint32_t len = h->tok_off[(size_t)v + 1] - h->tok_off[(size_t)v];
         if (len == 0) continue;
         h->len_present[len] = 1;
         if (len < 64) h->len_mask |= 1ull << len;
-        const uint64_t key = keys[(size_t)v];
-        const uint16_t fp = (uint16_t)fingerprint(key);
-        uint64_t b = (key & (cap - 1)) / kBucket;
-        bool placed = false;
-        while (!placed) {
-            for (int i = 0; i < kBucket && !placed; ++i) {
-                const uint64_t s = b * kBucket + (uint64_t)i;
-                if (h->fps[s] == 0) {
-                    h->fps[s] = fp;
-                    h->pay[s] = SlotPay{heads[(size_t)(2 * v)], heads[(size_t)(2 * v + 1)], (int32_t)v,
-                                        (uint16_t)len, 1, {0, 0}};
-                    last[s] = (int32_t)v;
-                    placed = true;
-                } else if (h->fps[s] == fp && h->pay[s].len == len) {
-                    const uint32_t o2 = h->tok_off[(size_t)h->pay[s].first];
-                    if (std::memcmp(blob + o2, blob + off, len) == 0) {
-                        if (h->pay[s].count == 65535) {
-                            *err = "more than 65535 tokens share one byte string";
-                            return TAM_E_TOOLARGE;
-                        }
-                        h->dup_next[(size_t)last[s]] = (int32_t)v;
-                        last[s] = (int32_t)v;
-                        ++h->pay[s].count;
-                        placed = true;
+    }
+    // Placement: token v goes to the first slot, from its home bucket on, that
+    // is empty or holds its string (a duplicate joins that slot's id chain, in
+    // ascending id order).  The buckets are cut into ranges placed in parallel,
+    // each taking the tokens whose home bucket it holds, in id order.  A token
+    // that would have to move past its range's last bucket is deferred to a
+    // serial pass, in id order, over the filled table; a key therefore still
+    // sits in a later bucket only if every bucket from its home to there was
+    // full when it was placed, which is what the device probe relies on.
+    std::atomic<bool> too_many{false};
+    // place(v, b, stop, wrap): from bucket b on; with wrap, through the whole
+    // table (wrapping at its end), else only up to bucket stop (exclusive).
+    // False if not placed.
+    auto place = [&](int64_t v, uint64_t b, uint64_t stop, bool wrap) -> bool {
+        const uint32_t off = h->tok_off[(size_t)v];
+        const uint32_t len = h->tok_off[(size_t)v + 1] - off;
+        const uint16_t fp = (uint16_t)fingerprint(keys[(size_t)v]);
+        for (uint64_t n = 0; n < nbuckets; ++n) {
+            for (int i = 0; i < kBucket; ++i) {
+                const uint64_t sl = b * kBucket + (uint64_t)i;
+                if (h->fps[sl] == 0) {
+                    h->fps[sl] = fp;
+                    h->pay[sl] = SlotPay{heads[(size_t)(2 * v)], heads[(size_t)(2 * v + 1)], (int32_t)v,
+                                         (uint16_t)len, 1, {0, 0}};
+                    last[sl] = (int32_t)v;
+                    return true;
+                }
+                if (h->fps[sl] == fp && h->pay[sl].len == len &&
+                    std::memcmp(blob + h->tok_off[(size_t)h->pay[sl].first], blob + off, len) == 0) {
+                    if (h->pay[sl].count == 65535) {
+                        too_many = true;
+                        return true;
                     }
+                    h->dup_next[(size_t)last[sl]] = (int32_t)v;
+                    last[sl] = (int32_t)v;
+                    ++h->pay[sl].count;
+                    return true;
                 }
             }
-            b = (b + 1) % nbuckets;
+            if (!wrap && b + 1 >= stop) return false;
+            b = b + 1 == nbuckets ? 0 : b + 1;
         }
+        return false;  // not reached: the table is at most half full
+    };
+    const int64_t R = std::min<int64_t>(256, (int64_t)nbuckets);  // bucket ranges
+    auto range_of = [&](uint64_t b) { return (int64_t)(b * (uint64_t)R / nbuckets); };
+    auto range_start = [&](int64_t r) { return ((uint64_t)r * nbuckets + (uint64_t)R - 1) / (uint64_t)R; };
+    // the non-empty tokens grouped by range, in id order: per-chunk counts, then
+    // each chunk scatters its tokens after those of the chunks before it
+    std::vector<int64_t> ccount((size_t)(nchunks * R), 0);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        int64_t *cnt = ccount.data() + c * R;
+        for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v)
+            if (h->tok_off[(size_t)v + 1] > h->tok_off[(size_t)v]) ++cnt[range_of(home[(size_t)v])];
+    });
+    std::vector<int64_t> rcount((size_t)R + 1, 0);
+    for (int64_t r = 0; r < R; ++r) {
+        int64_t at = rcount[(size_t)r];
+        for (int64_t c = 0; c < nchunks; ++c) {
+            const int64_t n = ccount[(size_t)(c * R + r)];
+            ccount[(size_t)(c * R + r)] = at;
+            at += n;
+        }
+        rcount[(size_t)r + 1] = at;
+    }
+    hvec<int32_t> order((size_t)rcount[(size_t)R]);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        int64_t *at = ccount.data() + c * R;
+        for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v)
+            if (h->tok_off[(size_t)v + 1] > h->tok_off[(size_t)v]) order[(size_t)at[range_of(home[(size_t)v])]++] = (int32_t)v;
+    });
+    std::vector<std::vector<int32_t>> deferred((size_t)R);
+    parallel_for(R, host_threads(R), [&](int64_t r) {
+        const uint64_t stop = r + 1 < R ? range_start(r + 1) : nbuckets;
+        for (int64_t k = rcount[(size_t)r]; k < rcount[(size_t)r + 1]; ++k) {
+            const int32_t v = order[(size_t)k];
+            if (!place(v, home[(size_t)v], stop, false)) deferred[(size_t)r].push_back(v);
+        }
+    });
+    std::vector<int32_t> rest;
+    for (const auto &d : deferred) rest.insert(rest.end(), d.begin(), d.end());
+    std::sort(rest.begin(), rest.end());
+    for (int32_t v : rest) place(v, home[(size_t)v], nbuckets, true);
+    if (too_many) {
+        *err = "more than 65535 tokens share one byte string";
+        return TAM_E_TOOLARGE;
     }
     // per length d, the running sum over lengths <= d of the largest number of
     // token ids sharing one string of that length (for the list size bound)
     std::vector<int64_t> dup((size_t)max_len + 1, 0);
-    for (const SlotPay &sp : h->pay)
-        if (sp.first >= 0) dup[(size_t)sp.len] = std::max<int64_t>(dup[(size_t)sp.len], sp.count);
+    {
+        std::vector<std::vector<int64_t>> part((size_t)npchunks);
+        parallel_for(npchunks, host_threads(npchunks), [&](int64_t c) {
+            std::vector<int64_t> &d = part[(size_t)c];
+            d.assign((size_t)max_len + 1, 0);
+            for (int64_t q = c * pchunk; q < std::min<int64_t>((int64_t)cap, (c + 1) * pchunk); ++q) {
+                const SlotPay &sp = h->pay[(size_t)q];
+                if (sp.first >= 0) d[(size_t)sp.len] = std::max<int64_t>(d[(size_t)sp.len], sp.count);
+            }
+        });
+        for (const auto &d : part)
+            for (int64_t l = 0; l <= max_len; ++l) dup[(size_t)l] = std::max(dup[(size_t)l], d[(size_t)l]);
+    }
     h->dup_cum.assign((size_t)max_len + 1, 0);
     for (int64_t d = 1; d <= max_len; ++d) h->dup_cum[(size_t)d] = h->dup_cum[(size_t)d - 1] + dup[(size_t)d];
     return TAM_OK;

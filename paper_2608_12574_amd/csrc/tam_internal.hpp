@@ -223,11 +223,11 @@ struct tam_vocab {
     double host_ms = 0, upload_ms = 0;
 
     // host tables
-    std::vector<uint32_t> tok_off;
+    tam::hvec<uint32_t> tok_off;
     std::vector<uint8_t> tok_blob, len_present;
-    std::vector<uint16_t> fps;
-    std::vector<tam::SlotPay> pay;
-    std::vector<int32_t> dup_next;
+    tam::hvec<uint16_t> fps;
+    tam::hvec<tam::SlotPay> pay;
+    tam::hvec<int32_t> dup_next;
     std::vector<int64_t> dup_cum;  // [max_len+1] see build_vocab (list size bound)
 
     // device copies (one arena)

@@ -352,8 +352,8 @@ class Vocab:
 def compile(strings, vocab, sets=None, terminator: int = 0x22, flags: int = 0, device=None,
             stream=None, cache_rows: int = 0) -> Handle:
     """tam_compile over ``strings`` (list[bytes], or a packed pair (uint8 blob,
-    int64 offsets[K+1])) and ``vocab`` (a ``Vocab`` or a list[bytes], token id =
-    index).
+    int64 offsets[K+1])) and ``vocab`` (a ``Vocab``, or a list[bytes] or packed
+    pair, token id = index).
 
     ``sets``: optional forest offsets (S+1 ints) splitting ``strings`` into S sets.
     With ``FLAG_HOST_ONLY`` no GPU is touched (host tables only).
