@@ -474,8 +474,9 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     h->V = V;
     h->W = (V + 63) / 64;
     h->tok_off.resize((size_t)(V + 1));
-    h->tok_blob.assign(tb ? tb + to[0] : nullptr, tb ? tb + to[V] : nullptr);
-    h->tok_blob.insert(h->tok_blob.end(), (size_t)kBlobPad, 0);  // room for 16-byte window loads
+    h->tok_blob.resize((size_t)total + kBlobPad);  // zero pad: room for 16-byte window loads
+    if (total > 0) std::memcpy(h->tok_blob.data(), tb + to[0], (size_t)total);
+    std::memset(h->tok_blob.data() + total, 0, (size_t)kBlobPad);
     const int64_t chunk = 1 << 14, nchunks = (V + chunk - 1) / chunk;
     std::vector<int64_t> cmax((size_t)nchunks, 0);
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {

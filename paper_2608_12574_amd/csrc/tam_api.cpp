@@ -169,6 +169,7 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     tam_status st;
     const auto t0 = std::chrono::steady_clock::now();
     try {
+        const tam::PinnedScope pinned(!(v->flags & TAM_FLAG_HOST_ONLY));  // uploaded tables: pinned blocks
         st = tam::build_vocab(tok_bytes, tok_off, V, v, &err);
     } catch (const std::bad_alloc &) {
         st = TAM_E_NOMEM;
@@ -227,6 +228,7 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     if (e != hipSuccess) {
         st = hip_fail(e, "vocabulary upload");
         const std::string msg = g_err;
+        (void)hipStreamSynchronize(s);  // copies already enqueued still read the host tables
         vocab_release(v);
         return fail(st, msg);
     }

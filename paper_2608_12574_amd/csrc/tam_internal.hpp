@@ -224,7 +224,8 @@ struct tam_vocab {
 
     // host tables
     tam::hvec<uint32_t> tok_off;
-    std::vector<uint8_t> tok_blob, len_present;
+    tam::hvec<uint8_t> tok_blob;
+    std::vector<uint8_t> len_present;
     tam::hvec<uint16_t> fps;
     tam::hvec<tam::SlotPay> pay;
     tam::hvec<int32_t> dup_next;
