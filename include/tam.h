@@ -172,7 +172,9 @@ typedef struct {
     float dev_lists_ms;    /* sparse valid lists after the probe pass: prefix sum, fill */
     float dev_zero_ms;     /* zero fill of the dense table */
     float dev_mark_ms;     /* the probe pass: suffix probes, table marks, list counts */
-    float dev_total_ms;    /* first device phase start to last device phase end */
+    float dev_total_ms;    /* first device phase start to last device phase end; a compile of a
+                              full table enqueues its zero fill while the host still writes the
+                              trie, so this span then includes waiting for the host and uploads */
 } tam_timing;
 
 /*

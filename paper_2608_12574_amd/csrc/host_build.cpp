@@ -305,7 +305,8 @@ void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::v
  * parts' other child lists follow in node order.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
-                      int64_t S, int T, tam_handle *h, std::string *err) {
+                      int64_t S, int T, tam_handle *h, std::string *err,
+                      const std::function<tam_status(tam_handle *)> &planned) {
     const uint8_t term = (uint8_t)T;
     const int64_t total = so[K] - so[0];
     if (total > 0) {
@@ -412,6 +413,10 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->N = N;
     h->S = S;
     h->blob_bytes = BB;
+    if (planned) {  // sizes known, nothing emitted yet
+        const tam_status st = planned(h);
+        if (st != TAM_OK) return st;
+    }
     h->roots.resize((size_t)S);
     h->parent.resize((size_t)N);
     h->depth.resize((size_t)N);

@@ -256,6 +256,16 @@ void release_device(tam_handle *h) {
     h->work_done = nullptr;
 }
 
+// The phase events of TAM_FLAG_TIMING (created once).
+hipError_t create_events(tam_handle *h) {
+    if (h->have_events) return hipSuccess;
+    hipError_t e = hipSuccess;
+    for (hipEvent_t &ev : h->ev)
+        if (e == hipSuccess) e = hipEventCreate(&ev);
+    h->have_events = e == hipSuccess;
+    return e;
+}
+
 void destroy_handle(tam_handle *h) {
     if (!(h->flags & TAM_FLAG_HOST_ONLY)) release_device(h);
     vocab_release(h->vocab);
@@ -279,14 +289,17 @@ unsigned default_phases(const tam_handle *h) {
 // the probe pass (marks into the table, counts for the lists), then the lists'
 // prefix sum and fill.  Phase events are recorded only for the handle's
 // default phases.
-tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
+// zero_enqueued: the table's zero fill was already enqueued on `s`, with its
+// events (compile starts it while the host writes the trie).
+tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool zero_enqueued = false) {
     const tam::DevTables &t = h->dt;
     // Under stream capture (a HIP graph) only the kernels are recorded: no
     // events, which belong to eager calls.
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     TAM_HIP(hipStreamIsCapturing(s, &cap));
     const bool capturing = cap != hipStreamCaptureStatusNone;
-    const bool timing = h->have_events && phases == default_phases(h) && !capturing;
+    const unsigned counted = phases | (zero_enqueued ? unsigned(TAM_PHASE_ZERO) : 0u);
+    const bool timing = h->have_events && counted == default_phases(h) && !capturing;
     if (is_lazy(h)) {  // rows built on demand: only the cache is reset
         if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
         TAM_HIP(tam::launch_lazy_reset(t, h->lazy, s));
@@ -300,11 +313,13 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s) {
         return TAM_OK;
     }
     const bool lists = (phases & TAM_PHASE_LISTS) != 0;
-    const bool zero = (phases & TAM_PHASE_ZERO) && t.table;
+    const bool zero = (phases & TAM_PHASE_ZERO) && t.table && !zero_enqueued;
     const bool mark = (phases & TAM_PHASE_MARK) && t.table;
-    if (timing) TAM_HIP(hipEventRecord(h->ev[0], s));
+    if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[0], s));
     if (zero) TAM_HIP(tam::launch_zero(t.table, t.R * t.Wp, s));
-    if (timing) TAM_HIP(hipEventRecord(h->ev[1], s));
+    if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[1], s));
+    if (timing && zero_enqueued) TAM_HIP(hipEventRecord(h->ev[4], s));  // the probe's own start
+    if (timing) h->mark_from_ev4 = zero_enqueued;
     if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
     if (t.fmt_L >= 0) {
         if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
@@ -364,11 +379,49 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->vocab = vocab;
     std::string err;
     tam_status st;
+    // A full table's zero fill needs only the node count: it is enqueued as
+    // soon as the trie is planned and runs while the host writes the trie.
+    const bool early_zero =
+        !host_only && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_TAIL_LISTS | TAM_FLAG_LAZY_ROWS));
+    uint64_t *early_table = nullptr;
+    auto planned = [&](tam_handle *hh) -> tam_status {
+        (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
+        if (hipGetDevice(&hh->device) != hipSuccess) {
+            err = "no HIP device";
+            return TAM_E_DEVICE;
+        }
+        if (hh->device != vocab->device) {
+            err = "the vocabulary lives on another device";
+            return TAM_E_STATE;
+        }
+        hh->own_alloc = alloc == nullptr;
+        if (alloc) hh->alloc = *alloc;
+        const int64_t Wp = (vocab->W + 7) & ~int64_t(7);
+        const size_t bytes = (size_t)hh->N * (size_t)Wp * sizeof(uint64_t);
+        early_table = static_cast<uint64_t *>(dev_alloc(hh, bytes));
+        if (!early_table) {
+            err = "device allocation failed (" + std::to_string(bytes) + " bytes requested)";
+            return TAM_E_NOMEM;
+        }
+        hipError_t e = hipSuccess;
+        const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
+        if (timing) e = create_events(hh);
+        if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[0], s);
+        if (e == hipSuccess) e = tam::launch_zero(early_table, hh->N * Wp, s);
+        if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[1], s);
+        if (e != hipSuccess) {
+            err = std::string("table zero fill: ") + hipGetErrorString(e);
+            return TAM_E_DEVICE;
+        }
+        return TAM_OK;
+    };
     try {
         const auto t0 = std::chrono::steady_clock::now();
         const bool lazy = (o.flags & TAM_FLAG_LAZY_ROWS) != 0;
         const tam::PinnedScope pinned(!host_only);  // the uploaded trie tables go to pinned memory
-        st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err);  // with the tail split
+        st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err,  // with the tail split
+                             early_zero ? std::function<tam_status(tam_handle *)>(planned)
+                                        : std::function<tam_status(tam_handle *)>());
         h->timing.host_trie_ms = ms_since(t0);
         // the lists (and their size bound) are needed without a table, or with
         // tail compression when tokens exceed the probe window
@@ -386,6 +439,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         err = "out of host memory";
     }
     if (st != TAM_OK) {
+        if (early_table) (void)hipStreamSynchronize(s);  // the zero fill may still write the table
         destroy_handle(h);
         return fail(st, err);
     }
@@ -408,17 +462,19 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
 
     // ---- device: allocate, upload, build the lists or the table ----
     const auto t0 = std::chrono::steady_clock::now();
-    (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
-    if (hipGetDevice(&h->device) != hipSuccess) {
-        destroy_handle(h);
-        return fail(TAM_E_DEVICE, "no HIP device");
+    if (!early_table) {  // else done when the trie was planned
+        (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
+        if (hipGetDevice(&h->device) != hipSuccess) {
+            destroy_handle(h);
+            return fail(TAM_E_DEVICE, "no HIP device");
+        }
+        if (h->device != vocab->device) {
+            destroy_handle(h);
+            return fail(TAM_E_STATE, "the vocabulary lives on another device");
+        }
+        h->own_alloc = alloc == nullptr;
+        if (alloc) h->alloc = *alloc;
     }
-    if (h->device != vocab->device) {
-        destroy_handle(h);
-        return fail(TAM_E_STATE, "the vocabulary lives on another device");
-    }
-    h->own_alloc = alloc == nullptr;
-    if (alloc) h->alloc = *alloc;
     const bool lazy = is_lazy(h);
     const bool want_table = !lazy && !(h->flags & TAM_FLAG_NO_TABLE);
     const bool tails = want_table && !h->tail_span.empty();
@@ -465,10 +521,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_miss_count = a.take<int32_t>(1);
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
-    uint64_t *table = nullptr;
+    uint64_t *table = early_table;
     const size_t table_bytes = (size_t)(lazy ? C : R) * (size_t)h->Wp * sizeof(uint64_t);
-    if (base && (want_table || lazy)) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
+    if (base && (want_table || lazy) && !table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
     if (!base || ((want_table || lazy) && !table)) {
+        if (early_table) (void)hipStreamSynchronize(s);  // the zero fill may still write the table
         destroy_handle(h);
         return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
                                      " bytes requested)");
@@ -548,11 +605,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     if (e == hipSuccess && lazy) e = up(o_sub_end, h->sub_end.data(), h->sub_end.size() * 4);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
-    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
-        for (hipEvent_t &ev : h->ev)
-            if (e == hipSuccess) e = hipEventCreate(&ev);
-        h->have_events = e == hipSuccess;
-    }
+    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);
     h->timing.upload_ms = ms_since(t0);
     if (e != hipSuccess) {
         st = hip_fail(e, "upload");
@@ -561,7 +614,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         destroy_handle(h);
         return fail(st, msg);
     }
-    st = run_device_phase(h, default_phases(h), s);
+    st = run_device_phase(h, default_phases(h) & ~(early_table ? unsigned(TAM_PHASE_ZERO) : 0u), s,
+                          early_table != nullptr);
     if (st != TAM_OK) {
         const std::string msg = g_err;
         destroy_handle(h);
@@ -682,11 +736,7 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
                                             hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
-    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) {
-        for (hipEvent_t &ev : h->ev)
-            if (e == hipSuccess) e = hipEventCreate(&ev);
-        h->have_events = e == hipSuccess;
-    }
+    if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);
     h->timing.upload_ms = ms_since(t1);
     tam_status st = e == hipSuccess ? TAM_OK : hip_fail(e, "upload");
     if (st == TAM_OK) st = run_device_phase(h, default_phases(h), s);
@@ -895,7 +945,7 @@ tam_status tam_timing_get(const tam_handle *h, tam_timing *out) {
     if (h->have_events && h->events_recorded) {
         TAM_HIP(hipEventSynchronize(h->ev[3]));
         TAM_HIP(hipEventElapsedTime(&out->dev_zero_ms, h->ev[0], h->ev[1]));
-        TAM_HIP(hipEventElapsedTime(&out->dev_mark_ms, h->ev[1], h->ev[2]));
+        TAM_HIP(hipEventElapsedTime(&out->dev_mark_ms, h->ev[h->mark_from_ev4 ? 4 : 1], h->ev[2]));
         TAM_HIP(hipEventElapsedTime(&out->dev_lists_ms, h->ev[2], h->ev[3]));
         TAM_HIP(hipEventElapsedTime(&out->dev_total_ms, h->ev[0], h->ev[3]));
     }

@@ -274,7 +274,10 @@ struct tam_handle {
     std::vector<void *> dev_ptrs;  // everything allocated for this handle
     tam::DevTables dt{};
 
-    hipEvent_t ev[4] = {};
+    // phase events: zero start, zero end, probe end, lists end, and probe start
+    // (ev[4]) when the zero fill was enqueued earlier than the probe pass
+    hipEvent_t ev[5] = {};
+    bool mark_from_ev4 = false;
     int32_t *pairs = nullptr;       // device [mark_blocks(N)] per-block valid-pair counts
     bool lists_built = false;
     bool have_events = false;
