@@ -3,7 +3,6 @@
 #include <algorithm>
 #include <atomic>
 #include <cstring>
-#include <numeric>
 #include <thread>
 
 #include "host_build.hpp"
@@ -296,9 +295,10 @@ void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::v
  * Tries of all sets.  A set's trie is its root plus one subtrie per distinct
  * first byte of s+T, and in preorder those subtries follow one another in byte
  * order.  The unit of host work is a part: a whole set, or (for a large set)
- * the strings of one first byte; parts are built on their own, in parallel over
- * host threads, and laid out one after another with the part roots merged into
- * their set's root.  Set j takes node ids [roots[j], roots[j] + N_j) and its
+ * the strings of one first byte.  The parts are planned in parallel over host
+ * threads (sorted, their sizes counted), laid out one after another with the
+ * part roots merged into their set's root, and then written in parallel
+ * straight into the handle's tables.  Set j takes node ids [roots[j], roots[j] + N_j) and its
  * own range of the blob, which carries kBlobPad zero bytes in front and behind
  * so that 16-byte window loads around any node never leave it.  Edges: a set's
  * root lists its first-byte children (those of its parts, in order), then the
