@@ -300,10 +300,10 @@ void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::v
  * part roots merged into their set's root, and then written in parallel
  * straight into the handle's tables.  Set j takes node ids
  * [roots[j], roots[j] + N_j) and its own range of the blob, which carries
- * kBlobPad zero bytes in front and behind
- * so that 16-byte window loads around any node never leave it.  Edges: a set's
- * root lists its first-byte children (those of its parts, in order), then the
- * parts' other child lists follow in node order.
+ * kBlobPad zero bytes in front and behind so that 16-byte window loads around
+ * any node never leave it.  Edges: a set's root lists its first-byte children
+ * (those of its parts, in order), then the parts' other child lists follow in
+ * node order.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err,
