@@ -1,0 +1,125 @@
+// Definitions shared by the HIP kernels and the host code of libtam: the
+// vocabulary hash, the device view of a handle and the row cache of rows
+// built on demand.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace tam {
+
+// ---------------------------------------------------------------------------
+// Vocabulary hash: keys are the token bytes read last-to-first, so that a
+// suffix of a trie path can be hashed incrementally while walking backwards
+// from the node where it ends.  Host (table build) and device (probe) must
+// agree bit for bit, hence one definition for both.
+// ---------------------------------------------------------------------------
+constexpr uint64_t kHashSeed = 0xcbf29ce484222325ull;
+
+__host__ __device__ __forceinline__ uint64_t hash_step(uint64_t h, uint32_t byte) {
+    return (h ^ (byte + 1u)) * 0x100000001b3ull;
+}
+
+__host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len) {
+    uint64_t z = h + 0x9e3779b97f4a7c15ull * (uint64_t)(len + 1u);
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    z ^= z >> 31;
+    return z | 1ull;  // 0 never occurs as a key
+}
+
+// Vocabulary table: open addressing over buckets of 16 16-bit fingerprints (32
+// bytes per bucket), one slot per distinct non-empty token string.  A
+// slot's 32-byte payload (its first 16 bytes stored last byte first, its
+// smallest token id, length and duplicate count) is read only on a fingerprint
+// match, with one load.
+constexpr int kBucket = 16;   // fingerprints per bucket
+constexpr int kWin = 16;      // path bytes a probing node keeps in registers
+constexpr int kBlobPad = 32;  // zero bytes before and after the string blob (and after the token blob)
+
+__host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
+    return (uint32_t)(key >> 48) | 1u;  // 16 bits; 0 marks an empty slot
+}
+
+struct alignas(32) SlotPay {
+    uint64_t lo, hi;  // byte k = token byte len-1-k for k < min(len, 16), then zeros
+    int32_t first;    // smallest token id with this string (-1: empty slot)
+    uint16_t len;     // string length in bytes
+    uint16_t count;   // number of token ids with this string
+    uint32_t pad[2];
+};
+
+// What the probe pass stores per (node, suffix length): the token id when the
+// string has one id, -2 - slot when it has several, -1 when no token matches.
+__host__ __device__ __forceinline__ int32_t hit_of_slot(int32_t slot, int32_t first, int count) {
+    return count == 1 ? first : -2 - slot;
+}
+
+// ---------------------------------------------------------------------------
+// Device-side view of a compiled handle (plain pointers, passed to kernels).
+// ---------------------------------------------------------------------------
+struct DevTables {
+    // trie (a1)
+    const uint8_t *blob;        // [pad 32][per string: pad, bytes, T][pad 32]
+    const int32_t *node_at;     // [blob_bytes] node whose edge byte is that blob byte (pad: root)
+    const int32_t *node_pos;    // [N] blob offset of the node's edge byte (-1 at roots)
+    const int32_t *depth;       // [N]
+    const int32_t *child_off;   // [N+1]
+    const uint8_t *child_byte;  // [N-S]
+    const int32_t *child_node;  // [N-S]
+    // vocabulary (a2)
+    const uint32_t *tok_off;    // [V+1]
+    const uint8_t *tok_blob;
+    const uint16_t *fps;        // [slot_mask+1] fingerprints, kBucket per bucket
+    const SlotPay *pay;         // [slot_mask+1]
+    const int32_t *dup_next;    // [V] next id with the same bytes, -1 at the end
+    const uint8_t *len_present; // [max_len+1] 1 if some token has that length
+    // valid lists (a4) and dense table
+    int32_t *hits;              // [kWin][N] hit_of_slot of the suffix of length d+1 of node m, or -1
+    int32_t *count;             // [N]
+    int32_t *row_ptr;           // [N+1]
+    int32_t *cursor;            // [N]
+    int32_t *entries;           // [entry_bound]
+    uint64_t *table;            // [R][Wp] or null
+    // tail compression (null unless the handle has both a table and lists):
+    // hits at distance d <= tail_span[m] above node m land on tail nodes (lists),
+    // the others on branching nodes (dense rows row_of[node])
+    const int32_t *tail_span;   // [N]
+    const int32_t *row_of;      // [N] dense row of a node; a tail a: -1 - (nodes below a); null: row = node id
+    const int32_t *row_at;      // [blob_bytes] row_of[node_at[p]]; equals node_at without row_of
+    const int32_t *sub_end;     // [N] one past the node's subtree (rows built on demand), or null
+    int32_t *scan_tmp;          // block sums of the scan
+    int64_t N, V, W, Wp;
+    int64_t R;                  // dense rows (N for a full table, 0 without one)
+    int32_t tail_long;          // tail compression with tokens longer than kWin: their hits on
+                                // tails go to the lists (row_ptr / entries)
+    int64_t blob_bytes;
+    uint64_t slot_mask;         // slots - 1 (slots = a power of two, >= kBucket)
+    uint64_t len_mask;          // bit d (d < 64): some token has length d
+    int32_t max_len;
+    int32_t terminator;
+    // character-position masks (tam_compile_format): classes of positions 0..L-1
+    const uint8_t *classes;     // [L][32] bit rows, or null for a trie handle
+    int32_t fmt_L;              // L, or -1 for a trie handle
+};
+
+// Rows built on demand (TAM_FLAG_LAZY_ROWS): the row cache, and the scratch
+// of one group of at most kLazyGroup batch rows.
+constexpr int kLazyGroup = 1024;
+struct LazyDev {
+    uint64_t *cache;       // [C][Wp] cached rows
+    int32_t *slot_of;      // [N] cache slot holding the node's row, or -1
+    int32_t *node_of;      // [C] node whose row a slot holds, or -1
+    uint32_t *stamp;       // [C] number of the group that last used the slot
+    uint32_t *ref;         // [C] CLOCK reference bit
+    uint32_t *state;       // [0] groups assigned so far, [1] CLOCK hand
+    int32_t *rows_src;     // [kLazyGroup] cache slot of each batch row of the group, -1 = dead
+    int32_t *miss_node;    // [kLazyGroup] nodes whose rows are built, in batch-row order
+    int32_t *miss_row;     // [kLazyGroup] their destination rows (slots, or output rows)
+    int64_t *miss_off;     // [kLazyGroup + 1] prefix sum of their subtree sizes (minus the node)
+    int32_t *miss_count;   // [1]
+    int64_t C;             // cache rows
+};
+
+}  // namespace tam
