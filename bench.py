@@ -319,6 +319,26 @@ class Bench:
             root_us, apply_us = apply_us, time_apply(traj)
         apply_gbps = apply_bytes / (apply_us * 1e-6) / 1e9
 
+        # logit reads no masking in place can avoid: a 16-byte chunk holding
+        # both valid and invalid tokens must be read; the algorithmic bytes
+        # above leave them out.  Counted from the exported rows of the timed ids.
+        def mixed_chunks(id_tensor):
+            rows = h.export_rows(id_tensor)                       # [B, W] int64 words
+            E = 16 // self.esize                                  # tokens per chunk
+            bytes_ = rows.view(torch.uint8)[:, : (V // 8)]        # whole bytes of full chunks
+            if E == 8:
+                chunk_bits = bytes_.to(torch.int32)
+                full = 0xFF
+            else:
+                b = bytes_.to(torch.int32)
+                chunk_bits = torch.stack([b & 0xF, b >> 4], dim=2).reshape(b.shape[0], -1)
+                full = 0xF
+            return int(((chunk_bits != 0) & (chunk_bits != full)).sum().item())
+
+        id_lists = traj if root_us is not None else [ids]
+        mixed = float(np.mean([mixed_chunks(x) for x in id_lists]))
+        required_bytes = apply_bytes + 16 * mixed
+
         a0, a1 = self.event(), self.event()
         torch.cuda.synchronize()
         a0.record()
@@ -371,6 +391,9 @@ class Bench:
                            "phases_cold": phases_cold, "phases_warm": phases_warm},
             "apply": {"us": round(apply_us, 3), "GBps": round(apply_gbps, 1), "bytes": apply_bytes,
                       "frac_of_hbm_roofline": round(apply_gbps / HBM_PEAK_GBPS, 4),
+                      "mixed_chunks_per_call": round(mixed, 1),
+                      "required_bytes": int(required_bytes),
+                      "frac_of_required": round(required_bytes / (apply_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                       "iters": self.args.apply_iters,
                       "rows": (f"{w.decode_steps}-step decode trajectory from the roots" if root_us is not None
                                else w.node_mode),
