@@ -307,7 +307,8 @@ void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::v
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err,
-                      const std::function<tam_status(tam_handle *)> &planned) {
+                      const std::function<tam_status(tam_handle *)> &planned,
+                      const std::function<tam_status(tam_handle *, const TrieRange &)> &emitted) {
     const uint8_t term = (uint8_t)T;
     const int64_t total = so[K] - so[0];
     if (total > 0) {
@@ -369,12 +370,13 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     // bases: node ids (a part's local root is its set's root, the rest follow),
     // blob offsets, edges (a set's root edges first, then its parts' others)
     std::vector<PartBase> base((size_t)NP);
-    std::vector<int64_t> root((size_t)S), root_edges((size_t)S);
+    std::vector<int64_t> root((size_t)S), root_edges((size_t)S), set_blob((size_t)S);
     int64_t N = 0, BB = kBlobPad, E = 0;
     h->K_unique = 0;
     for (int64_t j = 0; j < S; ++j) {
         root[(size_t)j] = N++;
         root_edges[(size_t)j] = E;
+        set_blob[(size_t)j] = BB;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
             const PartPlan &r = parts[(size_t)p];
             if (r.st != TAM_OK) {
@@ -414,6 +416,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->N = N;
     h->S = S;
     h->blob_bytes = BB;
+    h->edges = E;
     if (planned) {  // sizes known, nothing emitted yet
         const tam_status st = planned(h);
         if (st != TAM_OK) return st;
@@ -449,16 +452,30 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         h->child_off[(size_t)rt] = (int32_t)root_edges[(size_t)j];
         if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
     }
-    parallel_for(NP, host_threads(NP), [&](int64_t p) {
-        try {
-            emit_part(sb, so, term, parts[(size_t)p], base[(size_t)p], subtrees, tails, h);
-        } catch (const std::bad_alloc &) {
-            oom = true;
-        }
-    });
-    if (oom) throw std::bad_alloc();
-    if (tails) number_dense_rows(S, root, set_first, parts, base, h);
     h->child_off[(size_t)N] = (int32_t)E;
+    // Emission in groups of whole sets (a forest of many sets: four groups, so
+    // that a caller can upload a group while the next is written).
+    const int64_t groups = emitted && S >= 8 ? 4 : 1;
+    for (int64_t g = 0; g < groups; ++g) {
+        const int64_t j0 = S * g / groups, j1 = S * (g + 1) / groups;
+        const int64_t p0 = set_first[(size_t)j0], p1 = set_first[(size_t)j1];
+        parallel_for(p1 - p0, host_threads(p1 - p0), [&](int64_t i) {
+            try {
+                emit_part(sb, so, term, parts[(size_t)(p0 + i)], base[(size_t)(p0 + i)], subtrees, tails, h);
+            } catch (const std::bad_alloc &) {
+                oom = true;
+            }
+        });
+        if (oom) throw std::bad_alloc();
+        if (emitted) {
+            const TrieRange r{root[(size_t)j0], j1 < S ? root[(size_t)j1] : N,
+                              g == 0 ? 0 : set_blob[(size_t)j0], j1 < S ? set_blob[(size_t)j1] : BB,
+                              root_edges[(size_t)j0], j1 < S ? root_edges[(size_t)j1] : E};
+            const tam_status st = emitted(h, r);
+            if (st != TAM_OK) return st;
+        }
+    }
+    if (tails) number_dense_rows(S, root, set_first, parts, base, h);
     return TAM_OK;
 }
 

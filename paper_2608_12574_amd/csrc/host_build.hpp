@@ -8,11 +8,21 @@
 
 namespace tam {
 
-// planned (optional) runs once the trie's sizes (N, S, blob bytes) are set in
-// h and before any node is written; a non-OK status aborts the build.
+// Ranges of the trie tables that are complete: nodes [n_lo, n_hi) (child_off
+// also entry N when n_hi == N), blob bytes [b_lo, b_hi), edges [e_lo, e_hi).
+struct TrieRange {
+    int64_t n_lo, n_hi, b_lo, b_hi, e_lo, e_hi;
+};
+
+// planned (optional) runs once the trie's sizes (N, S, blob bytes, edges) are
+// set in h and before any node is written.  emitted (optional) runs after each
+// group of whole sets has been written (the trie's tables in those ranges are
+// then final; tail compression's tables come after the last group).  A non-OK
+// status of either aborts the build.
 tam_status build_trie(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
                       const int64_t *set_off, int64_t S, int terminator, tam_handle *h,
-                      std::string *err, const std::function<tam_status(tam_handle *)> &planned = {});
+                      std::string *err, const std::function<tam_status(tam_handle *)> &planned = {},
+                      const std::function<tam_status(tam_handle *, const TrieRange &)> &emitted = {});
 tam_status build_vocab(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, tam_vocab *h,
                        std::string *err);
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v);

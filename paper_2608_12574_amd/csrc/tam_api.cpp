@@ -379,12 +379,21 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->vocab = vocab;
     std::string err;
     tam_status st;
-    // A full table's zero fill needs only the node count: it is enqueued as
-    // soon as the trie is planned and runs while the host writes the trie.
+    // Device work starts before the host has finished the trie: once the trie
+    // is planned its device arrays are allocated (and a full table's zero fill,
+    // which needs only the node count, is enqueued); each group of sets is
+    // uploaded as soon as the host has written it, so that the copies run while
+    // the next group is written.
     const bool early_zero =
         !host_only && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_TAIL_LISTS | TAM_FLAG_LAZY_ROWS));
     uint64_t *early_table = nullptr;
+    uint8_t *trie_base = nullptr;  // blob, node_at, node_pos, depth, child_off, child_byte, child_node, sub_end
+    size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
+           o_child_node = 0, o_sub_end = 0;
+    bool enqueued = false;  // device work that reads host tables or writes device memory
+    double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
     auto planned = [&](tam_handle *hh) -> tam_status {
+        const auto t1 = std::chrono::steady_clock::now();
         (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
         if (hipGetDevice(&hh->device) != hipSuccess) {
             err = "no HIP device";
@@ -396,21 +405,67 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         }
         hh->own_alloc = alloc == nullptr;
         if (alloc) hh->alloc = *alloc;
-        const int64_t Wp = (vocab->W + 7) & ~int64_t(7);
-        const size_t bytes = (size_t)hh->N * (size_t)Wp * sizeof(uint64_t);
-        early_table = static_cast<uint64_t *>(dev_alloc(hh, bytes));
-        if (!early_table) {
-            err = "device allocation failed (" + std::to_string(bytes) + " bytes requested)";
+        Arena ta;
+        o_blob = ta.take<uint8_t>(hh->blob_bytes);
+        o_node_at = ta.take<int32_t>(hh->blob_bytes);
+        o_node_pos = ta.take<int32_t>(hh->N);
+        o_depth = ta.take<int32_t>(hh->N);
+        o_child_off = ta.take<int32_t>(hh->N + 1);
+        o_child_byte = ta.take<uint8_t>(hh->edges);
+        o_child_node = ta.take<int32_t>(hh->edges);
+        o_sub_end = ta.take<int32_t>((hh->flags & TAM_FLAG_LAZY_ROWS) ? hh->N : 0);
+        trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
+        if (!trie_base) {
+            err = "device allocation failed (" + std::to_string(ta.used) + " bytes requested)";
             return TAM_E_NOMEM;
         }
+        hh->device_bytes = (int64_t)ta.used;
+        if (early_zero) {
+            const int64_t Wp = (vocab->W + 7) & ~int64_t(7);
+            const size_t bytes = (size_t)hh->N * (size_t)Wp * sizeof(uint64_t);
+            early_table = static_cast<uint64_t *>(dev_alloc(hh, bytes));
+            if (!early_table) {
+                err = "device allocation failed (" + std::to_string(bytes) + " bytes requested)";
+                return TAM_E_NOMEM;
+            }
+            hh->device_bytes += (int64_t)bytes;
+            hipError_t e = hipSuccess;
+            const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
+            if (timing) e = create_events(hh);
+            if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[0], s);
+            if (e == hipSuccess) e = tam::launch_zero(early_table, hh->N * Wp, s);
+            enqueued = true;
+            if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[1], s);
+            if (e != hipSuccess) {
+                err = std::string("table zero fill: ") + hipGetErrorString(e);
+                return TAM_E_DEVICE;
+            }
+        }
+        hook_ms += ms_since(t1);
+        return TAM_OK;
+    };
+    auto emitted = [&](tam_handle *hh, const tam::TrieRange &r) -> tam_status {
+        const auto t1 = std::chrono::steady_clock::now();
         hipError_t e = hipSuccess;
-        const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
-        if (timing) e = create_events(hh);
-        if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[0], s);
-        if (e == hipSuccess) e = tam::launch_zero(early_table, hh->N * Wp, s);
-        if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[1], s);
+        auto up = [&](size_t off, const void *src, int64_t lo, int64_t hi, size_t elem) {
+            if (e == hipSuccess && hi > lo) {
+                e = hipMemcpyAsync(trie_base + off + (size_t)lo * elem, static_cast<const uint8_t *>(src) + (size_t)lo * elem,
+                                   (size_t)(hi - lo) * elem, hipMemcpyHostToDevice, s);
+                enqueued = true;
+            }
+        };
+        const int64_t n_top = r.n_hi == hh->N ? hh->N + 1 : r.n_hi;  // child_off[N] with the last group
+        up(o_blob, hh->blob.data(), r.b_lo, r.b_hi, 1);
+        up(o_node_at, hh->node_at.data(), r.b_lo, r.b_hi, 4);
+        up(o_node_pos, hh->node_pos.data(), r.n_lo, r.n_hi, 4);
+        up(o_depth, hh->depth.data(), r.n_lo, r.n_hi, 4);
+        up(o_child_off, hh->child_off.data(), r.n_lo, n_top, 4);
+        up(o_child_byte, hh->child_byte.data(), r.e_lo, r.e_hi, 1);
+        up(o_child_node, hh->child_node.data(), r.e_lo, r.e_hi, 4);
+        if (hh->flags & TAM_FLAG_LAZY_ROWS) up(o_sub_end, hh->sub_end.data(), r.n_lo, r.n_hi, 4);
+        hook_ms += ms_since(t1);
         if (e != hipSuccess) {
-            err = std::string("table zero fill: ") + hipGetErrorString(e);
+            err = std::string("upload: ") + hipGetErrorString(e);
             return TAM_E_DEVICE;
         }
         return TAM_OK;
@@ -419,10 +474,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         const auto t0 = std::chrono::steady_clock::now();
         const bool lazy = (o.flags & TAM_FLAG_LAZY_ROWS) != 0;
         const tam::PinnedScope pinned(!host_only);  // the uploaded trie tables go to pinned memory
+        using Planned = std::function<tam_status(tam_handle *)>;
+        using Emitted = std::function<tam_status(tam_handle *, const tam::TrieRange &)>;
         st = tam::build_trie(str_bytes, str_off, K, set_off, S, o.terminator, h, &err,  // with the tail split
-                             early_zero ? std::function<tam_status(tam_handle *)>(planned)
-                                        : std::function<tam_status(tam_handle *)>());
-        h->timing.host_trie_ms = ms_since(t0);
+                             host_only ? Planned() : Planned(planned), host_only ? Emitted() : Emitted(emitted));
+        h->timing.host_trie_ms = ms_since(t0) - hook_ms;
         // the lists (and their size bound) are needed without a table, or with
         // tail compression when tokens exceed the probe window
         const bool lists = !lazy && ((o.flags & TAM_FLAG_NO_TABLE) ||
@@ -439,7 +495,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         err = "out of host memory";
     }
     if (st != TAM_OK) {
-        if (early_table) (void)hipStreamSynchronize(s);  // the zero fill may still write the table
+        if (enqueued) (void)hipStreamSynchronize(s);  // copies may still read the host tables
         destroy_handle(h);
         return fail(st, err);
     }
@@ -448,6 +504,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->Wp = (h->W + 7) & ~int64_t(7);  // rows 64-byte aligned
     if (is_lazy(h)) {
         if (o.cache_rows < 0) {
+            if (enqueued) (void)hipStreamSynchronize(s);
             destroy_handle(h);
             return fail(TAM_E_INVAL, "cache_rows must be >= 0");
         }
@@ -460,21 +517,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         return TAM_OK;
     }
 
-    // ---- device: allocate, upload, build the lists or the table ----
+    // ---- device: the remaining tables, uploads and the device phases ----
     const auto t0 = std::chrono::steady_clock::now();
-    if (!early_table) {  // else done when the trie was planned
-        (void)hipGetLastError();  // clear a stale error of an earlier, unrelated call
-        if (hipGetDevice(&h->device) != hipSuccess) {
-            destroy_handle(h);
-            return fail(TAM_E_DEVICE, "no HIP device");
-        }
-        if (h->device != vocab->device) {
-            destroy_handle(h);
-            return fail(TAM_E_STATE, "the vocabulary lives on another device");
-        }
-        h->own_alloc = alloc == nullptr;
-        if (alloc) h->alloc = *alloc;
-    }
     const bool lazy = is_lazy(h);
     const bool want_table = !lazy && !(h->flags & TAM_FLAG_NO_TABLE);
     const bool tails = want_table && !h->tail_span.empty();
@@ -485,13 +529,6 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const int64_t R = !want_table ? 0 : tails ? std::max<int64_t>(h->dense_rows, 1) : h->N;
 
     Arena a;
-    const size_t o_blob = a.take<uint8_t>(h->blob_bytes);
-    const size_t o_node_at = a.take<int32_t>(h->blob_bytes);
-    const size_t o_node_pos = a.take<int32_t>(h->N);
-    const size_t o_depth = a.take<int32_t>(h->N);
-    const size_t o_child_off = a.take<int32_t>(h->N + 1);
-    const size_t o_child_byte = a.take<uint8_t>((int64_t)h->child_byte.size());
-    const size_t o_child_node = a.take<int32_t>((int64_t)h->child_node.size());
     // the probe pass's tables (none when rows are built on demand)
     const int64_t NP = lazy ? 0 : h->N;
     const size_t o_hits = a.take<int32_t>(tam::kWin * NP);
@@ -508,7 +545,6 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // rows built on demand: subtree extents, the cache's bookkeeping, the
     // scratch of one group of batch rows
     const int64_t C = lazy ? h->cache_rows : 0, G = lazy ? tam::kLazyGroup : 0;
-    const size_t o_sub_end = a.take<int32_t>(lazy ? h->N : 0);
     const size_t o_slot_of = a.take<int32_t>(lazy ? h->N : 0);
     const size_t o_node_of = a.take<int32_t>(C);
     const size_t o_stamp = a.take<uint32_t>(C);
@@ -525,22 +561,22 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t table_bytes = (size_t)(lazy ? C : R) * (size_t)h->Wp * sizeof(uint64_t);
     if (base && (want_table || lazy) && !table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
     if (!base || ((want_table || lazy) && !table)) {
-        if (early_table) (void)hipStreamSynchronize(s);  // the zero fill may still write the table
+        (void)hipStreamSynchronize(s);  // copies may still read the host tables
         destroy_handle(h);
         return fail(TAM_E_NOMEM, "device allocation failed (" + std::to_string(a.used + table_bytes) +
                                      " bytes requested)");
     }
-    h->device_bytes = (int64_t)a.used + (table ? (int64_t)table_bytes : 0);
+    h->device_bytes += (int64_t)a.used + (table && !early_table ? (int64_t)table_bytes : 0);
     h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
 
     tam::DevTables &t = h->dt;
-    t.blob = base + o_blob;
-    t.node_at = reinterpret_cast<const int32_t *>(base + o_node_at);
-    t.node_pos = reinterpret_cast<const int32_t *>(base + o_node_pos);
-    t.depth = reinterpret_cast<const int32_t *>(base + o_depth);
-    t.child_off = reinterpret_cast<const int32_t *>(base + o_child_off);
-    t.child_byte = base + o_child_byte;
-    t.child_node = reinterpret_cast<const int32_t *>(base + o_child_node);
+    t.blob = trie_base + o_blob;
+    t.node_at = reinterpret_cast<const int32_t *>(trie_base + o_node_at);
+    t.node_pos = reinterpret_cast<const int32_t *>(trie_base + o_node_pos);
+    t.depth = reinterpret_cast<const int32_t *>(trie_base + o_depth);
+    t.child_off = reinterpret_cast<const int32_t *>(trie_base + o_child_off);
+    t.child_byte = trie_base + o_child_byte;
+    t.child_node = reinterpret_cast<const int32_t *>(trie_base + o_child_node);
     t.tok_off = vocab->d_tok_off;
     t.tok_blob = vocab->d_tok_blob;
     t.fps = vocab->d_fps;
@@ -554,7 +590,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
     t.scan_tmp = reinterpret_cast<int32_t *>(base + o_scan);
     t.table = lazy ? nullptr : table;
-    t.sub_end = lazy ? reinterpret_cast<const int32_t *>(base + o_sub_end) : nullptr;
+    t.sub_end = lazy ? reinterpret_cast<const int32_t *>(trie_base + o_sub_end) : nullptr;
     if (lazy) {
         tam::LazyDev &z = h->lazy;
         z.cache = table;
@@ -592,21 +628,13 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         return hipMemcpyAsync(base + off, src, bytes, hipMemcpyHostToDevice, s);
     };
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
-    if (e == hipSuccess) e = up(o_blob, h->blob.data(), h->blob.size());
-    if (e == hipSuccess) e = up(o_node_at, h->node_at.data(), h->node_at.size() * 4);
-    if (e == hipSuccess) e = up(o_node_pos, h->node_pos.data(), h->node_pos.size() * 4);
-    if (e == hipSuccess) e = up(o_depth, h->depth.data(), h->depth.size() * 4);
-    if (e == hipSuccess) e = up(o_child_off, h->child_off.data(), h->child_off.size() * 4);
-    if (e == hipSuccess) e = up(o_child_byte, h->child_byte.data(), h->child_byte.size());
-    if (e == hipSuccess) e = up(o_child_node, h->child_node.data(), h->child_node.size() * 4);
     if (e == hipSuccess && tails) e = up(o_tail_span, h->tail_span.data(), h->tail_span.size() * 4);
     if (e == hipSuccess && tails) e = up(o_row_of, h->row_of.data(), h->row_of.size() * 4);
     if (e == hipSuccess && tails) e = up(o_row_at, h->row_at.data(), h->row_at.size() * 4);
-    if (e == hipSuccess && lazy) e = up(o_sub_end, h->sub_end.data(), h->sub_end.size() * 4);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);
-    h->timing.upload_ms = ms_since(t0);
+    h->timing.upload_ms = hook_ms + ms_since(t0);
     if (e != hipSuccess) {
         st = hip_fail(e, "upload");
         const std::string msg = g_err;

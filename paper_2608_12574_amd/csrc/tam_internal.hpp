@@ -141,7 +141,7 @@ struct tam_handle {
     tam_allocator alloc{};
     tam_vocab *vocab = nullptr;  // one reference held by the handle
 
-    int64_t N = 0, S = 0, K_unique = 0, V = 0, W = 0, Wp = 0;
+    int64_t N = 0, S = 0, K_unique = 0, V = 0, W = 0, Wp = 0, edges = 0;
     int64_t blob_bytes = 0, entry_bound = 0, device_bytes = 0;
 
     // host trie tables
