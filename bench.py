@@ -287,20 +287,34 @@ class Bench:
               flush=True)
 
         # mask apply alone: the paper's protocol (200 warm-up + 1,000 timed)
-        def time_apply(id_list):
+        def time_apply(id_list, iters=None):
+            iters = iters or self.args.apply_iters
             for i in range(self.args.apply_warmup):
                 h.apply_mask(id_list[i % len(id_list)], bufs[i % nbuf])
             a0, a1 = self.event(), self.event()
             torch.cuda.synchronize()
             a0.record()
-            for i in range(self.args.apply_iters):
+            for i in range(iters):
                 h.apply_mask(id_list[i % len(id_list)], bufs[i % nbuf])
             a1.record()
             torch.cuda.synchronize()
-            return a0.elapsed_time(a1) * 1e3 / self.args.apply_iters
+            return a0.elapsed_time(a1) * 1e3 / iters
 
         apply_bytes = B * (Wd * 8 + V * self.esize)
-        apply_us = time_apply([ids])
+        # uniform rows: a decode moves every row each step, so the timed calls
+        # take 64 id lists in turn and each call reads its mask rows from HBM;
+        # the same ids every call (their rows then stay in the caches) are
+        # reported beside
+        same_rows = None
+        if w.node_mode == "uniform":
+            id_lists = [ids] + [torch.as_tensor(W.uniform_nodes(w.config_id, N, B, seed_extra=1 + k), device=dev)
+                                for k in range(63)]
+            s_us = time_apply([ids], max(20, self.args.apply_iters // 5))
+            same_rows = {"us": round(s_us, 3), "GBps": round(apply_bytes / (s_us * 1e-6) / 1e9, 1),
+                         "frac_of_hbm_roofline": round(apply_bytes / (s_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+        else:
+            id_lists = [ids]
+        apply_us = time_apply(id_lists)
         root_us = None
         # workloads that decode from their roots: apply over the whole trajectory.
         # Rows take the argmax of their masked logits (a uniformly random valid
@@ -317,6 +331,7 @@ class Bench:
                 cur = torch.where((nxt < 0) | fin_dev[nxt.clamp(min=0).long()], ids, nxt)
                 del lg
             root_us, apply_us = apply_us, time_apply(traj)
+            id_lists = traj
         apply_gbps = apply_bytes / (apply_us * 1e-6) / 1e9
 
         # logit reads no masking in place can avoid: a 16-byte chunk holding
@@ -335,8 +350,21 @@ class Bench:
                 full = 0xF
             return int(((chunk_bits != 0) & (chunk_bits != full)).sum().item())
 
-        id_lists = traj if root_us is not None else [ids]
+        # 128-byte lines of the logits (whole lines only) holding both valid and
+        # invalid tokens: lines the call writes in part
+        def partial_lines(id_tensor):
+            rows = h.export_rows(id_tensor)
+            T = 128 // self.esize                                 # tokens per line: 64 or 32
+            if T == 64:
+                words = rows[:, : V // 64]
+                ones = -1
+            else:
+                w32 = rows.view(torch.int32)[:, : V // 32]
+                words, ones = w32, -1
+            return int(((words != 0) & (words != ones)).sum().item())
+
         mixed = float(np.mean([mixed_chunks(x) for x in id_lists]))
+        partial = float(np.mean([partial_lines(x) for x in id_lists]))
         required_bytes = apply_bytes + 16 * mixed
 
         a0, a1 = self.event(), self.event()
@@ -350,7 +378,14 @@ class Bench:
         # the same calls replayed from a HIP graph: the device time without the
         # Python call overhead that bounds the eager loop
         advance_us = self.graph_us(lambda: h.advance(ids, toks, out=out), 100)
-        apply_graph_us = self.graph_us(lambda: h.apply_mask(ids, bufs[0]), 100)
+        calls = [0]
+
+        def apply_next():  # the timed rows and buffers in turn
+            k = calls[0]
+            calls[0] += 1
+            h.apply_mask(id_lists[k % len(id_lists)], bufs[k % nbuf])
+
+        apply_graph_us = self.graph_us(apply_next, 100)
 
         # the dominant compile kernel and its algorithmic bytes
         if rep == "lists":
@@ -391,11 +426,14 @@ class Bench:
                            "phases_cold": phases_cold, "phases_warm": phases_warm},
             "apply": {"us": round(apply_us, 3), "GBps": round(apply_gbps, 1), "bytes": apply_bytes,
                       "frac_of_hbm_roofline": round(apply_gbps / HBM_PEAK_GBPS, 4),
+                      "same_rows_every_call": same_rows,
                       "mixed_chunks_per_call": round(mixed, 1),
+                      "partial_lines_per_call": round(partial, 1),
                       "required_bytes": int(required_bytes),
                       "frac_of_required": round(required_bytes / (apply_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                       "iters": self.args.apply_iters,
                       "rows": (f"{w.decode_steps}-step decode trajectory from the roots" if root_us is not None
+                               else "uniform, 64 id lists in turn (new rows every call)" if same_rows
                                else w.node_mode),
                       "first_step_at_roots": (
                           {"us": round(root_us, 3),
@@ -408,7 +446,8 @@ class Bench:
         }
         if res["compile_ms"]["one_set_warm"] is not None:
             print(f"[bench] {rep}: one set alone compiles in {res['compile_ms']['one_set_warm']:.3f} ms (warm)", flush=True)
-        print(f"[bench] {rep}: apply {apply_us:.2f} us ({apply_gbps:.0f} GB/s; graph-replayed {apply_graph_us:.2f} us), "
+        print(f"[bench] {rep}: apply {apply_us:.2f} us ({apply_gbps:.0f} GB/s; graph-replayed {apply_graph_us:.2f} us"
+              + (f"; same rows every call {same_rows['us']:.2f} us" if same_rows else "") + "), "
               f"advance {advance_us:.2f} us (graph-replayed; eager loop {advance_eager_us:.2f} us)", flush=True)
         return h, res
 

@@ -17,7 +17,9 @@
 //   k_rows   -- one wave per row builds rows in registers from the lists
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
-//   k_apply  -- write-mostly masking of [B, V] logits.
+//   k_apply  -- write-mostly masking of [B, V] logits (lists, tail rows, and
+//               unaligned rows); k_apply_dense for dense-table rows, two
+//               rows per block.
 //   k_advance-- B byte walks over the child tables, one wave per row.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
@@ -39,6 +41,7 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
 constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
+constexpr int kApplyRows = 2;        // rows per block of k_apply_dense (measured best on rows that change every call)
 constexpr int kProbeLanes = 4;       // lanes per node in k_probe (each takes 16 / 4 suffix lengths)
 // k_apply row sources: the dense table, the valid lists, or per row either
 // (tail compression: dense rows for branching nodes, lists for tails)
@@ -737,6 +740,72 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
     }
 }
 
+// Dense-table rows, kApplyRows rows per block: block (x, y) takes span x (one
+// chunk per thread) of rows y, y + gridDim.y, ...  All the rows' mask bytes
+// are loaded first, then the logits of their mixed chunks, then the stores:
+// a block keeps kApplyRows mask loads in flight, while at any moment the
+// blocks still write a few compact windows of the logits.  Write-mostly as in
+// k_apply (non-temporal -inf stores, read-merge-write of mixed chunks).
+template <typename T, int R>
+__global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32_t *__restrict__ node_ids,
+                                                        int64_t rows, T *__restrict__ logits, int64_t stride) {
+    constexpr int E = 16 / (int)sizeof(T);
+    constexpr uint32_t FULL = (1u << E) - 1u;
+    constexpr T NEG = NegInf<T>::bits;
+    const int64_t V = t.V, nchunks = (V + E - 1) / E;
+    const int64_t c = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t e0 = c * E;
+    const uint8_t *table = reinterpret_cast<const uint8_t *>(t.table);
+    const int64_t row_bytes = t.Wp * 8;
+    uint32_t bits[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        const int32_t n = b < rows ? node_ids[b] : -1;
+        bits[r] = 0;  // a dead row: every token invalid
+        if (n >= 0 && (int64_t)n < t.N && c < nchunks) {
+            const uint8_t *mrow = table + (int64_t)n * row_bytes;
+            bits[r] = E == 8 ? (uint32_t)mrow[c] : ((uint32_t)mrow[c >> 1] >> ((c & 1) * 4)) & FULL;
+        }
+    }
+    if (c >= nchunks) return;
+    const bool whole = e0 + E <= V;
+    u32x4 xv[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        if (b < rows && whole && bits[r] != 0 && bits[r] != FULL)
+            xv[r] = *reinterpret_cast<const u32x4 *>(logits + b * stride + e0);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        const uint32_t bu = bits[r];
+        if (b >= rows || bu == FULL) continue;
+        T *row = logits + b * stride;
+        if (whole) {
+            u32x4 *p = reinterpret_cast<u32x4 *>(row + e0);
+            if (bu == 0) {
+                const uint32_t w = sizeof(T) == 2 ? 0xFF80FF80u : 0xFF800000u;
+                __builtin_nontemporal_store(u32x4{w, w, w, w}, p);
+            } else {
+                T vals[E];
+                __builtin_memcpy(vals, &xv[r], 16);
+#pragma unroll
+                for (int i = 0; i < E; ++i)
+                    if (!((bu >> i) & 1u)) vals[i] = NEG;
+                u32x4 o;
+                __builtin_memcpy(&o, vals, 16);
+                *p = o;
+            }
+        } else {
+            const int lim = (int)min<int64_t>(E, V - e0);
+            for (int i = 0; i < lim; ++i)
+                if (!((bu >> i) & 1u)) row[e0 + i] = NEG;
+        }
+    }
+}
+
 // ------------------------------------------------- fixed-format strings ---
 
 // Token bytes tb[0..len) at position p of a fixed format: non-empty, within
@@ -1257,6 +1326,23 @@ hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, 
                         ? 1
                         : 0;
     const int mode = t.table == nullptr ? kApplyLists : (t.row_of ? kApplyTail : kApplyTable);
+    if (mode == kApplyTable && vec) {
+        const int64_t gx1 = grid_for(nchunks, kBlock);
+        // grid.y (row groups) is limited to 65535 per launch
+        for (int64_t r0 = 0; r0 < B; r0 += (int64_t)65535 * kApplyRows) {
+            const int64_t rows = std::min<int64_t>(B - r0, (int64_t)65535 * kApplyRows);
+            const dim3 grid((unsigned)gx1, (unsigned)grid_for(rows, kApplyRows));
+            if (dtype == TAM_DTYPE_BF16)
+                hipLaunchKernelGGL((k_apply_dense<uint16_t, kApplyRows>), grid, dim3(kBlock), 0, s, t, node_ids + r0,
+                                   rows, static_cast<uint16_t *>(logits) + r0 * row_stride, row_stride);
+            else
+                hipLaunchKernelGGL((k_apply_dense<uint32_t, kApplyRows>), grid, dim3(kBlock), 0, s, t, node_ids + r0,
+                                   rows, static_cast<uint32_t *>(logits) + r0 * row_stride, row_stride);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
     // grid.y is limited to 65535 rows per launch
     for (int64_t r0 = 0; r0 < B; r0 += 65535) {
         const dim3 grid(gx, (unsigned)std::min<int64_t>(B - r0, 65535));
