@@ -223,13 +223,7 @@ void parallel_for(int64_t n, int threads, F f) {
         for (int64_t j = 0; j < n; ++j) f(j);
         return;
     }
-    std::atomic<int64_t> next{0};
-    std::vector<std::thread> pool;
-    for (int i = 0; i < threads; ++i)
-        pool.emplace_back([&] {
-            for (int64_t j = next.fetch_add(1); j < n; j = next.fetch_add(1)) f(j);
-        });
-    for (auto &th : pool) th.join();
+    host_parallel_for(n, threads, std::function<void(int64_t)>(f));
 }
 
 int host_threads(int64_t work_items) {

@@ -27,4 +27,8 @@ tam_status build_vocab(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t
                        std::string *err);
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v);
 
+// Runs f(j) for every j in [0, n) on up to `threads` host threads (the caller
+// and workers of a process-wide pool); rethrows the first exception of f.
+void host_parallel_for(int64_t n, int threads, const std::function<void(int64_t)> &f);
+
 }  // namespace tam

@@ -308,3 +308,53 @@ def test_lazy_rows_option_errors(P):
     L = P.lib()
     assert L.tam_rebuild(h._raw, 0, None) == -6  # host only: no device state
     h.close()
+
+
+def _trie_digest(h):
+    return tuple(np.asarray(a).tobytes() for a in (h.roots, h.parent, h.depth, h.edge_byte, h.is_final))
+
+
+def test_host_compiles_on_several_threads(P):
+    """Host compiles from several host threads at once: one runs its parallel
+    loops on the worker pool, the others on threads of their own; every trie
+    equals the one built alone."""
+    import threading
+    w = W.config(3)
+    ref = _trie_digest(host(P, w.strings, [b"x"]))
+    out, errors = {}, []
+
+    def run(k):
+        try:
+            for r in range(3):
+                out[(k, r)] = _trie_digest(host(P, w.strings, [b"x"]))
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(e)
+
+    ts = [threading.Thread(target=run, args=(k,)) for k in range(4)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join(timeout=120)
+    assert not errors and not any(t.is_alive() for t in ts)
+    assert len(out) == 12 and all(v == ref for v in out.values())
+
+
+def _child_compile(q):
+    import paper_2608_12574_amd as P2
+    w = W.config(3)
+    q.put(_trie_digest(P2.compile(w.strings, [b"x"], flags=P2.FLAG_HOST_ONLY)))
+
+
+def test_host_compile_in_forked_child(P):
+    """A child forked after the parent's worker pool exists builds the same
+    trie (it starts a pool of its own)."""
+    import multiprocessing as mp
+    w = W.config(3)  # large enough to be built in parts, on the pool
+    ref = _trie_digest(host(P, w.strings, [b"x"]))
+    ctx = mp.get_context("fork")
+    q = ctx.Queue()
+    p = ctx.Process(target=_child_compile, args=(q,))
+    p.start()
+    got = q.get(timeout=120)
+    p.join(timeout=60)
+    assert p.exitcode == 0 and got == ref
