@@ -39,6 +39,7 @@ struct PartPlan {
     int64_t nodes = 1;          // including the part's root (its set's root)
     int64_t blob = 0;           // pad byte, bytes, T per string
     int64_t root_children = 0;  // strings starting a new first byte
+    int64_t branching = 0;      // nodes other than the part root that two or more strings pass through
     tam_status st = TAM_OK;
     std::string err;
 };
@@ -102,6 +103,13 @@ void plan_part(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t
             return;
         }
     }
+    // string u creates the nodes at path indices lcp[u] .. len; the next string
+    // also passes through those below index lcp[u+1] (sorted order: no later
+    // string shares more of them)
+    for (size_t u = 0; u < r.lcp.size(); ++u) {
+        const int64_t next = u + 1 < r.lcp.size() ? r.lcp[u + 1] : 0;
+        r.branching += std::max<int64_t>(0, next - r.lcp[u]);
+    }
 }
 
 // Where a part's nodes, blob bytes and edges go in the handle's tables.
@@ -112,11 +120,8 @@ struct PartBase {
     int64_t edge;         // first of its edges below depth 1
     int64_t root_edge;    // first of its depth-1 nodes' slots among the set root's edges
     bool root_tail;       // its set has one string (the set root is then a tail)
-    int64_t branching;    // out (tail split): branching nodes of the part
+    int64_t first_row;    // (tail split) dense row of the part's first branching node
 };
-
-// Marks a branching node's row_of entry until the dense rows are numbered.
-constexpr int32_t kBranchRow = INT32_MAX;
 
 /*
  * Writes a planned part into the handle: per string, a pad byte (standing for
@@ -126,53 +131,42 @@ constexpr int32_t kBranchRow = INT32_MAX;
  * where the first later string leaves its path).  Then the part's child lists:
  * children in ascending id order, which is ascending byte order; depth-1 nodes
  * are listed on the set root.
+ *
+ * Tail split, decided when a node is created: string u creates the nodes at
+ * path indices i >= lcp[u], and the next string passes through those with
+ * i < lcp[u+1] (no later string shares more of them).  Those are branching
+ * nodes and take the next dense rows, in creation order, which is id order.
+ * The others are tails: only string u passes through them, so len - i nodes
+ * lie below one, and the highest tail on the path is at index
+ * max(lcp[u], lcp[u+1]) (the root itself in a set of one string).
  */
 void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, PartBase &pb,
                bool subtrees, bool tails, tam_handle *h) {
     const int64_t nloc = r.nodes;
-    std::vector<int32_t> path;   // global ids of the current string's nodes by depth - 1
-    std::vector<int64_t> first;  // (tail split) index of the string that created each of them
-    int64_t N = 1, B = 0, prev_len = -1, branching = 0;
-    // The previous string's nodes at path indices l..prev_len leave the path
-    // before string u: their subtrees end here, and u - first[i] strings pass
-    // through each (a node is final for exactly one string).  Tail split: two
-    // or more make a branching node (a dense row); a tail's subtree is one
-    // path, the rest of that string (prev_len - i nodes below it), and its
-    // highest tail ancestor-or-self is the first tail of the range (the node
-    // above the range is shared with string u, hence branching, unless it is
-    // the root of a one-string set, itself a tail at depth 0).
-    auto close = [&](int64_t l, int64_t u) {
+    const int64_t nstr = (int64_t)r.str.size();
+    std::vector<int32_t> path;  // global ids of the current string's nodes by depth - 1
+    int64_t N = 1, B = 0, prev_len = -1;
+    int32_t row = (int32_t)pb.first_row;
+    // the previous string's nodes at path indices l..prev_len leave the path
+    // before the next string: their subtrees end here
+    auto close = [&](int64_t l) {
         if (subtrees)
             for (int64_t i = l; i <= prev_len; ++i) h->sub_end[(size_t)path[(size_t)i]] = (int32_t)(pb.node + N);
-        if (!tails) return;
-        int64_t top = -1;
-        for (int64_t i = l; i <= prev_len; ++i) {
-            const size_t g = (size_t)path[(size_t)i];
-            if (u - first[(size_t)i] >= 2) {
-                h->row_of[g] = kBranchRow;
-                h->tail_span[g] = 0;
-                ++branching;
-                continue;
-            }
-            if (top < 0) top = pb.root_tail ? 0 : i + 1;
-            h->row_of[g] = (int32_t)(-1 - (prev_len - i));
-            h->tail_span[g] = (int32_t)(i + 1 - top);
-        }
     };
-    for (size_t u = 0; u < r.str.size(); ++u) {
-        const int64_t k = r.str[u];
+    for (int64_t u = 0; u < nstr; ++u) {
+        const int64_t k = r.str[(size_t)u];
         const uint8_t *s = sb + so[k];
         const int64_t len = so[k + 1] - so[k];
-        const int64_t l = r.lcp[u];
-        close(l, (int64_t)u);
+        const int64_t l = r.lcp[(size_t)u];
+        const int64_t next = u + 1 < nstr ? r.lcp[(size_t)u + 1] : 0;
+        const int64_t top = pb.root_tail ? -1 : std::max(l, next);  // index above the highest tail
+        close(l);
         prev_len = len;
-        if ((int64_t)path.size() < len + 1) {
-            path.resize((size_t)(len + 1));
-            if (tails) first.resize((size_t)(len + 1));
-        }
+        if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
         const int64_t at = pb.blob + B;
         h->blob[(size_t)at] = 0;
         h->node_at[(size_t)at] = pb.root;
+        if (tails) h->row_at[(size_t)at] = h->row_of[(size_t)pb.root];
         for (int64_t i = 0; i <= len; ++i) {
             const uint8_t c = i < len ? s[i] : term;
             const size_t pos = (size_t)(at + 1 + i);
@@ -185,14 +179,18 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
                 h->is_final[g] = i == len ? 1 : 0;
                 h->node_pos[g] = (int32_t)pos;
                 path[(size_t)i] = (int32_t)g;
-                if (tails) first[(size_t)i] = (int64_t)u;
+                if (tails) {
+                    const bool branching = i < next;
+                    h->row_of[g] = branching ? row++ : (int32_t)(-1 - (len - i));
+                    h->tail_span[g] = branching ? 0 : (int32_t)(i - top);
+                }
             }
             h->node_at[pos] = path[(size_t)i];
+            if (tails) h->row_at[pos] = h->row_of[(size_t)path[(size_t)i]];
         }
         B += len + 2;
     }
-    close(0, (int64_t)r.str.size());
-    pb.branching = branching;
+    close(0);
     // child lists: count, offsets, then fill in id order
     std::vector<int32_t> cnt((size_t)nloc, 0);
     for (int64_t i = 1; i < nloc; ++i) {
@@ -236,52 +234,18 @@ int host_threads(int64_t work_items) {
  * node, i.e. below it the trie is a single path; its valid tokens are then the
  * tokens equal to a prefix of that one remaining suffix.  Every other node
  * (two or more finals below) is a branching node and gets a dense table row,
- * numbered in id order; a tail a gets row_of[a] = -1 - rem(a), rem(a) being the
- * number of nodes below it.  In preorder a tail's path has consecutive ids
- * a+1 .. a+rem(a), so the token of length d starting below a is the suffix hit
- * of node a+d at distance d: tails need no stored masks.  Tails are closed
- * under descent, so above any node m the tails form the first tail_span[m]
- * ancestors: a hit at distance d above m lands on a tail iff d <= tail_span[m]
- * = depth(m) - depth(highest tail ancestor-or-self of m), and 0 when m itself
- * branches.  emit_part classifies every node when it leaves the insertion
- * path; here the branching nodes are numbered in id order (a set's root, then
- * its parts' nodes), and row_at = row_of[node_at] is laid along the blob.
+ * numbered in id order (a set's root, then its parts' nodes); a tail a gets
+ * row_of[a] = -1 - rem(a), rem(a) being the number of nodes below it.  In
+ * preorder a tail's path has consecutive ids a+1 .. a+rem(a), so the token of
+ * length d starting below a is the suffix hit of node a+d at distance d: tails
+ * need no stored masks.  Tails are closed under descent, so above any node m
+ * the tails form the first tail_span[m] ancestors: a hit at distance d above m
+ * lands on a tail iff d <= tail_span[m] = depth(m) - depth(highest tail
+ * ancestor-or-self of m), and 0 when m itself branches.  row_at =
+ * row_of[node_at] is laid along the blob.  emit_part classifies the nodes as it
+ * creates them; the set roots and the first row of every part are fixed
+ * before, from the planned branching counts.
  */
-void number_dense_rows(int64_t S, const std::vector<int64_t> &root, const std::vector<int64_t> &set_first,
-                       const std::vector<PartPlan> &parts, const std::vector<PartBase> &base, tam_handle *h) {
-    const int64_t NP = (int64_t)parts.size();
-    std::vector<int64_t> first_row((size_t)NP, 0);
-    int64_t rows = 0;
-    for (int64_t j = 0; j < S; ++j) {
-        const size_t rt = (size_t)root[(size_t)j];
-        const int64_t p0 = set_first[(size_t)j], p1 = set_first[(size_t)j + 1];
-        h->tail_span[rt] = 0;
-        if (base[(size_t)p0].root_tail)  // one string: the whole path lies below the root
-            h->row_of[rt] = (int32_t)(-1 - (parts[(size_t)p0].nodes - 1));
-        else
-            h->row_of[rt] = (int32_t)rows++;
-        for (int64_t p = p0; p < p1; ++p) {
-            first_row[(size_t)p] = rows;
-            rows += base[(size_t)p].branching;
-        }
-    }
-    h->dense_rows = rows;
-    const int64_t BB = h->blob_bytes;
-    h->row_at.resize((size_t)BB);
-    parallel_for(NP, host_threads(NP), [&](int64_t p) {
-        const PartBase &pb = base[(size_t)p];
-        const PartPlan &r = parts[(size_t)p];
-        int32_t row = (int32_t)first_row[(size_t)p];
-        for (int64_t i = 1; i < r.nodes; ++i) {
-            const size_t g = (size_t)(pb.node + i);
-            if (h->row_of[g] == kBranchRow) h->row_of[g] = row++;
-        }
-        for (int64_t b = pb.blob; b < pb.blob + r.blob; ++b)
-            h->row_at[(size_t)b] = h->row_of[(size_t)h->node_at[(size_t)b]];
-    });
-    for (int64_t b = 0; b < kBlobPad; ++b)  // the outer pads stand for the first set's root
-        h->row_at[(size_t)b] = h->row_at[(size_t)(BB - 1 - b)] = h->row_of[0];
-}
 
 }  // namespace
 
@@ -365,7 +329,8 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     // blob offsets, edges (a set's root edges first, then its parts' others)
     std::vector<PartBase> base((size_t)NP);
     std::vector<int64_t> root((size_t)S), root_edges((size_t)S), set_blob((size_t)S);
-    int64_t N = 0, BB = kBlobPad, E = 0;
+    std::vector<int32_t> root_row((size_t)S);  // (tail split) row_of of each set root
+    int64_t N = 0, BB = kBlobPad, E = 0, rows = 0;
     h->K_unique = 0;
     for (int64_t j = 0; j < S; ++j) {
         root[(size_t)j] = N++;
@@ -383,11 +348,16 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         int64_t set_strings = 0;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p)
             set_strings += (int64_t)parts[(size_t)p].str.size();
+        // a set of one string: the whole path lies below its root, a tail;
+        // any other set root branches and takes the set's first dense row
+        const int64_t p0 = set_first[(size_t)j];
+        root_row[(size_t)j] = set_strings == 1 ? (int32_t)(-1 - (parts[(size_t)p0].nodes - 1)) : (int32_t)rows++;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
             const PartPlan &r = parts[(size_t)p];
             PartBase &pb = base[(size_t)p];
             pb.root_tail = set_strings == 1;
-            pb.branching = 0;
+            pb.first_row = rows;
+            rows += r.branching;
             pb.root = (int32_t)root[(size_t)j];
             pb.node = N - 1;
             pb.blob = BB;
@@ -431,6 +401,8 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->sub_end.resize(subtrees ? (size_t)N : 0);
     h->row_of.resize(tails ? (size_t)N : 0);
     h->tail_span.resize(tails ? (size_t)N : 0);
+    h->row_at.resize(tails ? (size_t)BB : 0);
+    h->dense_rows = tails ? rows : 0;
     for (int64_t p = 0; p < kBlobPad; ++p) {
         h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
         h->node_at[(size_t)p] = h->node_at[(size_t)(BB - 1 - p)] = 0;
@@ -445,7 +417,14 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         h->node_pos[(size_t)rt] = -1;
         h->child_off[(size_t)rt] = (int32_t)root_edges[(size_t)j];
         if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
+        if (tails) {
+            h->row_of[(size_t)rt] = root_row[(size_t)j];
+            h->tail_span[(size_t)rt] = 0;
+        }
     }
+    if (tails)
+        for (int64_t p = 0; p < kBlobPad; ++p)  // the outer pads stand for the first set's root
+            h->row_at[(size_t)p] = h->row_at[(size_t)(BB - 1 - p)] = h->row_of[0];
     h->child_off[(size_t)N] = (int32_t)E;
     // Emission in groups of whole sets (a forest of many sets: four groups, so
     // that a caller can upload a group while the next is written).
@@ -469,7 +448,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             if (st != TAM_OK) return st;
         }
     }
-    if (tails) number_dense_rows(S, root, set_first, parts, base, h);
     return TAM_OK;
 }
 

@@ -16,9 +16,9 @@ struct TrieRange {
 
 // planned (optional) runs once the trie's sizes (N, S, blob bytes, edges) are
 // set in h and before any node is written.  emitted (optional) runs after each
-// group of whole sets has been written (the trie's tables in those ranges are
-// then final; tail compression's tables come after the last group).  A non-OK
-// status of either aborts the build.
+// group of whole sets has been written (the trie's tables in those ranges,
+// tail compression's included, are then final).  A non-OK status of either
+// aborts the build.
 tam_status build_trie(const uint8_t *str_bytes, const int64_t *str_off, int64_t K,
                       const int64_t *set_off, int64_t S, int terminator, tam_handle *h,
                       std::string *err, const std::function<tam_status(tam_handle *)> &planned = {},

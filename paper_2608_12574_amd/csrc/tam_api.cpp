@@ -387,9 +387,12 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const bool early_zero =
         !host_only && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_TAIL_LISTS | TAM_FLAG_LAZY_ROWS));
     uint64_t *early_table = nullptr;
-    uint8_t *trie_base = nullptr;  // blob, node_at, node_pos, depth, child_off, child_byte, child_node, sub_end
+    // blob, node_at, node_pos, depth, child_off, child_byte, child_node, sub_end,
+    // and tail compression's tail_span, row_of, row_at
+    uint8_t *trie_base = nullptr;
     size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
-           o_child_node = 0, o_sub_end = 0;
+           o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0;
+    const bool split = (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
     bool enqueued = false;  // device work that reads host tables or writes device memory
     double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
     auto planned = [&](tam_handle *hh) -> tam_status {
@@ -414,6 +417,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_child_byte = ta.take<uint8_t>(hh->edges);
         o_child_node = ta.take<int32_t>(hh->edges);
         o_sub_end = ta.take<int32_t>((hh->flags & TAM_FLAG_LAZY_ROWS) ? hh->N : 0);
+        o_tail_span = ta.take<int32_t>(split ? hh->N : 0);
+        o_row_of = ta.take<int32_t>(split ? hh->N : 0);
+        o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
         trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
         if (!trie_base) {
             err = "device allocation failed (" + std::to_string(ta.used) + " bytes requested)";
@@ -463,6 +469,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         up(o_child_byte, hh->child_byte.data(), r.e_lo, r.e_hi, 1);
         up(o_child_node, hh->child_node.data(), r.e_lo, r.e_hi, 4);
         if (hh->flags & TAM_FLAG_LAZY_ROWS) up(o_sub_end, hh->sub_end.data(), r.n_lo, r.n_hi, 4);
+        if (split) {
+            up(o_tail_span, hh->tail_span.data(), r.n_lo, r.n_hi, 4);
+            up(o_row_of, hh->row_of.data(), r.n_lo, r.n_hi, 4);
+            up(o_row_at, hh->row_at.data(), r.b_lo, r.b_hi, 4);
+        }
         hook_ms += ms_since(t1);
         if (e != hipSuccess) {
             err = std::string("upload: ") + hipGetErrorString(e);
@@ -536,9 +547,6 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_row_ptr = a.take<int32_t>(NP + 1);
     const size_t o_cursor = a.take<int32_t>(NP);
     const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
-    const size_t o_tail_span = a.take<int32_t>(tails ? h->N : 0);
-    const size_t o_row_of = a.take<int32_t>(tails ? h->N : 0);
-    const size_t o_row_at = a.take<int32_t>(tails ? h->blob_bytes : 0);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(NP));
     h->npairs = lazy ? 0 : tam::mark_blocks(h->N);
     const size_t o_pairs = a.take<int32_t>(h->npairs);
@@ -606,9 +614,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         z.miss_count = reinterpret_cast<int32_t *>(base + o_miss_count);
         z.C = C;
     }
-    t.tail_span = tails ? reinterpret_cast<const int32_t *>(base + o_tail_span) : nullptr;
-    t.row_of = tails ? reinterpret_cast<const int32_t *>(base + o_row_of) : nullptr;
-    t.row_at = tails ? reinterpret_cast<const int32_t *>(base + o_row_at) : t.node_at;
+    t.tail_span = tails ? reinterpret_cast<const int32_t *>(trie_base + o_tail_span) : nullptr;
+    t.row_of = tails ? reinterpret_cast<const int32_t *>(trie_base + o_row_of) : nullptr;
+    t.row_at = tails ? reinterpret_cast<const int32_t *>(trie_base + o_row_at) : t.node_at;
     t.R = R;
     t.tail_long = tail_long ? 1 : 0;
     t.N = h->N;
@@ -623,14 +631,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.classes = nullptr;
     t.fmt_L = -1;
 
-    auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
-        if (bytes == 0) return hipSuccess;
-        return hipMemcpyAsync(base + off, src, bytes, hipMemcpyHostToDevice, s);
-    };
+    // the trie's tables were uploaded group by group while the host wrote them
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
-    if (e == hipSuccess && tails) e = up(o_tail_span, h->tail_span.data(), h->tail_span.size() * 4);
-    if (e == hipSuccess && tails) e = up(o_row_of, h->row_of.data(), h->row_of.size() * 4);
-    if (e == hipSuccess && tails) e = up(o_row_at, h->row_at.data(), h->row_at.size() * 4);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);
