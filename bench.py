@@ -194,9 +194,11 @@ class Bench:
             warm.append(ms)
         return h, cold, warm, phases_cold, h.timing()
 
-    def one_set_compile_ms(self, flags, runs=5):
+    def one_set_compile_ms(self, flags, runs=20):
         """A forest's first set compiled on its own, warm (the latency of one new
-        query's set), minimum over runs; None for a single-set workload."""
+        query's set), minimum over runs; None for a single-set workload.  The
+        first few compiles of a process enqueue their small uploads several
+        times slower than later ones, hence the runs."""
         torch, P, w = self.torch, self.P, self.w
         if w.set_offsets is None:
             return None
