@@ -14,11 +14,13 @@
 // there).  A pool is never destroyed: its workers sleep until the process ends.
 #include <pthread.h>
 
+#include <algorithm>
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
 #include <exception>
 #include <mutex>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -122,11 +124,14 @@ void spawn_loop(int64_t n, int threads, const std::function<void(int64_t)> &f) {
         }
     };
     std::vector<std::thread> ts;
-    for (int i = 1; i < threads; ++i)
-        ts.emplace_back([&] {
-            t_in_loop = true;
-            body();
-        });
+    try {
+        for (int i = 1; i < threads; ++i)
+            ts.emplace_back([&] {
+                t_in_loop = true;
+                body();
+            });
+    } catch (const std::system_error &) {  // no more threads: the ones made share the loop
+    }
     t_in_loop = true;
     body();
     t_in_loop = false;
@@ -147,10 +152,14 @@ void host_parallel_for(int64_t n, int threads, const std::function<void(int64_t)
         spawn_loop(n, threads, f);
         return;
     }
-    while (P.workers < threads - 1) {
-        std::thread([&P] { P.worker(); }).detach();
-        ++P.workers;
+    try {
+        while (P.workers < threads - 1) {
+            std::thread([&P] { P.worker(); }).detach();
+            ++P.workers;
+        }
+    } catch (const std::system_error &) {  // no more threads: the workers made share the loop
     }
+    const int helpers = std::min(threads - 1, P.workers);
     {
         std::lock_guard<std::mutex> g(P.m);
         P.f = &f;
@@ -158,14 +167,14 @@ void host_parallel_for(int64_t n, int threads, const std::function<void(int64_t)
         P.next.store(0);
         P.finished = 0;
         P.error = nullptr;
-        P.tickets.store(threads - 1);
+        P.tickets.store(helpers);
         P.generation.fetch_add(1);
         P.wake.notify_all();
     }
     t_in_loop = true;
     P.work();
     t_in_loop = false;
-    const int joined = threads - 1 - P.tickets.exchange(0);
+    const int joined = helpers - P.tickets.exchange(0);
     std::exception_ptr err;
     {
         std::unique_lock<std::mutex> lk(P.m);
