@@ -71,7 +71,7 @@ typedef enum {
     TAM_OK = 0,
     TAM_E_INVAL = -1,      /* bad argument (null pointer, negative size, bad dtype, ...) */
     TAM_E_TERMINATOR = -2, /* a set string contains the terminator byte */
-    TAM_E_NOMEM = -3,      /* host allocation or the device allocator failed */
+    TAM_E_NOMEM = -3,      /* host allocation, a host thread or the device allocator failed */
     TAM_E_DEVICE = -4,     /* a HIP call failed */
     TAM_E_TOOLARGE = -5,   /* sizes beyond the 32-bit index limits of the tables */
     TAM_E_STATE = -6       /* operation not available for this handle (see flags) */

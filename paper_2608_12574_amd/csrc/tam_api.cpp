@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cstring>
+#include <exception>
 #include <map>
 #include <mutex>
 #include <new>
@@ -174,6 +175,9 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     } catch (const std::bad_alloc &) {
         st = TAM_E_NOMEM;
         err = "out of host memory";
+    } catch (const std::exception &x) {  // e.g. no host thread could be made
+        st = TAM_E_NOMEM;
+        err = std::string("host build failed: ") + x.what();
     }
     v->host_ms = ms_since(t0);
     if (st != TAM_OK) {
@@ -504,6 +508,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     } catch (const std::bad_alloc &) {
         st = TAM_E_NOMEM;
         err = "out of host memory";
+    } catch (const std::exception &x) {  // e.g. no host thread could be made
+        st = TAM_E_NOMEM;
+        err = std::string("host build failed: ") + x.what();
     }
     if (st != TAM_OK) {
         if (enqueued) (void)hipStreamSynchronize(s);  // copies may still read the host tables
