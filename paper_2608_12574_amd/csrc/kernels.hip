@@ -620,6 +620,13 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
     T *row = logits + b * stride;
     // the row's source (uniform over the block): its dense table row, its list,
     // or (a tail with tail compression) the probe's hits along its path
+    const int lane = threadIdx.x & (kWave - 1);
+    // With tail compression most rows are tails: the hits along the path below
+    // n are loaded together with row_of[n] (lane d-1: the hit of node n+d at
+    // distance d), and kept only if n turns out to be a tail.
+    int32_t x_tail = -1;
+    if (kMode == kApplyTail && live && lane < kWin && lane < t.max_len && (int64_t)n + lane + 1 < t.N)
+        x_tail = t.hits[(int64_t)lane * t.N + n + lane + 1];
     int64_t trow = live ? n : -1;
     if (kMode == kApplyTail && live) trow = t.row_of[n];
     const bool tail_row = kMode == kApplyTail && live && trow < 0;
@@ -629,12 +636,11 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
 #pragma unroll
     for (int u = 0; u < kApplyUnits; ++u) bits[u] = 0;
     const uint32_t lo = (uint32_t)(c0 * E);
-    const int lane = threadIdx.x & (kWave - 1);
     if (tail_row) {
-        // lane d-1 takes the token of length d starting below the tail: the hit
-        // of node n+d at distance d (the path below a tail has consecutive ids)
+        // lane d-1 takes the token of length d starting below the tail (the
+        // path below a tail has consecutive ids, so all of them were loaded)
         const int Lt = min(min(-1 - (int)trow, kWin), (int)t.max_len);
-        const int32_t x = lane < Lt ? t.hits[(int64_t)lane * t.N + n + lane + 1] : -1;
+        const int32_t x = lane < Lt ? x_tail : -1;
         take_ids<E, kSpan>(x >= 0 ? (uint32_t)x - lo : 0xffffffffu, bits);
         // strings with several token ids (rare): walk their id chains
         uint64_t multi = __ballot(x <= -2);
