@@ -521,6 +521,40 @@ def test_forest_with_large_set(P, flags):
     h.close()
 
 
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
+def test_forest_written_in_groups(P, flags):
+    """A forest of 14 sets (8 or more: the host writes it in four groups of
+    sets and each group is uploaded while the next is written): the mixed
+    forest's sets (a large set cut by first byte, a one-string set) after ten
+    of c5's per-query sets, over the c1 vocabulary.  Every root's row, sampled
+    rows, the whole rows of the last set's nodes, and a decode in every set."""
+    w5 = W.config(5)
+    mixed, vocab, moffs = W.mixed_forest()
+    sets = [w5.strings[int(w5.set_offsets[j]):int(w5.set_offsets[j + 1])] for j in range(10)]
+    sets += [mixed[int(moffs[j]):int(moffs[j + 1])] for j in range(len(moffs) - 1)]
+    strings = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    o = Oracle(strings, vocab, set_offsets=offs)
+    h = P.compile(strings, vocab, sets=offs, flags=flags)
+    assert h.num_nodes == o.N and np.array_equal(h.roots, o.roots)
+    last = np.arange(o.roots[-1], o.N, dtype=np.int32)
+    nodes = np.unique(np.concatenate([sample_nodes(o, 2000, 91), o.roots, last])).astype(np.int32)
+    assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+    rng = np.random.default_rng(92)
+    start = np.repeat(o.roots, 8).astype(np.int32)
+    cur = start.copy()
+    for step in range(8):
+        rows = o.mask_rows(cur)
+        assert np.array_equal(gpu_rows(h, cur), rows)
+        toks = W.choose_valid_tokens(rng, rows, o.V)
+        exp = o.advance(cur, toks)
+        assert np.array_equal(gpu_advance(h, cur, toks), exp)
+        cur = np.where((exp < 0) | (o.is_final[np.maximum(exp, 0)] == 1), start, exp).astype(np.int32)
+    check_apply(P, h, o, cur, "bf16", seed=93)
+    check_apply(P, h, o, nodes[:500], "fp32", seed=94)
+    h.close()
+
+
 # ------------------------------------------------------ rows built on demand --
 
 @pytest.mark.parametrize("cache", [1, 7, 64])
