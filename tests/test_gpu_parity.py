@@ -555,6 +555,46 @@ def test_forest_written_in_groups(P, flags):
     h.close()
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_random_forests(P, seed):
+    """Random forests (1-19 sets of 1-1,500 strings over 2-9 byte values,
+    including 0x00, 0x80 and 0xff; sets that prefix, repeat and contain the
+    empty string) and random vocabularies (empty, long and duplicate tokens, the
+    terminator), in every representation: every row (or 20,000 sampled ones),
+    5,000 random advances with out-of-range ids, and apply on 700 rows."""
+    rng = np.random.default_rng(1000 + seed)
+    alpha = np.frombuffer(b"abcde_\x00\xff\x80!", dtype=np.uint8)[: rng.integers(2, 10)]
+    sets = []
+    for _ in range(int(rng.integers(1, 20))):
+        k = int(rng.integers(1, 300 if rng.random() < 0.8 else 1500))
+        maxlen = int(rng.integers(1, 24))
+        sets.append([bytes(alpha[rng.integers(0, len(alpha), size=rng.integers(0, maxlen + 1))]) for _ in range(k)])
+    strings = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    vocab = [bytes(alpha[rng.integers(0, len(alpha), size=rng.integers(0, 20 if rng.random() < 0.9 else 40))])
+             for _ in range(int(rng.integers(1, 2000)))]
+    if rng.random() < 0.5:
+        vocab += [b'"', bytes(alpha[:1]) + b'"']
+    o = Oracle(strings, vocab, set_offsets=offs)
+    if o.N <= 30000:
+        nodes = np.arange(-1, o.N + 1, dtype=np.int32)
+    else:
+        nodes = np.unique(np.concatenate([o.roots, rng.integers(0, o.N, 20000)])).astype(np.int32)
+    inside = (nodes >= 0) & (nodes < o.N)
+    exp_rows = np.zeros((len(nodes), o.W), dtype=np.uint64)
+    exp_rows[inside] = o.mask_rows(nodes[inside])
+    nn = rng.integers(-1, o.N + 1, size=5000).astype(np.int32)
+    tt = rng.integers(-1, o.V + 1, size=5000).astype(np.int32)
+    exp_adv = o.advance(nn, tt)
+    for flags in FLAGS:
+        h = P.compile(strings, vocab, sets=offs, flags=flags, cache_rows=int(rng.integers(1, 200)))
+        got = np.concatenate([gpu_rows(h, nodes[i:i + 1000]) for i in range(0, len(nodes), 1000)])
+        assert np.array_equal(got, exp_rows), flags
+        assert np.array_equal(gpu_advance(h, nn, tt), exp_adv), flags
+        check_apply(P, h, o, nodes[:700], "bf16", seed=seed)
+        h.close()
+
+
 # ------------------------------------------------------ rows built on demand --
 
 @pytest.mark.parametrize("cache", [1, 7, 64])
