@@ -294,14 +294,17 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
 //     atomic, and each block writes the number of valid (node, token) pairs its
 //     hits make, tails included, into pairs[blockIdx.x].
 //   kCount (lists): the listed hits are counted per node.
+// The grid covers the nodes [m0, m1): every node of the handle, or (lists of a
+// forest) one group of whole sets, whose nodes' ancestors are in the group too.
 template <bool kCount>
-__global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int do_mark, int32_t *__restrict__ pairs) {
+__global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64_t m1, int do_mark,
+                                                  int32_t *__restrict__ pairs) {
     constexpr int kPer = kWin / kProbeLanes;
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    const int64_t m = i / kProbeLanes;
+    const int64_t m = m0 + i / kProbeLanes;
     const int d0 = (int)(i % kProbeLanes) * kPer;
     int32_t found = 0;
-    const int64_t pos = m < t.N ? t.node_pos[m] : -1;  // a root ends no token
+    const int64_t pos = m < m1 ? t.node_pos[m] : -1;  // a root ends no token
     if (pos >= 0) {
         const int L = min(t.depth[m], t.max_len);
         const int Lw = min(L, kWin);
@@ -1263,9 +1266,17 @@ hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pair
     const int do_mark = mark && t.table ? 1 : 0;
     const dim3 grid((unsigned)mark_blocks(t.N));
     if (count)
-        hipLaunchKernelGGL(k_probe<true>, grid, dim3(kBlock), 0, s, t, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<true>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs);
     else
-        hipLaunchKernelGGL(k_probe<false>, grid, dim3(kBlock), 0, s, t, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<false>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs);
+    return hipGetLastError();
+}
+
+hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s) {
+    if (m1 <= m0) return hipSuccess;
+    if (m0 < 0 || m1 > t.N || t.table) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_probe<true>, dim3((unsigned)mark_blocks(m1 - m0)), dim3(kBlock), 0, s, t, m0, m1, 0,
+                       (int32_t *)nullptr);
     return hipGetLastError();
 }
 

@@ -295,7 +295,8 @@ unsigned default_phases(const tam_handle *h) {
 // default phases.
 // zero_enqueued: the table's zero fill was already enqueued on `s`, with its
 // events (compile starts it while the host writes the trie).
-tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool zero_enqueued = false) {
+tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool zero_enqueued = false,
+                            bool lists_counted = false) {
     const tam::DevTables &t = h->dt;
     // Under stream capture (a HIP graph) only the kernels are recorded: no
     // events, which belong to eager calls.
@@ -319,18 +320,24 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
     const bool lists = (phases & TAM_PHASE_LISTS) != 0;
     const bool zero = (phases & TAM_PHASE_ZERO) && t.table && !zero_enqueued;
     const bool mark = (phases & TAM_PHASE_MARK) && t.table;
-    if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[0], s));
-    if (zero) TAM_HIP(tam::launch_zero(t.table, t.R * t.Wp, s));
-    if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[1], s));
-    if (timing && zero_enqueued) TAM_HIP(hipEventRecord(h->ev[4], s));  // the probe's own start
-    if (timing) h->mark_from_ev4 = zero_enqueued;
-    if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
-    if (t.fmt_L >= 0) {
-        if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
-    } else if (lists || mark) {
-        TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+    // lists_counted: the list counts were made group by group while the host
+    // wrote the trie (events 0, 1, 4 and 2 recorded then)
+    if (!lists_counted) {
+        if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[0], s));
+        if (zero) TAM_HIP(tam::launch_zero(t.table, t.R * t.Wp, s));
+        if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[1], s));
+        if (timing && zero_enqueued) TAM_HIP(hipEventRecord(h->ev[4], s));  // the probe's own start
+        if (timing) h->mark_from_ev4 = zero_enqueued;
+        if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
+        if (t.fmt_L >= 0) {
+            if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
+        } else if (lists || mark) {
+            TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+        }
+        if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
+    } else if (timing) {
+        h->mark_from_ev4 = true;
     }
-    if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
     if (lists) {
         TAM_HIP(tam::launch_scan(t, s));
         TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
@@ -349,6 +356,45 @@ tam_status check_device_handle(const tam_handle *h) {
     if (!h) return fail(TAM_E_INVAL, "null handle");
     if (h->flags & TAM_FLAG_HOST_ONLY) return fail(TAM_E_STATE, "handle was compiled with TAM_FLAG_HOST_ONLY");
     return TAM_OK;
+}
+
+// The trie's tables (at their offsets in the trie's allocation `tb`) and the
+// vocabulary's tables in a DevTables, with the sizes they imply; no table,
+// tails or lists yet.
+void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v, uint8_t *tb, size_t o_blob,
+                     size_t o_node_at, size_t o_node_pos, size_t o_depth, size_t o_child_off, size_t o_child_byte,
+                     size_t o_child_node) {
+    t.blob = tb + o_blob;
+    t.node_at = reinterpret_cast<const int32_t *>(tb + o_node_at);
+    t.node_pos = reinterpret_cast<const int32_t *>(tb + o_node_pos);
+    t.depth = reinterpret_cast<const int32_t *>(tb + o_depth);
+    t.child_off = reinterpret_cast<const int32_t *>(tb + o_child_off);
+    t.child_byte = tb + o_child_byte;
+    t.child_node = reinterpret_cast<const int32_t *>(tb + o_child_node);
+    t.tok_off = v->d_tok_off;
+    t.tok_blob = v->d_tok_blob;
+    t.fps = v->d_fps;
+    t.pay = v->d_pay;
+    t.dup_next = v->d_dup_next;
+    t.len_present = v->d_len_present;
+    t.table = nullptr;
+    t.sub_end = nullptr;
+    t.tail_span = nullptr;
+    t.row_of = nullptr;
+    t.row_at = t.node_at;
+    t.R = 0;
+    t.tail_long = 0;
+    t.N = h->N;
+    t.V = v->V;
+    t.W = v->W;
+    t.Wp = (v->W + 7) & ~int64_t(7);
+    t.blob_bytes = h->blob_bytes;
+    t.slot_mask = (uint64_t)v->fps.size() - 1;
+    t.len_mask = v->len_mask;
+    t.max_len = (int32_t)v->max_tok_len;
+    t.terminator = h->terminator;
+    t.classes = nullptr;
+    t.fmt_L = -1;
 }
 
 // Compile against a built vocabulary (the handle takes one reference to it).
@@ -397,6 +443,12 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
            o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0;
     const bool split = (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
+    // Lists (no table): the probe pass that counts each node's list runs group
+    // by group, right after each group's upload (a node's ancestors are in its
+    // own set), so only the last group's counts follow the host build.
+    const bool early_count = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & TAM_FLAG_LAZY_ROWS);
+    size_t o_hits = 0, o_count = 0;
+    tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
     double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
     auto planned = [&](tam_handle *hh) -> tam_status {
@@ -424,12 +476,31 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_tail_span = ta.take<int32_t>(split ? hh->N : 0);
         o_row_of = ta.take<int32_t>(split ? hh->N : 0);
         o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
+        o_hits = ta.take<int32_t>(early_count ? tam::kWin * hh->N : 0);
+        o_count = ta.take<int32_t>(early_count ? hh->N : 0);
         trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
         if (!trie_base) {
             err = "device allocation failed (" + std::to_string(ta.used) + " bytes requested)";
             return TAM_E_NOMEM;
         }
         hh->device_bytes = (int64_t)ta.used;
+        if (early_count) {
+            set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off,
+                            o_child_byte, o_child_node);
+            te.hits = reinterpret_cast<int32_t *>(trie_base + o_hits);
+            te.count = reinterpret_cast<int32_t *>(trie_base + o_count);
+            hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
+            const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
+            if (e == hipSuccess && timing) e = create_events(hh);
+            if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[0], s);
+            if (e == hipSuccess && timing) e = hipEventRecord(hh->ev[1], s);  // no zero fill
+            if (e == hipSuccess) e = tam::launch_fill_i32(te.count, hh->N, 0, s);
+            enqueued = true;
+            if (e != hipSuccess) {
+                err = std::string("list counts: ") + hipGetErrorString(e);
+                return TAM_E_DEVICE;
+            }
+        }
         if (early_zero) {
             const int64_t Wp = (vocab->W + 7) & ~int64_t(7);
             const size_t bytes = (size_t)hh->N * (size_t)Wp * sizeof(uint64_t);
@@ -477,6 +548,12 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
             up(o_tail_span, hh->tail_span.data(), r.n_lo, r.n_hi, 4);
             up(o_row_of, hh->row_of.data(), r.n_lo, r.n_hi, 4);
             up(o_row_at, hh->row_at.data(), r.b_lo, r.b_hi, 4);
+        }
+        if (early_count && e == hipSuccess) {
+            const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
+            if (timing && r.n_lo == 0) e = hipEventRecord(hh->ev[4], s);  // the counts' start
+            if (e == hipSuccess) e = tam::launch_count_range(te, r.n_lo, r.n_hi, s);
+            if (e == hipSuccess && timing && r.n_hi == hh->N) e = hipEventRecord(hh->ev[2], s);
         }
         hook_ms += ms_since(t1);
         if (e != hipSuccess) {
@@ -547,10 +624,11 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const int64_t R = !want_table ? 0 : tails ? std::max<int64_t>(h->dense_rows, 1) : h->N;
 
     Arena a;
-    // the probe pass's tables (none when rows are built on demand)
+    // the probe pass's tables (none when rows are built on demand; the hits and
+    // counts of early list counts are in the trie's allocation)
     const int64_t NP = lazy ? 0 : h->N;
-    const size_t o_hits = a.take<int32_t>(tam::kWin * NP);
-    const size_t o_count = a.take<int32_t>(NP);
+    const size_t o_hits_b = a.take<int32_t>(early_count ? 0 : tam::kWin * NP);
+    const size_t o_count_b = a.take<int32_t>(early_count ? 0 : NP);
     const size_t o_row_ptr = a.take<int32_t>(NP + 1);
     const size_t o_cursor = a.take<int32_t>(NP);
     const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
@@ -585,21 +663,10 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
 
     tam::DevTables &t = h->dt;
-    t.blob = trie_base + o_blob;
-    t.node_at = reinterpret_cast<const int32_t *>(trie_base + o_node_at);
-    t.node_pos = reinterpret_cast<const int32_t *>(trie_base + o_node_pos);
-    t.depth = reinterpret_cast<const int32_t *>(trie_base + o_depth);
-    t.child_off = reinterpret_cast<const int32_t *>(trie_base + o_child_off);
-    t.child_byte = trie_base + o_child_byte;
-    t.child_node = reinterpret_cast<const int32_t *>(trie_base + o_child_node);
-    t.tok_off = vocab->d_tok_off;
-    t.tok_blob = vocab->d_tok_blob;
-    t.fps = vocab->d_fps;
-    t.pay = vocab->d_pay;
-    t.dup_next = vocab->d_dup_next;
-    t.len_present = vocab->d_len_present;
-    t.hits = reinterpret_cast<int32_t *>(base + o_hits);
-    t.count = reinterpret_cast<int32_t *>(base + o_count);
+    set_trie_tables(t, h, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
+                    o_child_node);
+    t.hits = early_count ? te.hits : reinterpret_cast<int32_t *>(base + o_hits_b);
+    t.count = early_count ? te.count : reinterpret_cast<int32_t *>(base + o_count_b);
     t.row_ptr = reinterpret_cast<int32_t *>(base + o_row_ptr);
     t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
@@ -626,17 +693,6 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.row_at = tails ? reinterpret_cast<const int32_t *>(trie_base + o_row_at) : t.node_at;
     t.R = R;
     t.tail_long = tail_long ? 1 : 0;
-    t.N = h->N;
-    t.V = h->V;
-    t.W = h->W;
-    t.Wp = h->Wp;
-    t.blob_bytes = h->blob_bytes;
-    t.slot_mask = (uint64_t)vocab->fps.size() - 1;
-    t.len_mask = vocab->len_mask;
-    t.max_len = (int32_t)vocab->max_tok_len;
-    t.terminator = h->terminator;
-    t.classes = nullptr;
-    t.fmt_L = -1;
 
     // the trie's tables were uploaded group by group while the host wrote them
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
@@ -652,7 +708,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         return fail(st, msg);
     }
     st = run_device_phase(h, default_phases(h) & ~(early_table ? unsigned(TAM_PHASE_ZERO) : 0u), s,
-                          early_table != nullptr);
+                          early_table != nullptr, early_count);
     if (st != TAM_OK) {
         const std::string msg = g_err;
         destroy_handle(h);

@@ -68,6 +68,9 @@ using hvec = std::vector<T, NoInitAlloc<T>>;
 // Launchers (kernels.hip).  All return hipSuccess or the launch error.
 hipError_t launch_fill_i32(int32_t *p, int64_t n, int32_t value, hipStream_t s);
 hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pairs, hipStream_t s);
+// the list counts of the nodes [m0, m1) (lists only: t.table null; t.count of
+// those nodes zeroed), nodes whose ancestors lie in the same range
+hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 int64_t mark_blocks(int64_t N);
