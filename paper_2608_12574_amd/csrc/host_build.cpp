@@ -38,7 +38,6 @@ struct PartPlan {
     std::vector<int32_t> lcp;   // common prefix with the previous string (0 for the first)
     int64_t nodes = 1;          // including the part's root (its set's root)
     int64_t blob = 0;           // pad byte, bytes, T per string
-    int64_t root_children = 0;  // strings starting a new first byte
     int64_t branching = 0;      // nodes other than the part root that two or more strings pass through
     tam_status st = TAM_OK;
     std::string err;
@@ -96,7 +95,6 @@ void plan_part(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t
         r.lcp.push_back((int32_t)l);
         r.nodes += len + 1 - l;
         r.blob += len + 2;
-        r.root_children += l == 0 ? 1 : 0;
         if (r.nodes >= INT32_MAX || r.blob >= INT32_MAX) {
             r.st = TAM_E_TOOLARGE;
             r.err = "trie exceeds 2^31-1 nodes or string bytes";
@@ -112,13 +110,11 @@ void plan_part(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t
     }
 }
 
-// Where a part's nodes, blob bytes and edges go in the handle's tables.
+// Where a part's nodes and blob bytes go in the handle's tables.
 struct PartBase {
     int32_t root;         // its set's root
     int64_t node;         // local node i >= 1 gets id node + i
     int64_t blob;         // local blob offset b goes to blob + b
-    int64_t edge;         // first of its edges below depth 1
-    int64_t root_edge;    // first of its depth-1 nodes' slots among the set root's edges
     bool root_tail;       // its set has one string (the set root is then a tail)
     int64_t first_row;    // (tail split) dense row of the part's first branching node
 };
@@ -126,11 +122,10 @@ struct PartBase {
 /*
  * Writes a planned part into the handle: per string, a pad byte (standing for
  * the root), its bytes and T into the blob; the nodes it creates (parent,
- * depth, edge byte, final flag, blob position); node_at along the string; and
- * with subtree extents, the end of every node's subtree (a node's subtree ends
- * where the first later string leaves its path).  Then the part's child lists:
- * children in ascending id order, which is ascending byte order; depth-1 nodes
- * are listed on the set root.
+ * depth, edge byte, final flag); node_at along the string; and with subtree
+ * extents, the end of every node's subtree (a node's subtree ends where the
+ * first later string leaves its path).  Node positions and child lists are
+ * derived on the device from the blob, node_at and depth.
  *
  * Tail split, decided when a node is created: string u creates the nodes at
  * path indices i >= lcp[u], and the next string passes through those with
@@ -142,7 +137,6 @@ struct PartBase {
  */
 void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, PartBase &pb,
                bool subtrees, bool tails, tam_handle *h) {
-    const int64_t nloc = r.nodes;
     const int64_t nstr = (int64_t)r.str.size();
     std::vector<int32_t> path;  // global ids of the current string's nodes by depth - 1
     int64_t N = 1, B = 0, prev_len = -1;
@@ -177,7 +171,6 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
                 h->depth[g] = (int32_t)(i + 1);
                 h->edge[g] = c;
                 h->is_final[g] = i == len ? 1 : 0;
-                h->node_pos[g] = (int32_t)pos;
                 path[(size_t)i] = (int32_t)g;
                 if (tails) {
                     const bool branching = i < next;
@@ -191,27 +184,6 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
         B += len + 2;
     }
     close(0);
-    // child lists: count, offsets, then fill in id order
-    std::vector<int32_t> cnt((size_t)nloc, 0);
-    for (int64_t i = 1; i < nloc; ++i) {
-        const int64_t p = h->parent[(size_t)(pb.node + i)];
-        if (p != pb.root) ++cnt[(size_t)(p - pb.node)];
-    }
-    int64_t e = pb.edge;
-    for (int64_t i = 1; i < nloc; ++i) {
-        h->child_off[(size_t)(pb.node + i)] = (int32_t)e;
-        const int32_t c = cnt[(size_t)i];
-        cnt[(size_t)i] = (int32_t)(e - pb.edge);  // becomes the fill cursor
-        e += c;
-    }
-    int64_t re = pb.root_edge;
-    for (int64_t i = 1; i < nloc; ++i) {
-        const int64_t g = pb.node + i;
-        const int64_t p = h->parent[(size_t)g];
-        const int64_t slot = p == pb.root ? re++ : pb.edge + cnt[(size_t)(p - pb.node)]++;
-        h->child_node[(size_t)slot] = (int32_t)g;
-        h->child_byte[(size_t)slot] = h->edge[(size_t)g];
-    }
 }
 
 // Runs f(j) for j in [0, n) on up to `threads` host threads.
@@ -259,9 +231,8 @@ int host_threads(int64_t work_items) {
  * straight into the handle's tables.  Set j takes node ids
  * [roots[j], roots[j] + N_j) and its own range of the blob, which carries
  * kBlobPad zero bytes in front and behind so that 16-byte window loads around
- * any node never leave it.  Edges: a set's root lists its first-byte children
- * (those of its parts, in order), then the parts' other child lists follow in
- * node order.
+ * any node never leave it.  Every node but a root has one parent edge, so
+ * the child lists (built on the device) hold N - S entries.
  */
 tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int64_t *set_off,
                       int64_t S, int T, tam_handle *h, std::string *err,
@@ -325,16 +296,15 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         }
     });
     if (oom) throw std::bad_alloc();
-    // bases: node ids (a part's local root is its set's root, the rest follow),
-    // blob offsets, edges (a set's root edges first, then its parts' others)
+    // bases: node ids (a part's local root is its set's root, the rest follow)
+    // and blob offsets
     std::vector<PartBase> base((size_t)NP);
-    std::vector<int64_t> root((size_t)S), root_edges((size_t)S), set_blob((size_t)S);
+    std::vector<int64_t> root((size_t)S), set_blob((size_t)S);
     std::vector<int32_t> root_row((size_t)S);  // (tail split) row_of of each set root
     int64_t N = 0, BB = kBlobPad, E = 0, rows = 0;
     h->K_unique = 0;
     for (int64_t j = 0; j < S; ++j) {
         root[(size_t)j] = N++;
-        root_edges[(size_t)j] = E;
         set_blob[(size_t)j] = BB;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
             const PartPlan &r = parts[(size_t)p];
@@ -342,8 +312,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
                 *err = r.err;
                 return r.st;
             }
-            base[(size_t)p].root_edge = E;
-            E += r.root_children;  // the part root's children become the set root's
         }
         int64_t set_strings = 0;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p)
@@ -361,10 +329,9 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             pb.root = (int32_t)root[(size_t)j];
             pb.node = N - 1;
             pb.blob = BB;
-            pb.edge = E;
             N += r.nodes - 1;
             BB += r.blob;
-            E += r.nodes - 1 - r.root_children;
+            E += r.nodes - 1;  // every node but a root has one parent
             h->K_unique += (int64_t)r.str.size();
             if (N >= INT32_MAX || BB >= INT32_MAX) {
                 *err = "trie exceeds 2^31-1 nodes or string bytes";
@@ -390,10 +357,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->depth.resize((size_t)N);
     h->edge.resize((size_t)N);
     h->is_final.resize((size_t)N);
-    h->node_pos.resize((size_t)N);
-    h->child_off.resize((size_t)N + 1);
-    h->child_node.resize((size_t)std::max<int64_t>(E, 1));
-    h->child_byte.resize((size_t)std::max<int64_t>(E, 1));
     h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
     h->node_at.resize((size_t)BB);
     const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
@@ -414,8 +377,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         h->depth[(size_t)rt] = 0;
         h->edge[(size_t)rt] = 0;
         h->is_final[(size_t)rt] = 0;
-        h->node_pos[(size_t)rt] = -1;
-        h->child_off[(size_t)rt] = (int32_t)root_edges[(size_t)j];
         if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
         if (tails) {
             h->row_of[(size_t)rt] = root_row[(size_t)j];
@@ -425,7 +386,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     if (tails)
         for (int64_t p = 0; p < kBlobPad; ++p)  // the outer pads stand for the first set's root
             h->row_at[(size_t)p] = h->row_at[(size_t)(BB - 1 - p)] = h->row_of[0];
-    h->child_off[(size_t)N] = (int32_t)E;
     // Emission in groups of whole sets (a forest of many sets: four groups, so
     // that a caller can upload a group while the next is written).
     const int64_t groups = emitted && S >= 8 ? 4 : 1;
@@ -442,8 +402,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         if (oom) throw std::bad_alloc();
         if (emitted) {
             const TrieRange r{root[(size_t)j0], j1 < S ? root[(size_t)j1] : N,
-                              g == 0 ? 0 : set_blob[(size_t)j0], j1 < S ? set_blob[(size_t)j1] : BB,
-                              root_edges[(size_t)j0], j1 < S ? root_edges[(size_t)j1] : E};
+                              g == 0 ? 0 : set_blob[(size_t)j0], j1 < S ? set_blob[(size_t)j1] : BB};
             const tam_status st = emitted(h, r);
             if (st != TAM_OK) return st;
         }

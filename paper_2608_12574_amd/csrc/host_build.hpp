@@ -8,10 +8,10 @@
 
 namespace tam {
 
-// Ranges of the trie tables that are complete: nodes [n_lo, n_hi) (child_off
-// also entry N when n_hi == N), blob bytes [b_lo, b_hi), edges [e_lo, e_hi).
+// Ranges of the trie tables that are complete: nodes [n_lo, n_hi) and blob
+// bytes [b_lo, b_hi).
 struct TrieRange {
-    int64_t n_lo, n_hi, b_lo, b_hi, e_lo, e_hi;
+    int64_t n_lo, n_hi, b_lo, b_hi;
 };
 
 // planned (optional) runs once the trie's sizes (N, S, blob bytes, edges) are

@@ -815,6 +815,52 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
     }
 }
 
+// ------------------------------------------- node positions, child lists ---
+
+// The trie's node positions and child lists, built on the device from the
+// uploaded blob, node_at and depth.  The strings lie in the blob in trie
+// order, so a node's first position is where the string that created it wrote
+// its edge byte (node_pos), and one position before sits its parent (the pad
+// byte before a string stands for the set root).  Roots have no position.
+
+// node_pos of the nodes [n0, n1): -1 for a root, else a large value that
+// k_first_pos lowers
+__global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__ depth, int64_t n0, int64_t n1,
+                                                     int32_t *__restrict__ node_pos) {
+    const int64_t g = n0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (g < n1) node_pos[g] = depth[g] == 0 ? -1 : INT_MAX;
+}
+
+// the first position of every non-root node in the blob range [b0, b1)
+__global__ void __launch_bounds__(kBlock) k_first_pos(const int32_t *__restrict__ node_at,
+                                                      const int32_t *__restrict__ depth, int64_t b0, int64_t b1,
+                                                      int32_t *node_pos) {
+    const int64_t p = b0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (p >= b1) return;
+    const int32_t g = node_at[p];
+    if (depth[g] > 0) atomicMin(&node_pos[g], (int32_t)p);
+}
+
+// children per node (cnt zeroed before)
+__global__ void __launch_bounds__(kBlock) k_child_count(DevTables t, int32_t *cnt) {
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (g >= t.N || t.depth[g] == 0) return;
+    atomicAdd(&cnt[t.node_at[t.node_pos[g] - 1]], 1);
+}
+
+// every non-root node into its parent's list (cursor zeroed before); the
+// order inside a list is free: a lookup matches the child byte
+__global__ void __launch_bounds__(kBlock) k_child_fill(DevTables t, int32_t *cursor, int32_t *child_node,
+                                                       uint8_t *child_byte) {
+    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (g >= t.N || t.depth[g] == 0) return;
+    const int64_t pos = t.node_pos[g];
+    const int32_t par = t.node_at[pos - 1];
+    const int32_t slot = t.child_off[par] + atomicAdd(&cursor[par], 1);
+    child_node[slot] = (int32_t)g;
+    child_byte[slot] = t.blob[pos];
+}
+
 // ------------------------------------------------- fixed-format strings ---
 
 // Token bytes tb[0..len) at position p of a fixed format: non-empty, within
@@ -1277,6 +1323,37 @@ hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStr
     if (m0 < 0 || m1 > t.N || t.table) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_probe<true>, dim3((unsigned)mark_blocks(m1 - m0)), dim3(kBlock), 0, s, t, m0, m1, 0,
                        (int32_t *)nullptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
+                           hipStream_t s) {
+    if (n0 < 0 || n1 > t.N || b0 < 0 || b1 > t.blob_bytes) return hipErrorInvalidValue;
+    if (n1 > n0)
+        hipLaunchKernelGGL(k_pos_init, dim3(grid_for(n1 - n0, kBlock)), dim3(kBlock), 0, s, t.depth, n0, n1, node_pos);
+    if (b1 > b0)
+        hipLaunchKernelGGL(k_first_pos, dim3(grid_for(b1 - b0, kBlock)), dim3(kBlock), 0, s, t.node_at, t.depth, b0,
+                           b1, node_pos);
+    return hipGetLastError();
+}
+
+hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *child_node, uint8_t *child_byte,
+                              int32_t *tmp, int32_t *scan_tmp, hipStream_t s) {
+    if (t.N <= 0) return hipSuccess;
+    const unsigned g = grid_for(t.N, kBlock);
+    hipError_t e = launch_fill_i32(tmp, t.N, 0, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_child_count, dim3(g), dim3(kBlock), 0, s, t, tmp);
+    DevTables ts = t;  // the scan: counts -> child_off[0..N], the total at N
+    ts.count = tmp;
+    ts.row_ptr = child_off;
+    ts.scan_tmp = scan_tmp;
+    e = launch_scan(ts, s);
+    if (e == hipSuccess) e = launch_fill_i32(tmp, t.N, 0, s);
+    if (e != hipSuccess) return e;
+    DevTables tf = t;
+    tf.child_off = child_off;
+    hipLaunchKernelGGL(k_child_fill, dim3(g), dim3(kBlock), 0, s, tf, tmp, child_node, child_byte);
     return hipGetLastError();
 }
 

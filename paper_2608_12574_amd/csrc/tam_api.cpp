@@ -447,7 +447,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // by group, right after each group's upload (a node's ancestors are in its
     // own set), so only the last group's counts follow the host build.
     const bool early_count = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & TAM_FLAG_LAZY_ROWS);
-    size_t o_hits = 0, o_count = 0;
+    size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0;
     tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
     double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
@@ -478,15 +478,17 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
         o_hits = ta.take<int32_t>(early_count ? tam::kWin * hh->N : 0);
         o_count = ta.take<int32_t>(early_count ? hh->N : 0);
+        o_tmp = ta.take<int32_t>(hh->N);  // scratch of the child lists' build
+        o_scan_tmp = ta.take<int32_t>(tam::scan_tmp_elems(hh->N));
         trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
         if (!trie_base) {
             err = "device allocation failed (" + std::to_string(ta.used) + " bytes requested)";
             return TAM_E_NOMEM;
         }
         hh->device_bytes = (int64_t)ta.used;
+        set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
+                        o_child_node);
         if (early_count) {
-            set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off,
-                            o_child_byte, o_child_node);
             te.hits = reinterpret_cast<int32_t *>(trie_base + o_hits);
             te.count = reinterpret_cast<int32_t *>(trie_base + o_count);
             hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
@@ -535,26 +537,30 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
                 enqueued = true;
             }
         };
-        const int64_t n_top = r.n_hi == hh->N ? hh->N + 1 : r.n_hi;  // child_off[N] with the last group
         up(o_blob, hh->blob.data(), r.b_lo, r.b_hi, 1);
         up(o_node_at, hh->node_at.data(), r.b_lo, r.b_hi, 4);
-        up(o_node_pos, hh->node_pos.data(), r.n_lo, r.n_hi, 4);
         up(o_depth, hh->depth.data(), r.n_lo, r.n_hi, 4);
-        up(o_child_off, hh->child_off.data(), r.n_lo, n_top, 4);
-        up(o_child_byte, hh->child_byte.data(), r.e_lo, r.e_hi, 1);
-        up(o_child_node, hh->child_node.data(), r.e_lo, r.e_hi, 4);
         if (hh->flags & TAM_FLAG_LAZY_ROWS) up(o_sub_end, hh->sub_end.data(), r.n_lo, r.n_hi, 4);
         if (split) {
             up(o_tail_span, hh->tail_span.data(), r.n_lo, r.n_hi, 4);
             up(o_row_of, hh->row_of.data(), r.n_lo, r.n_hi, 4);
             up(o_row_at, hh->row_at.data(), r.b_lo, r.b_hi, 4);
         }
+        // the group's node positions (its nodes lie in its blob range), then
+        // (lists) its counts; after the last group the child lists
+        int32_t *node_pos = reinterpret_cast<int32_t *>(trie_base + o_node_pos);
+        if (e == hipSuccess) e = tam::launch_node_pos(te, node_pos, r.n_lo, r.n_hi, r.b_lo, r.b_hi, s);
         if (early_count && e == hipSuccess) {
             const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
             if (timing && r.n_lo == 0) e = hipEventRecord(hh->ev[4], s);  // the counts' start
             if (e == hipSuccess) e = tam::launch_count_range(te, r.n_lo, r.n_hi, s);
             if (e == hipSuccess && timing && r.n_hi == hh->N) e = hipEventRecord(hh->ev[2], s);
         }
+        if (e == hipSuccess && r.n_hi == hh->N)
+            e = tam::launch_child_lists(te, reinterpret_cast<int32_t *>(trie_base + o_child_off),
+                                        reinterpret_cast<int32_t *>(trie_base + o_child_node),
+                                        trie_base + o_child_byte, reinterpret_cast<int32_t *>(trie_base + o_tmp),
+                                        reinterpret_cast<int32_t *>(trie_base + o_scan_tmp), s);
         hook_ms += ms_since(t1);
         if (e != hipSuccess) {
             err = std::string("upload: ") + hipGetErrorString(e);

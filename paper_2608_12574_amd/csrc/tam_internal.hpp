@@ -71,6 +71,15 @@ hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pair
 // the list counts of the nodes [m0, m1) (lists only: t.table null; t.count of
 // those nodes zeroed), nodes whose ancestors lie in the same range
 hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s);
+// node_pos of the nodes [n0, n1) from the blob range [b0, b1) they were
+// written in (node_at and depth of those ranges uploaded)
+hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
+                           hipStream_t s);
+// the child lists of every node (node_pos complete): child_off[N+1],
+// child_node/child_byte[N - roots]; tmp [N] and scan_tmp [scan_tmp_elems(N)]
+// are scratch
+hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *child_node, uint8_t *child_byte,
+                              int32_t *tmp, int32_t *scan_tmp, hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 int64_t mark_blocks(int64_t N);
@@ -148,9 +157,9 @@ struct tam_handle {
     int64_t blob_bytes = 0, entry_bound = 0, device_bytes = 0;
 
     // host trie tables
-    tam::hvec<int32_t> roots, parent, depth, node_pos, node_at, child_off, child_node;
+    tam::hvec<int32_t> roots, parent, depth, node_at;
     tam::hvec<int32_t> sub_end;  // [N] with TAM_FLAG_LAZY_ROWS: one past the node's subtree
-    tam::hvec<uint8_t> edge, is_final, blob, child_byte;
+    tam::hvec<uint8_t> edge, is_final, blob;
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
     tam::hvec<int32_t> tail_span, row_of, row_at;
     int64_t dense_rows = 0;
