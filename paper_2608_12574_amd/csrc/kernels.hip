@@ -918,7 +918,7 @@ __global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restr
 // --------------------------------------------------------------- advance ---
 
 // The extended transition function, one wave per batch row.  A child step
-// compares up to 64 of the node's sorted child bytes at once (one ballot)
+// compares up to 64 of the node's child bytes at once (one ballot)
 // instead of a binary search.  Between child steps the walk follows the
 // node's owner string (the first set string through it, stored in the blob
 // right after the node's edge byte): lane j compares token byte i+j with the
@@ -954,7 +954,7 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
         int32_t lo = t.child_off[n0], hi = t.child_off[n0 + 1];  // loaded beside the token's offsets
         while (i < len && n >= 0) {
             const uint32_t c = t.tok_blob[a + i];
-            // child of n along c: its sorted child bytes and ids, 64 lanes at a
+            // child of n along c: its child bytes and ids, 64 lanes at a
             // time, loaded together with the token byte
             int32_t nx = TAM_DEAD;
             for (int32_t k0 = lo; k0 < hi; k0 += kWave) {
