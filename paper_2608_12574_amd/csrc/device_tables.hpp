@@ -56,6 +56,16 @@ __host__ __device__ __forceinline__ int32_t hit_of_slot(int32_t slot, int32_t fi
     return count == 1 ? first : -2 - slot;
 }
 
+// One string of the trie's blob, in blob order; the device lays out node_at
+// and depth from these.  at: position of its pad byte; len: its length (the
+// terminator follows at at + 1 + len); lcp: its common prefix with the
+// previous string of its part; first: id of the first node it creates (at
+// path index lcp); psv: the nearest earlier string of its part with a shorter
+// common prefix (-1: none); root: its set's root.
+struct StrRec {
+    int32_t at, len, lcp, first, psv, root;
+};
+
 // ---------------------------------------------------------------------------
 // Device-side view of a compiled handle (plain pointers, passed to kernels).
 // ---------------------------------------------------------------------------

@@ -36,6 +36,7 @@ struct TerminatedLess {
 struct PartPlan {
     std::vector<int64_t> str;   // string indices in trie order, duplicates dropped
     std::vector<int32_t> lcp;   // common prefix with the previous string (0 for the first)
+    std::vector<int32_t> psv;   // nearest earlier string with a shorter common prefix (-1: none)
     int64_t nodes = 1;          // including the part's root (its set's root)
     int64_t blob = 0;           // pad byte, bytes, T per string
     int64_t branching = 0;      // nodes other than the part root that two or more strings pass through
@@ -108,6 +109,14 @@ void plan_part(const uint8_t *sb, const int64_t *so, const int64_t *idx, int64_t
         const int64_t next = u + 1 < r.lcp.size() ? r.lcp[u + 1] : 0;
         r.branching += std::max<int64_t>(0, next - r.lcp[u]);
     }
+    // previous strictly smaller common prefix (a stack of increasing lcp)
+    r.psv.resize(r.lcp.size());
+    std::vector<int32_t> stack;
+    for (size_t u = 0; u < r.lcp.size(); ++u) {
+        while (!stack.empty() && r.lcp[(size_t)stack.back()] >= r.lcp[u]) stack.pop_back();
+        r.psv[u] = stack.empty() ? -1 : stack.back();
+        stack.push_back((int32_t)u);
+    }
 }
 
 // Where a part's nodes and blob bytes go in the handle's tables.
@@ -116,16 +125,17 @@ struct PartBase {
     int64_t node;         // local node i >= 1 gets id node + i
     int64_t blob;         // local blob offset b goes to blob + b
     bool root_tail;       // its set has one string (the set root is then a tail)
+    int64_t str0;         // blob-order index of its first string
     int64_t first_row;    // (tail split) dense row of the part's first branching node
 };
 
 /*
  * Writes a planned part into the handle: per string, a pad byte (standing for
- * the root), its bytes and T into the blob; the nodes it creates (parent,
- * depth, edge byte, final flag); node_at along the string; and with subtree
- * extents, the end of every node's subtree (a node's subtree ends where the
- * first later string leaves its path).  Node positions and child lists are
- * derived on the device from the blob, node_at and depth.
+ * the root), its bytes and T into the blob, and its record (StrRec); the nodes
+ * it creates (parent, depth, edge byte, final flag); and with subtree extents,
+ * the end of every node's subtree (a node's subtree ends where the first later
+ * string leaves its path).  node_at, the device's depth, node positions and
+ * child lists are derived on the device from the blob and the records.
  *
  * Tail split, decided when a node is created: string u creates the nodes at
  * path indices i >= lcp[u], and the next string passes through those with
@@ -158,8 +168,10 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
         prev_len = len;
         if ((int64_t)path.size() < len + 1) path.resize((size_t)(len + 1));
         const int64_t at = pb.blob + B;
+        const int32_t psv = r.psv[(size_t)u];
+        h->strs[(size_t)(pb.str0 + u)] = StrRec{(int32_t)at, (int32_t)len, (int32_t)l, (int32_t)(pb.node + N),
+                                                psv < 0 ? -1 : (int32_t)(pb.str0 + psv), pb.root};
         h->blob[(size_t)at] = 0;
-        h->node_at[(size_t)at] = pb.root;
         if (tails) h->row_at[(size_t)at] = h->row_of[(size_t)pb.root];
         for (int64_t i = 0; i <= len; ++i) {
             const uint8_t c = i < len ? s[i] : term;
@@ -178,7 +190,6 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
                     h->tail_span[g] = branching ? 0 : (int32_t)(i - top);
                 }
             }
-            h->node_at[pos] = path[(size_t)i];
             if (tails) h->row_at[pos] = h->row_of[(size_t)path[(size_t)i]];
         }
         B += len + 2;
@@ -299,13 +310,14 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     // bases: node ids (a part's local root is its set's root, the rest follow)
     // and blob offsets
     std::vector<PartBase> base((size_t)NP);
-    std::vector<int64_t> root((size_t)S), set_blob((size_t)S);
+    std::vector<int64_t> root((size_t)S), set_blob((size_t)S), set_str((size_t)S);
     std::vector<int32_t> root_row((size_t)S);  // (tail split) row_of of each set root
     int64_t N = 0, BB = kBlobPad, E = 0, rows = 0;
     h->K_unique = 0;
     for (int64_t j = 0; j < S; ++j) {
         root[(size_t)j] = N++;
         set_blob[(size_t)j] = BB;
+        set_str[(size_t)j] = h->K_unique;
         for (int64_t p = set_first[(size_t)j]; p < set_first[(size_t)j + 1]; ++p) {
             const PartPlan &r = parts[(size_t)p];
             if (r.st != TAM_OK) {
@@ -329,12 +341,13 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             pb.root = (int32_t)root[(size_t)j];
             pb.node = N - 1;
             pb.blob = BB;
+            pb.str0 = h->K_unique;
             N += r.nodes - 1;
             BB += r.blob;
             E += r.nodes - 1;  // every node but a root has one parent
             h->K_unique += (int64_t)r.str.size();
-            if (N >= INT32_MAX || BB >= INT32_MAX) {
-                *err = "trie exceeds 2^31-1 nodes or string bytes";
+            if (N >= INT32_MAX || BB >= INT32_MAX || h->K_unique >= INT32_MAX) {
+                *err = "trie exceeds 2^31-1 nodes, strings or string bytes";
                 return TAM_E_TOOLARGE;
             }
         }
@@ -358,7 +371,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->edge.resize((size_t)N);
     h->is_final.resize((size_t)N);
     h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
-    h->node_at.resize((size_t)BB);
+    h->strs.resize((size_t)h->K_unique);
     const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
     const bool tails = (h->flags & TAM_FLAG_TAIL_LISTS) && !(h->flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
     h->sub_end.resize(subtrees ? (size_t)N : 0);
@@ -368,7 +381,6 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->dense_rows = tails ? rows : 0;
     for (int64_t p = 0; p < kBlobPad; ++p) {
         h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
-        h->node_at[(size_t)p] = h->node_at[(size_t)(BB - 1 - p)] = 0;
     }
     for (int64_t j = 0; j < S; ++j) {
         const int64_t rt = root[(size_t)j];
@@ -402,7 +414,8 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         if (oom) throw std::bad_alloc();
         if (emitted) {
             const TrieRange r{root[(size_t)j0], j1 < S ? root[(size_t)j1] : N,
-                              g == 0 ? 0 : set_blob[(size_t)j0], j1 < S ? set_blob[(size_t)j1] : BB};
+                              g == 0 ? 0 : set_blob[(size_t)j0], j1 < S ? set_blob[(size_t)j1] : BB,
+                              set_str[(size_t)j0], j1 < S ? set_str[(size_t)j1] : h->K_unique};
             const tam_status st = emitted(h, r);
             if (st != TAM_OK) return st;
         }

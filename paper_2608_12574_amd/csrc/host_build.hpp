@@ -8,10 +8,10 @@
 
 namespace tam {
 
-// Ranges of the trie tables that are complete: nodes [n_lo, n_hi) and blob
-// bytes [b_lo, b_hi).
+// Ranges of the trie tables that are complete: nodes [n_lo, n_hi), blob
+// bytes [b_lo, b_hi) and string records [s_lo, s_hi).
 struct TrieRange {
-    int64_t n_lo, n_hi, b_lo, b_hi;
+    int64_t n_lo, n_hi, b_lo, b_hi, s_lo, s_hi;
 };
 
 // planned (optional) runs once the trie's sizes (N, S, blob bytes, edges) are

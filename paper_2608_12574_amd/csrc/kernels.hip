@@ -823,6 +823,37 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
 // its edge byte (node_pos), and one position before sits its parent (the pad
 // byte before a string stands for the set root).  Roots have no position.
 
+// node_at and depth from the string records [s0, s1), one thread per string.
+// String u creates the nodes first .. first + len - lcp along path indices
+// lcp .. len (depth = index + 1).  Below index lcp its path is the previous
+// string's: index i belongs to the nearest earlier string v of the part with
+// lcp[v] <= i.  Walking from u - 1 along psv (each step lowers lcp), a string
+// whose lcp is below the indices still open owns [lcp[v], open bound); one
+// whose lcp is not below them owns none of them and is passed over.
+__global__ void __launch_bounds__(kBlock) k_node_at(const StrRec *__restrict__ strs, int64_t s0, int64_t s1,
+                                                    int32_t *__restrict__ node_at, int32_t *__restrict__ depth) {
+    const int64_t u = s0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (u >= s1) return;
+    const StrRec r = strs[u];
+    node_at[r.at] = r.root;  // the pad stands for the root
+    if (r.lcp == 0) depth[r.root] = 0;
+    for (int32_t i = r.lcp; i <= r.len; ++i) {
+        const int32_t g = r.first + (i - r.lcp);
+        node_at[r.at + 1 + i] = g;
+        depth[g] = i + 1;
+    }
+    int32_t hi = r.lcp;  // indices [0, hi) still open
+    int64_t v = u - 1;   // lcp > 0: not the first string of its part
+    while (hi > 0) {     // ends at a string with lcp 0, which owns all that is open
+        const StrRec q = strs[v];
+        if (q.lcp < hi) {
+            for (int32_t i = q.lcp; i < hi; ++i) node_at[r.at + 1 + i] = q.first + (i - q.lcp);
+            hi = q.lcp;
+        }
+        v = q.psv;
+    }
+}
+
 // node_pos of the nodes [n0, n1): -1 for a root, else a large value that
 // k_first_pos lowers
 __global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__ depth, int64_t n0, int64_t n1,
@@ -833,19 +864,29 @@ __global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__
 
 // the first position of every non-root node in the blob range [b0, b1)
 __global__ void __launch_bounds__(kBlock) k_first_pos(const int32_t *__restrict__ node_at,
-                                                      const int32_t *__restrict__ depth, int64_t b0, int64_t b1,
-                                                      int32_t *node_pos) {
+                                                      const int32_t *__restrict__ depth, int64_t N, int64_t b0,
+                                                      int64_t b1, int32_t *node_pos) {
     const int64_t p = b0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (p >= b1) return;
     const int32_t g = node_at[p];
-    if (depth[g] > 0) atomicMin(&node_pos[g], (int32_t)p);
+    if ((uint32_t)g < (uint64_t)N && depth[g] > 0) atomicMin(&node_pos[g], (int32_t)p);
 }
 
 // children per node (cnt zeroed before)
+// The parent of non-root node g, or -1 if g has no position (which the
+// uploaded tables rule out; the check keeps a bad table from faulting).
+__device__ __forceinline__ int32_t parent_of(const DevTables &t, int64_t g) {
+    const int64_t pos = t.node_pos[g];
+    if (pos <= 0 || pos >= t.blob_bytes) return -1;
+    const int32_t par = t.node_at[pos - 1];
+    return (uint32_t)par < (uint64_t)t.N ? par : -1;
+}
+
 __global__ void __launch_bounds__(kBlock) k_child_count(DevTables t, int32_t *cnt) {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= t.N || t.depth[g] == 0) return;
-    atomicAdd(&cnt[t.node_at[t.node_pos[g] - 1]], 1);
+    const int32_t par = parent_of(t, g);
+    if (par >= 0) atomicAdd(&cnt[par], 1);
 }
 
 // every non-root node into its parent's list (cursor zeroed before); the
@@ -854,11 +895,11 @@ __global__ void __launch_bounds__(kBlock) k_child_fill(DevTables t, int32_t *cur
                                                        uint8_t *child_byte) {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= t.N || t.depth[g] == 0) return;
-    const int64_t pos = t.node_pos[g];
-    const int32_t par = t.node_at[pos - 1];
+    const int32_t par = parent_of(t, g);
+    if (par < 0) return;
     const int32_t slot = t.child_off[par] + atomicAdd(&cursor[par], 1);
     child_node[slot] = (int32_t)g;
-    child_byte[slot] = t.blob[pos];
+    child_byte[slot] = t.blob[t.node_pos[g]];
 }
 
 // ------------------------------------------------- fixed-format strings ---
@@ -1326,14 +1367,21 @@ hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStr
     return hipGetLastError();
 }
 
+hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int32_t *node_at, int32_t *depth,
+                          hipStream_t s) {
+    if (s1 <= s0) return hipSuccess;
+    hipLaunchKernelGGL(k_node_at, dim3(grid_for(s1 - s0, kBlock)), dim3(kBlock), 0, s, strs, s0, s1, node_at, depth);
+    return hipGetLastError();
+}
+
 hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
                            hipStream_t s) {
     if (n0 < 0 || n1 > t.N || b0 < 0 || b1 > t.blob_bytes) return hipErrorInvalidValue;
     if (n1 > n0)
         hipLaunchKernelGGL(k_pos_init, dim3(grid_for(n1 - n0, kBlock)), dim3(kBlock), 0, s, t.depth, n0, n1, node_pos);
     if (b1 > b0)
-        hipLaunchKernelGGL(k_first_pos, dim3(grid_for(b1 - b0, kBlock)), dim3(kBlock), 0, s, t.node_at, t.depth, b0,
-                           b1, node_pos);
+        hipLaunchKernelGGL(k_first_pos, dim3(grid_for(b1 - b0, kBlock)), dim3(kBlock), 0, s, t.node_at, t.depth, t.N,
+                           b0, b1, node_pos);
     return hipGetLastError();
 }
 

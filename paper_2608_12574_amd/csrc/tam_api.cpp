@@ -447,7 +447,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // by group, right after each group's upload (a node's ancestors are in its
     // own set), so only the last group's counts follow the host build.
     const bool early_count = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & TAM_FLAG_LAZY_ROWS);
-    size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0;
+    size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0, o_strs = 0;
     tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
     double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
@@ -478,6 +478,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
         o_hits = ta.take<int32_t>(early_count ? tam::kWin * hh->N : 0);
         o_count = ta.take<int32_t>(early_count ? hh->N : 0);
+        o_strs = ta.take<tam::StrRec>(hh->K_unique);
         o_tmp = ta.take<int32_t>(hh->N);  // scratch of the child lists' build
         o_scan_tmp = ta.take<int32_t>(tam::scan_tmp_elems(hh->N));
         trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
@@ -488,6 +489,16 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         hh->device_bytes = (int64_t)ta.used;
         set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
                         o_child_node);
+        {  // the blob's outer pads stand for the first set's root
+            int32_t *node_at = reinterpret_cast<int32_t *>(trie_base + o_node_at);
+            hipError_t e = tam::launch_fill_i32(node_at, tam::kBlobPad, 0, s);
+            if (e == hipSuccess) e = tam::launch_fill_i32(node_at + hh->blob_bytes - tam::kBlobPad, tam::kBlobPad, 0, s);
+            enqueued = true;
+            if (e != hipSuccess) {
+                err = std::string("trie tables: ") + hipGetErrorString(e);
+                return TAM_E_DEVICE;
+            }
+        }
         if (early_count) {
             te.hits = reinterpret_cast<int32_t *>(trie_base + o_hits);
             te.count = reinterpret_cast<int32_t *>(trie_base + o_count);
@@ -538,17 +549,21 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
             }
         };
         up(o_blob, hh->blob.data(), r.b_lo, r.b_hi, 1);
-        up(o_node_at, hh->node_at.data(), r.b_lo, r.b_hi, 4);
-        up(o_depth, hh->depth.data(), r.n_lo, r.n_hi, 4);
+        up(o_strs, hh->strs.data(), r.s_lo, r.s_hi, sizeof(tam::StrRec));
         if (hh->flags & TAM_FLAG_LAZY_ROWS) up(o_sub_end, hh->sub_end.data(), r.n_lo, r.n_hi, 4);
         if (split) {
             up(o_tail_span, hh->tail_span.data(), r.n_lo, r.n_hi, 4);
             up(o_row_of, hh->row_of.data(), r.n_lo, r.n_hi, 4);
             up(o_row_at, hh->row_at.data(), r.b_lo, r.b_hi, 4);
         }
-        // the group's node positions (its nodes lie in its blob range), then
-        // (lists) its counts; after the last group the child lists
+        // the group's node_at and depth (from its strings), node positions
+        // (its nodes lie in its blob range), then (lists) its counts; after the
+        // last group the child lists
         int32_t *node_pos = reinterpret_cast<int32_t *>(trie_base + o_node_pos);
+        if (e == hipSuccess)
+            e = tam::launch_node_at(reinterpret_cast<const tam::StrRec *>(trie_base + o_strs), r.s_lo, r.s_hi,
+                                    reinterpret_cast<int32_t *>(trie_base + o_node_at),
+                                    reinterpret_cast<int32_t *>(trie_base + o_depth), s);
         if (e == hipSuccess) e = tam::launch_node_pos(te, node_pos, r.n_lo, r.n_hi, r.b_lo, r.b_hi, s);
         if (early_count && e == hipSuccess) {
             const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;

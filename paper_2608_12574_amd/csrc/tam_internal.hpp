@@ -71,6 +71,10 @@ hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pair
 // the list counts of the nodes [m0, m1) (lists only: t.table null; t.count of
 // those nodes zeroed), nodes whose ancestors lie in the same range
 hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s);
+// node_at and depth of the string records [s0, s1) (records uploaded; the
+// strings' earlier part-mates with shorter prefixes are in the same range)
+hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int32_t *node_at, int32_t *depth,
+                          hipStream_t s);
 // node_pos of the nodes [n0, n1) from the blob range [b0, b1) they were
 // written in (node_at and depth of those ranges uploaded)
 hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
@@ -157,7 +161,8 @@ struct tam_handle {
     int64_t blob_bytes = 0, entry_bound = 0, device_bytes = 0;
 
     // host trie tables
-    tam::hvec<int32_t> roots, parent, depth, node_at;
+    tam::hvec<int32_t> roots, parent, depth;
+    tam::hvec<tam::StrRec> strs;  // the blob's strings, in blob order
     tam::hvec<int32_t> sub_end;  // [N] with TAM_FLAG_LAZY_ROWS: one past the node's subtree
     tam::hvec<uint8_t> edge, is_final, blob;
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
