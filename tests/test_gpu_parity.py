@@ -555,6 +555,35 @@ def test_forest_written_in_groups(P, flags):
     h.close()
 
 
+def nested_chain(depth: int, a: bytes, b: bytes) -> list:
+    """a, aa, ..., a^depth, then a^i b and a^i b b for every i < depth: in trie
+    order the a^i b strings come deepest first, so each one shares a shorter
+    prefix with the string before it than that string did with its own
+    predecessor, and the prefix nodes it reuses lie several strings back."""
+    out = [a * i for i in range(1, depth + 1)]
+    out += [a * i + b for i in range(depth)] + [a * i + b + b for i in range(0, depth, 3)]
+    return out
+
+
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
+def test_nested_prefix_chains(P, flags):
+    """Strings nested as prefixes of each other, one set of depth 48 and a
+    forest of nine chains of depths 1-70 (written in groups of sets), every
+    row, every advance and apply against the oracle.  Each string's prefix
+    nodes are found by walking back over earlier strings that share ever
+    shorter prefixes with it."""
+    vocab = [b"a", b"b", b"c", b'"', b"aa", b"aaa", b"a" * 8, b"ab", b"bb", b'b"', b'a"', b"ba", b"c" * 5]
+    h, _ = full_check(P, nested_chain(48, b"a", b"b"), vocab, flags=flags)
+    h.close()
+    sets = [nested_chain(d, a, b) for d, a, b in
+            [(1, b"a", b"b"), (70, b"a", b"b"), (17, b"b", b"a"), (5, b"c", b"a"), (33, b"a", b"c"),
+             (2, b"b", b"b"), (64, b"c", b"b"), (9, b"a", b"a"), (40, b"b", b"c")]]
+    strings = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    h, _ = full_check(P, strings, vocab, sets=offs, flags=flags)
+    h.close()
+
+
 @pytest.mark.parametrize("seed", range(30))
 def test_random_forests(P, seed):
     """Random forests (1-19 sets of 1-1,500 strings over 2-9 byte values,
