@@ -584,6 +584,37 @@ def test_nested_prefix_chains(P, flags):
     h.close()
 
 
+def long_token_case():
+    """Strings of 60-200 bytes over {a, b, c}, some sharing their first 50+
+    bytes with another, and tokens of 60-130 bytes cut from them (some ending
+    in the terminator): token lengths of 64 and more, looked up in the
+    per-length table rather than the 64-bit length mask."""
+    rng = np.random.default_rng(64)
+    abc = np.frombuffer(b"abc", dtype=np.uint8)
+    base = [bytes(abc[rng.integers(0, 3, size=int(rng.integers(60, 201)))]) for _ in range(25)]
+    strings = base + [b[:int(rng.integers(50, len(b)))] + bytes(abc[rng.integers(0, 3, size=int(rng.integers(1, 60)))])
+                      for b in base[:15]]
+    vocab = [b"a", b"b", b"c", b'"', b"ab", b"ca"]
+    pool = [s for s in strings if len(s) >= 60]
+    for k in range(200):
+        src = pool[int(rng.integers(0, len(pool)))]
+        n = int(rng.integers(60, min(130, len(src)) + 1))
+        st = int(rng.integers(0, len(src) - n + 1))
+        vocab.append(src[st:] + b'"' if k % 5 == 0 else src[st:st + n])
+    vocab += [strings[0][:64], strings[1][3:68], strings[2][:63] + b'"']
+    return strings, vocab
+
+
+@pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
+def test_tokens_of_64_bytes_and_more(P, flags):
+    """Every row, every advance and apply against the oracle when valid tokens
+    are 64 to 200 bytes long and the trie branches below depth 64."""
+    strings, vocab = long_token_case()
+    h, o = full_check(P, strings, vocab, flags=flags)
+    assert h.max_token_len >= 130
+    h.close()
+
+
 @pytest.mark.parametrize("seed", range(30))
 def test_random_forests(P, seed):
     """Random forests (1-19 sets of 1-1,500 strings over 2-9 byte values,
