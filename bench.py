@@ -117,6 +117,7 @@ class Bench:
                      .to(self.logit_dtype) for _ in range(self.nbuf)]
         self.voc = None
         self.vocab_ms = None
+        self.oracle, self.sample = None, None  # set by the CPU-baseline leg
         # the strings in the C ABI's input form (CSR bytes + offsets); packing a
         # Python list is timed on its own
         from paper_2608_12574_amd.tam import csr
@@ -129,6 +130,89 @@ class Bench:
 
     def event(self):
         return self.torch.cuda.Event(enable_timing=True)
+
+    def structure(self, h):
+        """The paper's structural diagnostics of the workload.  Prefix sharing
+        (appendix "Prefix Sharing Analysis"): r = |T| / N_chars per set, |T| the
+        trie's nodes without the terminator nodes (the root counted, as in the
+        worked example's 29 nodes for 44 characters) and N_chars the bytes of
+        the set's distinct strings.  Valid-set sizes by depth (the appendix's
+        "Valid set size distribution"): |valid[n]| of every node, counted on the
+        device from the handle's rows (tam_valid_counts)."""
+        torch, w = self.torch, self.w
+        offs = list(w.set_offsets) if w.set_offsets is not None else [0, len(w.strings)]
+        roots = list(h.roots) + [h.num_nodes]
+        rs, nodes_t, chars_t, k_t = [], 0, 0, 0
+        for j in range(len(offs) - 1):
+            d = set(w.strings[int(offs[j]):int(offs[j + 1])])
+            chars = sum(len(x) for x in d)
+            nodes = int(roots[j + 1] - roots[j]) - len(d)  # without the terminator nodes
+            rs.append(nodes / max(chars, 1))
+            nodes_t, chars_t, k_t = nodes_t + nodes, chars_t + chars, k_t + len(d)
+        N = h.num_nodes
+        cnt = np.empty(N, dtype=np.int64)
+        step = 1 << 22
+        for a in range(0, N, step):
+            ids = torch.arange(a, min(N, a + step), dtype=torch.int32, device=self.dev)
+            cnt[a:a + ids.numel()] = h.valid_counts(ids).cpu().numpy()
+        depth = h.depth
+        D = int(depth.max()) + 1
+        nodes_d = np.bincount(depth, minlength=D)
+        sum_d = np.bincount(depth, weights=cnt, minlength=D)
+        max_d = np.zeros(D, dtype=np.int64)
+        np.maximum.at(max_d, depth, cnt)
+        keep = nodes_d > 0
+        res = {"prefix_sharing": {"strings": k_t, "N_chars": chars_t, "trie_nodes": nodes_t,
+                                  "r": round(nodes_t / chars_t, 4), "sets": len(rs)},
+               "valid_by_depth": {"depth": np.flatnonzero(keep).tolist(), "nodes": nodes_d[keep].tolist(),
+                                  "mean": np.round(sum_d[keep] / nodes_d[keep], 2).tolist(),
+                                  "max": max_d[keep].tolist()},
+               "valid_pairs_from_counts": int(cnt.sum())}
+        if len(rs) > 1:
+            res["prefix_sharing"]["r_per_set"] = {"min": round(min(rs), 4), "median": round(float(np.median(rs)), 4),
+                                                  "max": round(max(rs), 4)}
+        top = min(D, 9)
+        print(f"[bench] structure: r = {nodes_t}/{chars_t} = {nodes_t / chars_t:.3f}; |valid| by depth "
+              + ", ".join(f"{d}: mean {sum_d[d] / max(nodes_d[d], 1):.1f} max {max_d[d]} ({nodes_d[d]} nodes)"
+                          for d in range(top)), flush=True)
+        return res
+
+    def parity(self, h, ids):
+        """Bit-exactness of a timed handle against the oracle (None without it):
+        the oracle's sampled rows against the handle's exported rows; apply on
+        the timed batch and on a batch of sampled rows, raw bits against the
+        oracle's apply; advance of those rows on a valid token each and on
+        random ids (out of range included) against the oracle's advance."""
+        if self.oracle is None:
+            return None
+        torch, W, o, dev = self.torch, self.W, self.oracle, self.dev
+        nodes, rows = self.sample
+        k = min(len(nodes), 2048)
+        got = h.export_rows(torch.as_tensor(nodes[:k], device=dev)).cpu().numpy().view(np.uint64)
+        rows_ok = bool(np.array_equal(got, rows[:k]))
+        bits_t = torch.int16 if self.esize == 2 else torch.int32
+        bits_np = np.uint16 if self.esize == 2 else np.uint32
+        odt = 1 if self.esize == 2 else 0
+        g = torch.Generator()
+        g.manual_seed(77)
+        apply_ok, advance_ok = True, True
+        rng = np.random.default_rng(78)
+        batches = [ids.cpu().numpy().astype(np.int32), nodes[: self.B].astype(np.int32)]
+        for bi, id_np in enumerate(batches):
+            x = torch.randn((len(id_np), self.V), generator=g).to(self.logit_dtype)
+            exp = o.apply(id_np, x.view(bits_t).numpy().view(bits_np), odt)
+            xd = x.to(dev)
+            idt = torch.as_tensor(id_np, device=dev)
+            h.apply_mask(idt, xd)
+            apply_ok = apply_ok and bool(np.array_equal(xd.view(bits_t).cpu().numpy().view(bits_np), exp))
+            vrows = rows[: self.B] if bi == 1 else o.mask_rows(id_np)
+            for toks in (W.choose_valid_tokens(rng, vrows, self.V),
+                         rng.integers(-1, self.V + 1, size=len(id_np)).astype(np.int32)):
+                out = h.advance(idt, torch.as_tensor(toks, device=dev)).cpu().numpy()
+                advance_ok = advance_ok and bool(np.array_equal(out, o.advance(id_np, toks)))
+        return {"rows_checked": int(k), "rows": rows_ok, "apply_rows_checked": int(sum(len(b) for b in batches)),
+                "apply": apply_ok, "advance_checked": int(2 * sum(len(b) for b in batches)),
+                "advance": advance_ok}
 
     def fresh_logits(self, seed):
         """Unmasked logits (the rotating buffers are masked in place by the timed
@@ -450,6 +534,7 @@ class Bench:
             "advance_us": round(advance_us, 3),
             "advance_us_eager": round(advance_eager_us, 3),
             "apply_us_graph": round(apply_graph_us, 3),
+            "bit_exact": self.parity(h, ids),
         }
         if res["compile_ms"]["one_set_warm"] is not None:
             print(f"[bench] {rep}: one set alone compiles in {res['compile_ms']['one_set_warm']:.3f} ms (warm)", flush=True)
@@ -542,6 +627,7 @@ class Bench:
             del g
             return float(np.median(ts))
 
+        exact = self.parity(hz, ids0)
         cold, warm, ref = run(hz, True), run(hz, False), run(h_ref, False)
         gcold, gwarm, gref = run_graph(hz, True), run_graph(hz, False), run_graph(h_ref, False)
         res = {"cache_rows": hz.cache_rows, "device_bytes": hz.device_bytes,
@@ -551,7 +637,7 @@ class Bench:
                "compile_phases": hz.timing(),
                "decode_steps": S, "batch": B, "distinct_rows": distinct,
                "step_us_cache_emptied": round(cold, 2), "step_us_cache_kept": round(warm, 2),
-               "step_us_main_repr": round(ref, 2),
+               "step_us_main_repr": round(ref, 2), "bit_exact": exact,
                "graph_replayed": {"step_us_cache_emptied": round(gcold, 2), "step_us_cache_kept": round(gwarm, 2),
                                   "step_us_main_repr": round(gref, 2)}}
         hz.close()
@@ -576,10 +662,11 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(h, w, V, N, seconds, torch, dev, esize):
-    """The oracle on a bounded sample of rows, one thread pinned to one core;
-    the same rows from the GPU must be bit-identical.  Also the oracle's apply
-    on a few rows, as GB/s of the same algorithmic bytes as the GPU apply."""
+def cpu_baseline(w, V, seconds, esize):
+    """The oracle on a bounded sample of rows, one thread pinned to one core.
+    Also the oracle's apply on a few rows, as GB/s of the same algorithmic
+    bytes as the GPU apply.  Returns the baseline, the oracle and its sampled
+    (nodes, rows), which the parity checks of every timed representation use."""
     import oracle
     prev = None
     try:
@@ -616,14 +703,12 @@ def cpu_baseline(h, w, V, N, seconds, torch, dev, esize):
     cpu = {"value": round(opps, 1), "unit": "pairs/s", "cores": 1, "kind": "oracle",
            "sample": f"{rows_done} random rows x V={V} tokens of {w.name} ({done:.1f} s, one thread"
                      f"{' pinned to one core' if prev is not None else ''}), trie build {build_s * 1e3:.0f} ms; "
-                     f"full table extrapolates to {N * V / opps:.0f} s",
+                     f"full table extrapolates to {o.N * V / opps:.0f} s",
            "apply_GBps": round(applied * (Wd * 8 + V * esize) / apply_s / 1e9, 3),
            "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
-    exact = True
-    for nodes, rows in sample[:8]:
-        got = h.export_rows(torch.as_tensor(nodes, device=dev)).cpu().numpy().view(np.uint64)
-        exact = exact and bool(np.array_equal(got, rows))
-    return cpu, exact
+    nodes = np.concatenate([n for n, _ in sample])
+    rows = np.concatenate([r for _, r in sample])
+    return cpu, o, (nodes, rows)
 
 
 def main():
@@ -653,7 +738,11 @@ def main():
     print(f"[bench] workload {w.name}: K={K} V={V} B={B} ({gen_s:.1f}s to generate)", flush=True)
 
     bench = Bench(args, torch, P, W, w, dev)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu, bench.oracle, bench.sample = cpu_baseline(w, V, args.cpu_seconds, bench.esize)
     h, main_res = bench.measure(rep, args.steps, args.warmup, cold_runs=5)
+    structure = bench.structure(h)
 
     # achievable write bandwidth on this device: a 4 GiB fill
     fill = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
@@ -675,9 +764,6 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    cpu, exact = (None, None)
-    if not args.no_cpu_baseline:
-        cpu, exact = cpu_baseline(h, w, V, main_res["N"], args.cpu_seconds, torch, dev, bench.esize)
     lazy = None if args.no_secondary else bench.measure_lazy(h)
     h.close()
 
@@ -744,6 +830,7 @@ def main():
                            python_vocabulary_packing=round(bench.vocab_pack_ms, 3)),
         "apply": main_res["apply"],
         "compile_work": main_res["compile_work"],
+        "structure": structure,
         "advance_us": main_res["advance_us"],
         "advance_us_eager": main_res["advance_us_eager"],
         "apply_us_graph": main_res["apply_us_graph"],
@@ -752,7 +839,12 @@ def main():
         "lazy_rows": lazy,
         "char_position_masks": formats,
         "fill_GBps_4GiB": round(fill_gbps, 1),
-        "bit_exact_sampled_rows": exact,
+        "bit_exact": {"oracle_sample": None if bench.sample is None else
+                      f"{len(bench.sample[0])} oracle rows drawn uniformly over the trie; apply and advance on the "
+                      f"timed batch and on {B} sampled rows",
+                      rep: main_res["bit_exact"],
+                      "tail": None if secondary is None else secondary["bit_exact"],
+                      "lazy": None if lazy is None else lazy["bit_exact"]},
         "kernels_sha": sha,
     }
     for key in ("roofline", "roofline_apply"):  # against the measured fill as well

@@ -49,8 +49,16 @@
  *
  * Errors: every entry point returns a tam_status; a negative status leaves a
  * message in tam_last_error() (thread-local).  No exception crosses the ABI.
- * Per-row conditions on the device (dead or out-of-range ids) are not errors.
- * An asynchronous HIP failure surfaces as TAM_E_DEVICE on a later call.
+ * Argument errors (TAM_E_INVAL) are reported before the handle's state
+ * (TAM_E_STATE).  Per-row conditions on the device (dead or out-of-range ids)
+ * are not errors.  An asynchronous HIP failure surfaces as TAM_E_DEVICE on a
+ * later call.  The kernels that lay the trie out on the device, and the row
+ * cache of TAM_FLAG_LAZY_ROWS, count any table entry or cache state that is
+ * inconsistent (the library's own build makes none) instead of following it;
+ * the count is copied back at the end of tam_compile and tam_rebuild (not
+ * under stream capture), and once it is non-zero every later tam_apply_mask,
+ * tam_advance, tam_export_rows, tam_rebuild and tam_valid_pairs call on the
+ * handle returns TAM_E_DEVICE.
  */
 #ifndef TAM_H
 #define TAM_H
@@ -72,7 +80,7 @@ typedef enum {
     TAM_E_INVAL = -1,      /* bad argument (null pointer, negative size, bad dtype, ...) */
     TAM_E_TERMINATOR = -2, /* a set string contains the terminator byte */
     TAM_E_NOMEM = -3,      /* host allocation, a host thread or the device allocator failed */
-    TAM_E_DEVICE = -4,     /* a HIP call failed */
+    TAM_E_DEVICE = -4,     /* a HIP call failed, or the device met inconsistent trie tables */
     TAM_E_TOOLARGE = -5,   /* sizes beyond the 32-bit index limits of the tables */
     TAM_E_STATE = -6       /* operation not available for this handle (see flags) */
 } tam_status;
@@ -300,8 +308,40 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream);
  * tam_destroy does not wait for replays still running: synchronise first).
  * tam_valid_pairs and tam_timing_get synchronise and must not be captured. */
 
-/* tam_info_get -- sizes and host tables of a handle (no device access). */
+/* tam_info_get -- sizes and host tables of a handle (no device access).  The
+ * dense table it names holds one bitmask row per node (appendix "GPU-Based
+ * Masking Considerations": the masks are kept as per-node bitmasks on the GPU),
+ * or per branching node with TAM_FLAG_TAIL_LISTS. */
 tam_status tam_info_get(const tam_handle *h, tam_info *out);
+
+/* Position tables of a trie as the device lays them out on a device compile
+ * (Section 4.1: one node per distinct prefix, every string written once into a
+ * blob in trie order).  All arrays are host memory owned by the handle. */
+typedef struct {
+    int64_t blob_bytes;
+    const uint8_t *blob;      /* [blob_bytes]: 32 zero bytes; then for each set in order, for each
+                                 of its distinct strings in node-id (trie) order, a zero pad byte,
+                                 the string's bytes and the terminator; then 32 zero bytes */
+    const int32_t *node_at;   /* [blob_bytes] node whose edge byte sits at that position; a pad
+                                 byte stands for its set's root, the outer pads for root 0 */
+    const int32_t *depth;     /* [N] prefix length (-1 for a node no record reaches) */
+    const int32_t *node_pos;  /* [N] first position of the node's edge byte; -1 at roots */
+    const int32_t *parent;    /* [N] node_at[node_pos - 1]; -1 at roots and unplaced nodes */
+    int64_t errors;           /* inconsistent string records or positions met (0 for the
+                                 library's own build; on the device the same count makes later
+                                 calls return TAM_E_DEVICE) */
+} tam_layout;
+
+/*
+ * tam_layout_get -- the device's trie layout computed on the host: the same
+ * functions the layout kernels run on the device (node_at and depth from one
+ * record per string, first positions, parents), run over the same records, so
+ * that the layout can be checked without a GPU.  Only for TAM_FLAG_HOST_ONLY
+ * handles of string sets (else TAM_E_STATE); computed at the first call, kept
+ * until tam_destroy.  Errors: TAM_E_INVAL (null argument), TAM_E_STATE,
+ * TAM_E_NOMEM.
+ */
+tam_status tam_layout_get(const tam_handle *h, tam_layout *out);
 
 /*
  * tam_apply_mask -- Eq. 1 with the precomputed masks: for every row b in
@@ -316,7 +356,10 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out);
  *               (-inf = 0xFF800000) or TAM_DTYPE_BF16 (-inf = 0xFF80).
  *   row_stride  elements between rows, >= V.
  * Rows whose base is 16-byte aligned take the vector path; any other layout is
- * still handled (element path).  B = 0 is a no-op.  With TAM_FLAG_LAZY_ROWS the
+ * still handled (element path).  B = 0 is a no-op.
+ * Errors: TAM_E_INVAL (B < 0, a null pointer with B > 0, dtype not FP32 or
+ * BF16, row_stride < V, logits not aligned to their element size),
+ * TAM_E_STATE (host-only handle), TAM_E_DEVICE.  With TAM_FLAG_LAZY_ROWS the
  * rows of nodes missing from the row cache are built first (see the flag), in
  * groups of at most min(1024, cache rows) batch rows.
  */
@@ -335,10 +378,30 @@ tam_status tam_advance(const tam_handle *h, const int32_t *node_ids, const int32
 /*
  * tam_export_rows -- canonical mask rows of n nodes: out is device
  * uint64[n][W] (W = words_per_row); row r is the mask of node_ids[r], or all
- * zero when node_ids[r] is dead or out of range.
+ * zero when node_ids[r] is dead or out of range.  The canonical row is this
+ * interface's reading of the appendix's "GPU-Based Masking Considerations"
+ * (one bitmask per trie node, a bit per vocabulary token), whatever the
+ * handle keeps internally (dense rows, tails read back from the probe hits,
+ * sparse lists, or rows built on demand).
+ *   node_ids  device int32[n]; out  device, 8-byte aligned, written whole.
+ * Errors: TAM_E_INVAL (null pointer with n > 0, n < 0, misaligned out),
+ * TAM_E_STATE (host-only handle), TAM_E_DEVICE.
  */
 tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t n, uint64_t *out,
                            void *stream);
+
+/*
+ * tam_valid_counts -- out[r] = |valid[node_ids[r]]|, the number of token ids
+ * valid at that node (0 for a dead or out-of-range node): the valid-set sizes
+ * the appendix tabulates by trie depth ("Valid set size distribution"), and
+ * what a caller needs to choose between masking with the row and sampling
+ * from a short valid list.  Counted on the device from the handle's own rows
+ * (popcount of a dense row, a list's length, a tail's hits).
+ *   node_ids, out  device int32[n].
+ * Errors: TAM_E_INVAL, TAM_E_STATE (host-only handle, or TAM_FLAG_LAZY_ROWS:
+ * no row is kept for most nodes), TAM_E_DEVICE.
+ */
+tam_status tam_valid_counts(const tam_handle *h, const int32_t *node_ids, int64_t n, int32_t *out, void *stream);
 
 /*
  * tam_valid_pairs -- M = sum over all nodes of |valid[n]|, the number of

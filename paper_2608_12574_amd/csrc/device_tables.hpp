@@ -100,6 +100,8 @@ struct DevTables {
     const int32_t *row_at;      // [blob_bytes] row_of[node_at[p]]; equals node_at without row_of
     const int32_t *sub_end;     // [N] one past the node's subtree (rows built on demand), or null
     int32_t *scan_tmp;          // block sums of the scan
+    int32_t *err;               // [1] inconsistent table entries met on the device (0 for the host
+                                // build's tables); copied back and reported by later calls
     int64_t N, V, W, Wp;
     int64_t R;                  // dense rows (N for a full table, 0 without one)
     int32_t tail_long;          // tail compression with tokens longer than kWin: their hits on
@@ -129,6 +131,7 @@ struct LazyDev {
     int32_t *miss_row;     // [kLazyGroup] their destination rows (slots, or output rows)
     int64_t *miss_off;     // [kLazyGroup + 1] prefix sum of their subtree sizes (minus the node)
     int32_t *miss_count;   // [1]
+    int32_t *err;          // [1] the handle's device error count (see DevTables)
     int64_t C;             // cache rows
 };
 

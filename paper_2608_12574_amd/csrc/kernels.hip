@@ -34,6 +34,7 @@
 #include <climits>
 
 #include "tam_internal.hpp"
+#include "trie_layout.hpp"
 
 namespace tam {
 namespace {
@@ -823,35 +824,15 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
 // its edge byte (node_pos), and one position before sits its parent (the pad
 // byte before a string stands for the set root).  Roots have no position.
 
-// node_at and depth from the string records [s0, s1), one thread per string.
-// String u creates the nodes first .. first + len - lcp along path indices
-// lcp .. len (depth = index + 1).  Below index lcp its path is the previous
-// string's: index i belongs to the nearest earlier string v of the part with
-// lcp[v] <= i.  Walking from u - 1 along psv (each step lowers lcp), a string
-// whose lcp is below the indices still open owns [lcp[v], open bound); one
-// whose lcp is not below them owns none of them and is passed over.
+// node_at and depth from the string records [s0, s1), one thread per string
+// (lay_string); a record that does not fit the tables is counted in *err.
 __global__ void __launch_bounds__(kBlock) k_node_at(const StrRec *__restrict__ strs, int64_t s0, int64_t s1,
-                                                    int32_t *__restrict__ node_at, int32_t *__restrict__ depth) {
+                                                    int64_t blob_bytes, int64_t N, int32_t *__restrict__ node_at,
+                                                    int32_t *__restrict__ depth, int32_t *err) {
     const int64_t u = s0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (u >= s1) return;
-    const StrRec r = strs[u];
-    node_at[r.at] = r.root;  // the pad stands for the root
-    if (r.lcp == 0) depth[r.root] = 0;
-    for (int32_t i = r.lcp; i <= r.len; ++i) {
-        const int32_t g = r.first + (i - r.lcp);
-        node_at[r.at + 1 + i] = g;
-        depth[g] = i + 1;
-    }
-    int32_t hi = r.lcp;  // indices [0, hi) still open
-    int64_t v = u - 1;   // lcp > 0: not the first string of its part
-    while (hi > 0) {     // ends at a string with lcp 0, which owns all that is open
-        const StrRec q = strs[v];
-        if (q.lcp < hi) {
-            for (int32_t i = q.lcp; i < hi; ++i) node_at[r.at + 1 + i] = q.first + (i - q.lcp);
-            hi = q.lcp;
-        }
-        v = q.psv;
-    }
+    const int32_t bad = lay_string(strs, s0, u, blob_bytes, N, node_at, depth);
+    if (bad) atomicAdd(err, bad);
 }
 
 // node_pos of the nodes [n0, n1): -1 for a root, else a large value that
@@ -865,23 +846,25 @@ __global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__
 // the first position of every non-root node in the blob range [b0, b1)
 __global__ void __launch_bounds__(kBlock) k_first_pos(const int32_t *__restrict__ node_at,
                                                       const int32_t *__restrict__ depth, int64_t N, int64_t b0,
-                                                      int64_t b1, int32_t *node_pos) {
+                                                      int64_t b1, int32_t *node_pos, int32_t *err) {
     const int64_t p = b0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (p >= b1) return;
-    const int32_t g = node_at[p];
-    if ((uint32_t)g < (uint64_t)N && depth[g] > 0) atomicMin(&node_pos[g], (int32_t)p);
+    bool bad = false;
+    const int32_t g = lay_pos_node(node_at, depth, N, p, &bad);
+    if (g >= 0) atomicMin(&node_pos[g], (int32_t)p);
+    if (bad) atomicAdd(err, 1);
+}
+
+// The parent of non-root node g (lay_parent), or -1 after counting an
+// inconsistent position in t.err.
+__device__ __forceinline__ int32_t parent_of(const DevTables &t, int64_t g) {
+    bool bad = false;
+    const int32_t par = lay_parent(t.node_pos, t.node_at, t.N, t.blob_bytes, g, &bad);
+    if (bad) atomicAdd(t.err, 1);
+    return par;
 }
 
 // children per node (cnt zeroed before)
-// The parent of non-root node g, or -1 if g has no position (which the
-// uploaded tables rule out; the check keeps a bad table from faulting).
-__device__ __forceinline__ int32_t parent_of(const DevTables &t, int64_t g) {
-    const int64_t pos = t.node_pos[g];
-    if (pos <= 0 || pos >= t.blob_bytes) return -1;
-    const int32_t par = t.node_at[pos - 1];
-    return (uint32_t)par < (uint64_t)t.N ? par : -1;
-}
-
 __global__ void __launch_bounds__(kBlock) k_child_count(DevTables t, int32_t *cnt) {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= t.N || t.depth[g] == 0) return;
@@ -895,7 +878,8 @@ __global__ void __launch_bounds__(kBlock) k_child_fill(DevTables t, int32_t *cur
                                                        uint8_t *child_byte) {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= t.N || t.depth[g] == 0) return;
-    const int32_t par = parent_of(t, g);
+    bool bad = false;  // counted once, by k_child_count
+    const int32_t par = lay_parent(t.node_pos, t.node_at, t.N, t.blob_bytes, g, &bad);
     if (par < 0) return;
     const int32_t slot = t.child_off[par] + atomicAdd(&cursor[par], 1);
     child_node[slot] = (int32_t)g;
@@ -1083,6 +1067,34 @@ __global__ void __launch_bounds__(kBlock) k_export_tail(DevTables t, const int32
         for (int32_t k = t.row_ptr[n] + lane; k < t.row_ptr[n + 1]; k += kWave) set(t.entries[k]);
 }
 
+// |valid[n]| of the requested nodes, one wave per node: the popcount of its
+// dense row, the length of its list, or (a tail) its hits along the path plus
+// its long tokens' list; 0 for a dead node.  The same sources as k_apply.
+__global__ void __launch_bounds__(kBlock) k_row_counts(DevTables t, const int32_t *nodes, int64_t nrows,
+                                                       int32_t *out) {
+    const int64_t r = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (r >= nrows) return;  // uniform over the wave
+    const int32_t n = nodes[r];
+    int32_t c = 0;
+    if (n >= 0 && (int64_t)n < t.N) {
+        const int64_t trow = t.table ? (t.row_of ? (int64_t)t.row_of[n] : (int64_t)n) : -1;
+        if (trow >= 0) {
+            const uint64_t *row = t.table + trow * t.Wp;
+            for (int64_t w = lane; w < t.W; w += kWave) c += __popcll(row[w]);
+        } else {
+            if (t.table) {  // a tail: the token of length d starting below it is the hit of node n + d
+                const int Lt = min(min(-1 - (int)trow, kWin), (int)t.max_len);
+                const int32_t x = lane < Lt ? t.hits[(int64_t)lane * t.N + n + lane + 1] : -1;
+                c = x >= 0 ? 1 : (x <= -2 ? (int32_t)t.pay[-2 - x].count : 0);
+            }
+            if ((!t.table || t.tail_long) && lane == 0) c += t.row_ptr[n + 1] - t.row_ptr[n];
+        }
+    }
+    for (int o = kWave / 2; o > 0; o >>= 1) c += __shfl_xor(c, o, kWave);
+    if (lane == 0) out[r] = c;
+}
+
 // -------------------------------------------------------- rows on demand ---
 
 constexpr int kLazyProbeBlocks = 512;  // grid of k_lazy_probe (grid-stride)
@@ -1237,7 +1249,10 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
                 z.slot_of[n] = c;
                 store_wg(&z.ref[c], 1u);
             } else {
-                z.slot_of[n] = -1;  // not reached while nb <= C; the rows stay fully masked
+                // not reached while nb <= C (two turns of the hand find the
+                // slots); counted as an error, the rows stay fully masked
+                z.slot_of[n] = -1;
+                atomicAdd(z.err, 1);
             }
             s_slot[tid] = c;
         }
@@ -1367,10 +1382,11 @@ hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStr
     return hipGetLastError();
 }
 
-hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int32_t *node_at, int32_t *depth,
-                          hipStream_t s) {
+hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int64_t blob_bytes, int64_t N,
+                          int32_t *node_at, int32_t *depth, int32_t *err, hipStream_t s) {
     if (s1 <= s0) return hipSuccess;
-    hipLaunchKernelGGL(k_node_at, dim3(grid_for(s1 - s0, kBlock)), dim3(kBlock), 0, s, strs, s0, s1, node_at, depth);
+    hipLaunchKernelGGL(k_node_at, dim3(grid_for(s1 - s0, kBlock)), dim3(kBlock), 0, s, strs, s0, s1, blob_bytes, N,
+                       node_at, depth, err);
     return hipGetLastError();
 }
 
@@ -1381,7 +1397,7 @@ hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, in
         hipLaunchKernelGGL(k_pos_init, dim3(grid_for(n1 - n0, kBlock)), dim3(kBlock), 0, s, t.depth, n0, n1, node_pos);
     if (b1 > b0)
         hipLaunchKernelGGL(k_first_pos, dim3(grid_for(b1 - b0, kBlock)), dim3(kBlock), 0, s, t.node_at, t.depth, t.N,
-                           b0, b1, node_pos);
+                           b0, b1, node_pos, t.err);
     return hipGetLastError();
 }
 
@@ -1567,6 +1583,12 @@ hipError_t launch_lazy_reset(const DevTables &t, const LazyDev &z, hipStream_t s
     if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.ref), z.C, 0, s);
     if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.state), 2, 0, s);
     return e;
+}
+
+hipError_t launch_row_counts(const DevTables &t, const int32_t *node_ids, int64_t n, int32_t *out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_row_counts, dim3(grid_for(n, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, n, out);
+    return hipGetLastError();
 }
 
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,

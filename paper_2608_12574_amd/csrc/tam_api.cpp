@@ -14,6 +14,7 @@
 
 #include "host_build.hpp"
 #include "tam_internal.hpp"
+#include "trie_layout.hpp"
 
 namespace tam {
 
@@ -79,6 +80,52 @@ bool pinned_give(void *p) {
 
 PinnedScope::PinnedScope(bool on) : prev(t_pinned) { t_pinned = on; }
 PinnedScope::~PinnedScope() { t_pinned = prev; }
+
+namespace {
+
+constexpr int kErrSlots = 4096;
+
+struct ErrSlots {
+    std::mutex m;
+    int32_t *base = nullptr;
+    std::vector<int> free_slots;
+    bool tried = false;
+};
+
+// Never destroyed: handles destroyed at exit hand their slots back.
+ErrSlots &err_slots() {
+    static ErrSlots *p = new ErrSlots();
+    return *p;
+}
+
+}  // namespace
+
+int32_t *err_slot_take() {
+    ErrSlots &E = err_slots();
+    std::lock_guard<std::mutex> g(E.m);
+    if (!E.tried) {
+        E.tried = true;
+        void *p = nullptr;
+        if (hipHostMalloc(&p, kErrSlots * sizeof(int32_t), hipHostMallocPortable) == hipSuccess && p) {
+            E.base = static_cast<int32_t *>(p);
+            for (int i = kErrSlots - 1; i >= 0; --i) E.free_slots.push_back(i);
+        } else {
+            (void)hipGetLastError();
+        }
+    }
+    if (E.free_slots.empty()) return nullptr;
+    int32_t *slot = E.base + E.free_slots.back();
+    E.free_slots.pop_back();
+    *slot = 0;
+    return slot;
+}
+
+void err_slot_give(int32_t *slot) {
+    if (!slot) return;
+    ErrSlots &E = err_slots();
+    std::lock_guard<std::mutex> g(E.m);
+    E.free_slots.push_back((int)(slot - E.base));
+}
 
 }  // namespace tam
 
@@ -253,6 +300,9 @@ void release_device(tam_handle *h) {
     if (h->have_events) (void)hipEventSynchronize(h->ev[3]);
     for (void *p : h->dev_ptrs) free_with(h->own_alloc, h->alloc, p);
     h->dev_ptrs.clear();
+    tam::err_slot_give(h->h_err);  // its last copy is behind work_done
+    h->h_err = nullptr;
+    h->d_err = nullptr;
     if (h->have_events)
         for (hipEvent_t &e : h->ev) (void)hipEventDestroy(e);
     if (h->work_done) (void)hipEventDestroy(h->work_done);
@@ -289,6 +339,23 @@ unsigned default_phases(const tam_handle *h) {
     return (keeps_lists(h) ? unsigned(TAM_PHASE_LISTS) : 0u) | (h->dt.table ? unsigned(TAM_PHASE_TABLE) : 0u);
 }
 
+// The handle's device error count into its pinned host word (not under
+// stream capture: a graph carries kernels only).
+hipError_t copy_errors(const tam_handle *h, hipStream_t s, bool capturing) {
+    if (!h->h_err || !h->d_err || capturing) return hipSuccess;
+    return hipMemcpyAsync(h->h_err, h->d_err, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+}
+
+// TAM_E_DEVICE once a copied-back count shows that the device met
+// inconsistent table entries (the host build never makes them).
+tam_status device_errors(const tam_handle *h) {
+    const int32_t n = h->h_err ? __atomic_load_n(h->h_err, __ATOMIC_ACQUIRE) : 0;
+    if (n == 0) return TAM_OK;
+    return fail(TAM_E_DEVICE, "the device met " + std::to_string(n) +
+                                  " inconsistent trie-table entries or cache states; results of this handle are "
+                                  "not valid");
+}
+
 // The device part of compile, on the caller's stream: zero fill of the table,
 // the probe pass (marks into the table, counts for the lists), then the lists'
 // prefix sum and fill.  Phase events are recorded only for the handle's
@@ -314,6 +381,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
             TAM_HIP(hipEventRecord(h->ev[3], s));
             h->events_recorded = true;
         }
+        TAM_HIP(copy_errors(h, s, capturing));
         if (h->work_done && !capturing) TAM_HIP(hipEventRecord(h->work_done, s));
         return TAM_OK;
     }
@@ -348,6 +416,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
         TAM_HIP(hipEventRecord(h->ev[3], s));
         h->events_recorded = true;
     }
+    TAM_HIP(copy_errors(h, s, capturing));
     if (h->work_done && !capturing) TAM_HIP(hipEventRecord(h->work_done, s));
     return TAM_OK;
 }
@@ -447,7 +516,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // by group, right after each group's upload (a node's ancestors are in its
     // own set), so only the last group's counts follow the host build.
     const bool early_count = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & TAM_FLAG_LAZY_ROWS);
-    size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0, o_strs = 0;
+    size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0, o_strs = 0, o_err = 0;
     tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
     double hook_ms = 0;     // time spent in the two hooks (allocation and enqueue)
@@ -481,6 +550,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_strs = ta.take<tam::StrRec>(hh->K_unique);
         o_tmp = ta.take<int32_t>(hh->N);  // scratch of the child lists' build
         o_scan_tmp = ta.take<int32_t>(tam::scan_tmp_elems(hh->N));
+        o_err = ta.take<int32_t>(1);
         trie_base = static_cast<uint8_t *>(dev_alloc(hh, ta.used));
         if (!trie_base) {
             err = "device allocation failed (" + std::to_string(ta.used) + " bytes requested)";
@@ -489,9 +559,13 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         hh->device_bytes = (int64_t)ta.used;
         set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
                         o_child_node);
-        {  // the blob's outer pads stand for the first set's root
+        hh->d_err = reinterpret_cast<int32_t *>(trie_base + o_err);
+        hh->h_err = tam::err_slot_take();
+        te.err = hh->d_err;
+        {  // the blob's outer pads stand for the first set's root; no device error yet
             int32_t *node_at = reinterpret_cast<int32_t *>(trie_base + o_node_at);
-            hipError_t e = tam::launch_fill_i32(node_at, tam::kBlobPad, 0, s);
+            hipError_t e = tam::launch_fill_i32(hh->d_err, 1, 0, s);
+            if (e == hipSuccess) e = tam::launch_fill_i32(node_at, tam::kBlobPad, 0, s);
             if (e == hipSuccess) e = tam::launch_fill_i32(node_at + hh->blob_bytes - tam::kBlobPad, tam::kBlobPad, 0, s);
             enqueued = true;
             if (e != hipSuccess) {
@@ -562,8 +636,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         int32_t *node_pos = reinterpret_cast<int32_t *>(trie_base + o_node_pos);
         if (e == hipSuccess)
             e = tam::launch_node_at(reinterpret_cast<const tam::StrRec *>(trie_base + o_strs), r.s_lo, r.s_hi,
-                                    reinterpret_cast<int32_t *>(trie_base + o_node_at),
-                                    reinterpret_cast<int32_t *>(trie_base + o_depth), s);
+                                    hh->blob_bytes, hh->N, reinterpret_cast<int32_t *>(trie_base + o_node_at),
+                                    reinterpret_cast<int32_t *>(trie_base + o_depth), hh->d_err, s);
         if (e == hipSuccess) e = tam::launch_node_pos(te, node_pos, r.n_lo, r.n_hi, r.b_lo, r.b_hi, s);
         if (early_count && e == hipSuccess) {
             const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
@@ -686,6 +760,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     tam::DevTables &t = h->dt;
     set_trie_tables(t, h, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
                     o_child_node);
+    t.err = h->d_err;
     t.hits = early_count ? te.hits : reinterpret_cast<int32_t *>(base + o_hits_b);
     t.count = early_count ? te.count : reinterpret_cast<int32_t *>(base + o_count_b);
     t.row_ptr = reinterpret_cast<int32_t *>(base + o_row_ptr);
@@ -707,6 +782,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         z.miss_row = reinterpret_cast<int32_t *>(base + o_miss_row);
         z.miss_off = reinterpret_cast<int64_t *>(base + o_miss_off);
         z.miss_count = reinterpret_cast<int32_t *>(base + o_miss_count);
+        z.err = h->d_err;
         z.C = C;
     }
     t.tail_span = tails ? reinterpret_cast<const int32_t *>(trie_base + o_tail_span) : nullptr;
@@ -814,6 +890,7 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
     Arena a;
     const size_t o_cls = a.take<uint8_t>(32 * L);
     const size_t o_pairs = a.take<int32_t>(h->npairs);
+    const size_t o_err = a.take<int32_t>(1);
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     const size_t table_bytes = (size_t)N * (size_t)h->Wp * sizeof(uint64_t);
     uint64_t *table = base ? static_cast<uint64_t *>(dev_alloc(h, table_bytes)) : nullptr;
@@ -845,7 +922,11 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
     t.terminator = T;
     t.classes = base + o_cls;
     t.fmt_L = (int32_t)L;
+    h->d_err = reinterpret_cast<int32_t *>(base + o_err);
+    h->h_err = tam::err_slot_take();
+    t.err = h->d_err;
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
+    if (e == hipSuccess) e = tam::launch_fill_i32(h->d_err, 1, 0, s);
     if (e == hipSuccess) e = hipMemcpyAsync(base + o_cls, h->classes.data(), h->classes.size(),
                                             hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
@@ -863,9 +944,59 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
     return TAM_OK;
 }
 
+// The device's trie layout on the host (tam_layout_get): the layout kernels'
+// functions over the host's string records, in one pass each.
+void layout_on_host(tam_handle *h) {
+    const int64_t BB = h->blob_bytes, N = h->N;
+    h->lay_node_at.assign((size_t)BB, 0);  // the outer pads stand for root 0, as on the device
+    h->lay_depth.assign((size_t)N, -1);
+    h->lay_node_pos.assign((size_t)N, -1);
+    h->lay_parent.assign((size_t)N, -1);
+    int32_t *node_at = h->lay_node_at.data(), *depth = h->lay_depth.data();
+    int32_t *node_pos = h->lay_node_pos.data(), *parent = h->lay_parent.data();
+    int64_t errors = 0;
+    const int64_t K = (int64_t)h->strs.size();
+    for (int64_t u = 0; u < K; ++u) errors += tam::lay_string(h->strs.data(), 0, u, BB, N, node_at, depth);
+    for (int64_t g = 0; g < N; ++g) node_pos[g] = depth[g] == 0 ? -1 : INT32_MAX;
+    for (int64_t p = 0; p < BB; ++p) {
+        bool bad = false;
+        const int32_t g = tam::lay_pos_node(node_at, depth, N, p, &bad);
+        if (g >= 0 && p < node_pos[g]) node_pos[g] = (int32_t)p;
+        errors += bad ? 1 : 0;
+    }
+    for (int64_t g = 0; g < N; ++g) {
+        if (depth[g] == 0) continue;
+        bool bad = false;
+        parent[g] = tam::lay_parent(node_pos, node_at, N, BB, g, &bad);
+        errors += bad ? 1 : 0;
+    }
+    h->lay_errors = errors;
+}
+
 }  // namespace
 
 extern "C" {
+
+tam_status tam_layout_get(const tam_handle *h, tam_layout *out) {
+    g_err.clear();
+    if (!h || !out) return fail(TAM_E_INVAL, "null argument");
+    if (!(h->flags & TAM_FLAG_HOST_ONLY) || h->fmt_L >= 0)
+        return fail(TAM_E_STATE, "the host layout is kept for TAM_FLAG_HOST_ONLY handles of string sets");
+    tam_handle *m = const_cast<tam_handle *>(h);  // computed once, then read-only
+    try {
+        std::call_once(m->layout_once, [m] { layout_on_host(m); });
+    } catch (const std::bad_alloc &) {
+        return fail(TAM_E_NOMEM, "out of host memory");
+    }
+    out->blob_bytes = h->blob_bytes;
+    out->blob = h->blob.data();
+    out->node_at = h->lay_node_at.data();
+    out->depth = h->lay_depth.data();
+    out->node_pos = h->lay_node_pos.data();
+    out->parent = h->lay_parent.data();
+    out->errors = h->lay_errors;
+    return TAM_OK;
+}
 
 const char *tam_last_error(void) { return g_err.c_str(); }
 
@@ -928,6 +1059,7 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
 tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
     g_err.clear();
     tam_status st = check_device_handle(h);
+    if (st == TAM_OK) st = device_errors(h);
     if (st != TAM_OK) return st;
     if (is_lazy(h)) {
         if (phases != 0) return fail(TAM_E_STATE, "a handle with rows built on demand has only phase 0 (cache reset)");
@@ -972,15 +1104,17 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
 tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t B, void *logits,
                           int dtype, int64_t row_stride, void *stream) {
     g_err.clear();
-    tam_status st = check_device_handle(h);
-    if (st != TAM_OK) return st;
+    // argument errors first, then the handle's state
+    if (!h) return fail(TAM_E_INVAL, "null handle");
     if (B < 0) return fail(TAM_E_INVAL, "B must be >= 0");
-    if (B == 0) return TAM_OK;
-    if (!node_ids || !logits) return fail(TAM_E_INVAL, "null device pointer");
     if (dtype != TAM_DTYPE_FP32 && dtype != TAM_DTYPE_BF16) return fail(TAM_E_INVAL, "dtype must be FP32 or BF16");
     if (row_stride < h->V) return fail(TAM_E_INVAL, "row_stride must be >= V");
     const size_t elem = dtype == TAM_DTYPE_BF16 ? 2 : 4;
+    if (B > 0 && (!node_ids || !logits)) return fail(TAM_E_INVAL, "null device pointer");
     if ((reinterpret_cast<uintptr_t>(logits) % elem) != 0) return fail(TAM_E_INVAL, "logits are not element-aligned");
+    tam_status st = check_device_handle(h);
+    if (st == TAM_OK) st = device_errors(h);
+    if (st != TAM_OK || B == 0) return st;
     TAM_HIP(hipGetLastError());
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (is_lazy(h)) {  // groups of rows: cache lookup, missing rows built, masking
@@ -998,11 +1132,12 @@ tam_status tam_apply_mask(const tam_handle *h, const int32_t *node_ids, int64_t 
 tam_status tam_advance(const tam_handle *h, const int32_t *node_ids, const int32_t *token_ids, int64_t B,
                        int32_t *out, void *stream) {
     g_err.clear();
-    tam_status st = check_device_handle(h);
-    if (st != TAM_OK) return st;
+    if (!h) return fail(TAM_E_INVAL, "null handle");
     if (B < 0) return fail(TAM_E_INVAL, "B must be >= 0");
-    if (B == 0) return TAM_OK;
-    if (!node_ids || !token_ids || !out) return fail(TAM_E_INVAL, "null device pointer");
+    if (B > 0 && (!node_ids || !token_ids || !out)) return fail(TAM_E_INVAL, "null device pointer");
+    tam_status st = check_device_handle(h);
+    if (st == TAM_OK) st = device_errors(h);
+    if (st != TAM_OK || B == 0) return st;
     TAM_HIP(hipGetLastError());
     TAM_HIP(tam::launch_advance(h->dt, node_ids, token_ids, B, out, static_cast<hipStream_t>(stream)));
     return TAM_OK;
@@ -1011,12 +1146,13 @@ tam_status tam_advance(const tam_handle *h, const int32_t *node_ids, const int32
 tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t n, uint64_t *out,
                            void *stream) {
     g_err.clear();
-    tam_status st = check_device_handle(h);
-    if (st != TAM_OK) return st;
+    if (!h) return fail(TAM_E_INVAL, "null handle");
     if (n < 0) return fail(TAM_E_INVAL, "n must be >= 0");
-    if (n == 0) return TAM_OK;
-    if (!node_ids || !out) return fail(TAM_E_INVAL, "null device pointer");
+    if (n > 0 && (!node_ids || !out)) return fail(TAM_E_INVAL, "null device pointer");
     if ((reinterpret_cast<uintptr_t>(out) & 7) != 0) return fail(TAM_E_INVAL, "out must be 8-byte aligned");
+    tam_status st = check_device_handle(h);
+    if (st == TAM_OK) st = device_errors(h);
+    if (st != TAM_OK || n == 0) return st;
     TAM_HIP(hipGetLastError());
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (is_lazy(h)) {
@@ -1032,6 +1168,22 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
     return TAM_OK;
 }
 
+tam_status tam_valid_counts(const tam_handle *h, const int32_t *node_ids, int64_t n, int32_t *out, void *stream) {
+    g_err.clear();
+    if (!h) return fail(TAM_E_INVAL, "null handle");
+    if (n < 0) return fail(TAM_E_INVAL, "n must be >= 0");
+    if (n > 0 && (!node_ids || !out)) return fail(TAM_E_INVAL, "null device pointer");
+    tam_status st = check_device_handle(h);
+    if (st == TAM_OK) st = device_errors(h);
+    if (st != TAM_OK) return st;
+    if (is_lazy(h)) return fail(TAM_E_STATE, "rows built on demand keep no per-node valid sets");
+    if (!h->dt.table && !h->lists_built) return fail(TAM_E_STATE, "the handle's valid lists are not built");
+    if (n == 0) return TAM_OK;
+    TAM_HIP(hipGetLastError());
+    TAM_HIP(tam::launch_row_counts(h->dt, node_ids, n, out, static_cast<hipStream_t>(stream)));
+    return TAM_OK;
+}
+
 tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     g_err.clear();
     tam_status st = check_device_handle(h);
@@ -1041,12 +1193,15 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     // a table's marks count every pair (tails' too); without one the lists do
     std::vector<int32_t> part(h->dt.table ? (size_t)h->npairs : 0);
-    int32_t listed = 0;
+    int32_t listed = 0, errors = 0;
     if (h->dt.table)
         TAM_HIP(hipMemcpyAsync(part.data(), h->pairs, part.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     else
         TAM_HIP(hipMemcpyAsync(&listed, h->dt.row_ptr + h->N, sizeof(listed), hipMemcpyDeviceToHost, s));
+    if (h->d_err) TAM_HIP(hipMemcpyAsync(&errors, h->d_err, sizeof(errors), hipMemcpyDeviceToHost, s));
     TAM_HIP(hipStreamSynchronize(s));
+    if (errors != 0)
+        return fail(TAM_E_DEVICE, "the device met " + std::to_string(errors) + " inconsistent trie-table entries");
     int64_t m = listed;
     for (int32_t x : part) m += x;
     *out = m;

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 #include <cstdint>
 #include <string>
 #include <type_traits>
@@ -31,6 +32,13 @@ struct PinnedScope {
     PinnedScope &operator=(const PinnedScope &) = delete;
     bool prev;
 };
+
+// Pinned host words into which a handle's device error count is copied back
+// (process-wide array, one slot per handle for its life); null when no slot
+// is free or pinning fails, and the count is then only read back by calls
+// that synchronise.
+int32_t *err_slot_take();
+void err_slot_give(int32_t *slot);
 
 // An allocator whose value-initialisation (vector::resize) leaves elements of
 // trivial types unset, so that large host tables are first touched by the
@@ -73,8 +81,8 @@ hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pair
 hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s);
 // node_at and depth of the string records [s0, s1) (records uploaded; the
 // strings' earlier part-mates with shorter prefixes are in the same range)
-hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int32_t *node_at, int32_t *depth,
-                          hipStream_t s);
+hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int64_t blob_bytes, int64_t N,
+                          int32_t *node_at, int32_t *depth, int32_t *err, hipStream_t s);
 // node_pos of the nodes [n0, n1) from the blob range [b0, b1) they were
 // written in (node_at and depth of those ranges uploaded)
 hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
@@ -99,6 +107,8 @@ int64_t format_blocks(int64_t Wp);
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
                                hipStream_t s);
 int64_t scan_tmp_elems(int64_t N);
+// out[r] = |valid[node_ids[r]]| (0 for a dead node); not for rows built on demand
+hipError_t launch_row_counts(const DevTables &t, const int32_t *node_ids, int64_t n, int32_t *out, hipStream_t s);
 // one group of nb <= min(kLazyGroup, C) batch rows: cache lookup and
 // replacement, rows of the misses built in the cache, then the masking
 hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t *node_ids, int64_t nb,
@@ -189,4 +199,12 @@ struct tam_handle {
     bool events_recorded = false;
     hipEvent_t work_done = nullptr;  // end of the last upload / device phase
     tam_timing timing{};
+    // inconsistent table entries met on the device (DevTables::err), and the
+    // pinned host word the compile and rebuild calls copy the count into
+    int32_t *d_err = nullptr;
+    int32_t *h_err = nullptr;
+    // tam_layout_get: the position tables laid out on the host
+    std::once_flag layout_once;
+    tam::hvec<int32_t> lay_node_at, lay_depth, lay_node_pos, lay_parent;
+    int64_t lay_errors = 0;
 };

@@ -15,7 +15,9 @@ import os
 import numpy as np
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libtam.so")
+# TAM_LIBRARY names another build of the same library (e.g. the host-sanitized
+# one of ``build.py --sanitize``); the default is the in-tree build.
+LIB_PATH = os.environ.get("TAM_LIBRARY") or os.path.join(PKG, "libtam.so")
 
 TAM_OK = 0
 TAM_DEAD = -1
@@ -29,8 +31,9 @@ STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOM
 
 # the entry points declared in include/tam.h
 ENTRY_POINTS = ("tam_compile", "tam_vocab_create", "tam_compile_vocab", "tam_compile_format", "tam_rebuild",
-                "tam_info_get",
-                "tam_apply_mask", "tam_advance", "tam_export_rows", "tam_valid_pairs", "tam_timing_get",
+                "tam_info_get", "tam_layout_get",
+                "tam_apply_mask", "tam_advance", "tam_export_rows", "tam_valid_counts", "tam_valid_pairs",
+                "tam_timing_get",
                 "tam_vocab_destroy", "tam_destroy", "tam_last_error")
 
 
@@ -63,6 +66,13 @@ class Info(ctypes.Structure):
                 ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p),
                 ("dense_rows", ctypes.c_int64), ("dense_row", ctypes.POINTER(ctypes.c_int32)),
                 ("cache_rows", ctypes.c_int64), ("subtree_end", ctypes.POINTER(ctypes.c_int32))]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("blob_bytes", ctypes.c_int64), ("blob", ctypes.POINTER(ctypes.c_uint8)),
+                ("node_at", ctypes.POINTER(ctypes.c_int32)), ("depth", ctypes.POINTER(ctypes.c_int32)),
+                ("node_pos", ctypes.POINTER(ctypes.c_int32)), ("parent", ctypes.POINTER(ctypes.c_int32)),
+                ("errors", ctypes.c_int64)]
 
 
 class Timing(ctypes.Structure):
@@ -99,9 +109,11 @@ def lib() -> ctypes.CDLL:
         L.tam_vocab_destroy.restype = None
         L.tam_rebuild.argtypes = [P, ctypes.c_uint, P]
         L.tam_info_get.argtypes = [P, ctypes.POINTER(Info)]
+        L.tam_layout_get.argtypes = [P, ctypes.POINTER(Layout)]
         L.tam_apply_mask.argtypes = [P, P, i64, P, ctypes.c_int, i64, P]
         L.tam_advance.argtypes = [P, P, P, i64, P, P]
         L.tam_export_rows.argtypes = [P, P, i64, P, P]
+        L.tam_valid_counts.argtypes = [P, P, i64, P, P]
         L.tam_valid_pairs.argtypes = [P, P, ctypes.POINTER(i64)]
         L.tam_timing_get.argtypes = [P, ctypes.POINTER(Timing)]
         L.tam_destroy.argtypes = [P]
@@ -293,6 +305,16 @@ class Handle:
                "tam_export_rows")
         return out
 
+    def valid_counts(self, node_ids, stream=None):
+        """int32 tensor [n]: |valid[node_ids[r]]| (0 for a dead node)."""
+        import torch
+        assert node_ids.dtype == torch.int32 and node_ids.is_contiguous()
+        out = torch.empty(node_ids.numel(), dtype=torch.int32, device=node_ids.device)
+        _check(lib().tam_valid_counts(self._raw, ctypes.c_void_p(node_ids.data_ptr()), node_ids.numel(),
+                                      ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream, self.host_only)),
+               "tam_valid_counts")
+        return out
+
     def rebuild(self, phases: int = 0, stream=None):
         """Rerun device phases (PHASE_* mask; 0 = the handle's default; with
         FLAG_LAZY_ROWS, 0 empties the row cache)."""
@@ -303,6 +325,16 @@ class Handle:
         _check(lib().tam_valid_pairs(self._raw, _stream_ptr(stream, self.host_only), ctypes.byref(m)),
                "tam_valid_pairs")
         return int(m.value)
+
+    def layout(self) -> dict:
+        """The device's trie layout computed on the host (host-only handles):
+        blob, node_at, depth, node_pos, parent (numpy copies) and errors."""
+        lay = Layout()
+        _check(lib().tam_layout_get(self._raw, ctypes.byref(lay)), "tam_layout_get")
+        BB, N = int(lay.blob_bytes), self.num_nodes
+        arr = lambda p, n: np.ctypeslib.as_array(p, shape=(n,)).copy()  # noqa: E731
+        return {"blob": arr(lay.blob, BB), "node_at": arr(lay.node_at, BB), "depth": arr(lay.depth, N),
+                "node_pos": arr(lay.node_pos, N), "parent": arr(lay.parent, N), "errors": int(lay.errors)}
 
     def timing(self) -> dict:
         t = Timing()

@@ -358,3 +358,59 @@ def test_host_compile_in_forked_child(P):
     got = q.get(timeout=120)
     p.join(timeout=60)
     assert p.exitcode == 0 and got == ref
+
+
+def test_argument_errors_before_state(P):
+    """Argument errors of the serving calls are TAM_E_INVAL, reported before the
+    handle's state (a host-only handle would be TAM_E_STATE): an unsupported
+    dtype, a row stride below V, logits not aligned to their element, null
+    pointers with rows to process, negative sizes, a misaligned export."""
+    h = host(P, [b"ab", b"ac"], [b"a", b"b", b"c"])  # V = 3
+    L = P.lib()
+    fake = ctypes.c_void_p(0x10000)             # never dereferenced: the checks come first
+    odd = ctypes.c_void_p(0x10001)
+    assert L.tam_apply_mask(h._raw, fake, 4, fake, 2, 3, None) == -1      # dtype 2
+    assert L.tam_apply_mask(h._raw, fake, 4, fake, -1, 3, None) == -1     # dtype -1
+    assert L.tam_apply_mask(h._raw, fake, 4, fake, 1, 2, None) == -1      # row_stride < V
+    assert L.tam_apply_mask(h._raw, fake, 4, odd, 1, 3, None) == -1       # bf16 at an odd address
+    assert L.tam_apply_mask(h._raw, fake, 4, ctypes.c_void_p(0x10002), 0, 3, None) == -1  # fp32 at 2 mod 4
+    assert L.tam_apply_mask(h._raw, None, 4, fake, 1, 3, None) == -1      # null ids
+    assert L.tam_apply_mask(h._raw, fake, 4, None, 1, 3, None) == -1      # null logits
+    assert L.tam_apply_mask(h._raw, fake, -1, fake, 1, 3, None) == -1     # B < 0
+    assert L.tam_apply_mask(None, fake, 4, fake, 1, 3, None) == -1        # null handle
+    assert L.tam_apply_mask(h._raw, fake, 4, fake, 1, 3, None) == -6      # valid arguments: the state
+    assert L.tam_advance(h._raw, fake, None, 4, fake, None) == -1
+    assert L.tam_advance(h._raw, fake, fake, -2, fake, None) == -1
+    assert L.tam_advance(h._raw, fake, fake, 4, fake, None) == -6
+    assert L.tam_export_rows(h._raw, fake, 4, odd, None) == -1            # out not 8-byte aligned
+    assert L.tam_export_rows(h._raw, fake, -1, fake, None) == -1
+    assert L.tam_export_rows(h._raw, None, 4, fake, None) == -1
+    assert L.tam_export_rows(h._raw, fake, 4, fake, None) == -6
+    L.tam_export_rows(h._raw, fake, 4, odd, None)
+    assert "aligned" in L.tam_last_error().decode()
+    h.close()
+
+
+def test_token_too_long(P):
+    """A token of 65,536 bytes is beyond the 16-bit length field of the
+    vocabulary table: TAM_E_TOOLARGE, with no handle made; 65,535 bytes fit."""
+    with pytest.raises(P.TamError) as e:
+        P.Vocab([b"a", b"b" * 65536], host_only=True)
+    assert e.value.status == -5 and "65535" in str(e.value)
+    with pytest.raises(P.TamError) as e:
+        host(P, [b"ab"], [b"a", b"c" * 70000])
+    assert e.value.status == -5
+    v = P.Vocab([b"a", b"b" * 65535], host_only=True)
+    h = P.compile([b"ab"], v, flags=P.FLAG_HOST_ONLY)
+    assert h.max_token_len == 65535
+    h.close()
+    v.close()
+
+
+def test_duplicate_token_limit(P):
+    """More than 65,535 ids sharing one byte string: TAM_E_TOOLARGE."""
+    with pytest.raises(P.TamError) as e:
+        P.Vocab([b"q"] * 65536 + [b"r"], host_only=True)
+    assert e.value.status == -5
+    v = P.Vocab([b"q"] * 65535 + [b"r"], host_only=True)
+    v.close()

@@ -86,6 +86,10 @@ def full_check(P, strings, vocab, sets=None, flags=0, terminator=0x22):
     nodes = np.arange(-2, o.N + 2)
     assert np.array_equal(gpu_rows(h, nodes), np.concatenate(
         [np.zeros((2, o.W), np.uint64), o.mask_rows(np.arange(o.N)), np.zeros((2, o.W), np.uint64)]))
+    if not flags & LAZY:
+        cnt = h.valid_counts(torch.as_tensor(nodes.astype(np.int32), device="cuda")).cpu().numpy()
+        assert np.array_equal(cnt[2:-2], np.unpackbits(o.mask_rows(np.arange(o.N)).view(np.uint8), axis=1).sum(1))
+        assert not cnt[:2].any() and not cnt[-2:].any()
     nn, tt = np.meshgrid(nodes, np.arange(-1, o.V + 1), indexing="ij")
     assert np.array_equal(gpu_advance(h, nn.ravel(), tt.ravel()), o.advance(nn.ravel(), tt.ravel()))
     for dtype in ("fp32", "bf16"):
@@ -454,6 +458,65 @@ def test_long_and_duplicate_tokens(P, flags):
     h.close()
 
 
+@pytest.mark.parametrize("cid", [3, 4])
+def test_config_every_row(P, cid):
+    """Every row of the full table at c3 and c4 against the oracle (its rows
+    computed on a pool of host threads, in chunks), and every row of the tail
+    compression and rows-built-on-demand handles against the full table's on
+    the device: all three representations equal the oracle row for row."""
+    import concurrent.futures as cf
+    w = W.config(cid)
+    o = Oracle(w.strings, w.vocab)
+    hf = P.compile(w.strings, w.vocab)
+    ht = P.compile(w.strings, w.vocab, flags=8)
+    hz = P.compile(w.strings, w.vocab, flags=LAZY)
+    assert hf.num_nodes == o.N
+    chunk = 1024
+    starts = list(range(0, o.N, chunk))
+    with cf.ThreadPoolExecutor(max_workers=16) as pool:  # the oracle's C call releases the GIL
+        futs = [pool.submit(o.mask_rows, np.arange(a, min(o.N, a + chunk), dtype=np.int32)) for a in starts]
+        for a, f in zip(starts, futs):
+            ids = torch.arange(a, min(o.N, a + chunk), dtype=torch.int32, device="cuda")
+            full = hf.export_rows(ids)
+            assert torch.equal(ht.export_rows(ids), full), a
+            assert torch.equal(hz.export_rows(ids), full), a
+            exp = f.result()
+            assert np.array_equal(rows_np(full), exp), a
+            cnt = popcounts(exp)
+            assert np.array_equal(hf.valid_counts(ids).cpu().numpy(), cnt), a
+            assert np.array_equal(ht.valid_counts(ids).cpu().numpy(), cnt), a
+    for h in (hf, ht, hz):
+        h.close()
+    torch.cuda.empty_cache()
+
+
+def popcounts(rows: np.ndarray) -> np.ndarray:
+    return np.unpackbits(rows.view(np.uint8), axis=1).sum(axis=1).astype(np.int32)
+
+
+@pytest.mark.parametrize("cid", [1, 2])
+@pytest.mark.parametrize("flags", [0, 2, 8], ids=["dense", "no_table", "tail"])
+def test_valid_counts_every_node(P, cid, flags):
+    """|valid[n]| of every node (and of dead ids) counted on the device equals the
+    popcount of the oracle's row; rows built on demand keep no counts."""
+    w = W.config(cid)
+    o = Oracle(w.strings, w.vocab)
+    h = P.compile(w.strings, w.vocab, flags=flags)
+    nodes = np.arange(-3, o.N + 3, dtype=np.int32)
+    got = h.valid_counts(torch.as_tensor(nodes, device="cuda")).cpu().numpy()
+    exp = np.zeros(nodes.size, np.int32)
+    for a in range(0, o.N, 2048):
+        exp[3 + a:3 + min(o.N, a + 2048)] = popcounts(o.mask_rows(np.arange(a, min(o.N, a + 2048), dtype=np.int32)))
+    assert np.array_equal(got, exp)
+    assert int(got.sum()) == h.valid_pairs()
+    h.close()
+    hz = P.compile(w.strings, w.vocab, flags=LAZY)
+    with pytest.raises(P.TamError) as e:
+        hz.valid_counts(torch.zeros(1, dtype=torch.int32, device="cuda"))
+    assert e.value.status == -6
+    hz.close()
+
+
 # ---------------------------------------------------------- sparse / forest --
 
 def test_no_table_matches_dense_c4(P):
@@ -467,12 +530,13 @@ def test_no_table_matches_dense_c4(P):
     check_apply(P, h, o, W.uniform_nodes(4, o.N, 16, 1), "fp32", seed=5)
 
 
-@pytest.mark.parametrize("flags", [2, LAZY], ids=["no_table", "lazy"])
+@pytest.mark.parametrize("flags", [2, 8, LAZY], ids=["no_table", "tail", "lazy"])
 def test_forest_c5(P, flags):
     """Config 5: 256 per-query sets of 500 strings as one forest (sparse rows,
-    or rows built on demand into a 1024-row cache: 256 new rows per step evict
-    from the fifth step on).  The oracle runs on sampled rows and on every row
-    the 16-step decode visits."""
+    tail compression's dense rows for the branching nodes, or rows built on
+    demand into a 1024-row cache: 256 new rows per step evict from the fifth
+    step on).  The oracle runs on sampled rows and on every row the 16-step
+    decode visits."""
     w = W.config(5)
     o = Oracle(w.strings, w.vocab, set_offsets=w.set_offsets)
     h = P.compile(w.strings, w.vocab, sets=w.set_offsets, flags=flags, cache_rows=1024)
