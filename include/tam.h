@@ -419,6 +419,37 @@ tam_status tam_timing_get(const tam_handle *h, tam_timing *out);
  * calls are the caller's: wait for their streams first.  NULL is a no-op. */
 void tam_destroy(tam_handle *h);
 
+/* Largest L that tam_format_rows_noalloc takes. */
+#define TAM_NOALLOC_MAX_POSITIONS 1024
+
+/*
+ * tam_format_rows_noalloc -- for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the character-position masks of tam_compile_format written
+ * straight into the caller's memory, with no handle and no allocation (no
+ * hipMalloc, no allocator callback, no pageable copy: the class bits travel as
+ * kernel arguments).
+ *   classes     host uint8[L][32], as for tam_compile_format; 1 <= L <=
+ *               TAM_NOALLOC_MAX_POSITIONS (else TAM_E_INVAL).
+ *   terminator  0..255; no class may admit it (TAM_E_TERMINATOR).
+ *   vocab       a device vocabulary (tam_vocab_create without
+ *               TAM_FLAG_HOST_ONLY, else TAM_E_STATE) on the current device.
+ *   out         device uint64[L + 2][out_stride_words], 8-byte aligned,
+ *               out_stride_words >= W: row p receives the canonical row of
+ *               position p (rows 0..L, then L+1 after the terminator, all zero);
+ *               words W.. of each row are left as they are.
+ *   pairs_out   device int64[1] for the number of valid (position, token)
+ *               pairs, or NULL.
+ * Scratch: the class bits and a pair counter live in a static device array of
+ * 256 + 32 * TAM_NOALLOC_MAX_POSITIONS bytes per GPU, held until the process
+ * ends and shared by every call on that GPU: calls that overlap on one GPU
+ * (different streams, or threads without ordering) race; order them.  The
+ * result equals tam_export_rows of a tam_compile_format handle, row for row.
+ * Errors: TAM_E_INVAL, TAM_E_TERMINATOR, TAM_E_STATE, TAM_E_DEVICE.
+ */
+tam_status tam_format_rows_noalloc(const uint8_t *classes, int64_t L, int terminator, const tam_vocab *vocab,
+                                   uint64_t *out, int64_t out_stride_words, int64_t *pairs_out, void *stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char *tam_last_error(void);
 

@@ -32,6 +32,8 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <cstring>
+#include <mutex>
 
 #include "tam_internal.hpp"
 #include "trie_layout.hpp"
@@ -907,14 +909,17 @@ __device__ __forceinline__ bool format_fits(const DevTables &t, int p, const uin
 // Character-position masks (Appendix, Constraint-Aware Dispatch Beyond Finite
 // Sets), written whole: one wave per 64-token word w of every row.  Lane i
 // tests token 64 w + i at each position p; the wave's ballot is word w of row p
-// (lane 0 stores it), so no zero fill is needed, and padding words come out
-// zero.  Each block writes its number of valid (position, token) pairs.
-__global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restrict__ pairs) {
+// (lane 0 stores it at out[p * stride + w]), so no zero fill is needed, and
+// words past V come out zero.  The valid (position, token) pairs are counted:
+// per block into pairs[blockIdx.x], and/or added to *total.
+__global__ void __launch_bounds__(kBlock) k_format(DevTables t, uint64_t *__restrict__ out, int64_t stride,
+                                                   int64_t nwords, int32_t *__restrict__ pairs,
+                                                   unsigned long long *total) {
     const int64_t w = ((int64_t)blockIdx.x * kBlock + threadIdx.x) / kWave;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t v = w * kWave + lane;
     int32_t found = 0;
-    if (w < t.Wp) {
+    if (w < nwords) {
         int len = 0;
         const uint8_t *tb = t.tok_blob;
         if (v < t.V) {
@@ -925,7 +930,7 @@ __global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restr
         for (int p = 0; p <= t.fmt_L + 1; ++p) {
             const bool ok = format_fits(t, p, tb, len);
             const uint64_t word = __ballot(ok);
-            if (lane == 0) t.table[(int64_t)p * t.Wp + w] = word;
+            if (lane == 0) out[(int64_t)p * stride + w] = word;
             found += ok ? 1 : 0;
         }
     }
@@ -934,9 +939,10 @@ __global__ void __launch_bounds__(kBlock) k_format(DevTables t, int32_t *__restr
     if (lane == 0) wsum[threadIdx.x / kWave] = found;
     __syncthreads();
     if (threadIdx.x == 0) {
-        int32_t total = 0;
-        for (int k = 0; k < kBlock / kWave; ++k) total += wsum[k];
-        pairs[blockIdx.x] = total;
+        int32_t sum = 0;
+        for (int k = 0; k < kBlock / kWave; ++k) sum += wsum[k];
+        if (pairs) pairs[blockIdx.x] = sum;
+        if (total && sum) atomicAdd(total, (unsigned long long)sum);
     }
 }
 
@@ -1440,7 +1446,8 @@ int64_t mark_blocks(int64_t N) { return (N * kProbeLanes + kBlock - 1) / kBlock;
 int64_t format_blocks(int64_t Wp) { return (Wp * kWave + kBlock - 1) / kBlock; }
 
 hipError_t launch_format(const DevTables &t, int32_t *pairs, hipStream_t s) {
-    hipLaunchKernelGGL(k_format, dim3((unsigned)format_blocks(t.Wp)), dim3(kBlock), 0, s, t, pairs);
+    hipLaunchKernelGGL(k_format, dim3((unsigned)format_blocks(t.Wp)), dim3(kBlock), 0, s, t, t.table, t.Wp, t.Wp,
+                       pairs, (unsigned long long *)nullptr);
     return hipGetLastError();
 }
 
@@ -1602,6 +1609,92 @@ hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int6
     }
     if (!t.row_of) return hipSuccess;
     hipLaunchKernelGGL(k_export_tail, dim3(grid_for(n, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, n, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------- format rows, no allocation ---
+
+// The scratch of tam_format_rows_noalloc: a counter of the valid pairs, then
+// the class bits of up to TAM_NOALLOC_MAX_POSITIONS positions, staged from the
+// host through kernel arguments.  One copy per GPU, held until the process
+// ends; every call on a GPU shares it (overlapping calls race).  Host code
+// never names the array itself: it takes the device address that
+// hipGetSymbolAddress returns (noalloc_scratch) and passes that to kernels.
+constexpr size_t kScratchHeader = 256;
+constexpr size_t kScratchBytes = kScratchHeader + 32 * (size_t)TAM_NOALLOC_MAX_POSITIONS;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kStagePositions = 64;  // positions per staging launch (2 KiB of kernel arguments)
+
+struct ClassChunk {
+    int32_t first, count;                  // positions [first, first + count)
+    uint32_t words[kStagePositions * 8];   // their class bits, 32 bytes per position
+};
+
+// Copies one chunk of class bits into the scratch (the first chunk also
+// clears the pair counter).
+__global__ void __launch_bounds__(kBlock) k_stage_classes(ClassChunk c, uint32_t *__restrict__ cls,
+                                                          unsigned long long *counter) {
+    for (int i = threadIdx.x; i < c.count * 8; i += kBlock) cls[(int64_t)c.first * 8 + i] = c.words[i];
+    if (c.first == 0 && threadIdx.x == 0) *counter = 0ull;
+}
+
+__global__ void k_store_total(const unsigned long long *counter, int64_t *out) {
+    if (threadIdx.x == 0) *out = (int64_t)*counter;
+}
+
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[64] = {};
+
+}  // namespace
+
+// The device address of this GPU's scratch, looked up once per device with
+// that device current.
+hipError_t noalloc_scratch(uint8_t **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> g(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = static_cast<uint8_t *>(g_scratch_ptr[dev]);
+    return hipSuccess;
+}
+
+hipError_t launch_format_noalloc(const DevTables &t, const uint8_t *classes_host, uint64_t *out, int64_t stride,
+                                 int64_t *pairs_out, hipStream_t s) {
+    const int64_t L = t.fmt_L;
+    if (L < 1 || L > TAM_NOALLOC_MAX_POSITIONS || stride < t.W) return hipErrorInvalidValue;
+    uint8_t *base = nullptr;
+    hipError_t e = noalloc_scratch(&base);
+    if (e != hipSuccess) return e;
+    unsigned long long *counter = reinterpret_cast<unsigned long long *>(base);
+    uint32_t *cls = reinterpret_cast<uint32_t *>(base + kScratchHeader);
+    for (int64_t p0 = 0; p0 < L; p0 += kStagePositions) {
+        ClassChunk c;
+        c.first = (int32_t)p0;
+        c.count = (int32_t)std::min<int64_t>(kStagePositions, L - p0);
+        std::memset(c.words, 0, sizeof(c.words));
+        std::memcpy(c.words, classes_host + 32 * p0, (size_t)c.count * 32);
+        hipLaunchKernelGGL(k_stage_classes, dim3(1), dim3(kBlock), 0, s, c, cls, counter);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    DevTables tf = t;
+    tf.classes = reinterpret_cast<const uint8_t *>(cls);
+    hipLaunchKernelGGL(k_format, dim3((unsigned)format_blocks(t.W)), dim3(kBlock), 0, s, tf, out, stride, t.W,
+                       (int32_t *)nullptr, counter);
+    e = hipGetLastError();
+    if (e != hipSuccess || !pairs_out) return e;
+    hipLaunchKernelGGL(k_store_total, dim3(1), dim3(kWave), 0, s, counter, pairs_out);
     return hipGetLastError();
 }
 

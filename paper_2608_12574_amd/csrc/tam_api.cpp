@@ -977,6 +977,44 @@ void layout_on_host(tam_handle *h) {
 
 extern "C" {
 
+tam_status tam_format_rows_noalloc(const uint8_t *classes, int64_t L, int terminator, const tam_vocab *vocab,
+                                   uint64_t *out, int64_t out_stride_words, int64_t *pairs_out, void *stream) {
+    g_err.clear();
+    if (!classes || !vocab || !out) return fail(TAM_E_INVAL, "null argument");
+    if (L < 1 || L > TAM_NOALLOC_MAX_POSITIONS)
+        return fail(TAM_E_INVAL, "L must be in [1, " + std::to_string(TAM_NOALLOC_MAX_POSITIONS) +
+                                     "]: the static scratch holds the class bits of at most that many positions");
+    if (terminator < 0 || terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
+    if (out_stride_words < vocab->W) return fail(TAM_E_INVAL, "out_stride_words must be >= W");
+    if ((reinterpret_cast<uintptr_t>(out) & 7) != 0 || (reinterpret_cast<uintptr_t>(pairs_out) & 7) != 0)
+        return fail(TAM_E_INVAL, "out and pairs_out must be 8-byte aligned");
+    for (int64_t p = 0; p < L; ++p)
+        if ((classes[32 * p + (terminator >> 3)] >> (terminator & 7)) & 1)
+            return fail(TAM_E_TERMINATOR, "class " + std::to_string(p) + " admits the terminator byte");
+    if (vocab->flags & TAM_FLAG_HOST_ONLY) return fail(TAM_E_STATE, "the vocabulary has no device tables");
+    int dev = -1;
+    TAM_HIP(hipGetDevice(&dev));
+    if (dev != vocab->device) return fail(TAM_E_STATE, "the vocabulary lives on another device");
+    TAM_HIP(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // the vocabulary's uploads, if they may still be running
+    if (hipEventQuery(vocab->ready) != hipSuccess) {
+        (void)hipGetLastError();
+        TAM_HIP(hipStreamWaitEvent(s, vocab->ready, 0));
+    }
+    tam::DevTables t{};
+    t.tok_off = vocab->d_tok_off;
+    t.tok_blob = vocab->d_tok_blob;
+    t.V = vocab->V;
+    t.W = vocab->W;
+    t.Wp = vocab->W;
+    t.max_len = (int32_t)vocab->max_tok_len;
+    t.terminator = terminator;
+    t.fmt_L = (int32_t)L;
+    TAM_HIP(tam::launch_format_noalloc(t, classes, out, out_stride_words, pairs_out, s));
+    return TAM_OK;
+}
+
 tam_status tam_layout_get(const tam_handle *h, tam_layout *out) {
     g_err.clear();
     if (!h || !out) return fail(TAM_E_INVAL, "null argument");

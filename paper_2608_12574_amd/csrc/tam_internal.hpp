@@ -104,6 +104,11 @@ hipError_t launch_advance(const DevTables &t, const int32_t *node_ids, const int
                           int64_t B, int32_t *out, hipStream_t s);
 hipError_t launch_format(const DevTables &t, int32_t *pairs, hipStream_t s);
 int64_t format_blocks(int64_t Wp);
+// tam_format_rows_noalloc: the rows of positions 0..t.fmt_L+1 into out (stride
+// words, W written per row) with the class bits staged in the static scratch;
+// the pair count into *pairs_out when it is not null.  Allocates nothing.
+hipError_t launch_format_noalloc(const DevTables &t, const uint8_t *classes_host, uint64_t *out, int64_t stride,
+                                 int64_t *pairs_out, hipStream_t s);
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
                                hipStream_t s);
 int64_t scan_tmp_elems(int64_t N);

@@ -34,7 +34,7 @@ ENTRY_POINTS = ("tam_compile", "tam_vocab_create", "tam_compile_vocab", "tam_com
                 "tam_info_get", "tam_layout_get",
                 "tam_apply_mask", "tam_advance", "tam_export_rows", "tam_valid_counts", "tam_valid_pairs",
                 "tam_timing_get",
-                "tam_vocab_destroy", "tam_destroy", "tam_last_error")
+                "tam_format_rows_noalloc", "tam_vocab_destroy", "tam_destroy", "tam_last_error")
 
 
 class TamError(RuntimeError):
@@ -105,6 +105,7 @@ def lib() -> ctypes.CDLL:
                                         ctypes.POINTER(Allocator), P, ctypes.POINTER(P)]
         L.tam_compile_format.argtypes = [P, i64, P, ctypes.POINTER(Options), ctypes.POINTER(Allocator), P,
                                          ctypes.POINTER(P)]
+        L.tam_format_rows_noalloc.argtypes = [P, i64, ctypes.c_int, P, P, i64, P, P]
         L.tam_vocab_destroy.argtypes = [P]
         L.tam_vocab_destroy.restype = None
         L.tam_rebuild.argtypes = [P, ctypes.c_uint, P]
@@ -444,6 +445,22 @@ def format_class_rows(classes) -> np.ndarray:
         b = np.frombuffer(bytes(allowed), dtype=np.uint8)
         np.bitwise_or.at(rows[p], b >> 3, (1 << (b & 7)).astype(np.uint8))
     return rows
+
+
+def format_rows_noalloc(classes, vocab: "Vocab", out, pairs_out=None, terminator: int = 0x22, stream=None):
+    """tam_format_rows_noalloc: the character-position rows of ``classes`` (a list
+    of L byte strings) written into ``out`` (a device int64 tensor [L + 2, >= W])
+    without allocating; the valid-pair count into ``pairs_out`` (device int64
+    [1]) when given."""
+    import torch
+    rows = np.ascontiguousarray(format_class_rows(classes))
+    assert out.dtype == torch.int64 and out.is_cuda and out.dim() == 2 and out.stride(1) == 1
+    assert out.shape[0] == len(classes) + 2
+    _check(lib().tam_format_rows_noalloc(_ptr(rows), len(classes), terminator, vocab._raw,
+                                         ctypes.c_void_p(out.data_ptr()), out.stride(0),
+                                         ctypes.c_void_p(pairs_out.data_ptr()) if pairs_out is not None else None,
+                                         _stream_ptr(stream)), "tam_format_rows_noalloc")
+    return out
 
 
 def compile_format(classes, vocab, terminator: int = 0x22, flags: int = 0, device=None, stream=None) -> Handle:

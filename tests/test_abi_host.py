@@ -414,3 +414,29 @@ def test_duplicate_token_limit(P):
     assert e.value.status == -5
     v = P.Vocab([b"q"] * 65535 + [b"r"], host_only=True)
     v.close()
+
+
+def test_format_rows_noalloc_argument_errors(P):
+    """tam_format_rows_noalloc checks its arguments before touching a device:
+    L beyond the static scratch (TAM_NOALLOC_MAX_POSITIONS = 1024) or below 1,
+    a class admitting the terminator, a short output stride, a host-only
+    vocabulary."""
+    L = P.lib()
+    voc = P.Vocab([b"1", b"12", b"-"], host_only=True)
+    fake = ctypes.c_void_p(0x10000)
+
+    def call(classes, n, term=0x22, stride=1, out=fake, pairs=None):
+        rows = np.ascontiguousarray(P.tam.format_class_rows(classes)) if classes else np.zeros((1, 32), np.uint8)
+        return L.tam_format_rows_noalloc(ctypes.c_void_p(rows.ctypes.data), n, term, voc._raw, out, stride,
+                                         pairs, None)
+
+    assert call([b"0"] * 1025, 1025) == -1
+    assert "1024" in L.tam_last_error().decode()
+    assert call([b"0"], 0) == -1
+    assert call([b"0"], 1, term=256) == -1
+    assert call([b"0"], 1, stride=0) == -1
+    assert call([b"0"], 1, out=ctypes.c_void_p(0x10004)) == -1
+    assert call([b"0"], 1, pairs=ctypes.c_void_p(0x10004)) == -1
+    assert call([b'0"'], 1) == -2
+    assert call([b"0"] * 1024, 1024) == -6  # valid arguments: a host-only vocabulary has no device tables
+    voc.close()
