@@ -29,26 +29,38 @@ __host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len
     return z | 1ull;  // 0 never occurs as a key
 }
 
-// Vocabulary table: open addressing over buckets of 16 16-bit fingerprints (32
-// bytes per bucket), one slot per distinct non-empty token string.  A
-// slot's 32-byte payload (its first 16 bytes stored last byte first, its
-// smallest token id, length and duplicate count) is read only on a fingerprint
-// match, with one load.
-constexpr int kBucket = 16;   // fingerprints per bucket
+// Vocabulary table: open addressing over buckets of kBucket 16-bit
+// fingerprints (16 bytes per bucket: one load), one slot per distinct
+// non-empty token string.  A slot's 16-byte payload (its first 8 bytes stored
+// last byte first, its smallest token id, length and duplicate count) is read
+// only on a fingerprint match, with one load; bytes 8..15 of a longer token
+// sit in pay_hi[slot] and are read only when the first 8 match.  Suffixes of
+// at most kShortLen bytes skip the hash: short_hits maps them straight to
+// their hit (short_index).
+constexpr int kBucket = 8;    // fingerprints per bucket
 constexpr int kWin = 16;      // path bytes a probing node keeps in registers
 constexpr int kBlobPad = 32;  // zero bytes before and after the string blob (and after the token blob)
+constexpr int kShortLen = 2;  // suffix lengths answered by short_hits
+constexpr int kShortEntries = 256 + 65536;
 
 __host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
     return (uint32_t)(key >> 48) | 1u;  // 16 bits; 0 marks an empty slot
 }
 
-struct alignas(32) SlotPay {
-    uint64_t lo, hi;  // byte k = token byte len-1-k for k < min(len, 16), then zeros
+// Index in short_hits of the string of d <= kShortLen bytes whose last byte is
+// `last` and (d = 2) whose first byte is `prev`.
+__host__ __device__ __forceinline__ int32_t short_index(int d, uint32_t last, uint32_t prev) {
+    return d == 1 ? (int32_t)last : 256 + (int32_t)((prev << 8) | last);
+}
+
+struct alignas(16) SlotPay {
+    uint64_t lo;      // byte k = token byte len-1-k for k < min(len, 8), then zeros
     int32_t first;    // smallest token id with this string (-1: empty slot)
     uint16_t len;     // string length in bytes
     uint16_t count;   // number of token ids with this string
-    uint32_t pad[2];
 };
+// pay_hi[slot]: byte k - 8 = token byte len-1-k for 8 <= k < min(len, 16), then
+// zeros (0 for strings of at most 8 bytes).
 
 // What the probe pass stores per (node, suffix length): the token id when the
 // string has one id, -2 - slot when it has several, -1 when no token matches.
@@ -83,6 +95,8 @@ struct DevTables {
     const uint8_t *tok_blob;
     const uint16_t *fps;        // [slot_mask+1] fingerprints, kBucket per bucket
     const SlotPay *pay;         // [slot_mask+1]
+    const uint64_t *pay_hi;     // [slot_mask+1] bytes 8..15 of the reversed token
+    const int32_t *short_hits;  // [kShortEntries] hit_of_slot of every string of <= kShortLen bytes, or -1
     const int32_t *dup_next;    // [V] next id with the same bytes, -1 at the end
     const uint8_t *len_present; // [max_len+1] 1 if some token has that length
     // valid lists (a4) and dense table
@@ -130,6 +144,7 @@ struct LazyDev {
     int32_t *miss_node;    // [kLazyGroup] nodes whose rows are built, in batch-row order
     int32_t *miss_row;     // [kLazyGroup] their destination rows (slots, or output rows)
     int64_t *miss_off;     // [kLazyGroup + 1] prefix sum of their subtree sizes (minus the node)
+    int32_t *miss_dep;     // [kLazyGroup] depth of each miss
     int32_t *miss_count;   // [1]
     int32_t *err;          // [1] the handle's device error count (see DevTables)
     int64_t C;             // cache rows

@@ -465,20 +465,24 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     h->len_present.assign((size_t)(max_len + 1), 0);
     h->len_mask = 0;
 
+    // load <= 1/4 (at most 2 keys per 8-slot bucket on average): a full home
+    // bucket, which sends a probe down the slower general path, stays rare
     uint64_t cap = 64;
-    while (cap < (uint64_t)(2 * V)) cap <<= 1;
+    while (cap < (uint64_t)(4 * V)) cap <<= 1;
     const uint64_t nbuckets = cap / kBucket;
     // the tables are first touched, and set empty, in parallel
     h->fps.resize(cap);
     h->pay.resize(cap);
+    h->pay_hi.resize(cap);
     h->dup_next.resize((size_t)V);
     hvec<int32_t> last(cap);
-    const SlotPay empty{0, 0, -1, 0, 0, {0, 0}};
+    const SlotPay empty{0, -1, 0, 0};
     const int64_t pchunk = 1 << 15, npchunks = ((int64_t)cap + pchunk - 1) / pchunk;
     parallel_for(npchunks, host_threads(npchunks), [&](int64_t c) {
         for (int64_t q = c * pchunk; q < std::min<int64_t>((int64_t)cap, (c + 1) * pchunk); ++q) {
             h->fps[(size_t)q] = 0;
             h->pay[(size_t)q] = empty;
+            h->pay_hi[(size_t)q] = 0;
             last[(size_t)q] = -1;
         }
     });
@@ -532,8 +536,8 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
                 const uint64_t sl = b * kBucket + (uint64_t)i;
                 if (h->fps[sl] == 0) {
                     h->fps[sl] = fp;
-                    h->pay[sl] = SlotPay{heads[(size_t)(2 * v)], heads[(size_t)(2 * v + 1)], (int32_t)v,
-                                         (uint16_t)len, 1, {0, 0}};
+                    h->pay[sl] = SlotPay{heads[(size_t)(2 * v)], (int32_t)v, (uint16_t)len, 1};
+                    h->pay_hi[sl] = heads[(size_t)(2 * v + 1)];
                     last[sl] = (int32_t)v;
                     return true;
                 }
@@ -596,6 +600,15 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     if (too_many) {
         *err = "more than 65535 tokens share one byte string";
         return TAM_E_TOOLARGE;
+    }
+    // the hits of every string of at most kShortLen bytes, indexed by its bytes
+    h->short_hits.assign((size_t)kShortEntries, -1);
+    for (uint64_t q = 0; q < cap; ++q) {
+        const SlotPay &sp = h->pay[(size_t)q];
+        if (sp.first < 0 || sp.len > kShortLen) continue;
+        const uint8_t *tb = blob + h->tok_off[(size_t)sp.first];
+        const int32_t at = short_index(sp.len, tb[sp.len - 1], sp.len == 2 ? tb[0] : 0u);
+        h->short_hits[(size_t)at] = hit_of_slot((int32_t)q, sp.first, sp.count);
     }
     // per length d, the running sum over lengths <= d of the largest number of
     // token ids sharing one string of that length (for the list size bound)

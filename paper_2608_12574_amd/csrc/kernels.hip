@@ -102,48 +102,71 @@ __device__ __forceinline__ bool has_len(const DevTables &t, int d) {
     return d < 64 ? ((t.len_mask >> d) & 1ull) != 0 : t.len_present[d] != 0;
 }
 
-// The first min(d, 16) reversed bytes of the suffix equal the slot's.
-__device__ __forceinline__ bool same_head(uint64_t lo, uint64_t hi, const SlotPay &r, int d) {
-    if (d >= 16) return lo == r.lo && hi == r.hi;
-    if (d >= 8) {
-        const uint64_t m = d == 8 ? 0ull : (~0ull >> (64 - 8 * (d - 8)));
-        return lo == r.lo && (hi & m) == r.hi;
-    }
-    return (lo & (~0ull >> (64 - 8 * d))) == r.lo && r.hi == 0ull;
+// The first min(d, 8) reversed bytes of a suffix of d bytes (lo) equal the slot's.
+__device__ __forceinline__ bool lo_ok(uint64_t lo, const SlotPay &r, int d) {
+    return (d >= 8 ? lo : (lo & (~0ull >> (64 - 8 * d)))) == r.lo;
 }
 
-// The 16 fingerprints of the bucket holding `key` first (32 bytes, two loads).
-struct Bucket {
-    u32x4 a, b;
-};
+// Reversed bytes 8 .. min(d, 16) - 1 of the suffix (hi) equal the slot's (d > 8).
+__device__ __forceinline__ bool hi_ok(uint64_t hi, uint64_t rhi, int d) {
+    return (d >= 16 ? hi : (hi & (~0ull >> (64 - 8 * (d - 8))))) == rhi;
+}
 
 __device__ __forceinline__ uint64_t home_bucket(const DevTables &t, uint64_t key) {
     return (key & t.slot_mask) / kBucket;
 }
 
+// The kBucket fingerprints of a bucket: kBucket / 8 16-byte loads.
+struct Bucket {
+    u32x4 q[kBucket / 8];
+};
+
 __device__ __forceinline__ Bucket load_bucket(const DevTables &t, uint64_t b) {
-    const u32x4 *q = reinterpret_cast<const u32x4 *>(t.fps + b * kBucket);
-    return Bucket{q[0], q[1]};
+    const u32x4 *p = reinterpret_cast<const u32x4 *>(t.fps + b * kBucket);
+    Bucket k;
+#pragma unroll
+    for (int i = 0; i < kBucket / 8; ++i) k.q[i] = p[i];
+    return k;
 }
 
 // Bit i of *match: slot i holds fingerprint fp; bit i of *empty: slot i is empty.
 __device__ __forceinline__ void bucket_masks(const Bucket &bk, uint32_t fp, uint32_t *match, uint32_t *empty) {
-    const uint32_t w[8] = {bk.a.x, bk.a.y, bk.a.z, bk.a.w, bk.b.x, bk.b.y, bk.b.z, bk.b.w};
     uint32_t mm = 0, ee = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const uint32_t lo16 = w[i] & 0xffffu, hi16 = w[i] >> 16;
-        mm |= ((lo16 == fp ? 1u : 0u) | (hi16 == fp ? 2u : 0u)) << (2 * i);
-        ee |= ((lo16 == 0u ? 1u : 0u) | (hi16 == 0u ? 2u : 0u)) << (2 * i);
+    for (int q = 0; q < kBucket / 8; ++q) {
+        const uint32_t w[4] = {bk.q[q].x, bk.q[q].y, bk.q[q].z, bk.q[q].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t lo16 = w[i] & 0xffffu, hi16 = w[i] >> 16;
+            const int sh = 8 * q + 2 * i;
+            mm |= ((lo16 == fp ? 1u : 0u) | (hi16 == fp ? 2u : 0u)) << sh;
+            ee |= ((lo16 == 0u ? 1u : 0u) | (hi16 == 0u ? 2u : 0u)) << sh;
+        }
     }
     *match = mm;
     *empty = ee;
 }
 
+// The suffix of d bytes ending at blob[pos] (window (lo, hi)) equals slot s,
+// whose payload m and (d > 8) pay_hi word mhi have just been read: its first 8
+// reversed bytes, bytes 8..15, then (d > 16) the bytes beyond the window.
+__device__ __forceinline__ bool slot_equals(const DevTables &t, const SlotPay &m, uint64_t mhi, int d, uint64_t lo,
+                                            uint64_t hi, int64_t pos) {
+    if ((int)m.len != d || !lo_ok(lo, m, d)) return false;
+    if (d > 8 && !hi_ok(hi, mhi, d)) return false;
+    if (d > kWin) {
+        const uint8_t *tb = t.tok_blob + t.tok_off[m.first];
+        const uint8_t *pb = t.blob + (pos - d + 1);
+        for (int k = 0; k < d - kWin; ++k)
+            if (tb[k] != pb[k]) return false;
+    }
+    return true;
+}
+
 // Slot whose token equals the suffix of length d ending at blob[pos] (key =
 // its hash, (lo, hi) = its reversed window), or -1; its payload goes to *pay.
 // Buckets are scanned from the key's home bucket until one with an empty slot
-// (load <= 1/2 guarantees one exists): a key sits in a later bucket only if
+// (load <= 1/4 guarantees one exists): a key sits in a later bucket only if
 // every bucket before it was full when it was inserted.  The fingerprints of a
 // bucket are compared into a bit mask first, so a wave reads the payload of its
 // matching lanes in one step instead of one divergent branch per slot.
@@ -160,17 +183,10 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
             match &= match - 1;
             const int32_t s = (int32_t)(b * kBucket + (uint64_t)i);
             const SlotPay m = t.pay[s];
-            if ((int)m.len == d && same_head(lo, hi, m, d)) {
-                bool eq = true;
-                if (d > kWin) {  // bytes beyond the window: compare in memory
-                    const uint8_t *tb = t.tok_blob + t.tok_off[m.first];
-                    const uint8_t *pb = t.blob + (pos - d + 1);
-                    for (int k = 0; k < d - kWin && eq; ++k) eq = tb[k] == pb[k];
-                }
-                if (eq) {
-                    *pay = m;
-                    return s;
-                }
+            const uint64_t mhi = d > 8 ? t.pay_hi[s] : 0ull;
+            if (slot_equals(t, m, mhi, d, lo, hi, pos)) {
+                *pay = m;
+                return s;
             }
         }
         if (empty) return -1;
@@ -178,12 +194,19 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
     }
 }
 
+// The hit of a suffix of d <= kShortLen bytes (last byte b0, the one before it b1).
+__device__ __forceinline__ int32_t short_hit(const DevTables &t, int d, uint32_t b0, uint32_t b1) {
+    return t.short_hits[short_index(d, b0, b1)];
+}
+
 // The hits (hit_of_slot, or -1) of the suffixes of length d = d0+1 .. d0+kPer
-// (only d <= Lw <= 16 probed) of a node's path: their bucket loads are issued
-// together, then their payload loads, so a lane waits for two memory round
-// trips.  A length whose home bucket does not settle it (a full bucket, or a
-// second fingerprint match after a failed first) falls back to the general
-// probe.  The hash of the first d0 bytes is recomputed by the lane.
+// (only d <= Lw <= 16 probed) of a node's path.  Lengths up to kShortLen read
+// short_hits.  The others' bucket loads are issued together, then their
+// payload loads, then (matches longer than 8 bytes) their pay_hi loads, so a
+// lane waits for two or three memory round trips.  A length whose home bucket
+// does not settle it (a full bucket, or a second fingerprint match after a
+// failed first) falls back to the general probe.  The hash of the first d0
+// bytes is recomputed by the lane.
 template <int kPer>
 __device__ __forceinline__ void probe_lengths(const DevTables &t, int64_t pos, int Lw, int d0, uint64_t lo,
                                               uint64_t hi, int32_t (&hit)[kPer]) {
@@ -199,7 +222,10 @@ __device__ __forceinline__ void probe_lengths(const DevTables &t, int64_t pos, i
         key[j] = 0;
         if (d <= Lw) {
             h = hash_step(h, window_byte(lo, hi, d - 1));
-            act[j] = has_len(t, d);
+            if (d <= kShortLen)
+                hit[j] = short_hit(t, d, window_byte(lo, hi, 0), window_byte(lo, hi, 1));
+            else
+                act[j] = has_len(t, d);
             key[j] = hash_final(h, (uint32_t)d);
         }
     }
@@ -218,15 +244,29 @@ __device__ __forceinline__ void probe_lengths(const DevTables &t, int64_t pos, i
             if (match[j]) slot[j] = (int32_t)(home_bucket(t, key[j]) * kBucket + (uint64_t)__builtin_ctz(match[j]));
         }
     }
+    // the payload of the first matching slot, and for lengths beyond 8 bytes
+    // its pay_hi word, in the same round trip
     SlotPay p[kPer];
+    uint64_t phi[kPer];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j)
-        if (slot[j] >= 0) p[j] = t.pay[slot[j]];
+    for (int j = 0; j < kPer; ++j) {
+        phi[j] = 0;
+        if (slot[j] >= 0) {
+            p[j] = t.pay[slot[j]];
+            if (d0 + j + 1 > 8) phi[j] = t.pay_hi[slot[j]];
+        }
+    }
+    bool head[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int d = d0 + j + 1;
+        head[j] = slot[j] >= 0 && (int)p[j].len == d && lo_ok(lo, p[j], d);
+    }
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
         const int d = d0 + j + 1;
         if (!act[j]) continue;
-        if (slot[j] >= 0 && (int)p[j].len == d && same_head(lo, hi, p[j], d)) {
+        if (head[j] && (d <= 8 || hi_ok(hi, phi[j], d))) {
             hit[j] = hit_of_slot(slot[j], p[j].first, p[j].count);
         } else if (empty[j] != 0 && (match[j] & (match[j] - 1)) == 0) {
             hit[j] = -1;  // the home bucket settles it: no such token
@@ -753,11 +793,12 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
 }
 
 // Dense-table rows, kApplyRows rows per block: block (x, y) takes span x (one
-// chunk per thread) of rows y, y + gridDim.y, ...  All the rows' mask bytes
-// are loaded first, then the logits of their mixed chunks, then the stores:
-// a block keeps kApplyRows mask loads in flight, while at any moment the
-// blocks still write a few compact windows of the logits.  Write-mostly as in
-// k_apply (non-temporal -inf stores, read-merge-write of mixed chunks).
+// chunk per thread) of the adjacent rows R y .. R y + R - 1.  All the rows'
+// mask bytes are loaded first, then the logits of their mixed chunks, then the
+// stores: a block keeps kApplyRows mask loads in flight, while at any moment
+// the blocks still write a few compact windows of the logits.  Write-mostly as
+// in k_apply (non-temporal -inf stores, read-merge-write of mixed chunks, also
+// stored non-temporally).
 template <typename T, int R>
 __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32_t *__restrict__ node_ids,
                                                         int64_t rows, T *__restrict__ logits, int64_t stride) {
@@ -772,7 +813,7 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
     uint32_t bits[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        const int64_t b = (int64_t)blockIdx.y * R + r;
         const int32_t n = b < rows ? node_ids[b] : -1;
         bits[r] = 0;  // a dead row: every token invalid
         if (n >= 0 && (int64_t)n < t.N && c < nchunks) {
@@ -785,13 +826,13 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
     u32x4 xv[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        const int64_t b = (int64_t)blockIdx.y * R + r;
         if (b < rows && whole && bits[r] != 0 && bits[r] != FULL)
             xv[r] = *reinterpret_cast<const u32x4 *>(logits + b * stride + e0);
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        const int64_t b = blockIdx.y + (int64_t)r * gridDim.y;
+        const int64_t b = (int64_t)blockIdx.y * R + r;
         const uint32_t bu = bits[r];
         if (b >= rows || bu == FULL) continue;
         T *row = logits + b * stride;
@@ -808,7 +849,7 @@ __global__ void __launch_bounds__(kBlock) k_apply_dense(DevTables t, const int32
                     if (!((bu >> i) & 1u)) vals[i] = NEG;
                 u32x4 o;
                 __builtin_memcpy(&o, vals, 16);
-                *p = o;
+                __builtin_nontemporal_store(o, p);
             }
         } else {
             const int lim = (int)min<int64_t>(E, V - e0);
@@ -1103,7 +1144,8 @@ __global__ void __launch_bounds__(kBlock) k_row_counts(DevTables t, const int32_
 
 // -------------------------------------------------------- rows on demand ---
 
-constexpr int kLazyProbeBlocks = 512;  // grid of k_lazy_probe (grid-stride)
+constexpr int kLazyProbeBlocks = 2048;  // grid of k_lazy_probe (grid-stride; blocks past the work exit)
+constexpr int kLazyBatch = 4;           // candidates per thread and round in k_lazy_probe
 
 // Exclusive prefix sum of one value per thread over a block of kLazyGroup
 // threads; *total receives the sum.  sh holds kLazyGroup / kWave + 1 values.
@@ -1151,7 +1193,8 @@ __device__ __forceinline__ void store_wg(uint32_t *p, uint32_t v) {
 // kCache (tam_apply_mask):
 //   1. Each live row claims its node with a compare-and-swap on slot_of: a
 //      slot (>= 0) is a hit; -1 makes the row the builder of the node's row (a
-//      miss); -2 - b names builder b to the other rows of that node.
+//      miss); -2 - b names builder b to the other rows of that node.  A group
+//      without a miss ends here, its rows' slots written.
 //   2. Hits stamp their slot with the group's number, so it is not evicted.
 //   3. The misses take slots by CLOCK: sweeps from the hand over windows of up
 //      to kLazyGroup slots take those not used by the group and without a
@@ -1159,25 +1202,31 @@ __device__ __forceinline__ void store_wg(uint32_t *p, uint32_t v) {
 //      pass; the hand stops after the last slot taken.  With nb <= C at least
 //      as many slots are free as there are misses, so two turns of the hand
 //      suffice.
-//   4. A taken slot drops its old node; each builder records its node, slot
-//      and subtree size for the zero and probe passes, and every batch row
-//      its slot (rows_src).
+//   4. A taken slot drops its old node; each builder records its node, slot,
+//      depth and candidate offset for the zero and probe passes, and every
+//      batch row its slot (rows_src).
 // !kCache (tam_export_rows): every live row is built, into output row b.
 template <bool kCache>
-__global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__restrict__ sub_end, int64_t N,
+__global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__restrict__ sub_end,
+                                                            const int32_t *__restrict__ depth, int64_t N,
                                                             LazyDev z, const int32_t *__restrict__ ids,
                                                             int32_t nb) {
     __shared__ int32_t s_slot[kLazyGroup];
     __shared__ int32_t s_victim[kLazyGroup];
+    __shared__ int32_t s_vold[kLazyGroup];
     __shared__ int64_t s_scan[kLazyGroup / kWave + 1];
-    __shared__ uint32_t s_u[4];  // group number, hand, cut, counter wrapped
+    __shared__ uint32_t s_u[4];  // group number, -, cut, counter wrapped
     const int tid = threadIdx.x;
     const int32_t n = tid < nb ? ids[tid] : -1;
     const bool live = n >= 0 && (int64_t)n < N;
     const int64_t below = live ? (int64_t)sub_end[n] - n - 1 : 0;
+    const int32_t ndep = live ? depth[n] : 0;
     int32_t slot = -1, lead = -1;
     bool miss = live;
     uint32_t group = 0;
+    const int64_t C = z.C;
+    const int win = (int)min<int64_t>(C, kLazyGroup);
+    int64_t hand = 0;
     if (kCache) {
         if (tid == 0) {
             uint32_t g = z.state[0] + 1u;
@@ -1185,7 +1234,6 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             if (g == 0u) g = 1u;  // 0 marks a slot never used
             z.state[0] = g;
             s_u[0] = g;
-            s_u[1] = z.state[1];
         }
         if (live) {
             const int32_t v = atomicCAS(&z.slot_of[n], -1, -2 - tid);
@@ -1198,7 +1246,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
         __syncthreads();
         group = s_u[0];
         if (s_u[3]) {  // the group counter wrapped: forget every stamp
-            for (int64_t c = tid; c < z.C; c += kLazyGroup) store_wg(&z.stamp[c], 0u);
+            for (int64_t c = tid; c < C; c += kLazyGroup) store_wg(&z.stamp[c], 0u);
             __syncthreads();
         }
         if (slot >= 0) {
@@ -1207,15 +1255,25 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
         }
     }
     s_slot[tid] = slot;
+    // no miss in the group (every live row's node is cached): only the rows'
+    // slots are written
+    if (kCache && !__syncthreads_or(miss ? 1 : 0)) {
+        if (tid < nb) z.rows_src[tid] = slot;
+        if (tid == 0) {
+            z.miss_off[0] = 0;
+            *z.miss_count = 0;
+        }
+        return;
+    }
     int64_t nmiss, total;
     const int32_t rank = (int32_t)group_scan(miss ? 1 : 0, &nmiss, s_scan);
     const int64_t off = group_scan(miss ? below : 0, &total, s_scan);
     const int32_t M = (int32_t)nmiss;
     if (kCache) {
-        __syncthreads();  // the hits' stamps before the sweeps read them
-        const int64_t C = z.C;
-        const int win = (int)min<int64_t>(C, kLazyGroup);
-        int64_t hand = s_u[1];
+        // the hits' stamps are stored (the barrier of the scans above); each
+        // window of the sweep loads its slots' stamps, reference bits and
+        // nodes in one round trip
+        hand = z.state[1];
         int32_t taken = 0;
         const int64_t max_sweeps = 2 * ((C + win - 1) / win) + 2;
         for (int64_t it = 0; it < max_sweeps && taken < M; ++it) {
@@ -1224,6 +1282,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             if (c >= C) c -= C;
             const uint32_t st = in ? load_wg(&z.stamp[c]) : group;
             const uint32_t rf = in ? load_wg(&z.ref[c]) : 1u;
+            const int32_t old = in ? z.node_of[c] : -1;
             const bool free_slot = in && st != group;
             const bool take = free_slot && rf == 0u;
             int64_t avail64;
@@ -1235,6 +1294,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             if (tid <= cut) {
                 if (take && er < need) {
                     s_victim[taken + er] = (int32_t)c;
+                    s_vold[taken + er] = old;
                     store_wg(&z.stamp[c], group);
                 } else if (free_slot && rf != 0u) {
                     store_wg(&z.ref[c], 0u);  // second chance
@@ -1249,7 +1309,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
         if (miss) {
             const int32_t c = rank < taken ? s_victim[rank] : -1;
             if (c >= 0) {
-                const int32_t old = z.node_of[c];
+                const int32_t old = s_vold[rank];
                 if (old >= 0) z.slot_of[old] = -1;
                 z.node_of[c] = n;
                 z.slot_of[n] = c;
@@ -1269,6 +1329,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
         z.miss_node[rank] = n;
         z.miss_row[rank] = kCache ? s_slot[tid] : tid;
         z.miss_off[rank] = off;
+        z.miss_dep[rank] = ndep;
     }
     if (tid == 0) {
         z.miss_off[M] = total;
@@ -1287,66 +1348,179 @@ __global__ void __launch_bounds__(kBlock) k_lazy_zero(LazyDev z, int64_t Wp) {
     for (int64_t c = threadIdx.x; c < Wp / 2; c += kBlock) p[c] = u32x4{0u, 0u, 0u, 0u};
 }
 
-// The rows of the group's misses: valid[n] from the suffix probes of n's
-// subtree only.  Candidate i of miss u is node m = n + 1 + (i - miss_off[u]),
-// a descendant d = depth(m) - depth(n) bytes below n (preorder: the subtree is
-// [n, sub_end[n])).  When d <= max_len and the last d bytes of prefix(m), the
-// path from n to m, are a token string, its ids are valid at n and are set in
-// the row with 64-bit atomics; every token valid at n ends its walk at exactly
-// one such m.  Grid-stride over all candidates of the group.
-__global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, uint64_t *dest, int64_t stride) {
-    __shared__ int64_t s_off[kLazyGroup + 1];
-    __shared__ int32_t s_node[kLazyGroup];
-    __shared__ int32_t s_row[kLazyGroup];
-    __shared__ int32_t s_dep[kLazyGroup];
-    const int32_t M = *z.miss_count;
-    if (M <= 0) return;
-    const int64_t total = z.miss_off[M];
-    const int64_t first = (int64_t)blockIdx.x * kBlock;
-    if (first >= total) return;
-    for (int i = threadIdx.x; i <= M; i += kBlock) s_off[i] = z.miss_off[i];
-    for (int i = threadIdx.x; i < M; i += kBlock) {
-        const int32_t n = z.miss_node[i];
-        s_node[i] = n;
-        s_row[i] = z.miss_row[i];
-        s_dep[i] = t.depth[n];
-    }
-    __syncthreads();
-    unsigned long long *out = reinterpret_cast<unsigned long long *>(dest);
-    for (int64_t i = first + threadIdx.x; i < total; i += (int64_t)gridDim.x * kBlock) {
-        int lo = 0, hi = M - 1;  // the last miss whose candidates start at or before i
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (s_off[mid] <= i)
-                lo = mid;
-            else
-                hi = mid - 1;
+// The hits of K independent suffixes (the one of d[k] bytes ending at blob
+// position pos[k], window (lo[k], hi[k]); act[k] false: none) with their
+// memory round trips issued together: short suffixes read short_hits, the
+// others their home bucket, then the payload (and pay_hi) of the first
+// fingerprint match; a length the home bucket does not settle falls back to
+// the general probe.
+template <int K>
+__device__ __forceinline__ void probe_batch(const DevTables &t, const int64_t (&pos)[K], const int (&d)[K],
+                                            const bool (&act)[K], const uint64_t (&lo)[K], const uint64_t (&hi)[K],
+                                            int32_t (&hit)[K]) {
+    uint64_t key[K];
+    bool hashed[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        hit[k] = -1;
+        hashed[k] = act[k] && d[k] > kShortLen;
+        key[k] = 0;
+        if (act[k] && d[k] <= kShortLen) hit[k] = short_hit(t, d[k], window_byte(lo[k], hi[k], 0), window_byte(lo[k], hi[k], 1));
+        if (hashed[k]) {
+            uint64_t h = kHashSeed;
+            for (int j = 0; j < d[k]; ++j)
+                h = hash_step(h, j < kWin ? window_byte(lo[k], hi[k], j) : (uint32_t)t.blob[pos[k] - j]);
+            key[k] = hash_final(h, (uint32_t)d[k]);
         }
-        const int32_t row = s_row[lo];
-        const int64_t m = (int64_t)s_node[lo] + 1 + (i - s_off[lo]);
-        const int d = t.depth[m] - s_dep[lo];
-        if (row < 0 || d > t.max_len || !has_len(t, d)) continue;
-        const int64_t pos = t.node_pos[m];
-        uint64_t wlo, whi;
-        load_window(t.blob, pos, wlo, whi);
-        uint64_t h = kHashSeed;
-        for (int k = 0; k < d; ++k) h = hash_step(h, k < kWin ? window_byte(wlo, whi, k) : (uint32_t)t.blob[pos - k]);
-        SlotPay mt;
-        const int32_t sl = probe(t, hash_final(h, (uint32_t)d), d, wlo, whi, pos, &mt);
-        if (sl < 0) continue;
-        const int32_t hx = hit_of_slot(sl, mt.first, mt.count);
-        unsigned long long *r = out + (int64_t)row * stride;
-        if (hx >= 0) {  // one token id (the common case)
-            atomicOr(r + (hx >> 6), 1ull << (hx & 63));
+    }
+    Bucket bk[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+        if (hashed[k]) bk[k] = load_bucket(t, home_bucket(t, key[k]));
+    uint32_t match[K], empty[K];
+    int32_t slot[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        match[k] = empty[k] = 0;
+        slot[k] = -1;
+        if (hashed[k]) {
+            bucket_masks(bk[k], fingerprint(key[k]), &match[k], &empty[k]);
+            if (match[k]) slot[k] = (int32_t)(home_bucket(t, key[k]) * kBucket + (uint64_t)__builtin_ctz(match[k]));
+        }
+    }
+    SlotPay p[K];
+    uint64_t phi[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        phi[k] = 0;
+        if (slot[k] >= 0) {
+            p[k] = t.pay[slot[k]];
+            if (d[k] > 8) phi[k] = t.pay_hi[slot[k]];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        if (!hashed[k]) continue;
+        if (slot[k] >= 0 && slot_equals(t, p[k], phi[k], d[k], lo[k], hi[k], pos[k])) {
+            hit[k] = hit_of_slot(slot[k], p[k].first, p[k].count);
+        } else if (!(empty[k] != 0 && (match[k] & (match[k] - 1)) == 0)) {
+            SlotPay mt;  // the home bucket does not settle it
+            const int32_t sl = probe(t, key[k], d[k], lo[k], hi[k], pos[k], &mt);
+            if (sl >= 0) hit[k] = hit_of_slot(sl, mt.first, mt.count);
+        }
+    }
+}
+
+// The candidates of misses: candidate i of miss u is node m = n + 1 + (i -
+// miss_off[u]) for the misses the pass covers, a descendant d = depth(m) -
+// depth(n) bytes below n (preorder: the subtree is [n, sub_end[n])).  When
+// d <= max_len and the last d bytes of prefix(m), the path from n to m, are a
+// token string, its ids are valid at n; every token valid at n ends its walk
+// at exactly one such m.  set(row, id) records a valid id.
+template <typename F>
+__device__ __forceinline__ void lazy_candidates(const DevTables &t, const int64_t (&m)[kLazyBatch],
+                                                const int (&dep)[kLazyBatch], bool (&act)[kLazyBatch],
+                                                const int32_t (&row)[kLazyBatch], F &&set) {
+    constexpr int K = kLazyBatch;
+    int dm[K], d[K];
+    int64_t pos[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) dm[k] = act[k] ? t.depth[m[k]] : 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        d[k] = dm[k] - dep[k];
+        act[k] = act[k] && row[k] >= 0 && d[k] <= t.max_len && has_len(t, d[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) pos[k] = act[k] ? t.node_pos[m[k]] : 0;
+    uint64_t wlo[K], whi[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        wlo[k] = whi[k] = 0;
+        if (act[k]) load_window(t.blob, pos[k], wlo[k], whi[k]);
+    }
+    int32_t hx[K];
+    probe_batch<K>(t, pos, d, act, wlo, whi, hx);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        if (hx[k] == -1) continue;
+        if (hx[k] >= 0) {  // one token id (the common case)
+            set(row[k], hx[k]);
             continue;
         }
-        const SlotPay pm = t.pay[sl];  // a string with several ids
+        const SlotPay pm = t.pay[-2 - hx[k]];  // a string with several ids
         int32_t v = pm.first;
-        for (int k = 0; k < (int)pm.count; ++k) {
-            atomicOr(r + (v >> 6), 1ull << (v & 63));
+        for (int j = 0; j < (int)pm.count; ++j) {
+            set(row[k], v);
             v = t.dup_next[v];
         }
     }
+}
+
+// The grid-stride pass over the candidates of the misses miss_off covers,
+// with 64-bit atomics into the zeroed rows dest + row * stride; block bx of nbx,
+// kLazyBatch candidates per thread and round with their loads issued together.
+// LDS of the pass: the misses' candidate offsets, nodes, rows and depths.
+struct LazyMisses {
+    int64_t off[kLazyGroup + 1];
+    int32_t node[kLazyGroup], row[kLazyGroup], dep[kLazyGroup];
+};
+
+__device__ __forceinline__ void lazy_probe_pass(const DevTables &t, const LazyDev &z, uint64_t *dest, int64_t stride,
+                                                int64_t bx, int64_t nbx, LazyMisses &sm) {
+    constexpr int K = kLazyBatch;
+    int64_t *s_off = sm.off;
+    int32_t *s_node = sm.node, *s_row = sm.row, *s_dep = sm.dep;
+    const int32_t M = *z.miss_count;
+    if (M <= 0) return;
+    const int64_t total = z.miss_off[M];
+    const int64_t first = bx * kBlock;
+    if (first >= total) return;
+    for (int i = threadIdx.x; i <= M; i += kBlock) s_off[i] = z.miss_off[i];
+    for (int i = threadIdx.x; i < M; i += kBlock) {
+        s_node[i] = z.miss_node[i];
+        s_row[i] = z.miss_row[i];
+        s_dep[i] = z.miss_dep[i];
+    }
+    __syncthreads();
+    unsigned long long *out = reinterpret_cast<unsigned long long *>(dest);
+    const int64_t threads = nbx * kBlock;
+    for (int64_t base = first + threadIdx.x; base < total; base += K * threads) {
+        int64_t m[K];
+        int32_t row[K];
+        int dep[K];
+        bool act[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int64_t i = base + k * threads;
+            act[k] = i < total;
+            row[k] = -1;
+            m[k] = 0;
+            dep[k] = 0;
+            if (!act[k]) continue;
+            int lo = 0, hi = M - 1;  // the last miss whose candidates start at or before i
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_off[mid] <= i)
+                    lo = mid;
+                else
+                    hi = mid - 1;
+            }
+            row[k] = s_row[lo];
+            m[k] = (int64_t)s_node[lo] + 1 + (i - s_off[lo]);
+            dep[k] = s_dep[lo];
+        }
+        lazy_candidates(t, m, dep, act, row, [&](int32_t r, int32_t v) {
+            atomicOr(out + (int64_t)r * stride + (v >> 6), 1ull << (v & 63));
+        });
+    }
+}
+
+// The rows of the group's misses, in the zeroed cache rows (tam_apply_mask)
+// or straight into the zeroed output rows (tam_export_rows).
+__global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, uint64_t *dest, int64_t stride) {
+    __shared__ LazyMisses sm;
+    lazy_probe_pass(t, z, dest, stride, blockIdx.x, gridDim.x, sm);
 }
 
 __global__ void __launch_bounds__(kBlock) k_fill_u64(uint64_t *p, int64_t n, uint64_t value) {
@@ -1547,7 +1721,7 @@ hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t
                              void *logits, int dtype, int64_t row_stride, hipStream_t s) {
     if (nb <= 0) return hipSuccess;
     if (nb > kLazyGroup || nb > z.C || !t.sub_end) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.N, z, node_ids,
+    hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.depth, t.N, z, node_ids,
                        (int32_t)nb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1575,7 +1749,7 @@ hipError_t launch_lazy_export(const DevTables &t, const LazyDev &z, const int32_
                        0, s, out, words, 0ull);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_assign<false>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.N, z, node_ids,
+    hipLaunchKernelGGL(k_lazy_assign<false>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.depth, t.N, z, node_ids,
                        (int32_t)nb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -248,6 +248,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     const size_t o_blob = a.take<uint8_t>((int64_t)v->tok_blob.size());
     const size_t o_fps = a.take<uint16_t>((int64_t)v->fps.size());
     const size_t o_pay = a.take<tam::SlotPay>((int64_t)v->pay.size());
+    const size_t o_pay_hi = a.take<uint64_t>((int64_t)v->pay_hi.size());
+    const size_t o_short = a.take<int32_t>((int64_t)v->short_hits.size());
     const size_t o_dup = a.take<int32_t>(V);
     const size_t o_len = a.take<uint8_t>((int64_t)v->len_present.size());
     uint8_t *base = static_cast<uint8_t *>(alloc_with(v->own_alloc, v->alloc, a.used));
@@ -261,6 +263,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     v->d_tok_blob = base + o_blob;
     v->d_fps = reinterpret_cast<const uint16_t *>(base + o_fps);
     v->d_pay = reinterpret_cast<const tam::SlotPay *>(base + o_pay);
+    v->d_pay_hi = reinterpret_cast<const uint64_t *>(base + o_pay_hi);
+    v->d_short_hits = reinterpret_cast<const int32_t *>(base + o_short);
     v->d_dup_next = reinterpret_cast<const int32_t *>(base + o_dup);
     v->d_len_present = base + o_len;
     auto up = [&](size_t off, const void *src, size_t bytes) -> hipError_t {
@@ -271,6 +275,8 @@ tam_status vocab_create(const uint8_t *tok_bytes, const int64_t *tok_off, int64_
     if (e == hipSuccess) e = up(o_blob, v->tok_blob.data(), v->tok_blob.size());
     if (e == hipSuccess) e = up(o_fps, v->fps.data(), v->fps.size() * sizeof(uint16_t));
     if (e == hipSuccess) e = up(o_pay, v->pay.data(), v->pay.size() * sizeof(tam::SlotPay));
+    if (e == hipSuccess) e = up(o_pay_hi, v->pay_hi.data(), v->pay_hi.size() * sizeof(uint64_t));
+    if (e == hipSuccess) e = up(o_short, v->short_hits.data(), v->short_hits.size() * sizeof(int32_t));
     if (e == hipSuccess) e = up(o_dup, v->dup_next.data(), v->dup_next.size() * 4);
     if (e == hipSuccess) e = up(o_len, v->len_present.data(), v->len_present.size());
     if (e == hipSuccess) e = hipEventCreateWithFlags(&v->ready, hipEventDisableTiming);
@@ -444,6 +450,8 @@ void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v,
     t.tok_blob = v->d_tok_blob;
     t.fps = v->d_fps;
     t.pay = v->d_pay;
+    t.pay_hi = v->d_pay_hi;
+    t.short_hits = v->d_short_hits;
     t.dup_next = v->d_dup_next;
     t.len_present = v->d_len_present;
     t.table = nullptr;
@@ -742,6 +750,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_miss_node = a.take<int32_t>(G);
     const size_t o_miss_row = a.take<int32_t>(G);
     const size_t o_miss_off = a.take<int64_t>(G + 1);
+    const size_t o_miss_dep = a.take<int32_t>(G);
     const size_t o_miss_count = a.take<int32_t>(1);
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
@@ -781,6 +790,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         z.miss_node = reinterpret_cast<int32_t *>(base + o_miss_node);
         z.miss_row = reinterpret_cast<int32_t *>(base + o_miss_row);
         z.miss_off = reinterpret_cast<int64_t *>(base + o_miss_off);
+        z.miss_dep = reinterpret_cast<int32_t *>(base + o_miss_dep);
         z.miss_count = reinterpret_cast<int32_t *>(base + o_miss_count);
         z.err = h->d_err;
         z.C = C;
@@ -907,6 +917,8 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
     t.tok_blob = vocab->d_tok_blob;
     t.fps = vocab->d_fps;
     t.pay = vocab->d_pay;
+    t.pay_hi = vocab->d_pay_hi;
+    t.short_hits = vocab->d_short_hits;
     t.dup_next = vocab->d_dup_next;
     t.len_present = vocab->d_len_present;
     t.table = table;

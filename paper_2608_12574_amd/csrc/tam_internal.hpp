@@ -147,6 +147,8 @@ struct tam_vocab {
     std::vector<uint8_t> len_present;
     tam::hvec<uint16_t> fps;
     tam::hvec<tam::SlotPay> pay;
+    tam::hvec<uint64_t> pay_hi;
+    tam::hvec<int32_t> short_hits;
     tam::hvec<int32_t> dup_next;
     std::vector<int64_t> dup_cum;  // [max_len+1] see build_vocab (list size bound)
 
@@ -156,6 +158,8 @@ struct tam_vocab {
     const uint8_t *d_tok_blob = nullptr;
     const uint16_t *d_fps = nullptr;
     const tam::SlotPay *d_pay = nullptr;
+    const uint64_t *d_pay_hi = nullptr;
+    const int32_t *d_short_hits = nullptr;
     const int32_t *d_dup_next = nullptr;
     const uint8_t *d_len_present = nullptr;
     hipEvent_t ready = nullptr;  // recorded after the uploads
