@@ -44,7 +44,9 @@ os.environ.setdefault("OMP_WAIT_POLICY", "PASSIVE")
 
 METRIC = "compile ms + (node,token) pairs/s; mask-apply GB/s at B=256 (bit-exact)"
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
-FLAGS = {"full": 0, "tail": 8, "lists": 2}  # TAM_FLAG_TAIL_LISTS, TAM_FLAG_NO_TABLE
+# TAM_FLAG_TAIL_LISTS (8), TAM_FLAG_NO_TABLE (2); tail_lists = tail compression
+# without a table (the branching nodes keep sparse lists)
+FLAGS = {"full": 0, "tail": 8, "lists": 2, "tail_lists": 10}
 
 
 def parse():
@@ -53,11 +55,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4)
-    ap.add_argument("--repr", choices=["auto", "full", "tail", "lists"], default="auto",
+    ap.add_argument("--repr", choices=["auto", "full", "tail", "lists", "tail_lists"], default="auto",
                     help="mask representation of the headline figures: full dense table, tail "
-                         "compression, or lists only; auto = full for one set, lists for a forest")
+                         "compression (dense rows for branching nodes), lists only, or tail "
+                         "compression with lists for the branching nodes; auto = full for one set, "
+                         "tail_lists for a forest")
     ap.add_argument("--no-secondary", action="store_true",
-                    help="skip the second (tail compression) measurement")
+                    help="skip the other representations (tail compression; for a forest lists and "
+                         "tail compression) and the rows built on demand")
     ap.add_argument("--apply-iters", type=int, default=1000)
     ap.add_argument("--apply-warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -358,9 +363,11 @@ class Bench:
         apply_step_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
         adv_step_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
 
-        # the device phases alone: zero fill, probe pass (marks), lists
+        # the device phases alone: zero fill, probe pass (marks, or list
+        # counts), the whole lists phase (probe pass, prefix sum, fill)
         alone = {}
-        for name, ph in (("zero", P.PHASE_ZERO), ("probe_marks", P.PHASE_MARK), ("lists", P.PHASE_LISTS)):
+        for name, ph in (("zero", P.PHASE_ZERO), ("probe_marks", P.PHASE_MARK), ("probe_counts", P.PHASE_COUNT),
+                         ("lists", P.PHASE_LISTS)):
             try:
                 h.rebuild(phases=ph)
             except P.TamError:
@@ -478,17 +485,31 @@ class Bench:
 
         apply_graph_us = self.graph_us(apply_next, 100)
 
-        # the dominant compile kernel and its algorithmic bytes
-        if rep == "lists":
-            kernel, nbytes, kms = "k_probe+k_scan+k_fill", (M + N + 1) * 4, alone.get("lists", dev_ms)
-        elif rep == "full" or alone.get("zero", 0.0) >= alone.get("probe_marks", 0.0):
-            kernel, nbytes, kms = "k_zero", h.dense_rows * Wd * 8, alone["zero"]
-        else:
-            # tail compression: the probe pass writes the hits that hold the
-            # tails' masks (4 bytes per node and suffix length <= 16)
-            lw = np.minimum(np.minimum(h.depth, h.max_token_len), 16)
-            kernel, nbytes, kms = "k_probe", 4 * int(lw.sum()), alone["probe_marks"]
-        traffic = load_traffic(f"{kernel}_{w.name}_{rep}_traffic.json", sha=kernels_sha())
+        # the compile kernels, each with its algorithmic bytes: the zero fill
+        # writes the dense rows; the probe pass writes the hits, 4 bytes per node
+        # and suffix length <= 16 (they hold the tails' masks and feed the
+        # lists); the lists' prefix sum and fill write row offsets and entries
+        lw = np.minimum(np.minimum(h.depth, h.max_token_len), 16)
+        hit_bytes = 4 * int(lw.sum())
+        sha = kernels_sha()
+        kernels = {}
+        if "zero" in alone and h.dense_rows:
+            kernels["k_zero"] = hbm_roofline("k_zero", h.dense_rows * Wd * 8, alone["zero"],
+                                             load_traffic(f"k_zero_{w.name}_{rep}_traffic.json", sha))
+        probe_ms = alone.get("probe_marks", alone.get("probe_counts"))
+        if probe_ms is not None:
+            kernels["k_probe"] = hbm_roofline("k_probe", hit_bytes, probe_ms,
+                                              load_traffic(f"k_probe_{w.name}_{rep}_traffic.json", sha))
+        if "lists" in alone and "probe_counts" in alone:
+            listed = M if rep == "lists" else None  # plain lists hold every valid pair
+            ms = max(alone["lists"] - alone["probe_counts"], 1e-6)
+            kernels["k_scan+k_fill"] = {"kernel": "k_scan_*+k_fill", "avg_launch_ms": round(ms, 4),
+                                        "algorithmic_bytes": None if listed is None else int((listed + N + 1) * 4),
+                                        "achieved": None if listed is None else
+                                        round((listed + N + 1) * 4 / (ms * 1e-3) / 1e9, 1), "unit": "GB/s"}
+        # the dominant one (longest launch) is the line's roofline
+        dom = max((k for k in kernels if k in ("k_zero", "k_probe")), key=lambda k: kernels[k]["avg_launch_ms"])
+        roofline = kernels[dom]
         # work of the validity computation: the suffix probes made here, and the
         # (node, token) pairs a walk over first-byte token buckets would test
         tb, to = self.packed_vocab
@@ -502,7 +523,8 @@ class Bench:
             "ms_per_step": round(ms_step, 4),
             "N": N, "dense_rows": h.dense_rows, "valid_pairs": M,
             "device_bytes": h.device_bytes,
-            "roofline": hbm_roofline(kernel, nbytes, kms, traffic),
+            "roofline": roofline,
+            "rooflines_per_kernel": kernels,
             "compile_work": work,
             "compile_ms": {"device": round(dev_ms, 4),
                            "device_alone": {k: round(v, 4) for k, v in alone.items()},
@@ -734,7 +756,7 @@ def main():
     gen_s = time.time() - t
     K, V, B = w.K, w.V, w.batch
     forest = w.set_offsets is not None
-    rep = args.repr if args.repr != "auto" else ("lists" if forest else "full")
+    rep = args.repr if args.repr != "auto" else ("tail_lists" if forest else "full")
     print(f"[bench] workload {w.name}: K={K} V={V} B={B} ({gen_s:.1f}s to generate)", flush=True)
 
     bench = Bench(args, torch, P, W, w, dev)
@@ -795,16 +817,25 @@ def main():
         f"{k} {v['device_ms'] * 1e3:.0f} us device / {v['compile_warm_ms']:.2f} ms" for k, v in formats.items()),
         flush=True)
 
-    secondary = None
-    if not args.no_secondary and rep != "tail":
-        h2, secondary = bench.measure("tail", args.steps, args.warmup, cold_runs=0)
-        h2.close()
+    # the other representations of the same workload
+    others = {}
+    if not args.no_secondary:
+        for r2 in (["lists", "tail"] if forest else ["tail"]):
+            if r2 == rep:
+                continue
+            h2, others[r2] = bench.measure(r2, args.steps, args.warmup, cold_runs=0)
+            h2.close()
+    secondary = others.get("tail")
 
     N, M = main_res["N"], main_res["valid_pairs"]
     result = {
         "metric": METRIC,
         "value": main_res["value"],
         "unit": "(node,token) pairs/s",
+        "value_note": ("(node, token) pairs resolved per second of the device step; the full table stores one "
+                       "bit per pair (roofline 8 pairs per byte x 8 TB/s = 6.4e13 pairs/s), while tail "
+                       "compression and lists store no bit for most pairs, so their pairs/s is not comparable "
+                       "to that roofline"),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -817,7 +848,8 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "repr": rep, "K": K, "V": V, "N": N, "B": B,
                    "logits_dtype": w.dtype, "num_sets": w.num_sets, "valid_pairs": M},
         "roofline": main_res["roofline"],
-        "roofline_apply": {"kernel": "k_apply", "bound": "hbm", "achieved": main_res["apply"]["GBps"],
+        "roofline_apply": {"kernel": "k_apply_dense" if rep == "full" else "k_apply", "bound": "hbm",
+                           "achieved": main_res["apply"]["GBps"],
                            "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                            "frac": main_res["apply"]["frac_of_hbm_roofline"],
                            "traffic": (load_traffic(f"k_apply_{w.name}_{rep}_traffic.json", sha) or {})
@@ -836,6 +868,7 @@ def main():
         "apply_us_graph": main_res["apply_us_graph"],
         "device_bytes": main_res["device_bytes"],
         "tail_compression": secondary,
+        "sparse_lists": others.get("lists"),
         "lazy_rows": lazy,
         "char_position_masks": formats,
         "fill_GBps_4GiB": round(fill_gbps, 1),
@@ -843,7 +876,7 @@ def main():
                       f"{len(bench.sample[0])} oracle rows drawn uniformly over the trie; apply and advance on the "
                       f"timed batch and on {B} sampled rows",
                       rep: main_res["bit_exact"],
-                      "tail": None if secondary is None else secondary["bit_exact"],
+                      **{r2: others[r2]["bit_exact"] for r2 in others},
                       "lazy": None if lazy is None else lazy["bit_exact"]},
         "kernels_sha": sha,
     }

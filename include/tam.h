@@ -108,7 +108,10 @@ enum {
      * the probe pass; tokens longer than 16 bytes go to per-node lists.
      * Results are identical to the full table, which holds dense_rows rows
      * instead of N (c. 2.5% of the nodes of a set of 10,000 code-like
-     * strings).  Ignored with TAM_FLAG_NO_TABLE. */
+     * strings).  With TAM_FLAG_NO_TABLE there is no table at all: the
+     * branching nodes keep sparse valid lists instead of dense rows (the
+     * tails still read theirs from the probe hits), so a forest of many
+     * per-query sets lists only 1-2% of its nodes. */
     TAM_FLAG_TAIL_LISTS = 1u << 3,
     /* Rows built on demand (the lazy computation of the Appendix's memory
      * discussion, with the matching restricted to the subtree below the
@@ -161,10 +164,12 @@ typedef struct {
     const uint8_t *edge_byte; /* [N] byte on the edge into the node (roots: 0) */
     const uint8_t *is_final;  /* [N] 1 if the node is reached by the terminator */
     const uint64_t *table;    /* device [dense_rows][row_stride_words]; NULL with TAM_FLAG_NO_TABLE */
-    int64_t dense_rows;       /* rows of `table`: N, or the branching nodes with TAM_FLAG_TAIL_LISTS, or 0 */
-    const int32_t *dense_row; /* [N] table row of each node (>= 0); for a tail node a,
-                                 -1 - (number of nodes below a).  NULL when row = node id
-                                 (full table) or there is no table */
+    int64_t dense_rows;       /* rows of `table`: N, or the branching nodes with TAM_FLAG_TAIL_LISTS,
+                                 or 0 without a table */
+    const int32_t *dense_row; /* [N] with TAM_FLAG_TAIL_LISTS: table row (or, with
+                                 TAM_FLAG_NO_TABLE, number) of each branching node (>= 0);
+                                 for a tail node a, -1 - (number of nodes below a).  NULL
+                                 otherwise */
     int64_t cache_rows;        /* TAM_FLAG_LAZY_ROWS: rows of the row cache (else 0) */
     const int32_t *subtree_end; /* [N] with TAM_FLAG_LAZY_ROWS: one past the last node of the
                                  node's subtree (preorder ids); else NULL */
@@ -286,7 +291,11 @@ enum {
                                   with TAM_PHASE_MARK one probe pass serves both */
     TAM_PHASE_ZERO = 1u << 1,  /* zero fill of the dense table */
     TAM_PHASE_MARK = 1u << 2,  /* suffix probes setting the valid bits of the zeroed table */
-    TAM_PHASE_TABLE = TAM_PHASE_ZERO | TAM_PHASE_MARK
+    TAM_PHASE_TABLE = TAM_PHASE_ZERO | TAM_PHASE_MARK,
+    TAM_PHASE_COUNT = 1u << 3  /* (with lists) the probe pass that writes the hits and counts the
+                                  lists, without the prefix sum and fill: the lists already built
+                                  stay as they are (the pass recomputes the same hits); for timing
+                                  the probe pass alone */
 };
 
 /*
@@ -294,8 +303,9 @@ enum {
  * device tables (bit-identical result).  `phases` is a TAM_PHASE_* mask; 0 =
  * the handle's default: TAM_PHASE_TABLE for a table (TAM_PHASE_MARK for a
  * format handle, which recomputes every word of its rows), TAM_PHASE_LISTS with
- * TAM_FLAG_NO_TABLE, both with TAM_FLAG_TAIL_LISTS when the vocabulary has
- * tokens longer than 16 bytes.  A phase the handle does not keep returns
+ * TAM_FLAG_NO_TABLE (with or without TAM_FLAG_TAIL_LISTS), both with
+ * TAM_FLAG_TAIL_LISTS and a table when the vocabulary has tokens longer than
+ * 16 bytes.  A phase the handle does not keep returns
  * TAM_E_STATE.  TAM_PHASE_MARK without TAM_PHASE_ZERO ORs the
  * same bits into the current table.  Used to time the device phase kernel by
  * kernel.  With TAM_FLAG_LAZY_ROWS the only phase is 0: it empties the row

@@ -120,6 +120,8 @@ struct DevTables {
     int64_t R;                  // dense rows (N for a full table, 0 without one)
     int32_t tail_long;          // tail compression with tokens longer than kWin: their hits on
                                 // tails go to the lists (row_ptr / entries)
+    int32_t tail_lists;         // tail compression without a table: the branching nodes' hits go
+                                // to the lists, with the tails' tokens longer than kWin
     int64_t blob_bytes;
     uint64_t slot_mask;         // slots - 1 (slots = a power of two, >= kBucket)
     uint64_t len_mask;          // bit d (d < 64): some token has length d

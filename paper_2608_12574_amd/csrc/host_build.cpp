@@ -373,7 +373,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->blob.resize((size_t)BB);  // the parts fill all but the outer pads
     h->strs.resize((size_t)h->K_unique);
     const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
-    const bool tails = (h->flags & TAM_FLAG_TAIL_LISTS) && !(h->flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
+    const bool tails = (h->flags & TAM_FLAG_TAIL_LISTS) && !(h->flags & TAM_FLAG_LAZY_ROWS);
     h->sub_end.resize(subtrees ? (size_t)N : 0);
     h->row_of.resize(tails ? (size_t)N : 0);
     h->tail_span.resize(tails ? (size_t)N : 0);
@@ -640,17 +640,21 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     const int64_t L = v->max_tok_len;
     const std::vector<int64_t> &cum = v->dup_cum;
-    // A hit at distance d above node m lands in a list iff d <= the node's list
-    // span; with tail compression only the hits longer than the probe window do
-    // (the shorter ones are read straight from the probe's hits).
+    // Which hits at distance d above node m land in lists: all of them (lists
+    // only); with tail compression and a table, those on the tails above m
+    // (d <= tail_span[m]) longer than the probe window; with tail compression
+    // and no table, also every hit on a branching ancestor (d > tail_span[m]).
     const bool split = !h->tail_span.empty();
+    const bool branching_listed = split && (h->flags & TAM_FLAG_NO_TABLE);
     const int64_t chunk = 1 << 16, nchunks = (h->N + chunk - 1) / chunk;
     std::vector<int64_t> part((size_t)nchunks, 0);
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         int64_t b = 0;
         for (int64_t m = c * chunk; m < std::min(h->N, (c + 1) * chunk); ++m) {
+            const int64_t all = std::min<int64_t>(h->depth[(size_t)m], L);
             const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
             b += cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
+            if (branching_listed) b += cum[(size_t)all] - cum[(size_t)span];
         }
         part[(size_t)c] = b;
     });

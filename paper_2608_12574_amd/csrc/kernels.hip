@@ -336,7 +336,11 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
 //     blob position; not a tail) is OR-ed into the zeroed table with a 64-bit
 //     atomic, and each block writes the number of valid (node, token) pairs its
 //     hits make, tails included, into pairs[blockIdx.x].
-//   kCount (lists): the listed hits are counted per node.
+//   kCount (lists): the listed hits are counted per node: every hit (lists
+//     only); with tail compression and a table, the tails' hits of tokens
+//     longer than the window; with tail compression and no table (tail_lists),
+//     also every hit on a branching node, and each block then writes its
+//     number of valid pairs as do_mark does.
 // The grid covers the nodes [m0, m1): every node of the handle, or (lists of a
 // forest) one group of whole sets, whose nodes' ancestors are in the group too.
 template <bool kCount>
@@ -354,6 +358,7 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
         const int lspan = kCount ? list_span(t, m) : 0;              // listed up to here
         const int sspan = t.row_of ? 0 : lspan;                      // short hits listed up to here
         const int mspan = do_mark ? (t.tail_span ? t.tail_span[m] : 0) : INT_MAX;  // marked beyond
+        const int bspan = kCount && t.tail_lists ? t.tail_span[m] : INT_MAX;      // (no table) listed beyond
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
         // one hit: the pairs it makes (do_mark), marked at table row `row` (>= 0),
         // counted for list node `ln` (>= 0)
@@ -383,7 +388,7 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
 #pragma unroll
             for (int j = 0; j < kPer; ++j) {
                 const int d = d0 + j + 1;
-                n[j] = kCount && hit[j] != -1 && d <= sspan ? t.node_at[pos - d] : -1;
+                n[j] = kCount && hit[j] != -1 && (d <= sspan || d > bspan) ? t.node_at[pos - d] : -1;
                 r[j] = hit[j] != -1 && d > mspan ? t.row_at[pos - d] : -1;
             }
 #pragma unroll
@@ -394,12 +399,13 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
                 if (hit[j] != -1) take(hit[j], r[j], n[j]);
         }
         // tokens longer than the window (rare), by the node's last lane
-        if (d0 + kPer == kWin && L > kWin && (do_mark || lspan > kWin))
+        if (d0 + kPer == kWin && L > kWin && (do_mark || lspan > kWin || (kCount && t.tail_lists)))
             long_hits(t, pos, L, [&](int32_t hx, int d) {
-                take(hx, d > mspan ? t.row_at[pos - d] : -1, d <= lspan ? t.node_at[pos - d] : -1);
+                take(hx, d > mspan ? t.row_at[pos - d] : -1,
+                     d <= lspan || (kCount && t.tail_lists) ? t.node_at[pos - d] : -1);
             });
     }
-    if (!do_mark) return;
+    if (!do_mark && !(kCount && t.tail_lists)) return;
     // block sum of the pairs
     __shared__ int32_t wsum[kBlock / kWave];
     for (int o = kWave / 2; o > 0; o >>= 1) found += __shfl_xor(found, o, kWave);
@@ -413,7 +419,8 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
 }
 
 // Fill pass (lists): the hits' token ids written into the per-node lists (with
-// tail compression only those of tokens longer than the window).
+// tail compression those of tokens longer than the window, and without a
+// table also those on branching nodes).
 __global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
     const int64_t m = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (m >= t.N) return;
@@ -423,15 +430,17 @@ __global__ void __launch_bounds__(kBlock) k_fill(DevTables t) {
     const int Lw = min(L, kWin);
     const int span = list_span(t, m);
     const int Ls = t.row_of ? 0 : min(Lw, span);  // tail compression lists long hits only
+    const int bspan = t.tail_lists ? t.tail_span[m] : INT_MAX;  // no table: branching nodes' hits too
     int32_t s[kWin];
 #pragma unroll
-    for (int d = 1; d <= kWin; ++d) s[d - 1] = d <= Ls ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
+    for (int d = 1; d <= kWin; ++d)
+        s[d - 1] = d <= Lw && (d <= Ls || d > bspan) ? t.hits[(int64_t)(d - 1) * t.N + m] : -1;
 #pragma unroll
     for (int d = 1; d <= kWin; ++d)
         if (s[d - 1] != -1) emit(t, s[d - 1], t.node_at[pos - d]);
-    if (L > kWin && span > kWin)
+    if (L > kWin && (span > kWin || t.tail_lists))
         long_hits(t, pos, L, [&](int32_t hx, int d) {
-            if (d <= span) emit(t, hx, t.node_at[pos - d]);
+            if (d <= span || t.tail_lists) emit(t, hx, t.node_at[pos - d]);
         });
 }
 
@@ -676,7 +685,8 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
     int64_t trow = live ? n : -1;
     if (kMode == kApplyTail && live) trow = t.row_of[n];
     const bool tail_row = kMode == kApplyTail && live && trow < 0;
-    const bool use_list = kMode == kApplyLists;
+    // lists: every row; tail compression without a table: the branching rows
+    const bool use_list = kMode == kApplyLists || (kMode == kApplyTail && !tail_row && t.table == nullptr);
 
     uint32_t bits[kApplyUnits];
 #pragma unroll
@@ -700,7 +710,7 @@ __global__ void __launch_bounds__(kBlock) k_apply(DevTables t, const int32_t *__
                 v = t.dup_next[v];
             }
         }
-        if (t.tail_long) {  // tokens longer than the window: the tail's list
+        if (t.tail_long || t.tail_lists) {  // tokens longer than the window: the tail's list
             const int32_t e0 = t.row_ptr[n], e1 = t.row_ptr[n + 1];
             for (int32_t k0 = e0; k0 < e1; k0 += kWave) {
                 const uint32_t rel = k0 + lane < e1 ? (uint32_t)t.entries[k0 + lane] - lo : 0xffffffffu;
@@ -1125,12 +1135,13 @@ __global__ void __launch_bounds__(kBlock) k_row_counts(DevTables t, const int32_
     const int32_t n = nodes[r];
     int32_t c = 0;
     if (n >= 0 && (int64_t)n < t.N) {
-        const int64_t trow = t.table ? (t.row_of ? (int64_t)t.row_of[n] : (int64_t)n) : -1;
-        if (trow >= 0) {
+        const int64_t trow = t.row_of ? (int64_t)t.row_of[n] : (int64_t)n;
+        const bool tail = t.row_of && trow < 0;
+        if (t.table && !tail) {
             const uint64_t *row = t.table + trow * t.Wp;
             for (int64_t w = lane; w < t.W; w += kWave) c += __popcll(row[w]);
         } else {
-            if (t.table) {  // a tail: the token of length d starting below it is the hit of node n + d
+            if (tail) {  // a tail: the token of length d starting below it is the hit of node n + d
                 const int Lt = min(min(-1 - (int)trow, kWin), (int)t.max_len);
                 const int32_t x = lane < Lt ? t.hits[(int64_t)lane * t.N + n + lane + 1] : -1;
                 c = x >= 0 ? 1 : (x <= -2 ? (int32_t)t.pay[-2 - x].count : 0);
@@ -1664,7 +1675,7 @@ hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, 
     const int vec = ((reinterpret_cast<uintptr_t>(logits) & 15) == 0 && ((row_stride * elem) & 15) == 0)
                         ? 1
                         : 0;
-    const int mode = t.table == nullptr ? kApplyLists : (t.row_of ? kApplyTail : kApplyTable);
+    const int mode = t.row_of ? kApplyTail : (t.table ? kApplyTable : kApplyLists);
     if (mode == kApplyTable && vec) {
         const int64_t gx1 = grid_for(nchunks, kBlock);
         // grid.y (row groups) is limited to 65535 per launch
@@ -1769,6 +1780,12 @@ hipError_t launch_lazy_reset(const DevTables &t, const LazyDev &z, hipStream_t s
 hipError_t launch_row_counts(const DevTables &t, const int32_t *node_ids, int64_t n, int32_t *out, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_row_counts, dim3(grid_for(n, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_export_tail(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out, hipStream_t s) {
+    if (n <= 0 || !t.row_of) return hipSuccess;
+    hipLaunchKernelGGL(k_export_tail, dim3(grid_for(n, kBlock / kWave)), dim3(kBlock), 0, s, t, node_ids, n, out);
     return hipGetLastError();
 }
 

@@ -392,6 +392,7 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
         return TAM_OK;
     }
     const bool lists = (phases & TAM_PHASE_LISTS) != 0;
+    const bool count_only = !lists && (phases & TAM_PHASE_COUNT) != 0;  // the probe pass of the lists alone
     const bool zero = (phases & TAM_PHASE_ZERO) && t.table && !zero_enqueued;
     const bool mark = (phases & TAM_PHASE_MARK) && t.table;
     // lists_counted: the list counts were made group by group while the host
@@ -402,11 +403,11 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
         if (timing && !zero_enqueued) TAM_HIP(hipEventRecord(h->ev[1], s));
         if (timing && zero_enqueued) TAM_HIP(hipEventRecord(h->ev[4], s));  // the probe's own start
         if (timing) h->mark_from_ev4 = zero_enqueued;
-        if (lists) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
+        if (lists || count_only) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
         if (t.fmt_L >= 0) {
             if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
-        } else if (lists || mark) {
-            TAM_HIP(tam::launch_probe(t, lists, mark, h->pairs, s));
+        } else if (lists || count_only || mark) {
+            TAM_HIP(tam::launch_probe(t, lists || count_only, mark, h->pairs, s));
         }
         if (timing) TAM_HIP(hipEventRecord(h->ev[2], s));
     } else if (timing) {
@@ -461,6 +462,7 @@ void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v,
     t.row_at = t.node_at;
     t.R = 0;
     t.tail_long = 0;
+    t.tail_lists = 0;
     t.N = h->N;
     t.V = v->V;
     t.W = v->W;
@@ -519,11 +521,14 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     uint8_t *trie_base = nullptr;
     size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
            o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0;
-    const bool split = (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & (TAM_FLAG_NO_TABLE | TAM_FLAG_LAZY_ROWS));
+    // tail compression's split (with a table for the branching nodes, or with
+    // sparse lists for them)
+    const bool split = (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_LAZY_ROWS);
     // Lists (no table): the probe pass that counts each node's list runs group
     // by group, right after each group's upload (a node's ancestors are in its
     // own set), so only the last group's counts follow the host build.
-    const bool early_count = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & TAM_FLAG_LAZY_ROWS);
+    const bool early_count =
+        !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & (TAM_FLAG_LAZY_ROWS | TAM_FLAG_TAIL_LISTS));
     size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0, o_strs = 0, o_err = 0;
     tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
@@ -719,8 +724,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const auto t0 = std::chrono::steady_clock::now();
     const bool lazy = is_lazy(h);
     const bool want_table = !lazy && !(h->flags & TAM_FLAG_NO_TABLE);
-    const bool tails = want_table && !h->tail_span.empty();
-    const bool tail_long = tails && vocab->max_tok_len > tam::kWin;
+    const bool tails = !lazy && !h->tail_span.empty();
+    const bool tail_long = tails && want_table && vocab->max_tok_len > tam::kWin;
+    const bool tail_lists = tails && !want_table;  // branching nodes keep sparse lists
     const bool want_lists = !want_table || tail_long;
     // dense rows: every node, or the branching nodes (at least one row is kept
     // so that a tail-compressed handle always has a table)
@@ -800,6 +806,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.row_at = tails ? reinterpret_cast<const int32_t *>(trie_base + o_row_at) : t.node_at;
     t.R = R;
     t.tail_long = tail_long ? 1 : 0;
+    t.tail_lists = tail_lists ? 1 : 0;
 
     // the trie's tables were uploaded group by group while the host wrote them
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
@@ -1116,8 +1123,11 @@ tam_status tam_rebuild(tam_handle *h, unsigned phases, void *stream) {
         return run_device_phase(h, 0, static_cast<hipStream_t>(stream));
     }
     if (phases == 0) phases = default_phases(h);
-    if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE)) return fail(TAM_E_INVAL, "unknown phase bits");
+    if (phases & ~unsigned(TAM_PHASE_LISTS | TAM_PHASE_TABLE | TAM_PHASE_COUNT))
+        return fail(TAM_E_INVAL, "unknown phase bits");
     if ((phases & TAM_PHASE_TABLE) && !h->dt.table) return fail(TAM_E_STATE, "handle has no dense table");
+    if ((phases & TAM_PHASE_COUNT) && (!keeps_lists(h) || !h->lists_built))
+        return fail(TAM_E_STATE, "TAM_PHASE_COUNT needs a handle whose lists are built");
     if ((phases & TAM_PHASE_LISTS) && !keeps_lists(h))
         return fail(TAM_E_STATE, "valid lists are kept only with TAM_FLAG_NO_TABLE, or with "
                                  "TAM_FLAG_TAIL_LISTS and tokens longer than 16 bytes");
@@ -1143,7 +1153,7 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
     out->is_final = h->is_final.data();
     out->table = h->dt.table;
     const bool tails = !h->tail_span.empty();
-    out->dense_rows = tails ? h->dense_rows : (h->flags & TAM_FLAG_NO_TABLE) ? 0 : h->N;
+    out->dense_rows = (h->flags & TAM_FLAG_NO_TABLE) ? 0 : tails ? h->dense_rows : h->N;
     out->dense_row = tails ? h->row_of.data() : nullptr;
     out->cache_rows = is_lazy(h) ? h->cache_rows : 0;
     out->subtree_end = h->sub_end.empty() ? nullptr : h->sub_end.data();
@@ -1211,10 +1221,12 @@ tam_status tam_export_rows(const tam_handle *h, const int32_t *node_ids, int64_t
                                             out + r0 * h->W, s));
         return TAM_OK;
     }
-    if (h->dt.table)
+    if (h->dt.table) {
         TAM_HIP(tam::launch_export_dense(h->dt, node_ids, n, out, s));
-    else
+    } else {
         TAM_HIP(tam::launch_rows(h->dt, node_ids, n, out, h->W, h->W, s));
+        if (h->dt.tail_lists) TAM_HIP(tam::launch_export_tail(h->dt, node_ids, n, out, s));
+    }
     return TAM_OK;
 }
 
@@ -1241,10 +1253,12 @@ tam_status tam_valid_pairs(const tam_handle *h, void *stream, int64_t *out) {
     if (!out) return fail(TAM_E_INVAL, "out is null");
     if (is_lazy(h)) return fail(TAM_E_STATE, "rows built on demand: no pass counts the valid pairs");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // a table's marks count every pair (tails' too); without one the lists do
-    std::vector<int32_t> part(h->dt.table ? (size_t)h->npairs : 0);
+    // a table's marks (or, tail compression with lists, the probe pass) count
+    // every pair, tails' too; plain lists count theirs
+    const bool counted = h->dt.table || h->dt.tail_lists;
+    std::vector<int32_t> part(counted ? (size_t)h->npairs : 0);
     int32_t listed = 0, errors = 0;
-    if (h->dt.table)
+    if (counted)
         TAM_HIP(hipMemcpyAsync(part.data(), h->pairs, part.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     else
         TAM_HIP(hipMemcpyAsync(&listed, h->dt.row_ptr + h->N, sizeof(listed), hipMemcpyDeviceToHost, s));

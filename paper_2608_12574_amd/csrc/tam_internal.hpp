@@ -111,6 +111,8 @@ hipError_t launch_format_noalloc(const DevTables &t, const uint8_t *classes_host
                                  int64_t *pairs_out, hipStream_t s);
 hipError_t launch_export_dense(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out,
                                hipStream_t s);
+// OR the tails' tokens (from the probe hits) into exported rows (tail compression)
+hipError_t launch_export_tail(const DevTables &t, const int32_t *node_ids, int64_t n, uint64_t *out, hipStream_t s);
 int64_t scan_tmp_elems(int64_t N);
 // out[r] = |valid[node_ids[r]]| (0 for a dead node); not for rows built on demand
 hipError_t launch_row_counts(const DevTables &t, const int32_t *node_ids, int64_t n, int32_t *out, hipStream_t s);

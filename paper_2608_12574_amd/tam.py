@@ -23,7 +23,7 @@ TAM_OK = 0
 TAM_DEAD = -1
 DTYPE_FP32, DTYPE_BF16 = 0, 1
 FLAG_HOST_ONLY, FLAG_NO_TABLE, FLAG_TIMING, FLAG_TAIL_LISTS, FLAG_LAZY_ROWS = 1, 2, 4, 8, 16
-PHASE_LISTS, PHASE_ZERO, PHASE_MARK = 1, 2, 4
+PHASE_LISTS, PHASE_ZERO, PHASE_MARK, PHASE_COUNT = 1, 2, 4, 8
 PHASE_TABLE = PHASE_ZERO | PHASE_MARK
 
 STATUS = {0: "TAM_OK", -1: "TAM_E_INVAL", -2: "TAM_E_TERMINATOR", -3: "TAM_E_NOMEM",

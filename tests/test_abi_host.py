@@ -210,8 +210,10 @@ def test_tail_split_host_only(P, oracle_mod, cid):
     assert np.array_equal(-1 - h.dense_row[~branch], size[~branch] - 1)
     full = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY)
     assert full.dense_row is None and full.dense_rows == o.N
+    # without a table the split is the same, the branching nodes keeping lists
     lists = P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY | P.FLAG_NO_TABLE | P.FLAG_TAIL_LISTS)
-    assert lists.dense_row is None and lists.dense_rows == 0
+    assert lists.dense_rows == 0 and np.array_equal(lists.dense_row, h.dense_row)
+    assert P.compile(w.strings, w.vocab, flags=P.FLAG_HOST_ONLY | P.FLAG_NO_TABLE).dense_row is None
 
 
 def test_tail_split_forest_host_only(P, oracle_mod):

@@ -97,11 +97,13 @@ def full_check(P, strings, vocab, sets=None, flags=0, terminator=0x22):
     return h, o
 
 
-# the representations: full dense table, lists only, tail compression, rows
-# built on demand into a row cache
+# the representations: full dense table, lists only, tail compression (dense
+# rows for the branching nodes), tail compression without a table (lists for
+# the branching nodes), rows built on demand into a row cache
 LAZY = 16
-FLAGS = [0, 2, 8, LAZY]
-FLAG_IDS = ["dense", "no_table", "tail", "lazy"]
+TAIL_LISTS = 2 | 8
+FLAGS = [0, 2, 8, TAIL_LISTS, LAZY]
+FLAG_IDS = ["dense", "no_table", "tail", "tail_lists", "lazy"]
 
 
 def branching_nodes(o: Oracle) -> np.ndarray:
@@ -139,7 +141,7 @@ def test_tiny_random_sets(P, flags):
         strings = [bytes(alphabet[rng.integers(0, 2, size=rng.integers(0, 7))]).replace(b'"', b"a")
                    for _ in range(rng.integers(1, 7))]
         h, o = full_check(P, strings, vocab, flags=flags)
-        if flags == 8:
+        if flags & 8:
             assert np.array_equal(h.dense_row >= 0, branching_nodes(o))
         b = Brute(strings, vocab)
         for n in range(o.N):
@@ -235,8 +237,10 @@ _oracles = {}
 
 
 @pytest.fixture(scope="module", params=[(1, 0), (2, 0), (3, 0), (4, 0), (1, 8), (2, 8), (3, 8), (4, 8),
+                                        (2, TAIL_LISTS), (4, TAIL_LISTS),
                                         (1, LAZY), (2, LAZY), (3, LAZY), (4, LAZY)],
                 ids=["c1", "c2", "c3", "c4", "c1-tail", "c2-tail", "c3-tail", "c4-tail",
+                     "c2-tail_lists", "c4-tail_lists",
                      "c1-lazy", "c2-lazy", "c3-lazy", "c4-lazy"])
 def compiled(request, P):
     cid, flags = request.param
@@ -265,8 +269,8 @@ def test_config_table_properties(P, compiled):
     tail compression the table holds exactly the branching nodes (none final),
     and the lists and the table together count the full table's pairs."""
     w, o, h = compiled
-    if h.flags & LAZY:
-        pytest.skip("rows built on demand: no table")
+    if h.flags & (LAZY | 2):
+        pytest.skip("no dense table (rows built on demand, or tail compression with lists)")
     R = h.dense_rows
     table = h._alloc.live[h.table_ptr].view(torch.int64)[: R * h.row_stride_words].view(R, h.row_stride_words)
     nonempty = torch.zeros(R, dtype=torch.bool, device="cuda")
@@ -358,6 +362,19 @@ def test_config_rebuild_identical(P, compiled):
     h.rebuild()
     assert np.array_equal(gpu_rows(h, nodes), before)
     assert h.valid_pairs() == M
+    if h.flags & 2:  # tail compression with lists: the lists are its only phase
+        for bad in (P.PHASE_MARK, P.PHASE_TABLE):
+            with pytest.raises(P.TamError):
+                h.rebuild(phases=bad)
+        h.rebuild(phases=P.PHASE_LISTS)
+        assert np.array_equal(gpu_rows(h, nodes), before)
+        assert h.valid_pairs() == M
+        h.rebuild(phases=P.PHASE_COUNT)  # the probe pass alone leaves the lists as they are
+        assert np.array_equal(gpu_rows(h, nodes), before)
+        assert h.valid_pairs() == M
+        return
+    with pytest.raises(P.TamError):
+        h.rebuild(phases=P.PHASE_COUNT)  # no lists (no token is longer than 16 bytes)
     h.rebuild(phases=P.PHASE_MARK)
     assert np.array_equal(gpu_rows(h, nodes), before)
     assert h.valid_pairs() == M
@@ -469,6 +486,7 @@ def test_config_every_row(P, cid):
     o = Oracle(w.strings, w.vocab)
     hf = P.compile(w.strings, w.vocab)
     ht = P.compile(w.strings, w.vocab, flags=8)
+    hl = P.compile(w.strings, w.vocab, flags=TAIL_LISTS)
     hz = P.compile(w.strings, w.vocab, flags=LAZY)
     assert hf.num_nodes == o.N
     chunk = 1024
@@ -479,13 +497,16 @@ def test_config_every_row(P, cid):
             ids = torch.arange(a, min(o.N, a + chunk), dtype=torch.int32, device="cuda")
             full = hf.export_rows(ids)
             assert torch.equal(ht.export_rows(ids), full), a
+            assert torch.equal(hl.export_rows(ids), full), a
             assert torch.equal(hz.export_rows(ids), full), a
             exp = f.result()
             assert np.array_equal(rows_np(full), exp), a
             cnt = popcounts(exp)
             assert np.array_equal(hf.valid_counts(ids).cpu().numpy(), cnt), a
             assert np.array_equal(ht.valid_counts(ids).cpu().numpy(), cnt), a
-    for h in (hf, ht, hz):
+            assert np.array_equal(hl.valid_counts(ids).cpu().numpy(), cnt), a
+    assert hf.valid_pairs() == ht.valid_pairs() == hl.valid_pairs()
+    for h in (hf, ht, hl, hz):
         h.close()
     torch.cuda.empty_cache()
 
@@ -495,7 +516,7 @@ def popcounts(rows: np.ndarray) -> np.ndarray:
 
 
 @pytest.mark.parametrize("cid", [1, 2])
-@pytest.mark.parametrize("flags", [0, 2, 8], ids=["dense", "no_table", "tail"])
+@pytest.mark.parametrize("flags", [0, 2, 8, TAIL_LISTS], ids=["dense", "no_table", "tail", "tail_lists"])
 def test_valid_counts_every_node(P, cid, flags):
     """|valid[n]| of every node (and of dead ids) counted on the device equals the
     popcount of the oracle's row; rows built on demand keep no counts."""
@@ -530,7 +551,7 @@ def test_no_table_matches_dense_c4(P):
     check_apply(P, h, o, W.uniform_nodes(4, o.N, 16, 1), "fp32", seed=5)
 
 
-@pytest.mark.parametrize("flags", [2, 8, LAZY], ids=["no_table", "tail", "lazy"])
+@pytest.mark.parametrize("flags", [2, 8, TAIL_LISTS, LAZY], ids=["no_table", "tail", "tail_lists", "lazy"])
 def test_forest_c5(P, flags):
     """Config 5: 256 per-query sets of 500 strings as one forest (sparse rows,
     tail compression's dense rows for the branching nodes, or rows built on
