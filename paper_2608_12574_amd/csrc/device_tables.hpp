@@ -13,20 +13,23 @@ namespace tam {
 // Vocabulary hash: keys are the token bytes read last-to-first, so that a
 // suffix of a trie path can be hashed incrementally while walking backwards
 // from the node where it ends.  Host (table build) and device (probe) must
-// agree bit for bit, hence one definition for both.
+// agree bit for bit, hence one definition for both.  The state is 32-bit
+// FNV-1a (one multiply per byte); the key is the 64-bit product of the state
+// with an odd constant, its halves swapped: the low 32 bits (the home bucket)
+// are the product's well-mixed high half, the high 16 bits (the fingerprint)
+// come from its low half, which is a bijection of the state.  Two strings with
+// equal states share bucket and fingerprint; the payload compare tells them
+// apart.
 // ---------------------------------------------------------------------------
-constexpr uint64_t kHashSeed = 0xcbf29ce484222325ull;
+constexpr uint32_t kHashSeed = 0x811c9dc5u;
 
-__host__ __device__ __forceinline__ uint64_t hash_step(uint64_t h, uint32_t byte) {
-    return (h ^ (byte + 1u)) * 0x100000001b3ull;
+__host__ __device__ __forceinline__ uint32_t hash_step(uint32_t h, uint32_t byte) {
+    return (h ^ (byte + 1u)) * 0x01000193u;
 }
 
-__host__ __device__ __forceinline__ uint64_t hash_final(uint64_t h, uint32_t len) {
-    uint64_t z = h + 0x9e3779b97f4a7c15ull * (uint64_t)(len + 1u);
-    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
-    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
-    z ^= z >> 31;
-    return z | 1ull;  // 0 never occurs as a key
+__host__ __device__ __forceinline__ uint64_t hash_final(uint32_t h) {
+    const uint64_t p = (uint64_t)h * 0x9e3779b1ull;
+    return ((p >> 32) | (p << 32)) | 1ull;  // 0 never occurs as a key
 }
 
 // Vocabulary table: open addressing over buckets of kBucket 16-bit

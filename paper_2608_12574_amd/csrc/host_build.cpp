@@ -493,7 +493,8 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
         for (int64_t v = c * chunk; v < std::min(V, (c + 1) * chunk); ++v) {
             const uint32_t off = h->tok_off[(size_t)v];
             const uint32_t len = h->tok_off[(size_t)v + 1] - off;
-            uint64_t hh = kHashSeed, lo = 0, hi = 0;
+            uint32_t hh = kHashSeed;
+            uint64_t lo = 0, hi = 0;
             for (int64_t i = (int64_t)len - 1; i >= 0; --i) hh = hash_step(hh, blob[off + i]);
             for (uint32_t k = 0; k < len && k < 16; ++k) {
                 const uint64_t ch = blob[off + len - 1 - k];
@@ -502,7 +503,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
                 else
                     hi |= ch << (8 * (k - 8));
             }
-            keys[(size_t)v] = len ? hash_final(hh, len) : 0;
+            keys[(size_t)v] = len ? hash_final(hh) : 0;
             heads[(size_t)(2 * v)] = lo;
             heads[(size_t)(2 * v + 1)] = hi;
             home[(size_t)v] = (keys[(size_t)v] & (cap - 1)) / kBucket;

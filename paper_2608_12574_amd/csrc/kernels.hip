@@ -2,10 +2,10 @@
 //
 // Mask compile (Section 4.1, valid[n] for every trie node n):
 //   k_zero   -- zero fill of the dense table (pure streaming stores).
-//   k_probe  -- four lanes per non-root node m, four suffix lengths each: the
-//               last d <= min(depth(m), ℓ) bytes of prefix(m) are hashed (read
-//               backwards from a 16-byte register window) and looked up in the
-//               vocabulary table; a hit of
+//   k_probe  -- two lanes per non-root node m (in different waves), seven
+//               hashed suffix lengths each: the last d <= min(depth(m), ℓ)
+//               bytes of prefix(m) are hashed (read backwards from a 16-byte
+//               register window) and looked up in the vocabulary table; a hit of
 //               token t at d = |t| means t is valid at the ancestor d levels up,
 //               because t's walk from there ends at m.  This is the paper's
 //               crediting of a match to the node |t| bytes back (Section 4.2),
@@ -45,7 +45,6 @@ constexpr int kBlock = 256;
 constexpr int kWave = 64;
 constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
 constexpr int kApplyRows = 2;        // rows per block of k_apply_dense (measured best on rows that change every call)
-constexpr int kProbeLanes = 4;       // lanes per node in k_probe (each takes 16 / 4 suffix lengths)
 // k_apply row sources: the dense table, the valid lists, or per row either
 // (tail compression: dense rows for branching nodes, lists for tails)
 constexpr int kApplyTable = 0, kApplyLists = 1, kApplyTail = 2;
@@ -163,30 +162,52 @@ __device__ __forceinline__ bool slot_equals(const DevTables &t, const SlotPay &m
     return true;
 }
 
-// Slot whose token equals the suffix of length d ending at blob[pos] (key =
-// its hash, (lo, hi) = its reversed window), or -1; its payload goes to *pay.
-// Buckets are scanned from the key's home bucket until one with an empty slot
-// (load <= 1/4 guarantees one exists): a key sits in a later bucket only if
-// every bucket before it was full when it was inserted.  The fingerprints of a
-// bucket are compared into a bit mask first, so a wave reads the payload of its
-// matching lanes in one step instead of one divergent branch per slot.
-__device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d, uint64_t lo, uint64_t hi,
-                                         int64_t pos, SlotPay *pay) {
-    const uint32_t fp = fingerprint(key);
+// The hit of a suffix of d <= kShortLen bytes (last byte b0, the one before it b1).
+__device__ __forceinline__ int32_t short_hit(const DevTables &t, int d, uint32_t b0, uint32_t b1) {
+    return t.short_hits[short_index(d, b0, b1)];
+}
+
+// Slot (0..kBucket-1) of the first fingerprint fp in bucket bk, or -1.  The
+// eight 16-bit fingerprints are compared two per dword: a half of x = w ^ fp:fp
+// is zero exactly where the fingerprint matches, and (x - 0x00010001) & ~x
+// sets bit 15 of a zero half; a borrow out of a zero low half can flag the
+// high half too, but the lowest flagged half is always a true match.  *open:
+// the bucket's last slot is empty, so the bucket was never full and a key
+// whose home it is lies in it (slots fill in order and are never cleared).
+__device__ __forceinline__ int first_match(const Bucket &bk, uint32_t fp, bool *open) {
+    const uint32_t fp2 = fp * 0x00010001u;
+    const uint32_t w[4] = {bk.q[0].x, bk.q[0].y, bk.q[0].z, bk.q[0].w};
+    int s = -1;
+#pragma unroll
+    for (int i = 3; i >= 0; --i) {
+        const uint32_t x = w[i] ^ fp2;
+        const uint32_t z = (x - 0x00010001u) & ~x & 0x80008000u;
+        if (z) s = 2 * i + ((z & 0x8000u) ? 0 : 1);
+    }
+    *open = (w[3] >> 16) == 0u;
+    return s;
+}
+
+// The slot holding the string of d bytes that ends at blob[pos] (reversed
+// window (lo, hi)), with home bucket b and fingerprint fp, or -1; its payload
+// goes to *pay.  Buckets are scanned from b until one with an empty slot (load
+// <= 1/4 guarantees one exists): a key sits in a later bucket only if every
+// bucket before it was full when it was inserted.
+__device__ __forceinline__ int32_t probe_from(const DevTables &t, uint64_t b, uint32_t fp, int d, uint64_t lo,
+                                              uint64_t hi, int64_t pos, SlotPay *pay) {
     const uint64_t bmask = t.slot_mask / kBucket;
-    uint64_t b = home_bucket(t, key);
     for (;;) {
         uint32_t match, empty;
         bucket_masks(load_bucket(t, b), fp, &match, &empty);
         while (match) {
             const int i = __builtin_ctz(match);
             match &= match - 1;
-            const int32_t s = (int32_t)(b * kBucket + (uint64_t)i);
-            const SlotPay m = t.pay[s];
-            const uint64_t mhi = d > 8 ? t.pay_hi[s] : 0ull;
+            const int32_t sl = (int32_t)(b * kBucket + (uint64_t)i);
+            const SlotPay m = t.pay[sl];
+            const uint64_t mhi = d > 8 ? t.pay_hi[sl] : 0ull;
             if (slot_equals(t, m, mhi, d, lo, hi, pos)) {
                 *pay = m;
-                return s;
+                return sl;
             }
         }
         if (empty) return -1;
@@ -194,88 +215,89 @@ __device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d
     }
 }
 
-// The hit of a suffix of d <= kShortLen bytes (last byte b0, the one before it b1).
-__device__ __forceinline__ int32_t short_hit(const DevTables &t, int d, uint32_t b0, uint32_t b1) {
-    return t.short_hits[short_index(d, b0, b1)];
+// The same from the string's key (its hash).
+__device__ __forceinline__ int32_t probe(const DevTables &t, uint64_t key, int d, uint64_t lo, uint64_t hi,
+                                         int64_t pos, SlotPay *pay) {
+    return probe_from(t, home_bucket(t, key), fingerprint(key), d, lo, hi, pos, pay);
 }
 
-// The hits (hit_of_slot, or -1) of the suffixes of length d = d0+1 .. d0+kPer
-// (only d <= Lw <= 16 probed) of a node's path.  Lengths up to kShortLen read
-// short_hits.  The others' bucket loads are issued together, then their
-// payload loads, then (matches longer than 8 bytes) their pay_hi loads, so a
-// lane waits for two or three memory round trips.  A length whose home bucket
-// does not settle it (a full bucket, or a second fingerprint match after a
-// failed first) falls back to the general probe.  The hash of the first d0
-// bytes is recomputed by the lane.
-template <int kPer>
-__device__ __forceinline__ void probe_lengths(const DevTables &t, int64_t pos, int Lw, int d0, uint64_t lo,
-                                              uint64_t hi, int32_t (&hit)[kPer]) {
-    uint64_t h = kHashSeed;
-    for (int d = 1; d <= d0; ++d) h = hash_step(h, window_byte(lo, hi, d - 1));
-    uint64_t key[kPer];
-    bool act[kPer];
+// A node's suffix lengths are split over kProbeLanes lanes: lane g hashes the
+// lengths kShortLen + 1 + g * kLaneLens .. kShortLen + (g + 1) * kLaneLens,
+// lane 0 also reads the short ones.
+constexpr int kProbeLanes = 2;
+constexpr int kLaneLens = (kWin - kShortLen) / kProbeLanes;
+static_assert(kLaneLens * kProbeLanes == kWin - kShortLen, "lengths split evenly over the lanes");
+
+// The hits (hit_of_slot, or -1) of the suffixes of length d = kD0 + 1 ..
+// kD0 + kLaneLens (and, for lane 0, 1 .. kShortLen) of the path ending at
+// blob[pos], window (lo, hi); only d <= Lw <= kWin are probed.  hit[i] is the
+// hit of length kD0 + 1 + i (lane 0: hit[kLaneLens + d - 1] for the short d).
+// The hash state advances one byte per length, and the lengths are unrolled,
+// so every byte extract and mask is a constant.  The home buckets of the
+// lane's lengths are loaded together, then the payload (and for lengths beyond
+// 8 bytes the pay_hi word) of each first fingerprint match, so the lane waits
+// for two memory round trips.  Bit i of the returned mask marks a length its
+// home bucket does not settle (a full bucket, or a failed first match): the
+// caller probes it with the general probe.
+template <int kD0>
+__device__ __forceinline__ uint32_t probe_lengths(const DevTables &t, int Lw, uint64_t lo, uint64_t hi,
+                                                  int32_t (&hit)[kLaneLens + kShortLen]) {
+    if (kD0 == kShortLen) {
+        hit[kLaneLens] = short_hit(t, 1, window_byte(lo, hi, 0), 0u);
+        hit[kLaneLens + 1] = Lw >= 2 ? short_hit(t, 2, window_byte(lo, hi, 0), window_byte(lo, hi, 1)) : -1;
+    } else {
+        hit[kLaneLens] = hit[kLaneLens + 1] = -1;
+    }
+    uint32_t bidx[kLaneLens], fp[kLaneLens];
+    bool act[kLaneLens];
+    uint32_t h = kHashSeed;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        const int d = d0 + j + 1;
-        hit[j] = -1;
-        act[j] = false;
-        key[j] = 0;
-        if (d <= Lw) {
-            h = hash_step(h, window_byte(lo, hi, d - 1));
-            if (d <= kShortLen)
-                hit[j] = short_hit(t, d, window_byte(lo, hi, 0), window_byte(lo, hi, 1));
-            else
-                act[j] = has_len(t, d);
-            key[j] = hash_final(h, (uint32_t)d);
+    for (int k = 0; k < kD0 + kLaneLens; ++k) {
+        h = hash_step(h, window_byte(lo, hi, k));
+        if (k >= kD0) {
+            const int j = k - kD0, d = k + 1;
+            const uint64_t key = hash_final(h);
+            bidx[j] = (uint32_t)home_bucket(t, key);
+            fp[j] = fingerprint(key);
+            act[j] = d <= Lw && has_len(t, d);
         }
     }
-    Bucket bk[kPer];
+    Bucket bk[kLaneLens];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j)
-        if (act[j]) bk[j] = load_bucket(t, home_bucket(t, key[j]));
-    uint32_t match[kPer], empty[kPer];
-    int32_t slot[kPer];
+    for (int j = 0; j < kLaneLens; ++j)
+        if (act[j]) bk[j] = load_bucket(t, bidx[j]);
+    int32_t slot[kLaneLens];
+    uint32_t pending = 0;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        match[j] = empty[j] = 0;
+    for (int j = 0; j < kLaneLens; ++j) {
         slot[j] = -1;
         if (act[j]) {
-            bucket_masks(bk[j], fingerprint(key[j]), &match[j], &empty[j]);
-            if (match[j]) slot[j] = (int32_t)(home_bucket(t, key[j]) * kBucket + (uint64_t)__builtin_ctz(match[j]));
+            bool open;
+            const int sl = first_match(bk[j], fp[j], &open);
+            if (sl >= 0) slot[j] = (int32_t)(bidx[j] * (uint32_t)kBucket + (uint32_t)sl);
+            if (sl >= 0 || !open) pending |= 1u << j;  // cleared below when the match holds
         }
     }
-    // the payload of the first matching slot, and for lengths beyond 8 bytes
-    // its pay_hi word, in the same round trip
-    SlotPay p[kPer];
-    uint64_t phi[kPer];
+    SlotPay p[kLaneLens];
+    uint64_t phi[kLaneLens];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
+    for (int j = 0; j < kLaneLens; ++j) {
         phi[j] = 0;
         if (slot[j] >= 0) {
             p[j] = t.pay[slot[j]];
-            if (d0 + j + 1 > 8) phi[j] = t.pay_hi[slot[j]];
+            if (kD0 + j + 1 > 8) phi[j] = t.pay_hi[slot[j]];
         }
     }
-    bool head[kPer];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        const int d = d0 + j + 1;
-        head[j] = slot[j] >= 0 && (int)p[j].len == d && lo_ok(lo, p[j], d);
-    }
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        const int d = d0 + j + 1;
-        if (!act[j]) continue;
-        if (head[j] && (d <= 8 || hi_ok(hi, phi[j], d))) {
+    for (int j = 0; j < kLaneLens; ++j) {
+        const int d = kD0 + j + 1;
+        hit[j] = -1;
+        if (slot[j] >= 0 && (int)p[j].len == d && lo_ok(lo, p[j], d) && (d <= 8 || hi_ok(hi, phi[j], d))) {
             hit[j] = hit_of_slot(slot[j], p[j].first, p[j].count);
-        } else if (empty[j] != 0 && (match[j] & (match[j] - 1)) == 0) {
-            hit[j] = -1;  // the home bucket settles it: no such token
-        } else {
-            SlotPay mt;
-            const int32_t sl = probe(t, key[j], d, lo, hi, pos, &mt);
-            if (sl >= 0) hit[j] = hit_of_slot(sl, mt.first, mt.count);
+            pending &= ~(1u << j);
         }
     }
+    return pending;
 }
 
 // Writes the token ids of hit x (see hit_of_slot) into the list of node n.
@@ -304,13 +326,13 @@ template <typename F>
 __device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L, F &&f) {
     uint64_t lo, hi;
     load_window(t.blob, pos, lo, hi);
-    uint64_t h = kHashSeed;
+    uint32_t h = kHashSeed;
     for (int d = 1; d <= kWin; ++d) h = hash_step(h, window_byte(lo, hi, d - 1));
     for (int d = kWin + 1; d <= L; ++d) {
         h = hash_step(h, t.blob[pos - d + 1]);
         if (!has_len(t, d)) continue;
         SlotPay mt;
-        const int32_t s = probe(t, hash_final(h, (uint32_t)d), d, lo, hi, pos, &mt);
+        const int32_t s = probe(t, hash_final(h), d, lo, hi, pos, &mt);
         if (s >= 0) f(hit_of_slot(s, mt.first, mt.count), d);
     }
 }
@@ -323,15 +345,16 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
     return t.table ? 0 : INT_MAX;
 }
 
-// Probe pass: kProbeLanes lanes per node m, lane g taking the suffix lengths
-// d = g*kPer+1 .. (g+1)*kPer.  The suffix of length d of prefix(m) equal to
-// token t means t is valid at the ancestor d levels up, node_at[pos - d].  For
-// d <= 16 the hit (hit_of_slot: the token id, or the slot of a string with
-// several ids, or -1) goes to hits[d-1][m]; the tails of tail compression read
-// their tokens back from there.  Longer tokens are probed again where needed
-// (long_hits, by the node's last lane).  All loads of a lane are issued before
-// its first store or atomic (loads, stores and atomics share one vector-memory
-// counter here).
+// Probe pass: kProbeLanes lanes per node m, in different waves (lane g: the
+// suffix lengths of probe_lengths<kShortLen + g * kLaneLens>), all d <= min(depth, ℓ, 16) of
+// prefix(m).  The suffix of length d equal to token t means t is valid at the
+// ancestor d levels up, node_at[pos - d].  The hit (hit_of_slot: the token
+// id, or the slot of a string with several ids, or -1) goes to hits[d-1][m];
+// the tails of tail compression read their tokens back from there.  Longer
+// tokens are probed again where needed (long_hits, by the last lane).  All
+// loads of a lane's main path are issued before its first store or atomic
+// (loads, stores and atomics share one vector-memory counter here); the rare
+// lengths a home bucket does not settle follow, one at a time.
 //   do_mark (a table): every hit whose ancestor has a dense row (row_at of its
 //     blob position; not a tail) is OR-ed into the zeroed table with a 64-bit
 //     atomic, and each block writes the number of valid (node, token) pairs its
@@ -346,10 +369,13 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
 template <bool kCount>
 __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64_t m1, int do_mark,
                                                   int32_t *__restrict__ pairs) {
-    constexpr int kPer = kWin / kProbeLanes;
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    const int64_t m = m0 + i / kProbeLanes;
-    const int d0 = (int)(i % kProbeLanes) * kPer;
+    // lane group g is uniform over a wave (so a wave runs one unrolled path):
+    // wave w of the block takes lengths group w % kProbeLanes of nodes
+    // (w / kProbeLanes) * 64 .. + 63 of the block's kBlock / kProbeLanes
+    const int wv = (int)threadIdx.x / kWave;
+    const int g = wv % kProbeLanes;
+    const int64_t m = m0 + (int64_t)blockIdx.x * (kBlock / kProbeLanes) + (wv / kProbeLanes) * kWave +
+                      (threadIdx.x & (kWave - 1));
     int32_t found = 0;
     const int64_t pos = m < m1 ? t.node_pos[m] : -1;  // a root ends no token
     if (pos >= 0) {
@@ -360,8 +386,8 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
         const int mspan = do_mark ? (t.tail_span ? t.tail_span[m] : 0) : INT_MAX;  // marked beyond
         const int bspan = kCount && t.tail_lists ? t.tail_span[m] : INT_MAX;      // (no table) listed beyond
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
-        // one hit: the pairs it makes (do_mark), marked at table row `row` (>= 0),
-        // counted for list node `ln` (>= 0)
+        // one hit of length d: the pairs it makes, marked at the table row of
+        // its ancestor (>= 0), counted for its list node (>= 0)
         auto take = [&](int32_t hx, int32_t row, int32_t ln) {
             if (hx >= 0) {
                 if (row >= 0) atomicOr(table + (int64_t)row * t.Wp + (hx >> 6), 1ull << (hx & 63));
@@ -379,27 +405,45 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
                 v = t.dup_next[v];
             }
         };
-        if (d0 < Lw) {
-            uint64_t lo, hi;
-            load_window(t.blob, pos, lo, hi);
-            int32_t hit[kPer];
-            probe_lengths<kPer>(t, pos, Lw, d0, lo, hi, hit);
-            int32_t n[kPer], r[kPer];
+        auto list_node = [&](int d) { return kCount && (d <= sspan || d > bspan) ? t.node_at[pos - d] : -1; };
+        auto mark_row = [&](int d) { return d > mspan ? t.row_at[pos - d] : -1; };
+        uint64_t lo, hi;
+        load_window(t.blob, pos, lo, hi);
+        // hit[i]: length d0 + 1 + i; hit[kLaneLens + k]: the short length k + 1 (lane 0)
+        int32_t hit[kLaneLens + kShortLen];
+        const int d0 = g == 0 ? kShortLen : kShortLen + kLaneLens;
+        const uint32_t pending = g == 0 ? probe_lengths<kShortLen>(t, Lw, lo, hi, hit)
+                                        : probe_lengths<kShortLen + kLaneLens>(t, Lw, lo, hi, hit);
+        int32_t n[kLaneLens + kShortLen], r[kLaneLens + kShortLen];
 #pragma unroll
-            for (int j = 0; j < kPer; ++j) {
-                const int d = d0 + j + 1;
-                n[j] = kCount && hit[j] != -1 && (d <= sspan || d > bspan) ? t.node_at[pos - d] : -1;
-                r[j] = hit[j] != -1 && d > mspan ? t.row_at[pos - d] : -1;
-            }
-#pragma unroll
-            for (int j = 0; j < kPer; ++j)
-                if (d0 + j + 1 <= Lw) t.hits[(int64_t)(d0 + j) * t.N + m] = hit[j];
-#pragma unroll
-            for (int j = 0; j < kPer; ++j)
-                if (hit[j] != -1) take(hit[j], r[j], n[j]);
+        for (int k = 0; k < kLaneLens + kShortLen; ++k) {
+            const int d = k < kLaneLens ? d0 + 1 + k : k - kLaneLens + 1;
+            n[k] = hit[k] != -1 ? list_node(d) : -1;
+            r[k] = hit[k] != -1 ? mark_row(d) : -1;
         }
-        // tokens longer than the window (rare), by the node's last lane
-        if (d0 + kPer == kWin && L > kWin && (do_mark || lspan > kWin || (kCount && t.tail_lists)))
+        int32_t *hrow = t.hits + m;
+#pragma unroll
+        for (int k = 0; k < kLaneLens + kShortLen; ++k) {
+            const int d = k < kLaneLens ? d0 + 1 + k : k - kLaneLens + 1;
+            if (d <= Lw && (k < kLaneLens || g == 0)) hrow[(int64_t)(d - 1) * t.N] = hit[k];
+        }
+#pragma unroll
+        for (int k = 0; k < kLaneLens + kShortLen; ++k)
+            if (hit[k] != -1) take(hit[k], r[k], n[k]);
+        // lengths the home bucket did not settle (rare): the general probe
+        for (uint32_t pm = pending; pm; pm &= pm - 1) {
+            const int d = d0 + 1 + __builtin_ctz(pm);
+            uint32_t hh = kHashSeed;
+            for (int k = 0; k < d; ++k) hh = hash_step(hh, window_byte(lo, hi, k));
+            SlotPay mt;
+            const int32_t sl = probe(t, hash_final(hh), d, lo, hi, pos, &mt);
+            if (sl < 0) continue;
+            const int32_t hx = hit_of_slot(sl, mt.first, mt.count);
+            hrow[(int64_t)(d - 1) * t.N] = hx;
+            take(hx, mark_row(d), list_node(d));
+        }
+        // tokens longer than the window (rare), by the last lane
+        if (g == kProbeLanes - 1 && L > kWin && (do_mark || lspan > kWin || (kCount && t.tail_lists)))
             long_hits(t, pos, L, [&](int32_t hx, int d) {
                 take(hx, d > mspan ? t.row_at[pos - d] : -1,
                      d <= lspan || (kCount && t.tail_lists) ? t.node_at[pos - d] : -1);
@@ -1378,10 +1422,10 @@ __device__ __forceinline__ void probe_batch(const DevTables &t, const int64_t (&
         key[k] = 0;
         if (act[k] && d[k] <= kShortLen) hit[k] = short_hit(t, d[k], window_byte(lo[k], hi[k], 0), window_byte(lo[k], hi[k], 1));
         if (hashed[k]) {
-            uint64_t h = kHashSeed;
+            uint32_t h = kHashSeed;
             for (int j = 0; j < d[k]; ++j)
                 h = hash_step(h, j < kWin ? window_byte(lo[k], hi[k], j) : (uint32_t)t.blob[pos[k] - j]);
-            key[k] = hash_final(h, (uint32_t)d[k]);
+            key[k] = hash_final(h);
         }
     }
     Bucket bk[K];
