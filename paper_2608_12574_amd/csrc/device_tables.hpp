@@ -116,6 +116,12 @@ struct DevTables {
     const int32_t *row_of;      // [N] dense row of a node; a tail a: -1 - (nodes below a); null: row = node id
     const int32_t *row_at;      // [blob_bytes] row_of[node_at[p]]; equals node_at without row_of
     const int32_t *sub_end;     // [N] one past the node's subtree (rows built on demand), or null
+    // tail compression without a table: each listed hit's record (node, rank
+    // in the node's list, hit), written by the probe pass into its block's
+    // region and placed by k_fill_records once the lists' offsets are known
+    int32_t *rec;               // [3 * entry_bound] or null
+    const int32_t *rec_off;     // [probe blocks + 1] each probe block's region of rec, in records
+    int32_t *rec_cnt;           // [probe blocks] records each probe block wrote
     int32_t *scan_tmp;          // block sums of the scan
     int32_t *err;               // [1] inconsistent table entries met on the device (0 for the host
                                 // build's tables); copied back and reported by later calls

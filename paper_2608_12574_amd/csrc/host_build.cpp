@@ -638,6 +638,17 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
  * token string of each length d <= min(depth(m), max_len), carrying at most the
  * largest duplicate count among strings of that length.
  */
+// Node m's share of the bound: the ids of the hits at distance d above m that
+// land in lists (see entry_upper_bound).
+static inline int64_t listed_bound(const tam_handle *h, const std::vector<int64_t> &cum, int64_t L, bool split,
+                                   bool branching_listed, int64_t m) {
+    const int64_t all = std::min<int64_t>(h->depth[(size_t)m], L);
+    const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
+    int64_t b = cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
+    if (branching_listed) b += cum[(size_t)all] - cum[(size_t)span];
+    return b;
+}
+
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     const int64_t L = v->max_tok_len;
     const std::vector<int64_t> &cum = v->dup_cum;
@@ -651,17 +662,49 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     std::vector<int64_t> part((size_t)nchunks, 0);
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         int64_t b = 0;
-        for (int64_t m = c * chunk; m < std::min(h->N, (c + 1) * chunk); ++m) {
-            const int64_t all = std::min<int64_t>(h->depth[(size_t)m], L);
-            const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
-            b += cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
-            if (branching_listed) b += cum[(size_t)all] - cum[(size_t)span];
-        }
+        for (int64_t m = c * chunk; m < std::min(h->N, (c + 1) * chunk); ++m)
+            b += listed_bound(h, cum, L, split, branching_listed, m);
         part[(size_t)c] = b;
     });
     int64_t bound = 0;
     for (int64_t b : part) bound += b;
     return bound;
+}
+
+// A listed hit makes one record and at least one listed id, so a block's
+// records are at most the sum of its nodes' bounds, and all regions together
+// take at most entry_upper_bound records.
+void listed_regions(const tam_handle *h, const tam_vocab *v, int64_t per_block, hvec<int32_t> *off) {
+    const int64_t L = v->max_tok_len;
+    const std::vector<int64_t> &cum = v->dup_cum;
+    const bool split = !h->tail_span.empty();
+    const bool branching_listed = split && (h->flags & TAM_FLAG_NO_TABLE);
+    const int64_t blocks = (h->N + per_block - 1) / per_block;
+    off->resize((size_t)blocks + 1);
+    int32_t *o = off->data();
+    const int64_t chunk = 512, nchunks = (blocks + chunk - 1) / chunk;  // blocks per task
+    std::vector<int64_t> part((size_t)nchunks, 0);
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        int64_t run = 0;
+        for (int64_t b = c * chunk; b < std::min(blocks, (c + 1) * chunk); ++b) {
+            int64_t s = 0;
+            for (int64_t m = b * per_block; m < std::min(h->N, (b + 1) * per_block); ++m)
+                s += listed_bound(h, cum, L, split, branching_listed, m);
+            o[b] = (int32_t)run;  // within the task, for now
+            run += s;
+        }
+        part[(size_t)c] = run;
+    });
+    int64_t base = 0;
+    for (int64_t c = 0; c < nchunks; ++c) {
+        const int64_t n = part[(size_t)c];
+        part[(size_t)c] = base;
+        base += n;
+    }
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        for (int64_t b = c * chunk; b < std::min(blocks, (c + 1) * chunk); ++b) o[b] += (int32_t)part[(size_t)c];
+    });
+    o[blocks] = (int32_t)base;
 }
 
 }  // namespace tam

@@ -377,6 +377,11 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
     const int64_t m = m0 + (int64_t)blockIdx.x * (kBlock / kProbeLanes) + (wv / kProbeLanes) * kWave +
                       (threadIdx.x & (kWave - 1));
     int32_t found = 0;
+    __shared__ int32_t s_rec;  // records the block has written (tail_lists)
+    if (kCount && t.tail_lists) {
+        if (threadIdx.x == 0) s_rec = 0;
+        __syncthreads();
+    }
     const int64_t pos = m < m1 ? t.node_pos[m] : -1;  // a root ends no token
     if (pos >= 0) {
         const int L = min(t.depth[m], t.max_len);
@@ -387,8 +392,25 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
         const int bspan = kCount && t.tail_lists ? t.tail_span[m] : INT_MAX;      // (no table) listed beyond
         unsigned long long *table = reinterpret_cast<unsigned long long *>(t.table);
         // one hit of length d: the pairs it makes, marked at the table row of
-        // its ancestor (>= 0), counted for its list node (>= 0)
+        // its ancestor (>= 0), counted for its list node (>= 0); without a
+        // table (tail_lists) a listed hit takes its rank in the node's list and
+        // leaves a record in the block's region
         auto take = [&](int32_t hx, int32_t row, int32_t ln) {
+            if (kCount && t.tail_lists) {
+                const int32_t c = hx >= 0 ? 1 : (int32_t)t.pay[-2 - hx].count;
+                found += c;
+                if (ln < 0) return;
+                const int32_t rank = atomicAdd(&t.count[ln], c);
+                const int32_t at = t.rec_off[blockIdx.x] + atomicAdd(&s_rec, 1);
+                if (at >= t.rec_off[blockIdx.x + 1]) {  // more records than the host's bound
+                    atomicAdd(t.err, 1);
+                    return;
+                }
+                t.rec[3 * (int64_t)at] = ln;
+                t.rec[3 * (int64_t)at + 1] = rank;
+                t.rec[3 * (int64_t)at + 2] = hx;
+                return;
+            }
             if (hx >= 0) {
                 if (row >= 0) atomicOr(table + (int64_t)row * t.Wp + (hx >> 6), 1ull << (hx & 63));
                 if (ln >= 0) atomicAdd(&t.count[ln], 1);
@@ -459,6 +481,30 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
         int32_t total = 0;
         for (int w = 0; w < kBlock / kWave; ++w) total += wsum[w];
         pairs[blockIdx.x] = total;
+        if (kCount && t.tail_lists) t.rec_cnt[blockIdx.x] = s_rec;
+    }
+}
+
+// The records of probe block blockIdx.x (tail compression without a table):
+// each listed hit's ids go to its node's list at row_ptr[node] + rank.
+__global__ void __launch_bounds__(kWave) k_fill_records(DevTables t) {
+    const int64_t b = blockIdx.x;
+    const int64_t r0 = t.rec_off[b];
+    const int32_t n = min(t.rec_cnt[b], t.rec_off[b + 1] - t.rec_off[b]);
+    for (int32_t i = threadIdx.x; i < n; i += kWave) {
+        const int32_t *r = t.rec + 3 * (r0 + i);
+        const int32_t ln = r[0], rank = r[1], hx = r[2];
+        const int64_t at = (int64_t)t.row_ptr[ln] + rank;
+        if (hx >= 0) {
+            t.entries[at] = hx;
+            continue;
+        }
+        const SlotPay pm = t.pay[-2 - hx];  // a string with several token ids
+        int32_t v = pm.first;
+        for (int k = 0; k < (int)pm.count; ++k) {
+            t.entries[at + k] = v;
+            v = t.dup_next[v];
+        }
     }
 }
 
@@ -1653,6 +1699,15 @@ hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *c
     DevTables tf = t;
     tf.child_off = child_off;
     hipLaunchKernelGGL(k_child_fill, dim3(g), dim3(kBlock), 0, s, tf, tmp, child_node, child_byte);
+    return hipGetLastError();
+}
+
+int64_t probe_nodes_per_block() { return kBlock / kProbeLanes; }
+
+hipError_t launch_fill_records(const DevTables &t, hipStream_t s) {
+    const int64_t blocks = (t.N + probe_nodes_per_block() - 1) / probe_nodes_per_block();
+    if (blocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_records, dim3((unsigned)blocks), dim3(kWave), 0, s, t);
     return hipGetLastError();
 }
 

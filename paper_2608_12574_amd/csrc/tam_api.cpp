@@ -415,8 +415,12 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
     }
     if (lists) {
         TAM_HIP(tam::launch_scan(t, s));
-        TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
-        TAM_HIP(tam::launch_fill_lists(t, s));
+        if (t.rec) {  // the probe pass left a record of each listed hit
+            TAM_HIP(tam::launch_fill_records(t, s));
+        } else {
+            TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
+            TAM_HIP(tam::launch_fill_lists(t, s));
+        }
         h->lists_built = true;
     }
     if (timing) {
@@ -463,6 +467,9 @@ void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v,
     t.R = 0;
     t.tail_long = 0;
     t.tail_lists = 0;
+    t.rec = nullptr;
+    t.rec_off = nullptr;
+    t.rec_cnt = nullptr;
     t.N = h->N;
     t.V = v->V;
     t.W = v->W;
@@ -684,7 +691,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         const bool lists = !lazy && ((o.flags & TAM_FLAG_NO_TABLE) ||
                                      ((o.flags & TAM_FLAG_TAIL_LISTS) && vocab->max_tok_len > tam::kWin));
         if (st == TAM_OK && lists) {
-            h->entry_bound = tam::entry_upper_bound(h, vocab);
+            // tail compression without a table: the list bound per probe block
+            // gives each block its region of the listed hits' records
+            const bool records = (o.flags & TAM_FLAG_NO_TABLE) && !h->tail_span.empty() && !host_only;
+            if (records) {
+                tam::listed_regions(h, vocab, tam::probe_nodes_per_block(), &h->rec_off);
+                h->entry_bound = h->rec_off.empty() ? 0 : h->rec_off.back();
+            } else {
+                h->entry_bound = tam::entry_upper_bound(h, vocab);
+            }
             if (h->entry_bound >= INT32_MAX) {
                 st = TAM_E_TOOLARGE;
                 err = "more than 2^31-1 valid (node, token) pairs are possible";
@@ -742,6 +757,10 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const size_t o_cursor = a.take<int32_t>(NP);
     const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(NP));
+    const int64_t rec_blocks = tail_lists ? (int64_t)h->rec_off.size() - 1 : 0;
+    const size_t o_rec = a.take<int32_t>(tail_lists ? 3 * std::max<int64_t>(h->entry_bound, 1) : 0);
+    const size_t o_rec_off = a.take<int32_t>(tail_lists ? rec_blocks + 1 : 0);
+    const size_t o_rec_cnt = a.take<int32_t>(tail_lists ? rec_blocks : 0);
     h->npairs = lazy ? 0 : tam::mark_blocks(h->N);
     const size_t o_pairs = a.take<int32_t>(h->npairs);
     // rows built on demand: subtree extents, the cache's bookkeeping, the
@@ -807,9 +826,21 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.R = R;
     t.tail_long = tail_long ? 1 : 0;
     t.tail_lists = tail_lists ? 1 : 0;
+    t.rec = tail_lists ? reinterpret_cast<int32_t *>(base + o_rec) : nullptr;
+    t.rec_off = tail_lists ? reinterpret_cast<const int32_t *>(base + o_rec_off) : nullptr;
+    t.rec_cnt = tail_lists ? reinterpret_cast<int32_t *>(base + o_rec_cnt) : nullptr;
 
     // the trie's tables were uploaded group by group while the host wrote them
     hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
+    if (e == hipSuccess && tail_lists) {
+        if (rec_blocks != tam::mark_blocks(h->N)) {
+            (void)hipStreamSynchronize(s);
+            destroy_handle(h);
+            return fail(TAM_E_STATE, "listed-hit regions do not match the probe grid");
+        }
+        e = hipMemcpyAsync(base + o_rec_off, h->rec_off.data(), h->rec_off.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s);
+    }
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);

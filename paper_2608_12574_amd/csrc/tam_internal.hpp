@@ -96,6 +96,10 @@ hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 int64_t mark_blocks(int64_t N);
 hipError_t launch_fill_lists(const DevTables &t, hipStream_t s);
+// nodes per block of the probe pass (its block b takes nodes [b * n, (b + 1) * n))
+int64_t probe_nodes_per_block();
+// tail compression without a table: the records of the listed hits into the lists
+hipError_t launch_fill_records(const DevTables &t, hipStream_t s);
 hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
                        int64_t out_stride_words, int64_t out_words, hipStream_t s);
 hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, void *logits,
@@ -189,6 +193,7 @@ struct tam_handle {
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
     tam::hvec<int32_t> tail_span, row_of, row_at;
     int64_t dense_rows = 0;
+    tam::hvec<int32_t> rec_off;  // tail compression without a table: see DevTables::rec_off
     // character-position masks (tam_compile_format): L positions, their classes
     int64_t fmt_L = -1;
     std::vector<uint8_t> classes;
