@@ -142,23 +142,30 @@ struct DevTables {
 };
 
 // Rows built on demand (TAM_FLAG_LAZY_ROWS): the row cache, and the scratch
-// of one group of at most kLazyGroup batch rows.
+// of one group of at most kLazyGroup batch rows.  The cache has C + P rows:
+// C hold nodes' rows (or are empty), P are spares, kept in a ring.  A miss
+// takes the next spare, which is zero, and its CLOCK victim becomes a spare in
+// its place; the build pass of the same group clears the victims' rows while
+// it builds the misses' rows, so no row is cleared and built by one launch.
 constexpr int kLazyGroup = 1024;
 struct LazyDev {
-    uint64_t *cache;       // [C][Wp] cached rows
-    int32_t *slot_of;      // [N] cache slot holding the node's row, or -1
-    int32_t *node_of;      // [C] node whose row a slot holds, or -1
-    uint32_t *stamp;       // [C] number of the group that last used the slot
-    uint32_t *ref;         // [C] CLOCK reference bit
-    uint32_t *state;       // [0] groups assigned so far, [1] CLOCK hand
-    int32_t *rows_src;     // [kLazyGroup] cache slot of each batch row of the group, -1 = dead
+    uint64_t *cache;       // [C + P][Wp] cached rows
+    int32_t *slot_of;      // [N] cache row holding the node's row, or -1
+    int32_t *node_of;      // [C + P] node whose row a cache row holds, -1 empty, -2 spare
+    uint32_t *stamp;       // [C + P] number of the group that last used the row
+    uint32_t *ref;         // [C + P] CLOCK reference bit
+    uint32_t *state;       // [0] groups assigned so far, [1] CLOCK hand, [2] spare ring head
+    int32_t *spare;        // [P] the spare rows, zero once the group that freed them has ended
+    int32_t *rows_src;     // [kLazyGroup] cache row of each batch row of the group, -1 = dead
     int32_t *miss_node;    // [kLazyGroup] nodes whose rows are built, in batch-row order
-    int32_t *miss_row;     // [kLazyGroup] their destination rows (slots, or output rows)
+    int32_t *miss_row;     // [kLazyGroup] their destination rows (cache rows, or output rows)
+    int32_t *miss_free;    // [kLazyGroup] the cache rows their misses freed (cleared by the build)
     int64_t *miss_off;     // [kLazyGroup + 1] prefix sum of their subtree sizes (minus the node)
     int32_t *miss_dep;     // [kLazyGroup] depth of each miss
     int32_t *miss_count;   // [1]
     int32_t *err;          // [1] the handle's device error count (see DevTables)
-    int64_t C;             // cache rows
+    int64_t C;             // cache rows in use (the CLOCK's capacity)
+    int64_t P;             // spare rows: min(C, kLazyGroup), at least the misses of one group
 };
 
 }  // namespace tam

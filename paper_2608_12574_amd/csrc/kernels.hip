@@ -24,9 +24,11 @@
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
 // Rows built on demand (lazy computation with a bounded cache, Appendix):
-//   k_lazy_assign -- cache lookup and CLOCK replacement for a group of rows.
-//   k_lazy_zero, k_lazy_probe -- the missing rows, from the suffix probes of
-//               the node's subtree only; k_apply then reads the cache.
+//   k_lazy_assign -- cache lookup and CLOCK replacement for a group of rows;
+//               each miss takes a zero spare row, its victim becomes a spare.
+//   k_lazy_probe -- the missing rows, from the suffix probes of the node's
+//               subtree only, while the victims' rows are cleared; k_apply
+//               then reads the cache.
 // Fixed-format values (character-position masks):
 //   k_format -- every word of the rows of positions 0..L+1, by wave ballots.
 #include <hip/hip_runtime.h>
@@ -1297,7 +1299,7 @@ __device__ __forceinline__ void store_wg(uint32_t *p, uint32_t v) {
 //      miss); -2 - b names builder b to the other rows of that node.  A group
 //      without a miss ends here, its rows' slots written.
 //   2. Hits stamp their slot with the group's number, so it is not evicted.
-//   3. The misses take slots by CLOCK: sweeps from the hand over windows of up
+//   3. The misses take victims by CLOCK: sweeps from the hand over windows of up
 //      to kLazyGroup slots take those not used by the group and without a
 //      reference bit, in order, and clear the reference bit of the others they
 //      pass; the hand stops after the last slot taken.  With nb <= C at least
@@ -1322,10 +1324,10 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
     const bool live = n >= 0 && (int64_t)n < N;
     const int64_t below = live ? (int64_t)sub_end[n] - n - 1 : 0;
     const int32_t ndep = live ? depth[n] : 0;
-    int32_t slot = -1, lead = -1;
+    int32_t slot = -1, lead = -1, freed = -1;
     bool miss = live;
     uint32_t group = 0;
-    const int64_t C = z.C;
+    const int64_t C = z.C + z.P;  // the CLOCK sweeps every cache row and passes over the spares
     const int win = (int)min<int64_t>(C, kLazyGroup);
     int64_t hand = 0;
     if (kCache) {
@@ -1335,6 +1337,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             if (g == 0u) g = 1u;  // 0 marks a slot never used
             z.state[0] = g;
             s_u[0] = g;
+            s_u[1] = z.state[2];  // the spare ring's head
         }
         if (live) {
             const int32_t v = atomicCAS(&z.slot_of[n], -1, -2 - tid);
@@ -1384,7 +1387,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             const uint32_t st = in ? load_wg(&z.stamp[c]) : group;
             const uint32_t rf = in ? load_wg(&z.ref[c]) : 1u;
             const int32_t old = in ? z.node_of[c] : -1;
-            const bool free_slot = in && st != group;
+            const bool free_slot = in && st != group && old != -2;  // spares are not victims
             const bool take = free_slot && rf == 0u;
             int64_t avail64;
             const int32_t er = (int32_t)group_scan(take ? 1 : 0, &avail64, s_scan);
@@ -1406,22 +1409,34 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
             if (hand >= C) hand -= C;
             __syncthreads();
         }
-        if (tid == 0) z.state[1] = (uint32_t)hand;
+        if (tid == 0) {
+            z.state[1] = (uint32_t)hand;
+            z.state[2] = (uint32_t)(((int64_t)s_u[1] + taken) % z.P);
+        }
         if (miss) {
             const int32_t c = rank < taken ? s_victim[rank] : -1;
             if (c >= 0) {
+                // the miss's row is the next spare (zero); its victim c becomes a
+                // spare in that place, cleared by this group's build pass
+                const int64_t at = ((int64_t)s_u[1] + rank) % z.P;
+                const int32_t r = z.spare[at];
+                z.spare[at] = c;
+                freed = c;
                 const int32_t old = s_vold[rank];
                 if (old >= 0) z.slot_of[old] = -1;
-                z.node_of[c] = n;
-                z.slot_of[n] = c;
-                store_wg(&z.ref[c], 1u);
+                z.node_of[c] = -2;
+                z.node_of[r] = n;
+                z.slot_of[n] = r;
+                store_wg(&z.stamp[r], group);
+                store_wg(&z.ref[r], 1u);
+                s_slot[tid] = r;
             } else {
                 // not reached while nb <= C (two turns of the hand find the
                 // slots); counted as an error, the rows stay fully masked
                 z.slot_of[n] = -1;
                 atomicAdd(z.err, 1);
+                s_slot[tid] = -1;
             }
-            s_slot[tid] = c;
         }
         __syncthreads();
         if (tid < nb) z.rows_src[tid] = lead >= 0 ? s_slot[lead] : s_slot[tid];
@@ -1429,6 +1444,7 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
     if (miss) {
         z.miss_node[rank] = n;
         z.miss_row[rank] = kCache ? s_slot[tid] : tid;
+        z.miss_free[rank] = freed;
         z.miss_off[rank] = off;
         z.miss_dep[rank] = ndep;
     }
@@ -1436,17 +1452,6 @@ __global__ void __launch_bounds__(kLazyGroup) k_lazy_assign(const int32_t *__res
         z.miss_off[M] = total;
         *z.miss_count = M;
     }
-}
-
-// Zero fill of the cache rows the group's misses build: one block per miss
-// (grid = group size, blocks past the misses exit), 16-byte stores.
-__global__ void __launch_bounds__(kBlock) k_lazy_zero(LazyDev z, int64_t Wp) {
-    const int32_t u = (int32_t)blockIdx.x;
-    if (u >= *z.miss_count) return;
-    const int32_t row = z.miss_row[u];
-    if (row < 0) return;
-    u32x4 *p = reinterpret_cast<u32x4 *>(z.cache + (int64_t)row * Wp);
-    for (int64_t c = threadIdx.x; c < Wp / 2; c += kBlock) p[c] = u32x4{0u, 0u, 0u, 0u};
 }
 
 // The hits of K independent suffixes (the one of d[k] bytes ending at blob
@@ -1617,11 +1622,31 @@ __device__ __forceinline__ void lazy_probe_pass(const DevTables &t, const LazyDe
     }
 }
 
-// The rows of the group's misses, in the zeroed cache rows (tam_apply_mask)
-// or straight into the zeroed output rows (tam_export_rows).
-__global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, uint64_t *dest, int64_t stride) {
+// The rows of the group's misses, in their cache rows (spares, zero) for
+// tam_apply_mask, or straight into the zeroed output rows for tam_export_rows.
+// clear (tam_apply_mask): the cache rows the misses freed are zeroed first, so
+// that they are zero when a later group takes them as spares.
+__global__ void __launch_bounds__(kBlock) k_lazy_probe(DevTables t, LazyDev z, uint64_t *dest, int64_t stride,
+                                                       int clear) {
     __shared__ LazyMisses sm;
+    if (clear) {
+        const int32_t M = *z.miss_count;
+        const int32_t per = (int32_t)(t.Wp / 2);  // 16-byte chunks per row
+        const int64_t chunks = (int64_t)M * per;
+        for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < chunks; i += (int64_t)gridDim.x * kBlock) {
+            const int32_t u = (int32_t)(i / per);
+            const int32_t r = z.miss_free[u];
+            if (r >= 0 && (int64_t)r < z.C + z.P)
+                reinterpret_cast<u32x4 *>(z.cache + (int64_t)r * t.Wp)[i - (int64_t)u * per] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
     lazy_probe_pass(t, z, dest, stride, blockIdx.x, gridDim.x, sm);
+}
+
+// p[i] = first + i, i < n.
+__global__ void __launch_bounds__(kBlock) k_iota_i32(int32_t *p, int64_t n, int32_t first) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i < n) p[i] = first + (int32_t)i;
 }
 
 __global__ void __launch_bounds__(kBlock) k_fill_u64(uint64_t *p, int64_t n, uint64_t value) {
@@ -1831,22 +1856,20 @@ hipError_t launch_lazy_apply(const DevTables &t, const LazyDev &z, const int32_t
                              void *logits, int dtype, int64_t row_stride, hipStream_t s) {
     if (nb <= 0) return hipSuccess;
     if (nb > kLazyGroup || nb > z.C || !t.sub_end) return hipErrorInvalidValue;
+    if (nb > z.P) return hipErrorInvalidValue;  // a group's misses take at most P spares
     hipLaunchKernelGGL(k_lazy_assign<true>, dim3(1), dim3(kLazyGroup), 0, s, t.sub_end, t.depth, t.N, z, node_ids,
                        (int32_t)nb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_zero, dim3((unsigned)nb), dim3(kBlock), 0, s, z, t.Wp);
+    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, z.cache, t.Wp, 1);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, z.cache, t.Wp);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // the masking reads the cache as a dense table indexed by slot
+    // the masking reads the cache as a dense table indexed by cache row
     DevTables tc = t;
     tc.table = z.cache;
     tc.row_of = nullptr;
-    tc.N = z.C;
-    tc.R = z.C;
+    tc.N = z.C + z.P;
+    tc.R = z.C + z.P;
     return launch_apply(tc, z.rows_src, nb, logits, dtype, row_stride, s);
 }
 
@@ -1863,16 +1886,22 @@ hipError_t launch_lazy_export(const DevTables &t, const LazyDev &z, const int32_
                        (int32_t)nb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, out, t.W);
+    hipLaunchKernelGGL(k_lazy_probe, dim3(kLazyProbeBlocks), dim3(kBlock), 0, s, t, z, out, t.W, 0);
     return hipGetLastError();
 }
 
 hipError_t launch_lazy_reset(const DevTables &t, const LazyDev &z, hipStream_t s) {
+    // rows 0 .. C-1 empty, C .. C+P-1 the spares (zeroed), in ring order
     hipError_t e = launch_fill_i32(z.slot_of, t.N, -1, s);
     if (e == hipSuccess) e = launch_fill_i32(z.node_of, z.C, -1, s);
-    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.stamp), z.C, 0, s);
-    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.ref), z.C, 0, s);
-    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.state), 2, 0, s);
+    if (e == hipSuccess) e = launch_fill_i32(z.node_of + z.C, z.P, -2, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.stamp), z.C + z.P, 0, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.ref), z.C + z.P, 0, s);
+    if (e == hipSuccess) e = launch_fill_i32(reinterpret_cast<int32_t *>(z.state), 3, 0, s);
+    if (e != hipSuccess || z.P <= 0) return e;
+    hipLaunchKernelGGL(k_iota_i32, dim3(grid_for(z.P, kBlock)), dim3(kBlock), 0, s, z.spare, z.P, (int32_t)z.C);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = launch_zero(z.cache + z.C * t.Wp, z.P * t.Wp, s);
     return e;
 }
 

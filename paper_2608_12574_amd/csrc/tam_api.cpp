@@ -766,11 +766,14 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // rows built on demand: subtree extents, the cache's bookkeeping, the
     // scratch of one group of batch rows
     const int64_t C = lazy ? h->cache_rows : 0, G = lazy ? tam::kLazyGroup : 0;
+    const int64_t P = lazy ? std::min<int64_t>(C, tam::kLazyGroup) : 0;  // spare cache rows
     const size_t o_slot_of = a.take<int32_t>(lazy ? h->N : 0);
-    const size_t o_node_of = a.take<int32_t>(C);
-    const size_t o_stamp = a.take<uint32_t>(C);
-    const size_t o_ref = a.take<uint32_t>(C);
-    const size_t o_state = a.take<uint32_t>(2);
+    const size_t o_node_of = a.take<int32_t>(C + P);
+    const size_t o_stamp = a.take<uint32_t>(C + P);
+    const size_t o_ref = a.take<uint32_t>(C + P);
+    const size_t o_state = a.take<uint32_t>(3);
+    const size_t o_spare = a.take<int32_t>(P);
+    const size_t o_miss_free = a.take<int32_t>(G);
     const size_t o_rows_src = a.take<int32_t>(G);
     const size_t o_miss_node = a.take<int32_t>(G);
     const size_t o_miss_row = a.take<int32_t>(G);
@@ -780,7 +783,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
 
     uint8_t *base = static_cast<uint8_t *>(dev_alloc(h, a.used));
     uint64_t *table = early_table;
-    const size_t table_bytes = (size_t)(lazy ? C : R) * (size_t)h->Wp * sizeof(uint64_t);
+    const size_t table_bytes = (size_t)(lazy ? C + P : R) * (size_t)h->Wp * sizeof(uint64_t);
     if (base && (want_table || lazy) && !table) table = static_cast<uint64_t *>(dev_alloc(h, table_bytes));
     if (!base || ((want_table || lazy) && !table)) {
         (void)hipStreamSynchronize(s);  // copies may still read the host tables
@@ -811,6 +814,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         z.stamp = reinterpret_cast<uint32_t *>(base + o_stamp);
         z.ref = reinterpret_cast<uint32_t *>(base + o_ref);
         z.state = reinterpret_cast<uint32_t *>(base + o_state);
+        z.spare = reinterpret_cast<int32_t *>(base + o_spare);
+        z.miss_free = reinterpret_cast<int32_t *>(base + o_miss_free);
+        z.P = P;
         z.rows_src = reinterpret_cast<int32_t *>(base + o_rows_src);
         z.miss_node = reinterpret_cast<int32_t *>(base + o_miss_node);
         z.miss_row = reinterpret_cast<int32_t *>(base + o_miss_row);
