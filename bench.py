@@ -70,6 +70,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this size (counter calibration)")
+    ap.add_argument("--profile-apply", choices=["roots", "trajectory", "uniform"], default=None,
+                    help="profiling run: compile once, then only mask apply (--apply-warmup + --apply-iters "
+                         "calls) on the workload's root rows, its decode trajectory, or uniform rows, so that "
+                         "every apply dispatch a profiler records is of that kind; prints one JSON line")
     return ap.parse_args()
 
 
@@ -464,6 +468,15 @@ class Bench:
         mixed = float(np.mean([mixed_chunks(x) for x in id_lists]))
         partial = float(np.mean([partial_lines(x) for x in id_lists]))
         required_bytes = apply_bytes + 16 * mixed
+        # the same at the memory's granularity: a 128-byte line of logits that
+        # holds both valid and invalid tokens is read whole
+        required_lines = apply_bytes + 128 * partial
+        root_required = None
+        if root_us is not None:
+            r_lines = apply_bytes + 128 * partial_lines(ids)
+            root_required = {"partial_lines": partial_lines(ids), "mixed_chunks": mixed_chunks(ids),
+                             "required_bytes_lines": int(r_lines),
+                             "frac_of_required_lines": round(r_lines / (root_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
 
         a0, a1 = self.event(), self.event()
         torch.cuda.synchronize()
@@ -503,7 +516,8 @@ class Bench:
         if "lists" in alone and "probe_counts" in alone:
             listed = M if rep == "lists" else None  # plain lists hold every valid pair
             ms = max(alone["lists"] - alone["probe_counts"], 1e-6)
-            kernels["k_scan+k_fill"] = {"kernel": "k_scan_*+k_fill", "avg_launch_ms": round(ms, 4),
+            fill = "k_scan_*+k_fill_records" if rep == "tail_lists" else "k_scan_*+k_fill"
+            kernels[fill] = {"kernel": fill, "avg_launch_ms": round(ms, 4),
                                         "algorithmic_bytes": None if listed is None else int((listed + N + 1) * 4),
                                         "achieved": None if listed is None else
                                         round((listed + N + 1) * 4 / (ms * 1e-3) / 1e9, 1), "unit": "GB/s"}
@@ -544,6 +558,8 @@ class Bench:
                       "partial_lines_per_call": round(partial, 1),
                       "required_bytes": int(required_bytes),
                       "frac_of_required": round(required_bytes / (apply_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                      "required_bytes_lines": int(required_lines),
+                      "frac_of_required_lines": round(required_lines / (apply_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                       "iters": self.args.apply_iters,
                       "rows": (f"{w.decode_steps}-step decode trajectory from the roots" if root_us is not None
                                else "uniform, 64 id lists in turn (new rows every call)" if same_rows
@@ -551,7 +567,8 @@ class Bench:
                       "first_step_at_roots": (
                           {"us": round(root_us, 3),
                            "GBps": round(apply_bytes / (root_us * 1e-6) / 1e9, 1),
-                           "frac_of_hbm_roofline": round(apply_bytes / (root_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)}
+                           "frac_of_hbm_roofline": round(apply_bytes / (root_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                           **root_required}
                           if root_us is not None else None)},
             "advance_us": round(advance_us, 3),
             "advance_us_eager": round(advance_eager_us, 3),
@@ -733,6 +750,48 @@ def cpu_baseline(w, V, seconds, esize):
     return cpu, o, (nodes, rows)
 
 
+def profile_apply(bench, rep, rows):
+    """Mask apply alone on one kind of rows (see --profile-apply)."""
+    torch, P, W, w, dev = bench.torch, bench.P, bench.W, bench.w, bench.dev
+    B, V, args = bench.B, bench.V, bench.args
+    voc = P.Vocab(bench.packed_vocab)
+    h = P.compile(bench.packed, voc, sets=w.set_offsets, flags=FLAGS[rep])
+    N = h.num_nodes
+    if rows == "uniform":
+        lists = [torch.as_tensor(W.uniform_nodes(w.config_id, N, B, seed_extra=k), device=dev) for k in range(64)]
+    else:
+        roots = (h.roots[:B] if w.node_mode == "set_roots" else np.zeros(B)).astype(np.int32)
+        lists = [torch.as_tensor(roots, device=dev)]
+        if rows == "trajectory":
+            fin = torch.as_tensor(h.is_final.astype(np.bool_), device=dev)
+            ids, cur, lists = lists[0], lists[0].clone(), []
+            for s in range(max(1, w.decode_steps)):
+                lists.append(cur.clone())
+                lg = bench.fresh_logits(1 + s)
+                h.apply_mask(cur, lg)
+                nxt = h.advance(cur, lg.float().argmax(dim=1).to(torch.int32))
+                cur = torch.where((nxt < 0) | fin[nxt.clamp(min=0).long()], ids, nxt)
+                del lg
+    torch.cuda.synchronize()
+    n = args.apply_warmup + args.apply_iters
+    for i in range(args.apply_warmup):
+        h.apply_mask(lists[i % len(lists)], bench.bufs[i % bench.nbuf])
+    e0, e1 = bench.event(), bench.event()
+    e0.record()
+    for i in range(args.apply_warmup, n):
+        h.apply_mask(lists[i % len(lists)], bench.bufs[i % bench.nbuf])
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / max(1, args.apply_iters)
+    Wd = (V + 63) // 64
+    apply_bytes = B * (Wd * 8 + V * bench.esize)
+    print(json.dumps({"profile": "apply", "workload": w.name, "repr": rep, "rows": rows,
+                      "dispatch_lists": len(lists), "calls": n, "us": round(us, 3), "bytes": apply_bytes,
+                      "frac_of_hbm_roofline": round(apply_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                      "kernels_sha": kernels_sha()}), flush=True)
+    h.close()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -760,6 +819,9 @@ def main():
     print(f"[bench] workload {w.name}: K={K} V={V} B={B} ({gen_s:.1f}s to generate)", flush=True)
 
     bench = Bench(args, torch, P, W, w, dev)
+    if args.profile_apply:
+        profile_apply(bench, rep, args.profile_apply)
+        return
     cpu = None
     if not args.no_cpu_baseline:
         cpu, bench.oracle, bench.sample = cpu_baseline(w, V, args.cpu_seconds, bench.esize)
