@@ -790,6 +790,11 @@ def profile_apply(bench, rep, rows):
                       "frac_of_hbm_roofline": round(apply_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
                       "kernels_sha": kernels_sha()}), flush=True)
     h.close()
+    if args.calib_copy_mib:  # a copy of known size, for the counters' calibration
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
 
 
 def main():
