@@ -173,6 +173,8 @@ typedef struct {
     int64_t cache_rows;        /* TAM_FLAG_LAZY_ROWS: rows of the row cache (else 0) */
     const int32_t *subtree_end; /* [N] with TAM_FLAG_LAZY_ROWS: one past the last node of the
                                  node's subtree (preorder ids); else NULL */
+    int64_t list_capacity;     /* valid-list entries allocated: a host-computed upper bound on
+                                  the listed (node, token) pairs (0 without lists) */
 } tam_info;
 
 /* Host-side wall times of the last tam_compile, and device times (HIP events,

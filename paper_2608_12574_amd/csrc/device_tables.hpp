@@ -81,6 +81,16 @@ struct StrRec {
     int32_t at, len, lcp, first, psv, root;
 };
 
+// Tail compression: per string, what classifies the nodes it creates (path
+// indices lcp .. len).  Those below index `next` (the next string's common
+// prefix in its part) are branching and take dense rows row, row + 1, ... in
+// order; the others are tails, with len - i nodes below them and
+// tail_span = i - top (top: the path index above the string's highest tail,
+// -1 when the set's root is itself a tail).
+struct TailRec {
+    int32_t row, next, top;
+};
+
 // ---------------------------------------------------------------------------
 // Device-side view of a compiled handle (plain pointers, passed to kernels).
 // ---------------------------------------------------------------------------

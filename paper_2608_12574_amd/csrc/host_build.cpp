@@ -148,6 +148,10 @@ struct PartBase {
 void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPlan &r, PartBase &pb,
                bool subtrees, bool tails, tam_handle *h) {
     const int64_t nstr = (int64_t)r.str.size();
+    // tail_span and row_at are written here only for a host-only handle;
+    // otherwise the device lays them out from the records (row_of, which the
+    // host API reports, is written in both cases)
+    const bool host_tables = tails && !h->tail_span.empty();
     std::vector<int32_t> path;  // global ids of the current string's nodes by depth - 1
     int64_t N = 1, B = 0, prev_len = -1;
     int32_t row = (int32_t)pb.first_row;
@@ -172,7 +176,8 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
         h->strs[(size_t)(pb.str0 + u)] = StrRec{(int32_t)at, (int32_t)len, (int32_t)l, (int32_t)(pb.node + N),
                                                 psv < 0 ? -1 : (int32_t)(pb.str0 + psv), pb.root};
         h->blob[(size_t)at] = 0;
-        if (tails) h->row_at[(size_t)at] = h->row_of[(size_t)pb.root];
+        if (tails) h->tail_rec[(size_t)(pb.str0 + u)] = TailRec{row, (int32_t)next, (int32_t)top};
+        if (host_tables) h->row_at[(size_t)at] = h->row_of[(size_t)pb.root];
         for (int64_t i = 0; i <= len; ++i) {
             const uint8_t c = i < len ? s[i] : term;
             const size_t pos = (size_t)(at + 1 + i);
@@ -186,11 +191,12 @@ void emit_part(const uint8_t *sb, const int64_t *so, uint8_t term, const PartPla
                 path[(size_t)i] = (int32_t)g;
                 if (tails) {
                     const bool branching = i < next;
-                    h->row_of[g] = branching ? row++ : (int32_t)(-1 - (len - i));
-                    h->tail_span[g] = branching ? 0 : (int32_t)(i - top);
+                    h->row_of[g] = branching ? row : (int32_t)(-1 - (len - i));
+                    if (host_tables) h->tail_span[g] = branching ? 0 : (int32_t)(i - top);
+                    if (branching) ++row;
                 }
             }
-            if (tails) h->row_at[pos] = h->row_of[(size_t)path[(size_t)i]];
+            if (host_tables) h->row_at[pos] = h->row_of[(size_t)path[(size_t)i]];
         }
         B += len + 2;
     }
@@ -374,10 +380,14 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
     h->strs.resize((size_t)h->K_unique);
     const bool subtrees = (h->flags & TAM_FLAG_LAZY_ROWS) != 0;
     const bool tails = (h->flags & TAM_FLAG_TAIL_LISTS) && !(h->flags & TAM_FLAG_LAZY_ROWS);
+    const bool host_tables = tails && (h->flags & TAM_FLAG_HOST_ONLY);  // else laid out on the device
+    h->tails = tails;
     h->sub_end.resize(subtrees ? (size_t)N : 0);
     h->row_of.resize(tails ? (size_t)N : 0);
-    h->tail_span.resize(tails ? (size_t)N : 0);
-    h->row_at.resize(tails ? (size_t)BB : 0);
+    h->tail_span.resize(host_tables ? (size_t)N : 0);
+    h->row_at.resize(host_tables ? (size_t)BB : 0);
+    h->tail_rec.resize(tails ? (size_t)h->K_unique : 0);
+    h->root_rows.assign(tails ? (size_t)(2 * S) : 0, 0);
     h->dense_rows = tails ? rows : 0;
     for (int64_t p = 0; p < kBlobPad; ++p) {
         h->blob[(size_t)p] = h->blob[(size_t)(BB - 1 - p)] = 0;
@@ -391,11 +401,13 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
         h->is_final[(size_t)rt] = 0;
         if (subtrees) h->sub_end[(size_t)rt] = (int32_t)(j + 1 < S ? root[(size_t)j + 1] : N);
         if (tails) {
-            h->row_of[(size_t)rt] = root_row[(size_t)j];
-            h->tail_span[(size_t)rt] = 0;
+            h->root_rows[(size_t)(2 * j)] = (int32_t)rt;
+            h->root_rows[(size_t)(2 * j + 1)] = root_row[(size_t)j];
         }
+        if (tails) h->row_of[(size_t)rt] = root_row[(size_t)j];
+        if (host_tables) h->tail_span[(size_t)rt] = 0;
     }
-    if (tails)
+    if (host_tables)
         for (int64_t p = 0; p < kBlobPad; ++p)  // the outer pads stand for the first set's root
             h->row_at[(size_t)p] = h->row_at[(size_t)(BB - 1 - p)] = h->row_of[0];
     // Emission in groups of whole sets (a forest of many sets: four groups, so
@@ -638,32 +650,74 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
  * token string of each length d <= min(depth(m), max_len), carrying at most the
  * largest duplicate count among strings of that length.
  */
-// Node m's share of the bound: the ids of the hits at distance d above m that
-// land in lists (see entry_upper_bound).
-static inline int64_t listed_bound(const tam_handle *h, const std::vector<int64_t> &cum, int64_t L, bool split,
-                                   bool branching_listed, int64_t m) {
-    const int64_t all = std::min<int64_t>(h->depth[(size_t)m], L);
-    const int64_t span = std::min<int64_t>(split ? h->tail_span[(size_t)m] : h->depth[(size_t)m], L);
-    int64_t b = cum[(size_t)span] - (split ? cum[(size_t)std::min<int64_t>(span, kWin)] : 0);
-    if (branching_listed) b += cum[(size_t)all] - cum[(size_t)span];
-    return b;
+// Sums of cum[min(x, cap)] over ranges of x, in constant time: cum is
+// constant from x = cap on.
+struct CumSums {
+    std::vector<int64_t> pre;  // pre[x] = sum of cum[y] for y < x <= cap + 1
+    int64_t cap, last;
+    CumSums(const std::vector<int64_t> &cum, int64_t c) : pre((size_t)c + 2, 0), cap(c), last(cum[(size_t)c]) {
+        for (int64_t y = 0; y <= c; ++y) pre[(size_t)y + 1] = pre[(size_t)y] + cum[(size_t)y];
+    }
+    int64_t below(int64_t n) const {  // sum over x in [0, n)
+        if (n <= 0) return 0;
+        return n <= cap + 1 ? pre[(size_t)n] : pre[(size_t)cap + 1] + (n - cap - 1) * last;
+    }
+    int64_t range(int64_t a, int64_t b) const { return b > a ? below(b) - below(a) : 0; }  // x in [a, b)
+};
+
+// Calls f(g0, g1, b) for consecutive pieces [g0, g1] of the nodes created by
+// the strings [s0, s1) (every node but the roots, whose bound is 0), cut at
+// multiples of `cut` (0: one piece per string), b being the pieces' share of
+// the list bound: the ids of the hits at distance d above each node that land
+// in lists (see entry_upper_bound).  A string creates nodes first, first + 1,
+// ... at path indices lcp .. len; node i has depth i + 1, all = min(i + 1, L)
+// and, with tail compression, tail span 0 (branching, i < next) or i - top.
+// Per node: lists only cum[all]; tail compression with a table (tails'
+// tokens longer than the window) cum[min(span, L)] - cum[min(span, L, kWin)];
+// without a table cum[all] - cum[min(span, L, kWin)].  Each is a range sum.
+template <typename F>
+static void string_bounds(const tam_handle *h, const CumSums &cl, const CumSums &cw, bool split,
+                          bool branching_listed, int64_t s0, int64_t s1, int64_t cut, F &&f) {
+    for (int64_t s = s0; s < s1; ++s) {
+        const StrRec &r = h->strs[(size_t)s];
+        const TailRec t = split ? h->tail_rec[(size_t)s] : TailRec{0, 0, 0};
+        int64_t g0 = r.first;
+        const int64_t gl = (int64_t)r.first + (r.len - r.lcp);
+        while (g0 <= gl) {
+            const int64_t g1 = cut > 0 ? std::min(gl, (g0 / cut + 1) * cut - 1) : gl;
+            const int64_t a = r.lcp + (g0 - r.first), b = r.lcp + (g1 - r.first);  // path indices
+            int64_t sum;
+            if (!split) {
+                sum = cl.range(a + 1, b + 2);
+            } else {
+                const int64_t t0 = std::max<int64_t>(a, t.next);  // first tail of the piece
+                const int64_t tails_w = t0 <= b ? cw.range(t0 - t.top, b - t.top + 1) : 0;
+                if (branching_listed)
+                    sum = cl.range(a + 1, b + 2) - tails_w;
+                else
+                    sum = (t0 <= b ? cl.range(t0 - t.top, b - t.top + 1) : 0) - tails_w;
+            }
+            f(g0, g1, sum);
+            g0 = g1 + 1;
+        }
+    }
 }
 
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     const int64_t L = v->max_tok_len;
-    const std::vector<int64_t> &cum = v->dup_cum;
+    const CumSums cl(v->dup_cum, L), cw(v->dup_cum, std::min<int64_t>(L, kWin));
     // Which hits at distance d above node m land in lists: all of them (lists
     // only); with tail compression and a table, those on the tails above m
     // (d <= tail_span[m]) longer than the probe window; with tail compression
     // and no table, also every hit on a branching ancestor (d > tail_span[m]).
-    const bool split = !h->tail_span.empty();
+    const bool split = h->tails;
     const bool branching_listed = split && (h->flags & TAM_FLAG_NO_TABLE);
-    const int64_t chunk = 1 << 16, nchunks = (h->N + chunk - 1) / chunk;
+    const int64_t K = (int64_t)h->strs.size(), chunk = 1 << 14, nchunks = (K + chunk - 1) / chunk;
     std::vector<int64_t> part((size_t)nchunks, 0);
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         int64_t b = 0;
-        for (int64_t m = c * chunk; m < std::min(h->N, (c + 1) * chunk); ++m)
-            b += listed_bound(h, cum, L, split, branching_listed, m);
+        string_bounds(h, cl, cw, split, branching_listed, c * chunk, std::min(K, (c + 1) * chunk), 0,
+                      [&](int64_t, int64_t, int64_t x) { b += x; });
         part[(size_t)c] = b;
     });
     int64_t bound = 0;
@@ -673,38 +727,29 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
 
 // A listed hit makes one record and at least one listed id, so a block's
 // records are at most the sum of its nodes' bounds, and all regions together
-// take at most entry_upper_bound records.
+// take at most entry_upper_bound records.  A block's nodes may come from the
+// strings of two tasks, whose sums meet in an atomic add.
 void listed_regions(const tam_handle *h, const tam_vocab *v, int64_t per_block, hvec<int32_t> *off) {
     const int64_t L = v->max_tok_len;
-    const std::vector<int64_t> &cum = v->dup_cum;
-    const bool split = !h->tail_span.empty();
+    const CumSums cl(v->dup_cum, L), cw(v->dup_cum, std::min<int64_t>(L, kWin));
+    const bool split = h->tails;
     const bool branching_listed = split && (h->flags & TAM_FLAG_NO_TABLE);
     const int64_t blocks = (h->N + per_block - 1) / per_block;
+    std::vector<int64_t> sums((size_t)blocks, 0);
+    const int64_t K = (int64_t)h->strs.size(), chunk = 1 << 14, nchunks = (K + chunk - 1) / chunk;
+    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
+        string_bounds(h, cl, cw, split, branching_listed, c * chunk, std::min(K, (c + 1) * chunk), per_block,
+                      [&](int64_t g0, int64_t, int64_t x) {
+                          if (x) __atomic_fetch_add(&sums[(size_t)(g0 / per_block)], x, __ATOMIC_RELAXED);
+                      });
+    });
     off->resize((size_t)blocks + 1);
-    int32_t *o = off->data();
-    const int64_t chunk = 512, nchunks = (blocks + chunk - 1) / chunk;  // blocks per task
-    std::vector<int64_t> part((size_t)nchunks, 0);
-    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
-        int64_t run = 0;
-        for (int64_t b = c * chunk; b < std::min(blocks, (c + 1) * chunk); ++b) {
-            int64_t s = 0;
-            for (int64_t m = b * per_block; m < std::min(h->N, (b + 1) * per_block); ++m)
-                s += listed_bound(h, cum, L, split, branching_listed, m);
-            o[b] = (int32_t)run;  // within the task, for now
-            run += s;
-        }
-        part[(size_t)c] = run;
-    });
-    int64_t base = 0;
-    for (int64_t c = 0; c < nchunks; ++c) {
-        const int64_t n = part[(size_t)c];
-        part[(size_t)c] = base;
-        base += n;
+    int64_t run = 0;
+    for (int64_t b = 0; b < blocks; ++b) {
+        (*off)[(size_t)b] = (int32_t)run;
+        run += sums[(size_t)b];
     }
-    parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
-        for (int64_t b = c * chunk; b < std::min(blocks, (c + 1) * chunk); ++b) o[b] += (int32_t)part[(size_t)c];
-    });
-    o[blocks] = (int32_t)base;
+    (*off)[(size_t)blocks] = (int32_t)run;
 }
 
 }  // namespace tam

@@ -982,6 +982,60 @@ __global__ void __launch_bounds__(kBlock) k_node_at(const StrRec *__restrict__ s
 
 // node_pos of the nodes [n0, n1): -1 for a root, else a large value that
 // k_first_pos lowers
+// Tail compression's tables from the string records [s0, s1), one thread per
+// string: row_of and tail_span of the nodes it creates (path indices lcp ..
+// len, ids first ...; see TailRec).  Ids outside [0, N) are counted in *err
+// and skipped.
+__global__ void __launch_bounds__(kBlock) k_tail_nodes(const StrRec *__restrict__ strs,
+                                                       const TailRec *__restrict__ trec, int64_t s0, int64_t s1,
+                                                       int64_t N, int32_t *__restrict__ row_of,
+                                                       int32_t *__restrict__ tail_span, int32_t *err) {
+    const int64_t u = s0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (u >= s1) return;
+    const StrRec r = strs[u];
+    const TailRec tr = trec[u];
+    for (int32_t i = r.lcp; i <= r.len; ++i) {
+        const int64_t g = (int64_t)r.first + (i - r.lcp);
+        if (g < 0 || g >= N) {
+            atomicAdd(err, 1);
+            return;
+        }
+        const bool branching = i < tr.next;
+        row_of[g] = branching ? tr.row + (i - r.lcp) : -1 - (r.len - i);
+        tail_span[g] = branching ? 0 : i - tr.top;
+    }
+}
+
+// The set roots' entries: rr holds (root id, row) pairs.
+__global__ void __launch_bounds__(kBlock) k_root_rows(const int32_t *__restrict__ rr, int64_t S, int64_t N,
+                                                      int32_t *__restrict__ row_of, int32_t *__restrict__ tail_span,
+                                                      int32_t *err) {
+    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (j >= S) return;
+    const int32_t rt = rr[2 * j];
+    if (rt < 0 || (int64_t)rt >= N) {
+        atomicAdd(err, 1);
+        return;
+    }
+    row_of[rt] = rr[2 * j + 1];
+    tail_span[rt] = 0;
+}
+
+// row_at[p] = row_of[node_at[p]] over the blob positions [b0, b1).
+__global__ void __launch_bounds__(kBlock) k_row_at(const int32_t *__restrict__ node_at,
+                                                   const int32_t *__restrict__ row_of, int64_t b0, int64_t b1,
+                                                   int64_t N, int32_t *__restrict__ row_at, int32_t *err) {
+    const int64_t p = b0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (p >= b1) return;
+    const int32_t n = node_at[p];
+    if (n < 0 || (int64_t)n >= N) {
+        atomicAdd(err, 1);
+        row_at[p] = -1;
+        return;
+    }
+    row_at[p] = row_of[n];
+}
+
 __global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__ depth, int64_t n0, int64_t n1,
                                                      int32_t *__restrict__ node_pos) {
     const int64_t g = n0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -1693,6 +1747,22 @@ hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int64_t bl
     if (s1 <= s0) return hipSuccess;
     hipLaunchKernelGGL(k_node_at, dim3(grid_for(s1 - s0, kBlock)), dim3(kBlock), 0, s, strs, s0, s1, blob_bytes, N,
                        node_at, depth, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_tail_tables(const StrRec *strs, const TailRec *trec, int64_t s0, int64_t s1,
+                              const int32_t *root_rows, int64_t S, const int32_t *node_at, int64_t b0, int64_t b1,
+                              int64_t N, int32_t *row_of, int32_t *tail_span, int32_t *row_at, int32_t *err,
+                              hipStream_t s) {
+    if (s1 > s0)
+        hipLaunchKernelGGL(k_tail_nodes, dim3(grid_for(s1 - s0, kBlock)), dim3(kBlock), 0, s, strs, trec, s0, s1, N,
+                           row_of, tail_span, err);
+    if (root_rows && S > 0)
+        hipLaunchKernelGGL(k_root_rows, dim3(grid_for(S, kBlock)), dim3(kBlock), 0, s, root_rows, S, N, row_of,
+                           tail_span, err);
+    if (b1 > b0)
+        hipLaunchKernelGGL(k_row_at, dim3(grid_for(b1 - b0, kBlock)), dim3(kBlock), 0, s, node_at, row_of, b0, b1, N,
+                           row_at, err);
     return hipGetLastError();
 }
 

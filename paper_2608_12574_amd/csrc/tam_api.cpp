@@ -527,7 +527,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // and tail compression's tail_span, row_of, row_at
     uint8_t *trie_base = nullptr;
     size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
-           o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0;
+           o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0, o_tail_rec = 0,
+           o_root_rows = 0;
     // tail compression's split (with a table for the branching nodes, or with
     // sparse lists for them)
     const bool split = (o.flags & TAM_FLAG_TAIL_LISTS) && !(o.flags & TAM_FLAG_LAZY_ROWS);
@@ -565,6 +566,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_tail_span = ta.take<int32_t>(split ? hh->N : 0);
         o_row_of = ta.take<int32_t>(split ? hh->N : 0);
         o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
+        o_tail_rec = ta.take<tam::TailRec>(split ? hh->K_unique : 0);
+        o_root_rows = ta.take<int32_t>(split ? 2 * hh->S : 0);
         o_hits = ta.take<int32_t>(early_count ? tam::kWin * hh->N : 0);
         o_count = ta.take<int32_t>(early_count ? hh->N : 0);
         o_strs = ta.take<tam::StrRec>(hh->K_unique);
@@ -645,10 +648,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         up(o_blob, hh->blob.data(), r.b_lo, r.b_hi, 1);
         up(o_strs, hh->strs.data(), r.s_lo, r.s_hi, sizeof(tam::StrRec));
         if (hh->flags & TAM_FLAG_LAZY_ROWS) up(o_sub_end, hh->sub_end.data(), r.n_lo, r.n_hi, 4);
-        if (split) {
-            up(o_tail_span, hh->tail_span.data(), r.n_lo, r.n_hi, 4);
-            up(o_row_of, hh->row_of.data(), r.n_lo, r.n_hi, 4);
-            up(o_row_at, hh->row_at.data(), r.b_lo, r.b_hi, 4);
+        if (split) {  // the tail tables are laid out on the device from these
+            up(o_tail_rec, hh->tail_rec.data(), r.s_lo, r.s_hi, sizeof(tam::TailRec));
+            if (r.n_lo == 0) up(o_root_rows, hh->root_rows.data(), 0, (int64_t)hh->root_rows.size(), 4);
         }
         // the group's node_at and depth (from its strings), node positions
         // (its nodes lie in its blob range), then (lists) its counts; after the
@@ -658,6 +660,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
             e = tam::launch_node_at(reinterpret_cast<const tam::StrRec *>(trie_base + o_strs), r.s_lo, r.s_hi,
                                     hh->blob_bytes, hh->N, reinterpret_cast<int32_t *>(trie_base + o_node_at),
                                     reinterpret_cast<int32_t *>(trie_base + o_depth), hh->d_err, s);
+        if (e == hipSuccess && split)
+            e = tam::launch_tail_tables(reinterpret_cast<const tam::StrRec *>(trie_base + o_strs),
+                                        reinterpret_cast<const tam::TailRec *>(trie_base + o_tail_rec), r.s_lo,
+                                        r.s_hi, r.n_lo == 0 ? reinterpret_cast<const int32_t *>(trie_base + o_root_rows)
+                                                            : nullptr,
+                                        hh->S, reinterpret_cast<const int32_t *>(trie_base + o_node_at), r.b_lo,
+                                        r.b_hi, hh->N, reinterpret_cast<int32_t *>(trie_base + o_row_of),
+                                        reinterpret_cast<int32_t *>(trie_base + o_tail_span),
+                                        reinterpret_cast<int32_t *>(trie_base + o_row_at), hh->d_err, s);
         if (e == hipSuccess) e = tam::launch_node_pos(te, node_pos, r.n_lo, r.n_hi, r.b_lo, r.b_hi, s);
         if (early_count && e == hipSuccess) {
             const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
@@ -693,7 +704,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         if (st == TAM_OK && lists) {
             // tail compression without a table: the list bound per probe block
             // gives each block its region of the listed hits' records
-            const bool records = (o.flags & TAM_FLAG_NO_TABLE) && !h->tail_span.empty() && !host_only;
+            const bool records = (o.flags & TAM_FLAG_NO_TABLE) && h->tails && !host_only;
             if (records) {
                 tam::listed_regions(h, vocab, tam::probe_nodes_per_block(), &h->rec_off);
                 h->entry_bound = h->rec_off.empty() ? 0 : h->rec_off.back();
@@ -739,7 +750,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     const auto t0 = std::chrono::steady_clock::now();
     const bool lazy = is_lazy(h);
     const bool want_table = !lazy && !(h->flags & TAM_FLAG_NO_TABLE);
-    const bool tails = !lazy && !h->tail_span.empty();
+    const bool tails = !lazy && h->tails;
     const bool tail_long = tails && want_table && vocab->max_tok_len > tam::kWin;
     const bool tail_lists = tails && !want_table;  // branching nodes keep sparse lists
     const bool want_lists = !want_table || tail_long;
@@ -1189,11 +1200,12 @@ tam_status tam_info_get(const tam_handle *h, tam_info *out) {
     out->edge_byte = h->edge.data();
     out->is_final = h->is_final.data();
     out->table = h->dt.table;
-    const bool tails = !h->tail_span.empty();
+    const bool tails = h->tails;
     out->dense_rows = (h->flags & TAM_FLAG_NO_TABLE) ? 0 : tails ? h->dense_rows : h->N;
     out->dense_row = tails ? h->row_of.data() : nullptr;
     out->cache_rows = is_lazy(h) ? h->cache_rows : 0;
     out->subtree_end = h->sub_end.empty() ? nullptr : h->sub_end.data();
+    out->list_capacity = h->entry_bound;
     if (is_lazy(h)) out->dense_rows = 0;
     return TAM_OK;
 }

@@ -96,6 +96,13 @@ hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 int64_t mark_blocks(int64_t N);
 hipError_t launch_fill_lists(const DevTables &t, hipStream_t s);
+// Tail compression's row_of and tail_span of the nodes the strings [s0, s1)
+// create, the roots' entries (root_rows: S (id, row) pairs; null: none) and
+// row_at over the blob positions [b0, b1) (after row_of of every node there).
+hipError_t launch_tail_tables(const StrRec *strs, const TailRec *trec, int64_t s0, int64_t s1,
+                              const int32_t *root_rows, int64_t S, const int32_t *node_at, int64_t b0, int64_t b1,
+                              int64_t N, int32_t *row_of, int32_t *tail_span, int32_t *row_at, int32_t *err,
+                              hipStream_t s);
 // nodes per block of the probe pass (its block b takes nodes [b * n, (b + 1) * n))
 int64_t probe_nodes_per_block();
 // tail compression without a table: the records of the listed hits into the lists
@@ -191,7 +198,13 @@ struct tam_handle {
     tam::hvec<int32_t> sub_end;  // [N] with TAM_FLAG_LAZY_ROWS: one past the node's subtree
     tam::hvec<uint8_t> edge, is_final, blob;
     // tail compression (TAM_FLAG_TAIL_LISTS): see DevTables
+    // row_of is kept on the host for the host API; tail_span and row_at only
+    // for host-only handles.  A device compile lays all three out on the
+    // device from tail_rec and root_rows.
     tam::hvec<int32_t> tail_span, row_of, row_at;
+    bool tails = false;                  // tail compression's split is kept
+    tam::hvec<tam::TailRec> tail_rec;    // [K_unique] one per blob string
+    std::vector<int32_t> root_rows;      // [2 S] each set root's id and row_of
     int64_t dense_rows = 0;
     tam::hvec<int32_t> rec_off;  // tail compression without a table: see DevTables::rec_off
     // character-position masks (tam_compile_format): L positions, their classes

@@ -65,7 +65,8 @@ class Info(ctypes.Structure):
                 ("depth", ctypes.POINTER(ctypes.c_int32)), ("edge_byte", ctypes.POINTER(ctypes.c_uint8)),
                 ("is_final", ctypes.POINTER(ctypes.c_uint8)), ("table", ctypes.c_void_p),
                 ("dense_rows", ctypes.c_int64), ("dense_row", ctypes.POINTER(ctypes.c_int32)),
-                ("cache_rows", ctypes.c_int64), ("subtree_end", ctypes.POINTER(ctypes.c_int32))]
+                ("cache_rows", ctypes.c_int64), ("subtree_end", ctypes.POINTER(ctypes.c_int32)),
+                ("list_capacity", ctypes.c_int64)]
 
 
 class Layout(ctypes.Structure):
@@ -216,6 +217,7 @@ class Handle:
         self.terminator = int(info.terminator)
         self.dense_rows = int(info.dense_rows)
         self.cache_rows = int(info.cache_rows)
+        self.list_capacity = int(info.list_capacity)
         self.roots = np.ctypeslib.as_array(info.roots, shape=(self.num_sets,)).copy()
         self.table_ptr = info.table
         self._info = info  # per-node host arrays are copied on first use

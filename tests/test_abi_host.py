@@ -442,3 +442,62 @@ def test_format_rows_noalloc_argument_errors(P):
     assert call([b'0"'], 1) == -2
     assert call([b"0"] * 1024, 1024) == -6  # valid arguments: a host-only vocabulary has no device tables
     voc.close()
+
+
+def _list_bound(P, h, vocab, flags):
+    """The list capacity by its per-node definition: node m can end at most one
+    distinct token string of each length d <= min(depth(m), max_len), which
+    lands in a list according to the representation (all lengths for plain
+    lists; with tail compression, lengths above the window on tail ancestors
+    (d <= tail_span) and, without a table, every length on branching
+    ancestors (d > tail_span)); each length counts the largest number of ids
+    sharing one string of that length."""
+    L = max(len(t) for t in vocab)
+    dup = np.zeros(L + 1, dtype=np.int64)
+    counts = {}
+    for t in vocab:
+        if t:
+            counts[t] = counts.get(t, 0) + 1
+    for t, c in counts.items():
+        dup[len(t)] = max(dup[len(t)], c)
+    cum = np.cumsum(dup)  # cum[d]: sum over lengths <= d (dup[0] = 0)
+    depth = h.depth.astype(np.int64)
+    all_ = np.minimum(depth, L)
+    if not flags & P.FLAG_TAIL_LISTS:
+        return int(cum[all_].sum())
+    row, parent = h.dense_row, h.parent
+    span = np.zeros(h.num_nodes, dtype=np.int64)  # tail ancestors of each node
+    for m in range(h.num_nodes):  # preorder: a parent precedes its children
+        p = parent[m]
+        if row[m] < 0 and p >= 0 and row[p] < 0:
+            span[m] = span[p] + 1
+    sc = np.minimum(span, L)
+    win = cum[np.minimum(sc, 16)]
+    if flags & P.FLAG_NO_TABLE:
+        return int((cum[all_] - win).sum())
+    return int((cum[sc] - win).sum())
+
+
+@pytest.mark.parametrize("flags", [2, 2 | 8, 8], ids=["lists", "tail_lists", "tail_long"])  # NO_TABLE, TAIL_LISTS
+def test_list_capacity_matches_per_node_bound(P, flags):
+    """The list capacity (computed per string in closed form) equals the
+    per-node bound, on one set, a forest, and a vocabulary with tokens longer
+    than the probe window (so that tail compression with a table keeps lists)."""
+    w1, w5 = W.config(1), W.config(5)
+    rng = np.random.default_rng(5)
+    longs = []
+    for s in w1.strings[:60]:
+        if len(s) >= 18:
+            a = int(rng.integers(0, len(s) - 17))
+            longs.append(s[a:a + int(rng.integers(17, min(len(s) - a, 30) + 1))])
+    vocab = list(w1.vocab[:3000]) + longs + longs[:5]  # duplicates of long strings too
+    assert max(len(t) for t in vocab) > 16
+    offs = [int(x) for x in w5.set_offsets[:7]]
+    cases = [(w1.strings, None), (w5.strings[:offs[-1]], offs)]
+    for strings, sets in cases:
+        h = P.compile(strings, vocab, sets=sets, flags=flags | P.FLAG_HOST_ONLY)
+        assert h.list_capacity == _list_bound(P, h, vocab, flags), (flags, sets is not None)
+        h.close()
+    # no lists without long tokens under tail compression with a table
+    h = P.compile(w1.strings, w1.vocab[:3000], flags=P.FLAG_TAIL_LISTS | P.FLAG_HOST_ONLY)
+    assert h.list_capacity == 0
