@@ -94,6 +94,20 @@ struct TailRec {
 // ---------------------------------------------------------------------------
 // Device-side view of a compiled handle (plain pointers, passed to kernels).
 // ---------------------------------------------------------------------------
+// Tail compression without a table: the probe grid in the groups of whole
+// sets that the compile uploads one after another.  Group k covers the nodes
+// [n_lo[k], n_hi[k]) with the probe blocks [blk0[k], blk0[k + 1]) (block
+// blk0[k] + j holds nodes n_lo[k] + j * nodes-per-block ..), their region
+// offsets at rec_off[off0[k] ..] and their records in rec[k].
+constexpr int kMaxRecGroups = 4;
+struct RecGroups {
+    int64_t n_lo[kMaxRecGroups], n_hi[kMaxRecGroups];
+    int64_t blk0[kMaxRecGroups + 1];
+    int64_t off0[kMaxRecGroups];
+    int32_t *rec[kMaxRecGroups];  // [3 * the group's region total]
+    int32_t n;                    // groups (0: the grid is the plain one)
+};
+
 struct DevTables {
     // trie (a1)
     const uint8_t *blob;        // [pad 32][per string: pad, bytes, T][pad 32]
@@ -128,9 +142,9 @@ struct DevTables {
     const int32_t *sub_end;     // [N] one past the node's subtree (rows built on demand), or null
     // tail compression without a table: each listed hit's record (node, rank
     // in the node's list, hit), written by the probe pass into its block's
-    // region and placed by k_fill_records once the lists' offsets are known
-    int32_t *rec;               // [3 * entry_bound] or null
-    const int32_t *rec_off;     // [probe blocks + 1] each probe block's region of rec, in records
+    // region of its group's records (RecGroups) and placed by k_fill_records
+    // once the lists' offsets are known
+    const int32_t *rec_off;     // per group, its blocks + 1 region offsets, in records
     int32_t *rec_cnt;           // [probe blocks] records each probe block wrote
     int32_t *scan_tmp;          // block sums of the scan
     int32_t *err;               // [1] inconsistent table entries met on the device (0 for the host

@@ -412,7 +412,7 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
             h->row_at[(size_t)p] = h->row_at[(size_t)(BB - 1 - p)] = h->row_of[0];
     // Emission in groups of whole sets (a forest of many sets: four groups, so
     // that a caller can upload a group while the next is written).
-    const int64_t groups = emitted && S >= 8 ? 4 : 1;
+    const int64_t groups = emitted && S >= 8 ? kMaxRecGroups : 1;
     for (int64_t g = 0; g < groups; ++g) {
         const int64_t j0 = S * g / groups, j1 = S * (g + 1) / groups;
         const int64_t p0 = set_first[(size_t)j0], p1 = set_first[(size_t)j1];
@@ -667,7 +667,7 @@ struct CumSums {
 
 // Calls f(g0, g1, b) for consecutive pieces [g0, g1] of the nodes created by
 // the strings [s0, s1) (every node but the roots, whose bound is 0), cut at
-// multiples of `cut` (0: one piece per string), b being the pieces' share of
+// base + multiples of `cut` (0: one piece per string), b being the pieces' share of
 // the list bound: the ids of the hits at distance d above each node that land
 // in lists (see entry_upper_bound).  A string creates nodes first, first + 1,
 // ... at path indices lcp .. len; node i has depth i + 1, all = min(i + 1, L)
@@ -677,14 +677,14 @@ struct CumSums {
 // without a table cum[all] - cum[min(span, L, kWin)].  Each is a range sum.
 template <typename F>
 static void string_bounds(const tam_handle *h, const CumSums &cl, const CumSums &cw, bool split,
-                          bool branching_listed, int64_t s0, int64_t s1, int64_t cut, F &&f) {
+                          bool branching_listed, int64_t s0, int64_t s1, int64_t cut, int64_t base, F &&f) {
     for (int64_t s = s0; s < s1; ++s) {
         const StrRec &r = h->strs[(size_t)s];
         const TailRec t = split ? h->tail_rec[(size_t)s] : TailRec{0, 0, 0};
         int64_t g0 = r.first;
         const int64_t gl = (int64_t)r.first + (r.len - r.lcp);
         while (g0 <= gl) {
-            const int64_t g1 = cut > 0 ? std::min(gl, (g0 / cut + 1) * cut - 1) : gl;
+            const int64_t g1 = cut > 0 ? std::min(gl, base + ((g0 - base) / cut + 1) * cut - 1) : gl;
             const int64_t a = r.lcp + (g0 - r.first), b = r.lcp + (g1 - r.first);  // path indices
             int64_t sum;
             if (!split) {
@@ -716,7 +716,7 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
     std::vector<int64_t> part((size_t)nchunks, 0);
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
         int64_t b = 0;
-        string_bounds(h, cl, cw, split, branching_listed, c * chunk, std::min(K, (c + 1) * chunk), 0,
+        string_bounds(h, cl, cw, split, branching_listed, c * chunk, std::min(K, (c + 1) * chunk), 0, 0,
                       [&](int64_t, int64_t, int64_t x) { b += x; });
         part[(size_t)c] = b;
     });
@@ -727,29 +727,31 @@ int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v) {
 
 // A listed hit makes one record and at least one listed id, so a block's
 // records are at most the sum of its nodes' bounds, and all regions together
-// take at most entry_upper_bound records.  A block's nodes may come from the
+// take at most entry_upper_bound records.  The blocks of a group cover its
+// nodes [n0, n0 + blocks * per_block); a block's nodes may come from the
 // strings of two tasks, whose sums meet in an atomic add.
-void listed_regions(const tam_handle *h, const tam_vocab *v, int64_t per_block, hvec<int32_t> *off) {
+int64_t group_regions(const tam_handle *h, const tam_vocab *v, int64_t s0, int64_t s1, int64_t n0,
+                      int64_t per_block, int64_t blocks, int32_t *off) {
     const int64_t L = v->max_tok_len;
     const CumSums cl(v->dup_cum, L), cw(v->dup_cum, std::min<int64_t>(L, kWin));
     const bool split = h->tails;
     const bool branching_listed = split && (h->flags & TAM_FLAG_NO_TABLE);
-    const int64_t blocks = (h->N + per_block - 1) / per_block;
     std::vector<int64_t> sums((size_t)blocks, 0);
-    const int64_t K = (int64_t)h->strs.size(), chunk = 1 << 14, nchunks = (K + chunk - 1) / chunk;
+    const int64_t K = s1 - s0, chunk = 1 << 12, nchunks = (K + chunk - 1) / chunk;
     parallel_for(nchunks, host_threads(nchunks), [&](int64_t c) {
-        string_bounds(h, cl, cw, split, branching_listed, c * chunk, std::min(K, (c + 1) * chunk), per_block,
-                      [&](int64_t g0, int64_t, int64_t x) {
-                          if (x) __atomic_fetch_add(&sums[(size_t)(g0 / per_block)], x, __ATOMIC_RELAXED);
+        string_bounds(h, cl, cw, split, branching_listed, s0 + c * chunk, s0 + std::min(K, (c + 1) * chunk),
+                      per_block, n0, [&](int64_t g0, int64_t, int64_t x) {
+                          const int64_t b = (g0 - n0) / per_block;
+                          if (x && b >= 0 && b < blocks) __atomic_fetch_add(&sums[(size_t)b], x, __ATOMIC_RELAXED);
                       });
     });
-    off->resize((size_t)blocks + 1);
     int64_t run = 0;
     for (int64_t b = 0; b < blocks; ++b) {
-        (*off)[(size_t)b] = (int32_t)run;
+        off[b] = (int32_t)std::min<int64_t>(run, INT32_MAX);
         run += sums[(size_t)b];
     }
-    (*off)[(size_t)blocks] = (int32_t)run;
+    off[blocks] = (int32_t)std::min<int64_t>(run, INT32_MAX);
+    return run;
 }
 
 }  // namespace tam

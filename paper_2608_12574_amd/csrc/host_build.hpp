@@ -26,10 +26,13 @@ tam_status build_trie(const uint8_t *str_bytes, const int64_t *str_off, int64_t 
 tam_status build_vocab(const uint8_t *tok_bytes, const int64_t *tok_off, int64_t V, tam_vocab *h,
                        std::string *err);
 int64_t entry_upper_bound(const tam_handle *h, const tam_vocab *v);
-// Tail compression without a table: the region of each probe block (nodes
-// [b * per_block, (b + 1) * per_block)) in the records of its listed hits,
-// sized by the same bound: off[b] .. off[b + 1], off[blocks] = the total.
-void listed_regions(const tam_handle *h, const tam_vocab *v, int64_t per_block, hvec<int32_t> *off);
+// Tail compression without a table, one group of nodes [n0, ...) created by
+// the strings [s0, s1): the region of each of its probe blocks (nodes
+// [n0 + b * per_block, n0 + (b + 1) * per_block)) in the group's records of
+// listed hits, sized by the same bound: off[b] .. off[b + 1] for b < blocks,
+// off[blocks] = the group's total, which is returned.
+int64_t group_regions(const tam_handle *h, const tam_vocab *v, int64_t s0, int64_t s1, int64_t n0,
+                      int64_t per_block, int64_t blocks, int32_t *off);
 
 // Runs f(j) for every j in [0, n) on up to `threads` host threads (the caller
 // and workers of a process-wide pool); rethrows the first exception of f.

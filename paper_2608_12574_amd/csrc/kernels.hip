@@ -18,7 +18,7 @@
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
 //   k_apply  -- write-mostly masking of [B, V] logits (lists, tail rows, and
-//               unaligned rows); k_apply_dense for dense-table rows, two
+//               unaligned rows); k_apply_dense for dense-table rows, three
 //               rows per block.
 //   k_advance-- B byte walks over the child tables, one wave per row.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
@@ -46,7 +46,7 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWave = 64;
 constexpr int kApplyUnits = 1;       // 16-byte chunks per thread in k_apply (measured best)
-constexpr int kApplyRows = 2;        // rows per block of k_apply_dense (measured best on rows that change every call)
+constexpr int kApplyRows = 3;        // rows per block of k_apply_dense (measured best on rows that change every call)
 // k_apply row sources: the dense table, the valid lists, or per row either
 // (tail compression: dense rows for branching nodes, lists for tails)
 constexpr int kApplyTable = 0, kApplyLists = 1, kApplyTail = 2;
@@ -339,6 +339,21 @@ __device__ __forceinline__ void long_hits(const DevTables &t, int64_t pos, int L
     }
 }
 
+// The group of probe block b in the groups' grid (0 without groups), and an
+// entry of a group array: block-uniform selects, so that the kernel argument is
+// never indexed dynamically (which would copy it to scratch memory).
+__device__ __forceinline__ int group_of(const RecGroups &rg, int64_t b) {
+    return (rg.n > 1 && b >= rg.blk0[1]) + (rg.n > 2 && b >= rg.blk0[2]) + (rg.n > 3 && b >= rg.blk0[3]);
+}
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxRecGroups], int k) {
+    return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
+}
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxRecGroups + 1], int k) {
+    return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
+}
+
 // Hits at distance d <= list_span(m) above node m belong to the valid lists:
 // all of them with lists only, the tail ancestors of m with tail compression
 // (where the lists hold only tokens longer than the window).
@@ -368,19 +383,36 @@ __device__ __forceinline__ int list_span(const DevTables &t, int64_t m) {
 //     number of valid pairs as do_mark does.
 // The grid covers the nodes [m0, m1): every node of the handle, or (lists of a
 // forest) one group of whole sets, whose nodes' ancestors are in the group too.
+// With tail compression and no table the groups' grid (rg) decides instead:
+// this launch runs its probe blocks blk + blockIdx.x.
 template <bool kCount>
 __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64_t m1, int do_mark,
-                                                  int32_t *__restrict__ pairs) {
+                                                  int32_t *__restrict__ pairs, RecGroups rg, int64_t blk) {
+    constexpr int64_t kPer = kBlock / kProbeLanes;  // nodes per block
+    const int64_t gb = blk + blockIdx.x;            // the block in the grid of pairs (and rec_cnt)
+    const int gk = group_of(rg, gb);
+    if (kCount && t.tail_lists) {
+        m0 = pick(rg.n_lo, gk) + (gb - pick(rg.blk0, gk)) * kPer;
+        m1 = pick(rg.n_hi, gk);
+    } else {
+        m0 += (int64_t)blockIdx.x * kPer;
+    }
     // lane group g is uniform over a wave (so a wave runs one unrolled path):
     // wave w of the block takes lengths group w % kProbeLanes of nodes
-    // (w / kProbeLanes) * 64 .. + 63 of the block's kBlock / kProbeLanes
+    // (w / kProbeLanes) * 64 .. + 63 of the block's kPer
     const int wv = (int)threadIdx.x / kWave;
     const int g = wv % kProbeLanes;
-    const int64_t m = m0 + (int64_t)blockIdx.x * (kBlock / kProbeLanes) + (wv / kProbeLanes) * kWave +
-                      (threadIdx.x & (kWave - 1));
+    const int64_t m = m0 + (wv / kProbeLanes) * kWave + (threadIdx.x & (kWave - 1));
     int32_t found = 0;
-    __shared__ int32_t s_rec;  // records the block has written (tail_lists)
+    // tail_lists: the block's region of its group's records
+    __shared__ int32_t s_rec;  // records the block has written
+    int32_t *rec = nullptr;
+    int32_t reg0 = 0, reg1 = 0;
     if (kCount && t.tail_lists) {
+        const int64_t o = pick(rg.off0, gk) + (gb - pick(rg.blk0, gk));
+        rec = pick(rg.rec, gk);
+        reg0 = t.rec_off[o];
+        reg1 = t.rec_off[o + 1];
         if (threadIdx.x == 0) s_rec = 0;
         __syncthreads();
     }
@@ -403,14 +435,14 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
                 found += c;
                 if (ln < 0) return;
                 const int32_t rank = atomicAdd(&t.count[ln], c);
-                const int32_t at = t.rec_off[blockIdx.x] + atomicAdd(&s_rec, 1);
-                if (at >= t.rec_off[blockIdx.x + 1]) {  // more records than the host's bound
+                const int32_t at = reg0 + atomicAdd(&s_rec, 1);
+                if (at >= reg1) {  // more records than the host's bound
                     atomicAdd(t.err, 1);
                     return;
                 }
-                t.rec[3 * (int64_t)at] = ln;
-                t.rec[3 * (int64_t)at + 1] = rank;
-                t.rec[3 * (int64_t)at + 2] = hx;
+                rec[3 * (int64_t)at] = ln;
+                rec[3 * (int64_t)at + 1] = rank;
+                rec[3 * (int64_t)at + 2] = hx;
                 return;
             }
             if (hx >= 0) {
@@ -482,19 +514,23 @@ __global__ void __launch_bounds__(kBlock) k_probe(DevTables t, int64_t m0, int64
     if (threadIdx.x == 0) {
         int32_t total = 0;
         for (int w = 0; w < kBlock / kWave; ++w) total += wsum[w];
-        pairs[blockIdx.x] = total;
-        if (kCount && t.tail_lists) t.rec_cnt[blockIdx.x] = s_rec;
+        pairs[gb] = total;
+        if (kCount && t.tail_lists) t.rec_cnt[gb] = s_rec;
     }
 }
 
-// The records of probe block blockIdx.x (tail compression without a table):
-// each listed hit's ids go to its node's list at row_ptr[node] + rank.
-__global__ void __launch_bounds__(kWave) k_fill_records(DevTables t) {
+// The records of probe block blockIdx.x of the groups' grid (tail compression
+// without a table): each listed hit's ids go to its node's list at
+// row_ptr[node] + rank.
+__global__ void __launch_bounds__(kWave) k_fill_records(DevTables t, RecGroups rg) {
     const int64_t b = blockIdx.x;
-    const int64_t r0 = t.rec_off[b];
-    const int32_t n = min(t.rec_cnt[b], t.rec_off[b + 1] - t.rec_off[b]);
+    const int gk = group_of(rg, b);
+    const int64_t o = pick(rg.off0, gk) + (b - pick(rg.blk0, gk));
+    const int64_t r0 = t.rec_off[o];
+    const int32_t n = min(t.rec_cnt[b], t.rec_off[o + 1] - t.rec_off[o]);
+    const int32_t *rec = pick(rg.rec, gk);
     for (int32_t i = threadIdx.x; i < n; i += kWave) {
-        const int32_t *r = t.rec + 3 * (r0 + i);
+        const int32_t *r = rec + 3 * (r0 + i);
         const int32_t ln = r[0], rank = r[1], hx = r[2];
         const int64_t at = (int64_t)t.row_ptr[ln] + rank;
         if (hx >= 0) {
@@ -1727,18 +1763,47 @@ hipError_t launch_probe(const DevTables &t, bool count, bool mark, int32_t *pair
     if (t.N <= 0) return hipSuccess;
     const int do_mark = mark && t.table ? 1 : 0;
     const dim3 grid((unsigned)mark_blocks(t.N));
+    if (t.tail_lists) return hipErrorInvalidValue;  // the groups' grid (launch_probe_groups)
+    const RecGroups none{};
     if (count)
-        hipLaunchKernelGGL(k_probe<true>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<true>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs, none,
+                           (int64_t)0);
     else
-        hipLaunchKernelGGL(k_probe<false>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs);
+        hipLaunchKernelGGL(k_probe<false>, grid, dim3(kBlock), 0, s, t, (int64_t)0, t.N, do_mark, pairs, none,
+                           (int64_t)0);
+    return hipGetLastError();
+}
+
+// The host checks the groups' grid: consecutive node ranges within [0, N),
+// each with as many blocks as its nodes need, blocks and offsets increasing.
+static bool groups_ok(const DevTables &t, const RecGroups &rg) {
+    if (rg.n < 1 || rg.n > kMaxRecGroups || rg.blk0[0] != 0) return false;
+    for (int k = 0; k < rg.n; ++k) {
+        const int64_t nodes = rg.n_hi[k] - rg.n_lo[k];
+        if (rg.n_lo[k] < 0 || nodes <= 0 || rg.n_hi[k] > t.N || !rg.rec[k]) return false;
+        if (rg.blk0[k + 1] - rg.blk0[k] != mark_blocks(nodes)) return false;
+        if (k > 0 && (rg.n_lo[k] != rg.n_hi[k - 1] || rg.off0[k] < rg.off0[k - 1] + (rg.blk0[k] - rg.blk0[k - 1]) + 1))
+            return false;
+    }
+    return true;
+}
+
+hipError_t launch_probe_groups(const DevTables &t, const RecGroups &rg, int64_t k0, int64_t k1, int32_t *pairs,
+                               hipStream_t s) {
+    if (!t.tail_lists || t.table || !pairs || !groups_ok(t, rg) || k0 < 0 || k1 > rg.n || k0 >= k1)
+        return hipErrorInvalidValue;
+    const int64_t b0 = rg.blk0[k0], b1 = rg.blk0[k1];
+    hipLaunchKernelGGL(k_probe<true>, dim3((unsigned)(b1 - b0)), dim3(kBlock), 0, s, t, (int64_t)0, t.N, 0, pairs,
+                       rg, b0);
     return hipGetLastError();
 }
 
 hipError_t launch_count_range(const DevTables &t, int64_t m0, int64_t m1, hipStream_t s) {
     if (m1 <= m0) return hipSuccess;
-    if (m0 < 0 || m1 > t.N || t.table) return hipErrorInvalidValue;
+    if (m0 < 0 || m1 > t.N || t.table || t.tail_lists) return hipErrorInvalidValue;
+    const RecGroups none{};
     hipLaunchKernelGGL(k_probe<true>, dim3((unsigned)mark_blocks(m1 - m0)), dim3(kBlock), 0, s, t, m0, m1, 0,
-                       (int32_t *)nullptr);
+                       (int32_t *)nullptr, none, (int64_t)0);
     return hipGetLastError();
 }
 
@@ -1799,10 +1864,9 @@ hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *c
 
 int64_t probe_nodes_per_block() { return kBlock / kProbeLanes; }
 
-hipError_t launch_fill_records(const DevTables &t, hipStream_t s) {
-    const int64_t blocks = (t.N + probe_nodes_per_block() - 1) / probe_nodes_per_block();
-    if (blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_fill_records, dim3((unsigned)blocks), dim3(kWave), 0, s, t);
+hipError_t launch_fill_records(const DevTables &t, const RecGroups &rg, hipStream_t s) {
+    if (!groups_ok(t, rg)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fill_records, dim3((unsigned)rg.blk0[rg.n]), dim3(kWave), 0, s, t, rg);
     return hipGetLastError();
 }
 

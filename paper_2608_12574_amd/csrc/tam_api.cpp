@@ -362,6 +362,8 @@ tam_status device_errors(const tam_handle *h) {
                                   "not valid");
 }
 
+// The device view of one group of the probe pass under tail lists: its record
+// buffer, and its blocks' region offsets and record counts.
 // The device part of compile, on the caller's stream: zero fill of the table,
 // the probe pass (marks into the table, counts for the lists), then the lists'
 // prefix sum and fill.  Phase events are recorded only for the handle's
@@ -406,6 +408,8 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
         if (lists || count_only) TAM_HIP(tam::launch_fill_i32(t.count, t.N, 0, s));
         if (t.fmt_L >= 0) {
             if (mark) TAM_HIP(tam::launch_format(t, h->pairs, s));  // every word of every row
+        } else if (h->rec_groups.n > 0 && (lists || count_only)) {  // tail lists: the compile's groups
+            TAM_HIP(tam::launch_probe_groups(t, h->rec_groups, 0, h->rec_groups.n, h->pairs, s));
         } else if (lists || count_only || mark) {
             TAM_HIP(tam::launch_probe(t, lists || count_only, mark, h->pairs, s));
         }
@@ -415,8 +419,8 @@ tam_status run_device_phase(tam_handle *h, unsigned phases, hipStream_t s, bool 
     }
     if (lists) {
         TAM_HIP(tam::launch_scan(t, s));
-        if (t.rec) {  // the probe pass left a record of each listed hit
-            TAM_HIP(tam::launch_fill_records(t, s));
+        if (h->rec_groups.n > 0) {  // the probe pass left a record of each listed hit
+            TAM_HIP(tam::launch_fill_records(t, h->rec_groups, s));
         } else {
             TAM_HIP(tam::launch_fill_i32(t.cursor, t.N, 0, s));
             TAM_HIP(tam::launch_fill_lists(t, s));
@@ -467,7 +471,6 @@ void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v,
     t.R = 0;
     t.tail_long = 0;
     t.tail_lists = 0;
-    t.rec = nullptr;
     t.rec_off = nullptr;
     t.rec_cnt = nullptr;
     t.N = h->N;
@@ -537,6 +540,13 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // own set), so only the last group's counts follow the host build.
     const bool early_count =
         !host_only && (o.flags & TAM_FLAG_NO_TABLE) && !(o.flags & (TAM_FLAG_LAZY_ROWS | TAM_FLAG_TAIL_LISTS));
+    // Tail compression without a table: the same, each group of sets with its
+    // own records of listed hits (their regions sized on the host from the
+    // group's strings).
+    const bool early_tail = !host_only && (o.flags & TAM_FLAG_NO_TABLE) && (o.flags & TAM_FLAG_TAIL_LISTS) &&
+                            !(o.flags & TAM_FLAG_LAZY_ROWS);
+    size_t o_pairs_t = 0, o_rec_off_t = 0, o_rec_cnt_t = 0;
+    int64_t next_blk = 0, next_off = 0, listed_total = 0;  // early_tail: the groups' blocks, offsets, records
     size_t o_hits = 0, o_count = 0, o_tmp = 0, o_scan_tmp = 0, o_strs = 0, o_err = 0;
     tam::DevTables te{};  // the trie and vocabulary tables the early counts read
     bool enqueued = false;  // device work that reads host tables or writes device memory
@@ -568,8 +578,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_row_at = ta.take<int32_t>(split ? hh->blob_bytes : 0);
         o_tail_rec = ta.take<tam::TailRec>(split ? hh->K_unique : 0);
         o_root_rows = ta.take<int32_t>(split ? 2 * hh->S : 0);
-        o_hits = ta.take<int32_t>(early_count ? tam::kWin * hh->N : 0);
-        o_count = ta.take<int32_t>(early_count ? hh->N : 0);
+        o_hits = ta.take<int32_t>(early_count || early_tail ? tam::kWin * hh->N : 0);
+        o_count = ta.take<int32_t>(early_count || early_tail ? hh->N : 0);
+        // a group's blocks start a new block of nodes: at most one more block
+        // than the whole range per group
+        const int64_t gblocks = tam::mark_blocks(hh->N) + tam::kMaxRecGroups;
+        o_pairs_t = ta.take<int32_t>(early_tail ? gblocks : 0);
+        o_rec_off_t = ta.take<int32_t>(early_tail ? gblocks + tam::kMaxRecGroups : 0);  // blocks + 1 per group
+        o_rec_cnt_t = ta.take<int32_t>(early_tail ? gblocks : 0);
+        if (early_tail) hh->rec_off.resize((size_t)(gblocks + tam::kMaxRecGroups));
         o_strs = ta.take<tam::StrRec>(hh->K_unique);
         o_tmp = ta.take<int32_t>(hh->N);  // scratch of the child lists' build
         o_scan_tmp = ta.take<int32_t>(tam::scan_tmp_elems(hh->N));
@@ -596,7 +613,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
                 return TAM_E_DEVICE;
             }
         }
-        if (early_count) {
+        if (early_tail) {
+            te.tail_lists = 1;
+            te.tail_span = reinterpret_cast<const int32_t *>(trie_base + o_tail_span);
+            te.row_of = reinterpret_cast<const int32_t *>(trie_base + o_row_of);
+            te.row_at = reinterpret_cast<const int32_t *>(trie_base + o_row_at);
+            te.rec_off = reinterpret_cast<const int32_t *>(trie_base + o_rec_off_t);
+            te.rec_cnt = reinterpret_cast<int32_t *>(trie_base + o_rec_cnt_t);
+        }
+        if (early_count || early_tail) {
             te.hits = reinterpret_cast<int32_t *>(trie_base + o_hits);
             te.count = reinterpret_cast<int32_t *>(trie_base + o_count);
             hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
@@ -676,6 +701,47 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
             if (e == hipSuccess) e = tam::launch_count_range(te, r.n_lo, r.n_hi, s);
             if (e == hipSuccess && timing && r.n_hi == hh->N) e = hipEventRecord(hh->ev[2], s);
         }
+        if (early_tail && e == hipSuccess && r.n_hi > r.n_lo) {
+            // the group's record regions (sized on the host from its strings),
+            // their upload, the group's record buffer, then its probe pass
+            const int64_t per = tam::probe_nodes_per_block();
+            const int64_t blocks = (r.n_hi - r.n_lo + per - 1) / per;
+            tam::RecGroups &rg = hh->rec_groups;
+            if (rg.n >= tam::kMaxRecGroups || next_blk + blocks > tam::mark_blocks(hh->N) + tam::kMaxRecGroups ||
+                next_off + blocks + 1 > (int64_t)hh->rec_off.size()) {
+                err = "listed-hit regions exceed the probe grid";
+                return TAM_E_STATE;
+            }
+            const int64_t total = tam::group_regions(hh, vocab, r.s_lo, r.s_hi, r.n_lo, per, blocks,
+                                                     hh->rec_off.data() + next_off);
+            if (listed_total + total >= INT32_MAX) {
+                err = "more than 2^31-1 valid (node, token) pairs are possible";
+                return TAM_E_TOOLARGE;
+            }
+            const size_t rec_bytes = (size_t)(3 * std::max<int64_t>(total, 1)) * sizeof(int32_t);
+            int32_t *rec = static_cast<int32_t *>(dev_alloc(hh, rec_bytes));
+            if (!rec) {
+                err = "device allocation failed (" + std::to_string(rec_bytes) + " bytes requested)";
+                return TAM_E_NOMEM;
+            }
+            hh->device_bytes += (int64_t)rec_bytes;
+            up(o_rec_off_t, hh->rec_off.data(), next_off, next_off + blocks + 1, 4);
+            const int k = rg.n++;
+            rg.n_lo[k] = r.n_lo;
+            rg.n_hi[k] = r.n_hi;
+            rg.blk0[k] = next_blk;
+            rg.blk0[k + 1] = next_blk + blocks;
+            rg.off0[k] = next_off;
+            rg.rec[k] = rec;
+            const bool timing = (hh->flags & TAM_FLAG_TIMING) != 0;
+            if (e == hipSuccess && timing && r.n_lo == 0) e = hipEventRecord(hh->ev[4], s);  // the probe's start
+            if (e == hipSuccess)
+                e = tam::launch_probe_groups(te, rg, k, k + 1, reinterpret_cast<int32_t *>(trie_base + o_pairs_t), s);
+            if (e == hipSuccess && timing && r.n_hi == hh->N) e = hipEventRecord(hh->ev[2], s);
+            next_blk += blocks;
+            next_off += blocks + 1;
+            listed_total += total;
+        }
         if (e == hipSuccess && r.n_hi == hh->N)
             e = tam::launch_child_lists(te, reinterpret_cast<int32_t *>(trie_base + o_child_off),
                                         reinterpret_cast<int32_t *>(trie_base + o_child_node),
@@ -702,15 +768,9 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         const bool lists = !lazy && ((o.flags & TAM_FLAG_NO_TABLE) ||
                                      ((o.flags & TAM_FLAG_TAIL_LISTS) && vocab->max_tok_len > tam::kWin));
         if (st == TAM_OK && lists) {
-            // tail compression without a table: the list bound per probe block
-            // gives each block its region of the listed hits' records
-            const bool records = (o.flags & TAM_FLAG_NO_TABLE) && h->tails && !host_only;
-            if (records) {
-                tam::listed_regions(h, vocab, tam::probe_nodes_per_block(), &h->rec_off);
-                h->entry_bound = h->rec_off.empty() ? 0 : h->rec_off.back();
-            } else {
-                h->entry_bound = tam::entry_upper_bound(h, vocab);
-            }
+            // tail compression without a table: the groups' record regions,
+            // summed as each group was uploaded
+            h->entry_bound = early_tail ? listed_total : tam::entry_upper_bound(h, vocab);
             if (h->entry_bound >= INT32_MAX) {
                 st = TAM_E_TOOLARGE;
                 err = "more than 2^31-1 valid (node, token) pairs are possible";
@@ -762,18 +822,16 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // the probe pass's tables (none when rows are built on demand; the hits and
     // counts of early list counts are in the trie's allocation)
     const int64_t NP = lazy ? 0 : h->N;
-    const size_t o_hits_b = a.take<int32_t>(early_count ? 0 : tam::kWin * NP);
-    const size_t o_count_b = a.take<int32_t>(early_count ? 0 : NP);
+    const bool early = early_count || early_tail;  // hits and counts are in the trie's allocation
+    const size_t o_hits_b = a.take<int32_t>(early ? 0 : tam::kWin * NP);
+    const size_t o_count_b = a.take<int32_t>(early ? 0 : NP);
     const size_t o_row_ptr = a.take<int32_t>(NP + 1);
     const size_t o_cursor = a.take<int32_t>(NP);
     const size_t o_entries = a.take<int32_t>(want_lists ? std::max<int64_t>(h->entry_bound, 1) : 1);
     const size_t o_scan = a.take<int32_t>(tam::scan_tmp_elems(NP));
-    const int64_t rec_blocks = tail_lists ? (int64_t)h->rec_off.size() - 1 : 0;
-    const size_t o_rec = a.take<int32_t>(tail_lists ? 3 * std::max<int64_t>(h->entry_bound, 1) : 0);
-    const size_t o_rec_off = a.take<int32_t>(tail_lists ? rec_blocks + 1 : 0);
-    const size_t o_rec_cnt = a.take<int32_t>(tail_lists ? rec_blocks : 0);
-    h->npairs = lazy ? 0 : tam::mark_blocks(h->N);
-    const size_t o_pairs = a.take<int32_t>(h->npairs);
+    // tail lists: the probe grid's pair slots are the groups' (trie allocation)
+    h->npairs = lazy ? 0 : early_tail ? next_blk : tam::mark_blocks(h->N);
+    const size_t o_pairs = a.take<int32_t>(early_tail ? 0 : h->npairs);
     // rows built on demand: subtree extents, the cache's bookkeeping, the
     // scratch of one group of batch rows
     const int64_t C = lazy ? h->cache_rows : 0, G = lazy ? tam::kLazyGroup : 0;
@@ -803,14 +861,15 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
                                      " bytes requested)");
     }
     h->device_bytes += (int64_t)a.used + (table && !early_table ? (int64_t)table_bytes : 0);
-    h->pairs = reinterpret_cast<int32_t *>(base + o_pairs);
+    h->pairs = early_tail ? reinterpret_cast<int32_t *>(trie_base + o_pairs_t)
+                          : reinterpret_cast<int32_t *>(base + o_pairs);
 
     tam::DevTables &t = h->dt;
     set_trie_tables(t, h, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
                     o_child_node);
     t.err = h->d_err;
-    t.hits = early_count ? te.hits : reinterpret_cast<int32_t *>(base + o_hits_b);
-    t.count = early_count ? te.count : reinterpret_cast<int32_t *>(base + o_count_b);
+    t.hits = early ? te.hits : reinterpret_cast<int32_t *>(base + o_hits_b);
+    t.count = early ? te.count : reinterpret_cast<int32_t *>(base + o_count_b);
     t.row_ptr = reinterpret_cast<int32_t *>(base + o_row_ptr);
     t.cursor = reinterpret_cast<int32_t *>(base + o_cursor);
     t.entries = reinterpret_cast<int32_t *>(base + o_entries);
@@ -843,21 +902,16 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     t.R = R;
     t.tail_long = tail_long ? 1 : 0;
     t.tail_lists = tail_lists ? 1 : 0;
-    t.rec = tail_lists ? reinterpret_cast<int32_t *>(base + o_rec) : nullptr;
-    t.rec_off = tail_lists ? reinterpret_cast<const int32_t *>(base + o_rec_off) : nullptr;
-    t.rec_cnt = tail_lists ? reinterpret_cast<int32_t *>(base + o_rec_cnt) : nullptr;
+    t.rec_off = early_tail ? te.rec_off : nullptr;
+    t.rec_cnt = early_tail ? te.rec_cnt : nullptr;
 
     // the trie's tables were uploaded group by group while the host wrote them
-    hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
-    if (e == hipSuccess && tail_lists) {
-        if (rec_blocks != tam::mark_blocks(h->N)) {
-            (void)hipStreamSynchronize(s);
-            destroy_handle(h);
-            return fail(TAM_E_STATE, "listed-hit regions do not match the probe grid");
-        }
-        e = hipMemcpyAsync(base + o_rec_off, h->rec_off.data(), h->rec_off.size() * sizeof(int32_t),
-                           hipMemcpyHostToDevice, s);
+    if (tail_lists != early_tail) {  // the listed hits' records were planned with the trie
+        (void)hipStreamSynchronize(s);
+        destroy_handle(h);
+        return fail(TAM_E_STATE, "tail lists without their records");
     }
+    hipError_t e = hipStreamWaitEvent(s, vocab->ready, 0);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->work_done, hipEventDisableTiming);
     if (e == hipSuccess) e = hipEventRecord(h->work_done, s);
     if (e == hipSuccess && (h->flags & TAM_FLAG_TIMING)) e = create_events(h);
@@ -870,7 +924,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         return fail(st, msg);
     }
     st = run_device_phase(h, default_phases(h) & ~(early_table ? unsigned(TAM_PHASE_ZERO) : 0u), s,
-                          early_table != nullptr, early_count);
+                          early_table != nullptr, early);
     if (st != TAM_OK) {
         const std::string msg = g_err;
         destroy_handle(h);

@@ -105,8 +105,16 @@ hipError_t launch_tail_tables(const StrRec *strs, const TailRec *trec, int64_t s
                               hipStream_t s);
 // nodes per block of the probe pass (its block b takes nodes [b * n, (b + 1) * n))
 int64_t probe_nodes_per_block();
-// tail compression without a table: the records of the listed hits into the lists
-hipError_t launch_fill_records(const DevTables &t, hipStream_t s);
+// tail compression without a table: the records of the listed hits (of
+// `blocks` probe blocks) into the lists
+hipError_t launch_fill_records(const DevTables &t, const RecGroups &rg, hipStream_t s);
+// the probe pass's counts over nodes [m0, m1) (lists, tail lists with their
+// records), with each block's valid pairs at pairs[blockIdx] (pairs may be null
+// without tail lists)
+// the probe pass (lists counted, records written) over groups [k0, k1) of the
+// groups' grid, into pairs[blocks of those groups]
+hipError_t launch_probe_groups(const DevTables &t, const RecGroups &rg, int64_t k0, int64_t k1, int32_t *pairs,
+                               hipStream_t s);
 hipError_t launch_rows(const DevTables &t, const int32_t *nodes, int64_t nrows, uint64_t *out,
                        int64_t out_stride_words, int64_t out_words, hipStream_t s);
 hipError_t launch_apply(const DevTables &t, const int32_t *node_ids, int64_t B, void *logits,
@@ -206,7 +214,10 @@ struct tam_handle {
     tam::hvec<tam::TailRec> tail_rec;    // [K_unique] one per blob string
     std::vector<int32_t> root_rows;      // [2 S] each set root's id and row_of
     int64_t dense_rows = 0;
-    tam::hvec<int32_t> rec_off;  // tail compression without a table: see DevTables::rec_off
+    // tail compression without a table: the probe grid in the groups of nodes
+    // the compile uploaded, each with its own buffer of records
+    tam::RecGroups rec_groups{};
+    tam::hvec<int32_t> rec_off;  // host copy of the groups' region offsets (see DevTables::rec_off)
     // character-position masks (tam_compile_format): L positions, their classes
     int64_t fmt_L = -1;
     std::vector<uint8_t> classes;

@@ -624,7 +624,16 @@ def test_forest_written_in_groups(P, flags):
     assert h.num_nodes == o.N and np.array_equal(h.roots, o.roots)
     last = np.arange(o.roots[-1], o.N, dtype=np.int32)
     nodes = np.unique(np.concatenate([sample_nodes(o, 2000, 91), o.roots, last])).astype(np.int32)
-    assert np.array_equal(gpu_rows(h, nodes), o.mask_rows(nodes))
+    exp_rows = o.mask_rows(nodes)
+    assert np.array_equal(gpu_rows(h, nodes), exp_rows)
+    if not flags & LAZY:  # counts, and the device phases run again over the groups' grid
+        cnt = popcounts(exp_rows)
+        assert np.array_equal(h.valid_counts(torch.as_tensor(nodes, device="cuda")).cpu().numpy(), cnt)
+        M = h.valid_pairs()
+        h.rebuild()
+        assert np.array_equal(gpu_rows(h, nodes), exp_rows)
+        assert np.array_equal(h.valid_counts(torch.as_tensor(nodes, device="cuda")).cpu().numpy(), cnt)
+        assert h.valid_pairs() == M
     rng = np.random.default_rng(92)
     start = np.repeat(o.roots, 8).astype(np.int32)
     cur = start.copy()
