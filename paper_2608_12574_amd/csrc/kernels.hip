@@ -71,9 +71,19 @@ DevProps props_for_current_device() {
     return cache[dev];
 }
 
+// p[i] = value, i < n: 16-byte stores where p is 16-byte aligned.
 __global__ void __launch_bounds__(kBlock) k_fill_i32(int32_t *p, int64_t n, int32_t value) {
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlock)
-        p[i] = value;
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t i0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    int64_t done = 0;
+    if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+        const uint32_t u = (uint32_t)value;
+        const u32x4 v4{u, u, u, u};
+        done = n / 4;
+        for (int64_t i = i0; i < done; i += stride) reinterpret_cast<u32x4 *>(p)[i] = v4;
+        done *= 4;
+    }
+    for (int64_t i = done + i0; i < n; i += stride) p[i] = value;
 }
 
 // ---------------------------------------------------------------- probes ---
@@ -584,7 +594,7 @@ __global__ void __launch_bounds__(kBlock) k_zero(u32x4 *__restrict__ p, int64_t 
 
 // ------------------------------------------------------------------ scan ---
 
-constexpr int kScanItems = 8;
+constexpr int kScanItems = 16;
 constexpr int kScanTile = kBlock * kScanItems;  // elements per block
 
 // Exclusive scan of one value per thread over the 256-thread block.
@@ -608,17 +618,38 @@ __device__ __forceinline__ int32_t block_exclusive_scan(int32_t x, int32_t *tota
     return before + inc - x;
 }
 
+// A thread's kScanItems consecutive values from base (0 past n): four 16-byte
+// loads where the whole run is in range and aligned.
+__device__ __forceinline__ void scan_load(const int32_t *in, int64_t base, int64_t n, int32_t (&v)[kScanItems]) {
+    if (base + kScanItems <= n && (reinterpret_cast<uintptr_t>(in + base) & 15) == 0) {
+#pragma unroll
+        for (int q = 0; q < kScanItems / 4; ++q) {
+            const u32x4 x = reinterpret_cast<const u32x4 *>(in + base)[q];
+            v[4 * q] = (int32_t)x.x;
+            v[4 * q + 1] = (int32_t)x.y;
+            v[4 * q + 2] = (int32_t)x.z;
+            v[4 * q + 3] = (int32_t)x.w;
+        }
+        return;
+    }
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) v[k] = base + k < n ? in[base + k] : 0;
+}
+
 __global__ void __launch_bounds__(kBlock) k_scan_blocks(const int32_t *in, int64_t n, int32_t *sums) {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int32_t v[kScanItems];
+    scan_load(in, base, n, v);
     int32_t s = 0;
-    for (int k = 0; k < kScanItems; ++k)
-        if (base + k < n) s += in[base + k];
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) s += v[k];
     int32_t total;
     block_exclusive_scan(s, &total);
     if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
 // One block: exclusive scan of the nb block sums in place; grand total -> *total_out.
+// (Used when the block sums are more than one block of the apply pass adds up.)
 __global__ void __launch_bounds__(kBlock) k_scan_top(int32_t *sums, int64_t nb, int32_t *total_out) {
     int32_t carry = 0;
     for (int64_t base = 0; base < nb; base += kScanTile) {
@@ -641,20 +672,42 @@ __global__ void __launch_bounds__(kBlock) k_scan_top(int32_t *sums, int64_t nb, 
     if (threadIdx.x == 0) *total_out = carry;
 }
 
+// The scan's second pass.  own_prefix (nb <= kScanTile): each block adds up the
+// block sums before its own (at most kScanTile of them, from L2) and the last
+// block writes the grand total; otherwise sums holds k_scan_top's prefixes.
 __global__ void __launch_bounds__(kBlock) k_scan_apply(const int32_t *in, int64_t n, const int32_t *sums,
-                                                       int32_t *out) {
+                                                       int own_prefix, int32_t *out, int32_t *total_out) {
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
     int32_t v[kScanItems];
+    scan_load(in, base, n, v);
     int32_t s = 0;
-    for (int k = 0; k < kScanItems; ++k) {
-        v[k] = base + k < n ? in[base + k] : 0;
-        s += v[k];
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) s += v[k];
+    int32_t prefix, total;
+    if (own_prefix) {
+        int32_t p = 0;
+        for (int64_t j = threadIdx.x; j < (int64_t)blockIdx.x; j += kBlock) p += sums[j];
+        block_exclusive_scan(p, &prefix);
+    } else {
+        prefix = sums[blockIdx.x];
     }
-    int32_t total;
-    int32_t run = sums[blockIdx.x] + block_exclusive_scan(s, &total);
+    int32_t run = prefix + block_exclusive_scan(s, &total);
+    if (own_prefix && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *total_out = prefix + total;
+    int32_t o[kScanItems];
+#pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
-        if (base + k < n) out[base + k] = run;
+        o[k] = run;
         run += v[k];
+    }
+    if (base + kScanItems <= n && (reinterpret_cast<uintptr_t>(out + base) & 15) == 0) {
+#pragma unroll
+        for (int q = 0; q < kScanItems / 4; ++q)
+            reinterpret_cast<u32x4 *>(out + base)[q] =
+                u32x4{(uint32_t)o[4 * q], (uint32_t)o[4 * q + 1], (uint32_t)o[4 * q + 2], (uint32_t)o[4 * q + 3]};
+    } else {
+#pragma unroll
+        for (int k = 0; k < kScanItems; ++k)
+            if (base + k < n) out[base + k] = o[k];
     }
 }
 
@@ -1896,10 +1949,11 @@ hipError_t launch_format(const DevTables &t, int32_t *pairs, hipStream_t s) {
 
 hipError_t launch_scan(const DevTables &t, hipStream_t s) {
     const int64_t nb = grid_for(t.N, kScanTile);
+    const int own = nb <= kScanTile ? 1 : 0;  // the apply pass adds up the block sums itself
     hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)nb), dim3(kBlock), 0, s, t.count, t.N, t.scan_tmp);
-    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, t.scan_tmp, nb, t.row_ptr + t.N);
-    hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kBlock), 0, s, t.count, t.N, t.scan_tmp,
-                       t.row_ptr);
+    if (!own) hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, t.scan_tmp, nb, t.row_ptr + t.N);
+    hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kBlock), 0, s, t.count, t.N, t.scan_tmp, own,
+                       t.row_ptr, t.row_ptr + t.N);
     return hipGetLastError();
 }
 

@@ -649,6 +649,38 @@ def test_forest_written_in_groups(P, flags):
     h.close()
 
 
+@pytest.mark.parametrize("flags", [2, TAIL_LISTS], ids=["no_table", "tail_lists"])
+def test_lists_over_many_scan_blocks(P, flags):
+    """Four copies of c5's 256 sets as one forest of 1,024 sets (21.9 M nodes:
+    the lists' offsets are scanned over more block sums than one block adds
+    up, so the scan's middle pass runs).  Copy k's nodes are copy 0's shifted
+    by k * N0, so each holds the same rows and counts, and the valid pairs are
+    four times the single copy's; copy 0's rows are the oracle's (sampled, the
+    last nodes of every copy included)."""
+    import torch
+    w = W.config(5)
+    K = len(w.strings)
+    offs = np.asarray(w.set_offsets, dtype=np.int64)
+    offs4 = np.concatenate([offs[:-1] + k * K for k in range(4)] + [np.array([4 * K])])
+    h1 = P.compile(w.strings, w.vocab, sets=offs, flags=flags)
+    h4 = P.compile(w.strings * 4, w.vocab, sets=offs4, flags=flags)
+    N0 = h1.num_nodes
+    assert h4.num_nodes == 4 * N0 and 4 * N0 > 4096 * 4096
+    assert h4.valid_pairs() == 4 * h1.valid_pairs()
+    rng = np.random.default_rng(95)
+    nodes = np.unique(np.concatenate([rng.integers(0, N0, 1500), np.arange(N0 - 300, N0)])).astype(np.int32)
+    o = Oracle(w.strings, w.vocab, set_offsets=w.set_offsets)
+    rows = o.mask_rows(nodes)
+    cnt = popcounts(rows)
+    for k in range(4):
+        ids = (nodes + k * N0).astype(np.int32)
+        assert np.array_equal(gpu_rows(h4, ids), rows), k
+        assert np.array_equal(h4.valid_counts(torch.as_tensor(ids, device="cuda")).cpu().numpy(), cnt), k
+    h1.close()
+    h4.close()
+    torch.cuda.empty_cache()
+
+
 def nested_chain(depth: int, a: bytes, b: bytes) -> list:
     """a, aa, ..., a^depth, then a^i b and a^i b b for every i < depth: in trie
     order the a^i b strings come deepest first, so each one shares a shorter
