@@ -117,6 +117,8 @@ struct DevTables {
     const int32_t *child_off;   // [N+1]
     const uint8_t *child_byte;  // [N-S]
     const int32_t *child_node;  // [N-S]
+    const int32_t *child_pos;   // [N-S] node_pos of child_node[k]: where a walk goes on along its string
+    const uint64_t *child_at;   // [blob_bytes] child range of node_at[p]: child_off lo | hi << 32
     // vocabulary (a2)
     const uint32_t *tok_off;    // [V+1]
     const uint8_t *tok_blob;

@@ -1164,15 +1164,29 @@ __global__ void __launch_bounds__(kBlock) k_child_count(DevTables t, int32_t *cn
 // every non-root node into its parent's list (cursor zeroed before); the
 // order inside a list is free: a lookup matches the child byte
 __global__ void __launch_bounds__(kBlock) k_child_fill(DevTables t, int32_t *cursor, int32_t *child_node,
-                                                       uint8_t *child_byte) {
+                                                       uint8_t *child_byte, int32_t *child_pos) {
     const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (g >= t.N || t.depth[g] == 0) return;
     bool bad = false;  // counted once, by k_child_count
     const int32_t par = lay_parent(t.node_pos, t.node_at, t.N, t.blob_bytes, g, &bad);
     if (par < 0) return;
     const int32_t slot = t.child_off[par] + atomicAdd(&cursor[par], 1);
+    const int32_t pos = t.node_pos[g];
     child_node[slot] = (int32_t)g;
-    child_byte[slot] = t.blob[t.node_pos[g]];
+    child_pos[slot] = pos;
+    child_byte[slot] = t.blob[pos];
+}
+
+// child_at[p]: the child range of the node whose edge byte is blob[p] (the
+// pads: their set's root), for walks that stop inside a string
+__global__ void __launch_bounds__(kBlock) k_child_at(DevTables t, uint64_t *child_at) {
+    const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (p >= t.blob_bytes) return;
+    const int32_t n = t.node_at[p];
+    uint64_t r = 0;
+    if (n >= 0 && (int64_t)n < t.N)
+        r = (uint64_t)(uint32_t)t.child_off[n] | ((uint64_t)(uint32_t)t.child_off[n + 1] << 32);
+    child_at[p] = r;
 }
 
 // ------------------------------------------------- fixed-format strings ---
@@ -1272,17 +1286,20 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
         int32_t lo = t.child_off[n0], hi = t.child_off[n0 + 1];  // loaded beside the token's offsets
         while (i < len && n >= 0) {
             const uint32_t c = t.tok_blob[a + i];
-            // child of n along c: its child bytes and ids, 64 lanes at a
-            // time, loaded together with the token byte
-            int32_t nx = TAM_DEAD;
+            // child of n along c: its child bytes, ids and blob positions, 64
+            // lanes at a time, loaded together with the token byte
+            int32_t nx = TAM_DEAD, px = 0;
             for (int32_t k0 = lo; k0 < hi; k0 += kWave) {
                 const int32_t k = k0 + lane;
                 const bool in = k < hi;
                 const uint32_t cb = in ? (uint32_t)t.child_byte[k] : 0x100u;
                 const int32_t cn = in ? t.child_node[k] : TAM_DEAD;
+                const int32_t cp = in ? t.child_pos[k] : 0;
                 const uint64_t m = __ballot(cb == c);
                 if (m) {
-                    nx = __shfl(cn, (int)__builtin_ctzll(m), kWave);
+                    const int j = (int)__builtin_ctzll(m);
+                    nx = __shfl(cn, j, kWave);
+                    px = __shfl(cp, j, kWave);
                     break;
                 }
             }
@@ -1293,7 +1310,7 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
                 n = TAM_DEAD;
                 break;
             }
-            int64_t p = t.node_pos[n];
+            int64_t p = px;
             for (;;) {
                 const int64_t q = p + 1 + lane;
                 const uint32_t sb = q < t.blob_bytes ? (uint32_t)t.blob[q] : 0x200u;
@@ -1307,11 +1324,15 @@ __global__ void __launch_bounds__(kBlock) k_advance(DevTables t, const int32_t *
                 i += k;
                 if (k < kWave || i >= len || f < kWave) break;
             }
-            n = t.node_at[p];
-            if (i < len) {
-                lo = t.child_off[n];
-                hi = t.child_off[n + 1];
+            if (i >= len) {  // the token ends inside the string: its node
+                n = t.node_at[p];
+                break;
             }
+            // the token leaves the string at p: the child range of the node
+            // there, in one load (the node itself is not needed)
+            const uint64_t r = t.child_at[p];
+            lo = (int32_t)(uint32_t)r;
+            hi = (int32_t)(uint32_t)(r >> 32);
         }
     }
     if (lane == 0) out[b] = n;
@@ -1897,7 +1918,8 @@ hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, in
 }
 
 hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *child_node, uint8_t *child_byte,
-                              int32_t *tmp, int32_t *scan_tmp, hipStream_t s) {
+                              int32_t *child_pos, uint64_t *child_at, int32_t *tmp, int32_t *scan_tmp,
+                              hipStream_t s) {
     if (t.N <= 0) return hipSuccess;
     const unsigned g = grid_for(t.N, kBlock);
     hipError_t e = launch_fill_i32(tmp, t.N, 0, s);
@@ -1912,7 +1934,9 @@ hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *c
     if (e != hipSuccess) return e;
     DevTables tf = t;
     tf.child_off = child_off;
-    hipLaunchKernelGGL(k_child_fill, dim3(g), dim3(kBlock), 0, s, tf, tmp, child_node, child_byte);
+    hipLaunchKernelGGL(k_child_fill, dim3(g), dim3(kBlock), 0, s, tf, tmp, child_node, child_byte, child_pos);
+    if (t.blob_bytes > 0)
+        hipLaunchKernelGGL(k_child_at, dim3(grid_for(t.blob_bytes, kBlock)), dim3(kBlock), 0, s, tf, child_at);
     return hipGetLastError();
 }
 

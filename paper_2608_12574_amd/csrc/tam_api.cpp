@@ -447,7 +447,7 @@ tam_status check_device_handle(const tam_handle *h) {
 // tails or lists yet.
 void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v, uint8_t *tb, size_t o_blob,
                      size_t o_node_at, size_t o_node_pos, size_t o_depth, size_t o_child_off, size_t o_child_byte,
-                     size_t o_child_node) {
+                     size_t o_child_node, size_t o_child_pos, size_t o_child_at) {
     t.blob = tb + o_blob;
     t.node_at = reinterpret_cast<const int32_t *>(tb + o_node_at);
     t.node_pos = reinterpret_cast<const int32_t *>(tb + o_node_pos);
@@ -455,6 +455,8 @@ void set_trie_tables(tam::DevTables &t, const tam_handle *h, const tam_vocab *v,
     t.child_off = reinterpret_cast<const int32_t *>(tb + o_child_off);
     t.child_byte = tb + o_child_byte;
     t.child_node = reinterpret_cast<const int32_t *>(tb + o_child_node);
+    t.child_pos = reinterpret_cast<const int32_t *>(tb + o_child_pos);
+    t.child_at = reinterpret_cast<const uint64_t *>(tb + o_child_at);
     t.tok_off = v->d_tok_off;
     t.tok_blob = v->d_tok_blob;
     t.fps = v->d_fps;
@@ -530,7 +532,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     // and tail compression's tail_span, row_of, row_at
     uint8_t *trie_base = nullptr;
     size_t o_blob = 0, o_node_at = 0, o_node_pos = 0, o_depth = 0, o_child_off = 0, o_child_byte = 0,
-           o_child_node = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0, o_tail_rec = 0,
+           o_child_node = 0, o_child_pos = 0, o_child_at = 0, o_sub_end = 0, o_tail_span = 0, o_row_of = 0, o_row_at = 0, o_tail_rec = 0,
            o_root_rows = 0;
     // tail compression's split (with a table for the branching nodes, or with
     // sparse lists for them)
@@ -572,6 +574,8 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         o_child_off = ta.take<int32_t>(hh->N + 1);
         o_child_byte = ta.take<uint8_t>(hh->edges);
         o_child_node = ta.take<int32_t>(hh->edges);
+        o_child_pos = ta.take<int32_t>(hh->edges);
+        o_child_at = ta.take<uint64_t>(hh->blob_bytes);
         o_sub_end = ta.take<int32_t>((hh->flags & TAM_FLAG_LAZY_ROWS) ? hh->N : 0);
         o_tail_span = ta.take<int32_t>(split ? hh->N : 0);
         o_row_of = ta.take<int32_t>(split ? hh->N : 0);
@@ -598,7 +602,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         }
         hh->device_bytes = (int64_t)ta.used;
         set_trie_tables(te, hh, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
-                        o_child_node);
+                        o_child_node, o_child_pos, o_child_at);
         hh->d_err = reinterpret_cast<int32_t *>(trie_base + o_err);
         hh->h_err = tam::err_slot_take();
         te.err = hh->d_err;
@@ -745,7 +749,10 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
         if (e == hipSuccess && r.n_hi == hh->N)
             e = tam::launch_child_lists(te, reinterpret_cast<int32_t *>(trie_base + o_child_off),
                                         reinterpret_cast<int32_t *>(trie_base + o_child_node),
-                                        trie_base + o_child_byte, reinterpret_cast<int32_t *>(trie_base + o_tmp),
+                                        trie_base + o_child_byte,
+                                        reinterpret_cast<int32_t *>(trie_base + o_child_pos),
+                                        reinterpret_cast<uint64_t *>(trie_base + o_child_at),
+                                        reinterpret_cast<int32_t *>(trie_base + o_tmp),
                                         reinterpret_cast<int32_t *>(trie_base + o_scan_tmp), s);
         hook_ms += ms_since(t1);
         if (e != hipSuccess) {
@@ -866,7 +873,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
 
     tam::DevTables &t = h->dt;
     set_trie_tables(t, h, vocab, trie_base, o_blob, o_node_at, o_node_pos, o_depth, o_child_off, o_child_byte,
-                    o_child_node);
+                    o_child_node, o_child_pos, o_child_at);
     t.err = h->d_err;
     t.hits = early ? te.hits : reinterpret_cast<int32_t *>(base + o_hits_b);
     t.count = early ? te.count : reinterpret_cast<int32_t *>(base + o_count_b);

@@ -88,10 +88,12 @@ hipError_t launch_node_at(const StrRec *strs, int64_t s0, int64_t s1, int64_t bl
 hipError_t launch_node_pos(const DevTables &t, int32_t *node_pos, int64_t n0, int64_t n1, int64_t b0, int64_t b1,
                            hipStream_t s);
 // the child lists of every node (node_pos complete): child_off[N+1],
-// child_node/child_byte[N - roots]; tmp [N] and scan_tmp [scan_tmp_elems(N)]
-// are scratch
+// child_node/child_byte/child_pos[N - roots], and child_at[blob_bytes] (the
+// child range of the node at each blob position); tmp [N] and scan_tmp
+// [scan_tmp_elems(N)] are scratch
 hipError_t launch_child_lists(const DevTables &t, int32_t *child_off, int32_t *child_node, uint8_t *child_byte,
-                              int32_t *tmp, int32_t *scan_tmp, hipStream_t s);
+                              int32_t *child_pos, uint64_t *child_at, int32_t *tmp, int32_t *scan_tmp,
+                              hipStream_t s);
 hipError_t launch_scan(const DevTables &t, hipStream_t s);
 hipError_t launch_zero(uint64_t *p, int64_t words, hipStream_t s);
 int64_t mark_blocks(int64_t N);
