@@ -626,6 +626,10 @@ def test_forest_written_in_groups(P, flags):
     nodes = np.unique(np.concatenate([sample_nodes(o, 2000, 91), o.roots, last])).astype(np.int32)
     exp_rows = o.mask_rows(nodes)
     assert np.array_equal(gpu_rows(h, nodes), exp_rows)
+    if flags & 2:  # the lists' capacity: summed per group (device) or over all strings (host only)
+        hh = P.compile(strings, vocab, sets=offs, flags=flags | P.FLAG_HOST_ONLY)
+        assert h.list_capacity == hh.list_capacity > 0
+        hh.close()
     if not flags & LAZY:  # counts, and the device phases run again over the groups' grid
         cnt = popcounts(exp_rows)
         assert np.array_equal(h.valid_counts(torch.as_tensor(nodes, device="cuda")).cpu().numpy(), cnt)
@@ -667,6 +671,7 @@ def test_lists_over_many_scan_blocks(P, flags):
     N0 = h1.num_nodes
     assert h4.num_nodes == 4 * N0 and 4 * N0 > 4096 * 4096
     assert h4.valid_pairs() == 4 * h1.valid_pairs()
+    assert h4.list_capacity == 4 * h1.list_capacity
     rng = np.random.default_rng(95)
     nodes = np.unique(np.concatenate([rng.integers(0, N0, 1500), np.arange(N0 - 300, N0)])).astype(np.int32)
     o = Oracle(w.strings, w.vocab, set_offsets=w.set_offsets)
