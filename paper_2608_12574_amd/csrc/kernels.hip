@@ -1070,8 +1070,6 @@ __global__ void __launch_bounds__(kBlock) k_node_at(const StrRec *__restrict__ s
     if (bad) atomicAdd(err, bad);
 }
 
-// node_pos of the nodes [n0, n1): -1 for a root, else a large value that
-// k_first_pos lowers
 // Tail compression's tables from the string records [s0, s1), one thread per
 // string: row_of and tail_span of the nodes it creates (path indices lcp ..
 // len, ids first ...; see TailRec).  Ids outside [0, N) are counted in *err
@@ -1126,6 +1124,8 @@ __global__ void __launch_bounds__(kBlock) k_row_at(const int32_t *__restrict__ n
     row_at[p] = row_of[n];
 }
 
+// node_pos of the nodes [n0, n1): -1 for a root, else a large value that
+// k_first_pos lowers
 __global__ void __launch_bounds__(kBlock) k_pos_init(const int32_t *__restrict__ depth, int64_t n0, int64_t n1,
                                                      int32_t *__restrict__ node_pos) {
     const int64_t g = n0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
