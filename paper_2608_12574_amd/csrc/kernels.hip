@@ -11,16 +11,20 @@
 //               crediting of a match to the node |t| bytes back (Section 4.2),
 //               done for all nodes at once instead of along a DFS.  It keeps
 //               the hits, ORs them into the zeroed table with 64-bit atomics
-//               (nodes with a dense row) and, for lists, counts per node.
+//               (nodes with a dense row) and, for lists, counts per node
+//               (without a table under tail compression, it also records
+//               each hit listed on a branching node with its rank).
 //   k_scan_* -- exclusive prefix sum of the counts into row offsets.
-//   k_fill   -- writes the hits' token ids into the per-node lists.
+//   k_fill   -- writes the hits' token ids into the per-node lists;
+//               k_fill_records places the recorded hits instead.
 //   k_rows   -- one wave per row builds rows in registers from the lists
 //               (canonical rows of handles without a dense table).
 // Serving (Section 2, Eq. 1 and the extended transition function):
 //   k_apply  -- write-mostly masking of [B, V] logits (lists, tail rows, and
 //               unaligned rows); k_apply_dense for dense-table rows, three
-//               rows per block.
-//   k_advance-- B byte walks over the child tables, one wave per row.
+//               rows per block (two for small batches).
+//   k_advance-- B byte walks over the child tables and along the strings of
+//               the blob, one wave per row.
 //   k_export_dense, k_export_tail -- canonical rows out of the dense table and
 //               (tail compression) the probe's hits.
 // Rows built on demand (lazy computation with a bounded cache, Appendix):
@@ -29,6 +33,9 @@
 //   k_lazy_probe -- the missing rows, from the suffix probes of the node's
 //               subtree only, while the victims' rows are cleared; k_apply
 //               then reads the cache.
+// Trie tables on the device (from the blob and one record per string):
+//   k_node_at, k_pos_init, k_first_pos, k_child_count, k_child_fill,
+//   k_child_at, and under tail compression k_tail_nodes, k_root_rows, k_row_at.
 // Fixed-format values (character-position masks):
 //   k_format -- every word of the rows of positions 0..L+1, by wave ballots.
 #include <hip/hip_runtime.h>
