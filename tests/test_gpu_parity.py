@@ -151,21 +151,22 @@ def test_tiny_random_sets(P, flags):
 
 @pytest.mark.parametrize("flags", FLAGS, ids=FLAG_IDS)
 def test_apply_batch_beyond_one_launch(P, flags):
-    """A batch larger than one launch's row limit (65,535 row groups; two rows
-    per block for dense-table rows): every representation splits it into
-    several launches.  Dead and out-of-range rows are spread over it."""
+    """A batch larger than one launch's row limit (65,535 row groups; three
+    rows per block for dense-table rows here): every representation splits it
+    into several launches, and the fp32 batch ends exactly on a launch
+    boundary.  Dead and out-of-range rows are spread over it."""
     rng = np.random.default_rng(77)
     words = [b"get_", b"list_", b"item", b"user", b"s", b"_id"]
     strings = sorted({b"".join(words[i] for i in rng.integers(0, 6, size=rng.integers(1, 4))) for _ in range(40)})
     vocab = [bytes([c]) for c in range(256)] + words + [b"get", b"list", b"er", b'"']
     o = Oracle(strings, vocab)
     h = P.compile(strings, vocab, flags=flags)
-    B = 2 * 65535 + 3
+    B = 3 * 65535 + 3
     nodes = rng.integers(0, o.N, size=B).astype(np.int32)
     nodes[::1009] = -1
     nodes[5::2003] = o.N
     check_apply(P, h, o, nodes, "bf16", seed=1)
-    check_apply(P, h, o, nodes[: 65535 * 2], "fp32", seed=2)
+    check_apply(P, h, o, nodes[: 65535 * 3], "fp32", seed=2)
     h.close()
 
 
