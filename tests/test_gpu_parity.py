@@ -687,6 +687,64 @@ def test_lists_over_many_scan_blocks(P, flags):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("flags", [2, TAIL_LISTS], ids=["no_table", "tail_lists"])
+def test_graph_capture_replays_forest_groups(P, flags):
+    """A forest written in four groups (fourteen sets), captured in a HIP graph:
+    rebuild (for tail compression without a table, the probe pass over the
+    groups' table in one launch, the scan and the records' fill), apply and
+    advance; every replay, with eager rebuilds between replays, gives the
+    oracle's rows, masked logits and states."""
+    import torch
+    w5 = W.config(5)
+    mixed, vocab, moffs = W.mixed_forest()
+    sets = [w5.strings[int(w5.set_offsets[j]):int(w5.set_offsets[j + 1])] for j in range(10)]
+    sets += [mixed[int(moffs[j]):int(moffs[j + 1])] for j in range(len(moffs) - 1)]
+    strings = [s for g in sets for s in g]
+    offs = np.cumsum([0] + [len(g) for g in sets])
+    o = Oracle(strings, vocab, set_offsets=offs)
+    h = P.compile(strings, vocab, sets=offs, flags=flags)
+    B, V = 96, len(vocab)
+    nodes = np.unique(np.concatenate([o.roots, sample_nodes(o, 200, 96)])).astype(np.int32)[:B]
+    B = len(nodes)
+    ids = torch.as_tensor(nodes, device="cuda")
+    src = torch.as_tensor(host_logits(B, V, "fp32", seed=97).numpy(), device="cuda")
+    toks_np = W.choose_valid_tokens(np.random.default_rng(98), o.mask_rows(nodes), V)
+    toks = torch.as_tensor(toks_np, device="cuda")
+    x = src.clone()
+    out = torch.empty_like(ids)
+    exp_x = o.apply(nodes, bits_of(src.cpu()).view(np.uint32), 0)
+    exp_out = o.advance(nodes, toks_np)
+    M = h.valid_pairs()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        h.rebuild()
+        h.apply_mask(ids, x)
+        h.advance(ids, toks, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        h.rebuild()
+        h.apply_mask(ids, x)
+        h.advance(ids, toks, out=out)
+    for r in range(4):
+        x.copy_(src)
+        out.fill_(-7)
+        if r % 2:
+            h.rebuild()  # eager work on the same handle between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits_of(x).view(np.uint32), exp_x), r
+        assert np.array_equal(out.cpu().numpy(), exp_out), r
+        assert np.array_equal(gpu_rows(h, nodes[:48]), o.mask_rows(nodes[:48])), r
+    assert h.valid_pairs() == M
+    del graph
+    torch.cuda.synchronize()
+    h.close()
+
+
 def nested_chain(depth: int, a: bytes, b: bytes) -> list:
     """a, aa, ..., a^depth, then a^i b and a^i b b for every i < depth: in trie
     order the a^i b strings come deepest first, so each one shares a shorter
