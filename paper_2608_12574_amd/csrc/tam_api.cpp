@@ -504,7 +504,7 @@ tam_status compile_with(const uint8_t *str_bytes, const int64_t *str_off, int64_
     if (S < 0 || set_off[0] != 0 || set_off[S] != K) return fail(TAM_E_INVAL, "set_off must run from 0 to K");
     for (int64_t j = 0; j < S; ++j)
         if (set_off[j + 1] <= set_off[j]) return fail(TAM_E_INVAL, "every set must hold at least one string");
-    tam_options o{0x22, 0};
+    tam_options o{0x22, 0, 0};
     if (opt) o = *opt;
     if (o.terminator < 0 || o.terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
     if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
@@ -947,7 +947,7 @@ tam_status compile_format(const uint8_t *classes, int64_t L, tam_vocab *vocab, c
     *out = nullptr;
     if (L < 1 || L > INT32_MAX - 3) return fail(TAM_E_INVAL, "L must be in [1, 2^31-4]");
     if (!classes) return fail(TAM_E_INVAL, "classes is null");
-    tam_options o{0x22, 0};
+    tam_options o{0x22, 0, 0};
     if (opt) o = *opt;
     if (o.terminator < 0 || o.terminator > 255) return fail(TAM_E_INVAL, "terminator must be a byte value");
     if (alloc && (!alloc->alloc || !alloc->free)) return fail(TAM_E_INVAL, "allocator callbacks are null");
@@ -1207,7 +1207,7 @@ tam_status tam_compile(const uint8_t *str_bytes, const int64_t *str_off, int64_t
     *out = nullptr;
     if (K <= 0) return fail(TAM_E_INVAL, "K must be >= 1");
     if (!csr_ok(str_off, K)) return fail(TAM_E_INVAL, "str_off must start at 0 and be non-decreasing");
-    tam_options o{0x22, 0};
+    tam_options o{0x22, 0, 0};
     if (opt) o = *opt;
     tam_vocab *v = nullptr;
     hipStream_t s = static_cast<hipStream_t>(stream);
