@@ -85,6 +85,31 @@ def test_allocator_failure_gives_nomem_and_frees_all(P, flags):
         assert not a.live, (k, len(a.live))
 
 
+@pytest.mark.parametrize("flags", [2, 2 | 8], ids=["no_table", "tail_lists"])
+def test_allocator_failure_in_a_forest_written_in_groups(P, flags):
+    """A forest of ten sets (written and uploaded in four groups; without a
+    table under tail compression each group gets its own buffer of listed-hit
+    records): every allocation failing in turn gives TAM_E_NOMEM, no handle,
+    and every block back."""
+    w = W.config(5)
+    offs = [int(x) for x in w.set_offsets[:11]]
+    strings = w.strings[:offs[-1]]
+    ok = CountingAllocator(P)
+    rc, h = raw_compile(P, strings, w.vocab, flags, ok, sets=offs)
+    assert rc == 0 and ok.calls >= 3
+    P.lib().tam_destroy(h)
+    torch.cuda.synchronize()
+    assert not ok.live
+    for k in range(ok.calls):
+        a = CountingAllocator(P, fail_at=k)
+        rc, h = raw_compile(P, strings, w.vocab, flags, a, sets=offs)
+        assert rc == -3, (k, rc)
+        assert not h.value
+        assert "allocation failed" in P.lib().tam_last_error().decode()
+        torch.cuda.synchronize()
+        assert not a.live, (k, len(a.live))
+
+
 def test_allocator_failure_in_vocabulary_and_format(P):
     L = P.lib()
     tb, to = P.tam.csr([b"1", b"-", b'"', b"12"])
