@@ -32,14 +32,19 @@ __host__ __device__ __forceinline__ uint64_t hash_final(uint32_t h) {
     return ((p >> 32) | (p << 32)) | 1ull;  // 0 never occurs as a key
 }
 
-// Vocabulary table: open addressing over buckets of kBucket 16-bit
-// fingerprints (16 bytes per bucket: one load), one slot per distinct
-// non-empty token string.  A slot's 16-byte payload (its first 8 bytes stored
-// last byte first, its smallest token id, length and duplicate count) is read
-// only on a fingerprint match, with one load; bytes 8..15 of a longer token
-// sit in pay_hi[slot] and are read only when the first 8 match.  Suffixes of
-// at most kShortLen bytes skip the hash: short_hits maps them straight to
-// their hit (short_index).
+// Vocabulary table: open addressing over buckets of kBucket slots, one slot
+// per distinct non-empty token string.  A bucket is 16 bytes (one load): four
+// words, word i holding the 12-bit fingerprints of slots 2i and 2i + 1 in bits
+// 0..23 and byte i of the bucket's base in bits 24..31.  The strings of the
+// table are numbered bucket by bucket (a bucket's used slots come first), the
+// base being the number of the bucket's first slot, so a slot's string is
+// base + its index in the bucket.  That number indexes the 16-byte payloads
+// (its first 8 bytes stored last byte first, its smallest token id, length and
+// duplicate count), read only on a fingerprint match, with one load; bytes
+// 8..15 of a longer token sit in pay_hi[number] and are read only when the
+// first 8 match.  Payloads exist only for strings, not for empty slots, so the
+// tables the probes read stay small.  Suffixes of at most kShortLen bytes skip
+// the hash: short_hits maps them straight to their hit (short_index).
 constexpr int kBucket = 8;    // fingerprints per bucket
 constexpr int kWin = 16;      // path bytes a probing node keeps in registers
 constexpr int kBlobPad = 32;  // zero bytes before and after the string blob (and after the token blob)
@@ -47,7 +52,7 @@ constexpr int kShortLen = 2;  // suffix lengths answered by short_hits
 constexpr int kShortEntries = 256 + 65536;
 
 __host__ __device__ __forceinline__ uint32_t fingerprint(uint64_t key) {
-    return (uint32_t)(key >> 48) | 1u;  // 16 bits; 0 marks an empty slot
+    return (uint32_t)(key >> 52) | 1u;  // 12 bits; 0 marks an empty slot
 }
 
 // Index in short_hits of the string of d <= kShortLen bytes whose last byte is
@@ -62,11 +67,12 @@ struct alignas(16) SlotPay {
     uint16_t len;     // string length in bytes
     uint16_t count;   // number of token ids with this string
 };
-// pay_hi[slot]: byte k - 8 = token byte len-1-k for 8 <= k < min(len, 16), then
-// zeros (0 for strings of at most 8 bytes).
+// pay_hi[string]: byte k - 8 = token byte len-1-k for 8 <= k < min(len, 16),
+// then zeros (0 for strings of at most 8 bytes).
 
 // What the probe pass stores per (node, suffix length): the token id when the
-// string has one id, -2 - slot when it has several, -1 when no token matches.
+// string has one id, -2 - its string number when it has several, -1 when no
+// token matches.
 __host__ __device__ __forceinline__ int32_t hit_of_slot(int32_t slot, int32_t first, int count) {
     return count == 1 ? first : -2 - slot;
 }

@@ -438,10 +438,11 @@ tam_status build_trie(const uint8_t *sb, const int64_t *so, int64_t K, const int
 /*
  * Vocabulary tables (the paper's vocabulary decoding and its per-tokenizer
  * matcher, built here as an exact hash of every distinct token string keyed by
- * its bytes read last-to-first).  Slots live in buckets of kBucket 16-bit
+ * its bytes read last-to-first).  Slots live in buckets of kBucket 12-bit
  * fingerprints; a key starts at its home bucket and moves to the next bucket
  * only when the bucket is full.  Duplicate strings share a slot and chain their
- * ids in ascending order.
+ * ids in ascending order.  Once placed, the strings are numbered bucket by
+ * bucket and the payloads stored by that number (see device_tables.hpp).
  */
 tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_vocab *h,
                        std::string *err) {
@@ -543,7 +544,7 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     auto place = [&](int64_t v, uint64_t b, uint64_t stop, bool wrap) -> bool {
         const uint32_t off = h->tok_off[(size_t)v];
         const uint32_t len = h->tok_off[(size_t)v + 1] - off;
-        const uint16_t fp = (uint16_t)fingerprint(keys[(size_t)v]);
+        const uint16_t fp = (uint16_t)fingerprint(keys[(size_t)v]);  // 12 bits, never 0
         for (uint64_t n = 0; n < nbuckets; ++n) {
             for (int i = 0; i < kBucket; ++i) {
                 const uint64_t sl = b * kBucket + (uint64_t)i;
@@ -614,9 +615,49 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
         *err = "more than 65535 tokens share one byte string";
         return TAM_E_TOOLARGE;
     }
+    // The strings numbered bucket by bucket (a bucket's used slots are its
+    // first ones: slots fill in order), the payloads moved to that number, and
+    // each bucket packed into four words: the 12-bit fingerprints of slots 2i
+    // and 2i + 1 in bits 0..23 of word i, byte i of the bucket's base (its
+    // first string's number) in bits 24..31.
+    const int64_t bchunk = 1 << 14, nbchunks = ((int64_t)nbuckets + bchunk - 1) / bchunk;
+    std::vector<int64_t> bsum((size_t)nbchunks + 1, 0);
+    parallel_for(nbchunks, host_threads(nbchunks), [&](int64_t c) {
+        int64_t n = 0;
+        for (int64_t b = c * bchunk; b < std::min<int64_t>((int64_t)nbuckets, (c + 1) * bchunk); ++b)
+            for (int i = 0; i < kBucket; ++i) n += h->fps[(size_t)(b * kBucket + i)] != 0;
+        bsum[(size_t)c + 1] = n;
+    });
+    for (int64_t c = 0; c < nbchunks; ++c) bsum[(size_t)c + 1] += bsum[(size_t)c];
+    const int64_t nstr = bsum[(size_t)nbchunks];
+    hvec<SlotPay> pay_c((size_t)std::max<int64_t>(nstr, 1));
+    hvec<uint64_t> pay_hi_c((size_t)std::max<int64_t>(nstr, 1), 0);
+    hvec<uint16_t> packed(cap);  // the buckets' words, as 16-bit halves
+    if (nstr == 0) pay_c[0] = empty;
+    parallel_for(nbchunks, host_threads(nbchunks), [&](int64_t c) {
+        int64_t at = bsum[(size_t)c];
+        uint32_t *words = reinterpret_cast<uint32_t *>(packed.data());
+        for (int64_t b = c * bchunk; b < std::min<int64_t>((int64_t)nbuckets, (c + 1) * bchunk); ++b) {
+            const uint32_t base = (uint32_t)at;
+            for (int i = 0; i < kBucket / 2; ++i) {
+                const uint32_t f0 = h->fps[(size_t)(b * kBucket + 2 * i)], f1 = h->fps[(size_t)(b * kBucket + 2 * i + 1)];
+                words[(size_t)(b * 4 + i)] = f0 | (f1 << 12) | (((base >> (8 * i)) & 0xffu) << 24);
+            }
+            for (int i = 0; i < kBucket; ++i) {
+                const uint64_t sl = b * kBucket + (uint64_t)i;
+                if (h->fps[sl] == 0) break;
+                pay_c[(size_t)at] = h->pay[sl];
+                pay_hi_c[(size_t)at] = h->pay_hi[sl];
+                ++at;
+            }
+        }
+    });
+    h->fps.swap(packed);
+    h->pay.swap(pay_c);
+    h->pay_hi.swap(pay_hi_c);
     // the hits of every string of at most kShortLen bytes, indexed by its bytes
     h->short_hits.assign((size_t)kShortEntries, -1);
-    for (uint64_t q = 0; q < cap; ++q) {
+    for (int64_t q = 0; q < nstr; ++q) {
         const SlotPay &sp = h->pay[(size_t)q];
         if (sp.first < 0 || sp.len > kShortLen) continue;
         const uint8_t *tb = blob + h->tok_off[(size_t)sp.first];
@@ -627,11 +668,12 @@ tam_status build_vocab(const uint8_t *tb, const int64_t *to, int64_t V, tam_voca
     // token ids sharing one string of that length (for the list size bound)
     std::vector<int64_t> dup((size_t)max_len + 1, 0);
     {
-        std::vector<std::vector<int64_t>> part((size_t)npchunks);
-        parallel_for(npchunks, host_threads(npchunks), [&](int64_t c) {
+        const int64_t nsc = (nstr + pchunk - 1) / pchunk;
+        std::vector<std::vector<int64_t>> part((size_t)nsc);
+        parallel_for(nsc, host_threads(nsc), [&](int64_t c) {
             std::vector<int64_t> &d = part[(size_t)c];
             d.assign((size_t)max_len + 1, 0);
-            for (int64_t q = c * pchunk; q < std::min<int64_t>((int64_t)cap, (c + 1) * pchunk); ++q) {
+            for (int64_t q = c * pchunk; q < std::min<int64_t>(nstr, (c + 1) * pchunk); ++q) {
                 const SlotPay &sp = h->pay[(size_t)q];
                 if (sp.first >= 0) d[(size_t)sp.len] = std::max<int64_t>(d[(size_t)sp.len], sp.count);
             }

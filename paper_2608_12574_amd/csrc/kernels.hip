@@ -135,7 +135,7 @@ __device__ __forceinline__ uint64_t home_bucket(const DevTables &t, uint64_t key
     return (key & t.slot_mask) / kBucket;
 }
 
-// The kBucket fingerprints of a bucket: kBucket / 8 16-byte loads.
+// A bucket: its kBucket fingerprints and its base, in one 16-byte load.
 struct Bucket {
     u32x4 q[kBucket / 8];
 };
@@ -148,19 +148,20 @@ __device__ __forceinline__ Bucket load_bucket(const DevTables &t, uint64_t b) {
     return k;
 }
 
+// The number of the bucket's first string (byte i in bits 24..31 of word i).
+__device__ __forceinline__ uint32_t bucket_base(const Bucket &bk) {
+    return (bk.q[0].x >> 24) | ((bk.q[0].y >> 24) << 8) | ((bk.q[0].z >> 24) << 16) | (bk.q[0].w & 0xff000000u);
+}
+
 // Bit i of *match: slot i holds fingerprint fp; bit i of *empty: slot i is empty.
 __device__ __forceinline__ void bucket_masks(const Bucket &bk, uint32_t fp, uint32_t *match, uint32_t *empty) {
     uint32_t mm = 0, ee = 0;
+    const uint32_t w[4] = {bk.q[0].x, bk.q[0].y, bk.q[0].z, bk.q[0].w};
 #pragma unroll
-    for (int q = 0; q < kBucket / 8; ++q) {
-        const uint32_t w[4] = {bk.q[q].x, bk.q[q].y, bk.q[q].z, bk.q[q].w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t lo16 = w[i] & 0xffffu, hi16 = w[i] >> 16;
-            const int sh = 8 * q + 2 * i;
-            mm |= ((lo16 == fp ? 1u : 0u) | (hi16 == fp ? 2u : 0u)) << sh;
-            ee |= ((lo16 == 0u ? 1u : 0u) | (hi16 == 0u ? 2u : 0u)) << sh;
-        }
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t a = w[i] & 0xfffu, b = (w[i] >> 12) & 0xfffu;
+        mm |= ((a == fp ? 1u : 0u) | (b == fp ? 2u : 0u)) << (2 * i);
+        ee |= ((a == 0u ? 1u : 0u) | (b == 0u ? 2u : 0u)) << (2 * i);
     }
     *match = mm;
     *empty = ee;
@@ -188,27 +189,28 @@ __device__ __forceinline__ int32_t short_hit(const DevTables &t, int d, uint32_t
 }
 
 // Slot (0..kBucket-1) of the first fingerprint fp in bucket bk, or -1.  The
-// eight 16-bit fingerprints are compared two per dword: a half of x = w ^ fp:fp
-// is zero exactly where the fingerprint matches, and (x - 0x00010001) & ~x
-// sets bit 15 of a zero half; a borrow out of a zero low half can flag the
-// high half too, but the lowest flagged half is always a true match.  *open:
-// the bucket's last slot is empty, so the bucket was never full and a key
-// whose home it is lies in it (slots fill in order and are never cleared).
+// eight 12-bit fingerprints are compared two per word: a field of
+// x = (w ^ fp:fp) & 0xffffff is zero exactly where the fingerprint matches, and
+// (x - 0x001001) & ~x sets bit 11 of a zero field; a borrow out of a zero low
+// field can flag the high field too, but the lowest flagged field is always a
+// true match.  *open: the bucket's last slot is empty, so the bucket was never
+// full and a key whose home it is lies in it (slots fill in order and are
+// never cleared).
 __device__ __forceinline__ int first_match(const Bucket &bk, uint32_t fp, bool *open) {
-    const uint32_t fp2 = fp * 0x00010001u;
+    const uint32_t fp2 = fp | (fp << 12);
     const uint32_t w[4] = {bk.q[0].x, bk.q[0].y, bk.q[0].z, bk.q[0].w};
     int s = -1;
 #pragma unroll
     for (int i = 3; i >= 0; --i) {
-        const uint32_t x = w[i] ^ fp2;
-        const uint32_t z = (x - 0x00010001u) & ~x & 0x80008000u;
-        if (z) s = 2 * i + ((z & 0x8000u) ? 0 : 1);
+        const uint32_t x = (w[i] ^ fp2) & 0xffffffu;
+        const uint32_t z = (x - 0x001001u) & ~x & 0x800800u;
+        if (z) s = 2 * i + ((z & 0x800u) ? 0 : 1);
     }
-    *open = (w[3] >> 16) == 0u;
+    *open = ((w[3] >> 12) & 0xfffu) == 0u;
     return s;
 }
 
-// The slot holding the string of d bytes that ends at blob[pos] (reversed
+// The number of the string of d bytes that ends at blob[pos] (reversed
 // window (lo, hi)), with home bucket b and fingerprint fp, or -1; its payload
 // goes to *pay.  Buckets are scanned from b until one with an empty slot (load
 // <= 1/4 guarantees one exists): a key sits in a later bucket only if every
@@ -218,11 +220,13 @@ __device__ __forceinline__ int32_t probe_from(const DevTables &t, uint64_t b, ui
     const uint64_t bmask = t.slot_mask / kBucket;
     for (;;) {
         uint32_t match, empty;
-        bucket_masks(load_bucket(t, b), fp, &match, &empty);
+        const Bucket bk = load_bucket(t, b);
+        bucket_masks(bk, fp, &match, &empty);
+        const uint32_t base = bucket_base(bk);
         while (match) {
             const int i = __builtin_ctz(match);
             match &= match - 1;
-            const int32_t sl = (int32_t)(b * kBucket + (uint64_t)i);
+            const int32_t sl = (int32_t)(base + (uint32_t)i);
             const SlotPay m = t.pay[sl];
             const uint64_t mhi = d > 8 ? t.pay_hi[sl] : 0ull;
             if (slot_equals(t, m, mhi, d, lo, hi, pos)) {
@@ -294,7 +298,7 @@ __device__ __forceinline__ uint32_t probe_lengths(const DevTables &t, int Lw, ui
         if (act[j]) {
             bool open;
             const int sl = first_match(bk[j], fp[j], &open);
-            if (sl >= 0) slot[j] = (int32_t)(bidx[j] * (uint32_t)kBucket + (uint32_t)sl);
+            if (sl >= 0) slot[j] = (int32_t)(bucket_base(bk[j]) + (uint32_t)sl);
             if (sl >= 0 || !open) pending |= 1u << j;  // cleared below when the match holds
         }
     }
@@ -1663,7 +1667,7 @@ __device__ __forceinline__ void probe_batch(const DevTables &t, const int64_t (&
         slot[k] = -1;
         if (hashed[k]) {
             bucket_masks(bk[k], fingerprint(key[k]), &match[k], &empty[k]);
-            if (match[k]) slot[k] = (int32_t)(home_bucket(t, key[k]) * kBucket + (uint64_t)__builtin_ctz(match[k]));
+            if (match[k]) slot[k] = (int32_t)(bucket_base(bk[k]) + (uint32_t)__builtin_ctz(match[k]));
         }
     }
     SlotPay p[K];

@@ -168,7 +168,8 @@ struct tam_vocab {
     tam::hvec<uint32_t> tok_off;
     tam::hvec<uint8_t> tok_blob;
     std::vector<uint8_t> len_present;
-    tam::hvec<uint16_t> fps;
+    tam::hvec<uint16_t> fps;          // the buckets, four 32-bit words each (as 16-bit halves)
+    // pay / pay_hi: one entry per distinct string, by its number
     tam::hvec<tam::SlotPay> pay;
     tam::hvec<uint64_t> pay_hi;
     tam::hvec<int32_t> short_hits;
